@@ -1,0 +1,193 @@
+/*
+ * CPU oracle for the group-shared fixed fan-in (GS-FFI) output layer and its dense head.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file is the plain, slow, obviously-correct statement of what
+ * the GPU path computes.  Only the tests, the smoke check and the benchmark's CPU-baseline leg
+ * may load it.  It shares no code, header, table or helper with the GPU library.
+ *
+ * Definitions (paper, Section 3.1 "Representation", Section 3.2 "Kernels", Section 3.3 Eq.
+ * "head_tail_objective"):
+ *   - labels are partitioned into K = L/G contiguous groups; label l belongs to group g(l) = l/G;
+ *   - group k has one support I_k = idx[k, 0..F_in-1] (features of the input h);
+ *   - label l keeps its own weights w_l = W[l, 0..F_in-1], slot t lives on feature idx[g(l), t];
+ *   - logit   z_l(x) = <w_l, h_{I_g(l)}>                      (Section 3.1)
+ *   - dW      grad W_k = (grad Z_k)^T H_k,  H_k = h_{:, I_k}     (Section 3.2, backward-weight)
+ *   - dX      grad h_{:, I_k} += grad Z_k W_k, summed over k     (Section 3.2, backward-feature)
+ *   - head    a^H = W_head h_head                                (Section 3.3)
+ *
+ * Arithmetic: inputs are decoded exactly to double (bf16 -> fp64 and fp32 -> fp64 are exact);
+ * every sum is accumulated in double in the order the definition states (no blocking, no
+ * reordering).  Outputs are fp64 and are never rounded to the GPU's storage types.
+ *
+ * Parity pins: see the tests (brute-force dense zero-masked matrix, worked Fig. 2 instances,
+ * special cases, finite differences, adjoint identity, one-hot gathers).
+ */
+#include <stdint.h>
+#include <string.h>
+#include <omp.h>
+
+#define DT_F32 0
+#define DT_BF16 1
+
+/* element i of a stored buffer, decoded exactly */
+static double ld(const void *p, int64_t i, int dtype) {
+    if (dtype == DT_BF16) {
+        uint32_t u = ((uint32_t)((const uint16_t *)p)[i]) << 16;
+        float f;
+        memcpy(&f, &u, sizeof f);
+        return (double)f;
+    }
+    return (double)((const float *)p)[i];
+}
+
+static int bad_layer(int64_t B, int64_t F_s, int64_t L, int64_t G, int64_t F_in, int dtype) {
+    if (B < 0 || F_s <= 0 || L < 0 || G <= 0 || F_in <= 0) return 1;
+    if (L % G != 0) return 1;
+    if (dtype != DT_F32 && dtype != DT_BF16) return 1;
+    return 0;
+}
+
+int haste_oracle_num_threads(void) { return omp_get_max_threads(); }
+
+/* ---------------------------------------------------------------------------------------------
+ * Tail forward (Section 3.1):  Y[b, l] = bias[l] + sum_t X[b, idx[g(l), t]] * W[l, t]
+ * for labels l in [l0, l1) and all rows b; Y is [B, l1-l0] row-major.
+ * ------------------------------------------------------------------------------------------- */
+int haste_oracle_fwd(int64_t B, int64_t F_s, int64_t L, int64_t G, int64_t F_in, int dtype,
+                     const void *X, const int32_t *idx, const void *W, const float *bias,
+                     int64_t l0, int64_t l1, double *Y) {
+    if (bad_layer(B, F_s, L, G, F_in, dtype) || l0 < 0 || l1 > L || l0 > l1) return 1;
+    const int64_t n = l1 - l0;
+#pragma omp parallel for schedule(static)
+    for (int64_t l = l0; l < l1; ++l) {
+        const int64_t g = l / G;                 /* g(l): labels of a group are contiguous */
+        for (int64_t b = 0; b < B; ++b) {
+            double z = bias ? (double)bias[l] : 0.0;
+            for (int64_t t = 0; t < F_in; ++t) {
+                const int64_t f = idx[g * F_in + t];
+                z += ld(X, b * F_s + f, dtype) * ld(W, l * F_in + t, dtype);
+            }
+            Y[b * n + (l - l0)] = z;
+        }
+    }
+    return 0;
+}
+
+/* Forward logits at explicit (b, l) sample points. */
+int haste_oracle_fwd_at(int64_t B, int64_t F_s, int64_t L, int64_t G, int64_t F_in, int dtype,
+                        const void *X, const int32_t *idx, const void *W, const float *bias,
+                        int64_t n, const int64_t *bs, const int64_t *ls, double *out) {
+    if (bad_layer(B, F_s, L, G, F_in, dtype)) return 1;
+    for (int64_t i = 0; i < n; ++i)
+        if (bs[i] < 0 || bs[i] >= B || ls[i] < 0 || ls[i] >= L) return 1;
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < n; ++i) {
+        const int64_t b = bs[i], l = ls[i], g = l / G;
+        double z = bias ? (double)bias[l] : 0.0;
+        for (int64_t t = 0; t < F_in; ++t)
+            z += ld(X, b * F_s + idx[g * F_in + t], dtype) * ld(W, l * F_in + t, dtype);
+        out[i] = z;
+    }
+    return 0;
+}
+
+/* ---------------------------------------------------------------------------------------------
+ * Tail backward-weight (Section 3.2):  dW[l, t] = sum_b dY[b, l] * X[b, idx[g(l), t]]
+ * only on the F_in support slots; dbias[l] = sum_b dY[b, l].  Labels in [l0, l1).
+ * dW is [l1-l0, F_in], dbias is [l1-l0] (may be NULL).
+ * ------------------------------------------------------------------------------------------- */
+int haste_oracle_bwd_w(int64_t B, int64_t F_s, int64_t L, int64_t G, int64_t F_in, int dtype,
+                       const void *X, const int32_t *idx, const void *dY,
+                       int64_t l0, int64_t l1, double *dW, double *dbias) {
+    if (bad_layer(B, F_s, L, G, F_in, dtype) || l0 < 0 || l1 > L || l0 > l1) return 1;
+#pragma omp parallel for schedule(static)
+    for (int64_t l = l0; l < l1; ++l) {
+        const int64_t g = l / G;
+        for (int64_t t = 0; t < F_in; ++t) {
+            const int64_t f = idx[g * F_in + t];
+            double s = 0.0;
+            for (int64_t b = 0; b < B; ++b)
+                s += ld(dY, b * L + l, dtype) * ld(X, b * F_s + f, dtype);
+            dW[(l - l0) * F_in + t] = s;
+        }
+        if (dbias) {
+            double s = 0.0;
+            for (int64_t b = 0; b < B; ++b) s += ld(dY, b * L + l, dtype);
+            dbias[l - l0] = s;
+        }
+    }
+    return 0;
+}
+
+/* ---------------------------------------------------------------------------------------------
+ * Tail backward-feature (Section 3.2):
+ *   dX[b, f] = sum_k sum_{t : idx[k,t] = f} sum_{j < G} dY[b, kG + j] * W[kG + j, t]
+ * written as a per-row scatter over labels: every label's contribution is added to the feature
+ * its slot lives on.  Rows b in [b0, b1); dX is [b1-b0, F_s] (overwritten).
+ * ------------------------------------------------------------------------------------------- */
+int haste_oracle_bwd_x(int64_t B, int64_t F_s, int64_t L, int64_t G, int64_t F_in, int dtype,
+                       const int32_t *idx, const void *W, const void *dY,
+                       int64_t b0, int64_t b1, double *dX) {
+    if (bad_layer(B, F_s, L, G, F_in, dtype) || b0 < 0 || b1 > B || b0 > b1) return 1;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t b = b0; b < b1; ++b) {
+        double *row = dX + (b - b0) * F_s;
+        for (int64_t f = 0; f < F_s; ++f) row[f] = 0.0;
+        for (int64_t l = 0; l < L; ++l) {
+            const double d = ld(dY, b * L + l, dtype);
+            const int64_t g = l / G;
+            for (int64_t t = 0; t < F_in; ++t)
+                row[idx[g * F_in + t]] += d * ld(W, l * F_in + t, dtype);
+        }
+    }
+    return 0;
+}
+
+/* ---------------------------------------------------------------------------------------------
+ * Dense head (Section 3.3):  Yh[b, h] = bias_h[h] + sum_f X[b, f] * Wh[h, f], heads in [h0, h1).
+ * Yh is [B, h1-h0].
+ * ------------------------------------------------------------------------------------------- */
+int haste_oracle_head_fwd(int64_t B, int64_t F_s, int64_t H, int dtype, const void *X,
+                          const void *Wh, const float *bias_h, int64_t h0, int64_t h1, double *Yh) {
+    if (B < 0 || F_s <= 0 || H < 0 || h0 < 0 || h1 > H || h0 > h1) return 1;
+    if (dtype != DT_F32 && dtype != DT_BF16) return 1;
+    const int64_t n = h1 - h0;
+#pragma omp parallel for schedule(static)
+    for (int64_t h = h0; h < h1; ++h)
+        for (int64_t b = 0; b < B; ++b) {
+            double z = bias_h ? (double)bias_h[h] : 0.0;
+            for (int64_t f = 0; f < F_s; ++f) z += ld(X, b * F_s + f, dtype) * ld(Wh, h * F_s + f, dtype);
+            Yh[b * n + (h - h0)] = z;
+        }
+    return 0;
+}
+
+/* dWh[h, f] = sum_b dYh[b, h] * X[b, f] for heads in [h0, h1); dWh is [h1-h0, F_s]. */
+int haste_oracle_head_bwd_w(int64_t B, int64_t F_s, int64_t H, int dtype, const void *X,
+                            const void *dYh, int64_t h0, int64_t h1, double *dWh) {
+    if (B < 0 || F_s <= 0 || H < 0 || h0 < 0 || h1 > H || h0 > h1) return 1;
+    if (dtype != DT_F32 && dtype != DT_BF16) return 1;
+#pragma omp parallel for schedule(static)
+    for (int64_t h = h0; h < h1; ++h)
+        for (int64_t f = 0; f < F_s; ++f) {
+            double s = 0.0;
+            for (int64_t b = 0; b < B; ++b) s += ld(dYh, b * H + h, dtype) * ld(X, b * F_s + f, dtype);
+            dWh[(h - h0) * F_s + f] = s;
+        }
+    return 0;
+}
+
+/* dXh[b, f] = sum_h dYh[b, h] * Wh[h, f] for rows in [b0, b1); dXh is [b1-b0, F_s]. */
+int haste_oracle_head_bwd_x(int64_t B, int64_t F_s, int64_t H, int dtype, const void *Wh,
+                            const void *dYh, int64_t b0, int64_t b1, double *dXh) {
+    if (B < 0 || F_s <= 0 || H < 0 || b0 < 0 || b1 > B || b0 > b1) return 1;
+    if (dtype != DT_F32 && dtype != DT_BF16) return 1;
+#pragma omp parallel for schedule(static)
+    for (int64_t b = b0; b < b1; ++b)
+        for (int64_t f = 0; f < F_s; ++f) {
+            double s = 0.0;
+            for (int64_t h = 0; h < H; ++h) s += ld(dYh, b * H + h, dtype) * ld(Wh, h * F_s + f, dtype);
+            dXh[(b - b0) * F_s + f] = s;
+        }
+    return 0;
+}

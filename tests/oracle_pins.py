@@ -1,0 +1,323 @@
+"""Pins of the CPU oracle against facts fixed outside the oracle itself.
+
+Every ``pin_*`` takes an oracle object (the real one, or a build with a planted mistake) and
+raises AssertionError when the oracle disagrees with:
+
+* the paper's worked instances of the two index formats (Figure 2(c) and 2(d));
+* a brute-force dense layer whose full weight matrix is zero outside each group's support
+  (the sparse layer of Section 3.1 is exactly that matrix), evaluated with ``np.matmul``;
+* special cases with textbook answers (F_in = F_s with identity supports is a dense layer;
+  G = 1 is standard per-label fixed fan-in; G = L is one gathered GEMM);
+* finite differences of the Section 3.3 BCE objective and of the bilinear pairing;
+* the adjoint identity <dY, Y - bias> = <dX, X> = <dW, W> (bilinearity);
+* exact one-hot gathers/scatters and the group-permutation invariance.
+"""
+from __future__ import annotations
+
+import json
+import os
+
+import numpy as np
+
+import synth
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+F32, BF16 = synth.DT_F32, synth.DT_BF16
+
+
+# ------------------------------------------------------------------------------------------
+# independent helpers (NumPy only)
+# ------------------------------------------------------------------------------------------
+def dense_masked(idx, W, G, F_s):
+    """W_full[L, F_s]: W_full[l, idx[l//G, t]] += W[l, t]; zero elsewhere (duplicates add)."""
+    W = np.asarray(W, dtype=np.float64)
+    L, F_in = W.shape
+    Wf = np.zeros((L, F_s), dtype=np.float64)
+    rows = np.repeat(np.arange(L), F_in)
+    cols = idx[np.arange(L) // G].reshape(-1)
+    np.add.at(Wf, (rows, cols), W.reshape(-1))
+    return Wf
+
+
+def rand_layer(rng, B, F_s, L, G, F_in, dtype, distinct=True, bias=True):
+    X = rng.standard_normal((B, F_s)).astype(np.float32)
+    W = (rng.standard_normal((L, F_in)) / np.sqrt(F_in)).astype(np.float32)
+    dY = rng.standard_normal((B, L)).astype(np.float32)
+    K = L // G
+    if distinct:
+        idx = np.stack([np.sort(rng.choice(F_s, F_in, replace=False)) for _ in range(K)]).astype(np.int32)
+    else:
+        idx = rng.integers(0, F_s, size=(K, F_in)).astype(np.int32)
+    b = rng.standard_normal(L).astype(np.float32) if bias else None
+    if dtype == BF16:
+        X, W, dY = synth.bf16_bits(X), synth.bf16_bits(W), synth.bf16_bits(dY)
+    return X, idx, W, b, dY
+
+
+def f64(a, dtype):
+    return synth.to_f64(a, dtype)
+
+
+def close(a, b, rtol=1e-12, what=""):
+    a = np.asarray(a, np.float64)
+    b = np.asarray(b, np.float64)
+    assert a.shape == b.shape, f"{what}: shape {a.shape} vs {b.shape}"
+    scale = max(1.0, float(np.abs(b).max()) if b.size else 1.0)
+    err = float(np.abs(a - b).max()) if a.size else 0.0
+    assert err <= rtol * scale, f"{what}: max abs err {err:.3e} > {rtol:.1e} * {scale:.3e}"
+
+
+def _load_fig2():
+    with open(os.path.join(GOLDEN, "fig2_formats.json")) as fh:
+        return json.load(fh)
+
+
+def _grid(panel, n_labels, n_features):
+    # drawn values rounded to the fp32 storage type the layer holds them in
+    D = np.zeros((n_labels, n_features))
+    for l, f, v in panel["grid"]:
+        D[l, f] = float(np.float32(v))
+    return D
+
+
+# ------------------------------------------------------------------------------------------
+# pins
+# ------------------------------------------------------------------------------------------
+def pin_fig2_gs(o):
+    """Figure 2(d): supports {0,2} and {1,3} for groups of 3 labels; logits with X = I are the grid."""
+    g = _load_fig2()
+    p = g["gs"]
+    nl, nf, G = g["n_labels"], g["n_features"], p["group_size"]
+    idx = np.array(p["index_rows_slot_major"], dtype=np.int32).T.copy()   # [K, F]
+    W = np.array(p["weight_rows_slot_major"], dtype=np.float32).T.copy()  # [L, F]
+    D = _grid(p, nl, nf)
+    close(dense_masked(idx, W, G, nf), D, 0, "fig2(d) decode")
+    # forward with one-hot rows: Y[f, l] = W_full[l, f]
+    Y = o.fwd(np.eye(nf, dtype=np.float32), idx, W, None, G, F32)
+    close(Y, D.T, 0, "fig2(d) fwd")
+    # backward-feature with one-hot upstream rows: dX[l, f] = W_full[l, f]
+    dX = o.bwd_x(idx, W, np.eye(nl, dtype=np.float32), G, nf, F32)
+    close(dX, D, 0, "fig2(d) bwd_x")
+    # backward-weight with X = I and dY = grid^T returns each label's own weights
+    dW, _ = o.bwd_w(np.eye(nf, dtype=np.float32), idx, D.T.astype(np.float32), G, idx.shape[1], F32)
+    close(dW, W, 0, "fig2(d) bwd_w")
+
+
+def pin_fig2_ffi(o):
+    """Figure 2(c): per-label supports (G = 1) decode to the drawn grid."""
+    g = _load_fig2()
+    p = g["ffi"]
+    nl, nf = g["n_labels"], g["n_features"]
+    idx = np.array(p["index_rows_slot_major"], dtype=np.int32).T.copy()   # [L, F]
+    W = np.array(p["weight_rows_slot_major"], dtype=np.float32).T.copy()
+    D = _grid(p, nl, nf)
+    close(dense_masked(idx, W, 1, nf), D, 0, "fig2(c) decode")
+    close(o.fwd(np.eye(nf, dtype=np.float32), idx, W, None, 1, F32), D.T, 0, "fig2(c) fwd")
+    close(o.bwd_x(idx, W, np.eye(nl, dtype=np.float32), 1, nf, F32), D, 0, "fig2(c) bwd_x")
+
+
+_SHAPES = [
+    # B, F_s, L, G, F_in
+    (5, 17, 24, 4, 3),
+    (7, 40, 48, 8, 6),
+    (3, 9, 6, 1, 4),       # G = 1 (per-label fixed fan-in)
+    (4, 12, 10, 10, 5),    # G = L (one group)
+    (6, 16, 32, 4, 16),    # F_in = F_s
+    (1, 33, 64, 16, 7),    # single row
+]
+
+
+def pin_bruteforce(o):
+    """fwd, dW, dbias, dX equal the dense zero-masked layer (np.matmul, fp64)."""
+    rng = np.random.default_rng(1234)
+    for dtype in (F32, BF16):
+        for (B, F_s, L, G, F_in) in _SHAPES:
+            X, idx, W, b, dY = rand_layer(rng, B, F_s, L, G, F_in, dtype)
+            Wf = dense_masked(idx, f64(W, dtype), G, F_s)
+            Xd, dYd = f64(X, dtype), f64(dY, dtype)
+            Y = o.fwd(X, idx, W, b, G, dtype)
+            close(Y, Xd @ Wf.T + b.astype(np.float64), 1e-12, f"fwd {B,F_s,L,G,F_in}")
+            dW, db = o.bwd_w(X, idx, dY, G, F_in, dtype, with_dbias=True)
+            full = dYd.T @ Xd                                  # dense gradient [L, F_s]
+            close(dW, full[np.arange(L)[:, None], idx[np.arange(L) // G]], 1e-12, "bwd_w")
+            close(db, dYd.sum(0), 1e-12, "dbias")
+            close(o.bwd_x(idx, W, dY, G, F_s, dtype), dYd @ Wf, 1e-12, "bwd_x")
+
+
+def pin_duplicate_indices(o):
+    """A support with repeated features still equals the masked matrix (contributions add)."""
+    rng = np.random.default_rng(7)
+    X, idx, W, b, dY = rand_layer(rng, 4, 5, 12, 3, 6, F32, distinct=False)
+    Wf = dense_masked(idx, W, 3, 5)
+    close(o.fwd(X, idx, W, b, 3, F32), X.astype(np.float64) @ Wf.T + b, 1e-12, "dup fwd")
+    close(o.bwd_x(idx, W, dY, 3, 5, F32), dY.astype(np.float64) @ Wf, 1e-12, "dup bwd_x")
+
+
+def pin_dense_special_case(o):
+    """F_in = F_s with idx[k] = 0..F_s-1 is the dense layer Y = X W^T."""
+    rng = np.random.default_rng(3)
+    B, F_s, L, G = 6, 10, 14, 7
+    X = rng.standard_normal((B, F_s)).astype(np.float32)
+    W = rng.standard_normal((L, F_s)).astype(np.float32)
+    dY = rng.standard_normal((B, L)).astype(np.float32)
+    idx = np.tile(np.arange(F_s, dtype=np.int32), (L // G, 1))
+    Xd, Wd, dYd = X.astype(np.float64), W.astype(np.float64), dY.astype(np.float64)
+    close(o.fwd(X, idx, W, None, G, F32), Xd @ Wd.T, 1e-12, "dense fwd")
+    close(o.bwd_w(X, idx, dY, G, F_s, F32)[0], dYd.T @ Xd, 1e-12, "dense dW")
+    close(o.bwd_x(idx, W, dY, G, F_s, F32), dYd @ Wd, 1e-12, "dense dX")
+
+
+def pin_group_equals_expanded_ffi(o):
+    """GS with (idx, G) equals standard fixed fan-in with idx_ffi[l] = idx[l // G] (G = 1)."""
+    rng = np.random.default_rng(11)
+    B, F_s, L, G, F_in = 5, 30, 40, 8, 5
+    X, idx, W, b, dY = rand_layer(rng, B, F_s, L, G, F_in, F32)
+    idx1 = idx[np.arange(L) // G]
+    close(o.fwd(X, idx, W, b, G, F32), o.fwd(X, idx1, W, b, 1, F32), 0, "G vs FFI fwd")
+    close(o.bwd_w(X, idx, dY, G, F_in, F32)[0], o.bwd_w(X, idx1, dY, 1, F_in, F32)[0], 0, "G vs FFI dW")
+    close(o.bwd_x(idx, W, dY, G, F_s, F32), o.bwd_x(idx1, W, dY, 1, F_s, F32), 1e-14, "G vs FFI dX")
+
+
+def _bce(Y, T):
+    # sum of binary cross-entropies of sigmoid(Y) against targets T (Section 3.3 objective, unscaled)
+    return float(np.sum(np.logaddexp(0.0, Y) - T * Y))
+
+
+def pin_finite_differences(o):
+    """Central differences of the BCE objective and of <dY, Y> match dX and dW."""
+    rng = np.random.default_rng(5)
+    B, F_s, L, G, F_in = 4, 12, 16, 4, 5
+    X, idx, W, b, _ = rand_layer(rng, B, F_s, L, G, F_in, F32)
+    T = (rng.random((B, L)) < 0.2).astype(np.float64)
+    Y = o.fwd(X, idx, W, b, G, F32)
+    dY = (1.0 / (1.0 + np.exp(-Y)) - T).astype(np.float32)        # BCE gradient, fp32 upstream
+    # with dY rounded to fp32 the exact derivative of phi(X, W) = <dY, Y> is what we compare
+    dX = o.bwd_x(idx, W, dY, G, F_s, F32)
+    dW, _ = o.bwd_w(X, idx, dY, G, F_in, F32)
+    phi = lambda Xv, Wv: float(np.sum(dY.astype(np.float64) * o.fwd(Xv, idx, Wv, b, G, F32)))
+    for (bb, ff) in [(0, int(idx[0, 0])), (1, int(idx[1, 2])), (3, int(idx[3, 4])), (2, 0), (0, F_s - 1)]:
+        Xp, Xm = X.copy(), X.copy()
+        Xp[bb, ff] += np.float32(0.5)
+        Xm[bb, ff] -= np.float32(0.5)
+        fd = (phi(Xp, W) - phi(Xm, W)) / (float(Xp[bb, ff]) - float(Xm[bb, ff]))
+        assert abs(fd - dX[bb, ff]) <= 1e-10 * max(1.0, abs(dX[bb, ff])), f"FD dX[{bb},{ff}] {fd} vs {dX[bb, ff]}"
+    for (l, t) in [(0, 0), (5, 3), (15, 4), (9, 1)]:
+        Wp, Wm = W.copy(), W.copy()
+        Wp[l, t] += np.float32(0.25)
+        Wm[l, t] -= np.float32(0.25)
+        fd = (phi(X, Wp) - phi(X, Wm)) / (float(Wp[l, t]) - float(Wm[l, t]))
+        assert abs(fd - dW[l, t]) <= 1e-10 * max(1.0, abs(dW[l, t])), f"FD dW[{l},{t}] {fd} vs {dW[l, t]}"
+    # the BCE objective itself (nonlinear): O(eps^2) truncation
+    dY64 = 1.0 / (1.0 + np.exp(-Y)) - T
+    dY32 = dY64.astype(np.float32)
+    dX_bce = o.bwd_x(idx, W, dY32, G, F_s, F32)
+    for (bb, ff) in [(0, int(idx[0, 0])), (2, int(idx[2, 1]))]:
+        Xp, Xm = X.copy(), X.copy()
+        Xp[bb, ff] += np.float32(1e-3)
+        Xm[bb, ff] -= np.float32(1e-3)
+        fd = (_bce(o.fwd(Xp, idx, W, b, G, F32), T) - _bce(o.fwd(Xm, idx, W, b, G, F32), T)) / (
+            float(Xp[bb, ff]) - float(Xm[bb, ff]))
+        assert abs(fd - dX_bce[bb, ff]) <= 1e-5 * max(1.0, abs(fd)), f"BCE FD dX[{bb},{ff}] {fd} vs {dX_bce[bb, ff]}"
+
+
+def pin_adjoint_identity(o):
+    """<dY, Y - bias> = <dX, X> = <dW, W> (the layer is bilinear in (X, W))."""
+    rng = np.random.default_rng(9)
+    for dtype in (F32, BF16):
+        B, F_s, L, G, F_in = 9, 50, 96, 8, 12
+        X, idx, W, b, dY = rand_layer(rng, B, F_s, L, G, F_in, dtype)
+        Y = o.fwd(X, idx, W, b, G, dtype)
+        dX = o.bwd_x(idx, W, dY, G, F_s, dtype)
+        dW, _ = o.bwd_w(X, idx, dY, G, F_in, dtype)
+        a = float(np.sum(f64(dY, dtype) * (Y - b)))
+        c = float(np.sum(dX * f64(X, dtype)))
+        d = float(np.sum(dW * f64(W, dtype)))
+        scale = float(np.sum(np.abs(f64(dY, dtype) * (Y - b))))
+        assert abs(a - c) <= 1e-12 * scale and abs(a - d) <= 1e-12 * scale, f"adjoint {a} {c} {d}"
+
+
+def pin_one_hot(o):
+    """One-hot weights / upstream rows turn the three products into exact gathers and scatters."""
+    rng = np.random.default_rng(21)
+    B, F_s, L, G, F_in = 6, 20, 24, 4, 5
+    X, idx, _, _, dY = rand_layer(rng, B, F_s, L, G, F_in, F32, bias=False)
+    g = np.arange(L) // G
+    for t0 in range(F_in):
+        W = np.zeros((L, F_in), np.float32)
+        W[:, t0] = 1
+        close(o.fwd(X, idx, W, None, G, F32), X[:, idx[g, t0]], 0, f"one-hot fwd t0={t0}")
+    b0 = 4
+    dYo = np.zeros((B, L), np.float32)
+    dYo[b0] = 1
+    close(o.bwd_w(X, idx, dYo, G, F_in, F32)[0], X[b0][idx[g]], 0, "one-hot bwd_w")
+    l0, t0 = 9, 3
+    W = np.zeros((L, F_in), np.float32)
+    W[l0, t0] = 1
+    dX = o.bwd_x(idx, W, dY, G, F_s, F32)
+    exp = np.zeros((B, F_s))
+    exp[:, idx[l0 // G, t0]] = dY[:, l0]
+    close(dX, exp, 0, "one-hot bwd_x")
+    # features outside every support get exactly +0.0
+    W = rng.standard_normal((L, F_in)).astype(np.float32)
+    used = np.zeros(F_s, bool)
+    used[idx.reshape(-1)] = True
+    dX = o.bwd_x(idx, W, dY, G, F_s, F32)
+    assert np.all(dX[:, ~used] == 0.0), "untouched features must stay zero"
+
+
+def pin_group_permutation(o):
+    """Permuting groups (their labels and idx rows together) permutes Y columns and dW rows."""
+    rng = np.random.default_rng(31)
+    B, F_s, L, G, F_in = 5, 25, 36, 6, 4
+    X, idx, W, b, dY = rand_layer(rng, B, F_s, L, G, F_in, F32)
+    K = L // G
+    pk = rng.permutation(K)
+    lab = (pk[:, None] * G + np.arange(G)[None, :]).reshape(-1)   # new label n holds old label lab[n]
+    Y = o.fwd(X, idx, W, b, G, F32)
+    Yp = o.fwd(X, idx[pk], W[lab], b[lab], G, F32)
+    close(Yp, Y[:, lab], 0, "perm fwd")
+    dW = o.bwd_w(X, idx, dY, G, F_in, F32)[0]
+    close(o.bwd_w(X, idx[pk], dY[:, lab], G, F_in, F32)[0], dW[lab], 0, "perm dW")
+    close(o.bwd_x(idx[pk], W[lab], dY[:, lab], G, F_s, F32), o.bwd_x(idx, W, dY, G, F_s, F32), 1e-13, "perm dX")
+
+
+def pin_label_ranges(o):
+    """Label-range, row-range and sampled entry points agree with the full computation."""
+    rng = np.random.default_rng(41)
+    B, F_s, L, G, F_in = 7, 30, 64, 8, 6
+    X, idx, W, b, dY = rand_layer(rng, B, F_s, L, G, F_in, BF16)
+    Y = o.fwd(X, idx, W, b, G, BF16)
+    close(o.fwd(X, idx, W, b, G, BF16, 13, 41), Y[:, 13:41], 0, "fwd range")
+    bs = np.array([0, 6, 3, 3]); ls = np.array([0, 63, 17, 40])
+    close(o.fwd_at(X, idx, W, b, G, BF16, bs, ls), Y[bs, ls], 0, "fwd_at")
+    dW, db = o.bwd_w(X, idx, dY, G, F_in, BF16, with_dbias=True)
+    dW2, db2 = o.bwd_w(X, idx, dY, G, F_in, BF16, 8, 24, with_dbias=True)
+    close(dW2, dW[8:24], 0, "bwd_w range")
+    close(db2, db[8:24], 0, "dbias range")
+    dX = o.bwd_x(idx, W, dY, G, F_s, BF16)
+    close(o.bwd_x(idx, W, dY, G, F_s, BF16, 2, 5), dX[2:5], 0, "bwd_x range")
+
+
+def pin_head(o):
+    """Dense head: Yh = X Wh^T + bh, dWh = dYh^T X, dXh = dYh Wh (np.matmul, fp64)."""
+    rng = np.random.default_rng(51)
+    for dtype in (F32, BF16):
+        B, F_s, H = 6, 21, 13
+        X = rng.standard_normal((B, F_s)).astype(np.float32)
+        Wh = rng.standard_normal((H, F_s)).astype(np.float32)
+        dYh = rng.standard_normal((B, H)).astype(np.float32)
+        bh = rng.standard_normal(H).astype(np.float32)
+        if dtype == BF16:
+            X, Wh, dYh = synth.bf16_bits(X), synth.bf16_bits(Wh), synth.bf16_bits(dYh)
+        Xd, Whd, dYd = f64(X, dtype), f64(Wh, dtype), f64(dYh, dtype)
+        close(o.head_fwd(X, Wh, bh, dtype), Xd @ Whd.T + bh, 1e-12, "head fwd")
+        close(o.head_fwd(X, Wh, None, dtype, 3, 9), (Xd @ Whd.T)[:, 3:9], 1e-12, "head fwd range")
+        close(o.head_bwd_w(X, dYh, dtype), dYd.T @ Xd, 1e-12, "head dW")
+        close(o.head_bwd_w(X, dYh, dtype, 2, 7), (dYd.T @ Xd)[2:7], 1e-12, "head dW range")
+        close(o.head_bwd_x(Wh, dYh, dtype), dYd @ Whd, 1e-12, "head dX")
+        close(o.head_bwd_x(Wh, dYh, dtype, 1, 4), (dYd @ Whd)[1:4], 1e-12, "head dX range")
+
+
+ALL_PINS = [pin_fig2_gs, pin_fig2_ffi, pin_bruteforce, pin_duplicate_indices, pin_dense_special_case,
+            pin_group_equals_expanded_ffi, pin_finite_differences, pin_adjoint_identity, pin_one_hot,
+            pin_group_permutation, pin_label_ranges, pin_head]

@@ -1,0 +1,65 @@
+"""Planted mistakes in the oracle must each be caught by at least one pin.
+
+Each mutant is the oracle's C source with one plausible slip (a wrong group map, a transposed
+index, a dropped term, a scatter turned into a store at the wrong place ...), compiled on the CPU
+into a temporary library.  Every planted access stays in bounds for the pins' shapes.
+"""
+import os
+
+import pytest
+
+import oracle
+import oracle_pins as P
+
+SRC = open(oracle.SRC).read()
+
+MUTANTS = {
+    "group_map_mod": ("const int64_t g = l / G;                 /* g(l)", "const int64_t g = l % (L / G); /* g(l)"),
+    "idx_transposed_fwd": ("const int64_t f = idx[g * F_in + t];\n                z +=",
+                           "const int64_t f = idx[t * (L / G) + g];\n                z +="),
+    "bias_dropped": ("double z = bias ? (double)bias[l] : 0.0;\n            for (int64_t t = 0; t < F_in; ++t) {",
+                     "double z = 0.0;\n            for (int64_t t = 0; t < F_in; ++t) {"),
+    "fwd_last_slot_dropped": ("for (int64_t t = 0; t < F_in; ++t) {\n                const int64_t f = idx[g * F_in + t];\n                z +=",
+                              "for (int64_t t = 0; t + 1 < F_in; ++t) {\n                const int64_t f = idx[g * F_in + t];\n                z +="),
+    "bwd_w_slot_not_feature": ("s += ld(dY, b * L + l, dtype) * ld(X, b * F_s + f, dtype);",
+                               "s += ld(dY, b * L + l, dtype) * ld(X, b * F_s + t, dtype);"),
+    "bwd_w_sign": ("s += ld(dY, b * L + l, dtype) * ld(X, b * F_s + f, dtype);",
+                   "s -= ld(dY, b * L + l, dtype) * ld(X, b * F_s + f, dtype);"),
+    "dbias_wrong_row": ("for (int64_t b = 0; b < B; ++b) s += ld(dY, b * L + l, dtype);",
+                        "for (int64_t b = 0; b < B; ++b) s += ld(dY, l, dtype);"),
+    "bwd_x_scatter_to_slot": ("row[idx[g * F_in + t]] += d * ld(W, l * F_in + t, dtype);",
+                              "row[t] += d * ld(W, l * F_in + t, dtype);"),
+    "bwd_x_dy_transposed": ("const double d = ld(dY, b * L + l, dtype);",
+                            "const double d = ld(dY, l * B + b, dtype);"),
+    "bwd_x_group_of_slot": ("row[idx[g * F_in + t]] += d * ld(W, l * F_in + t, dtype);",
+                            "row[idx[g * F_in + t]] += d * ld(W, g * F_in + t, dtype);"),
+    "head_w_transposed": ("z += ld(X, b * F_s + f, dtype) * ld(Wh, h * F_s + f, dtype);",
+                          "z += ld(X, b * F_s + f, dtype) * ld(Wh, f * H + h, dtype);"),
+    "head_dw_dy_transposed": ("s += ld(dYh, b * H + h, dtype) * ld(X, b * F_s + f, dtype);",
+                              "s += ld(dYh, h * B + b, dtype) * ld(X, b * F_s + f, dtype);"),
+    "head_dx_w_transposed": ("s += ld(dYh, b * H + h, dtype) * ld(Wh, h * F_s + f, dtype);",
+                             "s += ld(dYh, b * H + h, dtype) * ld(Wh, f * H + h, dtype);"),
+    "bf16_decode_shift": ("uint32_t u = ((uint32_t)((const uint16_t *)p)[i]) << 16;",
+                          "uint32_t u = ((uint32_t)((const uint16_t *)p)[i]) << 15;"),
+}
+
+
+def _caught(o):
+    failed = []
+    for pin in P.ALL_PINS:
+        try:
+            pin(o)
+        except (AssertionError, ValueError, FloatingPointError):
+            failed.append(pin.__name__)
+    return failed
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_mutant_is_caught(tmp_path, name):
+    old, new = MUTANTS[name]
+    assert SRC.count(old) >= 1, f"mutation site for {name} not found"
+    src = tmp_path / f"{name}.c"
+    src.write_text(SRC.replace(old, new, 1))
+    lib = oracle.build(str(src), str(tmp_path / f"lib{name}.so"))
+    failed = _caught(oracle.Oracle(lib))
+    assert failed, f"planted mistake {name} passed every pin"
