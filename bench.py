@@ -1,0 +1,263 @@
+"""Benchmark of the group-shared fixed fan-in output layer on one MI355X.
+
+One step = the whole hot path on one batch of seeded synthetic input already resident in HBM:
+  tail forward (haste_fwd) -> head forward (haste_head_fwd) -> tail backward-weight (haste_bwd_w)
+  -> tail backward-feature (haste_bwd_x) -> head backward (haste_head_bwd, adds its dX onto the tail's).
+Default workload: the 2.95M-label tail (G = 32, F_in = 64) with a 65,536-label dense head, B = 512,
+F_s = 768, bf16 storage with fp32 accumulation.
+
+Prints ONE JSON line (rank 0): ms/step, per-call times from HIP events recorded on the stream the
+calls are launched on, the roofline of the dominant kernel, the FLOPs-matched dense bottleneck
+timed beside it, and the CPU oracle timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16 MFMA
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--workload", default="l2949k_g32_h65k")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-bottleneck", action="store_true")
+    return p.parse_args()
+
+
+def call_cost(wl, dt_bytes=2):
+    """Algorithmic bytes and FLOPs of each call (each operand moved once)."""
+    B, F_s, L, F_in, H, K = wl.B, wl.F_s, wl.L, wl.F_in, wl.H, wl.K
+    X = B * F_s * dt_bytes
+    idx = K * F_in * 4
+    W = L * F_in * dt_bytes
+    Y = B * L * dt_bytes
+    dW = L * F_in * 4
+    dX = B * F_s * 4
+    Wh, Yh, dWh = H * F_s * dt_bytes, B * H * dt_bytes, H * F_s * 4
+    tail_flops = 2 * B * L * F_in
+    head_flops = 2 * B * H * F_s
+    c = {
+        "fwd": (X + idx + W + Y, tail_flops),
+        "bwd_w": (X + idx + Y + dW, tail_flops),
+        "bwd_x": (idx + W + Y + dX, tail_flops),
+    }
+    if H:
+        c["head_fwd"] = (X + Wh + Yh, head_flops)
+        c["head_bwd"] = (X + Wh + Yh + dWh + 2 * dX, 2 * head_flops)
+    return c
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2606_01117_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(f.encode() + fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload, call):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if taken on the current kernels."""
+    try:
+        with open(TRAFFIC_FILE) as fh:
+            t = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    if t.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    return t.get("workloads", {}).get(workload, {}).get(call)
+
+
+def cpu_baseline(wl, X, idx, W, dY, Wh, dYh):
+    """The fp64 oracle on a bounded sample of the same workload, scaled to ms per full step."""
+    import oracle
+    orc = oracle.get()
+    dt = wl.dtype
+    nl = min(wl.L, 32768)
+    nb = min(wl.B, 4)
+    nh = min(wl.H, 2048)
+    parts = {}
+    t = time.perf_counter(); orc.fwd(X, idx, W, None, wl.G, dt, 0, nl); parts["fwd"] = (time.perf_counter() - t) * wl.L / nl
+    t = time.perf_counter(); orc.bwd_w(X, idx, dY, wl.G, wl.F_in, dt, 0, nl); parts["bwd_w"] = (time.perf_counter() - t) * wl.L / nl
+    t = time.perf_counter(); orc.bwd_x(idx, W, dY, wl.G, wl.F_s, dt, 0, nb); parts["bwd_x"] = (time.perf_counter() - t) * wl.B / nb
+    sample = f"tail fwd+bwd_w on labels [0,{nl}), bwd_x on rows [0,{nb})"
+    if wl.H:
+        t = time.perf_counter(); orc.head_fwd(X, Wh, None, dt, 0, nh); parts["head_fwd"] = (time.perf_counter() - t) * wl.H / nh
+        t = time.perf_counter(); orc.head_bwd_w(X, dYh, dt, 0, nh); tw = (time.perf_counter() - t) * wl.H / nh
+        t = time.perf_counter(); orc.head_bwd_x(Wh, dYh, dt, 0, nb); parts["head_bwd"] = tw + (time.perf_counter() - t) * wl.B / nb
+        sample += f"; head fwd+dW on heads [0,{nh}), head dX on rows [0,{nb})"
+    ms = 1e3 * sum(parts.values())
+    return {"value": round(ms, 1), "unit": "ms/step", "cores": orc.num_threads(), "kind": "oracle",
+            "sample": sample + "; each part's time scaled by (full size / sampled size)",
+            "per_call_ms": {k: round(1e3 * v, 1) for k, v in parts.items()}}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the layer's multi-GPU sharding "
+              "is a design note, not a measured path.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2606_01117_amd as hs
+    import synth
+
+    wl = synth.WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    t0 = time.perf_counter()
+    X = synth.draw_X(wl)
+    W = synth.draw_W(wl)
+    idx = synth.draw_idx(wl)
+    pos = synth.draw_positives(wl)
+    perm = synth.draw_perm(wl)
+    dY = synth.draw_dY(wl, positives=pos, perm=perm)
+    Wh = synth.draw_W_head(wl) if wl.H else None
+    dYh = synth.draw_dY_head(wl, positives=pos, perm=perm) if wl.H else None
+    gen_s = time.perf_counter() - t0
+    print(f"[bench] {wl.name}: inputs drawn in {gen_s:.1f}s", file=sys.stderr, flush=True)
+
+    def up(a):
+        if a is None:
+            return None
+        a = np.ascontiguousarray(a)
+        return torch.from_numpy(a.view(np.int16) if a.dtype == np.uint16 else a).to(dev)
+
+    is_bf = wl.dtype == synth.DT_BF16
+    odt = torch.int16 if is_bf else torch.float32
+    Xd, Wd, idxd, dYd = up(X), up(W), up(idx), up(dY)
+    desc = hs.make_desc(wl.B, wl.F_s, wl.L, wl.G, wl.F_in, wl.dtype)
+    Y = torch.empty((wl.B, wl.L), dtype=odt, device=dev)
+    dW = torch.empty((wl.L, wl.F_in), dtype=torch.float32, device=dev)
+    dX = torch.empty((wl.B, wl.F_s), dtype=torch.float32, device=dev)
+    ws_w = hs.workspace(hs.haste_workspace_bytes(desc, hs.HASTE_OP_BWD_W))
+    ws_x = hs.workspace(hs.haste_workspace_bytes(desc, hs.HASTE_OP_BWD_X))
+    if wl.H:
+        Whd, dYhd = up(Wh), up(dYh)
+        Yh = torch.empty((wl.B, wl.H), dtype=odt, device=dev)
+        dWh = torch.empty((wl.H, wl.F_s), dtype=torch.float32, device=dev)
+        ws_h = hs.workspace(hs.haste_head_workspace_bytes(wl.B, wl.F_s, wl.H, wl.dtype))
+    torch.cuda.synchronize()
+
+    calls = [("fwd", lambda: hs.haste_fwd(desc, Xd, idxd, Wd, None, Y))]
+    if wl.H:
+        calls.append(("head_fwd", lambda: hs.haste_head_fwd(wl.B, wl.F_s, wl.H, wl.dtype, Xd, Whd, None, Yh)))
+    calls.append(("bwd_w", lambda: hs.haste_bwd_w(desc, Xd, idxd, dYd, dW, None, 0, ws_w)))
+    calls.append(("bwd_x", lambda: hs.haste_bwd_x(desc, idxd, Wd, dYd, dX, 0, ws_x)))
+    if wl.H:
+        calls.append(("head_bwd", lambda: hs.haste_head_bwd(wl.B, wl.F_s, wl.H, wl.dtype, Xd, Whd, dYhd, dWh, dX,
+                                                            1, ws_h)))
+
+    for _ in range(args.warmup):
+        for _, fn in calls:
+            fn()
+    torch.cuda.synchronize()
+
+    # timed region: K steps, events between the calls on the launch stream
+    stream = torch.cuda.current_stream()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(calls) + 1)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    for s in range(args.steps):
+        evs[s][0].record(stream)
+        for i, (_, fn) in enumerate(calls):
+            fn()
+            evs[s][i + 1].record(stream)
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - w0) * 1e3
+    per_call = {name: 0.0 for name, _ in calls}
+    step_ms = 0.0
+    for s in range(args.steps):
+        step_ms += evs[s][0].elapsed_time(evs[s][-1])
+        for i, (name, _) in enumerate(calls):
+            per_call[name] += evs[s][i].elapsed_time(evs[s][i + 1])
+    step_ms /= args.steps
+    per_call = {k: v / args.steps for k, v in per_call.items()}
+
+    cost = call_cost(wl, 2 if is_bf else 4)
+    step_bytes = sum(b for b, _ in cost.values())
+    step_flops = sum(f for _, f in cost.values())
+    per_call_detail = {}
+    for name, ms in per_call.items():
+        b, f = cost[name]
+        per_call_detail[name] = {"ms": round(ms, 4), "GBps": round(b / ms / 1e6, 1),
+                                 "TFLOPs": round(f / ms / 1e9, 1), "alg_bytes": b, "flops": f}
+    dom = max(per_call, key=per_call.get)
+    db, df = cost[dom]
+    achieved = db / per_call[dom] / 1e6
+    roof = {"kernel": dom, "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": measured_traffic(wl.name, dom),
+            "alg_bytes_per_launch": db, "avg_launch_ms": round(per_call[dom], 4)}
+
+    out = {
+        "metric": "fwd+bwd ms/step (bf16, 3M-label tail); HBM GB/s and MFMA % of peak",
+        "value": round(step_ms, 4), "unit": "ms/step", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(step_ms, 4), "higher_is_better": False, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16" if is_bf else "f32", "data": "synthetic (seeded; see synth/)",
+        "config": {"workload": wl.name, "B": wl.B, "F_s": wl.F_s, "L_tail": wl.L, "G": wl.G, "F_in": wl.F_in,
+                   "H_head": wl.H, "parallelism": "single GPU"},
+        "labels_samples_per_s": round(wl.B * (wl.L + wl.H) / (step_ms / 1e3), 1),
+        "step_hbm_GBps": round(step_bytes / step_ms / 1e6, 1),
+        "step_hbm_frac": round(step_bytes / step_ms / 1e6 / HBM_PEAK_GBPS, 4),
+        "step_mfma_pct": round(100 * step_flops / (step_ms / 1e3) / (MFMA_BF16_PEAK_TFLOPS * 1e12), 2),
+        "wall_ms_per_step": round(wall_ms / args.steps, 4),
+        "per_call": per_call_detail,
+        "roofline": roof,
+    }
+
+    if not args.no_bottleneck and is_bf:
+        out["dense_bottleneck"] = bottleneck(wl, Xd, Wd, dYd, args)
+        out["tail_vs_bottleneck"] = round(sum(per_call[k] for k in ("fwd", "bwd_w", "bwd_x")) /
+                                          out["dense_bottleneck"]["ms"], 3)
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(wl, X, idx, W, dY, Wh, dYh)
+    print(json.dumps(out), flush=True)
+
+
+def bottleneck(wl, Xd, Wd, dYd, args):
+    """FLOPs-matched dense bottleneck: a dense layer of width F_in over all L labels, fwd + dW + dX
+    via torch.matmul (hipBLASLt), bf16 in and out, every operand contiguous."""
+    import torch
+    bf = lambda t: t.view(torch.bfloat16)
+    Xr = bf(Xd)[:, : wl.F_in].contiguous()            # [B, F_in]
+    Wt = bf(Wd).t().contiguous()                       # [F_in, L]
+    Wn = bf(Wd)                                        # [L, F_in]
+    dY = bf(dYd)                                       # [B, L]
+    dYt = dY.t().contiguous()                          # [L, B]
+    ops = [lambda: torch.matmul(Xr, Wt), lambda: torch.matmul(dYt, Xr), lambda: torch.matmul(dY, Wn)]
+    for _ in range(args.warmup):
+        for f in ops:
+            f()
+    torch.cuda.synchronize()
+    st = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(st)
+    for _ in range(args.steps):
+        for f in ops:
+            f()
+    e1.record(st)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    del Wt, dYt
+    return {"ms": round(ms, 4), "what": "[B,F_in]x[F_in,L] fwd + dW + dX, torch.matmul bf16 (dW, dX in bf16)"}
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,148 @@
+/*
+ * haste.h - C ABI of libhaste.so, the MI355X (gfx950) implementation of the group-shared fixed
+ * fan-in (GS-FFI) output layer and its dense head.
+ *
+ * The layer (paper, Section 3.1): L labels are split into K = L/G groups of exactly G labels.
+ * Labels of a group are contiguous, so label l belongs to group g(l) = l / G.  Group k owns one
+ * support I_k of F_in input features, stored as row k of idx[K, F_in].  Label l keeps its own
+ * weight vector W[l, 0..F_in-1]; slot t of that vector multiplies feature idx[g(l), t].
+ * G = 1 is standard (per-label) fixed fan-in: idx then has L rows.
+ *
+ * Conventions shared by every entry point:
+ *   - All array arguments are DEVICE pointers owned by the caller, dense, row-major, and aligned
+ *     to at least 16 bytes.  The library never allocates, frees or copies them.
+ *   - "dtype" selects the storage type of X, W, Y, dY (and W_head, Y_h, dY_h):
+ *       HASTE_DTYPE_F32  - IEEE fp32, all arithmetic fp32;
+ *       HASTE_DTYPE_BF16 - bf16 storage, products accumulated in fp32, bf16 outputs rounded to
+ *                          nearest-even.
+ *     bias, dbias, dW, dX and dW_head are always fp32.
+ *   - idx is int32.  Every row must be strictly increasing and lie in [0, F_s): a precondition,
+ *     not checked per call (haste_validate_idx checks it).
+ *   - "stream" is a hipStream_t passed as void* (NULL = the default stream).  Every call only
+ *     enqueues work on that stream and returns; a kernel fault surfaces at the caller's next
+ *     synchronisation.  Calls never synchronise the device.
+ *   - "ws" is caller-owned device scratch of ws_bytes bytes; the required size is given by
+ *     haste_workspace_bytes / haste_head_workspace_bytes.  Concurrent calls must use distinct
+ *     workspaces.
+ *   - Return value: HASTE_OK, or an error code; on error nothing is launched and
+ *     haste_last_error() describes the cause (per calling thread).
+ *   - 64-bit sizes throughout; B * L may exceed 2^31.
+ */
+#ifndef HASTE_H_
+#define HASTE_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum haste_dtype { HASTE_DTYPE_F32 = 0, HASTE_DTYPE_BF16 = 1 };
+
+enum haste_status {
+    HASTE_OK = 0,
+    HASTE_ERR_INVALID = 1,      /* bad shape, null pointer, misalignment, L % G != 0 ...   */
+    HASTE_ERR_UNSUPPORTED = 2,  /* valid arguments outside what the kernels implement      */
+    HASTE_ERR_WORKSPACE = 3,    /* ws_bytes smaller than the reported requirement           */
+    HASTE_ERR_HIP = 4           /* the HIP runtime refused a launch                         */
+};
+
+/* Workspace-query operation codes. */
+enum haste_op { HASTE_OP_FWD = 0, HASTE_OP_BWD_W = 1, HASTE_OP_BWD_X = 2 };
+
+/* Shape of one sparse tail layer. */
+typedef struct haste_desc {
+    int64_t B;      /* batch rows (>= 0)                                         */
+    int64_t F_s;    /* input feature width (> 0)                                 */
+    int64_t L;      /* tail labels (>= 0), a multiple of G                       */
+    int64_t G;      /* labels per group (> 0)                                    */
+    int64_t F_in;   /* support size per group, fixed fan-in (1 <= F_in <= F_s)   */
+    int32_t dtype;  /* enum haste_dtype                                          */
+    int32_t reserved;  /* must be 0                                              */
+} haste_desc_t;
+
+/*
+ * Forward logits of the tail (Section 3.1 logit; Section 3.2 "gather-once and dense MMA"):
+ *   Y[b, l] = bias[l] + sum_{t < F_in} X[b, idx[l/G, t]] * W[l, t]
+ * X[B, F_s], idx[L/G, F_in] int32, W[L, F_in], bias[L] fp32 or NULL (no bias), Y[B, L] (dtype),
+ * overwritten.
+ */
+int haste_fwd(const haste_desc_t *desc, const void *X, const int32_t *idx, const void *W,
+              const float *bias, void *Y, void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * Backward-weight of the tail (Section 3.2: grad W_k = (grad Z_k)^T H_k, formed only on the
+ * support of each group):
+ *   dW[l, t] = beta * dW[l, t] + sum_b dY[b, l] * X[b, idx[l/G, t]]
+ *   dbias[l] = beta * dbias[l] + sum_b dY[b, l]            (skipped when dbias is NULL)
+ * dY[B, L] (dtype); dW[L, F_in] fp32; beta is 0 (overwrite) or 1 (accumulate).
+ */
+int haste_bwd_w(const haste_desc_t *desc, const void *X, const int32_t *idx, const void *dY,
+                float *dW, float *dbias, int beta, void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * Backward-feature of the tail (Section 3.2: grad h_{:, I_k} += grad Z_k W_k, reduced over all
+ * groups with a split over the label dimension):
+ *   dX[b, f] = beta * dX[b, f] + sum_k sum_{t : idx[k,t] = f} sum_{j < G} dY[b, kG+j] * W[kG+j, t]
+ * dX[B, F_s] fp32; beta is 0 (overwrite) or 1 (accumulate).  Partial sums over label segments
+ * live in ws and are reduced in a fixed segment order.
+ */
+int haste_bwd_x(const haste_desc_t *desc, const int32_t *idx, const void *W, const void *dY,
+                float *dX, int beta, void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * Dense head forward (Section 3.3: a^H = W_head h_head):
+ *   Y_h[b, h] = bias_h[h] + sum_f X[b, f] * W_head[h, f]
+ * X[B, F_s], W_head[H, F_s] (dtype), bias_h[H] fp32 or NULL, Y_h[B, H] (dtype) overwritten.
+ */
+int haste_head_fwd(int64_t B, int64_t F_s, int64_t H, int32_t dtype, const void *X,
+                   const void *W_head, const float *bias_h, void *Y_h, void *stream);
+
+/*
+ * Dense head backward (Section 3.3 objective, head branch):
+ *   dW_h[h, f] = sum_b dY_h[b, h] * X[b, f]                        (overwritten, fp32)
+ *   dX[b, f]   = beta_dx * dX[b, f] + sum_h dY_h[b, h] * W_head[h, f]
+ * beta_dx = 1 adds the head's input gradient onto an existing one (e.g. the tail's when both
+ * branches read the same X).  dW_h or dX may be NULL to skip that product.  ws holds the
+ * split-K partials of dX (haste_head_workspace_bytes).
+ */
+int haste_head_bwd(int64_t B, int64_t F_s, int64_t H, int32_t dtype, const void *X,
+                   const void *W_head, const void *dY_h, float *dW_h, float *dX, int beta_dx,
+                   void *ws, size_t ws_bytes, void *stream);
+
+/* Bytes of workspace `op` (enum haste_op) needs for this layer; 0 if none.  Never fails; for an
+ * invalid descriptor it returns 0 and the call itself reports the error. */
+size_t haste_workspace_bytes(const haste_desc_t *desc, int op);
+
+/* Bytes of workspace haste_head_bwd needs. */
+size_t haste_head_workspace_bytes(int64_t B, int64_t F_s, int64_t H, int32_t dtype);
+
+/*
+ * Debug check of the idx precondition: *n_bad_rows (device int32, overwritten) receives the
+ * number of rows of idx[n_rows, F_in] that are not strictly increasing within [0, F_s).
+ * n_rows = L/G (or L when G = 1).
+ */
+int haste_validate_idx(const haste_desc_t *desc, const int32_t *idx, int32_t *n_bad_rows,
+                       void *stream);
+
+/*
+ * Debug export of the gather step (Section 3.2, H_k = h_{:, I_k}): for groups k in [k0, k0+nk)
+ *   out[k - k0, b, t] = X[b, idx[k, t]]      out is [nk, B, F_in] in the dtype of X (bit copy).
+ */
+int haste_debug_gather(const haste_desc_t *desc, const void *X, const int32_t *idx, int64_t k0,
+                       int64_t nk, void *out, void *stream);
+
+/* Human-readable name of a status code (static storage). */
+const char *haste_status_str(int status);
+
+/* Message for the last error on the calling thread ("" if none). */
+const char *haste_last_error(void);
+
+/* Library version string. */
+const char *haste_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* HASTE_H_ */

@@ -1,0 +1,240 @@
+// C ABI of libhaste.so: argument validation, kernel selection and launch on the caller's stream.
+// Nothing here allocates, frees or synchronises; scratch comes only from the caller's workspace.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "common.hpp"
+
+namespace {
+
+thread_local char g_err[512];
+
+int fail(int code, const char *fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof g_err, fmt, ap);
+    va_end(ap);
+    return code;
+}
+
+int ok() {
+    g_err[0] = 0;
+    return HASTE_OK;
+}
+
+int hip_status(hipError_t e, const char *what) {
+    if (e == hipSuccess) return ok();
+    return fail(HASTE_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+int check_desc(const haste_desc_t *d) {
+    if (!d) return fail(HASTE_ERR_INVALID, "desc is NULL");
+    if (d->reserved != 0) return fail(HASTE_ERR_INVALID, "desc.reserved must be 0");
+    if (d->dtype != HASTE_DTYPE_F32 && d->dtype != HASTE_DTYPE_BF16)
+        return fail(HASTE_ERR_INVALID, "dtype %d is neither HASTE_DTYPE_F32 nor HASTE_DTYPE_BF16", d->dtype);
+    if (d->B < 0 || d->L < 0) return fail(HASTE_ERR_INVALID, "B and L must be >= 0");
+    if (d->F_s <= 0 || d->F_s > INT32_MAX) return fail(HASTE_ERR_INVALID, "F_s must be in [1, 2^31)");
+    if (d->G <= 0) return fail(HASTE_ERR_INVALID, "G must be > 0");
+    if (d->L % d->G != 0) return fail(HASTE_ERR_INVALID, "L (%lld) must be a multiple of G (%lld)", (long long)d->L,
+                                      (long long)d->G);
+    if (d->F_in < 1 || d->F_in > d->F_s) return fail(HASTE_ERR_INVALID, "F_in must be in [1, F_s]");
+    if (d->B > INT32_MAX || d->G > INT32_MAX) return fail(HASTE_ERR_INVALID, "B and G must be < 2^31");
+    if (d->F_s > kMaxFs)
+        return fail(HASTE_ERR_UNSUPPORTED, "F_s = %lld exceeds the supported maximum %d", (long long)d->F_s, kMaxFs);
+    return HASTE_OK;
+}
+
+int need_ptr(const void *p, const char *name) {
+    if (!p) return fail(HASTE_ERR_INVALID, "%s is NULL", name);
+    if (!aligned16(p)) return fail(HASTE_ERR_INVALID, "%s is not 16-byte aligned", name);
+    return HASTE_OK;
+}
+
+haste::TailArgs targs(const haste_desc_t *d) { return haste::TailArgs{d->B, d->F_s, d->L, d->G, d->F_in, d->dtype}; }
+
+hipStream_t as_stream(void *s) { return reinterpret_cast<hipStream_t>(s); }
+
+#define TRY(x)                      \
+    do {                            \
+        int _rc = (x);              \
+        if (_rc != HASTE_OK) return _rc; \
+    } while (0)
+
+}  // namespace
+
+extern "C" {
+
+const char *haste_version(void) { return "haste-mi355x 0.1 (gfx950)"; }
+
+const char *haste_status_str(int status) {
+    switch (status) {
+        case HASTE_OK: return "ok";
+        case HASTE_ERR_INVALID: return "invalid argument";
+        case HASTE_ERR_UNSUPPORTED: return "unsupported";
+        case HASTE_ERR_WORKSPACE: return "workspace too small";
+        case HASTE_ERR_HIP: return "HIP error";
+    }
+    return "unknown status";
+}
+
+const char *haste_last_error(void) { return g_err; }
+
+size_t haste_workspace_bytes(const haste_desc_t *d, int op) {
+    if (check_desc(d) != HASTE_OK) return 0;
+    const haste::TailArgs a = targs(d);
+    if (a.B == 0 || a.L == 0) return 0;
+    switch (op) {
+        case HASTE_OP_FWD: return 0;
+        case HASTE_OP_BWD_W: return haste::bwd_w_mfma_supported(a) ? haste::bwd_w_mfma_ws(a) : 0;
+        case HASTE_OP_BWD_X: return haste::bwd_x_mfma_supported(a) ? haste::bwd_x_mfma_ws(a) : haste::bwd_x_valu_ws(a);
+    }
+    return 0;
+}
+
+size_t haste_head_workspace_bytes(int64_t B, int64_t F_s, int64_t H, int32_t dtype) {
+    if (B <= 0 || F_s <= 0 || H <= 0) return 0;
+    return haste::head_ws(B, F_s, H, dtype);
+}
+
+int haste_fwd(const haste_desc_t *d, const void *X, const int32_t *idx, const void *W, const float *bias, void *Y,
+              void *ws, size_t ws_bytes, void *stream) {
+    (void)ws;
+    (void)ws_bytes;
+    TRY(check_desc(d));
+    const haste::TailArgs a = targs(d);
+    if (a.B == 0 || a.L == 0) return ok();
+    TRY(need_ptr(X, "X"));
+    TRY(need_ptr(idx, "idx"));
+    TRY(need_ptr(W, "W"));
+    TRY(need_ptr(Y, "Y"));
+    if (bias && !aligned16(bias)) return fail(HASTE_ERR_INVALID, "bias is not 16-byte aligned");
+    if (haste::fwd_mfma_supported(a)) return hip_status(haste::fwd_mfma(a, X, idx, W, bias, Y, as_stream(stream)), "haste_fwd");
+    if (!haste::valu_supported(a)) return fail(HASTE_ERR_UNSUPPORTED, "no forward kernel for this shape");
+    return hip_status(haste::fwd_valu(a, X, idx, W, bias, Y, as_stream(stream)), "haste_fwd");
+}
+
+int haste_bwd_w(const haste_desc_t *d, const void *X, const int32_t *idx, const void *dY, float *dW, float *dbias,
+                int beta, void *ws, size_t ws_bytes, void *stream) {
+    TRY(check_desc(d));
+    if (beta != 0 && beta != 1) return fail(HASTE_ERR_INVALID, "beta must be 0 or 1");
+    const haste::TailArgs a = targs(d);
+    hipStream_t s = as_stream(stream);
+    if (a.L == 0) return ok();
+    TRY(need_ptr(dW, "dW"));
+    if (dbias && !aligned16(dbias)) return fail(HASTE_ERR_INVALID, "dbias is not 16-byte aligned");
+    if (a.B == 0) {  // empty batch: the sum is zero
+        if (beta) return ok();
+        hipError_t e = haste::fill_f32(dW, a.L * a.F_in, 0.0f, s);
+        if (e == hipSuccess && dbias) e = haste::fill_f32(dbias, a.L, 0.0f, s);
+        return hip_status(e, "haste_bwd_w");
+    }
+    TRY(need_ptr(X, "X"));
+    TRY(need_ptr(idx, "idx"));
+    TRY(need_ptr(dY, "dY"));
+    if (haste::bwd_w_mfma_supported(a)) {
+        const size_t need = haste::bwd_w_mfma_ws(a);
+        if (!ws || ws_bytes < need)
+            return fail(HASTE_ERR_WORKSPACE, "haste_bwd_w needs %zu workspace bytes, got %zu", need, ws ? ws_bytes : 0);
+        TRY(need_ptr(ws, "ws"));
+        return hip_status(haste::bwd_w_mfma(a, X, idx, dY, dW, dbias, beta, ws, s), "haste_bwd_w");
+    }
+    if (!haste::valu_supported(a)) return fail(HASTE_ERR_UNSUPPORTED, "no backward-weight kernel for this shape");
+    return hip_status(haste::bwd_w_valu(a, X, idx, dY, dW, dbias, beta, s), "haste_bwd_w");
+}
+
+int haste_bwd_x(const haste_desc_t *d, const int32_t *idx, const void *W, const void *dY, float *dX, int beta,
+                void *ws, size_t ws_bytes, void *stream) {
+    TRY(check_desc(d));
+    if (beta != 0 && beta != 1) return fail(HASTE_ERR_INVALID, "beta must be 0 or 1");
+    const haste::TailArgs a = targs(d);
+    hipStream_t s = as_stream(stream);
+    if (a.B == 0) return ok();
+    TRY(need_ptr(dX, "dX"));
+    if (a.L == 0) {  // no labels: nothing flows back
+        if (beta) return ok();
+        return hip_status(haste::fill_f32(dX, a.B * a.F_s, 0.0f, s), "haste_bwd_x");
+    }
+    TRY(need_ptr(idx, "idx"));
+    TRY(need_ptr(W, "W"));
+    TRY(need_ptr(dY, "dY"));
+    const bool mf = haste::bwd_x_mfma_supported(a);
+    if (!mf && !haste::valu_supported(a)) return fail(HASTE_ERR_UNSUPPORTED, "no backward-feature kernel for this shape");
+    const size_t need = mf ? haste::bwd_x_mfma_ws(a) : haste::bwd_x_valu_ws(a);
+    if (!ws || ws_bytes < need)
+        return fail(HASTE_ERR_WORKSPACE, "haste_bwd_x needs %zu workspace bytes, got %zu", need, ws ? ws_bytes : 0);
+    TRY(need_ptr(ws, "ws"));
+    if (mf) return hip_status(haste::bwd_x_mfma(a, idx, W, dY, dX, beta, ws, s), "haste_bwd_x");
+    return hip_status(haste::bwd_x_valu(a, idx, W, dY, dX, beta, ws, s), "haste_bwd_x");
+}
+
+static int check_head(int64_t B, int64_t F_s, int64_t H, int32_t dtype) {
+    if (dtype != HASTE_DTYPE_F32 && dtype != HASTE_DTYPE_BF16) return fail(HASTE_ERR_INVALID, "bad dtype %d", dtype);
+    if (B < 0 || F_s <= 0 || H < 0) return fail(HASTE_ERR_INVALID, "head needs B >= 0, F_s > 0, H >= 0");
+    if (B > INT32_MAX || F_s > INT32_MAX) return fail(HASTE_ERR_INVALID, "B and F_s must be < 2^31");
+    return HASTE_OK;
+}
+
+int haste_head_fwd(int64_t B, int64_t F_s, int64_t H, int32_t dtype, const void *X, const void *W_head,
+                   const float *bias_h, void *Y_h, void *stream) {
+    TRY(check_head(B, F_s, H, dtype));
+    if (B == 0 || H == 0) return ok();
+    TRY(need_ptr(X, "X"));
+    TRY(need_ptr(W_head, "W_head"));
+    TRY(need_ptr(Y_h, "Y_h"));
+    if (bias_h && !aligned16(bias_h)) return fail(HASTE_ERR_INVALID, "bias_h is not 16-byte aligned");
+    return hip_status(haste::head_fwd(B, F_s, H, dtype, X, W_head, bias_h, Y_h, as_stream(stream)), "haste_head_fwd");
+}
+
+int haste_head_bwd(int64_t B, int64_t F_s, int64_t H, int32_t dtype, const void *X, const void *W_head,
+                   const void *dY_h, float *dW_h, float *dX, int beta_dx, void *ws, size_t ws_bytes, void *stream) {
+    TRY(check_head(B, F_s, H, dtype));
+    if (beta_dx != 0 && beta_dx != 1) return fail(HASTE_ERR_INVALID, "beta_dx must be 0 or 1");
+    hipStream_t s = as_stream(stream);
+    if (dW_h) TRY(need_ptr(dW_h, "dW_h"));
+    if (dX) TRY(need_ptr(dX, "dX"));
+    if (H == 0) {
+        if (dX && !beta_dx) return hip_status(haste::fill_f32(dX, B * F_s, 0.0f, s), "haste_head_bwd");
+        return ok();
+    }
+    if (B == 0) {
+        if (dW_h) return hip_status(haste::fill_f32(dW_h, H * F_s, 0.0f, s), "haste_head_bwd");
+        return ok();
+    }
+    TRY(need_ptr(dY_h, "dY_h"));
+    if (dW_h) TRY(need_ptr(X, "X"));
+    if (dX) {
+        TRY(need_ptr(W_head, "W_head"));
+        const size_t need = haste::head_ws(B, F_s, H, dtype);
+        if (!ws || ws_bytes < need)
+            return fail(HASTE_ERR_WORKSPACE, "haste_head_bwd needs %zu workspace bytes, got %zu", need, ws ? ws_bytes : 0);
+        TRY(need_ptr(ws, "ws"));
+    }
+    return hip_status(haste::head_bwd(B, F_s, H, dtype, X, W_head, dY_h, dW_h, dX, beta_dx, ws, s), "haste_head_bwd");
+}
+
+int haste_validate_idx(const haste_desc_t *d, const int32_t *idx, int32_t *n_bad_rows, void *stream) {
+    TRY(check_desc(d));
+    if (!n_bad_rows) return fail(HASTE_ERR_INVALID, "n_bad_rows is NULL");
+    const int64_t rows = d->L / d->G;
+    if (rows > 0) TRY(need_ptr(idx, "idx"));
+    return hip_status(haste::validate_idx(idx, rows, d->F_in, d->F_s, n_bad_rows, as_stream(stream)),
+                      "haste_validate_idx");
+}
+
+int haste_debug_gather(const haste_desc_t *d, const void *X, const int32_t *idx, int64_t k0, int64_t nk, void *out,
+                       void *stream) {
+    TRY(check_desc(d));
+    const int64_t K = d->L / d->G;
+    if (k0 < 0 || nk < 0 || k0 + nk > K) return fail(HASTE_ERR_INVALID, "group range [k0, k0+nk) outside [0, L/G)");
+    if (nk == 0 || d->B == 0) return ok();
+    TRY(need_ptr(X, "X"));
+    TRY(need_ptr(idx, "idx"));
+    TRY(need_ptr(out, "out"));
+    return hip_status(haste::debug_gather(X, d->dtype, idx, d->B, d->F_s, d->F_in, k0, nk, out, as_stream(stream)),
+                      "haste_debug_gather");
+}
+
+}  // extern "C"

@@ -1,0 +1,99 @@
+// Internal declarations shared by the HIP translation units of libhaste.so (gfx950 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "haste.h"
+
+typedef uint16_t bf16_t;  // bf16 bit pattern
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+// Hardware layout facts used by every kernel (CDNA4, 64-wide wavefronts).
+constexpr int kWave = 64;
+constexpr int kXcds = 8;          // MI355X: 8 XCDs, workgroups dispatched round-robin over them
+constexpr int kCusPerXcd = 32;    // 256 CUs in total
+constexpr int kMaxFs = 1024;      // widest input feature dimension the on-chip tiles are sized for
+
+__device__ __forceinline__ float bf16_to_f32(bf16_t v) { return __uint_as_float(((uint32_t)v) << 16); }
+
+// fp32 -> bf16, round to nearest even (finite inputs; the hardware conversion on gfx950).
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) {
+    __bf16 h = (__bf16)f;
+    return __builtin_bit_cast(bf16_t, h);
+}
+
+__device__ __forceinline__ float load_f32(const float *p, int64_t i) { return p[i]; }
+__device__ __forceinline__ float load_f32(const bf16_t *p, int64_t i) { return bf16_to_f32(p[i]); }
+__device__ __forceinline__ void store_out(float *p, int64_t i, float v) { p[i] = v; }
+__device__ __forceinline__ void store_out(bf16_t *p, int64_t i, float v) { p[i] = f32_to_bf16(v); }
+
+// D(32x32, fp32) += A(32x16, bf16) * B(16x32, bf16).
+// Lane l holds A[l % 32][8*(l/32) .. +7], B[8*(l/32) .. +7][l % 32] and
+// D[8*i + 4*(l/32) + j][l % 32] in register 4*i + j.
+__device__ __forceinline__ f32x16_t mfma32x32x16(const bf16x8_t &a, const bf16x8_t &b, const f32x16_t &c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8_t, v); }
+
+__device__ __forceinline__ uint32_t pack2(bf16_t lo, bf16_t hi) { return (uint32_t)lo | ((uint32_t)hi << 16); }
+
+// ---- host-side launchers (one translation unit each) -----------------------------------------
+namespace haste {
+
+struct TailArgs {
+    int64_t B, F_s, L, G, F_in;
+    int32_t dtype;
+};
+
+// tail, MFMA (bf16)
+bool fwd_mfma_supported(const TailArgs &a);
+hipError_t fwd_mfma(const TailArgs &a, const void *X, const int32_t *idx, const void *W, const float *bias,
+                    void *Y, hipStream_t s);
+bool bwd_w_mfma_supported(const TailArgs &a);
+size_t bwd_w_mfma_ws(const TailArgs &a);
+hipError_t bwd_w_mfma(const TailArgs &a, const void *X, const int32_t *idx, const void *dY, float *dW,
+                      float *dbias, int beta, void *ws, hipStream_t s);
+bool bwd_x_mfma_supported(const TailArgs &a);
+size_t bwd_x_mfma_ws(const TailArgs &a);
+hipError_t bwd_x_mfma(const TailArgs &a, const int32_t *idx, const void *W, const void *dY, float *dX, int beta,
+                      void *ws, hipStream_t s);
+
+// tail, VALU (fp32 and bf16, any G including per-label fixed fan-in)
+bool valu_supported(const TailArgs &a);
+hipError_t fwd_valu(const TailArgs &a, const void *X, const int32_t *idx, const void *W, const float *bias,
+                    void *Y, hipStream_t s);
+hipError_t bwd_w_valu(const TailArgs &a, const void *X, const int32_t *idx, const void *dY, float *dW,
+                      float *dbias, int beta, hipStream_t s);
+size_t bwd_x_valu_ws(const TailArgs &a);
+hipError_t bwd_x_valu(const TailArgs &a, const int32_t *idx, const void *W, const void *dY, float *dX, int beta,
+                      void *ws, hipStream_t s);
+
+// dense head
+size_t head_ws(int64_t B, int64_t F_s, int64_t H, int32_t dtype);
+hipError_t head_fwd(int64_t B, int64_t F_s, int64_t H, int32_t dtype, const void *X, const void *Wh,
+                    const float *bias_h, void *Yh, hipStream_t s);
+hipError_t head_bwd(int64_t B, int64_t F_s, int64_t H, int32_t dtype, const void *X, const void *Wh,
+                    const void *dYh, float *dWh, float *dX, int beta_dx, void *ws, hipStream_t s);
+
+// utilities
+hipError_t fill_f32(float *p, int64_t n, float v, hipStream_t s);
+hipError_t scale_f32(float *p, int64_t n, float beta, hipStream_t s);
+// dX[b, f] = beta*dX[b, f] + sum_s part[s][f][b]   (part is [S][F_s][ldp], feature-major)
+hipError_t reduce_fmajor(const float *part, int S, int64_t ldp, int64_t B, int64_t F_s, float *dX, int beta,
+                         hipStream_t s);
+// C[m, n] = beta*C[m, n] + sum_s part[s][m][n]     (part is [S][M][N], row-major)
+hipError_t reduce_rmajor(const float *part, int S, int64_t M, int64_t N, float *C, int beta, hipStream_t s);
+hipError_t validate_idx(const int32_t *idx, int64_t rows, int64_t F_in, int64_t F_s, int32_t *n_bad,
+                        hipStream_t s);
+hipError_t debug_gather(const void *X, int32_t dtype, const int32_t *idx, int64_t B, int64_t F_s, int64_t F_in,
+                        int64_t k0, int64_t nk, void *out, hipStream_t s);
+
+inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+inline int64_t round_up(int64_t a, int64_t b) { return cdiv(a, b) * b; }
+
+}  // namespace haste

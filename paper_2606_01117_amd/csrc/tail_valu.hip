@@ -1,0 +1,240 @@
+// Group-shared fixed fan-in tail on the vector ALUs (fp32 FMA), for any G including G = 1.
+//
+// Used for fp32 layers (the paper's logit definition, Section 3.1, evaluated with true fp32
+// products: gfx950 has no reduced-precision fp32 matrix path to fall into) and as the standard
+// per-label fixed fan-in comparator (G = 1, Section 3.1 / Fig. 2(c)): every label gathers its own
+// F_in features, so there is no shared tile and the work is thin dot products.
+//
+// A batch tile of TB rows of X is kept transposed in LDS as fp32 (xs[f][b], row stride TB+4
+// floats so 16-byte reads stay aligned).  One thread owns one label.
+#include "common.hpp"
+
+namespace {
+
+constexpr int TB = 16;        // batch rows per tile
+constexpr int XS = TB + 4;    // LDS row stride (floats) of the transposed tile
+
+template <typename T>
+__device__ __forceinline__ void load_slab(float *xs, const T *__restrict__ X, int b0, int B, int F_s) {
+    for (int e = threadIdx.x; e < TB * F_s; e += blockDim.x) {
+        const int r = e / F_s, f = e - r * F_s;
+        const int b = b0 + r;
+        xs[f * XS + r] = (b < B) ? load_f32(X, (int64_t)b * F_s + f) : 0.0f;
+    }
+}
+
+// Y[b, l] = bias[l] + sum_t X[b, idx[l/G, t]] * W[l, t]
+template <typename T>
+__global__ __launch_bounds__(256) void k_fwd_valu(const T *__restrict__ X, const int32_t *__restrict__ idx,
+                                                  const T *__restrict__ W, const float *__restrict__ bias,
+                                                  T *__restrict__ Y, int B, int F_s, int64_t L, int G, int F_in,
+                                                  int64_t nlt) {
+    extern __shared__ __align__(16) float xs[];
+    const int b0 = blockIdx.y * TB;
+    load_slab(xs, X, b0, B, F_s);
+    __syncthreads();
+    for (int64_t lt = blockIdx.x; lt < nlt; lt += gridDim.x) {
+        const int64_t l = lt * blockDim.x + threadIdx.x;
+        if (l >= L) continue;
+        const int64_t g = l / G;
+        float acc[TB];
+#pragma unroll
+        for (int b = 0; b < TB; ++b) acc[b] = 0.0f;
+        const int32_t *ip = idx + g * F_in;
+        const T *wp = W + l * F_in;
+        for (int t = 0; t < F_in; ++t) {
+            const int f = ip[t];
+            const float w = load_f32(wp, t);
+            const float4 *xr = reinterpret_cast<const float4 *>(xs + f * XS);
+#pragma unroll
+            for (int q = 0; q < TB / 4; ++q) {
+                const float4 x = xr[q];
+                acc[4 * q + 0] = fmaf(x.x, w, acc[4 * q + 0]);
+                acc[4 * q + 1] = fmaf(x.y, w, acc[4 * q + 1]);
+                acc[4 * q + 2] = fmaf(x.z, w, acc[4 * q + 2]);
+                acc[4 * q + 3] = fmaf(x.w, w, acc[4 * q + 3]);
+            }
+        }
+        const float bv = bias ? bias[l] : 0.0f;
+#pragma unroll
+        for (int b = 0; b < TB; ++b)
+            if (b0 + b < B) store_out(Y, (int64_t)(b0 + b) * L + l, acc[b] + bv);
+    }
+}
+
+// dW[l, t] = beta*dW + sum_b dY[b, l] * X[b, idx[l/G, t]];  dbias[l] = beta*dbias + sum_b dY[b, l]
+template <typename T>
+__global__ __launch_bounds__(256) void k_bwd_w_valu(const T *__restrict__ X, const int32_t *__restrict__ idx,
+                                                    const T *__restrict__ dY, float *__restrict__ dW,
+                                                    float *__restrict__ dbias, int beta, int B, int F_s, int64_t L,
+                                                    int G, int F_in) {
+    extern __shared__ __align__(16) float xs[];
+    const int64_t l = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const bool valid = l < L;
+    const int64_t g = valid ? l / G : 0;
+    constexpr int TC = 32;  // support slots per pass (register accumulators)
+    for (int tc = 0; tc < F_in; tc += TC) {
+        float acc[TC];
+#pragma unroll
+        for (int t = 0; t < TC; ++t) acc[t] = 0.0f;
+        float db = 0.0f;
+        const int nt = F_in - tc < TC ? F_in - tc : TC;
+        for (int b0 = 0; b0 < B; b0 += TB) {
+            __syncthreads();
+            load_slab(xs, X, b0, B, F_s);
+            __syncthreads();
+            if (valid) {
+                float dy[TB];
+#pragma unroll
+                for (int b = 0; b < TB; ++b) dy[b] = (b0 + b < B) ? load_f32(dY, (int64_t)(b0 + b) * L + l) : 0.0f;
+                if (tc == 0) {
+#pragma unroll
+                    for (int b = 0; b < TB; ++b) db += dy[b];
+                }
+#pragma unroll
+                for (int t = 0; t < TC; ++t) {
+                    if (t < nt) {
+                        const int f = idx[g * F_in + tc + t];
+                        const float4 *xr = reinterpret_cast<const float4 *>(xs + f * XS);
+                        float s = 0.0f;
+#pragma unroll
+                        for (int q = 0; q < TB / 4; ++q) {
+                            const float4 x = xr[q];
+                            s = fmaf(x.x, dy[4 * q + 0], s);
+                            s = fmaf(x.y, dy[4 * q + 1], s);
+                            s = fmaf(x.z, dy[4 * q + 2], s);
+                            s = fmaf(x.w, dy[4 * q + 3], s);
+                        }
+                        acc[t] += s;
+                    }
+                }
+            }
+        }
+        if (valid) {
+#pragma unroll
+            for (int t = 0; t < TC; ++t)
+                if (t < nt) {
+                    float *p = dW + l * F_in + tc + t;
+                    *p = beta ? *p + acc[t] : acc[t];
+                }
+            if (tc == 0 && dbias) dbias[l] = beta ? dbias[l] + db : db;
+        }
+    }
+}
+
+// Partial dX^T over one label segment and one batch tile: part[seg][f][b0 + b]
+template <typename T>
+__global__ __launch_bounds__(256) void k_bwd_x_valu(const int32_t *__restrict__ idx, const T *__restrict__ W,
+                                                    const T *__restrict__ dY, float *__restrict__ part, int B,
+                                                    int Bp, int F_s, int64_t L, int G, int F_in, int64_t lps) {
+    extern __shared__ __align__(16) float accs[];  // [F_s][TB]
+    const int64_t seg = blockIdx.x;
+    const int b0 = blockIdx.y * TB;
+    for (int e = threadIdx.x; e < F_s * TB; e += blockDim.x) accs[e] = 0.0f;
+    __syncthreads();
+    const int64_t l_begin = seg * lps;
+    const int64_t l_end = l_begin + lps < L ? l_begin + lps : L;
+    for (int64_t l = l_begin + threadIdx.x; l < l_end; l += blockDim.x) {
+        float dy[TB];
+#pragma unroll
+        for (int b = 0; b < TB; ++b) dy[b] = (b0 + b < B) ? load_f32(dY, (int64_t)(b0 + b) * L + l) : 0.0f;
+        const int64_t g = l / G;
+        for (int t = 0; t < F_in; ++t) {
+            const int f = idx[g * F_in + t];
+            const float w = load_f32(W, l * F_in + t);
+            float *row = accs + f * TB;
+#pragma unroll
+            for (int b = 0; b < TB; ++b)
+                __hip_atomic_fetch_add(row + b, dy[b] * w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        }
+    }
+    __syncthreads();
+    float *pp = part + (size_t)seg * F_s * Bp + b0;
+    for (int e = threadIdx.x; e < F_s * TB; e += blockDim.x) {
+        const int f = e / TB, b = e - f * TB;
+        pp[(size_t)f * Bp + b] = accs[e];
+    }
+}
+
+int64_t bwd_x_valu_segments(const haste::TailArgs &a) {
+    const int64_t nbt = haste::cdiv(a.B, TB);
+    int64_t S = 1024 / (nbt < 1 ? 1 : nbt);
+    const int64_t maxS = haste::cdiv(a.L, 256);
+    if (S > maxS) S = maxS;
+    return S < 1 ? 1 : S;
+}
+
+}  // namespace
+
+namespace haste {
+
+bool valu_supported(const TailArgs &a) {
+    return a.F_s <= kMaxFs && (size_t)a.F_s * XS * 4 <= 150 * 1024;
+}
+
+hipError_t fwd_valu(const TailArgs &a, const void *X, const int32_t *idx, const void *W, const float *bias,
+                    void *Y, hipStream_t s) {
+    const int64_t nbt = cdiv(a.B, TB);
+    const int64_t nlt = cdiv(a.L, 256);
+    int64_t gx = 2048 / nbt;
+    if (gx < 1) gx = 1;
+    if (gx > nlt) gx = nlt;
+    const size_t lds = (size_t)a.F_s * XS * 4;
+    const dim3 grid((unsigned)gx, (unsigned)nbt);
+    if (a.dtype == HASTE_DTYPE_F32) {
+        hipFuncSetAttribute((const void *)k_fwd_valu<float>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        hipLaunchKernelGGL(k_fwd_valu<float>, grid, dim3(256), lds, s, (const float *)X, idx, (const float *)W, bias,
+                           (float *)Y, (int)a.B, (int)a.F_s, a.L, (int)a.G, (int)a.F_in, nlt);
+    } else {
+        hipFuncSetAttribute((const void *)k_fwd_valu<bf16_t>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        hipLaunchKernelGGL(k_fwd_valu<bf16_t>, grid, dim3(256), lds, s, (const bf16_t *)X, idx, (const bf16_t *)W,
+                           bias, (bf16_t *)Y, (int)a.B, (int)a.F_s, a.L, (int)a.G, (int)a.F_in, nlt);
+    }
+    return hipGetLastError();
+}
+
+hipError_t bwd_w_valu(const TailArgs &a, const void *X, const int32_t *idx, const void *dY, float *dW,
+                      float *dbias, int beta, hipStream_t s) {
+    const size_t lds = (size_t)a.F_s * XS * 4;
+    const dim3 grid((unsigned)cdiv(a.L, 256));
+    if (a.dtype == HASTE_DTYPE_F32) {
+        hipFuncSetAttribute((const void *)k_bwd_w_valu<float>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        hipLaunchKernelGGL(k_bwd_w_valu<float>, grid, dim3(256), lds, s, (const float *)X, idx, (const float *)dY, dW,
+                           dbias, beta, (int)a.B, (int)a.F_s, a.L, (int)a.G, (int)a.F_in);
+    } else {
+        hipFuncSetAttribute((const void *)k_bwd_w_valu<bf16_t>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        hipLaunchKernelGGL(k_bwd_w_valu<bf16_t>, grid, dim3(256), lds, s, (const bf16_t *)X, idx, (const bf16_t *)dY,
+                           dW, dbias, beta, (int)a.B, (int)a.F_s, a.L, (int)a.G, (int)a.F_in);
+    }
+    return hipGetLastError();
+}
+
+size_t bwd_x_valu_ws(const TailArgs &a) {
+    const int64_t S = bwd_x_valu_segments(a);
+    return (size_t)S * (size_t)a.F_s * (size_t)(cdiv(a.B, TB) * TB) * 4 + 256;
+}
+
+hipError_t bwd_x_valu(const TailArgs &a, const int32_t *idx, const void *W, const void *dY, float *dX, int beta,
+                      void *ws, hipStream_t s) {
+    const int64_t nbt = cdiv(a.B, TB);
+    const int64_t S = bwd_x_valu_segments(a);
+    const int64_t lps = cdiv(a.L, S);
+    const int Bp = (int)(nbt * TB);
+    const size_t lds = (size_t)a.F_s * TB * 4;
+    float *part = reinterpret_cast<float *>(ws);
+    const dim3 grid((unsigned)S, (unsigned)nbt);
+    if (a.dtype == HASTE_DTYPE_F32) {
+        hipFuncSetAttribute((const void *)k_bwd_x_valu<float>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        hipLaunchKernelGGL(k_bwd_x_valu<float>, grid, dim3(256), lds, s, idx, (const float *)W, (const float *)dY, part,
+                           (int)a.B, Bp, (int)a.F_s, a.L, (int)a.G, (int)a.F_in, lps);
+    } else {
+        hipFuncSetAttribute((const void *)k_bwd_x_valu<bf16_t>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        hipLaunchKernelGGL(k_bwd_x_valu<bf16_t>, grid, dim3(256), lds, s, idx, (const bf16_t *)W, (const bf16_t *)dY,
+                           part, (int)a.B, Bp, (int)a.F_s, a.L, (int)a.G, (int)a.F_in, lps);
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return reduce_fmajor(part, (int)S, Bp, a.B, a.F_s, dX, beta, s);
+}
+
+}  // namespace haste
