@@ -42,6 +42,60 @@ __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_ca
 
 __device__ __forceinline__ uint32_t pack2(bf16_t lo, bf16_t hi) { return (uint32_t)lo | ((uint32_t)hi << 16); }
 
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+// two fp32 -> packed bf16 pair (round to nearest even; one v_cvt_pk_bf16_f32 on gfx950)
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{lo, hi}, bf16x2_t));
+}
+
+// registers r0..r0+7 of an MFMA result as one bf16x8 operand
+__device__ __forceinline__ uint4 pack8(const f32x16_t &d, int r0) {
+    return make_uint4(pack_bf16(d[r0 + 0], d[r0 + 1]), pack_bf16(d[r0 + 2], d[r0 + 3]),
+                      pack_bf16(d[r0 + 4], d[r0 + 5]), pack_bf16(d[r0 + 6], d[r0 + 7]));
+}
+
+// Transposing through the matrix core.  With A = a 32x16 block in its natural layout (lane
+// (m = l%32, h = l/32) holds row m, columns 8h..8h+7) and B = the identity slice
+// E_off[k][n] = (n == off + k), D = A*E_0 + A'*E_16 is the 32x32 block itself, but in the MFMA
+// result layout, where lane (n, h) holds column n for rows 8i + 4h + j.  Each output is a single
+// product x*1 accumulated onto zeros, so the copy is exact for finite inputs.
+__device__ __forceinline__ bf16x8_t eye_operand(int ln, int hh, int off) {
+    uint32_t w[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int k = off + 8 * hh + 2 * q;
+        w[q] = (ln == k ? 0x3F80u : 0u) | (ln == k + 1 ? 0x3F800000u : 0u);
+    }
+    return as_bf16x8(make_uint4(w[0], w[1], w[2], w[3]));
+}
+
+// Bounds-checked buffer access (raw buffer resource, stride 0).  Loads at byte offsets at or past
+// `bytes` return zero and stores there are dropped by the hardware, so masked lanes simply use
+// kOob: no branch around the memory instruction, which keeps the count of outstanding memory
+// operations the same on every path (the compiler can then wait for exactly the loads a use
+// needs).  `base` must be wave-uniform; offsets are 32-bit.
+constexpr uint32_t kOob = 0x80000000u;
+constexpr int kRawBufferWord3 = 0x00020000;  // gfx9-family raw buffer format word
+
+struct Buf {
+    __amdgpu_buffer_rsrc_t r;
+    __device__ __forceinline__ Buf(const void *base, uint32_t bytes)
+        : r(__builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0,
+                                              (int)(bytes < kOob ? bytes : kOob - 1), kRawBufferWord3)) {}
+    __device__ __forceinline__ uint2 ld8(uint32_t off) const {
+        return __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, 0));
+    }
+    __device__ __forceinline__ uint4 ld16(uint32_t off) const {
+        return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0));
+    }
+    __device__ __forceinline__ void st8(uint2 v, uint32_t off) const {
+        __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(decltype(__builtin_amdgcn_raw_buffer_load_b64(r, 0, 0, 0)), v),
+                                              r, (int)off, 0, 0);
+    }
+};
+
 // ---- host-side launchers (one translation unit each) -----------------------------------------
 namespace haste {
 

@@ -316,6 +316,6 @@ def test_repeatable(hs):
     Y1, dW1, dX1 = lay.Y.clone(), lay.dW.clone(), lay.dX.clone()
     lay.fwd(); lay.bwd_w(); lay.bwd_x()
     _sync()
+    # every reduction runs in a fixed order (no atomics): all three outputs are bitwise repeatable
     assert bool((Y1 == lay.Y).all()) and bool((dW1 == lay.dW).all()), "fwd / bwd_w must be bitwise repeatable"
-    e = rel_err(lay.dX.cpu().numpy(), dX1.cpu().numpy())
-    assert e <= 1e-6, f"bwd_x run-to-run difference {e:.2e}"
+    assert bool((dX1 == lay.dX).all()), "bwd_x must be bitwise repeatable"
