@@ -86,7 +86,8 @@ int haste_bwd_w(const haste_desc_t *desc, const void *X, const int32_t *idx, con
  * groups with a split over the label dimension):
  *   dX[b, f] = beta * dX[b, f] + sum_k sum_{t : idx[k,t] = f} sum_{j < G} dY[b, kG+j] * W[kG+j, t]
  * dX[B, F_s] fp32; beta is 0 (overwrite) or 1 (accumulate).  Partial sums over label segments
- * live in ws and are reduced in a fixed segment order.
+ * live in ws and are reduced in a fixed segment order; on the bf16 matrix-core path ws also
+ * holds a group-transposed copy of W (about L * F_in * 2 bytes), rebuilt by every call.
  */
 int haste_bwd_x(const haste_desc_t *desc, const int32_t *idx, const void *W, const void *dY,
                 float *dX, int beta, void *ws, size_t ws_bytes, void *stream);

@@ -304,22 +304,34 @@ __global__ __launch_bounds__(256) void k_bwd_w(const bf16_t *__restrict__ Xt, co
 }
 
 // --------------------------------------------------------------------------------------------
-// Backward-feature (split over label segments).  A workgroup owns a 32-row batch tile and one
-// contiguous segment of groups; its partial dX^T[F_s][32] (fp32, rows padded to 36 floats)
-// lives in LDS.  All waves of the workgroup work on the same group at the same time, each on a
-// disjoint 16-slot x 16-row tile of dZ_k W_k.  The features of one group are distinct, so the
-// tiles of one group update disjoint accumulator cells and plain (non-atomic) read-add-write is
-// race free; one barrier per group orders consecutive groups.  This keeps every accumulation in
-// fp32 in a fixed order (bit-reproducible) and avoids LDS float atomics, which run at a small
-// fraction of the LDS rate on gfx950.
-// Per tile (v_mfma_f32_16x16x32_bf16, M = rows, N = slots, K = labels):
-//   B operand (labels x slots) = W_k rows in their natural layout, turned into slot-major
-//     registers by two identity MFMAs (exact, see eye16_operand);
-//   A operand (rows x labels) = dY rows, two 8-byte loads per 32-label chunk;
+// Backward-feature (split over label segments).
+//
+// The contraction runs over the labels of a group, which are strided in W's natural layout
+// (one row of F_in slots per label), so k_transpose_w first writes every group's block as
+// W_k^T [F_in][Gp] (Gp = G rounded up to 8, zero padded) into the workspace: one pass over W
+// instead of one transpose per group and batch tile.
+//
+// A workgroup owns a 32-row batch tile and one contiguous segment of groups; its partial
+// dX^T[F_s][32] (fp32, rows padded to 36 floats) lives in LDS.  Two consumer waves each own one
+// 16-row half of the tile for every group and every support slot, so no two waves ever touch
+// the same accumulator cell: each wave adds its products with plain read-add-write in its own
+// program order (LDS operations of one wave are executed in order), with no barrier between
+// groups.  Every accumulation is fp32 in a fixed order, so dX is bit-reproducible, and no LDS
+// float atomics are used (they run at a small fraction of the LDS rate on gfx950).
+//
+// Producer waves stage dY through LDS in chunks of CH consecutive groups (at most 256 labels):
+// one load instruction reads 512 contiguous bytes of a single row.  Reading dY straight into the
+// MFMA operand layout instead would touch 16 rows (16 pages megabytes apart) per instruction,
+// and such loads are limited by address translation rather than by HBM.  One barrier per chunk
+// hands a staged chunk to the consumers and the previous buffer back to the producers, which
+// keep the next chunk in flight meanwhile.
+//
+// Per group and 16-slot tile (v_mfma_f32_16x16x32_bf16, M = rows, N = slots, K = labels):
+//   A operand (rows x labels) = staged dY, labels 32c + 8q .. +7 of row l16 (two 8-byte LDS
+//     reads per 32-label block, shared by all slot tiles);
+//   B operand (labels x slots) = W_k^T row of slot l16, the same 8 labels (one 16-byte load);
 //   result lane (slot, q) holds rows 4q..4q+3 of one slot: one float4 read-add-write into the
-//   accumulator row idx[k, slot].
-// The tile products of the next group are computed before the barrier and the loads run two
-// groups ahead (ping-pong buffers, unconditional prefetch with a clamped group index).
+//     accumulator row idx[k, slot].
 // --------------------------------------------------------------------------------------------
 typedef float f32x4v_t __attribute__((ext_vector_type(4)));
 
@@ -327,34 +339,72 @@ __device__ __forceinline__ f32x4v_t mfma16x16x32(const bf16x8_t &a, const bf16x8
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
-// identity slice for the 16x16x32 transpose: B[k][n] = (k == n), lane (n = l%16, q = l/16) holds k = 8q..8q+7
-__device__ __forceinline__ bf16x8_t eye16_operand(int l16, int q) {
-    uint32_t w[4];
-#pragma unroll
-    for (int p = 0; p < 4; ++p) {
-        const int k = 8 * q + 2 * p;
-        w[p] = (l16 == k ? 0x3F80u : 0u) | (l16 == k + 1 ? 0x3F800000u : 0u);
+// W [K][G][F_in] -> WT [K][F_in][Gp], labels G .. Gp-1 zero.  One group per workgroup step.
+__global__ __launch_bounds__(256) void k_transpose_w(const bf16_t *__restrict__ W, bf16_t *__restrict__ WT,
+                                                     int64_t K, int G, int Gp, int F_in) {
+    extern __shared__ __align__(16) bf16_t tw[];  // [F_in][Gp + 4]
+    const int TS = Gp + 4;
+    const int tid = threadIdx.x;
+    const int nq = F_in / 4;                      // slot quads per label
+    for (int64_t k = blockIdx.x; k < K; k += gridDim.x) {
+        const uint2 *src = reinterpret_cast<const uint2 *>(W + k * G * F_in);
+        for (int e = tid; e < G * nq; e += blockDim.x) {
+            const int g = e / nq, s4 = (e - g * nq) * 4;
+            const uint2 v = src[e];
+            tw[(s4 + 0) * TS + g] = (bf16_t)(v.x & 0xFFFFu);
+            tw[(s4 + 1) * TS + g] = (bf16_t)(v.x >> 16);
+            tw[(s4 + 2) * TS + g] = (bf16_t)(v.y & 0xFFFFu);
+            tw[(s4 + 3) * TS + g] = (bf16_t)(v.y >> 16);
+        }
+        __syncthreads();
+        uint2 *dst = reinterpret_cast<uint2 *>(WT + k * F_in * Gp);
+        const int gq = Gp / 4;                    // label quads per slot
+        for (int e = tid; e < F_in * gq; e += blockDim.x) {
+            const int sl = e / gq, g4 = (e - sl * gq) * 4;
+            const bf16_t *t = tw + sl * TS + g4;
+            uint32_t lo = (g4 + 0 < G ? t[0] : 0u) | ((uint32_t)(g4 + 1 < G ? t[1] : 0u) << 16);
+            uint32_t hi = (g4 + 2 < G ? t[2] : 0u) | ((uint32_t)(g4 + 3 < G ? t[3] : 0u) << 16);
+            dst[e] = make_uint2(lo, hi);
+        }
+        __syncthreads();
     }
-    return as_bf16x8(make_uint4(w[0], w[1], w[2], w[3]));
 }
 
-template <int NLB>
-struct BwdXTile {
-    uint4 w[NLB][2];   // W[kG + 32c + 16h + l16][16st + 8q .. +7] (q < 2), natural layout
-    uint2 dy[NLB][2];  // dY[row][kG + 32c + 16h + 4q .. +3]
-    int f;             // accumulator row idx[k, 16st + l16]
+template <int F_IN, int NLB>
+struct BwdXGroup {
+    uint4 w[NLB][F_IN / 16];  // W_k^T[16st + l16][32c + 8q .. +7]
+    int f[F_IN / 16];         // accumulator rows idx[k, 16st + l16]
 };
 
+constexpr int kBxAS = 36;         // accumulator row stride (floats): 32 rows + 4 pad
+constexpr int kBxRowBytes = 512;  // staged dY per row and chunk (256 labels)
+constexpr int kBxConsumers = 2;   // consumer waves (one per 16-row half)
+constexpr int kBxProducers = 2;   // producer waves
+
+// groups of weights in flight per consumer wave: registers, and at most 63 outstanding loads
 template <int F_IN, int NLB>
-__global__ __launch_bounds__(512) void k_bwd_x(const int32_t *__restrict__ idx, const bf16_t *__restrict__ W,
+constexpr int bx_depth() {
+    constexpr int per = NLB * (F_IN / 16) * 4 + F_IN / 16;
+    return per <= 20 ? 6 : (per <= 40 ? 4 : 2);  // even: products alternate between two buffers
+}
+
+// Staged dY layout: [2 buffers][32 rows][64 units of 8 bytes]; unit u of row r sits at
+// position u ^ 2(r % 16), so that the 16 rows read by one MFMA operand load fall in distinct
+// banks while each producer store still writes one whole row.
+__device__ __forceinline__ int bx_swz(int u, int r) { return (u & 63) ^ (2 * (r & 15)); }
+
+template <int F_IN, int NLB>
+__global__ __launch_bounds__(256) void k_bwd_x(const int32_t *__restrict__ idx, const bf16_t *__restrict__ WT,
                                                const bf16_t *__restrict__ dY, float *__restrict__ part, int B,
-                                               int Bp, int F_s, int64_t L, int G, int64_t K, int nbt,
-                                               int64_t gps) {
-    extern __shared__ __align__(16) float accs[];  // [F_s][AS]
-    constexpr int AS = 36;
-    constexpr int NT = (F_IN / 16) * 2;            // tiles per group: slot tiles x two 16-row halves
-    constexpr int NWV = NT < 8 ? NT : 8;           // waves
-    constexpr int TPW = NT / NWV;                  // tiles per wave
+                                               int Bp, int F_s, int64_t L, int G, int Gp, int64_t K, int nbt,
+                                               int64_t gps, int CH) {
+    extern __shared__ __align__(16) float accs[];  // [F_s][kBxAS], then the staged dY
+    constexpr int AS = kBxAS;
+    constexpr int NST = F_IN / 16;                 // 16-slot tiles
+    constexpr int NP = kBxProducers;
+    constexpr int NJ = 32 / NP;                    // rows per producer wave and chunk
+    constexpr int NB = bx_depth<F_IN, NLB>();
+    char *ys = reinterpret_cast<char *>(accs + F_s * AS);
     const int w = blockIdx.x;
     const int xcd = w % kXcds;
     const int jj = w / kXcds;
@@ -362,124 +412,161 @@ __global__ __launch_bounds__(512) void k_bwd_x(const int32_t *__restrict__ idx, 
     const int64_t seg = (int64_t)(jj / nbt) * kXcds + xcd;
     const int b0 = bt * 32;
     const int tid = threadIdx.x;
+    const int nthr = (kBxConsumers + NP) * 64;
     const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int l16 = lane & 15, q = lane >> 4;
-
-    for (int e = tid; e < F_s * AS; e += NWV * 64) accs[e] = 0.0f;
-    __syncthreads();
+    float *pp = part + (size_t)seg * F_s * Bp + b0;
 
     const int64_t g_begin = seg * gps;
     const int64_t g_end = g_begin + gps < K ? g_begin + gps : K;
     if (g_begin >= g_end) {
         // empty segment: the partial is zero
-        float *pp = part + (size_t)seg * F_s * Bp + b0;
-        for (int e = tid; e < F_s * 32; e += NWV * 64) pp[(size_t)(e >> 5) * Bp + (e & 31)] = 0.0f;
+        for (int e = tid; e < F_s * 32; e += nthr) pp[(size_t)(e >> 5) * Bp + (e & 31)] = 0.0f;
         return;
     }
-    const int64_t lastk = g_end - 1;
-    auto cl = [&](int64_t v) { return v < lastk ? v : lastk; };
+    for (int e = tid; e < F_s * AS; e += nthr) accs[e] = 0.0f;
+    const int n = (int)(g_end - g_begin);          // groups of this segment
+    const int nch = (n + CH - 1) / CH;             // dY chunks
 
-    int st[TPW], bh[TPW];
-    int64_t drows[TPW];   // valid rows of this tile's 16-row half
+    if (wave >= kBxConsumers) {
+        // ---- producers: dY chunk c (groups cCH .. of the segment) -> staging buffer c % 2 ----
+        const int p = wave - kBxConsumers;
+        const int rows = B - b0 < 32 ? B - b0 : 32;
+        const uint32_t u8 = (uint32_t)lane * 8;
+        const bool lane_ok = (int)u8 < CH * G * 2;
+        uint2 v[NJ];
+        auto load = [&](int c) {
+            // rows past B and bytes past the end of dY read as zero
+            const int64_t lab0 = (g_begin + (int64_t)c * CH) * G;
+            const Buf db(dY + (int64_t)b0 * L + lab0, (uint32_t)(((int64_t)rows * L - lab0) * 2));
 #pragma unroll
-    for (int i = 0; i < TPW; ++i) {
-        const int t = wave + NWV * i;
-        st[i] = t >> 1;
-        bh[i] = t & 1;
-        const int r = B - (b0 + 16 * bh[i]);
-        drows[i] = r < 0 ? 0 : (r > 16 ? 16 : r);
-    }
+            for (int i = 0; i < NJ; ++i) {
+                const int r = p + NP * i;
+                v[i] = db.ld8(lane_ok ? (uint32_t)((int64_t)r * L * 2) + u8 : kOob);
+            }
+        };
+        auto store = [&](int c) {
+            char *yb = ys + (c & 1) * 32 * kBxRowBytes;
+#pragma unroll
+            for (int i = 0; i < NJ; ++i) {
+                const int r = p + NP * i;
+                *reinterpret_cast<uint2 *>(yb + r * kBxRowBytes + bx_swz(lane, r) * 8) = v[i];
+            }
+        };
+        load(0);
+        store(0);
+        if (nch > 1) load(1);
+        for (int c = 0; c < nch; ++c) {
+            __syncthreads();  // chunk c staged, chunk c - 1 consumed
+            if (c + 1 < nch) store(c + 1);
+            if (c + 2 < nch) load(c + 2);
+        }
+    } else {
+        // ---- consumers: rows 16bh .. 16bh + 15 of the tile ----
+        const int bh = wave;
+        const int last = n - 1;
+        auto cl = [&](int v) { return v < last ? v : last; };
 
-    auto issue = [&](int64_t k, BwdXTile<NLB> (&tl)[TPW]) {
-        // group k's weights: labels past G read as zero; lanes q >= 2 hold K-slots past the
-        // tile's 16 slots and are sent out of range
-        const Buf wb(W + k * G * F_IN, (uint32_t)(G * F_IN * 2));
+        // This segment's transposed weights and support, addressed by a per-lane offset within
+        // a group plus a wave-uniform group offset (the segment spans less than 2 GB).
+        const uint32_t gbytes = (uint32_t)(F_IN * Gp * 2);
+        const Buf wseg(WT + g_begin * F_IN * Gp, (uint32_t)n * gbytes);
+        const Buf iseg(idx + g_begin * F_IN, (uint32_t)(n * F_IN * 4));
+        uint32_t wvo[NLB][NST];
 #pragma unroll
-        for (int i = 0; i < TPW; ++i) {
-            // rows past B fall outside the buffer, labels past G are sent out of range
-            const Buf db(dY + (int64_t)(b0 + 16 * bh[i]) * L + k * G, (uint32_t)(drows[i] * L * 2));
+        for (int c = 0; c < NLB; ++c)
+#pragma unroll
+            for (int st = 0; st < NST; ++st) {
+                const int lab = 32 * c + 8 * q;   // labels past Gp read as zero
+                wvo[c][st] = lab < Gp ? (uint32_t)(((16 * st + l16) * Gp + lab) * 2) : kOob;
+            }
+        auto issue = [&](int sg, BwdXGroup<F_IN, NLB> &t) {
 #pragma unroll
             for (int c = 0; c < NLB; ++c)
 #pragma unroll
-                for (int h = 0; h < 2; ++h) {
-                    const int lab = 32 * c + 16 * h + l16;
-                    const uint32_t woff = (uint32_t)((lab * F_IN + 16 * st[i] + 8 * q) * 2);
-                    tl[i].w[c][h] = wb.ld16(q < 2 ? woff : kOob);
-                    const int c4 = 32 * c + 16 * h + 4 * q;   // 4 labels c4..c4+3 of the group
-                    tl[i].dy[c][h] = db.ld8(c4 < G ? (uint32_t)((int64_t)l16 * L * 2) + 2 * c4 : kOob);
-                }
-            // a relaxed atomic load is not sunk towards its use (the scatter, two steps later), so it
-            // stays in the prefetch batch
-            tl[i].f = __hip_atomic_load(idx + k * F_IN + 16 * st[i] + l16, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
-    };
-
-    const bf16x8_t eye = eye16_operand(l16, q);
-    auto compute = [&](const BwdXTile<NLB> (&tl)[TPW], f32x4v_t (&pr)[TPW], int (&ad)[TPW]) {
+                for (int st = 0; st < NST; ++st)
+                    t.w[c][st] = __builtin_bit_cast(
+                        uint4, __builtin_amdgcn_raw_buffer_load_b128(wseg.r, (int)wvo[c][st], (int)(sg * gbytes), 0));
 #pragma unroll
-        for (int i = 0; i < TPW; ++i) {
-            f32x4v_t acc = f32x4v_t{0.f, 0.f, 0.f, 0.f};
+            for (int st = 0; st < NST; ++st)
+                t.f[st] = __builtin_amdgcn_raw_buffer_load_b32(iseg.r, (16 * st + l16) * 4, sg * F_IN * 4, 0);
+        };
+
+        const int r = 16 * bh + l16;               // tile row of this lane's dY operand
+        char *accb = reinterpret_cast<char *>(accs) + (16 * bh + 4 * q) * 4;  // this lane's accumulator column
+        bool lab_ok[NLB][2];                       // label quads of this lane within the group
+#pragma unroll
+        for (int c = 0; c < NLB; ++c) {
+            lab_ok[c][0] = 32 * c + 8 * q < G;
+            lab_ok[c][1] = 32 * c + 8 * q + 4 < G;
+        }
+
+        // dY operand of the next group: labels 32c + 8q .. +7 of this lane's row.  Groups are
+        // read in order, so their place in the staged chunks is tracked as they go; the first
+        // group of a chunk waits for the chunk's barrier.  Label quads past G (the next group's
+        // labels) and groups past the end (repeats of the last group) read as zero, so the latter
+        // add nothing.
+        int cbuf = 0, cgl = 0;
+        auto read_dy = [&](uint4 (&ay)[NLB], bool live) {
+            if (cgl == 0 && live) __syncthreads();  // a new chunk is staged
+            const char *yrow = ys + cbuf * 32 * kBxRowBytes + r * kBxRowBytes;
 #pragma unroll
             for (int c = 0; c < NLB; ++c) {
-                // W chunk transposed: lane (slot l16, q) holds labels 32c + 4q + j and 32c + 16 + 4q + j
-                const f32x4v_t d0 = mfma16x16x32(as_bf16x8(tl[i].w[c][0]), eye, f32x4v_t{0.f, 0.f, 0.f, 0.f});
-                const f32x4v_t d1 = mfma16x16x32(as_bf16x8(tl[i].w[c][1]), eye, f32x4v_t{0.f, 0.f, 0.f, 0.f});
-                const uint4 bo = make_uint4(pack_bf16(d0[0], d0[1]), pack_bf16(d0[2], d0[3]), pack_bf16(d1[0], d1[1]),
-                                            pack_bf16(d1[2], d1[3]));
-                // K-slot 8q + p  <->  label 32c + (p < 4 ? 4q + p : 16 + 4q + p - 4)
-                const uint4 ao = make_uint4(tl[i].dy[c][0].x, tl[i].dy[c][0].y, tl[i].dy[c][1].x, tl[i].dy[c][1].y);
-                acc = mfma16x16x32(as_bf16x8(ao), as_bf16x8(bo), acc);
+                const int c8 = 32 * c + 8 * q;
+                uint2 a0 = *reinterpret_cast<const uint2 *>(yrow + bx_swz((cgl + c8) >> 2, r) * 8);
+                uint2 a1 = *reinterpret_cast<const uint2 *>(yrow + bx_swz((cgl + c8 + 4) >> 2, r) * 8);
+                if (!(live && lab_ok[c][0])) a0 = make_uint2(0u, 0u);
+                if (!(live && lab_ok[c][1])) a1 = make_uint2(0u, 0u);
+                ay[c] = make_uint4(a0.x, a0.y, a1.x, a1.y);
             }
-            pr[i] = acc;
-            ad[i] = tl[i].f * AS + 16 * bh[i] + 4 * q;   // scatter address (floats)
-        }
-    };
+            cgl += G;
+            if (cgl == CH * G) {
+                cgl = 0;
+                cbuf ^= 1;
+            }
+        };
 
-    auto rmw = [&](const int (&ad)[TPW], const f32x4v_t (&pr)[TPW]) {
+        // Group g's weights live in buffer g % NB, loaded NB groups ahead (clamped index past the
+        // end, so every wait covers only its own loads); its dY operand is read one step ahead, in
+        // buffer g % 2.  Step s: read the accumulator rows of group s, read the dY operand of
+        // group s + 1, then D = dZ_s W_s + old through the matrix core (its accumulator input) and
+        // write D back.  The group count is padded to a multiple of NB so that the unrolled body
+        // has no branch around a load.
+        BwdXGroup<F_IN, NLB> tl[NB];
+        uint4 ay[2][NLB];
 #pragma unroll
-        for (int i = 0; i < TPW; ++i) {
-            float4 *p = reinterpret_cast<float4 *>(accs + ad[i]);
-            float4 v = *p;
-            v.x += pr[i][0];
-            v.y += pr[i][1];
-            v.z += pr[i][2];
-            v.w += pr[i][3];
-            *p = v;
+        for (int b = 0; b < NB; ++b) {
+            issue(cl(b), tl[b]);
+            __builtin_amdgcn_sched_barrier(0);  // keep prefetch order
         }
-    };
-
-    // Two buffers in ping-pong (loop unrolled by two, as in the forward kernel): compute() turns a
-    // buffer into registers (tile products and scatter addresses) and the buffer is refilled right
-    // after, so loads get a full step to land and nothing loaded is carried across a refill.
-    // Scatter order: group k - 1, then k, each behind one barrier.
-    BwdXTile<NLB> ta[TPW], tb[TPW];
-    f32x4v_t pa[TPW], pb[TPW];
-    int aa[TPW], ab[TPW];
-    issue(g_begin, ta);
-    __builtin_amdgcn_sched_barrier(0);
-    issue(cl(g_begin + 1), tb);
-    __builtin_amdgcn_sched_barrier(0);
-    for (int64_t k = g_begin; k <= lastk; k += 2) {
-        compute(ta, pa, aa);                            // group k
-        issue(cl(k + 2), ta);
-        __builtin_amdgcn_sched_barrier(0);
-        if (k > g_begin) {
-            __syncthreads();
-            rmw(ab, pb);                                // group k - 1
+        const int n_pad = (n + NB - 1) / NB * NB;
+        read_dy(ay[0], true);
+        for (int s0 = 0; s0 < n_pad; s0 += NB) {
+#pragma unroll
+            for (int b = 0; b < NB; ++b) {
+                const int sg = s0 + b;
+                f32x4v_t acc[NST];
+                uint32_t ao[NST];
+#pragma unroll
+                for (int st = 0; st < NST; ++st) {
+                    ao[st] = __umul24((uint32_t)tl[b].f[st], AS * 4);
+                    acc[st] = *reinterpret_cast<const f32x4v_t *>(accb + ao[st]);
+                }
+                read_dy(ay[(b + 1) & 1], sg + 1 < n);
+#pragma unroll
+                for (int st = 0; st < NST; ++st) {
+#pragma unroll
+                    for (int c = 0; c < NLB; ++c)
+                        acc[st] = mfma16x16x32(as_bf16x8(ay[b & 1][c]), as_bf16x8(tl[b].w[c][st]), acc[st]);
+                    *reinterpret_cast<f32x4v_t *>(accb + ao[st]) = acc[st];
+                }
+                issue(cl(sg + NB), tl[b]);
+                __builtin_amdgcn_sched_barrier(0);  // keep prefetch order
+            }
         }
-        compute(tb, pb, ab);                            // group k + 1 (clamped past the end)
-        issue(cl(k + 3), tb);
-        __builtin_amdgcn_sched_barrier(0);
-        __syncthreads();
-        rmw(aa, pa);                                    // group k
-    }
-    if (((g_end - g_begin) & 1) == 0) {
-        __syncthreads();
-        rmw(ab, pb);                                    // the last group
     }
     __syncthreads();
-    float *pp = part + (size_t)seg * F_s * Bp + b0;
-    for (int e = tid; e < F_s * 32; e += NWV * 64) {
+    for (int e = tid; e < F_s * 32; e += nthr) {
         const int f = e >> 5, b = e & 31;
         pp[(size_t)f * Bp + b] = accs[f * AS + b];
     }
@@ -503,7 +590,7 @@ hipError_t allow_lds(Kern k, size_t bytes) {
 }
 
 struct BwdXGeom {
-    int nbt, nwaves;
+    int nbt, nwaves, ch;
     int64_t nseg, gps;
     size_t lds;
 };
@@ -512,8 +599,9 @@ BwdXGeom bwd_x_geom(const haste::TailArgs &a) {
     BwdXGeom g;
     g.nbt = (int)haste::cdiv(a.B, 32);
     const int nt = (int)(a.F_in / 16) * 2;
-    g.nwaves = nt < 8 ? nt : 8;
-    g.lds = (size_t)a.F_s * 36 * 4;
+    g.nwaves = kBxConsumers + kBxProducers;
+    g.ch = (int)((kBxRowBytes / 2) / a.G);  // groups per staged dY chunk
+    g.lds = (size_t)a.F_s * kBxAS * 4 + 2 * 32 * kBxRowBytes;
     const int64_t K = a.L / a.G;
     int64_t spx = kCusPerXcd / g.nbt;  // one workgroup per CU: the accumulator takes most of the LDS
     if (spx < 1) spx = 1;
@@ -531,9 +619,11 @@ namespace haste {
 // ---- forward ----------------------------------------------------------------------------------
 // The MFMA path needs bf16 storage, groups in multiples of 4 labels (8-byte label quads), a
 // support of 32/64/128 slots and an even feature width that fits the LDS slab.
+// Byte offsets within 64 rows of the [B, L] logits must fit the 31-bit buffer range.
 bool fwd_mfma_supported(const TailArgs &a) {
     return a.dtype == HASTE_DTYPE_BF16 && a.G >= 4 && (a.G % 4) == 0 &&
-           (a.F_in == 32 || a.F_in == 64 || a.F_in == 128) && (a.F_s % 2) == 0 && a.F_s <= kMaxFs;
+           (a.F_in == 32 || a.F_in == 64 || a.F_in == 128) && (a.F_s % 2) == 0 && a.F_s <= kMaxFs &&
+           a.L * 128 < ((int64_t)1 << 31);
 }
 
 template <int BT, int F_IN, bool HAS_BIAS>
@@ -616,38 +706,45 @@ hipError_t bwd_w_mfma(const TailArgs &a, const void *X, const int32_t *idx, cons
 }
 
 // ---- backward-feature ---------------------------------------------------------------------------
-// Groups of up to 128 labels (four 32-label blocks held in registers per group).
+// Groups of up to 128 labels (four 32-label blocks held in registers per group), at least two
+// groups per staged dY chunk, and the accumulator plus the staging buffers within the LDS.
 bool bwd_x_mfma_supported(const TailArgs &a) {
     if (!fwd_mfma_supported(a) || a.G > 128) return false;
-    return bwd_x_geom(a).lds <= kLdsBudget;
+    const BwdXGeom g = bwd_x_geom(a);
+    return g.ch >= 2 && g.lds <= kLdsBudget;
+}
+
+// workspace: the per-segment partials, then W^T (group blocks [F_in][Gp])
+static size_t bwd_x_part_bytes(const TailArgs &a, const BwdXGeom &g) {
+    return round_up((int64_t)g.nseg * a.F_s * (g.nbt * 32) * 4, 256);
 }
 
 size_t bwd_x_mfma_ws(const TailArgs &a) {
-    BwdXGeom g = bwd_x_geom(a);
-    return (size_t)g.nseg * (size_t)a.F_s * (size_t)(g.nbt * 32) * 4 + 256;
+    const BwdXGeom g = bwd_x_geom(a);
+    return bwd_x_part_bytes(a, g) + (size_t)(a.L / a.G) * (size_t)a.F_in * (size_t)round_up(a.G, 8) * 2 + 256;
 }
 
 template <int F_IN, int NLB>
-static hipError_t launch_bwd_x(const TailArgs &a, const BwdXGeom &g, const int32_t *idx, const void *W,
+static hipError_t launch_bwd_x(const TailArgs &a, const BwdXGeom &g, const int32_t *idx, const bf16_t *WT,
                                const void *dY, float *part, hipStream_t s) {
     auto kern = k_bwd_x<F_IN, NLB>;
     hipError_t e = allow_lds(kern, g.lds);
     if (e != hipSuccess) return e;
     const int64_t K = a.L / a.G;
-    hipLaunchKernelGGL(kern, dim3((unsigned)(g.nseg * g.nbt)), dim3(g.nwaves * 64), g.lds, s, idx,
-                       (const bf16_t *)W, (const bf16_t *)dY, part, (int)a.B, g.nbt * 32, (int)a.F_s, a.L, (int)a.G,
-                       K, g.nbt, g.gps);
+    hipLaunchKernelGGL(kern, dim3((unsigned)(g.nseg * g.nbt)), dim3(g.nwaves * 64), g.lds, s, idx, WT,
+                       (const bf16_t *)dY, part, (int)a.B, g.nbt * 32, (int)a.F_s, a.L, (int)a.G,
+                       (int)round_up(a.G, 8), K, g.nbt, g.gps, g.ch);
     return hipGetLastError();
 }
 
 template <int F_IN>
-static hipError_t launch_bwd_x_g(const TailArgs &a, const BwdXGeom &g, const int32_t *idx, const void *W,
+static hipError_t launch_bwd_x_g(const TailArgs &a, const BwdXGeom &g, const int32_t *idx, const bf16_t *WT,
                                  const void *dY, float *part, hipStream_t s) {
     switch ((a.G + 31) / 32) {
-        case 1: return launch_bwd_x<F_IN, 1>(a, g, idx, W, dY, part, s);
-        case 2: return launch_bwd_x<F_IN, 2>(a, g, idx, W, dY, part, s);
-        case 3: return launch_bwd_x<F_IN, 3>(a, g, idx, W, dY, part, s);
-        case 4: return launch_bwd_x<F_IN, 4>(a, g, idx, W, dY, part, s);
+        case 1: return launch_bwd_x<F_IN, 1>(a, g, idx, WT, dY, part, s);
+        case 2: return launch_bwd_x<F_IN, 2>(a, g, idx, WT, dY, part, s);
+        case 3: return launch_bwd_x<F_IN, 3>(a, g, idx, WT, dY, part, s);
+        case 4: return launch_bwd_x<F_IN, 4>(a, g, idx, WT, dY, part, s);
     }
     return hipErrorInvalidValue;
 }
@@ -656,11 +753,18 @@ hipError_t bwd_x_mfma(const TailArgs &a, const int32_t *idx, const void *W, cons
                       void *ws, hipStream_t s) {
     const BwdXGeom g = bwd_x_geom(a);
     float *part = reinterpret_cast<float *>(ws);
-    hipError_t e;
+    bf16_t *WT = reinterpret_cast<bf16_t *>(reinterpret_cast<char *>(ws) + bwd_x_part_bytes(a, g));
+    const int64_t K = a.L / a.G;
+    const int Gp = (int)round_up(a.G, 8);
+    const int64_t tgrid = K < 4096 ? K : 4096;
+    hipLaunchKernelGGL(k_transpose_w, dim3((unsigned)tgrid), dim3(256), (size_t)a.F_in * (Gp + 4) * 2, s,
+                       (const bf16_t *)W, WT, K, (int)a.G, Gp, (int)a.F_in);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
     switch (a.F_in) {
-        case 32: e = launch_bwd_x_g<32>(a, g, idx, W, dY, part, s); break;
-        case 64: e = launch_bwd_x_g<64>(a, g, idx, W, dY, part, s); break;
-        case 128: e = launch_bwd_x_g<128>(a, g, idx, W, dY, part, s); break;
+        case 32: e = launch_bwd_x_g<32>(a, g, idx, WT, dY, part, s); break;
+        case 64: e = launch_bwd_x_g<64>(a, g, idx, WT, dY, part, s); break;
+        case 128: e = launch_bwd_x_g<128>(a, g, idx, WT, dY, part, s); break;
         default: return hipErrorInvalidValue;
     }
     if (e != hipSuccess) return e;

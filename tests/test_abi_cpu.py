@@ -105,10 +105,13 @@ def test_workspace_too_small_rejected(hs):
 
 
 def test_workspace_sizes_scale_with_shape(hs):
-    # backward-feature partials: one fp32 [F_s x batch-tile] block per label segment and tile
+    # backward-feature: fp32 [F_s x batch-tile] partials per label segment and tile; the bf16
+    # path also keeps a group-transposed copy of W (L x F_in bf16, G padded to 8)
     small = hs.haste_workspace_bytes(hs.make_desc(32, 256, 4096, 8, 32, hs.HASTE_DTYPE_F32), hs.HASTE_OP_BWD_X)
     big = hs.haste_workspace_bytes(hs.make_desc(512, 768, 2949120, 32, 64, hs.HASTE_DTYPE_BF16), hs.HASTE_OP_BWD_X)
-    assert 0 < small < big < 256 << 20
+    wt = 2949120 * 64 * 2
+    assert 0 < small < 256 << 20
+    assert wt < big < wt + (256 << 20)
 
 
 def test_debug_gather_range_checked(hs):
