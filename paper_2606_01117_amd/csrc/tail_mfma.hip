@@ -167,12 +167,22 @@ __global__ __launch_bounds__(512) void k_fwd(const bf16_t *__restrict__ X, const
 }
 
 // --------------------------------------------------------------------------------------------
-// Backward-weight.  One wave per (group, 32-label tile), contracting over the whole batch in
-// blocks of 32 rows, so dW is formed in one pass on the support slots only.
-// A = dY^T block (labels x rows): dY is read in its natural layout (16 bytes = 8 labels of one
-// row per lane) and transposed through the matrix core (identity operand, exact).
-// B = H_k (rows x slots): gathered from rows of X^T (staged by k_transpose_x), 8 bytes per load.
-// The next block's loads are issued before the current block computes.
+// Backward-weight.  dW_k = dZ_k^T H_k is formed on the support slots only, one wave per
+// (group, 32-label tile) unit, contracting over the whole batch in 32-row blocks
+// (v_mfma_f32_32x32x16_bf16, M = labels, N = slots, K = batch rows).
+//
+// The 8 waves of a workgroup take 8 consecutive units, i.e. a contiguous span of at most 256
+// labels.  Each 32-row block of dY over that span is loaded cooperatively, one 512-byte row
+// segment per load instruction, and staged in LDS (double buffered, one barrier per block):
+// loading each unit's 32x32 block straight into registers would touch 32 rows per instruction,
+// and such loads are limited by address translation rather than by HBM.
+//
+// A operand (labels x rows): a wave reads its block from LDS in the natural layout (lane = row,
+// 8 labels) and transposes it through the matrix core (identity operand, exact).  The rows are
+// read in the order that swaps bits 2 and 3 of the row index, so that after the transpose each
+// lane holds 8 consecutive batch rows per K-step.
+// B operand (rows x slots): 8 consecutive batch rows of X^T (staged by k_transpose_x) at the
+// slot's feature, one 16-byte load.
 // --------------------------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void k_transpose_x(const bf16_t *__restrict__ X, bf16_t *__restrict__ Xt,
                                                      int B, int Bp, int F_s) {
@@ -190,53 +200,81 @@ __global__ __launch_bounds__(256) void k_transpose_x(const bf16_t *__restrict__ 
     }
 }
 
-template <int NT>
-struct BwdWBlock {
-    uint2 dy[4];        // dY[row][label block], natural layout, as two 16-label halves
-    uint2 x[NT][2][2];  // X^T gathers: [slot tile][K-step][half]
-};
+constexpr int kBwUnits = 8;        // units (waves) per workgroup
+constexpr int kBwRowBytes = 512;   // staged dY per row and block (256 labels)
 
+// Staged dY layout: [2 buffers][32 rows][64 units of 8 bytes]; unit u of row r sits at
+// position u ^ (r % 16), so that 16 rows read at the same label fall in distinct banks while
+// each cooperative store still writes one whole row.
+__device__ __forceinline__ int bw_swz(int u, int r) { return (u & 63) ^ (r & 15); }
 
 template <int F_IN>
-__global__ __launch_bounds__(256) void k_bwd_w(const bf16_t *__restrict__ Xt, const int32_t *__restrict__ idx,
+__global__ __launch_bounds__(512) void k_bwd_w(const bf16_t *__restrict__ Xt, const int32_t *__restrict__ idx,
                                                const bf16_t *__restrict__ dY, float *__restrict__ dW,
                                                float *__restrict__ dbias, int beta, int B, int Bp, int64_t L,
                                                int G, int64_t K) {
+    __shared__ __align__(16) char ys[2 * 32 * kBwRowBytes];
+    constexpr int NT = F_IN / 32;           // N-tiles over the support slots
+    constexpr int RPW = 32 / kBwUnits;      // dY rows each wave stages per block
     const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int ln = lane & 31, hh = lane >> 5;
     const int mtiles = (G + 31) >> 5;
-    const int64_t unit = (int64_t)blockIdx.x * 4 + wave;
-    if (unit >= K * mtiles) return;
+    const int64_t nunits = K * mtiles;
+    const int64_t u0 = (int64_t)blockIdx.x * kBwUnits;
+    const int64_t ulast = u0 + kBwUnits - 1 < nunits ? u0 + kBwUnits - 1 : nunits - 1;
+    // label span of the workgroup's units
+    const int64_t kf = u0 / mtiles, kl = ulast / mtiles;
+    const int64_t span0 = kf * G + 32 * (u0 - kf * mtiles);
+    const int mtl = (int)(ulast - kl * mtiles);
+    const int64_t span_end = kl * G + (32 * (mtl + 1) < G ? 32 * (mtl + 1) : G);
+    const int span_bytes = (int)(span_end - span0) * 2;
+    // this wave's unit (waves past the last unit repeat it and write nothing)
+    const bool active = u0 + wave <= ulast;
+    const int64_t unit = active ? u0 + wave : ulast;
     const int64_t k = unit / mtiles;
     const int mt = (int)(unit - k * mtiles);
-    const int c0 = mt * 32;                 // first label of the tile within the group
+    const int c0 = mt * 32;                  // first label of the tile within the group
     const int64_t lab0 = k * G + c0;
-    constexpr int NT = F_IN / 32;           // N-tiles over the support slots
+    const int cu = (int)(lab0 - span0) / 4;  // 8-byte unit of the tile's first label in a staged row
 
     const bf16_t *xrow[NT];
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) xrow[nt] = Xt + (int64_t)idx[k * F_IN + nt * 32 + ln] * Bp + 4 * hh;
-    // natural dY load of this lane: row ln of the block, labels c0 + 8hh + 16s' + {0..3, 4..7}
+    for (int nt = 0; nt < NT; ++nt) xrow[nt] = Xt + (int64_t)idx[k * F_IN + nt * 32 + ln] * Bp + 8 * hh;
+    // natural-layout dY of this lane: labels c0 + 8hh + 16(q/2) + 4(q%2) .. +3; past G read as zero
     bool lab_ok[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) lab_ok[q] = c0 + 8 * hh + 16 * (q >> 1) + 4 * (q & 1) < G;
+    const int rr = (ln & ~12) | ((ln & 4) << 1) | ((ln & 8) >> 1);  // staged row read by this lane
 
-    auto issue = [&](int b0, BwdWBlock<NT> &blk) {
-        // rows past B fall outside the buffer, labels past G are sent out of range; a block past
-        // the end of the batch reads all zeros (its X^T reads stay inside the padded rows)
+    // cooperative dY staging: this wave stores rows wave + 8i of each block
+    uint2 yv[RPW];
+    const bool col_ok = 8 * lane < span_bytes;
+    auto load_dy = [&](int b0) {
+        // rows past B (a whole block past the batch, too) and bytes past the end of dY read as zero
         const int rows = B - b0 < 32 ? (B - b0 > 0 ? B - b0 : 0) : 32;
-        const Buf db(dY + (int64_t)b0 * L + lab0, (uint32_t)((int64_t)rows * L * 2));
-        const uint32_t rowoff = (uint32_t)((int64_t)ln * L * 2) + 16 * hh;
+        const int64_t nbytes = rows > 0 ? ((int64_t)rows * L - span0) * 2 : 0;
+        const Buf db(dY + (int64_t)b0 * L + span0, (uint32_t)nbytes);
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
-            blk.dy[q] = db.ld8(lab_ok[q] ? rowoff + 32 * (q >> 1) + 8 * (q & 1) : kOob);
+        for (int i = 0; i < RPW; ++i) {
+            const int r = wave + kBwUnits * i;
+            yv[i] = db.ld8(col_ok ? (uint32_t)((int64_t)r * L * 2) + 8 * lane : kOob);
+        }
+    };
+    auto store_dy = [&](int buf) {
+#pragma unroll
+        for (int i = 0; i < RPW; ++i) {
+            const int r = wave + kBwUnits * i;
+            *reinterpret_cast<uint2 *>(ys + (buf * 32 + r) * kBwRowBytes + bw_swz(lane, r) * 8) = yv[i];
+        }
+    };
+    // X^T rows b0 + 16s + 8hh .. +7 at each slot's feature (blocks past the batch re-read the last
+    // block; their dY is zero)
+    auto load_x = [&](int b0, uint4 (&x)[NT][2]) {
+        const int bb = b0 < Bp ? b0 : Bp - 32;
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-            for (int s = 0; s < 2; ++s)
-#pragma unroll
-                for (int h = 0; h < 2; ++h)
-                    blk.x[nt][s][h] = *reinterpret_cast<const uint2 *>(xrow[nt] + (b0 < Bp ? b0 : Bp - 32) + 16 * s + 8 * h);
+            for (int s = 0; s < 2; ++s) x[nt][s] = *reinterpret_cast<const uint4 *>(xrow[nt] + bb + 16 * s);
     };
 
     const bf16x8_t e0 = eye_operand(ln, hh, 0), e16 = eye_operand(ln, hh, 16);
@@ -245,43 +283,56 @@ __global__ __launch_bounds__(256) void k_bwd_w(const bf16_t *__restrict__ Xt, co
     for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x16_t{0};
     float dsum = 0.0f;
 
-    auto compute = [&](const BwdWBlock<NT> &cb) {
-        // transpose the 32x32 dY block: D[m = row][n = label], lane (label ln, hh) holds rows 8i+4hh+j
+    auto compute = [&](int buf, const uint4 (&x)[NT][2]) {
+        const char *row = ys + (buf * 32 + rr) * kBwRowBytes;
+        uint2 dy[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            dy[q] = *reinterpret_cast<const uint2 *>(row + bw_swz(cu + 2 * hh + 4 * (q >> 1) + (q & 1), rr) * 8);
+            if (!lab_ok[q]) dy[q] = make_uint2(0u, 0u);
+        }
+        // transpose: D[m][n = label], lane (label ln, hh) holds m = 8i + 4hh + j, the block row rr(m)
         f32x16_t d = f32x16_t{0};
-        d = mfma32x32x16(as_bf16x8(make_uint4(cb.dy[0].x, cb.dy[0].y, cb.dy[1].x, cb.dy[1].y)), e0, d);
-        d = mfma32x32x16(as_bf16x8(make_uint4(cb.dy[2].x, cb.dy[2].y, cb.dy[3].x, cb.dy[3].y)), e16, d);
+        d = mfma32x32x16(as_bf16x8(make_uint4(dy[0].x, dy[0].y, dy[1].x, dy[1].y)), e0, d);
+        d = mfma32x32x16(as_bf16x8(make_uint4(dy[2].x, dy[2].y, dy[3].x, dy[3].y)), e16, d);
         if (dbias) {
 #pragma unroll
             for (int r = 0; r < 16; ++r) dsum += d[r];
         }
 #pragma unroll
         for (int s = 0; s < 2; ++s) {
-            // K-slot 8hh + q  <->  row b0 + 16s + 8(q/4) + 4hh + q%4  (registers 8s .. 8s+7)
+            // K-slot 8hh + p  <->  block row 16s + 8hh + p (registers 8s .. 8s+7)
             const bf16x8_t a = as_bf16x8(pack8(d, 8 * s));
 #pragma unroll
-            for (int nt = 0; nt < NT; ++nt) {
-                const uint4 bx = make_uint4(cb.x[nt][s][0].x, cb.x[nt][s][0].y, cb.x[nt][s][1].x, cb.x[nt][s][1].y);
-                acc[nt] = mfma32x32x16(a, as_bf16x8(bx), acc[nt]);
-            }
+            for (int nt = 0; nt < NT; ++nt) acc[nt] = mfma32x32x16(a, as_bf16x8(x[nt][s]), acc[nt]);
         }
     };
 
-    // blocks in ping-pong buffers, two 32-row blocks in flight
-    // Two 32-row blocks per iteration in ping-pong buffers; every load and every compute is
-    // unconditional (blocks past the batch are all-zero), so each wait covers only its own loads.
-    BwdWBlock<NT> ba, bb;
-    issue(0, ba);
-    __builtin_amdgcn_sched_barrier(0);  // keep prefetch order
-    issue(32, bb);
-    __builtin_amdgcn_sched_barrier(0);  // keep prefetch order
-    for (int b0 = 0; b0 < B; b0 += 64) {
-        compute(ba);
-        issue(b0 + 64, ba);
+    // Block j: compute from buffer j % 2 and X^T set j % 2; stage block j + 1 (loaded one block
+    // ago) into the other buffer; load block j + 2; barrier.  The block count is rounded up to
+    // even so that the loop body has no branch around a load (a block past the batch is zero).
+    uint4 xa[NT][2], xb[NT][2];
+    load_dy(0);
+    load_x(0, xa);
+    store_dy(0);
+    load_dy(32);
+    load_x(32, xb);
+    __syncthreads();
+    for (int b0 = 0; b0 < Bp; b0 += 64) {
+        compute(0, xa);
+        store_dy(1);
+        load_dy(b0 + 64);
+        load_x(b0 + 64, xa);
         __builtin_amdgcn_sched_barrier(0);  // keep prefetch order
-        compute(bb);
-        issue(b0 + 96, bb);
+        __syncthreads();
+        compute(1, xb);
+        store_dy(0);
+        load_dy(b0 + 96);
+        load_x(b0 + 96, xb);
         __builtin_amdgcn_sched_barrier(0);  // keep prefetch order
+        __syncthreads();
     }
+    if (!active) return;
     // D[m = label 8i + 4hh + j][n = slot ln] -> dW[lab0 + m][nt*32 + ln]
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt)
@@ -686,18 +737,19 @@ hipError_t bwd_w_mfma(const TailArgs &a, const void *X, const int32_t *idx, cons
     if (e != hipSuccess) return e;
     const int64_t K = a.L / a.G;
     const int64_t units = K * cdiv(a.G, 32);
-    const dim3 grid((unsigned)cdiv(units, 4));
+    const dim3 grid((unsigned)cdiv(units, kBwUnits));
+    const dim3 block(kBwUnits * 64);
     switch (a.F_in) {
         case 32:
-            hipLaunchKernelGGL(k_bwd_w<32>, grid, dim3(256), 0, s, Xt, idx, (const bf16_t *)dY, dW, dbias, beta,
+            hipLaunchKernelGGL(k_bwd_w<32>, grid, block, 0, s, Xt, idx, (const bf16_t *)dY, dW, dbias, beta,
                                (int)a.B, Bp, a.L, (int)a.G, K);
             break;
         case 64:
-            hipLaunchKernelGGL(k_bwd_w<64>, grid, dim3(256), 0, s, Xt, idx, (const bf16_t *)dY, dW, dbias, beta,
+            hipLaunchKernelGGL(k_bwd_w<64>, grid, block, 0, s, Xt, idx, (const bf16_t *)dY, dW, dbias, beta,
                                (int)a.B, Bp, a.L, (int)a.G, K);
             break;
         case 128:
-            hipLaunchKernelGGL(k_bwd_w<128>, grid, dim3(256), 0, s, Xt, idx, (const bf16_t *)dY, dW, dbias, beta,
+            hipLaunchKernelGGL(k_bwd_w<128>, grid, block, 0, s, Xt, idx, (const bf16_t *)dY, dW, dbias, beta,
                                (int)a.B, Bp, a.L, (int)a.G, K);
             break;
         default: return hipErrorInvalidValue;
