@@ -169,23 +169,27 @@ __global__ __launch_bounds__(512) void k_fwd(const bf16_t *__restrict__ X, const
 // --------------------------------------------------------------------------------------------
 // Backward-weight.  dW_k = dZ_k^T H_k is formed on the support slots only, one wave per
 // (group, 32-label tile) unit, contracting over the whole batch in 32-row blocks
-// (v_mfma_f32_32x32x16_bf16, M = labels, N = slots, K = batch rows).
+// (v_mfma_f32_16x16x32_bf16, M = 16 labels, N = 16 slots, K = the block's 32 batch rows).
 //
-// The 8 waves of a workgroup take 8 consecutive units, i.e. a contiguous span of at most 256
-// labels.  Each 32-row block of dY over that span is loaded cooperatively, one 512-byte row
-// segment per load instruction, and staged in LDS (double buffered, one barrier per block):
+// The 4 waves of a workgroup take 4 consecutive units, i.e. a contiguous span of at most 128
+// labels.  Each 32-row block of dY over that span is loaded cooperatively, two 256-byte row
+// segments per load instruction, and staged in LDS (double buffered, one barrier per block):
 // loading each unit's 32x32 block straight into registers would touch 32 rows per instruction,
 // and such loads are limited by address translation rather than by HBM.
 //
 // A operand (labels x rows): a wave reads its block from LDS in the natural layout (lane = row,
-// 8 labels) and transposes it through the matrix core (identity operand, exact).  The rows are
-// read in the order that swaps bits 2 and 3 of the row index, so that after the transpose each
-// lane holds 8 consecutive batch rows per K-step.
-// B operand (rows x slots): 8 consecutive batch rows of X^T (staged by k_transpose_x) at the
-// slot's feature, one 16-byte load.
+// 8 labels) and transposes it through the matrix core (identity operand, exact), feeding the
+// rows in an order that leaves each lane with 8 consecutive batch rows.
+// B operand (rows x slots): those 8 batch rows of X^T (staged block by block by k_transpose_x)
+// at the slot's feature, one 16-byte load; the 4 lanes of a slot read its 64 contiguous bytes.
+// A tile's 16 slots are consecutive in the sorted support, so one load instruction stays within
+// a few pages of the block (gathers spread over many pages are limited by address translation).
 // --------------------------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_transpose_x(const bf16_t *__restrict__ X, bf16_t *__restrict__ Xt,
-                                                     int B, int Bp, int F_s) {
+// X [B][F_s] -> Xb [Bp/32][F_s][32]: X^T in 32-row batch blocks (rows past B zero).  Within a
+// block, the 64-byte rows of nearby features are adjacent, so a gather over a tile's sorted
+// support stays within a few pages.
+__global__ __launch_bounds__(256) void k_transpose_x(const bf16_t *__restrict__ X, bf16_t *__restrict__ Xb,
+                                                     int B, int F_s) {
     __shared__ bf16_t tile[32][33];
     const int f0 = blockIdx.x * 32, b0 = blockIdx.y * 32;
     const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;  // 32 x 8
@@ -194,30 +198,51 @@ __global__ __launch_bounds__(256) void k_transpose_x(const bf16_t *__restrict__ 
         tile[r][tx] = (b < B && f < F_s) ? X[(int64_t)b * F_s + f] : (bf16_t)0;
     }
     __syncthreads();
+    bf16_t *blk = Xb + (int64_t)blockIdx.y * F_s * 32;
     for (int r = ty; r < 32; r += 8) {
-        const int f = f0 + r, b = b0 + tx;
-        if (f < F_s && b < Bp) Xt[(int64_t)f * Bp + b] = tile[tx][r];
+        const int f = f0 + r;
+        if (f < F_s) blk[(int64_t)f * 32 + tx] = tile[tx][r];
     }
 }
 
-constexpr int kBwUnits = 8;        // units (waves) per workgroup
-constexpr int kBwRowBytes = 512;   // staged dY per row and block (256 labels)
+constexpr int kBwUnits = 4;                   // units (waves) per workgroup
+constexpr int kBwRowBytes = kBwUnits * 64;    // staged dY per row and block (32 labels per unit)
+constexpr int kBwLanesPerRow = kBwRowBytes / 8;
 
-// Staged dY layout: [2 buffers][32 rows][64 units of 8 bytes]; unit u of row r sits at
-// position u ^ (r % 16), so that 16 rows read at the same label fall in distinct banks while
-// each cooperative store still writes one whole row.
-__device__ __forceinline__ int bw_swz(int u, int r) { return (u & 63) ^ (r & 15); }
+// Staged dY layout: [2 buffers][32 rows][kBwRowBytes / 8 units of 8 bytes]; unit u of row r sits
+// at position u ^ (r % 16), so that 16 rows read at the same label fall in distinct banks while
+// each cooperative store still writes whole rows.
+__device__ __forceinline__ int bw_swz(int u, int r) { return (u & (kBwLanesPerRow - 1)) ^ (r & 15); }
+
+__device__ __forceinline__ f32x4_t mfma16x16x32(const bf16x8_t &a, const bf16x8_t &b, const f32x4_t &c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// Identity slice for the 16x16x32 transpose: B[k][n] = (k == 16s + n); lane (n = l%16, q = l/16)
+// holds k = 8q..8q+7.  With A = 16 rows x 32 columns in the natural layout, A*B is columns
+// 16s..16s+15 of A in the result layout, where lane (n, q) holds rows 4q..4q+3 of column 16s + n.
+__device__ __forceinline__ bf16x8_t eye16_operand(int l16, int q, int s) {
+    uint32_t w[4];
+    const int col = 16 * s + l16;
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+        const int k = 8 * q + 2 * p;
+        w[p] = (col == k ? 0x3F80u : 0u) | (col == k + 1 ? 0x3F800000u : 0u);
+    }
+    return as_bf16x8(make_uint4(w[0], w[1], w[2], w[3]));
+}
 
 template <int F_IN>
-__global__ __launch_bounds__(512) void k_bwd_w(const bf16_t *__restrict__ Xt, const int32_t *__restrict__ idx,
-                                               const bf16_t *__restrict__ dY, float *__restrict__ dW,
-                                               float *__restrict__ dbias, int beta, int B, int Bp, int64_t L,
-                                               int G, int64_t K) {
+__global__ __launch_bounds__(kBwUnits * 64) void k_bwd_w(const bf16_t *__restrict__ Xb, const int32_t *__restrict__ idx,
+                                                         const bf16_t *__restrict__ dY, float *__restrict__ dW,
+                                                         float *__restrict__ dbias, int beta, int B, int Bp, int F_s,
+                                                         int64_t L, int G, int64_t K) {
     __shared__ __align__(16) char ys[2 * 32 * kBwRowBytes];
-    constexpr int NT = F_IN / 32;           // N-tiles over the support slots
-    constexpr int RPW = 32 / kBwUnits;      // dY rows each wave stages per block
+    constexpr int NST = F_IN / 16;            // 16-slot N-tiles
+    constexpr int RPI = 64 / kBwLanesPerRow;  // dY rows per staging load instruction
+    constexpr int NSL = 32 / (RPI * kBwUnits); // staging loads per wave and block
     const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int ln = lane & 31, hh = lane >> 5;
+    const int l16 = lane & 15, q = lane >> 4;
     const int mtiles = (G + 31) >> 5;
     const int64_t nunits = K * mtiles;
     const int64_t u0 = (int64_t)blockIdx.x * kBwUnits;
@@ -237,120 +262,132 @@ __global__ __launch_bounds__(512) void k_bwd_w(const bf16_t *__restrict__ Xt, co
     const int64_t lab0 = k * G + c0;
     const int cu = (int)(lab0 - span0) / 4;  // 8-byte unit of the tile's first label in a staged row
 
-    const bf16_t *xrow[NT];
+    // X^T rows b0 + 8q .. +7 at the feature of slot 16nt + l16 (offsets within a block)
+    const bf16_t *xrow[NST];
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) xrow[nt] = Xt + (int64_t)idx[k * F_IN + nt * 32 + ln] * Bp + 8 * hh;
-    // natural-layout dY of this lane: labels c0 + 8hh + 16(q/2) + 4(q%2) .. +3; past G read as zero
-    bool lab_ok[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) lab_ok[q] = c0 + 8 * hh + 16 * (q >> 1) + 4 * (q & 1) < G;
-    const int rr = (ln & ~12) | ((ln & 4) << 1) | ((ln & 8) >> 1);  // staged row read by this lane
+    for (int nt = 0; nt < NST; ++nt) xrow[nt] = Xb + (int64_t)idx[k * F_IN + 16 * nt + l16] * 32 + 8 * q;
+    // natural-layout dY of this lane: labels c0 + 8q .. +3 and +4 .. +7; past G read as zero
+    const bool lab_ok0 = c0 + 8 * q < G, lab_ok1 = c0 + 8 * q + 4 < G;
 
-    // cooperative dY staging: this wave stores rows wave + 8i of each block
-    uint2 yv[RPW];
-    const bool col_ok = 8 * lane < span_bytes;
-    auto load_dy = [&](int b0) {
+    // cooperative dY staging: load instruction i of this wave covers rows RPI * (wave + 4i) ..
+    const int su = lane % kBwLanesPerRow;   // 8-byte unit of a staged row
+    const int sr = lane / kBwLanesPerRow;   // row within the instruction's rows
+    const bool col_ok = 8 * su < span_bytes;
+    auto load_dy = [&](int b0, uint2 (&yv)[NSL]) {
         // rows past B (a whole block past the batch, too) and bytes past the end of dY read as zero
         const int rows = B - b0 < 32 ? (B - b0 > 0 ? B - b0 : 0) : 32;
         const int64_t nbytes = rows > 0 ? ((int64_t)rows * L - span0) * 2 : 0;
         const Buf db(dY + (int64_t)b0 * L + span0, (uint32_t)nbytes);
 #pragma unroll
-        for (int i = 0; i < RPW; ++i) {
-            const int r = wave + kBwUnits * i;
-            yv[i] = db.ld8(col_ok ? (uint32_t)((int64_t)r * L * 2) + 8 * lane : kOob);
+        for (int i = 0; i < NSL; ++i) {
+            const int r = RPI * (wave + kBwUnits * i) + sr;
+            yv[i] = db.ld8(col_ok ? (uint32_t)((int64_t)r * L * 2) + 8 * su : kOob);
         }
     };
-    auto store_dy = [&](int buf) {
+    auto store_dy = [&](int buf, const uint2 (&yv)[NSL]) {
 #pragma unroll
-        for (int i = 0; i < RPW; ++i) {
-            const int r = wave + kBwUnits * i;
-            *reinterpret_cast<uint2 *>(ys + (buf * 32 + r) * kBwRowBytes + bw_swz(lane, r) * 8) = yv[i];
+        for (int i = 0; i < NSL; ++i) {
+            const int r = RPI * (wave + kBwUnits * i) + sr;
+            *reinterpret_cast<uint2 *>(ys + (buf * 32 + r) * kBwRowBytes + bw_swz(su, r) * 8) = yv[i];
         }
     };
-    // X^T rows b0 + 16s + 8hh .. +7 at each slot's feature (blocks past the batch re-read the last
-    // block; their dY is zero)
-    auto load_x = [&](int b0, uint4 (&x)[NT][2]) {
-        const int bb = b0 < Bp ? b0 : Bp - 32;
+    // blocks past the batch re-read the last block of X^T; their dY is zero
+    auto load_x = [&](int b0, uint4 (&x)[NST]) {
+        const int64_t bo = (int64_t)((b0 < Bp ? b0 : Bp - 32) / 32) * F_s * 32;
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-            for (int s = 0; s < 2; ++s) x[nt][s] = *reinterpret_cast<const uint4 *>(xrow[nt] + bb + 16 * s);
+        for (int nt = 0; nt < NST; ++nt) x[nt] = *reinterpret_cast<const uint4 *>(xrow[nt] + bo);
     };
 
-    const bf16x8_t e0 = eye_operand(ln, hh, 0), e16 = eye_operand(ln, hh, 16);
-    f32x16_t acc[NT];
+    const bf16x8_t e0 = eye16_operand(l16, q, 0), e1 = eye16_operand(l16, q, 1);
+    f32x4_t acc[2][NST];
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x16_t{0};
-    float dsum = 0.0f;
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int nt = 0; nt < NST; ++nt) acc[h][nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    float dsum[2] = {0.0f, 0.0f};
 
-    auto compute = [&](int buf, const uint4 (&x)[NT][2]) {
-        const char *row = ys + (buf * 32 + rr) * kBwRowBytes;
-        uint2 dy[4];
+    auto compute = [&](int buf, const uint4 (&x)[NST]) {
+        // Transposes: for row set t, lane (m = l16, q) supplies block row 8(m/4) + 4t + m%4, labels
+        // 8q .. 8q+7; the result for label half h gives lane (label 16h + l16, q) the rows
+        // 8q + 4t .. +3.  Together: 8 consecutive block rows per lane, K-slot 8q + p <-> row 8q + p.
+        f32x4_t d[2][2];  // [t][h]
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            dy[q] = *reinterpret_cast<const uint2 *>(row + bw_swz(cu + 2 * hh + 4 * (q >> 1) + (q & 1), rr) * 8);
-            if (!lab_ok[q]) dy[q] = make_uint2(0u, 0u);
+        for (int t = 0; t < 2; ++t) {
+            const int rr = 8 * (l16 >> 2) + 4 * t + (l16 & 3);
+            const char *row = ys + (buf * 32 + rr) * kBwRowBytes;
+            uint2 y0 = *reinterpret_cast<const uint2 *>(row + bw_swz(cu + 2 * q, rr) * 8);
+            uint2 y1 = *reinterpret_cast<const uint2 *>(row + bw_swz(cu + 2 * q + 1, rr) * 8);
+            if (!lab_ok0) y0 = make_uint2(0u, 0u);
+            if (!lab_ok1) y1 = make_uint2(0u, 0u);
+            const bf16x8_t a = as_bf16x8(make_uint4(y0.x, y0.y, y1.x, y1.y));
+            d[t][0] = mfma16x16x32(a, e0, f32x4_t{0.f, 0.f, 0.f, 0.f});
+            d[t][1] = mfma16x16x32(a, e1, f32x4_t{0.f, 0.f, 0.f, 0.f});
         }
-        // transpose: D[m][n = label], lane (label ln, hh) holds m = 8i + 4hh + j, the block row rr(m)
-        f32x16_t d = f32x16_t{0};
-        d = mfma32x32x16(as_bf16x8(make_uint4(dy[0].x, dy[0].y, dy[1].x, dy[1].y)), e0, d);
-        d = mfma32x32x16(as_bf16x8(make_uint4(dy[2].x, dy[2].y, dy[3].x, dy[3].y)), e16, d);
-        if (dbias) {
 #pragma unroll
-            for (int r = 0; r < 16; ++r) dsum += d[r];
-        }
+        for (int h = 0; h < 2; ++h) {
+            if (dbias) dsum[h] += (d[0][h][0] + d[0][h][1]) + (d[0][h][2] + d[0][h][3]) +
+                                  (d[1][h][0] + d[1][h][1]) + (d[1][h][2] + d[1][h][3]);
+            const bf16x8_t a = as_bf16x8(make_uint4(pack_bf16(d[0][h][0], d[0][h][1]), pack_bf16(d[0][h][2], d[0][h][3]),
+                                                    pack_bf16(d[1][h][0], d[1][h][1]), pack_bf16(d[1][h][2], d[1][h][3])));
 #pragma unroll
-        for (int s = 0; s < 2; ++s) {
-            // K-slot 8hh + p  <->  block row 16s + 8hh + p (registers 8s .. 8s+7)
-            const bf16x8_t a = as_bf16x8(pack8(d, 8 * s));
-#pragma unroll
-            for (int nt = 0; nt < NT; ++nt) acc[nt] = mfma32x32x16(a, as_bf16x8(x[nt][s]), acc[nt]);
+            for (int nt = 0; nt < NST; ++nt) acc[h][nt] = mfma16x16x32(a, as_bf16x8(x[nt]), acc[h][nt]);
         }
     };
 
-    // Block j: compute from buffer j % 2 and X^T set j % 2; stage block j + 1 (loaded one block
-    // ago) into the other buffer; load block j + 2; barrier.  The block count is rounded up to
-    // even so that the loop body has no branch around a load (a block past the batch is zero).
-    uint4 xa[NT][2], xb[NT][2];
-    load_dy(0);
+    // Block j: compute from LDS buffer j % 2 with X^T set j % 2; stage block j + 1 (loaded two
+    // blocks ago, dY set (j + 1) % 2) into the other buffer; load dY of block j + 3 into the set
+    // just staged and X^T of block j + 2 into the set just used; barrier.  The block count is
+    // rounded up to even so that the loop body has no branch around a load (a block past the
+    // batch is zero).
+    uint4 xa[NST], xb[NST];
+    uint2 ya[NSL], yb[NSL];
+    load_dy(0, ya);
     load_x(0, xa);
-    store_dy(0);
-    load_dy(32);
+    load_dy(32, yb);
     load_x(32, xb);
+    store_dy(0, ya);
+    load_dy(64, ya);
+    __builtin_amdgcn_sched_barrier(0);  // keep prefetch order
     __syncthreads();
     for (int b0 = 0; b0 < Bp; b0 += 64) {
         compute(0, xa);
-        store_dy(1);
-        load_dy(b0 + 64);
+        store_dy(1, yb);
+        load_dy(b0 + 96, yb);
         load_x(b0 + 64, xa);
         __builtin_amdgcn_sched_barrier(0);  // keep prefetch order
         __syncthreads();
         compute(1, xb);
-        store_dy(0);
-        load_dy(b0 + 96);
+        store_dy(0, ya);
+        load_dy(b0 + 128, ya);
         load_x(b0 + 96, xb);
         __builtin_amdgcn_sched_barrier(0);  // keep prefetch order
         __syncthreads();
     }
     if (!active) return;
-    // D[m = label 8i + 4hh + j][n = slot ln] -> dW[lab0 + m][nt*32 + ln]
+    // D[m = label 16h + 4q + j][n = slot 16nt + l16]
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
+    for (int h = 0; h < 2; ++h)
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int nt = 0; nt < NST; ++nt)
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                const int m = 8 * i + 4 * hh + j;
+                const int m = 16 * h + 4 * q + j;
                 if (c0 + m < G) {
-                    float *p = dW + (lab0 + m) * F_IN + nt * 32 + ln;
-                    const float v = acc[nt][4 * i + j];
+                    float *p = dW + (lab0 + m) * F_IN + 16 * nt + l16;
+                    const float v = acc[h][nt][j];
                     *p = beta ? *p + v : v;
                 }
             }
     if (dbias) {
-        // lanes (ln, 0) and (ln, 1) hold the two halves of label c0 + ln's row sum
-        dsum += __shfl_xor(dsum, 32);
-        if (hh == 0 && c0 + ln < G) dbias[lab0 + ln] = beta ? dbias[lab0 + ln] + dsum : dsum;
+        // lanes (l16, q) hold the row sums of label 16h + l16 over rows 8q .. 8q+7 of every block
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            float v = dsum[h];
+            v += __shfl_xor(v, 16);
+            v += __shfl_xor(v, 32);
+            if (q == 0 && c0 + 16 * h + l16 < G)
+                dbias[lab0 + 16 * h + l16] = beta ? dbias[lab0 + 16 * h + l16] + v : v;
+        }
     }
 }
 
@@ -384,11 +421,6 @@ __global__ __launch_bounds__(512) void k_bwd_w(const bf16_t *__restrict__ Xt, co
 //   result lane (slot, q) holds rows 4q..4q+3 of one slot: one float4 read-add-write into the
 //     accumulator row idx[k, slot].
 // --------------------------------------------------------------------------------------------
-typedef float f32x4v_t __attribute__((ext_vector_type(4)));
-
-__device__ __forceinline__ f32x4v_t mfma16x16x32(const bf16x8_t &a, const bf16x8_t &b, const f32x4v_t &c) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
-}
 
 // W [K][G][F_in] -> WT [K][F_in][Gp], labels G .. Gp-1 zero.  One group per workgroup step.
 __global__ __launch_bounds__(256) void k_transpose_w(const bf16_t *__restrict__ W, bf16_t *__restrict__ WT,
@@ -596,12 +628,12 @@ __global__ __launch_bounds__(256) void k_bwd_x(const int32_t *__restrict__ idx, 
 #pragma unroll
             for (int b = 0; b < NB; ++b) {
                 const int sg = s0 + b;
-                f32x4v_t acc[NST];
+                f32x4_t acc[NST];
                 uint32_t ao[NST];
 #pragma unroll
                 for (int st = 0; st < NST; ++st) {
                     ao[st] = __umul24((uint32_t)tl[b].f[st], AS * 4);
-                    acc[st] = *reinterpret_cast<const f32x4v_t *>(accb + ao[st]);
+                    acc[st] = *reinterpret_cast<const f32x4_t *>(accb + ao[st]);
                 }
                 read_dy(ay[(b + 1) & 1], sg + 1 < n);
 #pragma unroll
@@ -609,7 +641,7 @@ __global__ __launch_bounds__(256) void k_bwd_x(const int32_t *__restrict__ idx, 
 #pragma unroll
                     for (int c = 0; c < NLB; ++c)
                         acc[st] = mfma16x16x32(as_bf16x8(ay[b & 1][c]), as_bf16x8(tl[b].w[c][st]), acc[st]);
-                    *reinterpret_cast<f32x4v_t *>(accb + ao[st]) = acc[st];
+                    *reinterpret_cast<f32x4_t *>(accb + ao[st]) = acc[st];
                 }
                 issue(cl(sg + NB), tl[b]);
                 __builtin_amdgcn_sched_barrier(0);  // keep prefetch order
@@ -724,15 +756,15 @@ hipError_t fwd_mfma(const TailArgs &a, const void *X, const int32_t *idx, const 
 // ---- backward-weight ----------------------------------------------------------------------------
 bool bwd_w_mfma_supported(const TailArgs &a) { return fwd_mfma_supported(a); }
 
-// X^T staged with the batch padded to whole 32-row blocks
+// X^T staged in 32-row batch blocks (the batch padded to whole blocks)
 size_t bwd_w_mfma_ws(const TailArgs &a) { return (size_t)a.F_s * (size_t)round_up(a.B, 32) * 2 + 256; }
 
 hipError_t bwd_w_mfma(const TailArgs &a, const void *X, const int32_t *idx, const void *dY, float *dW,
                       float *dbias, int beta, void *ws, hipStream_t s) {
     const int Bp = (int)round_up(a.B, 32);
-    bf16_t *Xt = reinterpret_cast<bf16_t *>(ws);
+    bf16_t *Xb = reinterpret_cast<bf16_t *>(ws);
     hipLaunchKernelGGL(k_transpose_x, dim3((unsigned)cdiv(a.F_s, 32), (unsigned)cdiv(Bp, 32)), dim3(256), 0, s,
-                       (const bf16_t *)X, Xt, (int)a.B, Bp, (int)a.F_s);
+                       (const bf16_t *)X, Xb, (int)a.B, (int)a.F_s);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int64_t K = a.L / a.G;
@@ -741,16 +773,16 @@ hipError_t bwd_w_mfma(const TailArgs &a, const void *X, const int32_t *idx, cons
     const dim3 block(kBwUnits * 64);
     switch (a.F_in) {
         case 32:
-            hipLaunchKernelGGL(k_bwd_w<32>, grid, block, 0, s, Xt, idx, (const bf16_t *)dY, dW, dbias, beta,
-                               (int)a.B, Bp, a.L, (int)a.G, K);
+            hipLaunchKernelGGL(k_bwd_w<32>, grid, block, 0, s, Xb, idx, (const bf16_t *)dY, dW, dbias, beta,
+                               (int)a.B, Bp, (int)a.F_s, a.L, (int)a.G, K);
             break;
         case 64:
-            hipLaunchKernelGGL(k_bwd_w<64>, grid, block, 0, s, Xt, idx, (const bf16_t *)dY, dW, dbias, beta,
-                               (int)a.B, Bp, a.L, (int)a.G, K);
+            hipLaunchKernelGGL(k_bwd_w<64>, grid, block, 0, s, Xb, idx, (const bf16_t *)dY, dW, dbias, beta,
+                               (int)a.B, Bp, (int)a.F_s, a.L, (int)a.G, K);
             break;
         case 128:
-            hipLaunchKernelGGL(k_bwd_w<128>, grid, block, 0, s, Xt, idx, (const bf16_t *)dY, dW, dbias, beta,
-                               (int)a.B, Bp, a.L, (int)a.G, K);
+            hipLaunchKernelGGL(k_bwd_w<128>, grid, block, 0, s, Xb, idx, (const bf16_t *)dY, dW, dbias, beta,
+                               (int)a.B, Bp, (int)a.F_s, a.L, (int)a.G, K);
             break;
         default: return hipErrorInvalidValue;
     }
