@@ -24,7 +24,17 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16 MFMA
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+PROFILES = os.path.join(ROOT, "profiles")
+COPY_BYTES = 1 << 30            # plain device copy used to calibrate the HBM byte counters
+
+# kernels launched by each call (symbol prefixes in rocprofv3 output)
+CALL_KERNELS = {
+    "fwd": ["k_fwd"],
+    "bwd_w": ["k_transpose_x", "k_bwd_w"],
+    "bwd_x": ["k_transpose_w", "k_bwd_x", "k_reduce_fmajor"],
+    "head_fwd": ["k_gemm_bf16"],
+    "head_bwd": ["k_gemm_bf16", "k_reduce_rmajor"],
+}
 
 
 def parse():
@@ -35,6 +45,13 @@ def parse():
     p.add_argument("--workload", default="l2949k_g32_h65k")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-bottleneck", action="store_true")
+    p.add_argument("--copy-calibration", action="store_true",
+                   help="after the timed steps, run a plain %d-byte device copy (for counter calibration)" % COPY_BYTES)
+    p.add_argument("--summarize-trace", metavar="DB",
+                   help="write profiles/kernels_<workload>.md from a rocprofv3 --kernel-trace --stats database")
+    p.add_argument("--summarize-traffic", nargs=2, metavar=("FETCH_DB", "WRITE_DB"),
+                   help="write profiles/traffic_<workload>.txt from rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE databases")
+    p.add_argument("--command", default="", help="the profiling command, recorded in the written summary")
     return p.parse_args()
 
 
@@ -70,16 +87,93 @@ def kernel_source_hash():
     return h.hexdigest()[:16]
 
 
+def traffic_file(workload):
+    return os.path.join(PROFILES, f"traffic_{workload}.txt")
+
+
 def measured_traffic(workload, call):
-    """HBM bytes per launch from committed rocprofv3 counter runs, if taken on the current kernels."""
+    """HBM bytes per launch of a call's kernels from the committed rocprofv3 counter summary, if its
+    counters were taken on the current kernel sources (null otherwise)."""
     try:
-        with open(TRAFFIC_FILE) as fh:
-            t = json.load(fh)
-    except (OSError, ValueError):
+        with open(traffic_file(workload)) as fh:
+            line = next(l for l in fh if l.startswith("{"))
+        t = json.loads(line)
+    except (OSError, ValueError, StopIteration):
         return None
     if t.get("kernel_source_hash") != kernel_source_hash():
         return None
-    return t.get("workloads", {}).get(workload, {}).get(call)
+    return t.get("calls", {}).get(call)
+
+
+def _short(name):
+    n = name.replace("(anonymous namespace)::", "").replace("void ", "")
+    return n.split("(")[0]
+
+
+def _db_rows(db, query):
+    import sqlite3
+    con = sqlite3.connect(db)
+    try:
+        return con.execute(query).fetchall()
+    finally:
+        con.close()
+
+
+def summarize_trace(db, workload, command):
+    """Per-kernel launch counts and average durations from a rocprofv3 kernel-trace database."""
+    rows = _db_rows(db, "select name, total_calls, total_duration, average, percentage from top_kernels")
+    lines = [f"# Kernel times, workload {workload}", "",
+             "rocprofv3 --kernel-trace --stats; durations in microseconds (average per launch).", "",
+             f"Command: `{command}`", "", f"Kernel sources: {kernel_source_hash()}", "",
+             "| kernel | launches | avg us | total us | % |", "|---|---|---|---|---|"]
+    for name, n, tot, avg, pct in rows:
+        lines.append(f"| `{_short(name)}` | {n} | {avg:.1f} | {tot:.1f} | {pct:.1f} |")
+    path = os.path.join(PROFILES, f"kernels_{workload}.md")
+    with open(path, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print(path)
+
+
+def summarize_traffic(fetch_db, write_db, workload, command):
+    """HBM bytes per kernel launch from FETCH_SIZE and WRITE_SIZE (KiB per dispatch), each scaled by what
+    the same counter reads for the plain COPY_BYTES device copy run in the same process."""
+    def per_kernel(db, counter):
+        rows = _db_rows(db, f"select name, dispatch_id, sum(counter_value) from pmc_events "
+                            f"where counter_name = '{counter}' group by name, dispatch_id")
+        acc = {}
+        for name, _, v in rows:
+            k = _short(name)
+            s, n = acc.get(k, (0.0, 0))
+            acc[k] = (s + v * 1024.0, n + 1)
+        return {k: s / n for k, (s, n) in acc.items()}
+    fetch, write = per_kernel(fetch_db, "FETCH_SIZE"), per_kernel(write_db, "WRITE_SIZE")
+    copy_keys = [k for k in fetch if "copy" in k.lower()]
+    if not copy_keys:
+        raise SystemExit("no copy kernel in the counter runs (run bench.py with --copy-calibration)")
+    ck = max(copy_keys, key=lambda k: fetch[k])
+    f_fetch = COPY_BYTES / fetch[ck]
+    f_write = COPY_BYTES / write[ck] if write.get(ck) else None
+    calls = {}
+    for call, prefixes in CALL_KERNELS.items():
+        ks = [k for k in fetch if any(k.startswith(p) for p in prefixes)]
+        if not ks or f_write is None:
+            continue
+        calls[call] = round(sum(fetch[k] * f_fetch + write.get(k, 0.0) * f_write for k in ks))
+    rec = {"workload": workload, "kernel_source_hash": kernel_source_hash(), "copy_kernel": ck,
+           "fetch_factor": round(f_fetch, 4), "write_factor": round(f_write, 4), "calls": calls}
+    lines = [f"HBM traffic per launch, workload {workload}",
+             "rocprofv3 --pmc FETCH_SIZE, then --pmc WRITE_SIZE (KiB per dispatch), each scaled by the factor",
+             f"that maps the same counter to the {COPY_BYTES} bytes a plain device copy ({ck}) reads or writes.",
+             f"Command: {command}", "",
+             "kernel | FETCH bytes (raw) | WRITE bytes (raw) | scaled HBM bytes"]
+    for k in sorted(fetch, key=lambda k: -fetch[k]):
+        sc = fetch[k] * f_fetch + write.get(k, 0.0) * f_write
+        lines.append(f"{k} | {fetch[k]:.4g} | {write.get(k, 0.0):.4g} | {sc:.4g}")
+    lines += ["", json.dumps(rec)]
+    path = traffic_file(workload)
+    with open(path, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print(path)
 
 
 def cpu_baseline(wl, X, idx, W, dY, Wh, dYh):
@@ -108,6 +202,12 @@ def cpu_baseline(wl, X, idx, W, dY, Wh, dYh):
 
 def main():
     args = parse()
+    if args.summarize_trace:
+        summarize_trace(args.summarize_trace, args.workload, args.command)
+        return
+    if args.summarize_traffic:
+        summarize_traffic(*args.summarize_traffic, args.workload, args.command)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the layer's multi-GPU sharding "
               "is a design note, not a measured path.", file=sys.stderr)
@@ -201,9 +301,10 @@ def main():
     dom = max(per_call, key=per_call.get)
     db, df = cost[dom]
     achieved = db / per_call[dom] / 1e6
-    roof = {"kernel": dom, "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-            "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": measured_traffic(wl.name, dom),
-            "alg_bytes_per_launch": db, "avg_launch_ms": round(per_call[dom], 4)}
+    roof = {"call": dom, "kernels": CALL_KERNELS[dom], "bound": "hbm", "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+            "traffic": measured_traffic(wl.name, dom), "alg_bytes_per_launch": db,
+            "avg_launch_ms": round(per_call[dom], 4)}
 
     out = {
         "metric": "fwd+bwd ms/step (bf16, 3M-label tail); HBM GB/s and MFMA % of peak",
@@ -225,6 +326,13 @@ def main():
         out["dense_bottleneck"] = bottleneck(wl, Xd, Wd, dYd, args)
         out["tail_vs_bottleneck"] = round(sum(per_call[k] for k in ("fwd", "bwd_w", "bwd_x")) /
                                           out["dense_bottleneck"]["ms"], 3)
+    if args.copy_calibration:
+        src = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(wl, X, idx, W, dY, Wh, dYh)

@@ -18,21 +18,28 @@ constexpr int kSlabPadDw = 1;  // LDS row padding of the X slab (keeps row strid
 // --------------------------------------------------------------------------------------------
 // Forward.
 // A workgroup keeps BT rows of X resident in LDS (the "slab") and sweeps a contiguous stream of
-// groups.  Each wave owns one (group, 32-label tile) unit at a time: it gathers the group's
-// support columns straight from the slab into A-operand registers (gathered once per unit and
-// batch tile, shared by the tile's 32 labels through the MFMA N dimension), takes the labels'
-// weights as the B operand in their natural row layout, and writes bf16 logits.  The next
-// unit's indices and weights are loaded while the current one computes.  The nbt workgroups of
-// one stream (one per batch tile) carry the same blockIdx % 8, so they run on one XCD and W is
-// fetched from HBM about once per stream.
-// Orientation: Z = H_k W_k^T (M = batch rows, N = labels, K = support slots).
+// groups.  Each wave owns one (group, 32-label tile) unit at a time: it takes the labels' weights
+// as the A operand in their natural row layout and gathers the group's support columns straight
+// from the slab into B-operand registers (gathered once per unit and batch tile, shared by the
+// tile's 32 labels through the MFMA M dimension).  The next unit's indices and weights are loaded
+// while the current one computes.  The nbt workgroups of one stream (one per batch tile) carry
+// the same blockIdx % 8, so they run on one XCD and W is fetched from HBM about once per stream.
+// Orientation: Z^T = W_k H_k^T (M = labels, N = batch rows, K = support slots); a result lane
+// holds 4 consecutive labels of one row.
+// Stores: each 32-row x 32-label tile goes through a small per-wave LDS buffer and leaves as
+// 8-byte pieces, 8 lanes per row and 8 rows per store instruction.  (Storing straight from the
+// result layout takes 4x the instructions, or touches 32 rows of the [B, L] logits, megabytes
+// apart, per instruction; both limit the kernel well below HBM bandwidth.)
 // --------------------------------------------------------------------------------------------
 template <int F_IN, bool HAS_BIAS>
 struct FwdUnit {
-    int4 fi[F_IN / 8];     // support indices, this lane's half of every 16-slot K-step
-    uint4 w[F_IN / 16];    // weights of this lane's label, same slots
-    float bias;            // bias of this lane's label
+    int4 fi[F_IN / 8];                // support indices, this lane's half of every 16-slot K-step
+    uint4 w[F_IN / 16];               // weights of this lane's label, same slots
+    float4 bias[HAS_BIAS ? 4 : 1];    // bias of the labels this lane stores (8i + 4hh .. +3)
 };
+
+constexpr int kFwdStageRow = 72;                   // bytes per staged row: 32 labels + 4 pad
+constexpr int kFwdStageBytes = 32 * kFwdStageRow;  // per wave
 
 template <int BT, int F_IN, bool HAS_BIAS>
 __global__ __launch_bounds__(512) void k_fwd(const bf16_t *__restrict__ X, const int32_t *__restrict__ idx,
@@ -74,6 +81,7 @@ __global__ __launch_bounds__(512) void k_fwd(const bf16_t *__restrict__ X, const
     const int64_t u_end = g_end * ntn;
     constexpr int KS = F_IN / 16;   // MFMA K-steps over the support slots
     constexpr int NT = BT / 32;     // MFMA N-tiles over the batch rows
+    char *stg = reinterpret_cast<char *>(xs) + (size_t)BT * S16 * 2 + wave * kFwdStageBytes;
 
     auto issue = [&](int64_t u, FwdUnit<F_IN, HAS_BIAS> &f) {
         const int64_t k = u / ntn;
@@ -91,15 +99,13 @@ __global__ __launch_bounds__(512) void k_fwd(const bf16_t *__restrict__ X, const
         for (int s = 0; s < KS; ++s) f.w[s] = wb.ld16((uint32_t)((col * F_IN + 8 * hh + 16 * s) * 2));
         if (HAS_BIAS) {
             const Buf bb(bias + k * G, (uint32_t)(G * 4));
-            f.bias = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(bb.r, (int)(col * 4), 0, 0));
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                f.bias[i] = __builtin_bit_cast(float4, bb.ld16((uint32_t)((tile * 32 + 8 * i + 4 * hh) * 4)));
         }
     };
 
-    // one unit: gather H_k for this tile from the slab, MFMA against the labels' weights, store.
-    // Orientation Z = H_k W_k^T (M = batch rows, N = labels, K = slots): the result lane (label,
-    // hh) holds rows 8i + 4hh + j, so one 2-byte store instruction writes 64 contiguous bytes in
-    // each of just two rows.  (Memory instructions that span many rows of the [B, L] logits, which
-    // are megabytes apart, are limited by address translation, not by HBM.)
+    // one unit: gather H_k for this tile from the slab, MFMA with the labels' weights, store
     auto compute = [&](int64_t u, const FwdUnit<F_IN, HAS_BIAS> &cu) {
         const int64_t k = u / ntn;
         const int tile = (int)(u - k * ntn);
@@ -112,34 +118,42 @@ __global__ __launch_bounds__(512) void k_fwd(const bf16_t *__restrict__ X, const
                                cu.fi[2 * s + 1].x, cu.fi[2 * s + 1].y, cu.fi[2 * s + 1].z, cu.fi[2 * s + 1].w};
 #pragma unroll
             for (int n = 0; n < NT; ++n) {
-                // gather: A[m = row][k = slot] = X[b0 + 32n + ln][idx[k, slot]]
+                // gather: B[k = slot][n = row] = X[b0 + 32n + ln][idx[k, slot]]
                 const bf16_t *row = xs + (n * 32 + ln) * S16;
-                uint4 av;
-                av.x = pack2(row[fa[0]], row[fa[1]]);
-                av.y = pack2(row[fa[2]], row[fa[3]]);
-                av.z = pack2(row[fa[4]], row[fa[5]]);
-                av.w = pack2(row[fa[6]], row[fa[7]]);
-                acc[n] = mfma32x32x16(as_bf16x8(av), as_bf16x8(cu.w[s]), acc[n]);
+                uint4 bv;
+                bv.x = pack2(row[fa[0]], row[fa[1]]);
+                bv.y = pack2(row[fa[2]], row[fa[3]]);
+                bv.z = pack2(row[fa[4]], row[fa[5]]);
+                bv.w = pack2(row[fa[6]], row[fa[7]]);
+                acc[n] = mfma32x32x16(as_bf16x8(cu.w[s]), as_bf16x8(bv), acc[n]);
             }
         }
-        // D[m = row 8i + 4hh + j][n = label ln]; rows past B fall outside the buffer, labels past G
-        // are sent out of range
+        // D[m = label 8i + 4hh + j][n = row ln]: stage each 32x32 tile as [row][label], then store
+        // 8 bytes (4 labels) per lane: lane -> row 8p + lane/8, labels 4(lane%8) .. +3.  Rows past
+        // B fall outside the buffer, labels past G are sent out of range.
         const int64_t lab0 = k * G + tile * 32;
+        const int nlab = G - tile * 32 < 32 ? G - tile * 32 : 32;
         const int rows = B - b0 < BT ? B - b0 : BT;
         const Buf yb(Y + (int64_t)b0 * L + lab0, (uint32_t)((int64_t)rows * L * 2));
-        const bool ok = tile * 32 + ln < G;
-        const float bv = HAS_BIAS ? cu.bias : 0.0f;
+        const int sr = lane >> 3, sc = lane & 7;
+        const bool ok = 4 * sc < nlab;
 #pragma unroll
-        for (int n = 0; n < NT; ++n)
+        for (int n = 0; n < NT; ++n) {
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
+            for (int i = 0; i < 4; ++i) {
+                const float4 bv = HAS_BIAS ? cu.bias[i] : make_float4(0.f, 0.f, 0.f, 0.f);
+                const uint2 v = make_uint2(pack_bf16(acc[n][4 * i + 0] + bv.x, acc[n][4 * i + 1] + bv.y),
+                                           pack_bf16(acc[n][4 * i + 2] + bv.z, acc[n][4 * i + 3] + bv.w));
+                *reinterpret_cast<uint2 *>(stg + ln * kFwdStageRow + (8 * i + 4 * hh) * 2) = v;
+            }
 #pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const int r = n * 32 + 8 * i + 4 * hh + j;
-                    const uint32_t off = (uint32_t)(((int64_t)r * L + ln) * 2);
-                    __builtin_amdgcn_raw_buffer_store_b16(f32_to_bf16(acc[n][4 * i + j] + bv), yb.r,
-                                                          (int)(ok ? off : kOob), 0, 0);
-                }
+            for (int p = 0; p < 4; ++p) {
+                const int r = 8 * p + sr;
+                const uint2 v = *reinterpret_cast<const uint2 *>(stg + r * kFwdStageRow + sc * 8);
+                const uint32_t off = (uint32_t)(((int64_t)(32 * n + r) * L + 4 * sc) * 2);
+                yb.st8(v, ok ? off : kOob);
+            }
+        }
     };
 
     // Two units in flight per wave in ping-pong buffers (no register copies).  A wave takes two
@@ -713,8 +727,8 @@ template <int BT, int F_IN, bool HAS_BIAS>
 static hipError_t launch_fwd(const TailArgs &a, const void *X, const int32_t *idx, const void *W,
                              const float *bias, void *Y, hipStream_t s) {
     const int S16 = slab_s16((int)a.F_s);
-    const size_t lds = (size_t)BT * S16 * 2;
     const int threads = BT == 64 ? 512 : 256;
+    const size_t lds = (size_t)BT * S16 * 2 + (size_t)(threads / 64) * kFwdStageBytes;
     const int occ = (int)(kLdsBudget / lds) < 1 ? 1 : (int)(kLdsBudget / lds);
     const int occ_eff = BT == 64 ? 1 : (occ > 3 ? 3 : occ);
     const int nbt = (int)cdiv(a.B, BT);
