@@ -39,7 +39,6 @@ struct FwdUnit {
 };
 
 constexpr int kFwdStageRow = 72;                   // bytes per staged row: 32 labels + 4 pad
-constexpr int kFwdStageBytes = 32 * kFwdStageRow;  // per wave
 
 template <int BT, int F_IN, bool HAS_BIAS>
 __global__ __launch_bounds__(512) void k_fwd(const bf16_t *__restrict__ X, const int32_t *__restrict__ idx,
@@ -81,34 +80,34 @@ __global__ __launch_bounds__(512) void k_fwd(const bf16_t *__restrict__ X, const
     const int64_t u_end = g_end * ntn;
     constexpr int KS = F_IN / 16;   // MFMA K-steps over the support slots
     constexpr int NT = BT / 32;     // MFMA N-tiles over the batch rows
-    char *stg = reinterpret_cast<char *>(xs) + (size_t)BT * S16 * 2 + wave * kFwdStageBytes;
+    char *stg = reinterpret_cast<char *>(xs) + (size_t)BT * S16 * 2 + wave * (BT * kFwdStageRow);
 
     auto issue = [&](int64_t u, FwdUnit<F_IN, HAS_BIAS> &f) {
-        const int64_t k = u / ntn;
-        const int tile = (int)(u - k * ntn);
+        const uint32_t uu = (uint32_t)u;   // unit indices fit in 32 bits (L * 128 < 2^31)
+        const uint32_t k = ntn == 1 ? uu : uu / (uint32_t)ntn;
+        const int tile = (int)(uu - k * (uint32_t)ntn);
         const int col = tile * 32 + ln;
-        const int32_t *ip = idx + k * F_IN + 8 * hh;
+        const int32_t *ip = idx + (int64_t)k * F_IN + 8 * hh;
 #pragma unroll
         for (int s = 0; s < KS; ++s) {
             f.fi[2 * s] = *reinterpret_cast<const int4 *>(ip + 16 * s);
             f.fi[2 * s + 1] = *reinterpret_cast<const int4 *>(ip + 16 * s + 4);
         }
         // weights of the group (labels past G read as zero)
-        const Buf wb(W + k * G * F_IN, (uint32_t)(G * F_IN * 2));
+        const Buf wb(W + (int64_t)k * G * F_IN, (uint32_t)(G * F_IN * 2));
 #pragma unroll
         for (int s = 0; s < KS; ++s) f.w[s] = wb.ld16((uint32_t)((col * F_IN + 8 * hh + 16 * s) * 2));
         if (HAS_BIAS) {
-            const Buf bb(bias + k * G, (uint32_t)(G * 4));
+            const Buf bb(bias + (int64_t)k * G, (uint32_t)(G * 4));
 #pragma unroll
             for (int i = 0; i < 4; ++i)
                 f.bias[i] = __builtin_bit_cast(float4, bb.ld16((uint32_t)((tile * 32 + 8 * i + 4 * hh) * 4)));
         }
     };
 
-    // one unit: gather H_k for this tile from the slab, MFMA with the labels' weights, store
+    // one unit: gather H_k for this tile from the slab, MFMA with the labels' weights, and stage
+    // the bf16 tile in this wave's LDS buffer as [row][label]
     auto compute = [&](int64_t u, const FwdUnit<F_IN, HAS_BIAS> &cu) {
-        const int64_t k = u / ntn;
-        const int tile = (int)(u - k * ntn);
         f32x16_t acc[NT];
 #pragma unroll
         for (int n = 0; n < NT; ++n) acc[n] = f32x16_t{0};
@@ -128,32 +127,41 @@ __global__ __launch_bounds__(512) void k_fwd(const bf16_t *__restrict__ X, const
                 acc[n] = mfma32x32x16(as_bf16x8(cu.w[s]), as_bf16x8(bv), acc[n]);
             }
         }
-        // D[m = label 8i + 4hh + j][n = row ln]: stage each 32x32 tile as [row][label], then store
-        // 8 bytes (4 labels) per lane: lane -> row 8p + lane/8, labels 4(lane%8) .. +3.  Rows past
-        // B fall outside the buffer, labels past G are sent out of range.
-        const int64_t lab0 = k * G + tile * 32;
-        const int nlab = G - tile * 32 < 32 ? G - tile * 32 : 32;
-        const int rows = B - b0 < BT ? B - b0 : BT;
-        const Buf yb(Y + (int64_t)b0 * L + lab0, (uint32_t)((int64_t)rows * L * 2));
-        const int sr = lane >> 3, sc = lane & 7;
-        const bool ok = 4 * sc < nlab;
+        // D[m = label 8i + 4hh + j][n = row ln] -> stage[n][row ln][labels 8i + 4hh .. +3]
 #pragma unroll
-        for (int n = 0; n < NT; ++n) {
+        for (int n = 0; n < NT; ++n)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const float4 bv = HAS_BIAS ? cu.bias[i] : make_float4(0.f, 0.f, 0.f, 0.f);
                 const uint2 v = make_uint2(pack_bf16(acc[n][4 * i + 0] + bv.x, acc[n][4 * i + 1] + bv.y),
                                            pack_bf16(acc[n][4 * i + 2] + bv.z, acc[n][4 * i + 3] + bv.w));
-                *reinterpret_cast<uint2 *>(stg + ln * kFwdStageRow + (8 * i + 4 * hh) * 2) = v;
+                *reinterpret_cast<uint2 *>(stg + (n * 32 + ln) * kFwdStageRow + (8 * i + 4 * hh) * 2) = v;
             }
+    };
+
+    // Store a staged unit: 8 bytes (4 labels) per lane, lane -> row 8p + lane/8, labels 4(lane%8)
+    // .. +3.  Rows past B fall outside the buffer, labels past G are sent out of range.  Stores are
+    // issued after the next unit's loads: on gfx9 one in-order counter covers loads and stores, so
+    // a wait for a load also waits for every store issued before it.
+    const int sr = lane >> 3, sc = lane & 7;
+    const int rows = B - b0 < BT ? B - b0 : BT;
+    auto store = [&](int64_t u) {
+        const uint32_t uu = (uint32_t)u;
+        const uint32_t k = ntn == 1 ? uu : uu / (uint32_t)ntn;
+        const int tile = (int)(uu - k * (uint32_t)ntn);
+        const int64_t lab0 = (int64_t)k * G + tile * 32;
+        const int nlab = G - tile * 32 < 32 ? G - tile * 32 : 32;
+        const Buf yb(Y + (int64_t)b0 * L + lab0, (uint32_t)((int64_t)rows * L * 2));
+        const bool ok = 4 * sc < nlab;
+#pragma unroll
+        for (int n = 0; n < NT; ++n)
 #pragma unroll
             for (int p = 0; p < 4; ++p) {
                 const int r = 8 * p + sr;
-                const uint2 v = *reinterpret_cast<const uint2 *>(stg + r * kFwdStageRow + sc * 8);
+                const uint2 v = *reinterpret_cast<const uint2 *>(stg + (n * 32 + r) * kFwdStageRow + sc * 8);
                 const uint32_t off = (uint32_t)(((int64_t)(32 * n + r) * L + 4 * sc) * 2);
                 yb.st8(v, ok ? off : kOob);
             }
-        }
     };
 
     // Two units in flight per wave in ping-pong buffers (no register copies).  A wave takes two
@@ -174,9 +182,12 @@ __global__ __launch_bounds__(512) void k_fwd(const bf16_t *__restrict__ X, const
         compute(u, ua);
         issue(cl(u + st), ua);
         __builtin_amdgcn_sched_barrier(0);  // keep prefetch order
-        if (u + 1 <= last) compute(u + 1, ub);
+        store(u);
+        const bool two = u + 1 <= last;
+        if (two) compute(u + 1, ub);
         issue(cl(u + st + 1), ub);
         __builtin_amdgcn_sched_barrier(0);  // keep prefetch order
+        if (two) store(u + 1);
     }
 }
 
@@ -728,7 +739,7 @@ static hipError_t launch_fwd(const TailArgs &a, const void *X, const int32_t *id
                              const float *bias, void *Y, hipStream_t s) {
     const int S16 = slab_s16((int)a.F_s);
     const int threads = BT == 64 ? 512 : 256;
-    const size_t lds = (size_t)BT * S16 * 2 + (size_t)(threads / 64) * kFwdStageBytes;
+    const size_t lds = (size_t)BT * S16 * 2 + (size_t)(threads / 64) * BT * kFwdStageRow;
     const int occ = (int)(kLdsBudget / lds) < 1 ? 1 : (int)(kLdsBudget / lds);
     const int occ_eff = BT == 64 ? 1 : (occ > 3 ? 3 : occ);
     const int nbt = (int)cdiv(a.B, BT);
