@@ -121,6 +121,152 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(const bf16_t *__restrict__ A,
         }
 }
 
+// ---------------------------------------------------------------------------------------------
+// bf16 GEMM, double buffered.  128x128 output tile, K in steps of 64, 4 waves in a 2x2 grid each
+// owning a 64x64 block (v_mfma_f32_32x32x16_bf16).  Each operand tile is staged in LDS in its
+// global layout, loaded with coalesced 16-byte loads:
+//   K contiguous      -> LDS [row][k], fragments read 16 bytes (8 k) per lane;
+//   M/N contiguous    -> LDS [k][row], fragments read with ds_read_b64_tr_b16, which returns to
+//                        lane i of a 16-lane group 4 consecutive k of row i when source lane 4a + b
+//                        addresses k0 + a, rows 4b .. 4b+3 (two reads give the 8 k of a fragment).
+// One barrier per K step: the next step's tiles are loaded into registers while the current
+// step computes, then written to the other LDS buffer.
+// ---------------------------------------------------------------------------------------------
+constexpr int G2K = 64;                 // K step
+constexpr int G2KC = G2K + 8;           // [row][k] row stride (bf16): 144 bytes
+constexpr int G2RC = TM + 16;           // [k][row] row stride (bf16): 288 bytes
+constexpr int G2TILE = (TM * G2KC > G2K * G2RC ? TM * G2KC : G2K * G2RC);  // bf16 per operand tile
+
+typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) bf16x4_t lds_bf16x4_t;
+
+__device__ __forceinline__ uint2 lds_read_tr(const bf16_t *p) {
+    const bf16x4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t *)(p));
+    return __builtin_bit_cast(uint2, v);
+}
+
+// One operand: rows r0 .. r0+127 (M or N) by k0 .. k0+63, element (r, k) at base + r*sr + k*sk,
+// with sk == 1 (KC) or sr == 1.  The whole matrix spans `bytes` (buffer bound: zero outside).
+template <bool KC>
+struct G2Operand {
+    Buf buf;
+    int64_t sr, sk;
+    uint4 v[4];  // this thread's 4 x 16 bytes of the next tile
+    __device__ __forceinline__ void load(int64_t r0, int64_t rlim, int64_t k0, int64_t klim) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int c = threadIdx.x + 256 * q;
+            int64_t r, k;
+            if (KC) { r = r0 + (c >> 3); k = k0 + (c & 7) * 8; }
+            else    { k = k0 + (c >> 4); r = r0 + (c & 15) * 8; }
+            // rows/k past the limits read as zero (limits are multiples of 8 along the contiguous dim)
+            const bool ok = r < rlim && k < klim;
+            const int64_t off = (r * sr + k * sk) * 2;
+            v[q] = buf.ld16(ok ? (uint32_t)off : kOob);
+        }
+    }
+    __device__ __forceinline__ void store(bf16_t *tile) const {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int c = threadIdx.x + 256 * q;
+            if (KC) *reinterpret_cast<uint4 *>(tile + (c >> 3) * G2KC + (c & 7) * 8) = v[q];
+            else    *reinterpret_cast<uint4 *>(tile + (c >> 4) * G2RC + (c & 15) * 8) = v[q];
+        }
+    }
+    // MFMA operand fragment: rows rb .. rb+31 (lane ln), k = ks*16 + 8hh .. +7
+    __device__ __forceinline__ uint4 frag(const bf16_t *tile, int rb, int ks, int lane) const {
+        const int ln = lane & 31, hh = lane >> 5;
+        if (KC) return *reinterpret_cast<const uint4 *>(tile + (rb + ln) * G2KC + ks * 16 + 8 * hh);
+        const int g = lane >> 4, i = lane & 15;               // 16-lane group, lane in group
+        const int rr = rb + 16 * (g & 1) + 4 * (i & 3);        // rows of this source lane
+        const int kk = ks * 16 + 8 * (g >> 1) + (i >> 2);      // k row of this source lane
+        const uint2 lo = lds_read_tr(tile + kk * G2RC + rr);
+        const uint2 hi = lds_read_tr(tile + (kk + 4) * G2RC + rr);
+        return make_uint4(lo.x, lo.y, hi.x, hi.y);
+    }
+};
+
+template <bool AK, bool BK, int EPI>
+__global__ __launch_bounds__(256, 2) void k_gemm2(const bf16_t *__restrict__ A, int64_t sam, int64_t sak,
+                                                  uint32_t a_bytes, const bf16_t *__restrict__ Bm, int64_t sbk,
+                                                  int64_t sbn, uint32_t b_bytes, void *__restrict__ C, int64_t ldc,
+                                                  const float *__restrict__ bias, int64_t M, int64_t N, int64_t K,
+                                                  int64_t kchunk) {
+    extern __shared__ __align__(16) bf16_t g2s[];   // [2 stages][A tile, B tile]
+    const int64_t n0 = (int64_t)blockIdx.x * TN, m0 = (int64_t)blockIdx.y * TM;
+    const int64_t kb = (int64_t)blockIdx.z * kchunk;
+    const int64_t ke = kb + kchunk < K ? kb + kchunk : K;
+    const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int ln = lane & 31, hh = lane >> 5;
+    const int wm = wave >> 1, wn = wave & 1;
+
+    G2Operand<AK> oa{Buf(A, a_bytes), sam, sak, {}};
+    G2Operand<BK> ob{Buf(Bm, b_bytes), sbn, sbk, {}};
+    auto tileA = [&](int st) { return g2s + st * 2 * G2TILE; };
+    auto tileB = [&](int st) { return g2s + st * 2 * G2TILE + G2TILE; };
+
+    f32x16_t acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = f32x16_t{0};
+
+    oa.load(m0, M, kb, ke);
+    ob.load(n0, N, kb, ke);
+    oa.store(tileA(0));
+    ob.store(tileB(0));
+    __syncthreads();
+    int st = 0;
+    for (int64_t k0 = kb; k0 < ke; k0 += G2K) {
+        // next step's tiles (past the end: out of range, zero, never used)
+        oa.load(m0, M, k0 + G2K, ke);
+        ob.load(n0, N, k0 + G2K, ke);
+        const bf16_t *ta = tileA(st), *tb = tileB(st);
+#pragma unroll
+        for (int ks = 0; ks < G2K / 16; ++ks) {
+            uint4 av[2], bv[2];
+#pragma unroll
+            for (int i = 0; i < 2; ++i) av[i] = oa.frag(ta, wm * 64 + i * 32, ks, lane);
+#pragma unroll
+            for (int j = 0; j < 2; ++j) bv[j] = ob.frag(tb, wn * 64 + j * 32, ks, lane);
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j) acc[i][j] = mfma32x32x16(as_bf16x8(av[i]), as_bf16x8(bv[j]), acc[i][j]);
+        }
+        st ^= 1;
+        oa.store(tileA(st));
+        ob.store(tileB(st));
+        __syncthreads();
+    }
+    // D[m = 8r + 4hh + q][n = ln] per 32x32 block
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int64_t n = n0 + wn * 64 + j * 32 + ln;
+            if (n >= N) continue;
+            const float bv = (EPI == EPI_BF16_BIAS && bias) ? bias[n] : 0.0f;
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int64_t m = m0 + wm * 64 + i * 32 + 8 * r + 4 * hh + q;
+                    if (m >= M) continue;
+                    const float v = acc[i][j][4 * r + q];
+                    if (EPI == EPI_BF16_BIAS) {
+                        reinterpret_cast<bf16_t *>(C)[m * ldc + n] = f32_to_bf16(v + bv);
+                    } else if (EPI == EPI_F32) {
+                        reinterpret_cast<float *>(C)[m * ldc + n] = v;
+                    } else {
+                        reinterpret_cast<float *>(C)[(int64_t)blockIdx.z * M * N + m * N + n] = v;
+                    }
+                }
+        }
+}
+
+constexpr size_t kG2Lds = (size_t)4 * G2TILE * 2;   // two stages of two operand tiles
+
 // fp32 GEMM on the vector ALUs (fp32 heads): 64x64 tiles, 4x4 outputs per thread.
 template <int EPI>
 __global__ __launch_bounds__(256) void k_gemm_f32(const float *__restrict__ A, int64_t sam, int64_t sak,
@@ -182,6 +328,26 @@ int64_t head_splits(int64_t B, int64_t F_s, int64_t H, int32_t dtype) {
     return S < 1 ? 1 : S;
 }
 
+// The double-buffered kernel needs 16-byte aligned rows along every operand's contiguous
+// dimension (F_s and H multiples of 8) and operands within the 31-bit buffer range.
+bool gemm2_ok(int64_t B, int64_t F_s, int64_t H) {
+    const int64_t lim = ((int64_t)1 << 31) - 1;
+    return F_s % 8 == 0 && H % 8 == 0 && B * F_s * 2 < lim && H * F_s * 2 < lim && B * H * 2 < lim;
+}
+
+template <bool AK, bool BK, int EPI>
+hipError_t launch_gemm2(dim3 grid, hipStream_t s, const bf16_t *A, int64_t sam, int64_t sak, int64_t a_elems,
+                        const bf16_t *Bm, int64_t sbk, int64_t sbn, int64_t b_elems, void *C, int64_t ldc,
+                        const float *bias, int64_t M, int64_t N, int64_t K, int64_t kchunk) {
+    auto kern = k_gemm2<AK, BK, EPI>;
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)kG2Lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(kern, grid, dim3(256), kG2Lds, s, A, sam, sak, (uint32_t)(a_elems * 2), Bm, sbk, sbn,
+                       (uint32_t)(b_elems * 2), C, ldc, bias, M, N, K, kchunk);
+    return hipGetLastError();
+}
+
 }  // namespace
 
 namespace haste {
@@ -195,6 +361,10 @@ hipError_t head_fwd(int64_t B, int64_t F_s, int64_t H, int32_t dtype, const void
     // M = B, N = H, K = F_s;  A(m,k) = X[m*F_s + k];  B(k,n) = Wh[n*F_s + k]
     if (dtype == HASTE_DTYPE_BF16) {
         const dim3 grid((unsigned)cdiv(H, TN), (unsigned)cdiv(B, TM), 1);
+        if (gemm2_ok(B, F_s, H))
+            return launch_gemm2<true, true, EPI_BF16_BIAS>(grid, s, (const bf16_t *)X, F_s, 1, B * F_s,
+                                                           (const bf16_t *)Wh, 1, F_s, H * F_s, Yh, H, bias_h, B, H,
+                                                           F_s, F_s);
         hipLaunchKernelGGL((k_gemm_bf16<true, true, EPI_BF16_BIAS>), grid, dim3(256), 0, s, (const bf16_t *)X, F_s,
                            (int64_t)1, (const bf16_t *)Wh, (int64_t)1, F_s, Yh, H, bias_h, B, H, F_s, F_s);
     } else {
@@ -212,9 +382,16 @@ hipError_t head_bwd(int64_t B, int64_t F_s, int64_t H, int32_t dtype, const void
         // M = H, N = F_s, K = B;  A(m,k) = dYh[k*H + m];  B(k,n) = X[k*F_s + n]
         if (bf) {
             const dim3 grid((unsigned)cdiv(F_s, TN), (unsigned)cdiv(H, TM), 1);
-            hipLaunchKernelGGL((k_gemm_bf16<false, false, EPI_F32>), grid, dim3(256), 0, s, (const bf16_t *)dYh,
-                               (int64_t)1, H, (const bf16_t *)X, F_s, (int64_t)1, (void *)dWh, F_s,
-                               (const float *)nullptr, H, F_s, B, B);
+            if (gemm2_ok(B, F_s, H)) {
+                hipError_t e = launch_gemm2<false, false, EPI_F32>(grid, s, (const bf16_t *)dYh, 1, H, B * H,
+                                                                   (const bf16_t *)X, F_s, 1, B * F_s, (void *)dWh,
+                                                                   F_s, nullptr, H, F_s, B, B);
+                if (e != hipSuccess) return e;
+            } else {
+                hipLaunchKernelGGL((k_gemm_bf16<false, false, EPI_F32>), grid, dim3(256), 0, s, (const bf16_t *)dYh,
+                                   (int64_t)1, H, (const bf16_t *)X, F_s, (int64_t)1, (void *)dWh, F_s,
+                                   (const float *)nullptr, H, F_s, B, B);
+            }
         } else {
             const dim3 grid((unsigned)cdiv(F_s, 64), (unsigned)cdiv(H, 64), 1);
             hipLaunchKernelGGL((k_gemm_f32<EPI_F32>), grid, dim3(256), 0, s, (const float *)dYh, (int64_t)1, H,
@@ -232,9 +409,16 @@ hipError_t head_bwd(int64_t B, int64_t F_s, int64_t H, int32_t dtype, const void
         float *part = reinterpret_cast<float *>(ws);
         if (bf) {
             const dim3 grid((unsigned)cdiv(F_s, TN), (unsigned)cdiv(B, TM), (unsigned)Sx);
-            hipLaunchKernelGGL((k_gemm_bf16<true, false, EPI_F32_PART>), grid, dim3(256), 0, s, (const bf16_t *)dYh,
-                               H, (int64_t)1, (const bf16_t *)Wh, F_s, (int64_t)1, (void *)part, F_s,
-                               (const float *)nullptr, B, F_s, H, kchunk);
+            if (gemm2_ok(B, F_s, H)) {
+                hipError_t e = launch_gemm2<true, false, EPI_F32_PART>(grid, s, (const bf16_t *)dYh, H, 1, B * H,
+                                                                       (const bf16_t *)Wh, F_s, 1, H * F_s,
+                                                                       (void *)part, F_s, nullptr, B, F_s, H, kchunk);
+                if (e != hipSuccess) return e;
+            } else {
+                hipLaunchKernelGGL((k_gemm_bf16<true, false, EPI_F32_PART>), grid, dim3(256), 0, s,
+                                   (const bf16_t *)dYh, H, (int64_t)1, (const bf16_t *)Wh, F_s, (int64_t)1,
+                                   (void *)part, F_s, (const float *)nullptr, B, F_s, H, kchunk);
+            }
         } else {
             const dim3 grid((unsigned)cdiv(F_s, 64), (unsigned)cdiv(B, 64), (unsigned)Sx);
             hipLaunchKernelGGL((k_gemm_f32<EPI_F32_PART>), grid, dim3(256), 0, s, (const float *)dYh, H, (int64_t)1,
