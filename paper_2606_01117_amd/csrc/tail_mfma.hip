@@ -447,14 +447,22 @@ __global__ __launch_bounds__(kBwUnits * 64) void k_bwd_w(const bf16_t *__restric
 //     accumulator row idx[k, slot].
 // --------------------------------------------------------------------------------------------
 
-// W [K][G][F_in] -> WT [K][F_in][Gp], labels G .. Gp-1 zero.  One group per workgroup step.
-__global__ __launch_bounds__(256) void k_transpose_w(const bf16_t *__restrict__ W, bf16_t *__restrict__ WT,
-                                                     int64_t K, int G, int Gp, int F_in) {
+// W [K][G][F_in] -> WT [K][F_in][Gp], labels G .. Gp-1 zero; and idx [K][F_in] -> idxl [K][16][F_in/16]
+// (the supports of slots l16, 16 + l16, ... side by side, one vector load per lane).  One group per
+// workgroup step.
+__global__ __launch_bounds__(256) void k_transpose_w(const bf16_t *__restrict__ W, const int32_t *__restrict__ idx,
+                                                     bf16_t *__restrict__ WT, int32_t *__restrict__ idxl, int64_t K,
+                                                     int G, int Gp, int F_in) {
     extern __shared__ __align__(16) bf16_t tw[];  // [F_in][Gp + 4]
     const int TS = Gp + 4;
     const int tid = threadIdx.x;
     const int nq = F_in / 4;                      // slot quads per label
+    const int nst = F_in / 16;
     for (int64_t k = blockIdx.x; k < K; k += gridDim.x) {
+        if (threadIdx.x < F_in) {
+            const int t = threadIdx.x;   // slot 16 st + l16 -> position l16 * nst + st
+            idxl[k * F_in + (t & 15) * nst + (t >> 4)] = idx[k * F_in + t];
+        }
         const uint2 *src = reinterpret_cast<const uint2 *>(W + k * G * F_in);
         for (int e = tid; e < G * nq; e += blockDim.x) {
             const int g = e / nq, s4 = (e - g * nq) * 4;
@@ -579,7 +587,7 @@ __global__ __launch_bounds__(256) void k_bwd_x(const int32_t *__restrict__ idx, 
         // a group plus a wave-uniform group offset (the segment spans less than 2 GB).
         const uint32_t gbytes = (uint32_t)(F_IN * Gp * 2);
         const Buf wseg(WT + g_begin * F_IN * Gp, (uint32_t)n * gbytes);
-        const Buf iseg(idx + g_begin * F_IN, (uint32_t)(n * F_IN * 4));
+        const Buf iseg(idx + g_begin * F_IN, (uint32_t)(n * F_IN * 4));  // lane-ordered supports
         uint32_t wvo[NLB][NST];
 #pragma unroll
         for (int c = 0; c < NLB; ++c)
@@ -595,9 +603,22 @@ __global__ __launch_bounds__(256) void k_bwd_x(const int32_t *__restrict__ idx, 
                 for (int st = 0; st < NST; ++st)
                     t.w[c][st] = __builtin_bit_cast(
                         uint4, __builtin_amdgcn_raw_buffer_load_b128(wseg.r, (int)wvo[c][st], (int)(sg * gbytes), 0));
+            // the NST supports of this lane's slots, side by side
+            if constexpr (NST == 2) {
+                const uint2 v = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(iseg.r, l16 * 8, sg * F_IN * 4, 0));
+                t.f[0] = (int)v.x;
+                t.f[1] = (int)v.y;
+            } else {
 #pragma unroll
-            for (int st = 0; st < NST; ++st)
-                t.f[st] = __builtin_amdgcn_raw_buffer_load_b32(iseg.r, (16 * st + l16) * 4, sg * F_IN * 4, 0);
+                for (int h = 0; h < NST / 4; ++h) {
+                    const uint4 v = __builtin_bit_cast(
+                        uint4, __builtin_amdgcn_raw_buffer_load_b128(iseg.r, (l16 * NST + 4 * h) * 4, sg * F_IN * 4, 0));
+                    t.f[4 * h + 0] = (int)v.x;
+                    t.f[4 * h + 1] = (int)v.y;
+                    t.f[4 * h + 2] = (int)v.z;
+                    t.f[4 * h + 3] = (int)v.w;
+                }
+            }
         };
 
         const int r = 16 * bh + l16;               // tile row of this lane's dY operand
@@ -634,16 +655,17 @@ __global__ __launch_bounds__(256) void k_bwd_x(const int32_t *__restrict__ idx, 
             }
         };
 
-        // Group g's weights live in buffer g % NB, loaded NB groups ahead (clamped index past the
-        // end, so every wait covers only its own loads); its dY operand is read one step ahead, in
-        // buffer g % 2.  Step s: read the accumulator rows of group s, read the dY operand of
-        // group s + 1, then D = dZ_s W_s + old through the matrix core (its accumulator input) and
+        // Group g's weights live in buffer g % NB, loaded NB - 1 groups ahead (clamped index past
+        // the end, so every wait covers only its own loads); its dY operand is read one step ahead,
+        // in buffer g % 2.  Step s: read the accumulator rows of group s; refill the buffer group
+        // s - 1 has finished with (the load issue overlaps the LDS reads); read the dY operand of
+        // group s + 1; then D = dZ_s W_s + old through the matrix core (its accumulator input) and
         // write D back.  The group count is padded to a multiple of NB so that the unrolled body
         // has no branch around a load.
         BwdXGroup<F_IN, NLB> tl[NB];
         uint4 ay[2][NLB];
 #pragma unroll
-        for (int b = 0; b < NB; ++b) {
+        for (int b = 0; b < NB - 1; ++b) {
             issue(cl(b), tl[b]);
             __builtin_amdgcn_sched_barrier(0);  // keep prefetch order
         }
@@ -660,6 +682,9 @@ __global__ __launch_bounds__(256) void k_bwd_x(const int32_t *__restrict__ idx, 
                     ao[st] = __umul24((uint32_t)tl[b].f[st], AS * 4);
                     acc[st] = *reinterpret_cast<const f32x4_t *>(accb + ao[st]);
                 }
+                __builtin_amdgcn_sched_barrier(0);  // accumulator reads first
+                issue(cl(sg + NB - 1), tl[(b + NB - 1) % NB]);
+                __builtin_amdgcn_sched_barrier(0);  // keep prefetch order
                 read_dy(ay[(b + 1) & 1], sg + 1 < n);
 #pragma unroll
                 for (int st = 0; st < NST; ++st) {
@@ -668,8 +693,6 @@ __global__ __launch_bounds__(256) void k_bwd_x(const int32_t *__restrict__ idx, 
                         acc[st] = mfma16x16x32(as_bf16x8(ay[b & 1][c]), as_bf16x8(tl[b].w[c][st]), acc[st]);
                     *reinterpret_cast<f32x4_t *>(accb + ao[st]) = acc[st];
                 }
-                issue(cl(sg + NB), tl[b]);
-                __builtin_amdgcn_sched_barrier(0);  // keep prefetch order
             }
         }
     }
@@ -823,14 +846,18 @@ bool bwd_x_mfma_supported(const TailArgs &a) {
     return g.ch >= 2 && g.lds <= kLdsBudget;
 }
 
-// workspace: the per-segment partials, then W^T (group blocks [F_in][Gp])
+// workspace: the per-segment partials, then W^T (group blocks [F_in][Gp]), then the supports in lane order
 static size_t bwd_x_part_bytes(const TailArgs &a, const BwdXGeom &g) {
     return round_up((int64_t)g.nseg * a.F_s * (g.nbt * 32) * 4, 256);
 }
 
+static size_t bwd_x_wt_bytes(const TailArgs &a) {
+    return (size_t)round_up((a.L / a.G) * a.F_in * round_up(a.G, 8) * 2, 256);
+}
+
 size_t bwd_x_mfma_ws(const TailArgs &a) {
     const BwdXGeom g = bwd_x_geom(a);
-    return bwd_x_part_bytes(a, g) + (size_t)(a.L / a.G) * (size_t)a.F_in * (size_t)round_up(a.G, 8) * 2 + 256;
+    return bwd_x_part_bytes(a, g) + bwd_x_wt_bytes(a) + (size_t)(a.L / a.G) * (size_t)a.F_in * 4 + 256;
 }
 
 template <int F_IN, int NLB>
@@ -863,17 +890,18 @@ hipError_t bwd_x_mfma(const TailArgs &a, const int32_t *idx, const void *W, cons
     const BwdXGeom g = bwd_x_geom(a);
     float *part = reinterpret_cast<float *>(ws);
     bf16_t *WT = reinterpret_cast<bf16_t *>(reinterpret_cast<char *>(ws) + bwd_x_part_bytes(a, g));
+    int32_t *idxl = reinterpret_cast<int32_t *>(reinterpret_cast<char *>(WT) + bwd_x_wt_bytes(a));
     const int64_t K = a.L / a.G;
     const int Gp = (int)round_up(a.G, 8);
     const int64_t tgrid = K < 4096 ? K : 4096;
     hipLaunchKernelGGL(k_transpose_w, dim3((unsigned)tgrid), dim3(256), (size_t)a.F_in * (Gp + 4) * 2, s,
-                       (const bf16_t *)W, WT, K, (int)a.G, Gp, (int)a.F_in);
+                       (const bf16_t *)W, idx, WT, idxl, K, (int)a.G, Gp, (int)a.F_in);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     switch (a.F_in) {
-        case 32: e = launch_bwd_x_g<32>(a, g, idx, WT, dY, part, s); break;
-        case 64: e = launch_bwd_x_g<64>(a, g, idx, WT, dY, part, s); break;
-        case 128: e = launch_bwd_x_g<128>(a, g, idx, WT, dY, part, s); break;
+        case 32: e = launch_bwd_x_g<32>(a, g, idxl, WT, dY, part, s); break;
+        case 64: e = launch_bwd_x_g<64>(a, g, idxl, WT, dY, part, s); break;
+        case 128: e = launch_bwd_x_g<128>(a, g, idxl, WT, dY, part, s); break;
         default: return hipErrorInvalidValue;
     }
     if (e != hipSuccess) return e;
