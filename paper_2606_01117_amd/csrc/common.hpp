@@ -94,6 +94,10 @@ struct Buf {
         __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(decltype(__builtin_amdgcn_raw_buffer_load_b64(r, 0, 0, 0)), v),
                                               r, (int)off, 0, 0);
     }
+    __device__ __forceinline__ void st16(uint4 v, uint32_t off) const {
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(decltype(__builtin_amdgcn_raw_buffer_load_b128(r, 0, 0, 0)), v),
+                                               r, (int)off, 0, 0);
+    }
 };
 
 // ---- host-side launchers (one translation unit each) -----------------------------------------

@@ -35,12 +35,12 @@ template <int F_IN, bool HAS_BIAS>
 struct FwdUnit {
     int4 fi[F_IN / 8];                // support indices, this lane's half of every 16-slot K-step
     uint4 w[F_IN / 16];               // weights of this lane's label, same slots
-    float4 bias[HAS_BIAS ? 4 : 1];    // bias of the labels this lane stores (8i + 4hh .. +3)
+    float4 bias[HAS_BIAS ? 4 : 1];    // bias of this lane's accumulator labels (8i + 4hh .. +3)
 };
 
-constexpr int kFwdStageRow = 72;                   // bytes per staged row: 32 labels + 4 pad
+constexpr int kFwdStageRow = 144;                  // bytes per staged row: 64 labels + 8 pad
 
-template <int BT, int F_IN, bool HAS_BIAS>
+template <int BT, int F_IN, bool HAS_BIAS, bool WIDE>
 __global__ __launch_bounds__(512) void k_fwd(const bf16_t *__restrict__ X, const int32_t *__restrict__ idx,
                                              const bf16_t *__restrict__ W, const float *__restrict__ bias,
                                              bf16_t *__restrict__ Y, int B, int F_s, int S16, int64_t L, int G,
@@ -80,9 +80,22 @@ __global__ __launch_bounds__(512) void k_fwd(const bf16_t *__restrict__ X, const
     const int64_t u_end = g_end * ntn;
     constexpr int KS = F_IN / 16;   // MFMA K-steps over the support slots
     constexpr int NT = BT / 32;     // MFMA N-tiles over the batch rows
-    char *stg = reinterpret_cast<char *>(xs) + (size_t)BT * S16 * 2 + wave * (BT * kFwdStageRow);
+    // wide supports: one n-tile of both units at a time, so that two units' operands and
+    // accumulators fit the registers
+    constexpr bool kFwdByTile = F_IN >= 128;
+    constexpr bool kPreBias = HAS_BIAS && !kFwdByTile;  // bias prefetched with the unit
+    using Unit = FwdUnit<F_IN, kPreBias>;
+    char *stg = reinterpret_cast<char *>(xs) + (size_t)BT * S16 * 2 + wave * (32 * kFwdStageRow);
 
-    auto issue = [&](int64_t u, FwdUnit<F_IN, HAS_BIAS> &f) {
+    // bias of this lane's accumulator labels in a unit: tile*32 + 8i + 4hh .. +3 of group k
+    auto load_bias = [&](uint32_t k, int tile, float4 (&b)[4]) {
+        const Buf bb(bias + (int64_t)k * G, (uint32_t)(G * 4));
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            b[i] = __builtin_bit_cast(float4, bb.ld16((uint32_t)((tile * 32 + 8 * i + 4 * hh) * 4)));
+    };
+
+    auto issue = [&](int64_t u, Unit &f) {
         const uint32_t uu = (uint32_t)u;   // unit indices fit in 32 bits (L * 128 < 2^31)
         const uint32_t k = ntn == 1 ? uu : uu / (uint32_t)ntn;
         const int tile = (int)(uu - k * (uint32_t)ntn);
@@ -97,26 +110,44 @@ __global__ __launch_bounds__(512) void k_fwd(const bf16_t *__restrict__ X, const
         const Buf wb(W + (int64_t)k * G * F_IN, (uint32_t)(G * F_IN * 2));
 #pragma unroll
         for (int s = 0; s < KS; ++s) f.w[s] = wb.ld16((uint32_t)((col * F_IN + 8 * hh + 16 * s) * 2));
-        if (HAS_BIAS) {
-            const Buf bb(bias + (int64_t)k * G, (uint32_t)(G * 4));
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-                f.bias[i] = __builtin_bit_cast(float4, bb.ld16((uint32_t)((tile * 32 + 8 * i + 4 * hh) * 4)));
-        }
+        if constexpr (kPreBias) load_bias(k, tile, f.bias);
     };
 
-    // one unit: gather H_k for this tile from the slab, MFMA with the labels' weights, and stage
-    // the bf16 tile in this wave's LDS buffer as [row][label]
-    auto compute = [&](int64_t u, const FwdUnit<F_IN, HAS_BIAS> &cu) {
-        f32x16_t acc[NT];
+    // one unit: gather H_k for this tile from the slab and MFMA with the labels' weights; the
+    // accumulators start from the labels' biases (D[m = label 8i + 4hh + j][n = row])
+    auto compute = [&](const Unit &cu, int64_t u, f32x16_t (&acc)[NT], int n0, int n1) {
+        float4 bv[4];
+        if constexpr (kPreBias) {
 #pragma unroll
-        for (int n = 0; n < NT; ++n) acc[n] = f32x16_t{0};
+            for (int i = 0; i < 4; ++i) bv[i] = cu.bias[i];
+        } else if constexpr (HAS_BIAS) {
+            // not prefetched (registers): loaded here, its latency exposed
+            const uint32_t uu = (uint32_t)u;
+            const uint32_t k = ntn == 1 ? uu : uu / (uint32_t)ntn;
+            load_bias(k, (int)(uu - k * (uint32_t)ntn), bv);
+        }
+#pragma unroll
+        for (int n = 0; n < NT; ++n) {
+            if (n < n0 || n >= n1) continue;
+            if (HAS_BIAS) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    acc[n][4 * i + 0] = bv[i].x;
+                    acc[n][4 * i + 1] = bv[i].y;
+                    acc[n][4 * i + 2] = bv[i].z;
+                    acc[n][4 * i + 3] = bv[i].w;
+                }
+            } else {
+                acc[n] = f32x16_t{0};
+            }
+        }
 #pragma unroll
         for (int s = 0; s < KS; ++s) {
             const int fa[8] = {cu.fi[2 * s].x, cu.fi[2 * s].y, cu.fi[2 * s].z, cu.fi[2 * s].w,
                                cu.fi[2 * s + 1].x, cu.fi[2 * s + 1].y, cu.fi[2 * s + 1].z, cu.fi[2 * s + 1].w};
 #pragma unroll
             for (int n = 0; n < NT; ++n) {
+                if (n < n0 || n >= n1) continue;
                 // gather: B[k = slot][n = row] = X[b0 + 32n + ln][idx[k, slot]]
                 const bf16_t *row = xs + (n * 32 + ln) * S16;
                 uint4 bv;
@@ -127,48 +158,64 @@ __global__ __launch_bounds__(512) void k_fwd(const bf16_t *__restrict__ X, const
                 acc[n] = mfma32x32x16(as_bf16x8(cu.w[s]), as_bf16x8(bv), acc[n]);
             }
         }
-        // D[m = label 8i + 4hh + j][n = row ln] -> stage[n][row ln][labels 8i + 4hh .. +3]
-#pragma unroll
-        for (int n = 0; n < NT; ++n)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const float4 bv = HAS_BIAS ? cu.bias[i] : make_float4(0.f, 0.f, 0.f, 0.f);
-                const uint2 v = make_uint2(pack_bf16(acc[n][4 * i + 0] + bv.x, acc[n][4 * i + 1] + bv.y),
-                                           pack_bf16(acc[n][4 * i + 2] + bv.z, acc[n][4 * i + 3] + bv.w));
-                *reinterpret_cast<uint2 *>(stg + (n * 32 + ln) * kFwdStageRow + (8 * i + 4 * hh) * 2) = v;
-            }
     };
 
-    // Store a staged unit: 8 bytes (4 labels) per lane, lane -> row 8p + lane/8, labels 4(lane%8)
-    // .. +3.  Rows past B fall outside the buffer, labels past G are sent out of range.  Stores are
-    // issued after the next unit's loads: on gfx9 one in-order counter covers loads and stores, so
-    // a wait for a load also waits for every store issued before it.
-    const int sr = lane >> 3, sc = lane & 7;
-    const int rows = B - b0 < BT ? B - b0 : BT;
-    auto store = [&](int64_t u) {
+    // D[m = label 8i + 4hh + j][n = row ln] of one n-tile -> stage[row ln][col0 + 8i + 4hh .. +3]
+    auto stage = [&](const f32x16_t &acc, int col0) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const uint2 v = make_uint2(pack_bf16(acc[4 * i + 0], acc[4 * i + 1]),
+                                       pack_bf16(acc[4 * i + 2], acc[4 * i + 3]));
+            *reinterpret_cast<uint2 *>(stg + ln * kFwdStageRow + (col0 + 8 * i + 4 * hh) * 2) = v;
+        }
+    };
+
+    // Labels of a unit: [k G + 32 tile, + nlab).  Units u and u + 1 cover contiguous labels.
+    auto unit_labels = [&](int64_t u, int64_t &lab0, int &nlab) {
         const uint32_t uu = (uint32_t)u;
         const uint32_t k = ntn == 1 ? uu : uu / (uint32_t)ntn;
         const int tile = (int)(uu - k * (uint32_t)ntn);
-        const int64_t lab0 = (int64_t)k * G + tile * 32;
-        const int nlab = G - tile * 32 < 32 ? G - tile * 32 : 32;
+        lab0 = (int64_t)k * G + tile * 32;
+        nlab = G - tile * 32 < 32 ? G - tile * 32 : 32;
+    };
+
+    // Store the staged 32-row tile of a unit pair (width labels from lab0): WIDE = 16 bytes per
+    // lane (8 lanes per 128-byte row, 8 rows per instruction; needs G and L multiples of 8), else
+    // 8 bytes per lane (16 lanes per row, 4 rows per instruction).  Rows past B fall outside the
+    // buffer; labels past the pair are sent out of range.
+    const int rows = B - b0 < BT ? B - b0 : BT;
+    auto store_tile = [&](int n, int64_t lab0, int width) {
         const Buf yb(Y + (int64_t)b0 * L + lab0, (uint32_t)((int64_t)rows * L * 2));
-        const bool ok = 4 * sc < nlab;
-#pragma unroll
-        for (int n = 0; n < NT; ++n)
+        if (WIDE) {
+            const int sr = lane >> 3, sc = lane & 7;
+            const bool ok = 8 * sc < width;
 #pragma unroll
             for (int p = 0; p < 4; ++p) {
                 const int r = 8 * p + sr;
-                const uint2 v = *reinterpret_cast<const uint2 *>(stg + (n * 32 + r) * kFwdStageRow + sc * 8);
+                const uint4 v = *reinterpret_cast<const uint4 *>(stg + r * kFwdStageRow + sc * 16);
+                const uint32_t off = (uint32_t)(((int64_t)(32 * n + r) * L + 8 * sc) * 2);
+                yb.st16(v, ok ? off : kOob);
+            }
+        } else {
+            const int sr = lane >> 4, sc = lane & 15;
+            const bool ok = 4 * sc < width;
+#pragma unroll
+            for (int p = 0; p < 8; ++p) {
+                const int r = 4 * p + sr;
+                const uint2 v = *reinterpret_cast<const uint2 *>(stg + r * kFwdStageRow + sc * 8);
                 const uint32_t off = (uint32_t)(((int64_t)(32 * n + r) * L + 4 * sc) * 2);
                 yb.st8(v, ok ? off : kOob);
             }
+        }
     };
 
     // Two units in flight per wave in ping-pong buffers (no register copies).  A wave takes two
-    // consecutive 32-label tiles at a time, so both halves of each 128-byte line of a Y row are
-    // written by the same wave back to back.  Prefetches are issued unconditionally (the index
-    // is clamped to the last unit) so that every wait only covers the loads it needs.
-    FwdUnit<F_IN, HAS_BIAS> ua, ub;
+    // consecutive 32-label tiles at a time and stores them together, so each 128-byte line of a
+    // Y row is written whole.  Prefetches are issued unconditionally (the index is clamped to
+    // the last unit) so that every wait only covers the loads it needs; the stores follow both
+    // prefetches, so those waits never cover them either (on gfx9 one in-order counter covers
+    // vector loads and stores).
+    Unit ua, ub;
     const int64_t st = 2 * nwaves;
     const int64_t last = u_end - 1;
     auto cl = [&](int64_t v) { return v < last ? v : last; };
@@ -179,15 +226,42 @@ __global__ __launch_bounds__(512) void k_fwd(const bf16_t *__restrict__ X, const
     issue(cl(u + 1), ub);
     __builtin_amdgcn_sched_barrier(0);  // keep prefetch order
     for (; u <= last; u += st) {
-        compute(u, ua);
-        issue(cl(u + st), ua);
-        __builtin_amdgcn_sched_barrier(0);  // keep prefetch order
-        store(u);
-        const bool two = u + 1 <= last;
-        if (two) compute(u + 1, ub);
-        issue(cl(u + st + 1), ub);
-        __builtin_amdgcn_sched_barrier(0);  // keep prefetch order
-        if (two) store(u + 1);
+        int64_t lab0, lab1;
+        int na, nb;
+        unit_labels(u, lab0, na);
+        unit_labels(cl(u + 1), lab1, nb);
+        const int width = na + (u + 1 <= last ? nb : 0);
+        f32x16_t acc_a[NT], acc_b[NT];
+        if (!kFwdByTile) {
+            compute(ua, u, acc_a, 0, NT);
+            __builtin_amdgcn_sched_barrier(0);
+            compute(ub, cl(u + 1), acc_b, 0, NT);     // past the last unit: a repeat, never stored
+            __builtin_amdgcn_sched_barrier(0);
+            // both units' registers are free once their products are done: prefetch the next pair
+            issue(cl(u + st), ua);
+            __builtin_amdgcn_sched_barrier(0);  // keep prefetch order
+            issue(cl(u + st + 1), ub);
+            __builtin_amdgcn_sched_barrier(0);  // keep prefetch order
+        }
+#pragma unroll
+        for (int n = 0; n < NT; ++n) {
+            if (kFwdByTile) {
+                // one n-tile of both units at a time: half the accumulators live
+                compute(ua, u, acc_a, n, n + 1);
+                __builtin_amdgcn_sched_barrier(0);
+                compute(ub, cl(u + 1), acc_b, n, n + 1);
+                __builtin_amdgcn_sched_barrier(0);
+                if (n == NT - 1) {
+                    issue(cl(u + st), ua);
+                    __builtin_amdgcn_sched_barrier(0);  // keep prefetch order
+                    issue(cl(u + st + 1), ub);
+                    __builtin_amdgcn_sched_barrier(0);  // keep prefetch order
+                }
+            }
+            stage(acc_a[n], 0);
+            stage(acc_b[n], na);   // a unit of fewer than 32 labels: its unused columns are overwritten
+            store_tile(n, lab0, width);
+        }
     }
 }
 
@@ -757,12 +831,12 @@ bool fwd_mfma_supported(const TailArgs &a) {
            a.L * 128 < ((int64_t)1 << 31);
 }
 
-template <int BT, int F_IN, bool HAS_BIAS>
+template <int BT, int F_IN, bool HAS_BIAS, bool WIDE>
 static hipError_t launch_fwd(const TailArgs &a, const void *X, const int32_t *idx, const void *W,
                              const float *bias, void *Y, hipStream_t s) {
     const int S16 = slab_s16((int)a.F_s);
     const int threads = BT == 64 ? 512 : 256;
-    const size_t lds = (size_t)BT * S16 * 2 + (size_t)(threads / 64) * BT * kFwdStageRow;
+    const size_t lds = (size_t)BT * S16 * 2 + (size_t)(threads / 64) * 32 * kFwdStageRow;
     const int occ = (int)(kLdsBudget / lds) < 1 ? 1 : (int)(kLdsBudget / lds);
     const int occ_eff = BT == 64 ? 1 : (occ > 3 ? 3 : occ);
     const int nbt = (int)cdiv(a.B, BT);
@@ -774,7 +848,7 @@ static hipError_t launch_fwd(const TailArgs &a, const void *X, const int32_t *id
     const int64_t nstream = spx * kXcds;
     const int64_t gps = cdiv(K, nstream);
     const int64_t grid = nstream * nbt;
-    auto kern = k_fwd<BT, F_IN, HAS_BIAS>;
+    auto kern = k_fwd<BT, F_IN, HAS_BIAS, WIDE>;
     hipError_t e = allow_lds(kern, lds);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(threads), lds, s, (const bf16_t *)X, idx, (const bf16_t *)W,
@@ -785,8 +859,13 @@ static hipError_t launch_fwd(const TailArgs &a, const void *X, const int32_t *id
 template <int BT, int F_IN>
 static hipError_t launch_fwd_b(const TailArgs &a, const void *X, const int32_t *idx, const void *W,
                                const float *bias, void *Y, hipStream_t s) {
-    return bias ? launch_fwd<BT, F_IN, true>(a, X, idx, W, bias, Y, s)
-                : launch_fwd<BT, F_IN, false>(a, X, idx, W, bias, Y, s);
+    // 16-byte stores need whole 8-label chunks: groups of a multiple of 8 labels, aligned logits
+    const bool wide = (a.G % 8) == 0 && (reinterpret_cast<uintptr_t>(Y) & 15) == 0;
+    if (wide)
+        return bias ? launch_fwd<BT, F_IN, true, true>(a, X, idx, W, bias, Y, s)
+                    : launch_fwd<BT, F_IN, false, true>(a, X, idx, W, bias, Y, s);
+    return bias ? launch_fwd<BT, F_IN, true, false>(a, X, idx, W, bias, Y, s)
+                : launch_fwd<BT, F_IN, false, false>(a, X, idx, W, bias, Y, s);
 }
 
 hipError_t fwd_mfma(const TailArgs &a, const void *X, const int32_t *idx, const void *W, const float *bias,

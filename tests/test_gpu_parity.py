@@ -55,6 +55,10 @@ SMALL = [
     ("bf16_g3_f16", 20, 128, 600, 3, 16, BF16),
     ("bf16_b300_g32", 300, 768, 8192, 32, 64, BF16),
     ("bf16_b511_g32_f128", 511, 768, 2048, 32, 128, BF16),
+    # a group of 72 = 32 + 32 + 8 labels: unit pairs that start on a partial tile
+    ("bf16_g72_f32", 48, 384, 72 * 29, 72, 32, BF16),
+    # 12-label groups (4-label stores) with a 128-slot support
+    ("bf16_g12_f128", 45, 512, 12 * 37, 12, 128, BF16),
     ("f32_g8", 32, 256, 4096, 8, 32, F32),
     ("f32_g1", 9, 100, 300, 1, 7, F32),
     ("f32_g32_f64", 50, 768, 2048, 32, 64, F32),
