@@ -11,6 +11,8 @@ typedef uint16_t bf16_t;  // bf16 bit pattern
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) bf16x4_t lds_bf16x4_t;
 
 // Hardware layout facts used by every kernel (CDNA4, 64-wide wavefronts).
 constexpr int kWave = 64;
@@ -30,6 +32,14 @@ __device__ __forceinline__ float load_f32(const float *p, int64_t i) { return p[
 __device__ __forceinline__ float load_f32(const bf16_t *p, int64_t i) { return bf16_to_f32(p[i]); }
 __device__ __forceinline__ void store_out(float *p, int64_t i, float v) { p[i] = v; }
 __device__ __forceinline__ void store_out(bf16_t *p, int64_t i, float v) { p[i] = f32_to_bf16(v); }
+
+// ds_read_b64_tr_b16: within each 16-lane group, lane r names an 8-byte word M[r] (4 bf16);
+// result lane i receives M[4j + i/4][i % 4] as element j (j = 0..3).  p must be 8-byte aligned
+// and point into LDS.
+__device__ __forceinline__ uint2 lds_read_tr(const void *p) {
+    const bf16x4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t *)(p));
+    return __builtin_bit_cast(uint2, v);
+}
 
 // D(32x32, fp32) += A(32x16, bf16) * B(16x32, bf16).
 // Lane l holds A[l % 32][8*(l/32) .. +7], B[8*(l/32) .. +7][l % 32] and

@@ -137,14 +137,6 @@ constexpr int G2KC = G2K + 8;           // [row][k] row stride (bf16): 144 bytes
 constexpr int G2RC = TM + 16;           // [k][row] row stride (bf16): 288 bytes
 constexpr int G2TILE = (TM * G2KC > G2K * G2RC ? TM * G2KC : G2K * G2RC);  // bf16 per operand tile
 
-typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) bf16x4_t lds_bf16x4_t;
-
-__device__ __forceinline__ uint2 lds_read_tr(const bf16_t *p) {
-    const bf16x4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t *)(p));
-    return __builtin_bit_cast(uint2, v);
-}
-
 // One operand: rows r0 .. r0+127 (M or N) by k0 .. k0+63, element (r, k) at base + r*sr + k*sk,
 // with sk == 1 (KC) or sr == 1.  The whole matrix spans `bytes` (buffer bound: zero outside).
 template <bool KC>

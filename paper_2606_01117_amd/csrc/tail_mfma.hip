@@ -11,41 +11,48 @@
 
 namespace {
 
-constexpr int kSlabPadDw = 1;  // LDS row padding of the X slab (keeps row strides an odd dword count)
 
 
 
 // --------------------------------------------------------------------------------------------
 // Forward.
 // A workgroup keeps BT rows of X resident in LDS (the "slab") and sweeps a contiguous stream of
-// groups.  Each wave owns one (group, 32-label tile) unit at a time: it takes the labels' weights
-// as the A operand in their natural row layout and gathers the group's support columns straight
-// from the slab into B-operand registers (gathered once per unit and batch tile, shared by the
-// tile's 32 labels through the MFMA M dimension).  The next unit's indices and weights are loaded
-// while the current one computes.  The nbt workgroups of one stream (one per batch tile) carry
-// the same blockIdx % 8, so they run on one XCD and W is fetched from HBM about once per stream.
-// Orientation: Z^T = W_k H_k^T (M = labels, N = batch rows, K = support slots); a result lane
-// holds 4 consecutive labels of one row.
-// Stores: each 32-row x 32-label tile goes through a small per-wave LDS buffer and leaves as
-// 8-byte pieces, 8 lanes per row and 8 rows per store instruction.  (Storing straight from the
+// groups.  Each wave owns two consecutive (group, 32-label tile) units at a time: it takes the
+// labels' weights as the A operand in their natural row layout and gathers the group's support
+// columns from the slab into B-operand registers (gathered once per unit and batch tile, shared by
+// the tile's 32 labels through the MFMA M dimension).  The next pair's indices and weights are
+// loaded while the current one computes.  The nbt workgroups of one stream (one per batch tile)
+// carry the same blockIdx % 8, so they run on one XCD and W is fetched from HBM about once per
+// stream.  Orientation: Z^T = W_k H_k^T (M = labels, N = batch rows, K = support slots); a result
+// lane holds 4 consecutive labels of one row.
+// Gather: the slab is stored transposed, one row of BT batch values per feature, so that a
+// feature's values for 4 consecutive rows are one 8-byte word.  ds_read_b64_tr_b16 then hands
+// each lane of a 16-lane group 4 support slots of its own row: source lane 4j + a names slot j of
+// a 4-slot quad and rows 4a .. 4a+3, and result lane i receives element i % 4 of the words of
+// lanes 4j + i / 4, i.e. row i of slots j = 0..3.  Two such reads fill one 8-slot B operand:
+// 16 elements per lane per LDS instruction instead of one.
+// Stores: the 32-row x 64-label output of a pair goes through a small per-wave LDS buffer and
+// leaves as whole 128-byte row pieces, 8 rows per store instruction.  (Storing straight from the
 // result layout takes 4x the instructions, or touches 32 rows of the [B, L] logits, megabytes
 // apart, per instruction; both limit the kernel well below HBM bandwidth.)
 // --------------------------------------------------------------------------------------------
 template <int F_IN, bool HAS_BIAS>
 struct FwdUnit {
-    int4 fi[F_IN / 8];                // support indices, this lane's half of every 16-slot K-step
-    uint4 w[F_IN / 16];               // weights of this lane's label, same slots
+    int fi[F_IN / 8];                 // support index of each of this lane's gather reads (2 per K-step)
+    uint4 w[F_IN / 16];               // weights of this lane's label, 8 slots per K-step
     float4 bias[HAS_BIAS ? 4 : 1];    // bias of this lane's accumulator labels (8i + 4hh .. +3)
 };
 
-constexpr int kFwdStageRow = 144;                  // bytes per staged row: 64 labels + 8 pad
+constexpr int kFwdStageRow = 144;     // bytes per staged row: 64 labels + 8 pad
+constexpr int kFwdXtPad = 4;          // bf16 padding of a transposed slab row (BT + 4 values)
 
 template <int BT, int F_IN, bool HAS_BIAS, bool WIDE>
 __global__ __launch_bounds__(512) void k_fwd(const bf16_t *__restrict__ X, const int32_t *__restrict__ idx,
                                              const bf16_t *__restrict__ W, const float *__restrict__ bias,
-                                             bf16_t *__restrict__ Y, int B, int F_s, int S16, int64_t L, int G,
+                                             bf16_t *__restrict__ Y, int B, int F_s, int64_t L, int G,
                                              int64_t K, int nbt, int64_t gps) {
     extern __shared__ __align__(16) bf16_t xs[];
+    constexpr int XR = BT + kFwdXtPad;   // values per transposed slab row (one feature)
     const int w = blockIdx.x;
     const int xcd = w % kXcds;
     const int jj = w / kXcds;
@@ -55,16 +62,19 @@ __global__ __launch_bounds__(512) void k_fwd(const bf16_t *__restrict__ X, const
     const int tid = threadIdx.x;
     const int nthr = blockDim.x;
 
-    // slab: rows b0 .. b0+BT-1 of X, zero rows past B (F_s is even: copy in bf16 pairs)
+    // transposed slab: xs[f * XR + r] = X[b0 + r, f], zero rows past B.  A thread takes two rows
+    // and two features (F_s and BT are even): two 4-byte reads, two 4-byte writes.
     {
         const int half = F_s >> 1;
         const uint32_t *X32 = reinterpret_cast<const uint32_t *>(X);
         uint32_t *xs32 = reinterpret_cast<uint32_t *>(xs);
-        const int rs32 = S16 >> 1;
-        for (int e = tid; e < BT * half; e += nthr) {
-            const int r = e / half, c = e - r * half;
-            const int b = b0 + r;
-            xs32[r * rs32 + c] = (b < B) ? X32[(int64_t)b * half + c] : 0u;
+        for (int e = tid; e < (BT / 2) * half; e += nthr) {
+            const int rp = e / half, c = e - rp * half;
+            const int b = b0 + 2 * rp;
+            const uint32_t v0 = b < B ? X32[(int64_t)b * half + c] : 0u;
+            const uint32_t v1 = b + 1 < B ? X32[(int64_t)(b + 1) * half + c] : 0u;
+            xs32[((2 * c) * XR >> 1) + rp] = (v0 & 0xffffu) | (v1 << 16);
+            xs32[((2 * c + 1) * XR >> 1) + rp] = (v0 >> 16) | (v1 & 0xffff0000u);
         }
     }
     __syncthreads();
@@ -80,12 +90,15 @@ __global__ __launch_bounds__(512) void k_fwd(const bf16_t *__restrict__ X, const
     const int64_t u_end = g_end * ntn;
     constexpr int KS = F_IN / 16;   // MFMA K-steps over the support slots
     constexpr int NT = BT / 32;     // MFMA N-tiles over the batch rows
-    // wide supports: one n-tile of both units at a time, so that two units' operands and
-    // accumulators fit the registers
-    constexpr bool kFwdByTile = F_IN >= 128;
-    constexpr bool kPreBias = HAS_BIAS && !kFwdByTile;  // bias prefetched with the unit
-    using Unit = FwdUnit<F_IN, kPreBias>;
-    char *stg = reinterpret_cast<char *>(xs) + (size_t)BT * S16 * 2 + wave * (32 * kFwdStageRow);
+    using Unit = FwdUnit<F_IN, HAS_BIAS>;
+    const size_t xt_bytes = ((size_t)F_s * XR * 2 + 15) & ~(size_t)15;
+    char *stg = reinterpret_cast<char *>(xs) + xt_bytes + wave * (32 * kFwdStageRow);
+
+    // gather roles: 16-lane group lane / 16 covers rows 16 ((lane / 16) % 2) .. +15 of an n-tile
+    // and K-half hh; as a source lane, i = lane % 16 = 4 jq + aq names slot jq of each 4-slot
+    // quad and rows 4 aq .. 4 aq + 3
+    const int jq = (lane & 15) >> 2;
+    const char *gbase = reinterpret_cast<const char *>(xs) + (16 * ((lane >> 4) & 1) + 4 * (lane & 3)) * 2;
 
     // bias of this lane's accumulator labels in a unit: tile*32 + 8i + 4hh .. +3 of group k
     auto load_bias = [&](uint32_t k, int tile, float4 (&b)[4]) {
@@ -100,42 +113,34 @@ __global__ __launch_bounds__(512) void k_fwd(const bf16_t *__restrict__ X, const
         const uint32_t k = ntn == 1 ? uu : uu / (uint32_t)ntn;
         const int tile = (int)(uu - k * (uint32_t)ntn);
         const int col = tile * 32 + ln;
-        const int32_t *ip = idx + (int64_t)k * F_IN + 8 * hh;
+        // read h of K-step s gathers slot 16 s + 8 hh + 4 h + jq
+        const int32_t *ip = idx + (int64_t)k * F_IN + 8 * hh + jq;
 #pragma unroll
         for (int s = 0; s < KS; ++s) {
-            f.fi[2 * s] = *reinterpret_cast<const int4 *>(ip + 16 * s);
-            f.fi[2 * s + 1] = *reinterpret_cast<const int4 *>(ip + 16 * s + 4);
+            f.fi[2 * s] = ip[16 * s];
+            f.fi[2 * s + 1] = ip[16 * s + 4];
         }
         // weights of the group (labels past G read as zero)
         const Buf wb(W + (int64_t)k * G * F_IN, (uint32_t)(G * F_IN * 2));
 #pragma unroll
         for (int s = 0; s < KS; ++s) f.w[s] = wb.ld16((uint32_t)((col * F_IN + 8 * hh + 16 * s) * 2));
-        if constexpr (kPreBias) load_bias(k, tile, f.bias);
+        if constexpr (HAS_BIAS) load_bias(k, tile, f.bias);
     };
 
     // one unit: gather H_k for this tile from the slab and MFMA with the labels' weights; the
     // accumulators start from the labels' biases (D[m = label 8i + 4hh + j][n = row])
-    auto compute = [&](const Unit &cu, int64_t u, f32x16_t (&acc)[NT], int n0, int n1) {
-        float4 bv[4];
-        if constexpr (kPreBias) {
-#pragma unroll
-            for (int i = 0; i < 4; ++i) bv[i] = cu.bias[i];
-        } else if constexpr (HAS_BIAS) {
-            // not prefetched (registers): loaded here, its latency exposed
-            const uint32_t uu = (uint32_t)u;
-            const uint32_t k = ntn == 1 ? uu : uu / (uint32_t)ntn;
-            load_bias(k, (int)(uu - k * (uint32_t)ntn), bv);
-        }
+    // after_step(j) runs after the j-th product (j = s * NT + n - n0)
+    // after_step(j) runs after the j-th product (j = s * NT + n)
+    auto compute = [&](const Unit &cu, f32x16_t (&acc)[NT], auto &&after_step) {
 #pragma unroll
         for (int n = 0; n < NT; ++n) {
-            if (n < n0 || n >= n1) continue;
-            if (HAS_BIAS) {
+            if constexpr (HAS_BIAS) {
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    acc[n][4 * i + 0] = bv[i].x;
-                    acc[n][4 * i + 1] = bv[i].y;
-                    acc[n][4 * i + 2] = bv[i].z;
-                    acc[n][4 * i + 3] = bv[i].w;
+                    acc[n][4 * i + 0] = cu.bias[i].x;
+                    acc[n][4 * i + 1] = cu.bias[i].y;
+                    acc[n][4 * i + 2] = cu.bias[i].z;
+                    acc[n][4 * i + 3] = cu.bias[i].w;
                 }
             } else {
                 acc[n] = f32x16_t{0};
@@ -143,19 +148,15 @@ __global__ __launch_bounds__(512) void k_fwd(const bf16_t *__restrict__ X, const
         }
 #pragma unroll
         for (int s = 0; s < KS; ++s) {
-            const int fa[8] = {cu.fi[2 * s].x, cu.fi[2 * s].y, cu.fi[2 * s].z, cu.fi[2 * s].w,
-                               cu.fi[2 * s + 1].x, cu.fi[2 * s + 1].y, cu.fi[2 * s + 1].z, cu.fi[2 * s + 1].w};
+            const char *p0 = gbase + cu.fi[2 * s] * (XR * 2);
+            const char *p1 = gbase + cu.fi[2 * s + 1] * (XR * 2);
 #pragma unroll
             for (int n = 0; n < NT; ++n) {
-                if (n < n0 || n >= n1) continue;
-                // gather: B[k = slot][n = row] = X[b0 + 32n + ln][idx[k, slot]]
-                const bf16_t *row = xs + (n * 32 + ln) * S16;
-                uint4 bv;
-                bv.x = pack2(row[fa[0]], row[fa[1]]);
-                bv.y = pack2(row[fa[2]], row[fa[3]]);
-                bv.z = pack2(row[fa[4]], row[fa[5]]);
-                bv.w = pack2(row[fa[6]], row[fa[7]]);
-                acc[n] = mfma32x32x16(as_bf16x8(cu.w[s]), as_bf16x8(bv), acc[n]);
+                // B[k = 8 hh + e][n = row] = X[b0 + 32 n + row][idx[k, 16 s + 8 hh + e]]
+                const uint2 lo = lds_read_tr(p0 + 64 * n);
+                const uint2 hi = lds_read_tr(p1 + 64 * n);
+                acc[n] = mfma32x32x16(as_bf16x8(cu.w[s]), as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y)), acc[n]);
+                after_step(s * NT + n);
             }
         }
     };
@@ -179,43 +180,48 @@ __global__ __launch_bounds__(512) void k_fwd(const bf16_t *__restrict__ X, const
         nlab = G - tile * 32 < 32 ? G - tile * 32 : 32;
     };
 
-    // Store the staged 32-row tile of a unit pair (width labels from lab0): WIDE = 16 bytes per
-    // lane (8 lanes per 128-byte row, 8 rows per instruction; needs G and L multiples of 8), else
-    // 8 bytes per lane (16 lanes per row, 4 rows per instruction).  Rows past B fall outside the
-    // buffer; labels past the pair are sent out of range.
+    // Stores of a unit pair's staged 32-row tiles (width labels from lab0).  WIDE: 16 bytes per
+    // lane, 8 lanes per 128-byte row and 8 rows per instruction (needs G and L multiples of 8);
+    // else 8 bytes per lane, 16 lanes per row and 4 rows per instruction.  Rows past B fall
+    // outside the buffer; labels past the pair are sent out of range.
+    constexpr int LPR = WIDE ? 8 : 16;          // lanes per staged row
+    constexpr int RPS = 64 / LPR;               // rows per store instruction
+    constexpr int SPT = 32 / RPS;               // store instructions per n-tile
+    constexpr int NS = NT * SPT;                // store instructions per pair
+    using SV = typename std::conditional<WIDE, uint4, uint2>::type;
     const int rows = B - b0 < BT ? B - b0 : BT;
-    auto store_tile = [&](int n, int64_t lab0, int width) {
-        const Buf yb(Y + (int64_t)b0 * L + lab0, (uint32_t)((int64_t)rows * L * 2));
-        if (WIDE) {
-            const int sr = lane >> 3, sc = lane & 7;
-            const bool ok = 8 * sc < width;
+    const int sr = lane / LPR, sc = lane % LPR;
+    // row 32 n + RPS p + sr of store i = n SPT + p; offsets stay below 64 rows (L * 128 < 2^31)
+    const uint32_t lane_off = (uint32_t)(((int64_t)sr * L + (int64_t)sc * (sizeof(SV) / 2)) * 2);
+    const uint32_t row_step = (uint32_t)(L * 2 * RPS);
+    auto unstage = [&](int n, SV (&sv)[NS]) {
 #pragma unroll
-            for (int p = 0; p < 4; ++p) {
-                const int r = 8 * p + sr;
-                const uint4 v = *reinterpret_cast<const uint4 *>(stg + r * kFwdStageRow + sc * 16);
-                const uint32_t off = (uint32_t)(((int64_t)(32 * n + r) * L + 8 * sc) * 2);
-                yb.st16(v, ok ? off : kOob);
-            }
-        } else {
-            const int sr = lane >> 4, sc = lane & 15;
-            const bool ok = 4 * sc < width;
-#pragma unroll
-            for (int p = 0; p < 8; ++p) {
-                const int r = 4 * p + sr;
-                const uint2 v = *reinterpret_cast<const uint2 *>(stg + r * kFwdStageRow + sc * 8);
-                const uint32_t off = (uint32_t)(((int64_t)(32 * n + r) * L + 4 * sc) * 2);
-                yb.st8(v, ok ? off : kOob);
-            }
-        }
+        for (int p = 0; p < SPT; ++p)
+            sv[n * SPT + p] = *reinterpret_cast<const SV *>(stg + (RPS * p + sr) * kFwdStageRow + sc * sizeof(SV));
+    };
+    Buf pyb(Y, 0);     // the pair whose tiles sv holds (none yet: every store out of range)
+    bool pok = false;  // this lane's labels lie within that pair
+    auto set_pair = [&](int64_t lab0, int width) {
+        pyb = Buf(Y + (int64_t)b0 * L + lab0, (uint32_t)((int64_t)rows * L * 2));
+        pok = sc * (int)(sizeof(SV) / 2) < width;
+    };
+    auto store_one = [&](int i, const SV (&sv)[NS]) {
+        const uint32_t off = pok ? lane_off + (uint32_t)i * row_step : kOob;
+        if constexpr (WIDE)
+            pyb.st16(sv[i], off);
+        else
+            pyb.st8(sv[i], off);
     };
 
     // Two units in flight per wave in ping-pong buffers (no register copies).  A wave takes two
     // consecutive 32-label tiles at a time and stores them together, so each 128-byte line of a
     // Y row is written whole.  Prefetches are issued unconditionally (the index is clamped to
-    // the last unit) so that every wait only covers the loads it needs; the stores follow both
-    // prefetches, so those waits never cover them either (on gfx9 one in-order counter covers
-    // vector loads and stores).
+    // the last unit) so that every wait only covers the loads it needs.  A pair's output is held
+    // in registers and its stores are spread over the next pair's products, so that loads and
+    // stores share the memory pipeline evenly; on gfx9 one in-order counter covers vector loads
+    // and stores, and the stores always follow the prefetches the next waits need.
     Unit ua, ub;
+    SV sv[NS];
     const int64_t st = 2 * nwaves;
     const int64_t last = u_end - 1;
     auto cl = [&](int64_t v) { return v < last ? v : last; };
@@ -232,37 +238,28 @@ __global__ __launch_bounds__(512) void k_fwd(const bf16_t *__restrict__ X, const
         unit_labels(cl(u + 1), lab1, nb);
         const int width = na + (u + 1 <= last ? nb : 0);
         f32x16_t acc_a[NT], acc_b[NT];
-        if (!kFwdByTile) {
-            compute(ua, u, acc_a, 0, NT);
-            __builtin_amdgcn_sched_barrier(0);
-            compute(ub, cl(u + 1), acc_b, 0, NT);     // past the last unit: a repeat, never stored
-            __builtin_amdgcn_sched_barrier(0);
-            // both units' registers are free once their products are done: prefetch the next pair
-            issue(cl(u + st), ua);
-            __builtin_amdgcn_sched_barrier(0);  // keep prefetch order
-            issue(cl(u + st + 1), ub);
-            __builtin_amdgcn_sched_barrier(0);  // keep prefetch order
-        }
+        compute(ua, acc_a, [&](int i) { if (i < NS) store_one(i, sv); });
+        __builtin_amdgcn_sched_barrier(0);
+        // past the last unit: a repeat, never stored
+        compute(ub, acc_b, [&](int i) { if (KS * NT + i < NS) store_one(KS * NT + i, sv); });
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int i = 2 * KS * NT; i < NS; ++i) store_one(i, sv);
+        // both units' registers are free once their products are done: prefetch the next pair
+        issue(cl(u + st), ua);
+        __builtin_amdgcn_sched_barrier(0);  // keep prefetch order
+        issue(cl(u + st + 1), ub);
+        __builtin_amdgcn_sched_barrier(0);  // keep prefetch order
 #pragma unroll
         for (int n = 0; n < NT; ++n) {
-            if (kFwdByTile) {
-                // one n-tile of both units at a time: half the accumulators live
-                compute(ua, u, acc_a, n, n + 1);
-                __builtin_amdgcn_sched_barrier(0);
-                compute(ub, cl(u + 1), acc_b, n, n + 1);
-                __builtin_amdgcn_sched_barrier(0);
-                if (n == NT - 1) {
-                    issue(cl(u + st), ua);
-                    __builtin_amdgcn_sched_barrier(0);  // keep prefetch order
-                    issue(cl(u + st + 1), ub);
-                    __builtin_amdgcn_sched_barrier(0);  // keep prefetch order
-                }
-            }
             stage(acc_a[n], 0);
             stage(acc_b[n], na);   // a unit of fewer than 32 labels: its unused columns are overwritten
-            store_tile(n, lab0, width);
+            unstage(n, sv);
         }
+        set_pair(lab0, width);
     }
+#pragma unroll
+    for (int i = 0; i < NS; ++i) store_one(i, sv);
 }
 
 // --------------------------------------------------------------------------------------------
@@ -780,11 +777,6 @@ __global__ __launch_bounds__(256) void k_bwd_x(const int32_t *__restrict__ idx, 
 // ---------------------------------------------------------------------------------------------
 // launch geometry
 // ---------------------------------------------------------------------------------------------
-int slab_s16(int F_s) {
-    int dw = (F_s + 1) / 2;
-    if ((dw & 1) == 0) dw += kSlabPadDw;
-    return 2 * dw;
-}
 
 constexpr size_t kLdsBudget = 160 * 1024;
 
@@ -831,12 +823,16 @@ bool fwd_mfma_supported(const TailArgs &a) {
            a.L * 128 < ((int64_t)1 << 31);
 }
 
+static size_t fwd_lds(int BT, int F_s) {
+    const size_t xt = ((size_t)F_s * (BT + kFwdXtPad) * 2 + 15) & ~(size_t)15;
+    return xt + (size_t)(BT == 64 ? 8 : 4) * 32 * kFwdStageRow;
+}
+
 template <int BT, int F_IN, bool HAS_BIAS, bool WIDE>
 static hipError_t launch_fwd(const TailArgs &a, const void *X, const int32_t *idx, const void *W,
                              const float *bias, void *Y, hipStream_t s) {
-    const int S16 = slab_s16((int)a.F_s);
     const int threads = BT == 64 ? 512 : 256;
-    const size_t lds = (size_t)BT * S16 * 2 + (size_t)(threads / 64) * 32 * kFwdStageRow;
+    const size_t lds = fwd_lds(BT, (int)a.F_s);
     const int occ = (int)(kLdsBudget / lds) < 1 ? 1 : (int)(kLdsBudget / lds);
     const int occ_eff = BT == 64 ? 1 : (occ > 3 ? 3 : occ);
     const int nbt = (int)cdiv(a.B, BT);
@@ -852,7 +848,7 @@ static hipError_t launch_fwd(const TailArgs &a, const void *X, const int32_t *id
     hipError_t e = allow_lds(kern, lds);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(threads), lds, s, (const bf16_t *)X, idx, (const bf16_t *)W,
-                       bias, (bf16_t *)Y, (int)a.B, (int)a.F_s, S16, a.L, (int)a.G, K, nbt, gps);
+                       bias, (bf16_t *)Y, (int)a.B, (int)a.F_s, a.L, (int)a.G, K, nbt, gps);
     return hipGetLastError();
 }
 
@@ -870,8 +866,8 @@ static hipError_t launch_fwd_b(const TailArgs &a, const void *X, const int32_t *
 
 hipError_t fwd_mfma(const TailArgs &a, const void *X, const int32_t *idx, const void *W, const float *bias,
                     void *Y, hipStream_t s) {
-    // 64-row slabs halve the weight re-reads once the batch is large enough
-    const bool big = a.B > 32;
+    // 64-row slabs halve the weight re-reads once the batch is large enough (and the slab fits)
+    const bool big = a.B > 32 && fwd_lds(64, (int)a.F_s) <= kLdsBudget;
     switch (a.F_in) {
         case 32: return big ? launch_fwd_b<64, 32>(a, X, idx, W, bias, Y, s) : launch_fwd_b<32, 32>(a, X, idx, W, bias, Y, s);
         case 64: return big ? launch_fwd_b<64, 64>(a, X, idx, W, bias, Y, s) : launch_fwd_b<32, 64>(a, X, idx, W, bias, Y, s);
