@@ -89,6 +89,8 @@ __device__ __forceinline__ bf16x8_t eye_operand(int ln, int hh, int off) {
 constexpr uint32_t kOob = 0x80000000u;
 constexpr int kRawBufferWord3 = 0x00020000;  // gfx9-family raw buffer format word
 
+constexpr int kStreaming = 2;  // non-temporal ("nt") cache policy of a buffer access
+
 struct Buf {
     __amdgpu_buffer_rsrc_t r;
     __device__ __forceinline__ Buf(const void *base, uint32_t bytes)
@@ -100,13 +102,16 @@ struct Buf {
     __device__ __forceinline__ uint4 ld16(uint32_t off) const {
         return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0));
     }
+    // POLICY: cache-policy bits of the instruction (kStreaming marks data not read again soon)
+    template <int POLICY = 0>
     __device__ __forceinline__ void st8(uint2 v, uint32_t off) const {
         __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(decltype(__builtin_amdgcn_raw_buffer_load_b64(r, 0, 0, 0)), v),
-                                              r, (int)off, 0, 0);
+                                              r, (int)off, 0, POLICY);
     }
+    template <int POLICY = 0>
     __device__ __forceinline__ void st16(uint4 v, uint32_t off) const {
         __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(decltype(__builtin_amdgcn_raw_buffer_load_b128(r, 0, 0, 0)), v),
-                                               r, (int)off, 0, 0);
+                                               r, (int)off, 0, POLICY);
     }
 };
 

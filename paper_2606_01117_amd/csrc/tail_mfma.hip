@@ -94,6 +94,17 @@ __global__ __launch_bounds__(512) void k_fwd(const bf16_t *__restrict__ X, const
     const size_t xt_bytes = ((size_t)F_s * XR * 2 + 15) & ~(size_t)15;
     char *stg = reinterpret_cast<char *>(xs) + xt_bytes + wave * (32 * kFwdStageRow);
 
+    // weight staging: WS slots per round, NR rounds; a load covers LPI labels x WS slots (CPL
+    // 16-byte chunks per label, whole 128-byte lines), IPR loads per round; LDS rows of RW bytes
+    constexpr int WS = F_IN < 64 ? F_IN : 64;
+    constexpr int NR = F_IN / WS;
+    constexpr int CPL = WS / 8;
+    constexpr int LPI = 64 / CPL;
+    constexpr int IPR = 32 / LPI;
+    constexpr int RW = WS * 2 + 16;
+    static_assert(32 * RW <= 32 * kFwdStageRow, "weight staging exceeds the wave's LDS buffer");
+    const int wl = lane / CPL, wc = lane % CPL;
+
     // gather roles: 16-lane group lane / 16 covers rows 16 ((lane / 16) % 2) .. +15 of an n-tile
     // and K-half hh; as a source lane, i = lane % 16 = 4 jq + aq names slot jq of each 4-slot
     // quad and rows 4 aq .. 4 aq + 3
@@ -112,7 +123,6 @@ __global__ __launch_bounds__(512) void k_fwd(const bf16_t *__restrict__ X, const
         const uint32_t uu = (uint32_t)u;   // unit indices fit in 32 bits (L * 128 < 2^31)
         const uint32_t k = ntn == 1 ? uu : uu / (uint32_t)ntn;
         const int tile = (int)(uu - k * (uint32_t)ntn);
-        const int col = tile * 32 + ln;
         // read h of K-step s gathers slot 16 s + 8 hh + 4 h + jq
         const int32_t *ip = idx + (int64_t)k * F_IN + 8 * hh + jq;
 #pragma unroll
@@ -120,17 +130,23 @@ __global__ __launch_bounds__(512) void k_fwd(const bf16_t *__restrict__ X, const
             f.fi[2 * s] = ip[16 * s];
             f.fi[2 * s + 1] = ip[16 * s + 4];
         }
-        // weights of the group (labels past G read as zero)
+        // weights of the tile's labels, whole 128-byte lines per instruction (labels past G read
+        // as zero): load s = r IPR + t holds slots r WS + 8 wc .. +7 of label LPI t + wl
         const Buf wb(W + (int64_t)k * G * F_IN, (uint32_t)(G * F_IN * 2));
+        const uint32_t wo = (uint32_t)(((tile * 32 + wl) * F_IN + 8 * wc) * 2);
 #pragma unroll
-        for (int s = 0; s < KS; ++s) f.w[s] = wb.ld16((uint32_t)((col * F_IN + 8 * hh + 16 * s) * 2));
+        for (int r = 0; r < NR; ++r)
+#pragma unroll
+            for (int t = 0; t < IPR; ++t)
+                f.w[r * IPR + t] = wb.ld16(wo + (uint32_t)((LPI * t * F_IN + r * WS) * 2));
         if constexpr (HAS_BIAS) load_bias(k, tile, f.bias);
     };
 
     // one unit: gather H_k for this tile from the slab and MFMA with the labels' weights; the
-    // accumulators start from the labels' biases (D[m = label 8i + 4hh + j][n = row])
-    // after_step(j) runs after the j-th product (j = s * NT + n - n0)
-    // after_step(j) runs after the j-th product (j = s * NT + n)
+    // accumulators start from the labels' biases (D[m = label 8i + 4hh + j][n = row]).  The
+    // weights pass through the wave's LDS buffer, WS slots at a time, to reach the A-operand
+    // layout (label ln, slots 16 s + 8 hh .. +7).  after_step(j) runs after the j-th product
+    // (j = s * NT + n).
     auto compute = [&](const Unit &cu, f32x16_t (&acc)[NT], auto &&after_step) {
 #pragma unroll
         for (int n = 0; n < NT; ++n) {
@@ -147,16 +163,27 @@ __global__ __launch_bounds__(512) void k_fwd(const bf16_t *__restrict__ X, const
             }
         }
 #pragma unroll
-        for (int s = 0; s < KS; ++s) {
-            const char *p0 = gbase + cu.fi[2 * s] * (XR * 2);
-            const char *p1 = gbase + cu.fi[2 * s + 1] * (XR * 2);
+        for (int r = 0; r < NR; ++r) {
 #pragma unroll
-            for (int n = 0; n < NT; ++n) {
-                // B[k = 8 hh + e][n = row] = X[b0 + 32 n + row][idx[k, 16 s + 8 hh + e]]
-                const uint2 lo = lds_read_tr(p0 + 64 * n);
-                const uint2 hi = lds_read_tr(p1 + 64 * n);
-                acc[n] = mfma32x32x16(as_bf16x8(cu.w[s]), as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y)), acc[n]);
-                after_step(s * NT + n);
+            for (int t = 0; t < IPR; ++t)
+                *reinterpret_cast<uint4 *>(stg + (LPI * t + wl) * RW + wc * 16) = cu.w[r * IPR + t];
+            uint4 wa[WS / 16];
+#pragma unroll
+            for (int sl = 0; sl < WS / 16; ++sl)
+                wa[sl] = *reinterpret_cast<const uint4 *>(stg + ln * RW + (16 * sl + 8 * hh) * 2);
+#pragma unroll
+            for (int sl = 0; sl < WS / 16; ++sl) {
+                const int s = r * (WS / 16) + sl;
+                const char *p0 = gbase + cu.fi[2 * s] * (XR * 2);
+                const char *p1 = gbase + cu.fi[2 * s + 1] * (XR * 2);
+#pragma unroll
+                for (int n = 0; n < NT; ++n) {
+                    // B[k = 8 hh + e][n = row] = X[b0 + 32 n + row][idx[k, 16 s + 8 hh + e]]
+                    const uint2 lo = lds_read_tr(p0 + 64 * n);
+                    const uint2 hi = lds_read_tr(p1 + 64 * n);
+                    acc[n] = mfma32x32x16(as_bf16x8(wa[sl]), as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y)), acc[n]);
+                    after_step(s * NT + n);
+                }
             }
         }
     };
@@ -207,10 +234,11 @@ __global__ __launch_bounds__(512) void k_fwd(const bf16_t *__restrict__ X, const
     };
     auto store_one = [&](int i, const SV (&sv)[NS]) {
         const uint32_t off = pok ? lane_off + (uint32_t)i * row_step : kOob;
+        // the logits are written once and not read again by this kernel: streaming stores
         if constexpr (WIDE)
-            pyb.st16(sv[i], off);
+            pyb.st16<kStreaming>(sv[i], off);
         else
-            pyb.st8(sv[i], off);
+            pyb.st8<kStreaming>(sv[i], off);
     };
 
     // Two units in flight per wave in ping-pong buffers (no register copies).  A wave takes two
