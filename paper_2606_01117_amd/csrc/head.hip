@@ -9,6 +9,8 @@
 // are contiguous along M/N are transposed while being written to LDS) and runs
 // v_mfma_f32_32x32x16_bf16 on a 2x2 grid of waves, each owning a 64x64 block.  dX contracts over
 // the H head labels, so it is split over K and the partials are reduced in a fixed order.
+#include <initializer_list>
+
 #include "common.hpp"
 
 namespace {
@@ -259,6 +261,225 @@ __global__ __launch_bounds__(256, 2) void k_gemm2(const bf16_t *__restrict__ A, 
 
 constexpr size_t kG2Lds = (size_t)4 * G2TILE * 2;   // two stages of two operand tiles
 
+// ---------------------------------------------------------------------------------------------
+// bf16 GEMM for large tiles: 256x256 output tile, 4 waves in a 2x2 grid each owning a 128x128
+// block (4x4 v_mfma_f32_32x32x16_bf16 accumulators, 256 registers per lane).  K advances in
+// steps of 32 through a ring of 4 LDS stages filled by direct global-to-LDS loads
+// (buffer_load_dwordx4 ... lds: 64 lanes x 16 bytes land contiguously at the address in M0), so
+// three steps are in flight while one is multiplied, without staging registers.  The loads are
+// issued from inline assembly and waited for explicitly (s_waitcnt vmcnt): issued through the
+// compiler's builtin, every LDS read would first wait for all of them.
+// Stage layouts carry an XOR swizzle of their 16-byte chunks instead of padding, so that a load
+// instruction still fills 1 KB of contiguous LDS:
+//   K-contiguous operand  [256 rows][32 k]:  chunk c of row r sits at c ^ ((r >> 1) & 3);
+//   M/N-contiguous        [32 k][256 rows]:  chunk c of k-row k sits at c ^ 2 (k & 3).
+// Both keep the fragment reads (16-byte row reads, and ds_read_b64_tr_b16 over 4 k-rows) free of
+// bank conflicts.  The products are formed as D^T = B^T A^T (the B tile is the MFMA A operand),
+// so a result lane holds 4 consecutive output columns of one row: 8-byte (bf16) or 16-byte
+// (fp32) stores.  Tiles that share an operand tile are placed on one XCD back to back.
+// ---------------------------------------------------------------------------------------------
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+constexpr int G4T = 256;                  // output tile (rows and columns)
+constexpr int G4K = 32;                   // K step
+constexpr int G4S = 4;                    // LDS stages
+constexpr int G4OP = G4T * G4K;           // bf16 per operand and stage (16 KB)
+constexpr size_t kG4Lds = (size_t)G4S * 2 * G4OP * 2;   // 128 KB
+
+// one direct global-to-LDS load: this lane's 16 bytes at byte offset voff of the buffer land at
+// LDS address lds + 16 * lane
+__device__ __forceinline__ void lds_dma16(const Buf &b, uint32_t voff, uint32_t lds) {
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+                 :: "s"(lds), "v"(voff), "s"(b.r) : "memory");
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    asm volatile("s_waitcnt vmcnt(%0)" :: "n"(N) : "memory");
+}
+
+// One operand's loads: wave w issues instructions i = 4w + t (t = 0..3), each filling 1 KB of
+// the stage: K-contiguous: rows 16i .. 16i+15 (4 lanes per 64-byte row); M/N-contiguous: k-rows
+// 2i, 2i+1 (32 lanes per 512-byte k-row).
+template <bool KC>
+struct G4Operand {
+    Buf buf;
+    int64_t ld;         // elements between consecutive rows (KC) or k-rows (M/N contiguous)
+    int64_t r0, rlim;   // tile rows and the operand's row count (M or N)
+    int64_t klim;       // end of this workgroup's K range
+    __device__ __forceinline__ void issue(int64_t k0, uint32_t lds_stage, int wave, int lane) const {
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            const int i = 4 * wave + t;
+            uint32_t off;
+            if (KC) {
+                const int row = 16 * i + (lane >> 2), c = (lane & 3) ^ ((row >> 1) & 3);
+                const int64_t k = k0 + 8 * c;
+                const bool ok = r0 + row < rlim && k < klim;   // klim is a multiple of 8
+                off = ok ? (uint32_t)(((r0 + row) * ld + k) * 2) : kOob;
+            } else {
+                const int kr = 2 * i + (lane >> 5), c = (lane & 31) ^ ((kr & 3) << 1);
+                const int64_t r = r0 + 8 * c;
+                const bool ok = k0 + kr < klim && r < rlim;    // rlim is a multiple of 8
+                off = ok ? (uint32_t)(((k0 + kr) * ld + r) * 2) : kOob;
+            }
+            lds_dma16(buf, off, __builtin_amdgcn_readfirstlane(lds_stage + i * 1024));
+        }
+    }
+    // MFMA operand fragment: rows rb .. rb+31 (lane ln), k = ks*16 + 8hh .. +7 of the stage
+    __device__ __forceinline__ uint4 frag(const char *stage, int rb, int ks, int lane) const {
+        const int ln = lane & 31, hh = lane >> 5;
+        if (KC) {
+            const int row = rb + ln, c = (2 * ks + hh) ^ ((row >> 1) & 3);
+            return *reinterpret_cast<const uint4 *>(stage + row * 64 + c * 16);
+        }
+        const int g = lane >> 4, i = lane & 15;                 // 16-lane group, lane in group
+        const int rr = rb + 16 * (g & 1) + 4 * (i & 3);          // rows of this source lane
+        const int kk = ks * 16 + 8 * (g >> 1) + (i >> 2);        // k-row of this source lane
+        const char *p = stage + kk * 512 + (((rr >> 3) ^ ((kk & 3) << 1)) * 16) + (rr & 7) * 2;
+        const uint2 lo = lds_read_tr(p);
+        const uint2 hi = lds_read_tr(p + 4 * 512);               // k-row kk + 4: same swizzle
+        return make_uint4(lo.x, lo.y, hi.x, hi.y);
+    }
+};
+
+template <bool AK, bool BK, int EPI>
+__global__ __launch_bounds__(256, 1) void k_gemm4(const bf16_t *__restrict__ A, int64_t sa, uint32_t a_bytes,
+                                                  const bf16_t *__restrict__ Bm, int64_t sb, uint32_t b_bytes,
+                                                  void *__restrict__ C, int64_t ldc, const float *__restrict__ bias,
+                                                  int64_t M, int64_t N, int64_t K, int64_t kchunk, int MT, int NT,
+                                                  int Z) {
+    extern __shared__ __align__(16) char g4s[];   // [stage][A tile, B tile]
+    // tile order: the workgroups that share an operand tile run on one XCD back to back
+    const int w = blockIdx.x, xcd = w % kXcds, local = w / kXcds;
+    int mt, nt, z = 0;
+    if (Z > 1) {
+        const int per = MT * NT, r = local % per;
+        z = (local / per) * kXcds + xcd;
+        mt = r / NT;
+        nt = r % NT;
+        if (z >= Z) return;
+    } else if (MT <= NT) {
+        nt = (local / MT) * kXcds + xcd;
+        mt = local % MT;
+        if (nt >= NT) return;
+    } else {
+        mt = (local / NT) * kXcds + xcd;
+        nt = local % NT;
+        if (mt >= MT) return;
+    }
+    const int64_t m0 = (int64_t)mt * G4T, n0 = (int64_t)nt * G4T;
+    const int64_t kb = (int64_t)z * kchunk;
+    const int64_t ke = kb + kchunk < K ? kb + kchunk : K;
+    const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int ln = lane & 31, hh = lane >> 5;
+    const int wm = wave >> 1, wn = wave & 1;
+
+    const G4Operand<AK> oa{Buf(A, a_bytes), sa, m0, M, ke};
+    const G4Operand<BK> ob{Buf(Bm, b_bytes), sb, n0, N, ke};
+    const uint32_t lds0 = (uint32_t)reinterpret_cast<uintptr_t>(g4s);
+    auto stA = [&](int st) { return lds0 + (uint32_t)(st * 2 * G4OP * 2); };
+    auto stB = [&](int st) { return lds0 + (uint32_t)(st * 2 * G4OP * 2 + G4OP * 2); };
+
+    f32x16_t acc[4][4];   // [n block j][m block i]: D^T[n][m]
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc[j][i] = f32x16_t{0};
+
+    const int nsteps = (int)((ke - kb + G4K - 1) / G4K);
+    // steps past the end are loaded out of range into stages that are never read
+#pragma unroll
+    for (int s = 0; s < G4S - 1; ++s) {
+        oa.issue(kb + (int64_t)s * G4K, stA(s), wave, lane);
+        ob.issue(kb + (int64_t)s * G4K, stB(s), wave, lane);
+    }
+    for (int j = 0; j < nsteps; ++j) {
+        wait_vmcnt<8 * (G4S - 2)>();   // this wave's loads of step j have landed
+        __syncthreads();               // everyone's have; stage (j - 1) % 4 is no longer read
+        const int sn = (j + G4S - 1) % G4S;
+        oa.issue(kb + (int64_t)(j + G4S - 1) * G4K, stA(sn), wave, lane);
+        ob.issue(kb + (int64_t)(j + G4S - 1) * G4K, stB(sn), wave, lane);
+        const char *ta = g4s + (j % G4S) * 2 * G4OP * 2, *tb = ta + G4OP * 2;
+#pragma unroll
+        for (int ks = 0; ks < G4K / 16; ++ks) {
+            uint4 av[4], bv[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) av[i] = oa.frag(ta, wm * 128 + i * 32, ks, lane);
+#pragma unroll
+            for (int jn = 0; jn < 4; ++jn) bv[jn] = ob.frag(tb, wn * 128 + jn * 32, ks, lane);
+#pragma unroll
+            for (int jn = 0; jn < 4; ++jn)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) acc[jn][i] = mfma32x32x16(as_bf16x8(bv[jn]), as_bf16x8(av[i]), acc[jn][i]);
+        }
+    }
+    wait_vmcnt<0>();   // no load may still be writing LDS
+    __syncthreads();   // and no wave still reads a stage: the LDS now stages the output
+
+    // Output: one 128-row half of the tile at a time goes through LDS as [128 rows][256 columns]
+    // (16-byte chunk c of row r at c ^ (r % 32): the 32 rows one store-to-LDS instruction touches
+    // fall in distinct banks), then leaves as whole row pieces of 512 B (bf16) or 1 KB (fp32),
+    // 1 KB per store instruction.
+    constexpr int OB = EPI == EPI_BF16_BIAS ? 2 : 4;    // output bytes per element
+    constexpr int RB = G4T * OB;                        // bytes per staged row
+    constexpr int RPI = 1024 / RB;                      // rows per store instruction
+    char *eb = g4s;
+    float *Cf = reinterpret_cast<float *>(C) + (EPI == EPI_F32_PART ? (int64_t)z * M * N : 0);
+    bf16_t *Cb = reinterpret_cast<bf16_t *>(C);
+    const int64_t ldo = EPI == EPI_F32_PART ? N : ldc;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        if (wm == h) {
+            // D^T[n = 8r + 4hh + q][m = ln] per 32x32 block: 4 consecutive columns per lane and r
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int nl = wn * 128 + j * 32 + 8 * r + 4 * hh;
+                    float4 b = make_float4(0.f, 0.f, 0.f, 0.f);
+                    if (EPI == EPI_BF16_BIAS && bias && n0 + nl < N)
+                        b = *reinterpret_cast<const float4 *>(bias + n0 + nl);   // 16-byte aligned
+                    const int byte = nl * OB;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const int ml = i * 32 + ln;
+                        const f32x16_t &d = acc[j][i];
+                        char *p = eb + ml * RB + ((((byte >> 4) ^ (ml & 31)) << 4) | (byte & 15));
+                        const float4 v = make_float4(d[4 * r + 0] + b.x, d[4 * r + 1] + b.y, d[4 * r + 2] + b.z,
+                                                     d[4 * r + 3] + b.w);
+                        if (EPI == EPI_BF16_BIAS)
+                            *reinterpret_cast<uint2 *>(p) = make_uint2(pack_bf16(v.x, v.y), pack_bf16(v.z, v.w));
+                        else
+                            *reinterpret_cast<float4 *>(p) = v;
+                    }
+                }
+        }
+        __syncthreads();
+        // 128 rows, RPI per instruction, spread over the 4 waves; columns past N are not stored
+        // (N is a multiple of 8: a 16-byte chunk is all in or all out)
+        const int rl = lane / (64 / RPI), c = lane % (64 / RPI);
+        const int64_t n = n0 + (int64_t)c * (16 / OB);
+#pragma unroll 4
+        for (int t = wave; t < 128 / RPI; t += 4) {
+            const int row = RPI * t + rl;
+            const int64_t m = m0 + 128 * h + row;
+            const uint4 v = *reinterpret_cast<const uint4 *>(eb + row * RB + ((c ^ (row & 31)) << 4));
+            if (m < M && n < N) {
+                // outputs written once and not read again soon: streaming stores
+                const u32x4_t w = __builtin_bit_cast(u32x4_t, v);
+                if (EPI == EPI_BF16_BIAS)
+                    __builtin_nontemporal_store(w, reinterpret_cast<u32x4_t *>(Cb + m * ldo + n));
+                else if (EPI == EPI_F32)
+                    __builtin_nontemporal_store(w, reinterpret_cast<u32x4_t *>(Cf + m * ldo + n));
+                else
+                    *reinterpret_cast<uint4 *>(Cf + m * ldo + n) = v;
+            }
+        }
+        __syncthreads();
+    }
+}
+
 // fp32 GEMM on the vector ALUs (fp32 heads): 64x64 tiles, 4x4 outputs per thread.
 template <int EPI>
 __global__ __launch_bounds__(256) void k_gemm_f32(const float *__restrict__ A, int64_t sam, int64_t sak,
@@ -310,14 +531,18 @@ __global__ __launch_bounds__(256) void k_gemm_f32(const float *__restrict__ A, i
         }
 }
 
-// split of the H contraction of dX: enough workgroups to cover the chip, never below 256 per chunk
-int64_t head_splits(int64_t B, int64_t F_s, int64_t H, int32_t dtype) {
-    const int64_t tm = dtype == HASTE_DTYPE_BF16 ? TM : 64, tn = dtype == HASTE_DTYPE_BF16 ? TN : 64;
+// split of the H contraction of dX for output tiles of tm x tn: enough workgroups to cover the
+// chip (about `target`), never below 256 head labels per chunk
+int64_t head_splits(int64_t B, int64_t F_s, int64_t H, int64_t tm, int64_t tn, int64_t target) {
     const int64_t tiles = haste::cdiv(B, tm) * haste::cdiv(F_s, tn);
-    int64_t S = haste::cdiv(512, tiles < 1 ? 1 : tiles);
+    int64_t S = haste::cdiv(target, tiles < 1 ? 1 : tiles);
     const int64_t maxS = haste::cdiv(H, 256);
     if (S > maxS) S = maxS;
     return S < 1 ? 1 : S;
+}
+int64_t head_splits_for(int64_t B, int64_t F_s, int64_t H, int32_t dtype, bool big) {
+    if (dtype != HASTE_DTYPE_BF16) return head_splits(B, F_s, H, 64, 64, 512);
+    return big ? head_splits(B, F_s, H, G4T, G4T, 256) : head_splits(B, F_s, H, TM, TN, 512);
 }
 
 // The double-buffered kernel needs 16-byte aligned rows along every operand's contiguous
@@ -325,6 +550,33 @@ int64_t head_splits(int64_t B, int64_t F_s, int64_t H, int32_t dtype) {
 bool gemm2_ok(int64_t B, int64_t F_s, int64_t H) {
     const int64_t lim = ((int64_t)1 << 31) - 1;
     return F_s % 8 == 0 && H % 8 == 0 && B * F_s * 2 < lim && H * F_s * 2 < lim && B * H * 2 < lim;
+}
+
+// the 256x256 kernel loads and stores 16 bytes per lane and reads the bias 4 floats at a time:
+// every pointer 16-byte aligned
+bool gemm4_ok(int64_t B, int64_t F_s, int64_t H, std::initializer_list<const void *> ptrs) {
+    if (!gemm2_ok(B, F_s, H)) return false;
+    for (const void *p : ptrs)
+        if ((reinterpret_cast<uintptr_t>(p) & 15) != 0) return false;
+    return true;
+}
+
+// C[M, N] (+)= A B over K, split into Z chunks of kchunk (a multiple of the K step); sa, sb are
+// the operands' row strides (elements)
+template <bool AK, bool BK, int EPI>
+hipError_t launch_gemm4(hipStream_t s, const bf16_t *A, int64_t sa, int64_t a_elems, const bf16_t *Bm, int64_t sb,
+                        int64_t b_elems, void *C, int64_t ldc, const float *bias, int64_t M, int64_t N, int64_t K,
+                        int64_t kchunk, int Z) {
+    const int MT = (int)haste::cdiv(M, G4T), NT = (int)haste::cdiv(N, G4T);
+    const int64_t grid = Z > 1 ? haste::round_up(Z, kXcds) * MT * NT
+                               : (MT <= NT ? haste::round_up(NT, kXcds) * MT : haste::round_up(MT, kXcds) * NT);
+    auto kern = k_gemm4<AK, BK, EPI>;
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)kG4Lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(256), kG4Lds, s, A, sa, (uint32_t)(a_elems * 2), Bm, sb,
+                       (uint32_t)(b_elems * 2), C, ldc, bias, M, N, K, kchunk, MT, NT, Z);
+    return hipGetLastError();
 }
 
 template <bool AK, bool BK, int EPI>
@@ -345,13 +597,18 @@ hipError_t launch_gemm2(dim3 grid, hipStream_t s, const bf16_t *A, int64_t sam, 
 namespace haste {
 
 size_t head_ws(int64_t B, int64_t F_s, int64_t H, int32_t dtype) {
-    return (size_t)head_splits(B, F_s, H, dtype) * (size_t)B * (size_t)F_s * 4 + 256;
+    // either tile size may run (it also depends on the output's alignment): room for the larger split
+    const int64_t S0 = head_splits_for(B, F_s, H, dtype, false), S1 = head_splits_for(B, F_s, H, dtype, true);
+    return (size_t)(S0 > S1 ? S0 : S1) * (size_t)B * (size_t)F_s * 4 + 256;
 }
 
 hipError_t head_fwd(int64_t B, int64_t F_s, int64_t H, int32_t dtype, const void *X, const void *Wh,
                     const float *bias_h, void *Yh, hipStream_t s) {
     // M = B, N = H, K = F_s;  A(m,k) = X[m*F_s + k];  B(k,n) = Wh[n*F_s + k]
     if (dtype == HASTE_DTYPE_BF16) {
+        if (gemm4_ok(B, F_s, H, {X, Wh, Yh, bias_h}))
+            return launch_gemm4<true, true, EPI_BF16_BIAS>(s, (const bf16_t *)X, F_s, B * F_s, (const bf16_t *)Wh, F_s,
+                                                           H * F_s, Yh, H, bias_h, B, H, F_s, F_s, 1);
         const dim3 grid((unsigned)cdiv(H, TN), (unsigned)cdiv(B, TM), 1);
         if (gemm2_ok(B, F_s, H))
             return launch_gemm2<true, true, EPI_BF16_BIAS>(grid, s, (const bf16_t *)X, F_s, 1, B * F_s,
@@ -372,7 +629,12 @@ hipError_t head_bwd(int64_t B, int64_t F_s, int64_t H, int32_t dtype, const void
     const bool bf = dtype == HASTE_DTYPE_BF16;
     if (dWh) {
         // M = H, N = F_s, K = B;  A(m,k) = dYh[k*H + m];  B(k,n) = X[k*F_s + n]
-        if (bf) {
+        if (bf && gemm4_ok(B, F_s, H, {X, dYh, dWh})) {
+            // A(m, k) = dYh[k][m] (k-rows of H), B(k, n) = X[k][n] (k-rows of F_s)
+            hipError_t e = launch_gemm4<false, false, EPI_F32>(s, (const bf16_t *)dYh, H, B * H, (const bf16_t *)X, F_s,
+                                                               B * F_s, (void *)dWh, F_s, nullptr, H, F_s, B, B, 1);
+            if (e != hipSuccess) return e;
+        } else if (bf) {
             const dim3 grid((unsigned)cdiv(F_s, TN), (unsigned)cdiv(H, TM), 1);
             if (gemm2_ok(B, F_s, H)) {
                 hipError_t e = launch_gemm2<false, false, EPI_F32>(grid, s, (const bf16_t *)dYh, 1, H, B * H,
@@ -395,11 +657,18 @@ hipError_t head_bwd(int64_t B, int64_t F_s, int64_t H, int32_t dtype, const void
     }
     if (dX) {
         // M = B, N = F_s, K = H;  A(m,k) = dYh[m*H + k];  B(k,n) = Wh[k*F_s + n]; split over K
-        const int64_t S = head_splits(B, F_s, H, dtype);
+        float *part = reinterpret_cast<float *>(ws);
+        const bool big = bf && gemm4_ok(B, F_s, H, {dYh, Wh, part});
+        const int64_t S = head_splits_for(B, F_s, H, dtype, big);
         const int64_t kchunk = round_up(cdiv(H, S), 32);
         const int64_t Sx = cdiv(H, kchunk);
-        float *part = reinterpret_cast<float *>(ws);
-        if (bf) {
+        if (big) {
+            // A(m, k) = dYh[m][k] (rows of H), B(k, n) = Wh[k][n] (k-rows of F_s)
+            hipError_t e = launch_gemm4<true, false, EPI_F32_PART>(s, (const bf16_t *)dYh, H, B * H, (const bf16_t *)Wh,
+                                                                   F_s, H * F_s, (void *)part, F_s, nullptr, B, F_s, H,
+                                                                   kchunk, (int)Sx);
+            if (e != hipSuccess) return e;
+        } else if (bf) {
             const dim3 grid((unsigned)cdiv(F_s, TN), (unsigned)cdiv(B, TM), (unsigned)Sx);
             if (gemm2_ok(B, F_s, H)) {
                 hipError_t e = launch_gemm2<true, false, EPI_F32_PART>(grid, s, (const bf16_t *)dYh, H, 1, B * H,

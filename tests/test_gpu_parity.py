@@ -180,7 +180,7 @@ def test_large_sampled(hs, orc, name):
 # dense head alone, ragged shapes
 # ------------------------------------------------------------------------------------------
 HEAD = [(33, 200, 300, BF16), (256, 768, 1024, BF16), (1, 64, 17, BF16), (130, 768, 4100, BF16),
-        (33, 200, 300, F32), (5, 96, 70, F32)]
+        (300, 520, 2056, BF16), (33, 200, 300, F32), (5, 96, 70, F32)]
 
 
 @pytest.mark.parametrize("case", HEAD, ids=[f"B{c[0]}_F{c[1]}_H{c[2]}_{'bf16' if c[3] else 'f32'}" for c in HEAD])
