@@ -388,31 +388,47 @@ __global__ __launch_bounds__(256, 1) void k_gemm4(const bf16_t *__restrict__ A, 
         for (int i = 0; i < 4; ++i) acc[j][i] = f32x16_t{0};
 
     const int nsteps = (int)((ke - kb + G4K - 1) / G4K);
-    // steps past the end are loaded out of range into stages that are never read
+    auto frags = [&](int st, int ks, uint4 (&av)[4], uint4 (&bv)[4]) {
+        const char *ta = g4s + st * 2 * G4OP * 2, *tb = ta + G4OP * 2;
 #pragma unroll
-    for (int s = 0; s < G4S - 1; ++s) {
+        for (int i = 0; i < 4; ++i) av[i] = oa.frag(ta, wm * 128 + i * 32, ks, lane);
+#pragma unroll
+        for (int jn = 0; jn < 4; ++jn) bv[jn] = ob.frag(tb, wn * 128 + jn * 32, ks, lane);
+    };
+    auto products = [&](const uint4 (&av)[4], const uint4 (&bv)[4]) {
+#pragma unroll
+        for (int jn = 0; jn < 4; ++jn)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) acc[jn][i] = mfma32x32x16(as_bf16x8(bv[jn]), as_bf16x8(av[i]), acc[jn][i]);
+    };
+    // Software pipeline over K steps of two 16-deep halves (h0, h1).  Iteration j: read h1 of step
+    // j while h0's products run; wait for step j + 1 and barrier (stage j % 4 is then fully read
+    // into registers by every wave); refill stage j % 4 with step j + 4; read h0 of step j + 1
+    // while h1's products run.  Steps past the end are loaded out of range into stages that are
+    // never read.
+#pragma unroll
+    for (int s = 0; s < G4S; ++s) {
         oa.issue(kb + (int64_t)s * G4K, stA(s), wave, lane);
         ob.issue(kb + (int64_t)s * G4K, stB(s), wave, lane);
     }
+    uint4 a0[4], b0[4], a1[4], b1[4];
+    wait_vmcnt<8 * (G4S - 1)>();   // this wave's loads of step 0 have landed
+    __syncthreads();               // everyone's have
+    frags(0, 0, a0, b0);
     for (int j = 0; j < nsteps; ++j) {
-        wait_vmcnt<8 * (G4S - 2)>();   // this wave's loads of step j have landed
-        __syncthreads();               // everyone's have; stage (j - 1) % 4 is no longer read
-        const int sn = (j + G4S - 1) % G4S;
-        oa.issue(kb + (int64_t)(j + G4S - 1) * G4K, stA(sn), wave, lane);
-        ob.issue(kb + (int64_t)(j + G4S - 1) * G4K, stB(sn), wave, lane);
-        const char *ta = g4s + (j % G4S) * 2 * G4OP * 2, *tb = ta + G4OP * 2;
-#pragma unroll
-        for (int ks = 0; ks < G4K / 16; ++ks) {
-            uint4 av[4], bv[4];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) av[i] = oa.frag(ta, wm * 128 + i * 32, ks, lane);
-#pragma unroll
-            for (int jn = 0; jn < 4; ++jn) bv[jn] = ob.frag(tb, wn * 128 + jn * 32, ks, lane);
-#pragma unroll
-            for (int jn = 0; jn < 4; ++jn)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) acc[jn][i] = mfma32x32x16(as_bf16x8(bv[jn]), as_bf16x8(av[i]), acc[jn][i]);
-        }
+        const int st = j % G4S;
+        frags(st, 1, a1, b1);
+        __builtin_amdgcn_sched_barrier(0);   // the reads go ahead of the products they overlap
+        products(a0, b0);
+        __builtin_amdgcn_sched_barrier(0);
+        wait_vmcnt<8 * (G4S - 2)>();   // this wave's loads of step j + 1 have landed
+        __syncthreads();               // everyone's have; stage j % 4 is read out
+        oa.issue(kb + (int64_t)(j + G4S) * G4K, stA(st), wave, lane);
+        ob.issue(kb + (int64_t)(j + G4S) * G4K, stB(st), wave, lane);
+        frags((j + 1) % G4S, 0, a0, b0);   // past the last step: never used
+        __builtin_amdgcn_sched_barrier(0);
+        products(a1, b1);
+        __builtin_amdgcn_sched_barrier(0);
     }
     wait_vmcnt<0>();   // no load may still be writing LDS
     __syncthreads();   // and no wave still reads a stage: the LDS now stages the output
@@ -460,20 +476,29 @@ __global__ __launch_bounds__(256, 1) void k_gemm4(const bf16_t *__restrict__ A, 
         // (N is a multiple of 8: a 16-byte chunk is all in or all out)
         const int rl = lane / (64 / RPI), c = lane % (64 / RPI);
         const int64_t n = n0 + (int64_t)c * (16 / OB);
-#pragma unroll 4
-        for (int t = wave; t < 128 / RPI; t += 4) {
-            const int row = RPI * t + rl;
-            const int64_t m = m0 + 128 * h + row;
-            const uint4 v = *reinterpret_cast<const uint4 *>(eb + row * RB + ((c ^ (row & 31)) << 4));
-            if (m < M && n < N) {
-                // outputs written once and not read again soon: streaming stores
-                const u32x4_t w = __builtin_bit_cast(u32x4_t, v);
-                if (EPI == EPI_BF16_BIAS)
-                    __builtin_nontemporal_store(w, reinterpret_cast<u32x4_t *>(Cb + m * ldo + n));
-                else if (EPI == EPI_F32)
-                    __builtin_nontemporal_store(w, reinterpret_cast<u32x4_t *>(Cf + m * ldo + n));
-                else
-                    *reinterpret_cast<uint4 *>(Cf + m * ldo + n) = v;
+        constexpr int NI = 128 / RPI / 4;                   // store instructions per wave
+        constexpr int NB = 8;                               // issued in batches: reads, then stores
+#pragma unroll
+        for (int t0 = 0; t0 < NI; t0 += NB) {
+            uint4 v[NB];
+#pragma unroll
+            for (int t = 0; t < NB; ++t) {
+                const int row = RPI * (4 * (t0 + t) + wave) + rl;
+                v[t] = *reinterpret_cast<const uint4 *>(eb + row * RB + ((c ^ (row & 31)) << 4));
+            }
+#pragma unroll
+            for (int t = 0; t < NB; ++t) {
+                const int64_t m = m0 + 128 * h + RPI * (4 * (t0 + t) + wave) + rl;
+                if (m < M && n < N) {
+                    // outputs written once and not read again soon: streaming stores
+                    const u32x4_t w = __builtin_bit_cast(u32x4_t, v[t]);
+                    if (EPI == EPI_BF16_BIAS)
+                        __builtin_nontemporal_store(w, reinterpret_cast<u32x4_t *>(Cb + m * ldo + n));
+                    else if (EPI == EPI_F32)
+                        __builtin_nontemporal_store(w, reinterpret_cast<u32x4_t *>(Cf + m * ldo + n));
+                    else
+                        *reinterpret_cast<uint4 *>(Cf + m * ldo + n) = v[t];
+                }
             }
         }
         __syncthreads();

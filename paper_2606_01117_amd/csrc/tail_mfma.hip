@@ -516,6 +516,169 @@ __global__ __launch_bounds__(kBwUnits * 64) void k_bwd_w(const bf16_t *__restric
 }
 
 // --------------------------------------------------------------------------------------------
+// Backward-weight, slab-staged.  A workgroup of 8 waves takes 16 consecutive units (a contiguous
+// span of at most 512 labels, two units per wave) and sweeps the batch in 32-row slabs.  Per slab
+// it stages in LDS, cooperatively and with whole-line loads, the X^T block of all F_s features
+// (contiguous in Xb, 64 bytes per feature) and the span's dY rows (up to 1 KB per row); each wave
+// then gathers its units' support rows from the staged block, one 16-byte LDS read per slot tile,
+// instead of from memory.  The next slab is loaded into registers while the current one is
+// multiplied.
+// Per unit and slab (v_mfma_f32_16x16x32_bf16, M = 16 slots, N = 16 labels, K = the 32 rows):
+//   A operand (slots x rows) = X^T rows of the slot's feature, rows 8q .. 8q+7 of slot l16;
+//   B operand (rows x labels) = dY, two ds_read_b64_tr_b16 (4 rows each) per 16-label tile;
+//   result lane (label l16, q) holds slots 4q .. 4q+3 of one label: a 16-byte store into dW.
+// dbias comes from the same B operands against an all-ones A operand.
+// --------------------------------------------------------------------------------------------
+constexpr int kBw2Waves = 8;
+constexpr int kBw2Units = 2 * kBw2Waves;        // units per workgroup (two per wave)
+constexpr int kBw2XRow = 80;                    // bytes per staged X^T feature row: 32 rows + 8 pad
+constexpr int kBw2YRow = 1056;                  // bytes per staged dY row: 512 labels + 16 pad
+constexpr int kBw2MaxXLoads = kMaxFs * 4 / (kBw2Waves * 64);   // 16-byte X^T loads per thread and slab
+
+static size_t bw2_lds(int F_s) { return (size_t)haste::round_up((int64_t)F_s * kBw2XRow, 16) + 32 * kBw2YRow; }
+
+template <int F_IN>
+__global__ __launch_bounds__(512) void k_bwd_w2(const bf16_t *__restrict__ Xb, const int32_t *__restrict__ idx,
+                                                const bf16_t *__restrict__ dY, float *__restrict__ dW,
+                                                float *__restrict__ dbias, int beta, int B, int Bp, int F_s,
+                                                int64_t L, int G, int64_t K) {
+    extern __shared__ __align__(16) char bw2s[];
+    constexpr int NST = F_IN / 16;              // 16-slot M-tiles
+    char *xs = bw2s;
+    char *ys = bw2s + ((F_s * kBw2XRow + 15) & ~15);
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int l16 = lane & 15, q = lane >> 4;
+    const int ntn = (G + 31) >> 5;
+    const int64_t nunits = K * ntn;
+    const int64_t u0 = (int64_t)blockIdx.x * kBw2Units;
+    auto lab_of = [&](int64_t v) {
+        const int64_t k = v / ntn;
+        return k * G + 32 * (int)(v - k * ntn);
+    };
+    auto nlab_of = [&](int64_t v) {
+        const int t = (int)(v % ntn);
+        return G - 32 * t < 32 ? G - 32 * t : 32;
+    };
+    const int64_t ul = u0 + kBw2Units - 1 < nunits ? u0 + kBw2Units - 1 : nunits - 1;
+    const int64_t lab0 = lab_of(u0);
+    const int span = (int)(lab_of(ul) + nlab_of(ul) - lab0);   // at most 512 labels
+
+    // this wave's units (a unit past the end repeats the last one and is never stored)
+    int64_t vu[2];
+    int off[2], nl[2];
+    int f[2][NST];
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+        const int64_t v = u0 + 2 * wave + j;
+        vu[j] = v < nunits ? v : nunits - 1;
+        off[j] = (int)(lab_of(vu[j]) - lab0);
+        nl[j] = v < nunits ? nlab_of(vu[j]) : 0;
+        const int64_t k = vu[j] / ntn;
+#pragma unroll
+        for (int st = 0; st < NST; ++st) f[j][st] = idx[k * F_IN + 16 * st + l16];
+    }
+
+    // cooperative slab loads: X^T block (4 F_s chunks of 16 bytes) and dY (32 rows x 64 chunks)
+    const int nxc = 4 * F_s;
+    uint4 xr[kBw2MaxXLoads], yr[4];
+    auto load = [&](int blk) {
+        const Buf xb(Xb + (int64_t)blk * F_s * 32, (uint32_t)(nxc * 16));
+#pragma unroll
+        for (int i = 0; i < kBw2MaxXLoads; ++i) xr[i] = xb.ld16((uint32_t)(tid + 512 * i) * 16);   // past the block: zero
+        // rows past B and labels past the span read as zero
+        const int b0 = blk * 32;
+        const int rows = B - b0 < 32 ? B - b0 : 32;
+        const Buf db(dY + (int64_t)b0 * L + lab0, (uint32_t)(rows > 0 ? ((int64_t)(rows - 1) * L + span) * 2 : 0));
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int c = tid + 512 * i, row = c >> 6, part = c & 63;
+            const bool ok = row < rows && 8 * part < span;
+            yr[i] = db.ld16(ok ? (uint32_t)(((int64_t)row * L + 8 * part) * 2) : kOob);
+        }
+    };
+    auto store = [&]() {
+#pragma unroll
+        for (int i = 0; i < kBw2MaxXLoads; ++i) {
+            const int c = tid + 512 * i;
+            if (c < nxc) *reinterpret_cast<uint4 *>(xs + (c >> 2) * kBw2XRow + (c & 3) * 16) = xr[i];
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int c = tid + 512 * i;
+            *reinterpret_cast<uint4 *>(ys + (c >> 6) * kBw2YRow + (c & 63) * 16) = yr[i];
+        }
+    };
+
+    f32x4_t acc[2][NST][2], db[2][2];
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+#pragma unroll
+        for (int lt = 0; lt < 2; ++lt) {
+            db[j][lt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int st = 0; st < NST; ++st) acc[j][st][lt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        }
+    }
+    const bf16x8_t ones = as_bf16x8(make_uint4(0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u));
+    // B-operand source lanes: 16-lane group q reads rows 8q + 4h + (l16 >> 2), labels 4 (l16 & 3) ..
+    const char *ysrc = ys + (8 * q + (l16 >> 2)) * kBw2YRow + (l16 & 3) * 8;
+
+    const int nblk = Bp / 32;
+    load(0);
+    for (int blk = 0; blk < nblk; ++blk) {
+        __syncthreads();   // the previous slab is no longer read
+        store();
+        __syncthreads();
+        if (blk + 1 < nblk) load(blk + 1);
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            uint4 yv[2];
+#pragma unroll
+            for (int lt = 0; lt < 2; ++lt) {
+                const char *p = ysrc + (off[j] + 16 * lt) * 2;
+                const uint2 lo = lds_read_tr(p);
+                const uint2 hi = lds_read_tr(p + 4 * kBw2YRow);
+                yv[lt] = make_uint4(lo.x, lo.y, hi.x, hi.y);
+            }
+#pragma unroll
+            for (int st = 0; st < NST; ++st) {
+                const uint4 xv = *reinterpret_cast<const uint4 *>(xs + f[j][st] * kBw2XRow + q * 16);
+#pragma unroll
+                for (int lt = 0; lt < 2; ++lt)
+                    acc[j][st][lt] = mfma16x16x32(as_bf16x8(xv), as_bf16x8(yv[lt]), acc[j][st][lt]);
+            }
+            if (dbias) {
+#pragma unroll
+                for (int lt = 0; lt < 2; ++lt) db[j][lt] = mfma16x16x32(ones, as_bf16x8(yv[lt]), db[j][lt]);
+            }
+        }
+    }
+
+    // dW[label][16 st + 4q .. +3] for label 16 lt + l16 of each unit; dbias from the q = 0 lanes
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+        const int64_t lb = lab_of(vu[j]);
+#pragma unroll
+        for (int lt = 0; lt < 2; ++lt) {
+            const int t = 16 * lt + l16;
+            if (t >= nl[j]) continue;
+            float *row = dW + (lb + t) * F_IN + 4 * q;
+#pragma unroll
+            for (int st = 0; st < NST; ++st) {
+                float4 v = make_float4(acc[j][st][lt][0], acc[j][st][lt][1], acc[j][st][lt][2], acc[j][st][lt][3]);
+                if (beta) {
+                    const float4 o = *reinterpret_cast<const float4 *>(row + 16 * st);
+                    v.x += o.x; v.y += o.y; v.z += o.z; v.w += o.w;
+                }
+                *reinterpret_cast<float4 *>(row + 16 * st) = v;
+            }
+            if (dbias && q == 0) dbias[lb + t] = (beta ? dbias[lb + t] : 0.0f) + db[j][lt][0];
+        }
+    }
+}
+
+// --------------------------------------------------------------------------------------------
 // Backward-feature (split over label segments).
 //
 // The contraction runs over the labels of a group, which are strided in W's natural layout
@@ -920,6 +1083,23 @@ hipError_t bwd_w_mfma(const TailArgs &a, const void *X, const int32_t *idx, cons
     if (e != hipSuccess) return e;
     const int64_t K = a.L / a.G;
     const int64_t units = K * cdiv(a.G, 32);
+    {
+        const size_t lds = bw2_lds((int)a.F_s);
+        const dim3 grid2((unsigned)cdiv(units, kBw2Units));
+        auto launch2 = [&](auto kern) {
+            hipError_t e2 = allow_lds(kern, lds);
+            if (e2 != hipSuccess) return e2;
+            hipLaunchKernelGGL(kern, grid2, dim3(kBw2Waves * 64), lds, s, Xb, idx, (const bf16_t *)dY, dW, dbias, beta,
+                               (int)a.B, Bp, (int)a.F_s, a.L, (int)a.G, K);
+            return hipGetLastError();
+        };
+        switch (a.F_in) {
+            case 32: return launch2(k_bwd_w2<32>);
+            case 64: return launch2(k_bwd_w2<64>);
+            case 128: return launch2(k_bwd_w2<128>);
+            default: break;
+        }
+    }
     const dim3 grid((unsigned)cdiv(units, kBwUnits));
     const dim3 block(kBwUnits * 64);
     switch (a.F_in) {
