@@ -32,8 +32,11 @@ CALL_KERNELS = {
     "fwd": ["k_fwd"],
     "bwd_w": ["k_transpose_x", "k_bwd_w"],
     "bwd_x": ["k_transpose_w", "k_bwd_x", "k_reduce_fmajor"],
-    "head_fwd": ["k_gemm_bf16"],
-    "head_bwd": ["k_gemm_bf16", "k_reduce_rmajor"],
+    # the head's GEMM kernels by operand layout and epilogue (three tile sizes: 256, 128, fallback)
+    "head_fwd": ["k_gemm4<true, true, 0>", "k_gemm2<true, true, 0>", "k_gemm_bf16<true, true, 0>"],
+    "head_bwd": ["k_gemm4<false, false, 1>", "k_gemm4<true, false, 2>", "k_gemm2<false, false, 1>",
+                 "k_gemm2<true, false, 2>", "k_gemm_bf16<false, false, 1>", "k_gemm_bf16<true, false, 2>",
+                 "k_reduce_rmajor"],
 }
 
 
