@@ -754,10 +754,10 @@ struct BwdXGroup {
     int f[F_IN / 16];         // accumulator rows idx[k, 16st + l16]
 };
 
-constexpr int kBxAS = 36;         // accumulator row stride (floats): 32 rows + 4 pad
-constexpr int kBxRowBytes = 512;  // staged dY per row and chunk (256 labels)
-constexpr int kBxConsumers = 2;   // consumer waves (one per 16-row half)
-constexpr int kBxProducers = 2;   // producer waves
+constexpr int kBxAS = 36;          // accumulator row stride (floats): 32 rows + 4 pad
+constexpr int kBxConsumers = 2;    // consumer waves (one per 16-row half)
+constexpr int kBxProducers = 2;    // producer waves
+constexpr int kBxChunkBytes = 20480;   // staged dY per chunk buffer, at most
 
 // groups of weights in flight per consumer wave: registers, and at most 63 outstanding loads
 template <int F_IN, int NLB>
@@ -766,23 +766,29 @@ constexpr int bx_depth() {
     return per <= 20 ? 6 : (per <= 40 ? 4 : 2);  // even: products alternate between two buffers
 }
 
-// Staged dY layout: [2 buffers][32 rows][64 units of 8 bytes]; unit u of row r sits at
-// position u ^ 2(r % 16), so that the 16 rows read by one MFMA operand load fall in distinct
-// banks while each producer store still writes one whole row.
-__device__ __forceinline__ int bx_swz(int u, int r) { return (u & 63) ^ (2 * (r & 15)); }
+// Staged dY layout, per chunk buffer: [CH groups][32 rows][32 NLB + 8 labels] bf16.  A consumer's
+// operand for one group is then one 16-byte read per 32-label block at a lane-constant offset
+// from the group's base; the 8 spare labels per row put the 16 rows one read touches in distinct
+// banks.  Labels G .. 32 NLB - 1 of every row stay zero (written once, never staged), and the
+// producers stage zeros for groups past the segment, so the consumers need no masking.  A
+// separate all-zero group serves the steps the consumers pad their loop with.
+__host__ __device__ constexpr int bx_row_bytes(int nlb) { return (32 * nlb + 8) * 2; }
 
 template <int F_IN, int NLB>
-__global__ __launch_bounds__(256) void k_bwd_x(const int32_t *__restrict__ idx, const bf16_t *__restrict__ WT,
-                                               const bf16_t *__restrict__ dY, float *__restrict__ part, int B,
-                                               int Bp, int F_s, int64_t L, int G, int Gp, int64_t K, int nbt,
-                                               int64_t gps, int CH) {
+__global__ __launch_bounds__((kBxConsumers + kBxProducers) * 64) void k_bwd_x(
+    const int32_t *__restrict__ idx, const bf16_t *__restrict__ WT, const bf16_t *__restrict__ dY,
+    float *__restrict__ part, int B, int Bp, int F_s, int64_t L, int G, int Gp, int64_t K, int nbt, int64_t gps,
+    int CH) {
     extern __shared__ __align__(16) float accs[];  // [F_s][kBxAS], then the staged dY
     constexpr int AS = kBxAS;
     constexpr int NST = F_IN / 16;                 // 16-slot tiles
     constexpr int NP = kBxProducers;
     constexpr int NJ = 32 / NP;                    // rows per producer wave and chunk
     constexpr int NB = bx_depth<F_IN, NLB>();
-    char *ys = reinterpret_cast<char *>(accs + F_s * AS);
+    constexpr int RB = bx_row_bytes(NLB);          // staged bytes per row and group
+    constexpr int GB = 32 * RB;                    // staged bytes per group
+    char *ys = reinterpret_cast<char *>(accs + F_s * AS);   // [2][CH][32][RB], then one zero group
+    const int cbytes = CH * GB;
     const int w = blockIdx.x;
     const int xcd = w % kXcds;
     const int jj = w / kXcds;
@@ -802,33 +808,46 @@ __global__ __launch_bounds__(256) void k_bwd_x(const int32_t *__restrict__ idx, 
         for (int e = tid; e < F_s * 32; e += nthr) pp[(size_t)(e >> 5) * Bp + (e & 31)] = 0.0f;
         return;
     }
-    for (int e = tid; e < F_s * AS; e += nthr) accs[e] = 0.0f;
+    // accumulator and the whole staging area (its zero label padding is never written again)
+    {
+        uint32_t *z = reinterpret_cast<uint32_t *>(accs);
+        const int nz = F_s * AS + (2 * cbytes + GB) / 4;
+        for (int e = tid; e < nz; e += nthr) z[e] = 0u;
+    }
+    __syncthreads();
     const int n = (int)(g_end - g_begin);          // groups of this segment
     const int nch = (n + CH - 1) / CH;             // dY chunks
 
     if (wave >= kBxConsumers) {
         // ---- producers: dY chunk c (groups cCH .. of the segment) -> staging buffer c % 2 ----
+        // Lane i loads labels 4i .. 4i+3 of the chunk (8 bytes) of one row per instruction; they
+        // belong to group 4i / G of the chunk.  Labels past the segment read as zero.
         const int p = wave - kBxConsumers;
         const int rows = B - b0 < 32 ? B - b0 : 32;
-        const uint32_t u8 = (uint32_t)lane * 8;
-        const bool lane_ok = (int)u8 < CH * G * 2;
+        const int lab4 = 4 * lane;
+        const int gi = lab4 / G, wl = lab4 - gi * G;
+        const uint32_t soff = (uint32_t)(gi * GB + wl * 2);   // within the chunk buffer, row 0
         uint2 v[NJ];
         auto load = [&](int c) {
-            // rows past B and bytes past the end of dY read as zero
             const int64_t lab0 = (g_begin + (int64_t)c * CH) * G;
+            const int nlab = (n - c * CH < CH ? n - c * CH : CH) * G;   // this chunk's labels
             const Buf db(dY + (int64_t)b0 * L + lab0, (uint32_t)(((int64_t)rows * L - lab0) * 2));
+            const bool ok = lab4 < nlab;
 #pragma unroll
             for (int i = 0; i < NJ; ++i) {
                 const int r = p + NP * i;
-                v[i] = db.ld8(lane_ok ? (uint32_t)((int64_t)r * L * 2) + u8 : kOob);
+                v[i] = db.ld8(ok ? (uint32_t)((int64_t)r * L * 2) + 8 * lane : kOob);
             }
         };
+        const bool lane_st = lab4 < CH * G;   // lanes past the chunk store nothing
         auto store = [&](int c) {
-            char *yb = ys + (c & 1) * 32 * kBxRowBytes;
+            char *yb = ys + (c & 1) * cbytes + soff;
+            if (lane_st) {
 #pragma unroll
-            for (int i = 0; i < NJ; ++i) {
-                const int r = p + NP * i;
-                *reinterpret_cast<uint2 *>(yb + r * kBxRowBytes + bx_swz(lane, r) * 8) = v[i];
+                for (int i = 0; i < NJ; ++i) {
+                    const int r = p + NP * i;
+                    *reinterpret_cast<uint2 *>(yb + r * RB) = v[i];
+                }
             }
         };
         load(0);
@@ -883,37 +902,25 @@ __global__ __launch_bounds__(256) void k_bwd_x(const int32_t *__restrict__ idx, 
             }
         };
 
-        const int r = 16 * bh + l16;               // tile row of this lane's dY operand
-        char *accb = reinterpret_cast<char *>(accs) + (16 * bh + 4 * q) * 4;  // this lane's accumulator column
-        bool lab_ok[NLB][2];                       // label quads of this lane within the group
-#pragma unroll
-        for (int c = 0; c < NLB; ++c) {
-            lab_ok[c][0] = 32 * c + 8 * q < G;
-            lab_ok[c][1] = 32 * c + 8 * q + 4 < G;
-        }
+        // this lane's dY operand: row 16 bh + l16 of a group, labels 32c + 8q .. +7
+        const int ylane = (16 * bh + l16) * RB + 16 * q;
+        // this lane's accumulator column: rows 16 bh + 4q .. +3 of an accumulator row
+        char *accb = reinterpret_cast<char *>(accs) + (16 * bh + 4 * q) * 4;
 
-        // dY operand of the next group: labels 32c + 8q .. +7 of this lane's row.  Groups are
-        // read in order, so their place in the staged chunks is tracked as they go; the first
-        // group of a chunk waits for the chunk's barrier.  Label quads past G (the next group's
-        // labels) and groups past the end (repeats of the last group) read as zero, so the latter
-        // add nothing.
-        int cbuf = 0, cgl = 0;
+        // Groups are read in order, so their place in the staged chunks is a wave-uniform cursor
+        // (chunk buffer, group in chunk); the first group of a chunk waits for the chunk's
+        // barrier.  Steps past the last group read the zero group and add nothing.
+        int cg = 0;        // group within the chunk of the next group to read
+        int cbuf = 0;      // byte offset of the chunk buffer holding it
         auto read_dy = [&](uint4 (&ay)[NLB], bool live) {
-            if (cgl == 0 && live) __syncthreads();  // a new chunk is staged
-            const char *yrow = ys + cbuf * 32 * kBxRowBytes + r * kBxRowBytes;
+            if (cg == 0 && live) __syncthreads();  // a new chunk is staged
+            const int gb = live ? cbuf + cg * GB : 2 * cbytes;   // the zero group follows both buffers
+            const char *yp = ys + gb + ylane;
 #pragma unroll
-            for (int c = 0; c < NLB; ++c) {
-                const int c8 = 32 * c + 8 * q;
-                uint2 a0 = *reinterpret_cast<const uint2 *>(yrow + bx_swz((cgl + c8) >> 2, r) * 8);
-                uint2 a1 = *reinterpret_cast<const uint2 *>(yrow + bx_swz((cgl + c8 + 4) >> 2, r) * 8);
-                if (!(live && lab_ok[c][0])) a0 = make_uint2(0u, 0u);
-                if (!(live && lab_ok[c][1])) a1 = make_uint2(0u, 0u);
-                ay[c] = make_uint4(a0.x, a0.y, a1.x, a1.y);
-            }
-            cgl += G;
-            if (cgl == CH * G) {
-                cgl = 0;
-                cbuf ^= 1;
+            for (int c = 0; c < NLB; ++c) ay[c] = *reinterpret_cast<const uint4 *>(yp + 64 * c);
+            if (++cg == CH) {
+                cg = 0;
+                cbuf = cbytes - cbuf;
             }
         };
 
@@ -938,11 +945,11 @@ __global__ __launch_bounds__(256) void k_bwd_x(const int32_t *__restrict__ idx, 
             for (int b = 0; b < NB; ++b) {
                 const int sg = s0 + b;
                 f32x4_t acc[NST];
-                uint32_t ao[NST];
+                char *ap[NST];
 #pragma unroll
                 for (int st = 0; st < NST; ++st) {
-                    ao[st] = __umul24((uint32_t)tl[b].f[st], AS * 4);
-                    acc[st] = *reinterpret_cast<const f32x4_t *>(accb + ao[st]);
+                    ap[st] = accb + __umul24((uint32_t)tl[b].f[st], AS * 4);
+                    acc[st] = *reinterpret_cast<const f32x4_t *>(ap[st]);
                 }
                 __builtin_amdgcn_sched_barrier(0);  // accumulator reads first
                 issue(cl(sg + NB - 1), tl[(b + NB - 1) % NB]);
@@ -953,7 +960,7 @@ __global__ __launch_bounds__(256) void k_bwd_x(const int32_t *__restrict__ idx, 
 #pragma unroll
                     for (int c = 0; c < NLB; ++c)
                         acc[st] = mfma16x16x32(as_bf16x8(ay[b & 1][c]), as_bf16x8(tl[b].w[c][st]), acc[st]);
-                    *reinterpret_cast<f32x4_t *>(accb + ao[st]) = acc[st];
+                    *reinterpret_cast<f32x4_t *>(ap[st]) = acc[st];
                 }
             }
         }
@@ -988,8 +995,10 @@ BwdXGeom bwd_x_geom(const haste::TailArgs &a) {
     g.nbt = (int)haste::cdiv(a.B, 32);
     const int nt = (int)(a.F_in / 16) * 2;
     g.nwaves = kBxConsumers + kBxProducers;
-    g.ch = (int)((kBxRowBytes / 2) / a.G);  // groups per staged dY chunk
-    g.lds = (size_t)a.F_s * kBxAS * 4 + 2 * 32 * kBxRowBytes;
+    // groups per staged dY chunk: at most 256 labels (one 512-byte load per row) and kBxChunkBytes
+    const int nlb = (int)((a.G + 31) / 32), gb = 32 * bx_row_bytes(nlb);
+    g.ch = (int)(256 / a.G) < kBxChunkBytes / gb ? (int)(256 / a.G) : kBxChunkBytes / gb;
+    g.lds = (size_t)a.F_s * kBxAS * 4 + (size_t)(2 * g.ch + 1) * gb;
     const int64_t K = a.L / a.G;
     int64_t spx = kCusPerXcd / g.nbt;  // one workgroup per CU: the accumulator takes most of the LDS
     if (spx < 1) spx = 1;
