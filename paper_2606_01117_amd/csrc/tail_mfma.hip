@@ -682,12 +682,12 @@ __global__ __launch_bounds__(512) void k_bwd_w2(const bf16_t *__restrict__ Xb, c
 // Backward-feature (split over label segments).
 //
 // The contraction runs over the labels of a group, which are strided in W's natural layout
-// (one row of F_in slots per label), so k_transpose_w first writes every group's block as
-// W_k^T [F_in][Gp] (Gp = G rounded up to 8, zero padded) into the workspace: one pass over W
-// instead of one transpose per group and batch tile.
+// (one row of F_in slots per label), so k_transpose_w first writes every group's block
+// transposed, in the order the matrix-core operand loads read it, into the workspace: one pass
+// over W instead of one transpose per group and batch tile.
 //
 // A workgroup owns a 32-row batch tile and one contiguous segment of groups; its partial
-// dX^T[F_s][32] (fp32, rows padded to 36 floats) lives in LDS.  Two consumer waves each own one
+// dX^T[F_s][32] (fp32, rows padded to 40 floats) lives in LDS.  Two consumer waves each own one
 // 16-row half of the tile for every group and every support slot, so no two waves ever touch
 // the same accumulator cell: each wave adds its products with plain read-add-write in its own
 // program order (LDS operations of one wave are executed in order), with no barrier between
@@ -699,52 +699,128 @@ __global__ __launch_bounds__(512) void k_bwd_w2(const bf16_t *__restrict__ Xb, c
 // MFMA operand layout instead would touch 16 rows (16 pages megabytes apart) per instruction,
 // and such loads are limited by address translation rather than by HBM.  One barrier per chunk
 // hands a staged chunk to the consumers and the previous buffer back to the producers, which
-// keep the next chunk in flight meanwhile.
+// keep the next chunks in flight meanwhile.
 //
 // Per group and 16-slot tile (v_mfma_f32_16x16x32_bf16, M = rows, N = slots, K = labels):
-//   A operand (rows x labels) = staged dY, labels 32c + 8q .. +7 of row l16 (two 8-byte LDS
-//     reads per 32-label block, shared by all slot tiles);
-//   B operand (labels x slots) = W_k^T row of slot l16, the same 8 labels (one 16-byte load);
+//   A operand (rows x labels) = staged dY, labels 32c + 8q .. +7 of row l16 (one 16-byte LDS
+//     read per 32-label block, shared by all slot tiles);
+//   B operand (labels x slots) = the same 8 labels of slot l16 (one 16-byte load);
 //   result lane (slot, q) holds rows 4q..4q+3 of one slot: one float4 read-add-write into the
 //     accumulator row idx[k, slot].
 // --------------------------------------------------------------------------------------------
 
-// W [K][G][F_in] -> WT [K][F_in][Gp], labels G .. Gp-1 zero; and idx [K][F_in] -> idxl [K][16][F_in/16]
-// (the supports of slots l16, 16 + l16, ... side by side, one vector load per lane).  One group per
-// workgroup step.
-__global__ __launch_bounds__(256) void k_transpose_w(const bf16_t *__restrict__ W, const int32_t *__restrict__ idx,
-                                                     bf16_t *__restrict__ WT, int32_t *__restrict__ idxl, int64_t K,
-                                                     int G, int Gp, int F_in) {
-    extern __shared__ __align__(16) bf16_t tw[];  // [F_in][Gp + 4]
+// W [K][G][F_in] -> WT [K][Gp / 8][F_in][8] and idx [K][F_in] -> idxl [K][F_in], both in lane
+// order: position p = 16 st + l16 is the slot that lane l16 of 16-slot tile st handles.  WT holds
+// label octet o of position p at (o F_in + p) 8 (labels G .. Gp - 1 zero, Gp = G rounded up to
+// 8), so a consumer's operand load (16 positions x one octet per 16 lanes) reads contiguous
+// 256-byte runs; idxl keeps the supports of lanes l16, 16 + l16, ... side by side (one vector load
+// per lane).
+//
+// Slot order.  The consumers read the accumulator rows of a group's first F_in / 2 positions (the
+// early half) before the previous group of the segment has written its rows back, so the early
+// half must hold no row of the previous group's support; the rows the two share go to the late
+// half, which is read after the write-back.  Within that constraint slots are ordered by (shared,
+// occurrence of the residue so far, row mod 8): each run of 8 positions (the lanes that one
+// accumulator access serves together) then holds distinct residues mod 8 where the support
+// allows, and with 40-float accumulator rows such a run touches every LDS bank once.  over[k] is
+// set when group k shares more than F_in / 2 rows with group k - 1, more than the late half
+// holds; segments containing such a group are processed without the overlap.
+// One group per wave step (the four waves of a workgroup work independently, each in its own LDS
+// region: the support of the previous group, the positions, and the transposed block).
+constexpr int kTwWaves = 4;
+
+__host__ __device__ constexpr int tw_wave_bytes(int f_in, int gp) {
+    return ((2 * f_in * 4 + f_in * (gp + 4) * 2) + 15) / 16 * 16;
+}
+
+__global__ __launch_bounds__(kTwWaves * 64) void k_transpose_w(const bf16_t *__restrict__ W, const int32_t *__restrict__ idx,
+                                                              bf16_t *__restrict__ WT, int32_t *__restrict__ idxl,
+                                                              uint8_t *__restrict__ over, int64_t K, int G, int Gp,
+                                                              int F_in, int64_t gps) {
+    extern __shared__ __align__(16) char twsh[];
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    char *mine = twsh + wv * tw_wave_bytes(F_in, Gp);
+    int *sprev = reinterpret_cast<int *>(mine);               // [F_in] previous support (or -1)
+    int *spos = sprev + F_in;                                 // [F_in] lane-order position of each slot
+    bf16_t *tw = reinterpret_cast<bf16_t *>(spos + F_in);     // [F_in][Gp + 4], rows by position
     const int TS = Gp + 4;
-    const int tid = threadIdx.x;
     const int nq = F_in / 4;                      // slot quads per label
     const int nst = F_in / 16;
-    for (int64_t k = blockIdx.x; k < K; k += gridDim.x) {
-        if (threadIdx.x < F_in) {
-            const int t = threadIdx.x;   // slot 16 st + l16 -> position l16 * nst + st
-            idxl[k * F_in + (t & 15) * nst + (t >> 4)] = idx[k * F_in + t];
+    const uint64_t lt = __lanemask_lt();
+    for (int64_t k = (int64_t)blockIdx.x * kTwWaves + wv; k < K; k += (int64_t)gridDim.x * kTwWaves) {
+        const bool has_prev = k % gps != 0;       // the first group of a segment has none
+        // slots t = lane and t = lane + 64 (F_in = 128)
+        int f[2], cls[2], occ[2] = {0, 0};
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const int t = lane + 64 * i;
+            f[i] = t < F_in ? idx[k * F_in + t] : -1;
+            if (t < F_in) sprev[t] = has_prev ? idx[(k - 1) * F_in + t] : -1;
         }
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            cls[i] = -1;                          // 8 shared + (row mod 8)
+            if (f[i] >= 0) {
+                int lo = 0, hi = F_in;            // first position of the ascending previous support >= f
+                while (lo < hi) {
+                    const int mid = (lo + hi) >> 1;
+                    if (sprev[mid] < f[i]) lo = mid + 1;
+                    else hi = mid;
+                }
+                cls[i] = (lo < F_in && sprev[lo] == f[i] ? 8 : 0) + (f[i] & 7);
+            }
+        }
+        int cnt[16];
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            const uint64_t m0 = __ballot(cls[0] == v), m1 = __ballot(cls[1] == v);
+            if (cls[0] == v) occ[0] = __popcll(m0 & lt);
+            if (cls[1] == v) occ[1] = __popcll(m0) + __popcll(m1 & lt);
+            cnt[v] = __popcll(m0) + __popcll(m1);
+        }
+        int n0 = 0;                               // slots not shared with the previous group
+#pragma unroll
+        for (int v = 0; v < 8; ++v) n0 += cnt[v];
+        if (lane == 0) over[k] = (uint8_t)(n0 < F_in / 2 ? 1 : 0);
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            if (cls[i] < 0) continue;
+            const int r = cls[i] & 7, o = occ[i];
+            int rk0 = 0, rk1 = n0;                // the rank if unshared / if shared (static counts)
+#pragma unroll
+            for (int v = 0; v < 8; ++v) {
+                rk0 += (cnt[v] < o ? cnt[v] : o) + (v < r && cnt[v] > o ? 1 : 0);
+                rk1 += (cnt[8 + v] < o ? cnt[8 + v] : o) + (v < r && cnt[8 + v] > o ? 1 : 0);
+            }
+            const int rank = (cls[i] & 8) ? rk1 : rk0;
+            spos[lane + 64 * i] = rank;
+            idxl[k * F_in + (rank & 15) * nst + (rank >> 4)] = f[i];
+        }
+        __builtin_amdgcn_wave_barrier();
         const uint2 *src = reinterpret_cast<const uint2 *>(W + k * G * F_in);
-        for (int e = tid; e < G * nq; e += blockDim.x) {
+        for (int e = lane; e < G * nq; e += 64) {
             const int g = e / nq, s4 = (e - g * nq) * 4;
             const uint2 v = src[e];
-            tw[(s4 + 0) * TS + g] = (bf16_t)(v.x & 0xFFFFu);
-            tw[(s4 + 1) * TS + g] = (bf16_t)(v.x >> 16);
-            tw[(s4 + 2) * TS + g] = (bf16_t)(v.y & 0xFFFFu);
-            tw[(s4 + 3) * TS + g] = (bf16_t)(v.y >> 16);
+            tw[spos[s4 + 0] * TS + g] = (bf16_t)(v.x & 0xFFFFu);
+            tw[spos[s4 + 1] * TS + g] = (bf16_t)(v.x >> 16);
+            tw[spos[s4 + 2] * TS + g] = (bf16_t)(v.y & 0xFFFFu);
+            tw[spos[s4 + 3] * TS + g] = (bf16_t)(v.y >> 16);
         }
-        __syncthreads();
-        uint2 *dst = reinterpret_cast<uint2 *>(WT + k * F_in * Gp);
-        const int gq = Gp / 4;                    // label quads per slot
-        for (int e = tid; e < F_in * gq; e += blockDim.x) {
-            const int sl = e / gq, g4 = (e - sl * gq) * 4;
-            const bf16_t *t = tw + sl * TS + g4;
-            uint32_t lo = (g4 + 0 < G ? t[0] : 0u) | ((uint32_t)(g4 + 1 < G ? t[1] : 0u) << 16);
-            uint32_t hi = (g4 + 2 < G ? t[2] : 0u) | ((uint32_t)(g4 + 3 < G ? t[3] : 0u) << 16);
-            dst[e] = make_uint2(lo, hi);
+        __builtin_amdgcn_wave_barrier();
+        // label-octet major: element (position p, label 8o + j) at (o F_in + p) 8 + j, so that the
+        // consumers' operand loads (16 positions x 8 labels per 16 lanes) read contiguous runs
+        uint4 *dst = reinterpret_cast<uint4 *>(WT + k * F_in * Gp);
+        for (int e = lane; e < F_in * (Gp / 8); e += 64) {
+            const int o = e / F_in, sl = e - o * F_in, g8 = 8 * o;
+            const bf16_t *t = tw + sl * TS + g8;
+            uint32_t w[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                w[j] = (g8 + 2 * j < G ? t[2 * j] : 0u) | ((uint32_t)(g8 + 2 * j + 1 < G ? t[2 * j + 1] : 0u) << 16);
+            dst[e] = make_uint4(w[0], w[1], w[2], w[3]);
         }
-        __syncthreads();
+        __builtin_amdgcn_wave_barrier();
     }
 }
 
@@ -754,41 +830,43 @@ struct BwdXGroup {
     int f[F_IN / 16];         // accumulator rows idx[k, 16st + l16]
 };
 
-constexpr int kBxAS = 36;          // accumulator row stride (floats): 32 rows + 4 pad
+constexpr int kBxAS = 40;          // accumulator row stride (floats): 32 rows + 8 pad (bank spread)
+constexpr int kBxASMin = 36;       // where the LDS does not hold the wide rows
 constexpr int kBxConsumers = 2;    // consumer waves (one per 16-row half)
-constexpr int kBxProducers = 2;    // producer waves
+constexpr int kBxProducers = 4;    // producer waves
+constexpr int kBxProdDepth = 4;    // staged dY chunks in flight per producer wave
 constexpr int kBxChunkBytes = 20480;   // staged dY per chunk buffer, at most
 
 // groups of weights in flight per consumer wave: registers, and at most 63 outstanding loads
-template <int F_IN, int NLB>
-constexpr int bx_depth() {
-    constexpr int per = NLB * (F_IN / 16) * 4 + F_IN / 16;
-    return per <= 20 ? 6 : (per <= 40 ? 4 : 2);  // even: products alternate between two buffers
+__host__ __device__ constexpr int bx_depth_for(int f_in, int nlb) {
+    const int per = nlb * (f_in / 16) * 4 + f_in / 16;   // registers per group
+    return per <= 20 ? 8 : (per <= 40 ? 4 : 2);          // a power of two: the chunk size is a multiple
 }
 
-// Staged dY layout, per chunk buffer: [CH groups][32 rows][32 NLB + 8 labels] bf16.  A consumer's
-// operand for one group is then one 16-byte read per 32-label block at a lane-constant offset
-// from the group's base; the 8 spare labels per row put the 16 rows one read touches in distinct
-// banks.  Labels G .. 32 NLB - 1 of every row stay zero (written once, never staged), and the
-// producers stage zeros for groups past the segment, so the consumers need no masking.  A
-// separate all-zero group serves the steps the consumers pad their loop with.
-__host__ __device__ constexpr int bx_row_bytes(int nlb) { return (32 * nlb + 8) * 2; }
+// Staged dY layout, per chunk buffer: [32 rows][CH groups x 32 NLB labels, then 16 spare labels]
+// bf16, row stride RS = 64 NLB CH + 32 bytes.  A producer store (one row, 64 lanes x 8 bytes) is
+// then one contiguous run, and a consumer's operand for one group is one 16-byte read per
+// 32-label block at a lane-constant offset plus a per-group constant; with RS = 32 (mod 256)
+// bytes the 8 rows one read pass serves fall in distinct banks.  Labels G .. 32 NLB - 1 of
+// every group stay zero (written once, never staged), and the producers stage zeros for groups
+// past the segment, so the consumers need no masking: the steps they pad their loop with (up to a
+// multiple of the prefetch depth, which divides CH) read staged zeros and add nothing.
+__host__ __device__ constexpr int bx_stage_row_bytes(int nlb, int ch) { return 64 * nlb * ch + 32; }
 
 template <int F_IN, int NLB>
 __global__ __launch_bounds__((kBxConsumers + kBxProducers) * 64) void k_bwd_x(
-    const int32_t *__restrict__ idx, const bf16_t *__restrict__ WT, const bf16_t *__restrict__ dY,
-    float *__restrict__ part, int B, int Bp, int F_s, int64_t L, int G, int Gp, int64_t K, int nbt, int64_t gps,
-    int CH) {
-    extern __shared__ __align__(16) float accs[];  // [F_s][kBxAS], then the staged dY
-    constexpr int AS = kBxAS;
+    const int32_t *__restrict__ idx, const bf16_t *__restrict__ WT, const uint8_t *__restrict__ over,
+    const bf16_t *__restrict__ dY, float *__restrict__ part, int B, int Bp, int F_s, int64_t L, int G, int Gp,
+    int64_t K, int nbt, int64_t gps, int CH, int AS) {
+    extern __shared__ __align__(16) float accs[];  // [F_s][AS], then the staged dY
     constexpr int NST = F_IN / 16;                 // 16-slot tiles
     constexpr int NP = kBxProducers;
     constexpr int NJ = 32 / NP;                    // rows per producer wave and chunk
-    constexpr int NB = bx_depth<F_IN, NLB>();
-    constexpr int RB = bx_row_bytes(NLB);          // staged bytes per row and group
-    constexpr int GB = 32 * RB;                    // staged bytes per group
-    char *ys = reinterpret_cast<char *>(accs + F_s * AS);   // [2][CH][32][RB], then one zero group
-    const int cbytes = CH * GB;
+    constexpr int NB = bx_depth_for(F_IN, NLB);
+    constexpr int GB = 64 * NLB;                   // staged bytes per group and row
+    const int RS = bx_stage_row_bytes(NLB, CH);    // staged row stride
+    char *ys = reinterpret_cast<char *>(accs + F_s * AS);   // [2][32][RS]
+    const int cbytes = 32 * RS;
     const int w = blockIdx.x;
     const int xcd = w % kXcds;
     const int jj = w / kXcds;
@@ -811,7 +889,7 @@ __global__ __launch_bounds__((kBxConsumers + kBxProducers) * 64) void k_bwd_x(
     // accumulator and the whole staging area (its zero label padding is never written again)
     {
         uint32_t *z = reinterpret_cast<uint32_t *>(accs);
-        const int nz = F_s * AS + (2 * cbytes + GB) / 4;
+        const int nz = F_s * AS + (2 * cbytes) / 4;
         for (int e = tid; e < nz; e += nthr) z[e] = 0u;
     }
     __syncthreads();
@@ -821,42 +899,63 @@ __global__ __launch_bounds__((kBxConsumers + kBxProducers) * 64) void k_bwd_x(
     if (wave >= kBxConsumers) {
         // ---- producers: dY chunk c (groups cCH .. of the segment) -> staging buffer c % 2 ----
         // Lane i loads labels 4i .. 4i+3 of the chunk (8 bytes) of one row per instruction; they
-        // belong to group 4i / G of the chunk.  Labels past the segment read as zero.
+        // belong to group 4i / G of the chunk.  Labels past the segment read as zero.  Each wave
+        // keeps PD chunks in flight in registers, so a load has PD chunk periods to arrive.
+        constexpr int PD = kBxProdDepth;
         const int p = wave - kBxConsumers;
         const int rows = B - b0 < 32 ? B - b0 : 32;
         const int lab4 = 4 * lane;
         const int gi = lab4 / G, wl = lab4 - gi * G;
-        const uint32_t soff = (uint32_t)(gi * GB + wl * 2);   // within the chunk buffer, row 0
-        uint2 v[NJ];
-        auto load = [&](int c) {
+        // Byte offset within the chunk buffer (row 0).  Lanes past the chunk write into the 8
+        // spare labels of the row, which no consumer reads, so every store is unconditional.
+        const bool lane_st = lab4 < CH * G;
+        const uint32_t soff = lane_st ? (uint32_t)(gi * GB + wl * 2) : (uint32_t)(CH * GB);
+        uint2 v[PD][NJ];
+        // chunk c (past the last one: all zeros)
+        auto load = [&](int c, uint2 (&vv)[NJ]) {
             const int64_t lab0 = (g_begin + (int64_t)c * CH) * G;
             const int nlab = (n - c * CH < CH ? n - c * CH : CH) * G;   // this chunk's labels
             const Buf db(dY + (int64_t)b0 * L + lab0, (uint32_t)(((int64_t)rows * L - lab0) * 2));
-            const bool ok = lab4 < nlab;
+            // a select, not a branch around the loads (which would cost the waits their depth)
+            uint32_t lo = lab4 < nlab ? 8 * (uint32_t)lane : kOob;
+            asm volatile("" : "+v"(lo));
 #pragma unroll
             for (int i = 0; i < NJ; ++i) {
                 const int r = p + NP * i;
-                v[i] = db.ld8(ok ? (uint32_t)((int64_t)r * L * 2) + 8 * lane : kOob);
+                vv[i] = db.ld8((uint32_t)((int64_t)r * L * 2) + lo);
             }
         };
-        const bool lane_st = lab4 < CH * G;   // lanes past the chunk store nothing
-        auto store = [&](int c) {
+        auto store = [&](int c, const uint2 (&vv)[NJ]) {
             char *yb = ys + (c & 1) * cbytes + soff;
-            if (lane_st) {
 #pragma unroll
-                for (int i = 0; i < NJ; ++i) {
-                    const int r = p + NP * i;
-                    *reinterpret_cast<uint2 *>(yb + r * RB) = v[i];
-                }
+            for (int i = 0; i < NJ; ++i) {
+                const int r = p + NP * i;
+                *reinterpret_cast<uint2 *>(yb + r * RS) = vv[i];
             }
         };
-        load(0);
-        store(0);
-        if (nch > 1) load(1);
-        for (int c = 0; c < nch; ++c) {
-            __syncthreads();  // chunk c staged, chunk c - 1 consumed
-            if (c + 1 < nch) store(c + 1);
-            if (c + 2 < nch) load(c + 2);
+#pragma unroll
+        for (int j = 0; j < PD; ++j) load(j, v[j]);
+        store(0, v[0]);
+        load(PD, v[0]);
+        // after the barrier of chunk c: chunk c + 1 into the buffer chunk c - 1 used (past the
+        // last chunk: unused zeros), then the registers it came from take chunk c + 1 + PD.
+        // Whole passes of PD chunks first (no exit inside a pass, so the load waits keep their
+        // depth across the loop's back edge), then the remaining chunks.
+        int c0 = 0;
+        for (; c0 + PD <= nch; c0 += PD) {
+#pragma unroll
+            for (int j = 0; j < PD; ++j) {
+                __syncthreads();  // chunk c0 + j staged, chunk c0 + j - 1 consumed
+                store(c0 + j + 1, v[(j + 1) % PD]);
+                load(c0 + j + 1 + PD, v[(j + 1) % PD]);
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < PD - 1; ++j) {
+            if (c0 + j < nch) {
+                __syncthreads();
+                store(c0 + j + 1, v[(j + 1) % PD]);
+            }
         }
     } else {
         // ---- consumers: rows 16bh .. 16bh + 15 of the tile ----
@@ -874,8 +973,8 @@ __global__ __launch_bounds__((kBxConsumers + kBxProducers) * 64) void k_bwd_x(
         for (int c = 0; c < NLB; ++c)
 #pragma unroll
             for (int st = 0; st < NST; ++st) {
-                const int lab = 32 * c + 8 * q;   // labels past Gp read as zero
-                wvo[c][st] = lab < Gp ? (uint32_t)(((16 * st + l16) * Gp + lab) * 2) : kOob;
+                const int o = 4 * c + q;          // label octet; octets past Gp read as zero
+                wvo[c][st] = 8 * o < Gp ? (uint32_t)((o * F_IN + 16 * st + l16) * 16) : kOob;
             }
         auto issue = [&](int sg, BwdXGroup<F_IN, NLB> &t) {
 #pragma unroll
@@ -903,34 +1002,29 @@ __global__ __launch_bounds__((kBxConsumers + kBxProducers) * 64) void k_bwd_x(
         };
 
         // this lane's dY operand: row 16 bh + l16 of a group, labels 32c + 8q .. +7
-        const int ylane = (16 * bh + l16) * RB + 16 * q;
+        const char *ylane = ys + (16 * bh + l16) * RS + 16 * q;
         // this lane's accumulator column: rows 16 bh + 4q .. +3 of an accumulator row
-        char *accb = reinterpret_cast<char *>(accs) + (16 * bh + 4 * q) * 4;
-
-        // Groups are read in order, so their place in the staged chunks is a wave-uniform cursor
-        // (chunk buffer, group in chunk); the first group of a chunk waits for the chunk's
-        // barrier.  Steps past the last group read the zero group and add nothing.
-        int cg = 0;        // group within the chunk of the next group to read
-        int cbuf = 0;      // byte offset of the chunk buffer holding it
-        auto read_dy = [&](uint4 (&ay)[NLB], bool live) {
-            if (cg == 0 && live) __syncthreads();  // a new chunk is staged
-            const int gb = live ? cbuf + cg * GB : 2 * cbytes;   // the zero group follows both buffers
-            const char *yp = ys + gb + ylane;
+        typedef __attribute__((address_space(3))) f32x4_t lds_f32x4_t;
+        const uint32_t acol = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) float *)accs +
+                              (uint32_t)((16 * bh + 4 * q) * 4);   // LDS byte address
+        auto read_dy = [&](uint4 (&ay)[NLB], const char *yp) {
 #pragma unroll
             for (int c = 0; c < NLB; ++c) ay[c] = *reinterpret_cast<const uint4 *>(yp + 64 * c);
-            if (++cg == CH) {
-                cg = 0;
-                cbuf = cbytes - cbuf;
-            }
         };
+
+        auto acc_addr = [&](int f) {
+            uint32_t ao = __umul24((uint32_t)f, (uint32_t)(AS * 4)) + acol;
+            asm volatile("" : "+v"(ao));   // computed once, kept for the write
+            return ao;
+        };
+        auto acc_read = [&](uint32_t ao) { return *(lds_f32x4_t *)(uintptr_t)ao; };
+        auto acc_write = [&](uint32_t ao, const f32x4_t &v) { *(lds_f32x4_t *)(uintptr_t)ao = v; };
 
         // Group g's weights live in buffer g % NB, loaded NB - 1 groups ahead (clamped index past
         // the end, so every wait covers only its own loads); its dY operand is read one step ahead,
-        // in buffer g % 2.  Step s: read the accumulator rows of group s; refill the buffer group
-        // s - 1 has finished with (the load issue overlaps the LDS reads); read the dY operand of
-        // group s + 1; then D = dZ_s W_s + old through the matrix core (its accumulator input) and
-        // write D back.  The group count is padded to a multiple of NB so that the unrolled body
-        // has no branch around a load.
+        // in buffer g % 2.  One unrolled pass covers NB groups, and a chunk holds CH = m NB groups,
+        // so a chunk ends after the last step of every m-th pass: there the consumers wait for the
+        // next chunk (if the segment has one) and switch buffers.
         BwdXGroup<F_IN, NLB> tl[NB];
         uint4 ay[2][NLB];
 #pragma unroll
@@ -938,29 +1032,122 @@ __global__ __launch_bounds__((kBxConsumers + kBxProducers) * 64) void k_bwd_x(
             issue(cl(b), tl[b]);
             __builtin_amdgcn_sched_barrier(0);  // keep prefetch order
         }
-        const int n_pad = (n + NB - 1) / NB * NB;
-        read_dy(ay[0], true);
-        for (int s0 = 0; s0 < n_pad; s0 += NB) {
+        const int m = CH / NB;                           // passes per chunk
+        const int n_pad = (n + NB - 1) / NB * NB;        // at most nch CH, as NB divides CH
+        const int nst = nch * CH;                        // groups staged, zeros past n included
+        int ic = 0;            // pass within the chunk
+        int ybuf = 0;          // byte offset of the chunk buffer in use
+        // dY operand of group s0 + b + 1, read during step b of the pass starting at s0
+        auto next_dy = [&](int b, int s0, const char *yit, uint4 (&ay)[NLB]) {
+            if (b < NB - 1) {
+                read_dy(ay, yit + (b + 1) * GB);
+            } else {
+                if (++ic == m) {
+                    ic = 0;
+                    ybuf = cbytes - ybuf;
+                    if (s0 + NB < nst) __syncthreads();   // the next chunk is staged
+                }
+                read_dy(ay, ylane + ybuf + ic * (NB * GB));
+            }
+        };
+
+        // Overlapped schedule (every group of the segment keeps the rows it shares with its
+        // predecessor in the late half of its tiles, and NB >= 3 so that the next group's support
+        // is in registers one step early).  Step s: read the early-half accumulator rows of group
+        // s + 1 (no row of group s among them); refill the weight buffer of group s - 1; read the
+        // dY operand of group s + 1; D = dZ_s W_s + old through the matrix core for the early
+        // half (rows read one step ago), then for the late half (read at the end of the previous
+        // step), writing each back; finally read the late-half rows of group s + 1, behind the
+        // write-back in the wave's LDS order.  Only that last read waits on this step's writes.
+        // The remaining groups (all of them without the overlap) take the serial schedule.
+        int n_main = 0;
+        if constexpr (NB >= 3) {
+            uint32_t o = 0;
+            for (int i = lane; i < n; i += 64) o |= over[g_begin + i];
+            n_main = __builtin_amdgcn_readfirstlane(__ballot(o != 0) == 0 ? n / NB * NB : 0);
+        }
+        __syncthreads();                                 // chunk 0 staged
+        read_dy(ay[0], ylane);
+        int s0 = 0;
+        if constexpr (NB >= 3) {
+            if (n_main > 0) {
+                constexpr int NE = NST / 2, NL = NST - NE;   // early / late tiles
+                f32x4_t ae[2][NE], al[NL];
+                uint32_t aoe[2][NE], aol[NL];
+#pragma unroll
+                for (int e = 0; e < NE; ++e) {
+                    aoe[0][e] = acc_addr(tl[0].f[e]);
+                    ae[0][e] = acc_read(aoe[0][e]);
+                }
+#pragma unroll
+                for (int l = 0; l < NL; ++l) {
+                    aol[l] = acc_addr(tl[0].f[NE + l]);
+                    al[l] = acc_read(aol[l]);
+                }
+                for (; s0 < n_main; s0 += NB) {
+                    const char *yit = ylane + ybuf + ic * (NB * GB);   // group s0 of this pass
+#pragma unroll
+                    for (int b = 0; b < NB; ++b) {
+                        const int sg = s0 + b;
+                        const int cur = b & 1, nxt = cur ^ 1, tn = (b + 1) % NB;
+#pragma unroll
+                        for (int e = 0; e < NE; ++e) {
+                            aoe[nxt][e] = acc_addr(tl[tn].f[e]);
+                            ae[nxt][e] = acc_read(aoe[nxt][e]);
+                        }
+                        __builtin_amdgcn_sched_barrier(0);  // early reads first
+                        issue(cl(sg + NB - 1), tl[(b + NB - 1) % NB]);
+                        __builtin_amdgcn_sched_barrier(0);  // keep prefetch order
+                        next_dy(b, s0, yit, ay[(b + 1) & 1]);
+#pragma unroll
+                        for (int e = 0; e < NE; ++e) {
+#pragma unroll
+                            for (int c = 0; c < NLB; ++c)
+                                ae[cur][e] = mfma16x16x32(as_bf16x8(ay[b & 1][c]), as_bf16x8(tl[b].w[c][e]), ae[cur][e]);
+                            acc_write(aoe[cur][e], ae[cur][e]);
+                        }
+#pragma unroll
+                        for (int l = 0; l < NL; ++l) {
+#pragma unroll
+                            for (int c = 0; c < NLB; ++c)
+                                al[l] = mfma16x16x32(as_bf16x8(ay[b & 1][c]), as_bf16x8(tl[b].w[c][NE + l]), al[l]);
+                            acc_write(aol[l], al[l]);
+                        }
+                        __builtin_amdgcn_sched_barrier(0);  // late reads behind the write-back
+#pragma unroll
+                        for (int l = 0; l < NL; ++l) {
+                            aol[l] = acc_addr(tl[tn].f[NE + l]);
+                            al[l] = acc_read(aol[l]);
+                        }
+                    }
+                }
+            }
+        }
+        // Serial schedule.  Step s: read the accumulator rows of group s; refill the buffer group
+        // s - 1 has finished with (the load issue overlaps the LDS reads); read the dY operand of
+        // group s + 1; then D = dZ_s W_s + old through the matrix core and write D back.
+        for (; s0 < n_pad; s0 += NB) {
+            const char *yit = ylane + ybuf + ic * (NB * GB);   // group s0 of this pass
 #pragma unroll
             for (int b = 0; b < NB; ++b) {
                 const int sg = s0 + b;
                 f32x4_t acc[NST];
-                char *ap[NST];
+                uint32_t ao[NST];
 #pragma unroll
                 for (int st = 0; st < NST; ++st) {
-                    ap[st] = accb + __umul24((uint32_t)tl[b].f[st], AS * 4);
-                    acc[st] = *reinterpret_cast<const f32x4_t *>(ap[st]);
+                    ao[st] = acc_addr(tl[b].f[st]);
+                    acc[st] = acc_read(ao[st]);
                 }
                 __builtin_amdgcn_sched_barrier(0);  // accumulator reads first
                 issue(cl(sg + NB - 1), tl[(b + NB - 1) % NB]);
                 __builtin_amdgcn_sched_barrier(0);  // keep prefetch order
-                read_dy(ay[(b + 1) & 1], sg + 1 < n);
+                next_dy(b, s0, yit, ay[(b + 1) & 1]);
 #pragma unroll
                 for (int st = 0; st < NST; ++st) {
 #pragma unroll
                     for (int c = 0; c < NLB; ++c)
                         acc[st] = mfma16x16x32(as_bf16x8(ay[b & 1][c]), as_bf16x8(tl[b].w[c][st]), acc[st]);
-                    *reinterpret_cast<f32x4_t *>(ap[st]) = acc[st];
+                    acc_write(ao[st], acc[st]);
                 }
             }
         }
@@ -985,7 +1172,7 @@ hipError_t allow_lds(Kern k, size_t bytes) {
 }
 
 struct BwdXGeom {
-    int nbt, nwaves, ch;
+    int nbt, nwaves, ch, as;
     int64_t nseg, gps;
     size_t lds;
 };
@@ -995,10 +1182,17 @@ BwdXGeom bwd_x_geom(const haste::TailArgs &a) {
     g.nbt = (int)haste::cdiv(a.B, 32);
     const int nt = (int)(a.F_in / 16) * 2;
     g.nwaves = kBxConsumers + kBxProducers;
-    // groups per staged dY chunk: at most 256 labels (one 512-byte load per row) and kBxChunkBytes
-    const int nlb = (int)((a.G + 31) / 32), gb = 32 * bx_row_bytes(nlb);
-    g.ch = (int)(256 / a.G) < kBxChunkBytes / gb ? (int)(256 / a.G) : kBxChunkBytes / gb;
-    g.lds = (size_t)a.F_s * kBxAS * 4 + (size_t)(2 * g.ch + 1) * gb;
+    // groups per staged dY chunk: at most 256 labels (one 512-byte load per row), kBxChunkBytes and
+    // what the LDS holds beside the accumulator, rounded down to a multiple of the prefetch depth
+    const int nlb = (int)((a.G + 31) / 32), gb = 32 * 64 * nlb;   // staged bytes per group
+    int ch = (int)(256 / a.G) < kBxChunkBytes / gb ? (int)(256 / a.G) : kBxChunkBytes / gb;
+    const int nb = bx_depth_for(a.F_in, nlb);
+    auto stage = [&](int c) { return (int64_t)2 * 32 * bx_stage_row_bytes(nlb, c); };   // both buffers
+    // the wide accumulator rows where the LDS still holds chunks of at least one pass
+    g.as = (int64_t)a.F_s * kBxAS * 4 + stage(nb) <= (int64_t)kLdsBudget ? kBxAS : kBxASMin;
+    while (ch > 0 && (int64_t)a.F_s * g.as * 4 + stage(ch) > (int64_t)kLdsBudget) --ch;
+    g.ch = ch / nb * nb;
+    g.lds = (size_t)a.F_s * g.as * 4 + (size_t)stage(g.ch);
     const int64_t K = a.L / a.G;
     int64_t spx = kCusPerXcd / g.nbt;  // one workgroup per CU: the accumulator takes most of the LDS
     if (spx < 1) spx = 1;
@@ -1135,10 +1329,11 @@ hipError_t bwd_w_mfma(const TailArgs &a, const void *X, const int32_t *idx, cons
 bool bwd_x_mfma_supported(const TailArgs &a) {
     if (!fwd_mfma_supported(a) || a.G > 128) return false;
     const BwdXGeom g = bwd_x_geom(a);
-    return g.ch >= 2 && g.lds <= kLdsBudget;
+    return g.ch > 0 && g.lds <= kLdsBudget;
 }
 
-// workspace: the per-segment partials, then W^T (group blocks [F_in][Gp]), then the supports in lane order
+// workspace: the per-segment partials, then W^T (group blocks [Gp / 8][F_in][8]), then the supports in lane
+// order, then one overlap flag per group
 static size_t bwd_x_part_bytes(const TailArgs &a, const BwdXGeom &g) {
     return round_up((int64_t)g.nseg * a.F_s * (g.nbt * 32) * 4, 256);
 }
@@ -1149,30 +1344,31 @@ static size_t bwd_x_wt_bytes(const TailArgs &a) {
 
 size_t bwd_x_mfma_ws(const TailArgs &a) {
     const BwdXGeom g = bwd_x_geom(a);
-    return bwd_x_part_bytes(a, g) + bwd_x_wt_bytes(a) + (size_t)(a.L / a.G) * (size_t)a.F_in * 4 + 256;
+    const int64_t K = a.L / a.G;
+    return bwd_x_part_bytes(a, g) + bwd_x_wt_bytes(a) + (size_t)round_up(K * a.F_in * 4, 256) + (size_t)K + 256;
 }
 
 template <int F_IN, int NLB>
 static hipError_t launch_bwd_x(const TailArgs &a, const BwdXGeom &g, const int32_t *idx, const bf16_t *WT,
-                               const void *dY, float *part, hipStream_t s) {
+                               const uint8_t *over, const void *dY, float *part, hipStream_t s) {
     auto kern = k_bwd_x<F_IN, NLB>;
     hipError_t e = allow_lds(kern, g.lds);
     if (e != hipSuccess) return e;
     const int64_t K = a.L / a.G;
-    hipLaunchKernelGGL(kern, dim3((unsigned)(g.nseg * g.nbt)), dim3(g.nwaves * 64), g.lds, s, idx, WT,
+    hipLaunchKernelGGL(kern, dim3((unsigned)(g.nseg * g.nbt)), dim3(g.nwaves * 64), g.lds, s, idx, WT, over,
                        (const bf16_t *)dY, part, (int)a.B, g.nbt * 32, (int)a.F_s, a.L, (int)a.G,
-                       (int)round_up(a.G, 8), K, g.nbt, g.gps, g.ch);
+                       (int)round_up(a.G, 8), K, g.nbt, g.gps, g.ch, g.as);
     return hipGetLastError();
 }
 
 template <int F_IN>
 static hipError_t launch_bwd_x_g(const TailArgs &a, const BwdXGeom &g, const int32_t *idx, const bf16_t *WT,
-                                 const void *dY, float *part, hipStream_t s) {
+                                 const uint8_t *over, const void *dY, float *part, hipStream_t s) {
     switch ((a.G + 31) / 32) {
-        case 1: return launch_bwd_x<F_IN, 1>(a, g, idx, WT, dY, part, s);
-        case 2: return launch_bwd_x<F_IN, 2>(a, g, idx, WT, dY, part, s);
-        case 3: return launch_bwd_x<F_IN, 3>(a, g, idx, WT, dY, part, s);
-        case 4: return launch_bwd_x<F_IN, 4>(a, g, idx, WT, dY, part, s);
+        case 1: return launch_bwd_x<F_IN, 1>(a, g, idx, WT, over, dY, part, s);
+        case 2: return launch_bwd_x<F_IN, 2>(a, g, idx, WT, over, dY, part, s);
+        case 3: return launch_bwd_x<F_IN, 3>(a, g, idx, WT, over, dY, part, s);
+        case 4: return launch_bwd_x<F_IN, 4>(a, g, idx, WT, over, dY, part, s);
     }
     return hipErrorInvalidValue;
 }
@@ -1184,16 +1380,20 @@ hipError_t bwd_x_mfma(const TailArgs &a, const int32_t *idx, const void *W, cons
     bf16_t *WT = reinterpret_cast<bf16_t *>(reinterpret_cast<char *>(ws) + bwd_x_part_bytes(a, g));
     int32_t *idxl = reinterpret_cast<int32_t *>(reinterpret_cast<char *>(WT) + bwd_x_wt_bytes(a));
     const int64_t K = a.L / a.G;
+    uint8_t *over = reinterpret_cast<uint8_t *>(idxl) + round_up(K * a.F_in * 4, 256);
     const int Gp = (int)round_up(a.G, 8);
-    const int64_t tgrid = K < 4096 ? K : 4096;
-    hipLaunchKernelGGL(k_transpose_w, dim3((unsigned)tgrid), dim3(256), (size_t)a.F_in * (Gp + 4) * 2, s,
-                       (const bf16_t *)W, idx, WT, idxl, K, (int)a.G, Gp, (int)a.F_in);
-    hipError_t e = hipGetLastError();
+    const int64_t tgrid = cdiv(K, kTwWaves) < 4096 ? cdiv(K, kTwWaves) : 4096;
+    const size_t tlds = (size_t)kTwWaves * tw_wave_bytes((int)a.F_in, Gp);
+    hipError_t e = allow_lds(k_transpose_w, tlds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_transpose_w, dim3((unsigned)tgrid), dim3(kTwWaves * 64), tlds, s, (const bf16_t *)W, idx,
+                       WT, idxl, over, K, (int)a.G, Gp, (int)a.F_in, g.gps);
+    e = hipGetLastError();
     if (e != hipSuccess) return e;
     switch (a.F_in) {
-        case 32: e = launch_bwd_x_g<32>(a, g, idxl, WT, dY, part, s); break;
-        case 64: e = launch_bwd_x_g<64>(a, g, idxl, WT, dY, part, s); break;
-        case 128: e = launch_bwd_x_g<128>(a, g, idxl, WT, dY, part, s); break;
+        case 32: e = launch_bwd_x_g<32>(a, g, idxl, WT, over, dY, part, s); break;
+        case 64: e = launch_bwd_x_g<64>(a, g, idxl, WT, over, dY, part, s); break;
+        case 128: e = launch_bwd_x_g<128>(a, g, idxl, WT, over, dY, part, s); break;
         default: return hipErrorInvalidValue;
     }
     if (e != hipSuccess) return e;
