@@ -7,6 +7,8 @@
 //   backward-feature dH_k = dZ_k W_k, scattered to X's columns idx[k,:] (M = slots,  N = batch,  K = labels)
 // Every contraction is a small dense GEMM once the group's support columns are gathered, which is
 // what makes the group-shared format MFMA-friendly (one gather serves all G labels).
+#include <type_traits>
+
 #include "common.hpp"
 
 namespace {
@@ -898,65 +900,75 @@ __global__ __launch_bounds__((kBxConsumers + kBxProducers) * 64) void k_bwd_x(
 
     if (wave >= kBxConsumers) {
         // ---- producers: dY chunk c (groups cCH .. of the segment) -> staging buffer c % 2 ----
-        // Lane i loads labels 4i .. 4i+3 of the chunk (8 bytes) of one row per instruction; they
-        // belong to group 4i / G of the chunk.  Labels past the segment read as zero.  Each wave
-        // keeps PD chunks in flight in registers, so a load has PD chunk periods to arrive.
-        constexpr int PD = kBxProdDepth;
-        const int p = wave - kBxConsumers;
-        const int rows = B - b0 < 32 ? B - b0 : 32;
-        const int lab4 = 4 * lane;
-        const int gi = lab4 / G, wl = lab4 - gi * G;
-        // Byte offset within the chunk buffer (row 0).  Lanes past the chunk write into the 8
-        // spare labels of the row, which no consumer reads, so every store is unconditional.
-        const bool lane_st = lab4 < CH * G;
-        const uint32_t soff = lane_st ? (uint32_t)(gi * GB + wl * 2) : (uint32_t)(CH * GB);
-        uint2 v[PD][NJ];
-        // chunk c (past the last one: all zeros)
-        auto load = [&](int c, uint2 (&vv)[NJ]) {
-            const int64_t lab0 = (g_begin + (int64_t)c * CH) * G;
-            const int nlab = (n - c * CH < CH ? n - c * CH : CH) * G;   // this chunk's labels
-            const Buf db(dY + (int64_t)b0 * L + lab0, (uint32_t)(((int64_t)rows * L - lab0) * 2));
-            // a select, not a branch around the loads (which would cost the waits their depth)
-            uint32_t lo = lab4 < nlab ? 8 * (uint32_t)lane : kOob;
-            asm volatile("" : "+v"(lo));
+        // Lane i loads WB bytes of one row per instruction: labels (i mod LPR) WB/2 .. of the
+        // chunk, which belong to one group (WB = 16 needs groups of a multiple of 8 labels, else
+        // WB = 8), and row half i / LPR of the instruction's RPI rows.  Labels past the segment read
+        // as zero.  Each wave keeps PD chunks in flight in registers, so a load has PD chunk
+        // periods to arrive.
+        auto produce = [&](auto wb) {
+            constexpr int WB = decltype(wb)::value;
+            constexpr int LPR = 512 / WB;            // lanes per row (a chunk row is at most 512 bytes)
+            constexpr int RPI = 64 / LPR;            // rows per instruction
+            constexpr int NI = NJ / RPI;             // instructions per chunk and wave
+            typedef typename std::conditional<WB == 16, uint4, uint2>::type V;
+            constexpr int PD = kBxProdDepth;
+            const int p = wave - kBxConsumers;
+            const int rows = B - b0 < 32 ? B - b0 : 32;
+            const int half = lane / LPR;
+            const int lab = (lane % LPR) * (WB / 2);
+            const int gi = lab / G, wl = lab - gi * G;
+            // Byte offset within the chunk buffer.  Lanes past the chunk write into the spare
+            // bytes at the end of the row, which no consumer reads, so every store is unconditional.
+            const bool lane_st = lab < CH * G;
+            const uint32_t soff = (lane_st ? (uint32_t)(gi * GB + wl * 2) : (uint32_t)(CH * GB)) + half * NP * RS;
+            V v[PD][NI];
+            // chunk c (past the last one: all zeros)
+            auto load = [&](int c, V (&vv)[NI]) {
+                const int64_t lab0 = (g_begin + (int64_t)c * CH) * G;
+                const int nlab = (n - c * CH < CH ? n - c * CH : CH) * G;   // this chunk's labels
+                const Buf db(dY + (int64_t)b0 * L + lab0, (uint32_t)(((int64_t)rows * L - lab0) * 2));
+                // a select, not a branch around the loads (which would cost the waits their depth)
+                uint32_t lo = lab < nlab ? (uint32_t)(2 * lab) + (uint32_t)((int64_t)half * NP * L * 2) : kOob;
+                asm volatile("" : "+v"(lo));
 #pragma unroll
-            for (int i = 0; i < NJ; ++i) {
-                const int r = p + NP * i;
-                vv[i] = db.ld8((uint32_t)((int64_t)r * L * 2) + lo);
+                for (int i = 0; i < NI; ++i) {
+                    const uint32_t ro = (uint32_t)((int64_t)(p + NP * RPI * i) * L * 2);
+                    if constexpr (WB == 16) vv[i] = db.ld16(ro + lo);
+                    else vv[i] = db.ld8(ro + lo);
+                }
+            };
+            auto store = [&](int c, const V (&vv)[NI]) {
+                char *yb = ys + (c & 1) * cbytes + soff;
+#pragma unroll
+                for (int i = 0; i < NI; ++i) *reinterpret_cast<V *>(yb + (p + NP * RPI * i) * RS) = vv[i];
+            };
+#pragma unroll
+            for (int j = 0; j < PD; ++j) load(j, v[j]);
+            store(0, v[0]);
+            load(PD, v[0]);
+            // after the barrier of chunk c: chunk c + 1 into the buffer chunk c - 1 used (past the
+            // last chunk: unused zeros), then the registers it came from take chunk c + 1 + PD.
+            // Whole passes of PD chunks first (no exit inside a pass, so the load waits keep their
+            // depth across the loop's back edge), then the remaining chunks.
+            int c0 = 0;
+            for (; c0 + PD <= nch; c0 += PD) {
+#pragma unroll
+                for (int j = 0; j < PD; ++j) {
+                    __syncthreads();  // chunk c0 + j staged, chunk c0 + j - 1 consumed
+                    store(c0 + j + 1, v[(j + 1) % PD]);
+                    load(c0 + j + 1 + PD, v[(j + 1) % PD]);
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < PD - 1; ++j) {
+                if (c0 + j < nch) {
+                    __syncthreads();
+                    store(c0 + j + 1, v[(j + 1) % PD]);
+                }
             }
         };
-        auto store = [&](int c, const uint2 (&vv)[NJ]) {
-            char *yb = ys + (c & 1) * cbytes + soff;
-#pragma unroll
-            for (int i = 0; i < NJ; ++i) {
-                const int r = p + NP * i;
-                *reinterpret_cast<uint2 *>(yb + r * RS) = vv[i];
-            }
-        };
-#pragma unroll
-        for (int j = 0; j < PD; ++j) load(j, v[j]);
-        store(0, v[0]);
-        load(PD, v[0]);
-        // after the barrier of chunk c: chunk c + 1 into the buffer chunk c - 1 used (past the
-        // last chunk: unused zeros), then the registers it came from take chunk c + 1 + PD.
-        // Whole passes of PD chunks first (no exit inside a pass, so the load waits keep their
-        // depth across the loop's back edge), then the remaining chunks.
-        int c0 = 0;
-        for (; c0 + PD <= nch; c0 += PD) {
-#pragma unroll
-            for (int j = 0; j < PD; ++j) {
-                __syncthreads();  // chunk c0 + j staged, chunk c0 + j - 1 consumed
-                store(c0 + j + 1, v[(j + 1) % PD]);
-                load(c0 + j + 1 + PD, v[(j + 1) % PD]);
-            }
-        }
-#pragma unroll
-        for (int j = 0; j < PD - 1; ++j) {
-            if (c0 + j < nch) {
-                __syncthreads();
-                store(c0 + j + 1, v[(j + 1) % PD]);
-            }
-        }
+        if (G % 8 == 0) produce(std::integral_constant<int, 16>{});
+        else produce(std::integral_constant<int, 8>{});
     } else {
         // ---- consumers: rows 16bh .. 16bh + 15 of the tile ----
         const int bh = wave;
