@@ -718,84 +718,54 @@ __global__ __launch_bounds__(512) void k_bwd_w2(const bf16_t *__restrict__ Xb, c
 // 256-byte runs; idxl keeps the supports of lanes l16, 16 + l16, ... side by side (one vector load
 // per lane).
 //
-// Slot order.  The consumers read the accumulator rows of a group's first F_in / 2 positions (the
-// early half) before the previous group of the segment has written its rows back, so the early
-// half must hold no row of the previous group's support; the rows the two share go to the late
-// half, which is read after the write-back.  Within that constraint slots are ordered by (shared,
-// occurrence of the residue so far, row mod 8): each run of 8 positions (the lanes that one
-// accumulator access serves together) then holds distinct residues mod 8 where the support
-// allows, and with 40-float accumulator rows such a run touches every LDS bank once.  over[k] is
-// set when group k shares more than F_in / 2 rows with group k - 1, more than the late half
-// holds; segments containing such a group are processed without the overlap.
+// Slot order.  An accumulator read or write of a tile is served 8 lanes at a time, and 8 rows of
+// distinct residue mod 8 fall in distinct LDS banks (40-float rows).  Slots are therefore ordered
+// by (occurrence of the residue so far, row mod 8), which deals the residues round-robin over the
+// runs of 8 positions: a residue held by at most F_in / 8 slots never appears twice in a run.
 // One group per wave step (the four waves of a workgroup work independently, each in its own LDS
-// region: the support of the previous group, the positions, and the transposed block).
+// region: the positions and the transposed block).
 constexpr int kTwWaves = 4;
 
 __host__ __device__ constexpr int tw_wave_bytes(int f_in, int gp) {
-    return ((2 * f_in * 4 + f_in * (gp + 4) * 2) + 15) / 16 * 16;
+    return ((f_in * 4 + f_in * (gp + 4) * 2) + 15) / 16 * 16;
 }
 
 __global__ __launch_bounds__(kTwWaves * 64) void k_transpose_w(const bf16_t *__restrict__ W, const int32_t *__restrict__ idx,
-                                                              bf16_t *__restrict__ WT, int32_t *__restrict__ idxl,
-                                                              uint8_t *__restrict__ over, int64_t K, int G, int Gp,
-                                                              int F_in, int64_t gps) {
+                                                              bf16_t *__restrict__ WT, int32_t *__restrict__ idxl, int64_t K,
+                                                              int G, int Gp, int F_in) {
     extern __shared__ __align__(16) char twsh[];
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
     char *mine = twsh + wv * tw_wave_bytes(F_in, Gp);
-    int *sprev = reinterpret_cast<int *>(mine);               // [F_in] previous support (or -1)
-    int *spos = sprev + F_in;                                 // [F_in] lane-order position of each slot
+    int *spos = reinterpret_cast<int *>(mine);                // [F_in] lane-order position of each slot
     bf16_t *tw = reinterpret_cast<bf16_t *>(spos + F_in);     // [F_in][Gp + 4], rows by position
     const int TS = Gp + 4;
     const int nq = F_in / 4;                      // slot quads per label
     const int nst = F_in / 16;
     const uint64_t lt = __lanemask_lt();
     for (int64_t k = (int64_t)blockIdx.x * kTwWaves + wv; k < K; k += (int64_t)gridDim.x * kTwWaves) {
-        const bool has_prev = k % gps != 0;       // the first group of a segment has none
         // slots t = lane and t = lane + 64 (F_in = 128)
         int f[2], cls[2], occ[2] = {0, 0};
 #pragma unroll
         for (int i = 0; i < 2; ++i) {
             const int t = lane + 64 * i;
             f[i] = t < F_in ? idx[k * F_in + t] : -1;
-            if (t < F_in) sprev[t] = has_prev ? idx[(k - 1) * F_in + t] : -1;
+            cls[i] = f[i] >= 0 ? (f[i] & 7) : -1;  // row mod 8
         }
-        __builtin_amdgcn_wave_barrier();
+        int cnt[8];
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            cls[i] = -1;                          // 8 shared + (row mod 8)
-            if (f[i] >= 0) {
-                int lo = 0, hi = F_in;            // first position of the ascending previous support >= f
-                while (lo < hi) {
-                    const int mid = (lo + hi) >> 1;
-                    if (sprev[mid] < f[i]) lo = mid + 1;
-                    else hi = mid;
-                }
-                cls[i] = (lo < F_in && sprev[lo] == f[i] ? 8 : 0) + (f[i] & 7);
-            }
-        }
-        int cnt[16];
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
+        for (int v = 0; v < 8; ++v) {
             const uint64_t m0 = __ballot(cls[0] == v), m1 = __ballot(cls[1] == v);
             if (cls[0] == v) occ[0] = __popcll(m0 & lt);
             if (cls[1] == v) occ[1] = __popcll(m0) + __popcll(m1 & lt);
             cnt[v] = __popcll(m0) + __popcll(m1);
         }
-        int n0 = 0;                               // slots not shared with the previous group
-#pragma unroll
-        for (int v = 0; v < 8; ++v) n0 += cnt[v];
-        if (lane == 0) over[k] = (uint8_t)(n0 < F_in / 2 ? 1 : 0);
 #pragma unroll
         for (int i = 0; i < 2; ++i) {
             if (cls[i] < 0) continue;
-            const int r = cls[i] & 7, o = occ[i];
-            int rk0 = 0, rk1 = n0;                // the rank if unshared / if shared (static counts)
+            const int r = cls[i], o = occ[i];
+            int rank = 0;                         // slots with a smaller (occurrence, residue)
 #pragma unroll
-            for (int v = 0; v < 8; ++v) {
-                rk0 += (cnt[v] < o ? cnt[v] : o) + (v < r && cnt[v] > o ? 1 : 0);
-                rk1 += (cnt[8 + v] < o ? cnt[8 + v] : o) + (v < r && cnt[8 + v] > o ? 1 : 0);
-            }
-            const int rank = (cls[i] & 8) ? rk1 : rk0;
+            for (int v = 0; v < 8; ++v) rank += (cnt[v] < o ? cnt[v] : o) + (v < r && cnt[v] > o ? 1 : 0);
             spos[lane + 64 * i] = rank;
             idxl[k * F_in + (rank & 15) * nst + (rank >> 4)] = f[i];
         }
@@ -857,8 +827,7 @@ __host__ __device__ constexpr int bx_stage_row_bytes(int nlb, int ch) { return 6
 
 template <int F_IN, int NLB>
 __global__ __launch_bounds__((kBxConsumers + kBxProducers) * 64) void k_bwd_x(
-    const int32_t *__restrict__ idx, const bf16_t *__restrict__ WT, const uint8_t *__restrict__ over,
-    const bf16_t *__restrict__ dY, float *__restrict__ part, int B, int Bp, int F_s, int64_t L, int G, int Gp,
+    const int32_t *__restrict__ idx, const bf16_t *__restrict__ WT, const bf16_t *__restrict__ dY, float *__restrict__ part, int B, int Bp, int F_s, int64_t L, int G, int Gp,
     int64_t K, int nbt, int64_t gps, int CH, int AS) {
     extern __shared__ __align__(16) float accs[];  // [F_s][AS], then the staged dY
     constexpr int NST = F_IN / 16;                 // 16-slot tiles
@@ -1063,81 +1032,12 @@ __global__ __launch_bounds__((kBxConsumers + kBxProducers) * 64) void k_bwd_x(
             }
         };
 
-        // Overlapped schedule (every group of the segment keeps the rows it shares with its
-        // predecessor in the late half of its tiles, and NB >= 3 so that the next group's support
-        // is in registers one step early).  Step s: read the early-half accumulator rows of group
-        // s + 1 (no row of group s among them); refill the weight buffer of group s - 1; read the
-        // dY operand of group s + 1; D = dZ_s W_s + old through the matrix core for the early
-        // half (rows read one step ago), then for the late half (read at the end of the previous
-        // step), writing each back; finally read the late-half rows of group s + 1, behind the
-        // write-back in the wave's LDS order.  Only that last read waits on this step's writes.
-        // The remaining groups (all of them without the overlap) take the serial schedule.
-        int n_main = 0;
-        if constexpr (NB >= 3) {
-            uint32_t o = 0;
-            for (int i = lane; i < n; i += 64) o |= over[g_begin + i];
-            n_main = __builtin_amdgcn_readfirstlane(__ballot(o != 0) == 0 ? n / NB * NB : 0);
-        }
         __syncthreads();                                 // chunk 0 staged
         read_dy(ay[0], ylane);
         int s0 = 0;
-        if constexpr (NB >= 3) {
-            if (n_main > 0) {
-                constexpr int NE = NST / 2, NL = NST - NE;   // early / late tiles
-                f32x4_t ae[2][NE], al[NL];
-                uint32_t aoe[2][NE], aol[NL];
-#pragma unroll
-                for (int e = 0; e < NE; ++e) {
-                    aoe[0][e] = acc_addr(tl[0].f[e]);
-                    ae[0][e] = acc_read(aoe[0][e]);
-                }
-#pragma unroll
-                for (int l = 0; l < NL; ++l) {
-                    aol[l] = acc_addr(tl[0].f[NE + l]);
-                    al[l] = acc_read(aol[l]);
-                }
-                for (; s0 < n_main; s0 += NB) {
-                    const char *yit = ylane + ybuf + ic * (NB * GB);   // group s0 of this pass
-#pragma unroll
-                    for (int b = 0; b < NB; ++b) {
-                        const int sg = s0 + b;
-                        const int cur = b & 1, nxt = cur ^ 1, tn = (b + 1) % NB;
-#pragma unroll
-                        for (int e = 0; e < NE; ++e) {
-                            aoe[nxt][e] = acc_addr(tl[tn].f[e]);
-                            ae[nxt][e] = acc_read(aoe[nxt][e]);
-                        }
-                        __builtin_amdgcn_sched_barrier(0);  // early reads first
-                        issue(cl(sg + NB - 1), tl[(b + NB - 1) % NB]);
-                        __builtin_amdgcn_sched_barrier(0);  // keep prefetch order
-                        next_dy(b, s0, yit, ay[(b + 1) & 1]);
-#pragma unroll
-                        for (int e = 0; e < NE; ++e) {
-#pragma unroll
-                            for (int c = 0; c < NLB; ++c)
-                                ae[cur][e] = mfma16x16x32(as_bf16x8(ay[b & 1][c]), as_bf16x8(tl[b].w[c][e]), ae[cur][e]);
-                            acc_write(aoe[cur][e], ae[cur][e]);
-                        }
-#pragma unroll
-                        for (int l = 0; l < NL; ++l) {
-#pragma unroll
-                            for (int c = 0; c < NLB; ++c)
-                                al[l] = mfma16x16x32(as_bf16x8(ay[b & 1][c]), as_bf16x8(tl[b].w[c][NE + l]), al[l]);
-                            acc_write(aol[l], al[l]);
-                        }
-                        __builtin_amdgcn_sched_barrier(0);  // late reads behind the write-back
-#pragma unroll
-                        for (int l = 0; l < NL; ++l) {
-                            aol[l] = acc_addr(tl[tn].f[NE + l]);
-                            al[l] = acc_read(aol[l]);
-                        }
-                    }
-                }
-            }
-        }
-        // Serial schedule.  Step s: read the accumulator rows of group s; refill the buffer group
-        // s - 1 has finished with (the load issue overlaps the LDS reads); read the dY operand of
-        // group s + 1; then D = dZ_s W_s + old through the matrix core and write D back.
+        // Step s: read the accumulator rows of group s; refill the buffer group s - 1 has finished
+        // with (the load issue overlaps the LDS reads); read the dY operand of group s + 1; then
+        // D = dZ_s W_s + old through the matrix core (its accumulator input) and write D back.
         for (; s0 < n_pad; s0 += NB) {
             const char *yit = ylane + ybuf + ic * (NB * GB);   // group s0 of this pass
 #pragma unroll
@@ -1344,8 +1244,8 @@ bool bwd_x_mfma_supported(const TailArgs &a) {
     return g.ch > 0 && g.lds <= kLdsBudget;
 }
 
-// workspace: the per-segment partials, then W^T (group blocks [Gp / 8][F_in][8]), then the supports in lane
-// order, then one overlap flag per group
+// workspace: the per-segment partials, then W^T (group blocks [Gp / 8][F_in][8]), then the supports
+// in lane order
 static size_t bwd_x_part_bytes(const TailArgs &a, const BwdXGeom &g) {
     return round_up((int64_t)g.nseg * a.F_s * (g.nbt * 32) * 4, 256);
 }
@@ -1357,17 +1257,17 @@ static size_t bwd_x_wt_bytes(const TailArgs &a) {
 size_t bwd_x_mfma_ws(const TailArgs &a) {
     const BwdXGeom g = bwd_x_geom(a);
     const int64_t K = a.L / a.G;
-    return bwd_x_part_bytes(a, g) + bwd_x_wt_bytes(a) + (size_t)round_up(K * a.F_in * 4, 256) + (size_t)K + 256;
+    return bwd_x_part_bytes(a, g) + bwd_x_wt_bytes(a) + (size_t)round_up(K * a.F_in * 4, 256) + 256;
 }
 
 template <int F_IN, int NLB>
 static hipError_t launch_bwd_x(const TailArgs &a, const BwdXGeom &g, const int32_t *idx, const bf16_t *WT,
-                               const uint8_t *over, const void *dY, float *part, hipStream_t s) {
+                               const void *dY, float *part, hipStream_t s) {
     auto kern = k_bwd_x<F_IN, NLB>;
     hipError_t e = allow_lds(kern, g.lds);
     if (e != hipSuccess) return e;
     const int64_t K = a.L / a.G;
-    hipLaunchKernelGGL(kern, dim3((unsigned)(g.nseg * g.nbt)), dim3(g.nwaves * 64), g.lds, s, idx, WT, over,
+    hipLaunchKernelGGL(kern, dim3((unsigned)(g.nseg * g.nbt)), dim3(g.nwaves * 64), g.lds, s, idx, WT,
                        (const bf16_t *)dY, part, (int)a.B, g.nbt * 32, (int)a.F_s, a.L, (int)a.G,
                        (int)round_up(a.G, 8), K, g.nbt, g.gps, g.ch, g.as);
     return hipGetLastError();
@@ -1375,12 +1275,12 @@ static hipError_t launch_bwd_x(const TailArgs &a, const BwdXGeom &g, const int32
 
 template <int F_IN>
 static hipError_t launch_bwd_x_g(const TailArgs &a, const BwdXGeom &g, const int32_t *idx, const bf16_t *WT,
-                                 const uint8_t *over, const void *dY, float *part, hipStream_t s) {
+                                 const void *dY, float *part, hipStream_t s) {
     switch ((a.G + 31) / 32) {
-        case 1: return launch_bwd_x<F_IN, 1>(a, g, idx, WT, over, dY, part, s);
-        case 2: return launch_bwd_x<F_IN, 2>(a, g, idx, WT, over, dY, part, s);
-        case 3: return launch_bwd_x<F_IN, 3>(a, g, idx, WT, over, dY, part, s);
-        case 4: return launch_bwd_x<F_IN, 4>(a, g, idx, WT, over, dY, part, s);
+        case 1: return launch_bwd_x<F_IN, 1>(a, g, idx, WT, dY, part, s);
+        case 2: return launch_bwd_x<F_IN, 2>(a, g, idx, WT, dY, part, s);
+        case 3: return launch_bwd_x<F_IN, 3>(a, g, idx, WT, dY, part, s);
+        case 4: return launch_bwd_x<F_IN, 4>(a, g, idx, WT, dY, part, s);
     }
     return hipErrorInvalidValue;
 }
@@ -1392,20 +1292,19 @@ hipError_t bwd_x_mfma(const TailArgs &a, const int32_t *idx, const void *W, cons
     bf16_t *WT = reinterpret_cast<bf16_t *>(reinterpret_cast<char *>(ws) + bwd_x_part_bytes(a, g));
     int32_t *idxl = reinterpret_cast<int32_t *>(reinterpret_cast<char *>(WT) + bwd_x_wt_bytes(a));
     const int64_t K = a.L / a.G;
-    uint8_t *over = reinterpret_cast<uint8_t *>(idxl) + round_up(K * a.F_in * 4, 256);
     const int Gp = (int)round_up(a.G, 8);
     const int64_t tgrid = cdiv(K, kTwWaves) < 4096 ? cdiv(K, kTwWaves) : 4096;
     const size_t tlds = (size_t)kTwWaves * tw_wave_bytes((int)a.F_in, Gp);
     hipError_t e = allow_lds(k_transpose_w, tlds);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(k_transpose_w, dim3((unsigned)tgrid), dim3(kTwWaves * 64), tlds, s, (const bf16_t *)W, idx,
-                       WT, idxl, over, K, (int)a.G, Gp, (int)a.F_in, g.gps);
+                       WT, idxl, K, (int)a.G, Gp, (int)a.F_in);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     switch (a.F_in) {
-        case 32: e = launch_bwd_x_g<32>(a, g, idxl, WT, over, dY, part, s); break;
-        case 64: e = launch_bwd_x_g<64>(a, g, idxl, WT, over, dY, part, s); break;
-        case 128: e = launch_bwd_x_g<128>(a, g, idxl, WT, over, dY, part, s); break;
+        case 32: e = launch_bwd_x_g<32>(a, g, idxl, WT, dY, part, s); break;
+        case 64: e = launch_bwd_x_g<64>(a, g, idxl, WT, dY, part, s); break;
+        case 128: e = launch_bwd_x_g<128>(a, g, idxl, WT, dY, part, s); break;
         default: return hipErrorInvalidValue;
     }
     if (e != hipSuccess) return e;
