@@ -14,26 +14,65 @@ __global__ void k_scale(float *__restrict__ p, int64_t n, float beta) {
 }
 
 // dX[b, f] = beta*dX[b, f] + sum_{s in order} part[s][f][b]; 32x32 tiles transposed through LDS
+// dX[b, f] = beta dX[b, f] + sum_{k < S} part[k][f][b], summed in ascending k.  A workgroup takes
+// 8 features x 128 rows: each thread reads 4 consecutive rows (16 bytes, 512 contiguous bytes per
+// feature and wave) of every partial, with the loads of 8 partials in flight, and the tile is
+// transposed through LDS so that dX is written 16 bytes per thread.
 __global__ __launch_bounds__(256) void k_reduce_fmajor(const float *__restrict__ part, int S, int64_t ldp,
                                                        int64_t B, int64_t F_s, float *__restrict__ dX, int beta) {
-    __shared__ float tile[32][33];
-    const int64_t f0 = (int64_t)blockIdx.x * 32, b0 = (int64_t)blockIdx.y * 32;
-    const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
-    for (int r = ty; r < 32; r += 8) {
-        const int64_t f = f0 + r, b = b0 + tx;
-        float s = 0.0f;
-        if (f < F_s && b < B) {
-            const float *p = part + f * ldp + b;
-            for (int k = 0; k < S; ++k) s += p[(int64_t)k * F_s * ldp];
+    __shared__ float tile[8][128 + 4];
+    const int64_t f0 = (int64_t)blockIdx.x * 8, b0 = (int64_t)blockIdx.y * 128;
+    const int t = threadIdx.x, bq = t & 31, fr = t >> 5;
+    const int64_t f = f0 + fr, b = b0 + 4 * bq;
+    float4 acc = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    if (f < F_s && b < ldp) {
+        const float4 *p = reinterpret_cast<const float4 *>(part + f * ldp + b);
+        const int64_t ks = F_s * ldp / 4;   // float4 stride between partials
+        int k = 0;
+        for (; k + 8 <= S; k += 8) {
+            float4 v[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) v[j] = p[(int64_t)(k + j) * ks];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                acc.x += v[j].x;
+                acc.y += v[j].y;
+                acc.z += v[j].z;
+                acc.w += v[j].w;
+            }
         }
-        tile[r][tx] = s;
+        for (; k < S; ++k) {
+            const float4 v = p[(int64_t)k * ks];
+            acc.x += v.x;
+            acc.y += v.y;
+            acc.z += v.z;
+            acc.w += v.w;
+        }
     }
+    tile[fr][4 * bq + 0] = acc.x;
+    tile[fr][4 * bq + 1] = acc.y;
+    tile[fr][4 * bq + 2] = acc.z;
+    tile[fr][4 * bq + 3] = acc.w;
     __syncthreads();
-    for (int r = ty; r < 32; r += 8) {
-        const int64_t b = b0 + r, f = f0 + tx;
-        if (b < B && f < F_s) {
-            float *q = dX + b * F_s + f;
-            *q = beta ? *q + tile[tx][r] : tile[tx][r];
+    // thread -> row b0 + t / 2, features f0 + 4 (t % 2) .. +3
+    const int64_t ob = b0 + (t >> 1), of = f0 + 4 * (t & 1);
+    if (ob < B) {
+        const int r = t >> 1, c = 4 * (t & 1);
+        float4 s4 = make_float4(tile[c][r], tile[c + 1][r], tile[c + 2][r], tile[c + 3][r]);
+        float *q = dX + ob * F_s + of;
+        if (of + 3 < F_s && ((F_s & 3) == 0)) {
+            if (beta) {
+                const float4 o = *reinterpret_cast<const float4 *>(q);
+                s4.x += o.x;
+                s4.y += o.y;
+                s4.z += o.z;
+                s4.w += o.w;
+            }
+            *reinterpret_cast<float4 *>(q) = s4;
+        } else {
+            const float v[4] = {s4.x, s4.y, s4.z, s4.w};
+            for (int j = 0; j < 4; ++j)
+                if (of + j < F_s) q[j] = beta ? q[j] + v[j] : v[j];
         }
     }
 }
@@ -98,7 +137,7 @@ hipError_t scale_f32(float *p, int64_t n, float beta, hipStream_t s) {
 hipError_t reduce_fmajor(const float *part, int S, int64_t ldp, int64_t B, int64_t F_s, float *dX, int beta,
                          hipStream_t s) {
     if (B <= 0) return hipSuccess;
-    hipLaunchKernelGGL(k_reduce_fmajor, dim3((unsigned)cdiv(F_s, 32), (unsigned)cdiv(B, 32)), dim3(256), 0, s, part,
+    hipLaunchKernelGGL(k_reduce_fmajor, dim3((unsigned)cdiv(F_s, 8), (unsigned)cdiv(B, 128)), dim3(256), 0, s, part,
                        S, ldp, B, F_s, dX, beta);
     return hipGetLastError();
 }
