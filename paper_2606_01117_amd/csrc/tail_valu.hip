@@ -122,44 +122,90 @@ __global__ __launch_bounds__(256) void k_bwd_w_valu(const T *__restrict__ X, con
     }
 }
 
-// Partial dX^T over one label segment and one batch tile: part[seg][f][b0 + b]
+// Partial dX^T over one label segment and one 32-row batch tile: part[seg][f][b0 + b].
+//
+// The accumulator dX^T[F_s][32] (fp32, rows of kOwnAS floats) lives in LDS.  Wave w owns rows
+// 4w .. 4w + 3 of the tile, so no two waves touch the same cell, and within a wave the lanes run
+// over one label's support slots, whose rows are distinct: every update is a plain float4
+// read-add-write in the wave's program order (LDS operations of a wave execute in order), with
+// no atomics, and dX is bit-reproducible.  The supports and weights of a block of LB labels are
+// staged in LDS once per workgroup (LB F_in = 4096), and the wave's dY values for the block are
+// read with one coalesced load per row and handed to the lanes label by label.
+constexpr int kOwnWaves = 8;
+constexpr int kOwnAS = 36;        // accumulator row stride (floats): 32 rows + 4 pad
+
 template <typename T>
-__global__ __launch_bounds__(256) void k_bwd_x_valu(const int32_t *__restrict__ idx, const T *__restrict__ W,
-                                                    const T *__restrict__ dY, float *__restrict__ part, int B,
-                                                    int Bp, int F_s, int64_t L, int G, int F_in, int64_t lps) {
-    extern __shared__ __align__(16) float accs[];  // [F_s][TB]
+__global__ __launch_bounds__(kOwnWaves * 64) void k_bwd_x_valu(const int32_t *__restrict__ idx,
+                                                                const T *__restrict__ W, const T *__restrict__ dY,
+                                                                float *__restrict__ part, int B, int Bp, int F_s,
+                                                                int64_t L, int G, int F_in, int64_t lps) {
+    extern __shared__ __align__(16) float accs[];   // [F_s][kOwnAS], then the staged block
+    const int LB = 4096 / F_in;                      // labels per staged block
+    int *sf = reinterpret_cast<int *>(accs + F_s * kOwnAS);   // [LB][F_in] supports
+    float *sw = reinterpret_cast<float *>(sf + LB * F_in);    // [LB][F_in] weights
     const int64_t seg = blockIdx.x;
-    const int b0 = blockIdx.y * TB;
-    for (int e = threadIdx.x; e < F_s * TB; e += blockDim.x) accs[e] = 0.0f;
-    __syncthreads();
+    const int b0 = blockIdx.y * 32;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int nthr = kOwnWaves * 64;
+    for (int e = tid; e < F_s * kOwnAS; e += nthr) accs[e] = 0.0f;
     const int64_t l_begin = seg * lps;
     const int64_t l_end = l_begin + lps < L ? l_begin + lps : L;
-    for (int64_t l = l_begin + threadIdx.x; l < l_end; l += blockDim.x) {
-        float dy[TB];
+    float *accw = accs + 4 * w;                      // this wave's 4 columns of a row
+    for (int64_t lb = l_begin; lb < l_end; lb += LB) {
+        const int nl = l_end - lb < LB ? (int)(l_end - lb) : LB;
+        __syncthreads();                             // the previous block is no longer read
+        for (int e = tid; e < nl * F_in; e += nthr) {
+            const int j = e / F_in, t = e - j * F_in;
+            const int64_t l = lb + j;
+            sf[e] = idx[(l / G) * F_in + t];
+            sw[e] = load_f32(W, l * F_in + t);
+        }
+        __syncthreads();
+        // dY of this wave's 4 rows for labels lb + 64c + lane (c < LB / 64 chunks of the block)
+        for (int c = 0; c * 64 < nl; ++c) {
+            float dyr[4];
 #pragma unroll
-        for (int b = 0; b < TB; ++b) dy[b] = (b0 + b < B) ? load_f32(dY, (int64_t)(b0 + b) * L + l) : 0.0f;
-        const int64_t g = l / G;
-        for (int t = 0; t < F_in; ++t) {
-            const int f = idx[g * F_in + t];
-            const float w = load_f32(W, l * F_in + t);
-            float *row = accs + f * TB;
+            for (int i = 0; i < 4; ++i) {
+                const int b = b0 + 4 * w + i;
+                const int j = 64 * c + lane;
+                dyr[i] = (b < B && j < nl) ? load_f32(dY, (int64_t)b * L + lb + j) : 0.0f;
+            }
+            const int ncl = nl - 64 * c < 64 ? nl - 64 * c : 64;
+            for (int jj = 0; jj < ncl; ++jj) {
+                const int j = 64 * c + jj;
+                float dy[4];
 #pragma unroll
-            for (int b = 0; b < TB; ++b)
-                __hip_atomic_fetch_add(row + b, dy[b] * w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+                for (int i = 0; i < 4; ++i) dy[i] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(dyr[i]), jj));
+                for (int t = lane; t < F_in; t += 64) {
+                    const int f = sf[j * F_in + t];
+                    const float wv = sw[j * F_in + t];
+                    float4 *p = reinterpret_cast<float4 *>(accw + f * kOwnAS);
+                    float4 v = *p;
+                    v.x = fmaf(dy[0], wv, v.x);
+                    v.y = fmaf(dy[1], wv, v.y);
+                    v.z = fmaf(dy[2], wv, v.z);
+                    v.w = fmaf(dy[3], wv, v.w);
+                    *p = v;
+                }
+            }
         }
     }
     __syncthreads();
     float *pp = part + (size_t)seg * F_s * Bp + b0;
-    for (int e = threadIdx.x; e < F_s * TB; e += blockDim.x) {
-        const int f = e / TB, b = e - f * TB;
-        pp[(size_t)f * Bp + b] = accs[e];
+    for (int e = tid; e < F_s * 32; e += nthr) {
+        const int f = e >> 5, b = e & 31;
+        pp[(size_t)f * Bp + b] = accs[f * kOwnAS + b];
     }
 }
 
+size_t bwd_x_valu_lds(const haste::TailArgs &a) {
+    return (size_t)a.F_s * kOwnAS * 4 + 2 * 4096 * 4;
+}
+
 int64_t bwd_x_valu_segments(const haste::TailArgs &a) {
-    const int64_t nbt = haste::cdiv(a.B, TB);
-    int64_t S = 1024 / (nbt < 1 ? 1 : nbt);
-    const int64_t maxS = haste::cdiv(a.L, 256);
+    const int64_t nbt = haste::cdiv(a.B, 32);
+    int64_t S = 512 / (nbt < 1 ? 1 : nbt);
+    const int64_t maxS = haste::cdiv(a.L, 64);
     if (S > maxS) S = maxS;
     return S < 1 ? 1 : S;
 }
@@ -169,7 +215,7 @@ int64_t bwd_x_valu_segments(const haste::TailArgs &a) {
 namespace haste {
 
 bool valu_supported(const TailArgs &a) {
-    return a.F_s <= kMaxFs && (size_t)a.F_s * XS * 4 <= 150 * 1024;
+    return a.F_s <= kMaxFs && (size_t)a.F_s * XS * 4 <= 150 * 1024 && bwd_x_valu_lds(a) <= 160 * 1024;
 }
 
 hipError_t fwd_valu(const TailArgs &a, const void *X, const int32_t *idx, const void *W, const float *bias,
@@ -211,26 +257,26 @@ hipError_t bwd_w_valu(const TailArgs &a, const void *X, const int32_t *idx, cons
 
 size_t bwd_x_valu_ws(const TailArgs &a) {
     const int64_t S = bwd_x_valu_segments(a);
-    return (size_t)S * (size_t)a.F_s * (size_t)(cdiv(a.B, TB) * TB) * 4 + 256;
+    return (size_t)S * (size_t)a.F_s * (size_t)(cdiv(a.B, 32) * 32) * 4 + 256;
 }
 
 hipError_t bwd_x_valu(const TailArgs &a, const int32_t *idx, const void *W, const void *dY, float *dX, int beta,
                       void *ws, hipStream_t s) {
-    const int64_t nbt = cdiv(a.B, TB);
+    const int64_t nbt = cdiv(a.B, 32);
     const int64_t S = bwd_x_valu_segments(a);
     const int64_t lps = cdiv(a.L, S);
-    const int Bp = (int)(nbt * TB);
-    const size_t lds = (size_t)a.F_s * TB * 4;
+    const int Bp = (int)(nbt * 32);
+    const size_t lds = bwd_x_valu_lds(a);
     float *part = reinterpret_cast<float *>(ws);
     const dim3 grid((unsigned)S, (unsigned)nbt);
     if (a.dtype == HASTE_DTYPE_F32) {
         hipFuncSetAttribute((const void *)k_bwd_x_valu<float>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        hipLaunchKernelGGL(k_bwd_x_valu<float>, grid, dim3(256), lds, s, idx, (const float *)W, (const float *)dY, part,
-                           (int)a.B, Bp, (int)a.F_s, a.L, (int)a.G, (int)a.F_in, lps);
+        hipLaunchKernelGGL(k_bwd_x_valu<float>, grid, dim3(kOwnWaves * 64), lds, s, idx, (const float *)W,
+                           (const float *)dY, part, (int)a.B, Bp, (int)a.F_s, a.L, (int)a.G, (int)a.F_in, lps);
     } else {
         hipFuncSetAttribute((const void *)k_bwd_x_valu<bf16_t>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        hipLaunchKernelGGL(k_bwd_x_valu<bf16_t>, grid, dim3(256), lds, s, idx, (const bf16_t *)W, (const bf16_t *)dY,
-                           part, (int)a.B, Bp, (int)a.F_s, a.L, (int)a.G, (int)a.F_in, lps);
+        hipLaunchKernelGGL(k_bwd_x_valu<bf16_t>, grid, dim3(kOwnWaves * 64), lds, s, idx, (const bf16_t *)W,
+                           (const bf16_t *)dY, part, (int)a.B, Bp, (int)a.F_s, a.L, (int)a.G, (int)a.F_in, lps);
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
