@@ -243,30 +243,41 @@ __global__ __launch_bounds__(512) void k_fwd(const bf16_t *__restrict__ X, const
             pyb.st8<kStreaming>(sv[i], off);
     };
 
-    // Two units in flight per wave in ping-pong buffers (no register copies).  A wave takes two
-    // consecutive 32-label tiles at a time and stores them together, so each 128-byte line of a
-    // Y row is written whole.  Prefetches are issued unconditionally (the index is clamped to
-    // the last unit) so that every wait only covers the loads it needs.  A pair's output is held
-    // in registers and its stores are spread over the next pair's products, so that loads and
-    // stores share the memory pipeline evenly; on gfx9 one in-order counter covers vector loads
-    // and stores, and the stores always follow the prefetches the next waits need.
-    Unit ua, ub;
+    // A wave takes two consecutive 32-label tiles (a pair) at a time and stores them together, so
+    // each 128-byte line of a Y row is written whole.  A pair's output is held in registers and
+    // its stores are spread over the next pair's products, so that loads and stores share the
+    // memory pipeline evenly.  On gfx9 one in-order counter covers vector loads and stores, so a
+    // wait for a pair's weights also waits for every store issued before them: the weights are
+    // therefore prefetched two pairs ahead (two pairs of unit buffers, used alternately with no
+    // register copies), which leaves the stores a whole pair's products to complete.  Prefetches
+    // are issued unconditionally (the index is clamped to the last unit) so that every wait only
+    // covers the loads it needs.  Where the registers do not hold four units (128-slot supports,
+    // or a bias with 8-byte stores) the weights are prefetched one pair ahead.
+    constexpr bool DEEP = F_IN <= 64 && (WIDE || !HAS_BIAS);
+    Unit ua0, ub0, ua1, ub1;
     SV sv[NS];
     const int64_t st = 2 * nwaves;
     const int64_t last = u_end - 1;
     auto cl = [&](int64_t v) { return v < last ? v : last; };
     int64_t u = u_begin + 2 * wave;
     if (u > last) return;
-    issue(u, ua);
+    issue(u, ua0);
     __builtin_amdgcn_sched_barrier(0);  // keep prefetch order
-    issue(cl(u + 1), ub);
+    issue(cl(u + 1), ub0);
     __builtin_amdgcn_sched_barrier(0);  // keep prefetch order
-    for (; u <= last; u += st) {
+    if constexpr (DEEP) {
+        issue(cl(u + st), ua1);
+        __builtin_amdgcn_sched_barrier(0);  // keep prefetch order
+        issue(cl(u + st + 1), ub1);
+        __builtin_amdgcn_sched_barrier(0);  // keep prefetch order
+    }
+    // the pair starting at unit v from buffers (ua, ub), which then take the pair `ahead` units on
+    auto step = [&](int64_t v, Unit &ua, Unit &ub, int64_t ahead) {
         int64_t lab0, lab1;
         int na, nb;
-        unit_labels(u, lab0, na);
-        unit_labels(cl(u + 1), lab1, nb);
-        const int width = na + (u + 1 <= last ? nb : 0);
+        unit_labels(v, lab0, na);
+        unit_labels(cl(v + 1), lab1, nb);
+        const int width = na + (v + 1 <= last ? nb : 0);
         f32x16_t acc_a[NT], acc_b[NT];
         compute(ua, acc_a, [&](int i) { if (i < NS) store_one(i, sv); });
         __builtin_amdgcn_sched_barrier(0);
@@ -275,10 +286,10 @@ __global__ __launch_bounds__(512) void k_fwd(const bf16_t *__restrict__ X, const
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int i = 2 * KS * NT; i < NS; ++i) store_one(i, sv);
-        // both units' registers are free once their products are done: prefetch the next pair
-        issue(cl(u + st), ua);
+        // both units' registers are free once their products are done
+        issue(cl(v + ahead), ua);
         __builtin_amdgcn_sched_barrier(0);  // keep prefetch order
-        issue(cl(u + st + 1), ub);
+        issue(cl(v + ahead + 1), ub);
         __builtin_amdgcn_sched_barrier(0);  // keep prefetch order
 #pragma unroll
         for (int n = 0; n < NT; ++n) {
@@ -287,6 +298,16 @@ __global__ __launch_bounds__(512) void k_fwd(const bf16_t *__restrict__ X, const
             unstage(n, sv);
         }
         set_pair(lab0, width);
+    };
+    if constexpr (DEEP) {
+        // whole double steps (no exit between the halves), then a last single step
+        for (; u + st <= last; u += 2 * st) {
+            step(u, ua0, ub0, 2 * st);
+            step(u + st, ua1, ub1, 2 * st);
+        }
+        if (u <= last) step(u, ua0, ub0, 2 * st);
+    } else {
+        for (; u <= last; u += st) step(u, ua0, ub0, st);
     }
 #pragma unroll
     for (int i = 0; i < NS; ++i) store_one(i, sv);
