@@ -66,21 +66,6 @@ __device__ __forceinline__ uint4 pack8(const f32x16_t &d, int r0) {
                       pack_bf16(d[r0 + 4], d[r0 + 5]), pack_bf16(d[r0 + 6], d[r0 + 7]));
 }
 
-// Transposing through the matrix core.  With A = a 32x16 block in its natural layout (lane
-// (m = l%32, h = l/32) holds row m, columns 8h..8h+7) and B = the identity slice
-// E_off[k][n] = (n == off + k), D = A*E_0 + A'*E_16 is the 32x32 block itself, but in the MFMA
-// result layout, where lane (n, h) holds column n for rows 8i + 4h + j.  Each output is a single
-// product x*1 accumulated onto zeros, so the copy is exact for finite inputs.
-__device__ __forceinline__ bf16x8_t eye_operand(int ln, int hh, int off) {
-    uint32_t w[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-        const int k = off + 8 * hh + 2 * q;
-        w[q] = (ln == k ? 0x3F80u : 0u) | (ln == k + 1 ? 0x3F800000u : 0u);
-    }
-    return as_bf16x8(make_uint4(w[0], w[1], w[2], w[3]));
-}
-
 // Bounds-checked buffer access (raw buffer resource, stride 0).  Loads at byte offsets at or past
 // `bytes` return zero and stores there are dropped by the hardware, so masked lanes simply use
 // kOob: no branch around the memory instruction, which keeps the count of outstanding memory
@@ -155,7 +140,6 @@ hipError_t head_bwd(int64_t B, int64_t F_s, int64_t H, int32_t dtype, const void
 
 // utilities
 hipError_t fill_f32(float *p, int64_t n, float v, hipStream_t s);
-hipError_t scale_f32(float *p, int64_t n, float beta, hipStream_t s);
 // dX[b, f] = beta*dX[b, f] + sum_s part[s][f][b]   (part is [S][F_s][ldp], feature-major)
 hipError_t reduce_fmajor(const float *part, int S, int64_t ldp, int64_t B, int64_t F_s, float *dX, int beta,
                          hipStream_t s);

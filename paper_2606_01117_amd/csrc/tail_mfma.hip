@@ -313,25 +313,6 @@ __global__ __launch_bounds__(512) void k_fwd(const bf16_t *__restrict__ X, const
     for (int i = 0; i < NS; ++i) store_one(i, sv);
 }
 
-// --------------------------------------------------------------------------------------------
-// Backward-weight.  dW_k = dZ_k^T H_k is formed on the support slots only, one wave per
-// (group, 32-label tile) unit, contracting over the whole batch in 32-row blocks
-// (v_mfma_f32_16x16x32_bf16, M = 16 labels, N = 16 slots, K = the block's 32 batch rows).
-//
-// The 4 waves of a workgroup take 4 consecutive units, i.e. a contiguous span of at most 128
-// labels.  Each 32-row block of dY over that span is loaded cooperatively, two 256-byte row
-// segments per load instruction, and staged in LDS (double buffered, one barrier per block):
-// loading each unit's 32x32 block straight into registers would touch 32 rows per instruction,
-// and such loads are limited by address translation rather than by HBM.
-//
-// A operand (labels x rows): a wave reads its block from LDS in the natural layout (lane = row,
-// 8 labels) and transposes it through the matrix core (identity operand, exact), feeding the
-// rows in an order that leaves each lane with 8 consecutive batch rows.
-// B operand (rows x slots): those 8 batch rows of X^T (staged block by block by k_transpose_x)
-// at the slot's feature, one 16-byte load; the 4 lanes of a slot read its 64 contiguous bytes.
-// A tile's 16 slots are consecutive in the sorted support, so one load instruction stays within
-// a few pages of the block (gathers spread over many pages are limited by address translation).
-// --------------------------------------------------------------------------------------------
 // X [B][F_s] -> Xb [Bp/32][F_s][32]: X^T in 32-row batch blocks (rows past B zero).  Within a
 // block, the 64-byte rows of nearby features are adjacent, so a gather over a tile's sorted
 // support stays within a few pages.
@@ -352,190 +333,8 @@ __global__ __launch_bounds__(256) void k_transpose_x(const bf16_t *__restrict__ 
     }
 }
 
-constexpr int kBwUnits = 4;                   // units (waves) per workgroup
-constexpr int kBwRowBytes = kBwUnits * 64;    // staged dY per row and block (32 labels per unit)
-constexpr int kBwLanesPerRow = kBwRowBytes / 8;
-
-// Staged dY layout: [2 buffers][32 rows][kBwRowBytes / 8 units of 8 bytes]; unit u of row r sits
-// at position u ^ (r % 16), so that 16 rows read at the same label fall in distinct banks while
-// each cooperative store still writes whole rows.
-__device__ __forceinline__ int bw_swz(int u, int r) { return (u & (kBwLanesPerRow - 1)) ^ (r & 15); }
-
 __device__ __forceinline__ f32x4_t mfma16x16x32(const bf16x8_t &a, const bf16x8_t &b, const f32x4_t &c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
-}
-
-// Identity slice for the 16x16x32 transpose: B[k][n] = (k == 16s + n); lane (n = l%16, q = l/16)
-// holds k = 8q..8q+7.  With A = 16 rows x 32 columns in the natural layout, A*B is columns
-// 16s..16s+15 of A in the result layout, where lane (n, q) holds rows 4q..4q+3 of column 16s + n.
-__device__ __forceinline__ bf16x8_t eye16_operand(int l16, int q, int s) {
-    uint32_t w[4];
-    const int col = 16 * s + l16;
-#pragma unroll
-    for (int p = 0; p < 4; ++p) {
-        const int k = 8 * q + 2 * p;
-        w[p] = (col == k ? 0x3F80u : 0u) | (col == k + 1 ? 0x3F800000u : 0u);
-    }
-    return as_bf16x8(make_uint4(w[0], w[1], w[2], w[3]));
-}
-
-template <int F_IN>
-__global__ __launch_bounds__(kBwUnits * 64) void k_bwd_w(const bf16_t *__restrict__ Xb, const int32_t *__restrict__ idx,
-                                                         const bf16_t *__restrict__ dY, float *__restrict__ dW,
-                                                         float *__restrict__ dbias, int beta, int B, int Bp, int F_s,
-                                                         int64_t L, int G, int64_t K) {
-    __shared__ __align__(16) char ys[2 * 32 * kBwRowBytes];
-    constexpr int NST = F_IN / 16;            // 16-slot N-tiles
-    constexpr int RPI = 64 / kBwLanesPerRow;  // dY rows per staging load instruction
-    constexpr int NSL = 32 / (RPI * kBwUnits); // staging loads per wave and block
-    const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int l16 = lane & 15, q = lane >> 4;
-    const int mtiles = (G + 31) >> 5;
-    const int64_t nunits = K * mtiles;
-    const int64_t u0 = (int64_t)blockIdx.x * kBwUnits;
-    const int64_t ulast = u0 + kBwUnits - 1 < nunits ? u0 + kBwUnits - 1 : nunits - 1;
-    // label span of the workgroup's units
-    const int64_t kf = u0 / mtiles, kl = ulast / mtiles;
-    const int64_t span0 = kf * G + 32 * (u0 - kf * mtiles);
-    const int mtl = (int)(ulast - kl * mtiles);
-    const int64_t span_end = kl * G + (32 * (mtl + 1) < G ? 32 * (mtl + 1) : G);
-    const int span_bytes = (int)(span_end - span0) * 2;
-    // this wave's unit (waves past the last unit repeat it and write nothing)
-    const bool active = u0 + wave <= ulast;
-    const int64_t unit = active ? u0 + wave : ulast;
-    const int64_t k = unit / mtiles;
-    const int mt = (int)(unit - k * mtiles);
-    const int c0 = mt * 32;                  // first label of the tile within the group
-    const int64_t lab0 = k * G + c0;
-    const int cu = (int)(lab0 - span0) / 4;  // 8-byte unit of the tile's first label in a staged row
-
-    // X^T rows b0 + 8q .. +7 at the feature of slot 16nt + l16 (offsets within a block)
-    const bf16_t *xrow[NST];
-#pragma unroll
-    for (int nt = 0; nt < NST; ++nt) xrow[nt] = Xb + (int64_t)idx[k * F_IN + 16 * nt + l16] * 32 + 8 * q;
-    // natural-layout dY of this lane: labels c0 + 8q .. +3 and +4 .. +7; past G read as zero
-    const bool lab_ok0 = c0 + 8 * q < G, lab_ok1 = c0 + 8 * q + 4 < G;
-
-    // cooperative dY staging: load instruction i of this wave covers rows RPI * (wave + 4i) ..
-    const int su = lane % kBwLanesPerRow;   // 8-byte unit of a staged row
-    const int sr = lane / kBwLanesPerRow;   // row within the instruction's rows
-    const bool col_ok = 8 * su < span_bytes;
-    auto load_dy = [&](int b0, uint2 (&yv)[NSL]) {
-        // rows past B (a whole block past the batch, too) and bytes past the end of dY read as zero
-        const int rows = B - b0 < 32 ? (B - b0 > 0 ? B - b0 : 0) : 32;
-        const int64_t nbytes = rows > 0 ? ((int64_t)rows * L - span0) * 2 : 0;
-        const Buf db(dY + (int64_t)b0 * L + span0, (uint32_t)nbytes);
-#pragma unroll
-        for (int i = 0; i < NSL; ++i) {
-            const int r = RPI * (wave + kBwUnits * i) + sr;
-            yv[i] = db.ld8(col_ok ? (uint32_t)((int64_t)r * L * 2) + 8 * su : kOob);
-        }
-    };
-    auto store_dy = [&](int buf, const uint2 (&yv)[NSL]) {
-#pragma unroll
-        for (int i = 0; i < NSL; ++i) {
-            const int r = RPI * (wave + kBwUnits * i) + sr;
-            *reinterpret_cast<uint2 *>(ys + (buf * 32 + r) * kBwRowBytes + bw_swz(su, r) * 8) = yv[i];
-        }
-    };
-    // blocks past the batch re-read the last block of X^T; their dY is zero
-    auto load_x = [&](int b0, uint4 (&x)[NST]) {
-        const int64_t bo = (int64_t)((b0 < Bp ? b0 : Bp - 32) / 32) * F_s * 32;
-#pragma unroll
-        for (int nt = 0; nt < NST; ++nt) x[nt] = *reinterpret_cast<const uint4 *>(xrow[nt] + bo);
-    };
-
-    const bf16x8_t e0 = eye16_operand(l16, q, 0), e1 = eye16_operand(l16, q, 1);
-    f32x4_t acc[2][NST];
-#pragma unroll
-    for (int h = 0; h < 2; ++h)
-#pragma unroll
-        for (int nt = 0; nt < NST; ++nt) acc[h][nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    float dsum[2] = {0.0f, 0.0f};
-
-    auto compute = [&](int buf, const uint4 (&x)[NST]) {
-        // Transposes: for row set t, lane (m = l16, q) supplies block row 8(m/4) + 4t + m%4, labels
-        // 8q .. 8q+7; the result for label half h gives lane (label 16h + l16, q) the rows
-        // 8q + 4t .. +3.  Together: 8 consecutive block rows per lane, K-slot 8q + p <-> row 8q + p.
-        f32x4_t d[2][2];  // [t][h]
-#pragma unroll
-        for (int t = 0; t < 2; ++t) {
-            const int rr = 8 * (l16 >> 2) + 4 * t + (l16 & 3);
-            const char *row = ys + (buf * 32 + rr) * kBwRowBytes;
-            uint2 y0 = *reinterpret_cast<const uint2 *>(row + bw_swz(cu + 2 * q, rr) * 8);
-            uint2 y1 = *reinterpret_cast<const uint2 *>(row + bw_swz(cu + 2 * q + 1, rr) * 8);
-            if (!lab_ok0) y0 = make_uint2(0u, 0u);
-            if (!lab_ok1) y1 = make_uint2(0u, 0u);
-            const bf16x8_t a = as_bf16x8(make_uint4(y0.x, y0.y, y1.x, y1.y));
-            d[t][0] = mfma16x16x32(a, e0, f32x4_t{0.f, 0.f, 0.f, 0.f});
-            d[t][1] = mfma16x16x32(a, e1, f32x4_t{0.f, 0.f, 0.f, 0.f});
-        }
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            if (dbias) dsum[h] += (d[0][h][0] + d[0][h][1]) + (d[0][h][2] + d[0][h][3]) +
-                                  (d[1][h][0] + d[1][h][1]) + (d[1][h][2] + d[1][h][3]);
-            const bf16x8_t a = as_bf16x8(make_uint4(pack_bf16(d[0][h][0], d[0][h][1]), pack_bf16(d[0][h][2], d[0][h][3]),
-                                                    pack_bf16(d[1][h][0], d[1][h][1]), pack_bf16(d[1][h][2], d[1][h][3])));
-#pragma unroll
-            for (int nt = 0; nt < NST; ++nt) acc[h][nt] = mfma16x16x32(a, as_bf16x8(x[nt]), acc[h][nt]);
-        }
-    };
-
-    // Block j: compute from LDS buffer j % 2 with X^T set j % 2; stage block j + 1 (loaded two
-    // blocks ago, dY set (j + 1) % 2) into the other buffer; load dY of block j + 3 into the set
-    // just staged and X^T of block j + 2 into the set just used; barrier.  The block count is
-    // rounded up to even so that the loop body has no branch around a load (a block past the
-    // batch is zero).
-    uint4 xa[NST], xb[NST];
-    uint2 ya[NSL], yb[NSL];
-    load_dy(0, ya);
-    load_x(0, xa);
-    load_dy(32, yb);
-    load_x(32, xb);
-    store_dy(0, ya);
-    load_dy(64, ya);
-    __builtin_amdgcn_sched_barrier(0);  // keep prefetch order
-    __syncthreads();
-    for (int b0 = 0; b0 < Bp; b0 += 64) {
-        compute(0, xa);
-        store_dy(1, yb);
-        load_dy(b0 + 96, yb);
-        load_x(b0 + 64, xa);
-        __builtin_amdgcn_sched_barrier(0);  // keep prefetch order
-        __syncthreads();
-        compute(1, xb);
-        store_dy(0, ya);
-        load_dy(b0 + 128, ya);
-        load_x(b0 + 96, xb);
-        __builtin_amdgcn_sched_barrier(0);  // keep prefetch order
-        __syncthreads();
-    }
-    if (!active) return;
-    // D[m = label 16h + 4q + j][n = slot 16nt + l16]
-#pragma unroll
-    for (int h = 0; h < 2; ++h)
-#pragma unroll
-        for (int nt = 0; nt < NST; ++nt)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int m = 16 * h + 4 * q + j;
-                if (c0 + m < G) {
-                    float *p = dW + (lab0 + m) * F_IN + 16 * nt + l16;
-                    const float v = acc[h][nt][j];
-                    *p = beta ? *p + v : v;
-                }
-            }
-    if (dbias) {
-        // lanes (l16, q) hold the row sums of label 16h + l16 over rows 8q .. 8q+7 of every block
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            float v = dsum[h];
-            v += __shfl_xor(v, 16);
-            v += __shfl_xor(v, 32);
-            if (q == 0 && c0 + 16 * h + l16 < G)
-                dbias[lab0 + 16 * h + l16] = beta ? dbias[lab0 + 16 * h + l16] + v : v;
-        }
-    }
 }
 
 // --------------------------------------------------------------------------------------------
@@ -1236,24 +1035,7 @@ hipError_t bwd_w_mfma(const TailArgs &a, const void *X, const int32_t *idx, cons
             default: break;
         }
     }
-    const dim3 grid((unsigned)cdiv(units, kBwUnits));
-    const dim3 block(kBwUnits * 64);
-    switch (a.F_in) {
-        case 32:
-            hipLaunchKernelGGL(k_bwd_w<32>, grid, block, 0, s, Xb, idx, (const bf16_t *)dY, dW, dbias, beta,
-                               (int)a.B, Bp, (int)a.F_s, a.L, (int)a.G, K);
-            break;
-        case 64:
-            hipLaunchKernelGGL(k_bwd_w<64>, grid, block, 0, s, Xb, idx, (const bf16_t *)dY, dW, dbias, beta,
-                               (int)a.B, Bp, (int)a.F_s, a.L, (int)a.G, K);
-            break;
-        case 128:
-            hipLaunchKernelGGL(k_bwd_w<128>, grid, block, 0, s, Xb, idx, (const bf16_t *)dY, dW, dbias, beta,
-                               (int)a.B, Bp, (int)a.F_s, a.L, (int)a.G, K);
-            break;
-        default: return hipErrorInvalidValue;
-    }
-    return hipGetLastError();
+    return hipErrorInvalidValue;
 }
 
 // ---- backward-feature ---------------------------------------------------------------------------

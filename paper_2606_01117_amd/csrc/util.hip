@@ -8,12 +8,6 @@ __global__ void k_fill(float *__restrict__ p, int64_t n, float v) {
         p[i] = v;
 }
 
-__global__ void k_scale(float *__restrict__ p, int64_t n, float beta) {
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
-        p[i] *= beta;
-}
-
-// dX[b, f] = beta*dX[b, f] + sum_{s in order} part[s][f][b]; 32x32 tiles transposed through LDS
 // dX[b, f] = beta dX[b, f] + sum_{k < S} part[k][f][b], summed in ascending k.  A workgroup takes
 // 8 features x 128 rows: each thread reads 4 consecutive rows (16 bytes, 512 contiguous bytes per
 // feature and wave) of every partial, with the loads of 8 partials in flight, and the tile is
@@ -125,12 +119,6 @@ namespace haste {
 hipError_t fill_f32(float *p, int64_t n, float v, hipStream_t s) {
     if (n <= 0) return hipSuccess;
     hipLaunchKernelGGL(k_fill, dim3(grid_for(n)), dim3(256), 0, s, p, n, v);
-    return hipGetLastError();
-}
-
-hipError_t scale_f32(float *p, int64_t n, float beta, hipStream_t s) {
-    if (n <= 0) return hipSuccess;
-    hipLaunchKernelGGL(k_scale, dim3(grid_for(n)), dim3(256), 0, s, p, n, beta);
     return hipGetLastError();
 }
 
