@@ -357,7 +357,12 @@ constexpr int kBw2XRow = 80;                    // bytes per staged X^T feature 
 constexpr int kBw2YRow = 1056;                  // bytes per staged dY row: 512 labels + 16 pad
 constexpr int kBw2MaxXLoads = kMaxFs * 4 / (kBw2Waves * 64);   // 16-byte X^T loads per thread and slab
 
-static size_t bw2_lds(int F_s) { return (size_t)haste::round_up((int64_t)F_s * kBw2XRow, 16) + 32 * kBw2YRow; }
+// the staged slabs, or at the end the per-wave dW staging ([32 labels][F_in + 4] fp32 per wave)
+static size_t bw2_lds(int F_s, int F_in) {
+    const size_t slabs = (size_t)haste::round_up((int64_t)F_s * kBw2XRow, 16) + 32 * kBw2YRow;
+    const size_t out = (size_t)kBw2Waves * 32 * (F_in + 4) * 4;
+    return slabs > out ? slabs : out;
+}
 
 template <int F_IN>
 __global__ __launch_bounds__(512) void k_bwd_w2(const bf16_t *__restrict__ Xb, const int32_t *__restrict__ idx,
@@ -477,25 +482,40 @@ __global__ __launch_bounds__(512) void k_bwd_w2(const bf16_t *__restrict__ Xb, c
         }
     }
 
-    // dW[label][16 st + 4q .. +3] for label 16 lt + l16 of each unit; dbias from the q = 0 lanes
+    // dW: a unit's block [32 labels][F_IN] fp32 is contiguous in dW, so each wave stages its
+    // unit's products (lane (label 16 lt + l16, q) holds slots 16 st + 4q .. +3) in its own LDS
+    // region and writes the block back as whole 1 KB runs (streaming stores; labels past the unit
+    // are not written).  dbias from the q = 0 lanes.
+    __syncthreads();   // every wave is done with the staged slabs
+    constexpr int OS = F_IN + 4;                       // staged row stride (floats)
+    float *ostg = reinterpret_cast<float *>(bw2s) + wave * 32 * OS;
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
         const int64_t lb = lab_of(vu[j]);
 #pragma unroll
-        for (int lt = 0; lt < 2; ++lt) {
-            const int t = 16 * lt + l16;
-            if (t >= nl[j]) continue;
-            float *row = dW + (lb + t) * F_IN + 4 * q;
+        for (int lt = 0; lt < 2; ++lt)
 #pragma unroll
-            for (int st = 0; st < NST; ++st) {
-                float4 v = make_float4(acc[j][st][lt][0], acc[j][st][lt][1], acc[j][st][lt][2], acc[j][st][lt][3]);
-                if (beta) {
-                    const float4 o = *reinterpret_cast<const float4 *>(row + 16 * st);
-                    v.x += o.x; v.y += o.y; v.z += o.z; v.w += o.w;
-                }
-                *reinterpret_cast<float4 *>(row + 16 * st) = v;
+            for (int st = 0; st < NST; ++st)
+                *reinterpret_cast<float4 *>(ostg + (16 * lt + l16) * OS + 16 * st + 4 * q) =
+                    make_float4(acc[j][st][lt][0], acc[j][st][lt][1], acc[j][st][lt][2], acc[j][st][lt][3]);
+        const Buf ob(dW + lb * F_IN, (uint32_t)(nl[j] * F_IN * 4));   // this unit's labels only
+#pragma unroll
+        for (int i = 0; i < F_IN / 8; ++i) {
+            const int e = 64 * i + lane;                   // float4 e of the block
+            const int r = e / (F_IN / 4), c = (e % (F_IN / 4)) * 4;
+            float4 v = *reinterpret_cast<const float4 *>(ostg + r * OS + c);
+            if (beta) {
+                const float4 o = __builtin_bit_cast(float4, ob.ld16((uint32_t)(e * 16)));
+                v.x += o.x; v.y += o.y; v.z += o.z; v.w += o.w;
             }
-            if (dbias && q == 0) dbias[lb + t] = (beta ? dbias[lb + t] : 0.0f) + db[j][lt][0];
+            ob.st16<kStreaming>(__builtin_bit_cast(uint4, v), (uint32_t)(e * 16));
+        }
+        if (dbias && q == 0) {
+#pragma unroll
+            for (int lt = 0; lt < 2; ++lt) {
+                const int t = 16 * lt + l16;
+                if (t < nl[j]) dbias[lb + t] = (beta ? dbias[lb + t] : 0.0f) + db[j][lt][0];
+            }
         }
     }
 }
@@ -1019,7 +1039,7 @@ hipError_t bwd_w_mfma(const TailArgs &a, const void *X, const int32_t *idx, cons
     const int64_t K = a.L / a.G;
     const int64_t units = K * cdiv(a.G, 32);
     {
-        const size_t lds = bw2_lds((int)a.F_s);
+        const size_t lds = bw2_lds((int)a.F_s, (int)a.F_in);
         const dim3 grid2((unsigned)cdiv(units, kBw2Units));
         auto launch2 = [&](auto kern) {
             hipError_t e2 = allow_lds(kern, lds);
