@@ -27,7 +27,7 @@ DT_BF16 = 1
 
 def build(src: str = SRC, out: str = LIB, extra: tuple = ()) -> str:
     """Compile the oracle with gcc (-O2, no fast-math: fp64 sums keep the written order)."""
-    cmd = ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c99", *extra, src, "-o", out + ".tmp"]
+    cmd = ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c99", *extra, src, "-o", out + ".tmp", "-lm"]
     subprocess.run(cmd, check=True)
     os.replace(out + ".tmp", out)
     return out
@@ -59,7 +59,10 @@ class Oracle:
         L.haste_oracle_head_fwd.argtypes = sig_head + [_P, _P, _P, _I64, _I64, _P]
         L.haste_oracle_head_bwd_w.argtypes = sig_head + [_P, _P, _I64, _I64, _P]
         L.haste_oracle_head_bwd_x.argtypes = sig_head + [_P, _P, _I64, _I64, _P]
-        for f in ("fwd", "fwd_at", "bwd_w", "bwd_x", "head_fwd", "head_bwd_w", "head_bwd_x"):
+        L.haste_oracle_bce_grad.argtypes = [_I64, _I64, _P, _P, _I64, _P]
+        L.haste_oracle_bce_grad_at.argtypes = [_I64, _I64, _P, _I64, _I64, _P, _P, _P, _P]
+        for f in ("fwd", "fwd_at", "bwd_w", "bwd_x", "head_fwd", "head_bwd_w", "head_bwd_x", "bce_grad",
+                  "bce_grad_at"):
             getattr(L, "haste_oracle_" + f).restype = ctypes.c_int
 
     # ---- helpers --------------------------------------------------------------------------
@@ -126,6 +129,29 @@ class Oracle:
                                          _ptr(dW), _ptr(db))
         self._check(rc, "bwd_w")
         return dW, db
+
+    def bce_grad(self, Z, pos):
+        """dY[B, N] = sigmoid(Z) - T (fp64); T[b, n] = 1 where n occurs in pos[b, :] (pos [B, P] int32)."""
+        Z = np.ascontiguousarray(Z, dtype=np.float64)
+        B, N = Z.shape
+        pos = np.ascontiguousarray(pos, dtype=np.int32).reshape(B, -1)
+        out = np.empty_like(Z)
+        rc = self.lib.haste_oracle_bce_grad(B, N, _ptr(Z), _ptr(pos), pos.shape[1], _ptr(out))
+        self._check(rc, "bce_grad")
+        return out
+
+    def bce_grad_at(self, pos, N, bs, ns, z):
+        """The BCE gradient at points (bs[i], ns[i]) whose logits are z[i]."""
+        pos = np.ascontiguousarray(pos, dtype=np.int32)
+        B = pos.shape[0]
+        bs = np.ascontiguousarray(bs, dtype=np.int64)
+        ns = np.ascontiguousarray(ns, dtype=np.int64)
+        z = np.ascontiguousarray(z, dtype=np.float64)
+        out = np.empty(bs.size, dtype=np.float64)
+        rc = self.lib.haste_oracle_bce_grad_at(B, N, _ptr(pos), pos.shape[1] if pos.ndim == 2 else 0, bs.size,
+                                               _ptr(bs), _ptr(ns), _ptr(z), _ptr(out))
+        self._check(rc, "bce_grad_at")
+        return out
 
     def bwd_x(self, idx, W, dY, G, F_s, dtype, b0=0, b1=None):
         """dX[b1-b0, F_s] in fp64 for rows [b0, b1)."""

@@ -14,6 +14,7 @@
  *   - dW      grad W_k = (grad Z_k)^T H_k,  H_k = h_{:, I_k}     (Section 3.2, backward-weight)
  *   - dX      grad h_{:, I_k} += grad Z_k W_k, summed over k     (Section 3.2, backward-feature)
  *   - head    a^H = W_head h_head                                (Section 3.3)
+ *   - BCE     d/dz of the binary cross-entropy of sigmoid(z)      (Section 3.3 objective)
  *
  * Arithmetic: inputs are decoded exactly to double (bf16 -> fp64 and fp32 -> fp64 are exact);
  * every sum is accumulated in double in the order the definition states (no blocking, no
@@ -22,6 +23,7 @@
  * Parity pins: see the tests (brute-force dense zero-masked matrix, worked Fig. 2 instances,
  * special cases, finite differences, adjoint identity, one-hot gathers).
  */
+#include <math.h>
 #include <stdint.h>
 #include <string.h>
 #include <omp.h>
@@ -189,5 +191,45 @@ int haste_oracle_head_bwd_x(int64_t B, int64_t F_s, int64_t H, int dtype, const 
             for (int64_t h = 0; h < H; ++h) s += ld(dYh, b * H + h, dtype) * ld(Wh, h * F_s + f, dtype);
             dXh[(b - b0) * F_s + f] = s;
         }
+    return 0;
+}
+
+/* ---------------------------------------------------------------------------------------------
+ * Gradient of the binary cross-entropy objective with respect to the logits (Section 3.3: the
+ * objective sums the BCE of sigmoid(z) against the 0/1 targets over labels; its derivative in z
+ * is sigmoid(z) - y):
+ *   dY[b, n] = 1 / (1 + exp(-Z[b, n])) - T[b, n]
+ *   T[b, n]  = 1 if n occurs among pos[b, 0..P-1], else 0
+ * Entries of pos outside [0, N) (e.g. -1 padding) are ignored; a repeated entry counts once (the
+ * target is set, not added).  Z and dY are [B, N] row-major doubles.
+ * ------------------------------------------------------------------------------------------- */
+static double sigmoid(double z) { return 1.0 / (1.0 + exp(-z)); }
+
+int haste_oracle_bce_grad(int64_t B, int64_t N, const double *Z, const int32_t *pos, int64_t P, double *dY) {
+    if (B < 0 || N < 0 || P < 0) return 1;
+#pragma omp parallel for schedule(static)
+    for (int64_t b = 0; b < B; ++b) {
+        for (int64_t n = 0; n < N; ++n) dY[b * N + n] = sigmoid(Z[b * N + n]);
+        for (int64_t p = 0; p < P; ++p) {
+            const int64_t c = pos[b * P + p];
+            if (c >= 0 && c < N) dY[b * N + c] = sigmoid(Z[b * N + c]) - 1.0;
+        }
+    }
+    return 0;
+}
+
+/* The same gradient at explicit (b, n) points: z[i] is the logit of (bs[i], ns[i]). */
+int haste_oracle_bce_grad_at(int64_t B, int64_t N, const int32_t *pos, int64_t P, int64_t n, const int64_t *bs,
+                             const int64_t *ns, const double *z, double *out) {
+    if (B < 0 || N < 0 || P < 0) return 1;
+    for (int64_t i = 0; i < n; ++i)
+        if (bs[i] < 0 || bs[i] >= B || ns[i] < 0 || ns[i] >= N) return 1;
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < n; ++i) {
+        double y = 0.0;
+        for (int64_t p = 0; p < P; ++p)
+            if (pos[bs[i] * P + p] == ns[i]) y = 1.0;
+        out[i] = sigmoid(z[i]) - y;
+    }
     return 0;
 }

@@ -8,7 +8,8 @@ raises AssertionError when the oracle disagrees with:
   (the sparse layer of Section 3.1 is exactly that matrix), evaluated with ``np.matmul``;
 * special cases with textbook answers (F_in = F_s with identity supports is a dense layer;
   G = 1 is standard per-label fixed fan-in; G = L is one gathered GEMM);
-* finite differences of the Section 3.3 BCE objective and of the bilinear pairing;
+* finite differences of the Section 3.3 BCE objective and of the bilinear pairing, and of the
+  objective with respect to the logits for the BCE-gradient function;
 * the adjoint identity <dY, Y - bias> = <dX, X> = <dW, W> (bilinearity);
 * exact one-hot gathers/scatters and the group-permutation invariance.
 """
@@ -318,6 +319,41 @@ def pin_head(o):
         close(o.head_bwd_x(Wh, dYh, dtype, 1, 4), (dYd @ Whd)[1:4], 1e-12, "head dX range")
 
 
+def pin_bce_grad(o):
+    """The BCE gradient is the derivative of the Section 3.3 objective: central differences of
+    sum(log(1 + e^z) - y z), closed forms at z = 0 and z = ln 3, and the target rule (pos entries
+    outside the row's range are ignored, repeats count once)."""
+    rng = np.random.default_rng(21)
+    B, N = 5, 23
+    Z = 3.0 * rng.standard_normal((B, N))
+    Z[0, :4] = 0.0
+    Z[1, 2] = np.log(3.0)
+    Z[2, 5], Z[2, 6] = 40.0, -40.0
+    pos = np.array([[0, 3, 3, -1], [2, 22, 23, -7], [5, 6, 5, 6], [-1, -1, -1, -1], [11, 0, 22, 1]], np.int32)
+    T = np.zeros((B, N))
+    for b in range(B):
+        for c in pos[b]:
+            if 0 <= c < N:
+                T[b, c] = 1.0
+    g = o.bce_grad(Z, pos)
+    h = 1e-5
+    for b in range(B):
+        for n in range(N):
+            Zp, Zm = Z.copy(), Z.copy()
+            Zp[b, n] += h
+            Zm[b, n] -= h
+            fd = (_bce(Zp, T) - _bce(Zm, T)) / (2 * h)
+            assert abs(fd - g[b, n]) <= 1e-7, f"BCE grad [{b},{n}]: {g[b, n]} vs central difference {fd}"
+    assert np.array_equal(g[0, :4], 0.5 - T[0, :4]), "sigmoid(0) - y must be 0.5 - y exactly"
+    assert abs(g[1, 2] - (0.75 - T[1, 2])) <= 1e-15, "sigmoid(ln 3) = 3/4"
+    # the sampled form agrees with the same central differences at every point
+    bs, ns = np.meshgrid(np.arange(B), np.arange(N), indexing="ij")
+    ga = o.bce_grad_at(pos, N, bs.ravel(), ns.ravel(), Z.ravel()).reshape(B, N)
+    assert np.abs(ga - g).max() <= 1e-15, "sampled BCE gradient differs from the dense one"
+    zero = o.bce_grad(Z, np.zeros((B, 0), np.int32))
+    assert np.abs(zero - 1.0 / (1.0 + np.exp(-Z))).max() <= 1e-15, "no positives: gradient is sigmoid(z)"
+
+
 ALL_PINS = [pin_fig2_gs, pin_fig2_ffi, pin_bruteforce, pin_duplicate_indices, pin_dense_special_case,
             pin_group_equals_expanded_ffi, pin_finite_differences, pin_adjoint_identity, pin_one_hot,
-            pin_group_permutation, pin_label_ranges, pin_head]
+            pin_group_permutation, pin_label_ranges, pin_head, pin_bce_grad]

@@ -39,6 +39,11 @@ MUTANTS = {
                               "s += ld(dYh, h * B + b, dtype) * ld(X, b * F_s + f, dtype);"),
     "head_dx_w_transposed": ("s += ld(dYh, b * H + h, dtype) * ld(Wh, h * F_s + f, dtype);",
                              "s += ld(dYh, b * H + h, dtype) * ld(Wh, f * H + h, dtype);"),
+    "bce_target_added": ("if (c >= 0 && c < N) dY[b * N + c] = sigmoid(Z[b * N + c]) - 1.0;",
+                         "if (c >= 0 && c < N) dY[b * N + c] -= 1.0;"),
+    "bce_sigmoid_sign": ("static double sigmoid(double z) { return 1.0 / (1.0 + exp(-z)); }",
+                         "static double sigmoid(double z) { return 1.0 / (1.0 + exp(z)); }"),
+    "bce_at_target_ignored": ("if (pos[bs[i] * P + p] == ns[i]) y = 1.0;", "if (pos[bs[i] * P + p] == ns[i]) y = 0.0;"),
     "bf16_decode_shift": ("uint32_t u = ((uint32_t)((const uint16_t *)p)[i]) << 16;",
                           "uint32_t u = ((uint32_t)((const uint16_t *)p)[i]) << 15;"),
 }
