@@ -49,7 +49,7 @@ enum haste_status {
 };
 
 /* Workspace-query operation codes. */
-enum haste_op { HASTE_OP_FWD = 0, HASTE_OP_BWD_W = 1, HASTE_OP_BWD_X = 2 };
+enum haste_op { HASTE_OP_FWD = 0, HASTE_OP_BWD_W = 1, HASTE_OP_BWD_X = 2, HASTE_OP_FWD_BCE = 3 };
 
 /* Shape of one sparse tail layer. */
 typedef struct haste_desc {
@@ -91,6 +91,38 @@ int haste_bwd_w(const haste_desc_t *desc, const void *X, const int32_t *idx, con
  */
 int haste_bwd_x(const haste_desc_t *desc, const int32_t *idx, const void *W, const void *dY,
                 float *dX, int beta, void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * Forward of the tail with the gradient of the binary cross-entropy objective as its epilogue
+ * (Section 3.1 logit; Section 3.3 objective, whose derivative in a logit z is sigmoid(z) - y),
+ * optionally fused with the backward-weight product of that gradient (Section 3.2):
+ *   z[b, l]  = bias[l] + sum_{t < F_in} X[b, idx[l/G, t]] * W[l, t]        (not stored)
+ *   dY[b, l] = sigmoid(z[b, l]) - T[b, l]                                  (dtype, overwritten)
+ *   T[b, l]  = 1 if l occurs among pos[b, 0..P-1], else 0
+ *   if dW != NULL:    dW[l, t] = beta * dW[l, t] + sum_b dY[b, l] * X[b, idx[l/G, t]]
+ *   if dbias != NULL: dbias[l] = beta * dbias[l] + sum_b dY[b, l]          (needs dW)
+ * The dW and dbias sums use dY as stored (rounded to dtype); they equal haste_bwd_w on the
+ * returned dY.
+ * pos[B, P] int32 holds each row's positive tail labels as column ids; entries outside [0, L)
+ * (e.g. -1 padding) are ignored and a repeated id counts once.  P >= 0; pos may be NULL when
+ * P == 0.  bias as in haste_fwd; beta is 0 (overwrite) or 1 (accumulate).
+ * bf16 layers whose groups are whole 16-label tiles, with P <= 64, run one fused kernel (the
+ * logits never reach memory).  Other layers run haste_fwd into dY, the gradient in place (for
+ * bf16 the sigmoid then sees the logits rounded to bf16), and haste_bwd_w.
+ * ws: haste_workspace_bytes(desc, HASTE_OP_FWD_BCE) bytes.
+ */
+int haste_fwd_bce(const haste_desc_t *desc, const void *X, const int32_t *idx, const void *W,
+                  const float *bias, const int32_t *pos, int32_t P, void *dY, float *dW,
+                  float *dbias, int beta, void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * Gradient of the binary cross-entropy objective at stored logits (Section 3.3), for the dense
+ * head or any [B, N] logit block:
+ *   dY[b, n] = sigmoid(Y[b, n]) - T[b, n],  T from pos[B, P] as in haste_fwd_bce (ids in [0, N)).
+ * Y and dY are [B, N] in dtype and may be the same buffer (in-place).  Arithmetic is fp32.
+ */
+int haste_bce_grad(int64_t B, int64_t N, int32_t dtype, const void *Y, const int32_t *pos,
+                   int32_t P, void *dY, void *stream);
 
 /*
  * Dense head forward (Section 3.3: a^H = W_head h_head):

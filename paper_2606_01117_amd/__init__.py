@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(PKG, "libhaste.so")
 
 HASTE_DTYPE_F32 = 0
 HASTE_DTYPE_BF16 = 1
-HASTE_OP_FWD, HASTE_OP_BWD_W, HASTE_OP_BWD_X = 0, 1, 2
+HASTE_OP_FWD, HASTE_OP_BWD_W, HASTE_OP_BWD_X, HASTE_OP_FWD_BCE = 0, 1, 2, 3
 STATUS = {0: "ok", 1: "invalid argument", 2: "unsupported", 3: "workspace too small", 4: "HIP error"}
 
 
@@ -44,6 +44,8 @@ def _load() -> ctypes.CDLL:
         "haste_fwd": [D, P, P, P, P, P, P, SZ, P],
         "haste_bwd_w": [D, P, P, P, P, P, ctypes.c_int, P, SZ, P],
         "haste_bwd_x": [D, P, P, P, P, ctypes.c_int, P, SZ, P],
+        "haste_fwd_bce": [D, P, P, P, P, P, I32, P, P, P, ctypes.c_int, P, SZ, P],
+        "haste_bce_grad": [I64, I64, I32, P, P, I32, P, P],
         "haste_head_fwd": [I64, I64, I64, I32, P, P, P, P, P],
         "haste_head_bwd": [I64, I64, I64, I32, P, P, P, P, P, ctypes.c_int, P, SZ, P],
         "haste_validate_idx": [D, P, P, P],
@@ -66,7 +68,7 @@ def _load() -> ctypes.CDLL:
 lib = _load()
 
 # every symbol the header declares
-EXPORTS = ("haste_fwd", "haste_bwd_w", "haste_bwd_x", "haste_head_fwd", "haste_head_bwd", "haste_workspace_bytes",
+EXPORTS = ("haste_fwd", "haste_bwd_w", "haste_bwd_x", "haste_fwd_bce", "haste_bce_grad", "haste_head_fwd", "haste_head_bwd", "haste_workspace_bytes",
            "haste_head_workspace_bytes", "haste_validate_idx", "haste_debug_gather", "haste_status_str",
            "haste_last_error", "haste_version")
 
@@ -152,6 +154,21 @@ def haste_bwd_x(desc, idx, W, dY, dX, beta=0, ws=None, stream=None):
     p, n = _ws(ws)
     _check(lib.haste_bwd_x(ctypes.byref(desc), _ptr(idx), _ptr(W), _ptr(dY), _ptr(dX), int(beta), p, n,
                            _stream(stream)))
+
+
+def _npos(pos) -> int:
+    return 0 if pos is None else int(pos.shape[1])
+
+
+def haste_fwd_bce(desc, X, idx, W, bias, pos, dY, dW=None, dbias=None, beta=0, ws=None, stream=None):
+    """pos: [B, P] int32 tensor of positive tail column ids (or None for no positives)."""
+    p, n = _ws(ws)
+    _check(lib.haste_fwd_bce(ctypes.byref(desc), _ptr(X), _ptr(idx), _ptr(W), _ptr(bias), _ptr(pos), _npos(pos),
+                             _ptr(dY), _ptr(dW), _ptr(dbias), int(beta), p, n, _stream(stream)))
+
+
+def haste_bce_grad(B, N, dtype, Y, pos, dY, stream=None):
+    _check(lib.haste_bce_grad(B, N, dtype, _ptr(Y), _ptr(pos), _npos(pos), _ptr(dY), _stream(stream)))
 
 
 def haste_head_fwd(B, F_s, H, dtype, X, W_head, bias_h, Y_h, stream=None):

@@ -90,6 +90,8 @@ size_t haste_workspace_bytes(const haste_desc_t *d, int op) {
         case HASTE_OP_FWD: return 0;
         case HASTE_OP_BWD_W: return haste::bwd_w_mfma_supported(a) ? haste::bwd_w_mfma_ws(a) : 0;
         case HASTE_OP_BWD_X: return haste::bwd_x_mfma_supported(a) ? haste::bwd_x_mfma_ws(a) : haste::bwd_x_valu_ws(a);
+        // the fused kernel and the backward-weight kernel stage the same X^T copy
+        case HASTE_OP_FWD_BCE: return haste::bwd_w_mfma_supported(a) ? haste::bwd_w_mfma_ws(a) : 0;
     }
     return 0;
 }
@@ -168,6 +170,64 @@ int haste_bwd_x(const haste_desc_t *d, const int32_t *idx, const void *W, const 
     TRY(need_ptr(ws, "ws"));
     if (mf) return hip_status(haste::bwd_x_mfma(a, idx, W, dY, dX, beta, ws, s), "haste_bwd_x");
     return hip_status(haste::bwd_x_valu(a, idx, W, dY, dX, beta, ws, s), "haste_bwd_x");
+}
+
+int haste_fwd_bce(const haste_desc_t *d, const void *X, const int32_t *idx, const void *W, const float *bias,
+                  const int32_t *pos, int32_t P, void *dY, float *dW, float *dbias, int beta, void *ws, size_t ws_bytes,
+                  void *stream) {
+    TRY(check_desc(d));
+    if (beta != 0 && beta != 1) return fail(HASTE_ERR_INVALID, "beta must be 0 or 1");
+    if (P < 0) return fail(HASTE_ERR_INVALID, "P must be >= 0");
+    if (dbias && !dW) return fail(HASTE_ERR_INVALID, "dbias needs dW (both come from the backward-weight product)");
+    const haste::TailArgs a = targs(d);
+    hipStream_t s = as_stream(stream);
+    if (a.L == 0) return ok();
+    if (dW) TRY(need_ptr(dW, "dW"));
+    if (dbias && !aligned16(dbias)) return fail(HASTE_ERR_INVALID, "dbias is not 16-byte aligned");
+    if (a.B == 0) {  // no rows: dY is empty and the sums are zero
+        if (!dW || beta) return ok();
+        hipError_t e = haste::fill_f32(dW, a.L * a.F_in, 0.0f, s);
+        if (e == hipSuccess && dbias) e = haste::fill_f32(dbias, a.L, 0.0f, s);
+        return hip_status(e, "haste_fwd_bce");
+    }
+    TRY(need_ptr(X, "X"));
+    TRY(need_ptr(idx, "idx"));
+    TRY(need_ptr(W, "W"));
+    TRY(need_ptr(dY, "dY"));
+    if (P > 0) TRY(need_ptr(pos, "pos"));
+    if (bias && !aligned16(bias)) return fail(HASTE_ERR_INVALID, "bias is not 16-byte aligned");
+    if (a.B * haste::cdiv(a.L, 2048) >= ((int64_t)1 << 31))
+        return fail(HASTE_ERR_UNSUPPORTED, "B * L too large for the gradient kernel's grid");
+    const bool bw_mfma = haste::bwd_w_mfma_supported(a);
+    const size_t need = bw_mfma ? haste::bwd_w_mfma_ws(a) : 0;
+    if (need && (!ws || ws_bytes < need))
+        return fail(HASTE_ERR_WORKSPACE, "haste_fwd_bce needs %zu workspace bytes, got %zu", need, ws ? ws_bytes : 0);
+    if (need) TRY(need_ptr(ws, "ws"));
+    if (haste::fwd_bce_mfma_supported(a, P))
+        return hip_status(haste::fwd_bce_mfma(a, X, idx, W, bias, P > 0 ? pos : nullptr, P, dY, dW, dbias, beta, ws, s),
+                          "haste_fwd_bce");
+    // composed: logits into dY, the gradient in place, then the backward-weight product
+    const bool fm = haste::fwd_mfma_supported(a);
+    if (!fm && !haste::valu_supported(a)) return fail(HASTE_ERR_UNSUPPORTED, "no forward kernel for this shape");
+    hipError_t e = fm ? haste::fwd_mfma(a, X, idx, W, bias, dY, s) : haste::fwd_valu(a, X, idx, W, bias, dY, s);
+    if (e == hipSuccess) e = haste::bce_grad(a.B, a.L, a.dtype, dY, P > 0 ? pos : nullptr, P, dY, s);
+    if (e == hipSuccess && dW)
+        e = bw_mfma ? haste::bwd_w_mfma(a, X, idx, dY, dW, dbias, beta, ws, s)
+                    : haste::bwd_w_valu(a, X, idx, dY, dW, dbias, beta, s);
+    return hip_status(e, "haste_fwd_bce");
+}
+
+int haste_bce_grad(int64_t B, int64_t N, int32_t dtype, const void *Y, const int32_t *pos, int32_t P, void *dY,
+                   void *stream) {
+    if (dtype != HASTE_DTYPE_F32 && dtype != HASTE_DTYPE_BF16) return fail(HASTE_ERR_INVALID, "bad dtype %d", dtype);
+    if (B < 0 || N < 0 || P < 0) return fail(HASTE_ERR_INVALID, "B, N and P must be >= 0");
+    if (B == 0 || N == 0) return ok();
+    TRY(need_ptr(Y, "Y"));
+    TRY(need_ptr(dY, "dY"));
+    if (P > 0) TRY(need_ptr(pos, "pos"));
+    if (B * haste::cdiv(N, 2048) >= ((int64_t)1 << 31)) return fail(HASTE_ERR_UNSUPPORTED, "B * N too large");
+    return hip_status(haste::bce_grad(B, N, dtype, Y, P > 0 ? pos : nullptr, P, dY, as_stream(stream)),
+                      "haste_bce_grad");
 }
 
 static int check_head(int64_t B, int64_t F_s, int64_t H, int32_t dtype) {

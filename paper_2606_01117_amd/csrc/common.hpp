@@ -81,6 +81,9 @@ struct Buf {
     __device__ __forceinline__ Buf(const void *base, uint32_t bytes)
         : r(__builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0,
                                               (int)(bytes < kOob ? bytes : kOob - 1), kRawBufferWord3)) {}
+    __device__ __forceinline__ uint32_t ld4(uint32_t off) const {
+        return __builtin_bit_cast(uint32_t, __builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, 0));
+    }
     __device__ __forceinline__ uint2 ld8(uint32_t off) const {
         return __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, 0));
     }
@@ -99,6 +102,14 @@ struct Buf {
                                                r, (int)off, 0, POLICY);
     }
 };
+
+// Gradient of the binary cross-entropy of sigmoid(z) against a 0/1 target with respect to the
+// logit z (Section 3.3 objective): sigmoid(z) - y, in fp32.  exp(-z) overflows to +inf for very
+// negative z, which gives sigmoid 0 as it should.
+__device__ __forceinline__ float bce_grad_f32(float z, bool positive) {
+    const float sg = __builtin_amdgcn_rcpf(1.0f + __expf(-z));
+    return positive ? sg - 1.0f : sg;
+}
 
 // ---- host-side launchers (one translation unit each) -----------------------------------------
 namespace haste {
@@ -120,6 +131,16 @@ bool bwd_x_mfma_supported(const TailArgs &a);
 size_t bwd_x_mfma_ws(const TailArgs &a);
 hipError_t bwd_x_mfma(const TailArgs &a, const int32_t *idx, const void *W, const void *dY, float *dX, int beta,
                       void *ws, hipStream_t s);
+
+// forward with the BCE-gradient epilogue, optionally fused with backward-weight (bf16, MFMA)
+bool fwd_bce_mfma_supported(const TailArgs &a, int P);
+size_t fwd_bce_mfma_ws(const TailArgs &a);
+hipError_t fwd_bce_mfma(const TailArgs &a, const void *X, const int32_t *idx, const void *W, const float *bias,
+                        const int32_t *pos, int P, void *dY, float *dW, float *dbias, int beta, void *ws,
+                        hipStream_t s);
+// dY[b, n] = sigmoid(Y[b, n]) - T[b, n] elementwise (Y and dY may alias)
+hipError_t bce_grad(int64_t B, int64_t N, int32_t dtype, const void *Y, const int32_t *pos, int P, void *dY,
+                    hipStream_t s);
 
 // tail, VALU (fp32 and bf16, any G including per-label fixed fan-in)
 bool valu_supported(const TailArgs &a);

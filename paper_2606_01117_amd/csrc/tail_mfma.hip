@@ -521,6 +521,301 @@ __global__ __launch_bounds__(512) void k_bwd_w2(const bf16_t *__restrict__ Xb, c
 }
 
 // --------------------------------------------------------------------------------------------
+// Forward with the BCE-gradient epilogue, and the backward-weight product of that gradient in the
+// same pass (Section 3.2 forward and backward-weight; Section 3.3 objective).  The logits are not
+// stored: the output is dY = sigmoid(z) - T, and dW = dY^T H_k is formed from the dY registers.
+// The workgroup layout is the slab-staged backward-weight one: 8 waves take UPW consecutive units
+// each (a contiguous span of at most 512 labels) and sweep the batch in 32-row slabs, with the X^T
+// block of each slab staged in LDS.  A wave keeps its units' weights in registers for the sweep,
+// so W is read from memory once.  Per unit and slab, with v_mfma_f32_16x16x32_bf16:
+//   forward, M = 16 rows, N = 16 labels, K = 32 slots:
+//     A = the gathered support columns, two ds_read_b64_tr_b16 per 32-slot step.  Source lane
+//         4j + a of 16-lane group q names slot 8q + 4h + j (read h) and rows 8a + 4m .. +3 of
+//         M-tile m, so result lane i holds row 8(i / 4) + 4m + i % 4 of those slots;
+//     B = W: 16 contiguous bytes of one label's row (slots 32s + 8q .. +7 of label l16) per lane.
+//   Result lane (label l16, q) then holds rows 8q .. 8q+3 (M-tile 0) and 8q+4 .. 8q+7 (M-tile 1)
+//   of its label.  After the epilogue these 8 values of dY are exactly the B operand of the
+//   backward-weight product (K = rows 8q .. 8q+7, N = label), which thus never leaves the
+//   registers; that product and its A operand are the backward-weight kernel's, in the same
+//   order, so dW equals what haste_bwd_w computes from the stored dY, bit for bit.
+//   dY leaves through a per-wave LDS buffer as 128-byte row pieces (8 rows per store): adjacent
+//   lanes swap halves (DPP) so that each writes two labels of four rows as 4-byte words.
+// Targets: the slab's positives that fall in the workgroup's span are set as bits of an LDS
+// bitmap, one 32-bit word of rows per label.  Two bitmaps alternate by slab parity: in one
+// barrier interval each thread clears its word of the previous slab's bitmap and sets the
+// current slab's bits, and the bitmap is read only after the next barrier.
+// --------------------------------------------------------------------------------------------
+constexpr int kFbWaves = 8;
+constexpr int kFbMaxSpan = 512;                 // labels per workgroup at most (16 units of 32)
+constexpr int kFbMaxPos = 64;                   // positives per row the slab prefetch holds
+constexpr int kFbPosLoads = 32 * kFbMaxPos / (kFbWaves * 64);
+
+__host__ __device__ constexpr int fb_upw(int F_in) { return F_in == 128 ? 1 : 2; }
+__host__ __device__ constexpr int fb_ys(int F_in) { return fb_upw(F_in) * 64 + 16; }   // staged dY row bytes
+
+// X^T block, both bitmaps and the per-wave dY staging, or at the end the per-wave dW staging
+static size_t fb_lds(int F_s, int F_in) {
+    const size_t main = (size_t)haste::round_up((int64_t)F_s * kBw2XRow, 16) + 2 * kFbMaxSpan * 4 +
+                        (size_t)kFbWaves * 32 * fb_ys(F_in);
+    const size_t out = (size_t)kFbWaves * 32 * (F_in + 4) * 4;
+    return main > out ? main : out;
+}
+
+__device__ __forceinline__ uint32_t dpp_swap_pairs(uint32_t v) {   // lane l receives lane l ^ 1's value
+    return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0xB1, 0xF, 0xF, false);   // quad_perm [1, 0, 3, 2]
+}
+
+template <int F_IN, bool HAS_BIAS, bool WITH_DW>
+__global__ __launch_bounds__(512) void k_fwd_bce(const bf16_t *__restrict__ Xb, const int32_t *__restrict__ idx,
+                                                 const bf16_t *__restrict__ W, const float *__restrict__ bias,
+                                                 const int32_t *__restrict__ pos, int P, bf16_t *__restrict__ dY,
+                                                 float *__restrict__ dW, float *__restrict__ dbias, int beta, int B,
+                                                 int Bp, int F_s, int64_t L, int G, int64_t K) {
+    extern __shared__ __align__(16) char fbs[];
+    constexpr int UPW = fb_upw(F_IN);
+    constexpr int KS = F_IN / 32;               // forward K-steps (32 slots)
+    constexpr int NST = F_IN / 16;              // backward-weight M-tiles (16 slots)
+    constexpr int YS = fb_ys(F_IN);
+    char *xs = fbs;
+    uint32_t *bm = reinterpret_cast<uint32_t *>(fbs + ((F_s * kBw2XRow + 15) & ~15));
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    char *ystg = reinterpret_cast<char *>(bm + 2 * kFbMaxSpan) + wave * 32 * YS;
+    const int l16 = lane & 15, q = lane >> 4;
+    const int ntn = (G + 31) >> 5;
+    const int64_t nunits = K * ntn;
+    const int64_t u0 = (int64_t)blockIdx.x * (kFbWaves * UPW);
+    auto lab_of = [&](int64_t v) {
+        const int64_t k = v / ntn;
+        return k * G + 32 * (int)(v - k * ntn);
+    };
+    auto nlab_of = [&](int64_t v) {
+        const int t = (int)(v % ntn);
+        return G - 32 * t < 32 ? G - 32 * t : 32;
+    };
+    const int64_t ul = u0 + kFbWaves * UPW - 1 < nunits ? u0 + kFbWaves * UPW - 1 : nunits - 1;
+    const int64_t lab0 = lab_of(u0);
+    const int span = (int)(lab_of(ul) + nlab_of(ul) - lab0);
+
+    // this wave's units (a unit past the end repeats the last one and is never stored), their
+    // supports in both operand roles, weights and biases
+    int64_t vu[UPW];
+    int off[UPW], nl[UPW], col[UPW];
+    int fa[UPW][KS][2];     // forward gather: slot 32 s + 8 q + 4 h + l16 / 4
+    int fw[UPW][NST];       // backward-weight A operand: slot 16 st + l16
+    uint4 wop[UPW][2][KS];  // W[label 16 nt + l16][32 s + 8 q .. +7]
+    float bl[UPW][2];
+    const int aq = l16 & 3;
+#pragma unroll
+    for (int j = 0; j < UPW; ++j) {
+        const int64_t v = u0 + UPW * wave + j;
+        vu[j] = v < nunits ? v : nunits - 1;
+        off[j] = (int)(lab_of(vu[j]) - lab0);
+        nl[j] = v < nunits ? nlab_of(vu[j]) : 0;
+        col[j] = j == 0 ? 0 : col[j - 1] + nl[j - 1];
+        const int64_t k = vu[j] / ntn;
+        const int32_t *ik = idx + k * F_IN;
+#pragma unroll
+        for (int s = 0; s < KS; ++s)
+#pragma unroll
+            for (int h = 0; h < 2; ++h) fa[j][s][h] = ik[32 * s + 8 * q + 4 * h + (l16 >> 2)];
+#pragma unroll
+        for (int st = 0; st < NST; ++st) fw[j][st] = ik[16 * st + l16];
+        const int64_t lb = lab_of(vu[j]);
+        const Buf wb(W + lb * F_IN, (uint32_t)(nlab_of(vu[j]) * F_IN * 2));
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt) {
+#pragma unroll
+            for (int s = 0; s < KS; ++s)
+                wop[j][nt][s] = wb.ld16((uint32_t)(((16 * nt + l16) * F_IN + 32 * s + 8 * q) * 2));
+            bl[j][nt] = 0.0f;
+            if constexpr (HAS_BIAS) {
+                const int t = 16 * nt + l16;
+                bl[j][nt] = t < nlab_of(vu[j]) ? bias[lb + t] : 0.0f;
+            }
+        }
+    }
+
+    // cooperative slab loads: the X^T block (4 F_s chunks of 16 bytes) and the slab's positives
+    const int nxc = 4 * F_s;
+    uint4 xr[kBw2MaxXLoads];
+    uint32_t pr[kFbPosLoads];
+    auto load = [&](int blk) {
+        const Buf xb(Xb + (int64_t)blk * F_s * 32, (uint32_t)(nxc * 16));
+#pragma unroll
+        for (int i = 0; i < kBw2MaxXLoads; ++i) xr[i] = xb.ld16((uint32_t)(tid + 512 * i) * 16);   // past the block: zero
+        const int b0 = blk * 32;
+        const int rows = B - b0 < 32 ? B - b0 : 32;
+        const Buf pb(pos + (int64_t)b0 * P, (uint32_t)(rows > 0 ? rows * P * 4 : 0));
+#pragma unroll
+        for (int i = 0; i < kFbPosLoads; ++i) pr[i] = pb.ld4((uint32_t)(tid + 512 * i) * 4);   // validity checked at use
+    };
+    auto store = [&](int blk) {
+#pragma unroll
+        for (int i = 0; i < kBw2MaxXLoads; ++i) {
+            const int c = tid + 512 * i;
+            if (c < nxc) *reinterpret_cast<uint4 *>(xs + (c >> 2) * kBw2XRow + (c & 3) * 16) = xr[i];
+        }
+        // clear this thread's word of the previous slab's bitmap, set the current slab's targets
+        uint32_t *cur = bm + (blk & 1) * kFbMaxSpan;
+        bm[((blk + 1) & 1) * kFbMaxSpan + tid] = 0u;
+        const int rows = B - blk * 32 < 32 ? B - blk * 32 : 32;
+#pragma unroll
+        for (int i = 0; i < kFbPosLoads; ++i) {
+            const int e = tid + 512 * i;
+            if (e < rows * P) {
+                const int64_t o = (int64_t)(int32_t)pr[i] - lab0;
+                if (o >= 0 && o < span) atomicOr(cur + o, 1u << (e / P));
+            }
+        }
+    };
+
+    f32x4_t acc[UPW][NST][2], db[UPW][2];
+#pragma unroll
+    for (int j = 0; j < UPW; ++j) {
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt) {
+            db[j][nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int st = 0; st < NST; ++st) acc[j][st][nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        }
+    }
+    const bf16x8_t ones = as_bf16x8(make_uint4(0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u));
+    const bool odd = (l16 & 1) != 0;
+
+    // dY stores of the wave's units: LPR lanes per staged row (16 bytes each), RPS rows per store
+    constexpr int LPR = UPW * 4;
+    constexpr int RPS = 64 / LPR;
+    constexpr int SPT = 32 / RPS;
+    const int sr = lane / LPR, sc = lane % LPR;
+    const int width = col[UPW - 1] + nl[UPW - 1];
+    const int64_t labw = lab0 + off[0];
+    const bool sok = 8 * sc < width;
+
+    for (int i = tid; i < 2 * kFbMaxSpan; i += kFbWaves * 64) bm[i] = 0u;
+    const int nblk = Bp / 32;
+    load(0);
+    for (int blk = 0; blk < nblk; ++blk) {
+        __syncthreads();   // the previous slab is no longer read
+        store(blk);
+        __syncthreads();
+        if (blk + 1 < nblk) load(blk + 1);
+        const uint32_t *cur = bm + (blk & 1) * kFbMaxSpan;
+        const int b0 = blk * 32;
+        const int rows = B - b0 < 32 ? B - b0 : 32;
+#pragma unroll
+        for (int j = 0; j < UPW; ++j) {
+            // forward: z^T tile [32 rows][32 labels] of unit j
+            f32x4_t z[2][2];
+#pragma unroll
+            for (int m = 0; m < 2; ++m)
+#pragma unroll
+                for (int nt = 0; nt < 2; ++nt) z[m][nt] = f32x4_t{bl[j][nt], bl[j][nt], bl[j][nt], bl[j][nt]};
+#pragma unroll
+            for (int s = 0; s < KS; ++s) {
+#pragma unroll
+                for (int m = 0; m < 2; ++m) {
+                    const uint2 lo = lds_read_tr(xs + fa[j][s][0] * kBw2XRow + 16 * aq + 8 * m);
+                    const uint2 hi = lds_read_tr(xs + fa[j][s][1] * kBw2XRow + 16 * aq + 8 * m);
+                    const bf16x8_t av = as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y));
+#pragma unroll
+                    for (int nt = 0; nt < 2; ++nt) z[m][nt] = mfma16x16x32(av, as_bf16x8(wop[j][nt][s]), z[m][nt]);
+                }
+            }
+            // epilogue: dY = sigmoid(z) - T for rows 8q .. 8q+7 of label 16 nt + l16 (zero on rows past B)
+            uint4 yb[2];
+#pragma unroll
+            for (int nt = 0; nt < 2; ++nt) {
+                const int t = 16 * nt + l16;
+                const uint32_t tw = t < nl[j] ? cur[off[j] + t] >> (8 * q) : 0u;
+                float d[8];
+#pragma unroll
+                for (int r = 0; r < 8; ++r) {
+                    const float zz = z[r >> 2][nt][r & 3];
+                    d[r] = 8 * q + r < rows ? bce_grad_f32(zz, (tw >> r) & 1u) : 0.0f;
+                }
+                yb[nt] = make_uint4(pack_bf16(d[0], d[1]), pack_bf16(d[2], d[3]), pack_bf16(d[4], d[5]),
+                                    pack_bf16(d[6], d[7]));
+            }
+            // stage: even lanes write rows 8q .. 8q+3 of labels (t, t+1), odd lanes rows 8q+4 .. +7 of (t-1, t)
+#pragma unroll
+            for (int nt = 0; nt < 2; ++nt) {
+                if (16 * nt >= nl[j]) continue;   // wave-uniform: groups are whole 16-label tiles
+                const uint4 v = yb[nt];
+                const uint32_t r0 = dpp_swap_pairs(odd ? v.x : v.z);
+                const uint32_t r1 = dpp_swap_pairs(odd ? v.y : v.w);
+                const uint32_t L0 = odd ? r0 : v.x, H0 = odd ? v.z : r0;
+                const uint32_t L1 = odd ? r1 : v.y, H1 = odd ? v.w : r1;
+                char *p = ystg + (8 * q + (odd ? 4 : 0)) * YS + (col[j] + 16 * nt + (l16 & ~1)) * 2;
+                *reinterpret_cast<uint32_t *>(p) = (L0 & 0xffffu) | (H0 << 16);
+                *reinterpret_cast<uint32_t *>(p + YS) = (L0 >> 16) | (H0 & 0xffff0000u);
+                *reinterpret_cast<uint32_t *>(p + 2 * YS) = (L1 & 0xffffu) | (H1 << 16);
+                *reinterpret_cast<uint32_t *>(p + 3 * YS) = (L1 >> 16) | (H1 & 0xffff0000u);
+            }
+            if constexpr (WITH_DW) {
+#pragma unroll
+                for (int st = 0; st < NST; ++st) {
+                    const uint4 xv = *reinterpret_cast<const uint4 *>(xs + fw[j][st] * kBw2XRow + q * 16);
+#pragma unroll
+                    for (int nt = 0; nt < 2; ++nt)
+                        acc[j][st][nt] = mfma16x16x32(as_bf16x8(xv), as_bf16x8(yb[nt]), acc[j][st][nt]);
+                }
+                if (dbias) {
+#pragma unroll
+                    for (int nt = 0; nt < 2; ++nt) db[j][nt] = mfma16x16x32(ones, as_bf16x8(yb[nt]), db[j][nt]);
+                }
+            }
+        }
+        // the wave's [32 rows][width] dY block leaves as 16-byte pieces, LPR lanes per row
+        const Buf yo(dY + (int64_t)b0 * L + labw, (uint32_t)(rows * L * 2));
+#pragma unroll
+        for (int p = 0; p < SPT; ++p) {
+            const int r = RPS * p + sr;
+            const uint4 v = *reinterpret_cast<const uint4 *>(ystg + r * YS + sc * 16);
+            const uint32_t o = sok && r < rows ? (uint32_t)(((int64_t)r * L + 8 * sc) * 2) : kOob;
+            yo.st16<kStreaming>(v, o);
+        }
+    }
+
+    if constexpr (WITH_DW) {
+        // dW: as in the backward-weight kernel, each wave stages its unit's [32 labels][F_IN] fp32
+        // block in LDS and writes it as whole contiguous runs; dbias from the q = 0 lanes.
+        __syncthreads();   // every wave is done with the staged slabs
+        constexpr int OS = F_IN + 4;
+        float *ostg = reinterpret_cast<float *>(fbs) + wave * 32 * OS;
+#pragma unroll
+        for (int j = 0; j < UPW; ++j) {
+            const int64_t lb = lab_of(vu[j]);
+#pragma unroll
+            for (int nt = 0; nt < 2; ++nt)
+#pragma unroll
+                for (int st = 0; st < NST; ++st)
+                    *reinterpret_cast<float4 *>(ostg + (16 * nt + l16) * OS + 16 * st + 4 * q) =
+                        make_float4(acc[j][st][nt][0], acc[j][st][nt][1], acc[j][st][nt][2], acc[j][st][nt][3]);
+            const Buf ob(dW + lb * F_IN, (uint32_t)(nl[j] * F_IN * 4));   // this unit's labels only
+#pragma unroll
+            for (int i = 0; i < F_IN / 8; ++i) {
+                const int e = 64 * i + lane;
+                const int r = e / (F_IN / 4), c = (e % (F_IN / 4)) * 4;
+                float4 v = *reinterpret_cast<const float4 *>(ostg + r * OS + c);
+                if (beta) {
+                    const float4 o = __builtin_bit_cast(float4, ob.ld16((uint32_t)(e * 16)));
+                    v.x += o.x; v.y += o.y; v.z += o.z; v.w += o.w;
+                }
+                ob.st16<kStreaming>(__builtin_bit_cast(uint4, v), (uint32_t)(e * 16));
+            }
+            if (dbias && q == 0) {
+#pragma unroll
+                for (int nt = 0; nt < 2; ++nt) {
+                    const int t = 16 * nt + l16;
+                    if (t < nl[j]) dbias[lb + t] = (beta ? dbias[lb + t] : 0.0f) + db[j][nt][0];
+                }
+            }
+        }
+    }
+}
+
+// --------------------------------------------------------------------------------------------
 // Backward-feature (split over label segments).
 //
 // The contraction runs over the labels of a group, which are strided in W's natural layout
@@ -932,7 +1227,6 @@ struct BwdXGeom {
 BwdXGeom bwd_x_geom(const haste::TailArgs &a) {
     BwdXGeom g;
     g.nbt = (int)haste::cdiv(a.B, 32);
-    const int nt = (int)(a.F_in / 16) * 2;
     g.nwaves = kBxConsumers + kBxProducers;
     // groups per staged dY chunk: at most 256 labels (one 512-byte load per row), kBxChunkBytes and
     // what the LDS holds beside the accumulator, rounded down to a multiple of the prefetch depth
@@ -1054,6 +1348,52 @@ hipError_t bwd_w_mfma(const TailArgs &a, const void *X, const int32_t *idx, cons
             case 128: return launch2(k_bwd_w2<128>);
             default: break;
         }
+    }
+    return hipErrorInvalidValue;
+}
+
+// ---- forward with the BCE-gradient epilogue, fused with backward-weight -------------------------
+// Groups of whole 16-label tiles (the staged dY columns of a wave's units stay contiguous), and at
+// most kFbMaxPos positives per row (the slab prefetch).
+bool fwd_bce_mfma_supported(const TailArgs &a, int P) {
+    return bwd_w_mfma_supported(a) && (a.G % 16) == 0 && P >= 0 && P <= kFbMaxPos &&
+           fb_lds((int)a.F_s, (int)a.F_in) <= kLdsBudget;
+}
+
+size_t fwd_bce_mfma_ws(const TailArgs &a) { return bwd_w_mfma_ws(a); }
+
+template <int F_IN>
+static hipError_t launch_fwd_bce(const TailArgs &a, const bf16_t *Xb, const int32_t *idx, const void *W,
+                                 const float *bias, const int32_t *pos, int P, void *dY, float *dW, float *dbias,
+                                 int beta, int Bp, hipStream_t s) {
+    const int64_t K = a.L / a.G;
+    const int64_t units = K * cdiv(a.G, 32);
+    const size_t lds = fb_lds((int)a.F_s, F_IN);
+    const dim3 grid((unsigned)cdiv(units, kFbWaves * fb_upw(F_IN)));
+    auto go = [&](auto kern) {
+        hipError_t e = allow_lds(kern, lds);
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(kern, grid, dim3(kFbWaves * 64), lds, s, Xb, idx, (const bf16_t *)W, bias, pos, P,
+                           (bf16_t *)dY, dW, dbias, beta, (int)a.B, Bp, (int)a.F_s, a.L, (int)a.G, K);
+        return hipGetLastError();
+    };
+    if (dW) return bias ? go(k_fwd_bce<F_IN, true, true>) : go(k_fwd_bce<F_IN, false, true>);
+    return bias ? go(k_fwd_bce<F_IN, true, false>) : go(k_fwd_bce<F_IN, false, false>);
+}
+
+hipError_t fwd_bce_mfma(const TailArgs &a, const void *X, const int32_t *idx, const void *W, const float *bias,
+                        const int32_t *pos, int P, void *dY, float *dW, float *dbias, int beta, void *ws,
+                        hipStream_t s) {
+    const int Bp = (int)round_up(a.B, 32);
+    bf16_t *Xb = reinterpret_cast<bf16_t *>(ws);
+    hipLaunchKernelGGL(k_transpose_x, dim3((unsigned)cdiv(a.F_s, 32), (unsigned)cdiv(Bp, 32)), dim3(256), 0, s,
+                       (const bf16_t *)X, Xb, (int)a.B, (int)a.F_s);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    switch (a.F_in) {
+        case 32: return launch_fwd_bce<32>(a, Xb, idx, W, bias, pos, P, dY, dW, dbias, beta, Bp, s);
+        case 64: return launch_fwd_bce<64>(a, Xb, idx, W, bias, pos, P, dY, dW, dbias, beta, Bp, s);
+        case 128: return launch_fwd_bce<128>(a, Xb, idx, W, bias, pos, P, dY, dW, dbias, beta, Bp, s);
     }
     return hipErrorInvalidValue;
 }

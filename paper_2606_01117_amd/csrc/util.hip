@@ -112,6 +112,38 @@ unsigned grid_for(int64_t n) {
     return (unsigned)(g < 1 ? 1 : g);
 }
 
+
+// BCE gradient of stored logits (Section 3.3 objective): dY[b, n] = sigmoid(Y[b, n]) - T[b, n], with
+// T[b, n] = 1 where n occurs in pos[b, 0..P-1].  A workgroup takes 2048 columns of one row and a
+// thread 8 consecutive columns; the row's positives are workgroup-uniform reads.  Y and dY may be
+// the same buffer (each element is read before it is written, by the same thread).
+template <typename T, bool VEC>
+__global__ __launch_bounds__(256) void k_bce_grad(const T *Y, const int32_t *__restrict__ pos, int P, T *dY,
+                                                  int64_t N, int64_t nchunk) {
+    const int64_t b = blockIdx.x / nchunk;
+    const int64_t c0 = (blockIdx.x - b * nchunk) * 2048 + 8 * (int64_t)threadIdx.x;
+    if (c0 >= N) return;
+    uint32_t t = 0;
+    for (int p = 0; p < P; ++p) {
+        const int64_t d = (int64_t)pos[b * P + p] - c0;
+        if (d >= 0 && d < 8) t |= 1u << d;
+    }
+    const T *y = Y + b * N + c0;
+    T *o = dY + b * N + c0;
+    if constexpr (VEC && sizeof(T) == 2) {   // bf16, whole 16-byte groups
+        const uint4 v = *reinterpret_cast<const uint4 *>(y);
+        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+        uint32_t r[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            r[i] = pack_bf16(bce_grad_f32(__uint_as_float(w[i] << 16), (t >> (2 * i)) & 1),
+                             bce_grad_f32(__uint_as_float(w[i] & 0xffff0000u), (t >> (2 * i + 1)) & 1));
+        *reinterpret_cast<uint4 *>(o) = make_uint4(r[0], r[1], r[2], r[3]);
+    } else {
+        const int n = N - c0 < 8 ? (int)(N - c0) : 8;
+        for (int i = 0; i < n; ++i) store_out(o, i, bce_grad_f32(load_f32(y, i), (t >> i) & 1));
+    }
+}
 }  // namespace
 
 namespace haste {
@@ -154,6 +186,23 @@ hipError_t debug_gather(const void *X, int32_t dtype, const int32_t *idx, int64_
     else
         hipLaunchKernelGGL(k_gather<float>, dim3(grid_for(n)), dim3(256), 0, s, (const float *)X, idx, B, F_s, F_in, k0,
                            nk, (float *)out);
+    return hipGetLastError();
+}
+
+
+hipError_t bce_grad(int64_t B, int64_t N, int32_t dtype, const void *Y, const int32_t *pos, int P, void *dY,
+                    hipStream_t s) {
+    const int64_t nchunk = cdiv(N, 2048);
+    const dim3 grid((unsigned)(B * nchunk)), block(256);
+    const bool vec = (N % 8) == 0 && ((reinterpret_cast<uintptr_t>(Y) | reinterpret_cast<uintptr_t>(dY)) & 15) == 0;
+    if (dtype == HASTE_DTYPE_BF16) {
+        if (vec)
+            hipLaunchKernelGGL((k_bce_grad<bf16_t, true>), grid, block, 0, s, (const bf16_t *)Y, pos, P, (bf16_t *)dY, N, nchunk);
+        else
+            hipLaunchKernelGGL((k_bce_grad<bf16_t, false>), grid, block, 0, s, (const bf16_t *)Y, pos, P, (bf16_t *)dY, N, nchunk);
+    } else {
+        hipLaunchKernelGGL((k_bce_grad<float, false>), grid, block, 0, s, (const float *)Y, pos, P, (float *)dY, N, nchunk);
+    }
     return hipGetLastError();
 }
 

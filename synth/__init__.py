@@ -214,6 +214,19 @@ def positive_neurons(wl: Workload, positives: np.ndarray, perm: np.ndarray):
     return (np.array(tail, dtype=np.int64).reshape(-1, 2), np.array(head, dtype=np.int64).reshape(-1, 2))
 
 
+def pos_matrix(pairs: np.ndarray, B: int, P: Optional[int] = None) -> np.ndarray:
+    """(b, column) pairs -> [B, P] int32 column lists per row, padded with -1 (P = longest row)."""
+    rows: list = [[] for _ in range(B)]
+    for b, n in np.asarray(pairs).reshape(-1, 2):
+        rows[int(b)].append(int(n))
+    if P is None:
+        P = max((len(r) for r in rows), default=0)
+    out = np.full((B, P), -1, dtype=np.int32)
+    for b, r in enumerate(rows):
+        out[b, :len(r)] = r[:P]
+    return out
+
+
 def bce_grad(wl: Workload, pos_pairs: np.ndarray, n_cols: int, seed: int = 0,
              logits: Optional[np.ndarray] = None, buf: int = _BUF_Z, chunk_rows: int = 8) -> np.ndarray:
     """dY[B, n_cols] = bf16(sigmoid(z) - y).  z = supplied logits or N(0,1) stand-ins."""

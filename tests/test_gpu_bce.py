@@ -1,0 +1,233 @@
+"""GPU parity of the BCE-gradient entry points (through the C ABI) against the fp64 CPU oracle.
+
+haste_fwd_bce computes dY = sigmoid(z) - T from the layer's own logits z and, when asked, the
+backward-weight product of that dY in the same pass; haste_bce_grad applies the same gradient to
+stored logits.  The oracle composes its forward, its BCE gradient and its backward-weight product
+in fp64.  Beyond the tolerance checks:
+* the target rule is checked exactly: dY < 0 exactly where a positive sits (sigmoid never
+  reaches 1 at these logits) and dY > 0 elsewhere;
+* the fused dW/dbias equal haste_bwd_w applied to the returned dY, bit for bit.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from gpu_helpers import TOL, host_f32, out_tensor, rel_err, say, to_dev
+
+pytestmark = pytest.mark.gpu
+F32, BF16 = synth.DT_F32, synth.DT_BF16
+
+
+@pytest.fixture(scope="module")
+def hs():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a ROCm device"
+    import paper_2606_01117_amd as m
+    return m
+
+
+@pytest.fixture(scope="module")
+def orc():
+    return oracle.get()
+
+
+def _sync():
+    import torch
+    torch.cuda.synchronize()
+
+
+def _check(name, got, ref, dtype):
+    e = rel_err(got, ref)
+    say(f"    {name:<10s} rel_inf_err={e:.3e} (tol {TOL[dtype]:.0e})")
+    assert e <= TOL[dtype], f"{name}: {e:.3e} > {TOL[dtype]:.0e}"
+
+
+def rand_pos(rng, B, L, P):
+    """[B, P] positives with the awkward entries: repeats, -1 padding, ids past L and below -1,
+    and ids on 512-label span edges and at both ends of the layer."""
+    if P == 0:
+        return np.zeros((B, 0), np.int32)
+    pos = rng.integers(0, L, size=(B, P)).astype(np.int32)
+    edges = [0, L - 1, min(511, L - 1), min(512, L - 1), L // 2]
+    for b in range(B):
+        r = rng.random()
+        if r < 0.2:
+            pos[b, -1] = -1
+        elif r < 0.3:
+            pos[b, -1] = L + int(rng.integers(0, 100))
+        elif r < 0.4:
+            pos[b, -1] = -int(rng.integers(2, 100))
+        elif r < 0.6 and P > 1:
+            pos[b, -1] = pos[b, 0]       # a repeat counts once
+        pos[b, 0] = edges[b % len(edges)] if b % 3 == 0 else pos[b, 0]
+    return pos
+
+
+def targets(pos, B, L):
+    T = np.zeros((B, L), bool)
+    for b in range(B):
+        for c in pos[b]:
+            if 0 <= c < L:
+                T[b, c] = True
+    return T
+
+
+def oracle_fwd_bce(orc, X, idx, W, bias, pos, G, F_in, dt):
+    """fp64 composition: logits, BCE gradient, backward-weight (dY passed at fp32 precision)."""
+    z = orc.fwd(X, idx, W, bias, G, dt)
+    dY = orc.bce_grad(z, pos)
+    Xf = synth.to_f64(X, dt).astype(np.float32)   # exact for bf16 and fp32 storage
+    dW, db = orc.bwd_w(Xf, idx, dY.astype(np.float32), G, F_in, F32, with_dbias=True)
+    return dY, dW, db
+
+
+CASES = [
+    # name, B, F_s, L, G, F_in, dtype, P, bias   (fused: bf16, G % 16 == 0, P <= 64)
+    ("fused_g32_f64", 40, 256, 2048, 32, 64, BF16, 6, False),
+    ("fused_g32_f64_bias", 64, 768, 4096, 32, 64, BF16, 8, True),
+    ("fused_g16_ragged_b33", 33, 768, 4096, 16, 64, BF16, 5, False),
+    ("fused_g64_f128", 70, 768, 4096, 64, 128, BF16, 8, True),
+    ("fused_g48_f32", 97, 384, 48 * 40, 48, 32, BF16, 3, False),
+    ("fused_b300_f32", 300, 768, 8192, 32, 32, BF16, 64, True),
+    ("fused_b1", 1, 768, 1024, 32, 64, BF16, 2, False),
+    ("fused_p0", 50, 512, 2048, 32, 64, BF16, 0, False),
+    ("composed_p80", 40, 256, 2048, 32, 64, BF16, 80, False),
+    ("composed_g8", 70, 768, 3072, 8, 32, BF16, 5, True),
+    ("composed_g4", 64, 512, 1536, 4, 64, BF16, 5, False),
+    ("composed_g1_ffi", 37, 768, 1024, 1, 64, BF16, 4, False),
+    ("composed_f32_g8", 32, 256, 4096, 8, 32, F32, 5, True),
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
+def test_fwd_bce(hs, orc, case):
+    import torch
+    name, B, F_s, L, G, F_in, dt, P, with_bias = case
+    say(f"[fwd_bce] {name}: B={B} F_s={F_s} L={L} G={G} F_in={F_in} dtype={dt} P={P}")
+    wl = synth.small(name, B=B, F_s=F_s, L=L, G=G, F_in=F_in, dtype=dt, wid=600 + CASES.index(case))
+    X, W, idx = synth.draw_X(wl), synth.draw_W(wl), synth.draw_idx(wl)
+    rng = np.random.default_rng(wl.wid)
+    bias = rng.standard_normal(L).astype(np.float32) if with_bias else None
+    pos = rand_pos(rng, B, L, P)
+    desc = hs.make_desc(B, F_s, L, G, F_in, dt)
+    Xd, idxd, Wd, bd = to_dev(X), to_dev(idx), to_dev(W), to_dev(bias)
+    posd = to_dev(pos) if P else None
+    dY = out_tensor((B, L), dt)
+    dW = torch.empty((L, F_in), dtype=torch.float32, device="cuda")
+    db = torch.empty((L,), dtype=torch.float32, device="cuda")
+    ws = hs.workspace(hs.haste_workspace_bytes(desc, hs.HASTE_OP_FWD_BCE))
+    hs.haste_fwd_bce(desc, Xd, idxd, Wd, bd, posd, dY, dW, db, 0, ws)
+    _sync()
+    dY_ref, dW_ref, db_ref = oracle_fwd_bce(orc, X, idx, W, bias, pos, G, F_in, dt)
+    got = host_f32(dY, dt)
+    _check("dY", got, dY_ref, dt)
+    _check("dW", dW.cpu().numpy(), dW_ref, dt)
+    _check("dbias", db.cpu().numpy(), db_ref, dt)
+    T = targets(pos, B, L)
+    assert np.array_equal(got < 0, T) and np.all(got[~T] > 0), "targets are not applied exactly where pos names them"
+    # the fused backward-weight product is haste_bwd_w on the returned dY, bit for bit
+    dW2 = torch.empty_like(dW)
+    db2 = torch.empty_like(db)
+    hs.haste_bwd_w(desc, Xd, idxd, dY, dW2, db2, 0, hs.workspace(hs.haste_workspace_bytes(desc, hs.HASTE_OP_BWD_W)))
+    _sync()
+    assert bool((dW2 == dW).all()) and bool((db2 == db).all()), "fused dW differs from haste_bwd_w on its dY"
+    # beta = 1 accumulates; without dW only dY is written
+    hs.haste_fwd_bce(desc, Xd, idxd, Wd, bd, posd, dY, dW, db, 1, ws)
+    dY2 = out_tensor((B, L), dt)
+    hs.haste_fwd_bce(desc, Xd, idxd, Wd, bd, posd, dY2, None, None, 0, ws)
+    _sync()
+    assert bool((dW == 2 * dW2).all()) and bool((db == 2 * db2).all()), "beta = 1 must add the same sums"
+    assert bool((dY2 == dY).all()), "dY without dW must equal dY with it"
+
+
+@pytest.mark.parametrize("B,N,dt,inplace", [(33, 1000, BF16, False), (64, 4096, BF16, True), (7, 1003, BF16, True),
+                                            (33, 1000, F32, False), (5, 77, F32, True)])
+def test_bce_grad_elementwise(hs, orc, B, N, dt, inplace):
+    say(f"[bce_grad] B={B} N={N} dtype={dt} inplace={inplace}")
+    rng = np.random.default_rng(B * N)
+    z = (2.5 * rng.standard_normal((B, N))).astype(np.float32)
+    z[0, :3] = [0.0, 30.0, -30.0]
+    zs = synth.bf16_bits(z) if dt == BF16 else z
+    pos = rand_pos(rng, B, N, 6)
+    Y = to_dev(zs)
+    out = Y if inplace else out_tensor((B, N), dt)
+    hs.haste_bce_grad(B, N, dt, Y, to_dev(pos), out)
+    _sync()
+    ref = orc.bce_grad(synth.to_f64(zs, dt), pos)
+    got = host_f32(out, dt)
+    _check("bce_grad", got, ref, dt)
+    T = targets(pos, B, N)
+    live = np.abs(synth.to_f64(zs, dt)) < 15          # sigmoid strictly inside (0, 1) in fp32
+    assert np.array_equal((got < 0) & live, T & live), "targets are not applied exactly where pos names them"
+
+
+def test_fwd_bce_empty_and_errors(hs):
+    import torch
+    dummy = torch.zeros(16, dtype=torch.int32, device="cuda")
+    d0 = hs.make_desc(0, 768, 4096, 32, 64, BF16)
+    dW = torch.full((4096, 64), 3.0, device="cuda")
+    db = torch.full((4096,), 3.0, device="cuda")
+    hs.haste_fwd_bce(d0, dummy, dummy, dummy, None, None, dummy, dW, db, 0)
+    _sync()
+    assert float(dW.abs().max()) == 0.0 and float(db.abs().max()) == 0.0
+    d = hs.make_desc(8, 768, 4096, 32, 64, BF16)
+    with pytest.raises(hs.HasteError):   # dbias without dW
+        hs.haste_fwd_bce(d, dummy, dummy, dummy, None, None, dummy, None, db, 0)
+    with pytest.raises(hs.HasteError):   # workspace missing
+        hs.haste_fwd_bce(d, dummy, dummy, dummy, None, None, dummy, dW, None, 0)
+
+
+LARGE = ["l2949k_g32_h65k", "l655k_g32_h16k", "gsweep_g16"]
+
+
+@pytest.mark.parametrize("name", LARGE)
+def test_fwd_bce_large_sampled(hs, orc, name):
+    """The full-size layers, launched as the benchmark launches them: label ranges at the start,
+    middle and end (every row), random points, the exact target rule over the whole dY, and the
+    fused dW against haste_bwd_w on the same dY over the whole layer."""
+    import torch
+    wl = synth.WORKLOADS[name]
+    dt = wl.dtype
+    say(f"[fwd_bce workload] {wl.name}: B={wl.B} L={wl.L} G={wl.G} F_in={wl.F_in}")
+    X, W, idx = synth.draw_X(wl), synth.draw_W(wl), synth.draw_idx(wl)
+    positives = synth.draw_positives(wl)
+    tail, _ = synth.positive_neurons(wl, positives, synth.draw_perm(wl))
+    pos = synth.pos_matrix(tail, wl.B)
+    desc = hs.make_desc(wl.B, wl.F_s, wl.L, wl.G, wl.F_in, dt)
+    Xd, idxd, Wd, posd = to_dev(X), to_dev(idx), to_dev(W), to_dev(pos)
+    dY = out_tensor((wl.B, wl.L), dt)
+    dW = torch.empty((wl.L, wl.F_in), dtype=torch.float32, device="cuda")
+    db = torch.empty((wl.L,), dtype=torch.float32, device="cuda")
+    ws = hs.workspace(hs.haste_workspace_bytes(desc, hs.HASTE_OP_FWD_BCE))
+    hs.haste_fwd_bce(desc, Xd, idxd, Wd, None, posd, dY, dW, db, 0, ws)
+    _sync()
+    Xf = synth.to_f64(X, dt).astype(np.float32)
+    n = 4096
+    for r0 in sorted({0, (wl.L // 2) // wl.G * wl.G, wl.L - n}):
+        r1 = r0 + n
+        say(f"  labels [{r0}, {r1})")
+        z = orc.fwd(X, idx, W, None, wl.G, dt, r0, r1)
+        dY_ref = orc.bce_grad(z, pos - r0)           # ids outside the range are ignored
+        _check("dY", host_f32(dY[:, r0:r1].contiguous(), dt), dY_ref, dt)
+        dW_ref, db_ref = orc.bwd_w(Xf, idx[r0 // wl.G:r1 // wl.G], dY_ref.astype(np.float32), wl.G, wl.F_in, F32,
+                                   with_dbias=True)
+        _check("dW", dW[r0:r1].cpu().numpy(), dW_ref, dt)
+        _check("dbias", db[r0:r1].cpu().numpy(), db_ref, dt)
+    rng = np.random.default_rng(11)
+    bs = rng.integers(0, wl.B, 4096)
+    ls = rng.integers(0, wl.L, 4096)
+    bs = np.concatenate([bs, tail[:, 0]])            # every positive is a sample point too
+    ls = np.concatenate([ls, tail[:, 1]])
+    got = host_f32(dY[torch.from_numpy(bs).cuda(), torch.from_numpy(ls).cuda()].contiguous(), dt)
+    ref = orc.bce_grad_at(pos, wl.L, bs, ls, orc.fwd_at(X, idx, W, None, wl.G, dt, bs, ls))
+    _check("dY@rand", got, ref, dt)
+    # exact target rule over the whole output: negative entries are exactly the positives
+    neg = (dY.view(torch.bfloat16) < 0) if dt == BF16 else (dY < 0)
+    n_pos = len({(int(b), int(c)) for b, c in tail})
+    assert int(neg.sum()) == n_pos, f"{int(neg.sum())} negative entries, {n_pos} positives"
+    assert bool(neg[torch.from_numpy(tail[:, 0]).cuda(), torch.from_numpy(tail[:, 1]).cuda()].all())
+    dW2 = torch.empty_like(dW)
+    hs.haste_bwd_w(desc, Xd, idxd, dY, dW2, None, 0, hs.workspace(hs.haste_workspace_bytes(desc, hs.HASTE_OP_BWD_W)))
+    _sync()
+    assert bool((dW2 == dW).all()), "fused dW differs from haste_bwd_w on its dY"
