@@ -1,8 +1,15 @@
 """Benchmark of the group-shared fixed fan-in output layer on one MI355X.
 
-One step = the whole hot path on one batch of seeded synthetic input already resident in HBM:
-  tail forward (haste_fwd) -> head forward (haste_head_fwd) -> tail backward-weight (haste_bwd_w)
+One step = one training pass of the layer on one batch of seeded synthetic input already resident
+in HBM, with the upstream gradient formed from the step's own logits as the BCE gradient
+sigmoid(z) - y of the Section 3.3 objective (the workload's definition of dY):
+  tail forward + BCE gradient + backward-weight, fused (haste_fwd_bce)
+  -> head forward (haste_head_fwd) -> head BCE gradient in place (haste_bce_grad)
   -> tail backward-feature (haste_bwd_x) -> head backward (haste_head_bwd, adds its dX onto the tail's).
+Timed beside it, on the same inputs:
+  - the same training pass unfused: haste_fwd, haste_bce_grad, haste_bwd_w instead of haste_fwd_bce;
+  - the five separate calls on a fixed dY (haste_fwd, haste_head_fwd, haste_bwd_w, haste_bwd_x,
+    haste_head_bwd), i.e. without the loss gradient.
 Default workload: the 2.95M-label tail (G = 32, F_in = 64) with a 65,536-label dense head, B = 512,
 F_s = 768, bf16 storage with fp32 accumulation.
 
@@ -29,7 +36,10 @@ COPY_BYTES = 1 << 30            # plain device copy used to calibrate the HBM by
 
 # kernels launched by each call (symbol prefixes in rocprofv3 output)
 CALL_KERNELS = {
-    "fwd": ["k_fwd"],
+    "fwd": ["k_fwd<"],
+    "fwd_bce": ["k_transpose_x", "k_fwd_bce"],
+    "bce": ["k_bce_grad"],
+    "head_bce": ["k_bce_grad"],
     "bwd_w": ["k_transpose_x", "k_bwd_w"],
     "bwd_x": ["k_transpose_w", "k_bwd_x", "k_reduce_fmajor"],
     # the head's GEMM kernels by operand layout and epilogue (three tile sizes: 256, 128, fallback)
@@ -58,8 +68,8 @@ def parse():
     return p.parse_args()
 
 
-def call_cost(wl, dt_bytes=2):
-    """Algorithmic bytes and FLOPs of each call (each operand moved once)."""
+def call_cost(wl, dt_bytes=2, n_pos=0):
+    """Algorithmic bytes and FLOPs of each call (each operand moved once).  n_pos: positives per row."""
     B, F_s, L, F_in, H, K = wl.B, wl.F_s, wl.L, wl.F_in, wl.H, wl.K
     X = B * F_s * dt_bytes
     idx = K * F_in * 4
@@ -70,13 +80,17 @@ def call_cost(wl, dt_bytes=2):
     Wh, Yh, dWh = H * F_s * dt_bytes, B * H * dt_bytes, H * F_s * 4
     tail_flops = 2 * B * L * F_in
     head_flops = 2 * B * H * F_s
+    pos = B * n_pos * 4
     c = {
         "fwd": (X + idx + W + Y, tail_flops),
+        "fwd_bce": (X + idx + W + pos + Y + dW, 2 * tail_flops),   # writes dY (Y's size) and dW
+        "bce": (2 * Y + pos, 0),
         "bwd_w": (X + idx + Y + dW, tail_flops),
         "bwd_x": (idx + W + Y + dX, tail_flops),
     }
     if H:
         c["head_fwd"] = (X + Wh + Yh, head_flops)
+        c["head_bce"] = (2 * Yh + pos, 0)
         c["head_bwd"] = (X + Wh + Yh + dWh + 2 * dX, 2 * head_flops)
     return c
 
@@ -179,7 +193,7 @@ def summarize_traffic(fetch_db, write_db, workload, command):
     print(path)
 
 
-def cpu_baseline(wl, X, idx, W, dY, Wh, dYh):
+def cpu_baseline(wl, X, idx, W, dY, Wh, dYh, pos_tail):
     """The fp64 oracle on a bounded sample of the same workload, scaled to ms per full step."""
     import oracle
     orc = oracle.get()
@@ -188,10 +202,12 @@ def cpu_baseline(wl, X, idx, W, dY, Wh, dYh):
     nb = min(wl.B, 4)
     nh = min(wl.H, 2048)
     parts = {}
-    t = time.perf_counter(); orc.fwd(X, idx, W, None, wl.G, dt, 0, nl); parts["fwd"] = (time.perf_counter() - t) * wl.L / nl
+    t = time.perf_counter(); z = orc.fwd(X, idx, W, None, wl.G, dt, 0, nl); parts["fwd"] = (time.perf_counter() - t) * wl.L / nl
+    t = time.perf_counter(); orc.bce_grad(z, pos_tail); parts["bce"] = (time.perf_counter() - t) * wl.L / nl
+    del z
     t = time.perf_counter(); orc.bwd_w(X, idx, dY, wl.G, wl.F_in, dt, 0, nl); parts["bwd_w"] = (time.perf_counter() - t) * wl.L / nl
     t = time.perf_counter(); orc.bwd_x(idx, W, dY, wl.G, wl.F_s, dt, 0, nb); parts["bwd_x"] = (time.perf_counter() - t) * wl.B / nb
-    sample = f"tail fwd+bwd_w on labels [0,{nl}), bwd_x on rows [0,{nb})"
+    sample = f"tail fwd+BCE gradient+bwd_w on labels [0,{nl}), bwd_x on rows [0,{nb})"
     if wl.H:
         t = time.perf_counter(); orc.head_fwd(X, Wh, None, dt, 0, nh); parts["head_fwd"] = (time.perf_counter() - t) * wl.H / nh
         t = time.perf_counter(); orc.head_bwd_w(X, dYh, dt, 0, nh); tw = (time.perf_counter() - t) * wl.H / nh
@@ -258,49 +274,82 @@ def main():
         ws_h = hs.workspace(hs.haste_head_workspace_bytes(wl.B, wl.F_s, wl.H, wl.dtype))
     torch.cuda.synchronize()
 
-    calls = [("fwd", lambda: hs.haste_fwd(desc, Xd, idxd, Wd, None, Y))]
+    # positives as per-row column lists of the tail and of the head (-1 padded)
+    tail_pairs, head_pairs = synth.positive_neurons(wl, pos, perm)
+    n_pos = pos.shape[1]
+    posd = up(synth.pos_matrix(tail_pairs, wl.B, n_pos))
+    dYt = torch.empty((wl.B, wl.L), dtype=odt, device=dev)   # the training step's own dY
+    ws_f = hs.workspace(hs.haste_workspace_bytes(desc, hs.HASTE_OP_FWD_BCE))
     if wl.H:
-        calls.append(("head_fwd", lambda: hs.haste_head_fwd(wl.B, wl.F_s, wl.H, wl.dtype, Xd, Whd, None, Yh)))
-    calls.append(("bwd_w", lambda: hs.haste_bwd_w(desc, Xd, idxd, dYd, dW, None, 0, ws_w)))
-    calls.append(("bwd_x", lambda: hs.haste_bwd_x(desc, idxd, Wd, dYd, dX, 0, ws_x)))
-    if wl.H:
-        calls.append(("head_bwd", lambda: hs.haste_head_bwd(wl.B, wl.F_s, wl.H, wl.dtype, Xd, Whd, dYhd, dWh, dX,
-                                                            1, ws_h)))
-
-    for _ in range(args.warmup):
-        for _, fn in calls:
-            fn()
+        posh = up(synth.pos_matrix(head_pairs, wl.B, n_pos))
+        dYht = torch.empty((wl.B, wl.H), dtype=odt, device=dev)
     torch.cuda.synchronize()
 
-    # timed region: K steps, events between the calls on the launch stream
+    def head_train():
+        return [("head_fwd", lambda: hs.haste_head_fwd(wl.B, wl.F_s, wl.H, wl.dtype, Xd, Whd, None, Yh)),
+                ("head_bce", lambda: hs.haste_bce_grad(wl.B, wl.H, wl.dtype, Yh, posh, dYht))] if wl.H else []
+
+    def head_back(dyh):
+        return [("head_bwd", lambda: hs.haste_head_bwd(wl.B, wl.F_s, wl.H, wl.dtype, Xd, Whd, dyh, dWh, dX, 1,
+                                                       ws_h))] if wl.H else []
+
+    fused = ([("fwd_bce", lambda: hs.haste_fwd_bce(desc, Xd, idxd, Wd, None, posd, dYt, dW, None, 0, ws_f))] +
+             head_train() + [("bwd_x", lambda: hs.haste_bwd_x(desc, idxd, Wd, dYt, dX, 0, ws_x))] +
+             (head_back(dYht) if wl.H else []))
+    unfused = ([("fwd", lambda: hs.haste_fwd(desc, Xd, idxd, Wd, None, Y)),
+                ("bce", lambda: hs.haste_bce_grad(wl.B, wl.L, wl.dtype, Y, posd, dYt))] + head_train() +
+               [("bwd_w", lambda: hs.haste_bwd_w(desc, Xd, idxd, dYt, dW, None, 0, ws_w)),
+                ("bwd_x", lambda: hs.haste_bwd_x(desc, idxd, Wd, dYt, dX, 0, ws_x))] +
+               (head_back(dYht) if wl.H else []))
+    separate = [("fwd", lambda: hs.haste_fwd(desc, Xd, idxd, Wd, None, Y))]
+    if wl.H:
+        separate.append(("head_fwd", lambda: hs.haste_head_fwd(wl.B, wl.F_s, wl.H, wl.dtype, Xd, Whd, None, Yh)))
+    separate.append(("bwd_w", lambda: hs.haste_bwd_w(desc, Xd, idxd, dYd, dW, None, 0, ws_w)))
+    separate.append(("bwd_x", lambda: hs.haste_bwd_x(desc, idxd, Wd, dYd, dX, 0, ws_x)))
+    separate += head_back(dYhd) if wl.H else []
+
     stream = torch.cuda.current_stream()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(calls) + 1)] for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    w0 = time.perf_counter()
-    for s in range(args.steps):
-        evs[s][0].record(stream)
-        for i, (_, fn) in enumerate(calls):
-            fn()
-            evs[s][i + 1].record(stream)
-    torch.cuda.synchronize()
-    wall_ms = (time.perf_counter() - w0) * 1e3
-    per_call = {name: 0.0 for name, _ in calls}
-    step_ms = 0.0
-    for s in range(args.steps):
-        step_ms += evs[s][0].elapsed_time(evs[s][-1])
-        for i, (name, _) in enumerate(calls):
-            per_call[name] += evs[s][i].elapsed_time(evs[s][i + 1])
-    step_ms /= args.steps
-    per_call = {k: v / args.steps for k, v in per_call.items()}
 
-    cost = call_cost(wl, 2 if is_bf else 4)
-    step_bytes = sum(b for b, _ in cost.values())
-    step_flops = sum(f for _, f in cost.values())
-    per_call_detail = {}
-    for name, ms in per_call.items():
-        b, f = cost[name]
-        per_call_detail[name] = {"ms": round(ms, 4), "GBps": round(b / ms / 1e6, 1),
-                                 "TFLOPs": round(f / ms / 1e9, 1), "alg_bytes": b, "flops": f}
+    def timed(calls):
+        """K steps after W warm-up steps; events between the calls on the launch stream."""
+        for _ in range(args.warmup):
+            for _, fn in calls:
+                fn()
+        torch.cuda.synchronize()
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(calls) + 1)] for _ in range(args.steps)]
+        torch.cuda.synchronize()
+        w0 = time.perf_counter()
+        for s in range(args.steps):
+            evs[s][0].record(stream)
+            for i, (_, fn) in enumerate(calls):
+                fn()
+                evs[s][i + 1].record(stream)
+        torch.cuda.synchronize()
+        wall = (time.perf_counter() - w0) * 1e3 / args.steps
+        per = {name: 0.0 for name, _ in calls}
+        step = 0.0
+        for s in range(args.steps):
+            step += evs[s][0].elapsed_time(evs[s][-1])
+            for i, (name, _) in enumerate(calls):
+                per[name] += evs[s][i].elapsed_time(evs[s][i + 1])
+        return step / args.steps, {k: v / args.steps for k, v in per.items()}, wall
+
+    cost = call_cost(wl, 2 if is_bf else 4, n_pos)
+
+    def detail(per):
+        d = {}
+        for name, ms in per.items():
+            b, f = cost[name]
+            d[name] = {"ms": round(ms, 4), "GBps": round(b / ms / 1e6, 1), "TFLOPs": round(f / ms / 1e9, 1),
+                       "alg_bytes": b, "flops": f}
+        return d
+
+    sep_ms, sep_per, _ = timed(separate)
+    unf_ms, unf_per, _ = timed(unfused)
+    step_ms, per_call, wall_ms = timed(fused)
+
+    step_bytes = sum(cost[k][0] for k in per_call)
+    step_flops = sum(cost[k][1] for k in per_call)
     dom = max(per_call, key=per_call.get)
     db, df = cost[dom]
     achieved = db / per_call[dom] / 1e6
@@ -315,20 +364,32 @@ def main():
         "ms_per_step": round(step_ms, 4), "higher_is_better": False, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16" if is_bf else "f32", "data": "synthetic (seeded; see synth/)",
         "config": {"workload": wl.name, "B": wl.B, "F_s": wl.F_s, "L_tail": wl.L, "G": wl.G, "F_in": wl.F_in,
-                   "H_head": wl.H, "parallelism": "single GPU"},
+                   "H_head": wl.H, "positives_per_row": int(n_pos), "parallelism": "single GPU"},
+        "step": "training pass: fused tail forward + BCE gradient + backward-weight, head forward + BCE "
+                "gradient, tail backward-feature, head backward",
         "labels_samples_per_s": round(wl.B * (wl.L + wl.H) / (step_ms / 1e3), 1),
+        "step_alg_bytes": step_bytes,
         "step_hbm_GBps": round(step_bytes / step_ms / 1e6, 1),
         "step_hbm_frac": round(step_bytes / step_ms / 1e6 / HBM_PEAK_GBPS, 4),
         "step_mfma_pct": round(100 * step_flops / (step_ms / 1e3) / (MFMA_BF16_PEAK_TFLOPS * 1e12), 2),
-        "wall_ms_per_step": round(wall_ms / args.steps, 4),
-        "per_call": per_call_detail,
+        "wall_ms_per_step": round(wall_ms, 4),
+        "per_call": detail(per_call),
         "roofline": roof,
+        "unfused_training_step": {"ms": round(unf_ms, 4), "per_call": detail(unf_per),
+                                  "what": "haste_fwd + haste_bce_grad + haste_bwd_w in place of haste_fwd_bce"},
+        "separate_calls_step": {
+            "ms": round(sep_ms, 4), "per_call": detail(sep_per),
+            "step_alg_bytes": sum(cost[k][0] for k in sep_per),
+            "step_hbm_frac": round(sum(cost[k][0] for k in sep_per) / sep_ms / 1e6 / HBM_PEAK_GBPS, 4),
+            "what": "haste_fwd, haste_head_fwd, haste_bwd_w, haste_bwd_x, haste_head_bwd on a fixed dY (no loss gradient)"},
     }
 
     if not args.no_bottleneck and is_bf:
         out["dense_bottleneck"] = bottleneck(wl, Xd, Wd, dYd, args)
-        out["tail_vs_bottleneck"] = round(sum(per_call[k] for k in ("fwd", "bwd_w", "bwd_x")) /
+        out["tail_vs_bottleneck"] = round(sum(per_call[k] for k in ("fwd_bce", "bwd_x")) /
                                           out["dense_bottleneck"]["ms"], 3)
+        out["separate_calls_step"]["tail_vs_bottleneck"] = round(
+            sum(sep_per[k] for k in ("fwd", "bwd_w", "bwd_x")) / out["dense_bottleneck"]["ms"], 3)
     if args.copy_calibration:
         src = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device=dev).fill_(1.0)
         dst = torch.empty_like(src)
@@ -338,7 +399,7 @@ def main():
         del src, dst
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(wl, X, idx, W, dY, Wh, dYh)
+        out["cpu_baseline"] = cpu_baseline(wl, X, idx, W, dY, Wh, dYh, synth.pos_matrix(tail_pairs, wl.B, n_pos))
     print(json.dumps(out), flush=True)
 
 

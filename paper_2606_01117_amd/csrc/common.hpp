@@ -106,8 +106,10 @@ struct Buf {
 // Gradient of the binary cross-entropy of sigmoid(z) against a 0/1 target with respect to the
 // logit z (Section 3.3 objective): sigmoid(z) - y, in fp32.  exp(-z) overflows to +inf for very
 // negative z, which gives sigmoid 0 as it should.
+__device__ __forceinline__ float sigmoid_f32(float z) { return __builtin_amdgcn_rcpf(1.0f + __expf(-z)); }
+
 __device__ __forceinline__ float bce_grad_f32(float z, bool positive) {
-    const float sg = __builtin_amdgcn_rcpf(1.0f + __expf(-z));
+    const float sg = sigmoid_f32(z);
     return positive ? sg - 1.0f : sg;
 }
 

@@ -524,9 +524,9 @@ __global__ __launch_bounds__(512) void k_bwd_w2(const bf16_t *__restrict__ Xb, c
 // Forward with the BCE-gradient epilogue, and the backward-weight product of that gradient in the
 // same pass (Section 3.2 forward and backward-weight; Section 3.3 objective).  The logits are not
 // stored: the output is dY = sigmoid(z) - T, and dW = dY^T H_k is formed from the dY registers.
-// The workgroup layout is the slab-staged backward-weight one: 8 waves take UPW consecutive units
-// each (a contiguous span of at most 512 labels) and sweep the batch in 32-row slabs, with the X^T
-// block of each slab staged in LDS.  A wave keeps its units' weights in registers for the sweep,
+// The workgroup layout follows the slab-staged backward-weight kernel: NW waves take one unit each
+// (a contiguous span of at most 512 labels) and sweep the batch in 32-row slabs, with the X^T
+// block of each slab staged in LDS.  A wave keeps its unit's weights in registers for the sweep,
 // so W is read from memory once.  Per unit and slab, with v_mfma_f32_16x16x32_bf16:
 //   forward, M = 16 rows, N = 16 labels, K = 32 slots:
 //     A = the gathered support columns, two ds_read_b64_tr_b16 per 32-slot step.  Source lane
@@ -538,26 +538,28 @@ __global__ __launch_bounds__(512) void k_bwd_w2(const bf16_t *__restrict__ Xb, c
 //   backward-weight product (K = rows 8q .. 8q+7, N = label), which thus never leaves the
 //   registers; that product and its A operand are the backward-weight kernel's, in the same
 //   order, so dW equals what haste_bwd_w computes from the stored dY, bit for bit.
-//   dY leaves through a per-wave LDS buffer as 128-byte row pieces (8 rows per store): adjacent
-//   lanes swap halves (DPP) so that each writes two labels of four rows as 4-byte words.
+// dY: adjacent lanes swap halves (DPP) so that each writes two labels of four rows as 4-byte
+// words into the slab's [32 rows][512 labels] LDS block.  The block's 32-byte column blocks are
+// XOR-permuted by row / 8 (the lanes of one write instruction then hit distinct banks), and the
+// whole block leaves as 1 KB row runs, cooperatively, in the next slab's barrier window: one row
+// per store instruction, the pattern the DRAM pages serve fastest.
 // Targets: the slab's positives that fall in the workgroup's span are set as bits of an LDS
 // bitmap, one 32-bit word of rows per label.  Two bitmaps alternate by slab parity: in one
 // barrier interval each thread clears its word of the previous slab's bitmap and sets the
 // current slab's bits, and the bitmap is read only after the next barrier.
 // --------------------------------------------------------------------------------------------
-constexpr int kFbWaves = 8;
-constexpr int kFbMaxSpan = 512;                 // labels per workgroup at most (16 units of 32)
+constexpr int kFbMaxSpan = 512;                 // labels per workgroup at most
 constexpr int kFbMaxPos = 64;                   // positives per row the slab prefetch holds
-constexpr int kFbPosLoads = 32 * kFbMaxPos / (kFbWaves * 64);
+constexpr int kFbYRow = 1056;                   // bytes per staged dY row: 512 labels + 32 pad
 
-__host__ __device__ constexpr int fb_upw(int F_in) { return F_in == 128 ? 1 : 2; }
-__host__ __device__ constexpr int fb_ys(int F_in) { return fb_upw(F_in) * 64 + 16; }   // staged dY row bytes
+// waves per workgroup: one 32-label unit each; 128-slot supports need twice the registers
+__host__ __device__ constexpr int fb_waves(int F_in) { return F_in == 128 ? 8 : 16; }
 
-// X^T block, both bitmaps and the per-wave dY staging, or at the end the per-wave dW staging
+// X^T block, both bitmaps and the staged dY block, or at the end the dW staging of half the waves
 static size_t fb_lds(int F_s, int F_in) {
     const size_t main = (size_t)haste::round_up((int64_t)F_s * kBw2XRow, 16) + 2 * kFbMaxSpan * 4 +
-                        (size_t)kFbWaves * 32 * fb_ys(F_in);
-    const size_t out = (size_t)kFbWaves * 32 * (F_in + 4) * 4;
+                        (size_t)32 * kFbYRow;
+    const size_t out = (size_t)(fb_waves(F_in) / 2) * 32 * (F_in + 4) * 4;
     return main > out ? main : out;
 }
 
@@ -565,26 +567,35 @@ __device__ __forceinline__ uint32_t dpp_swap_pairs(uint32_t v) {   // lane l rec
     return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0xB1, 0xF, 0xF, false);   // quad_perm [1, 0, 3, 2]
 }
 
-template <int F_IN, bool HAS_BIAS, bool WITH_DW>
-__global__ __launch_bounds__(512) void k_fwd_bce(const bf16_t *__restrict__ Xb, const int32_t *__restrict__ idx,
-                                                 const bf16_t *__restrict__ W, const float *__restrict__ bias,
-                                                 const int32_t *__restrict__ pos, int P, bf16_t *__restrict__ dY,
-                                                 float *__restrict__ dW, float *__restrict__ dbias, int beta, int B,
-                                                 int Bp, int F_s, int64_t L, int G, int64_t K) {
+// byte offset of dword d of staged dY row r (32-byte column blocks permuted by r / 8)
+__device__ __forceinline__ int fb_ystg_off(int r, int d) { return r * kFbYRow + 4 * (d ^ (8 * (r >> 3))); }
+
+// XS: F_s <= kFbSmallFs (fewer X^T prefetch registers)
+constexpr int kFbSmallFs = 768;
+
+template <int F_IN, bool HAS_BIAS, bool WITH_DW, bool WITH_DB, bool XS>
+__global__ __launch_bounds__(64 * fb_waves(F_IN)) void k_fwd_bce(
+    const bf16_t *__restrict__ Xb, const int32_t *__restrict__ idx, const bf16_t *__restrict__ W,
+    const float *__restrict__ bias, const int32_t *__restrict__ pos, int P, bf16_t *__restrict__ dY,
+    float *__restrict__ dW, float *__restrict__ dbias, int beta, int B, int Bp, int F_s, int64_t L, int G,
+    int64_t K) {
     extern __shared__ __align__(16) char fbs[];
-    constexpr int UPW = fb_upw(F_IN);
+    constexpr int NW = fb_waves(F_IN);
+    constexpr int NT = NW * 64;                 // threads
     constexpr int KS = F_IN / 32;               // forward K-steps (32 slots)
     constexpr int NST = F_IN / 16;              // backward-weight M-tiles (16 slots)
-    constexpr int YS = fb_ys(F_IN);
+    constexpr int XL = (XS ? kFbSmallFs : kMaxFs) * 4 / NT;   // 16-byte X^T loads per thread and slab
+    constexpr int PL = 32 * kFbMaxPos / NT;     // positives per thread and slab
+    constexpr int YL = 32 * 64 / NT;            // 16-byte dY stores per thread and slab
     char *xs = fbs;
     uint32_t *bm = reinterpret_cast<uint32_t *>(fbs + ((F_s * kBw2XRow + 15) & ~15));
+    char *ystg = reinterpret_cast<char *>(bm + 2 * kFbMaxSpan);
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    char *ystg = reinterpret_cast<char *>(bm + 2 * kFbMaxSpan) + wave * 32 * YS;
     const int l16 = lane & 15, q = lane >> 4;
     const int ntn = (G + 31) >> 5;
     const int64_t nunits = K * ntn;
-    const int64_t u0 = (int64_t)blockIdx.x * (kFbWaves * UPW);
+    const int64_t u0 = (int64_t)blockIdx.x * NW;
     auto lab_of = [&](int64_t v) {
         const int64_t k = v / ntn;
         return k * G + 32 * (int)(v - k * ntn);
@@ -593,222 +604,220 @@ __global__ __launch_bounds__(512) void k_fwd_bce(const bf16_t *__restrict__ Xb, 
         const int t = (int)(v % ntn);
         return G - 32 * t < 32 ? G - 32 * t : 32;
     };
-    const int64_t ul = u0 + kFbWaves * UPW - 1 < nunits ? u0 + kFbWaves * UPW - 1 : nunits - 1;
+    const int64_t ul = u0 + NW - 1 < nunits ? u0 + NW - 1 : nunits - 1;
     const int64_t lab0 = lab_of(u0);
     const int span = (int)(lab_of(ul) + nlab_of(ul) - lab0);
 
-    // this wave's units (a unit past the end repeats the last one and is never stored), their
-    // supports in both operand roles, weights and biases
-    int64_t vu[UPW];
-    int off[UPW], nl[UPW], col[UPW];
-    int fa[UPW][KS][2];     // forward gather: slot 32 s + 8 q + 4 h + l16 / 4
-    int fw[UPW][NST];       // backward-weight A operand: slot 16 st + l16
-    uint4 wop[UPW][2][KS];  // W[label 16 nt + l16][32 s + 8 q .. +7]
-    float bl[UPW][2];
+    // this wave's unit (past the end: a repeat of the last one, never stored), its supports in
+    // both operand roles, weights and biases
+    const int64_t v = u0 + wave;
+    const int64_t vu = v < nunits ? v : nunits - 1;
+    const int64_t lb = lab_of(vu);
+    const int off = (int)(lb - lab0);
+    const int nl = v < nunits ? nlab_of(vu) : 0;
+    int fa[KS][2];     // forward gather: slot 32 s + 8 q + 4 h + l16 / 4
+    int fw[NST];       // backward-weight A operand: slot 16 st + l16
+    uint4 wop[2][KS];  // W[label 16 nt + l16][32 s + 8 q .. +7]
+    float bl[2];
     const int aq = l16 & 3;
-#pragma unroll
-    for (int j = 0; j < UPW; ++j) {
-        const int64_t v = u0 + UPW * wave + j;
-        vu[j] = v < nunits ? v : nunits - 1;
-        off[j] = (int)(lab_of(vu[j]) - lab0);
-        nl[j] = v < nunits ? nlab_of(vu[j]) : 0;
-        col[j] = j == 0 ? 0 : col[j - 1] + nl[j - 1];
-        const int64_t k = vu[j] / ntn;
-        const int32_t *ik = idx + k * F_IN;
+    {
+        const int32_t *ik = idx + (vu / ntn) * F_IN;
 #pragma unroll
         for (int s = 0; s < KS; ++s)
 #pragma unroll
-            for (int h = 0; h < 2; ++h) fa[j][s][h] = ik[32 * s + 8 * q + 4 * h + (l16 >> 2)];
+            for (int h = 0; h < 2; ++h) fa[s][h] = ik[32 * s + 8 * q + 4 * h + (l16 >> 2)];
 #pragma unroll
-        for (int st = 0; st < NST; ++st) fw[j][st] = ik[16 * st + l16];
-        const int64_t lb = lab_of(vu[j]);
-        const Buf wb(W + lb * F_IN, (uint32_t)(nlab_of(vu[j]) * F_IN * 2));
+        for (int st = 0; st < NST; ++st) fw[st] = ik[16 * st + l16];
+        const int nv = nlab_of(vu);
+        const Buf wb(W + lb * F_IN, (uint32_t)(nv * F_IN * 2));
 #pragma unroll
         for (int nt = 0; nt < 2; ++nt) {
 #pragma unroll
             for (int s = 0; s < KS; ++s)
-                wop[j][nt][s] = wb.ld16((uint32_t)(((16 * nt + l16) * F_IN + 32 * s + 8 * q) * 2));
-            bl[j][nt] = 0.0f;
-            if constexpr (HAS_BIAS) {
-                const int t = 16 * nt + l16;
-                bl[j][nt] = t < nlab_of(vu[j]) ? bias[lb + t] : 0.0f;
-            }
+                wop[nt][s] = wb.ld16((uint32_t)(((16 * nt + l16) * F_IN + 32 * s + 8 * q) * 2));
+            const int t = 16 * nt + l16;
+            bl[nt] = HAS_BIAS && t < nv ? bias[lb + t] : 0.0f;
         }
     }
 
     // cooperative slab loads: the X^T block (4 F_s chunks of 16 bytes) and the slab's positives
     const int nxc = 4 * F_s;
-    uint4 xr[kBw2MaxXLoads];
-    uint32_t pr[kFbPosLoads];
+    uint4 xr[XL];
+    uint32_t pr[PL];
     auto load = [&](int blk) {
         const Buf xb(Xb + (int64_t)blk * F_s * 32, (uint32_t)(nxc * 16));
 #pragma unroll
-        for (int i = 0; i < kBw2MaxXLoads; ++i) xr[i] = xb.ld16((uint32_t)(tid + 512 * i) * 16);   // past the block: zero
+        for (int i = 0; i < XL; ++i) xr[i] = xb.ld16((uint32_t)(tid + NT * i) * 16);   // past the block: zero
         const int b0 = blk * 32;
         const int rows = B - b0 < 32 ? B - b0 : 32;
         const Buf pb(pos + (int64_t)b0 * P, (uint32_t)(rows > 0 ? rows * P * 4 : 0));
 #pragma unroll
-        for (int i = 0; i < kFbPosLoads; ++i) pr[i] = pb.ld4((uint32_t)(tid + 512 * i) * 4);   // validity checked at use
+        for (int i = 0; i < PL; ++i) pr[i] = pb.ld4((uint32_t)(tid + NT * i) * 4);   // validity checked at use
     };
-    auto store = [&](int blk) {
+    auto stage_slab = [&](int blk) {
 #pragma unroll
-        for (int i = 0; i < kBw2MaxXLoads; ++i) {
-            const int c = tid + 512 * i;
+        for (int i = 0; i < XL; ++i) {
+            const int c = tid + NT * i;
             if (c < nxc) *reinterpret_cast<uint4 *>(xs + (c >> 2) * kBw2XRow + (c & 3) * 16) = xr[i];
         }
         // clear this thread's word of the previous slab's bitmap, set the current slab's targets
         uint32_t *cur = bm + (blk & 1) * kFbMaxSpan;
-        bm[((blk + 1) & 1) * kFbMaxSpan + tid] = 0u;
+        if (tid < kFbMaxSpan) bm[((blk + 1) & 1) * kFbMaxSpan + tid] = 0u;
         const int rows = B - blk * 32 < 32 ? B - blk * 32 : 32;
 #pragma unroll
-        for (int i = 0; i < kFbPosLoads; ++i) {
-            const int e = tid + 512 * i;
+        for (int i = 0; i < PL; ++i) {
+            const int e = tid + NT * i;
             if (e < rows * P) {
                 const int64_t o = (int64_t)(int32_t)pr[i] - lab0;
                 if (o >= 0 && o < span) atomicOr(cur + o, 1u << (e / P));
             }
         }
     };
-
-    f32x4_t acc[UPW][NST][2], db[UPW][2];
+    // the staged dY block of slab blk leaves as 1 KB row runs: 64 chunks of 16 bytes per row
+    auto store_slab = [&](int blk) {
+        const int b0 = blk * 32;
+        const int rows = B - b0 < 32 ? B - b0 : 32;
+        const Buf yo(dY + (int64_t)b0 * L + lab0, (uint32_t)(rows * L * 2));
 #pragma unroll
-    for (int j = 0; j < UPW; ++j) {
-#pragma unroll
-        for (int nt = 0; nt < 2; ++nt) {
-            db[j][nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int st = 0; st < NST; ++st) acc[j][st][nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        for (int i = 0; i < YL; ++i) {
+            const int c = tid + NT * i, r = c >> 6, ch = c & 63;
+            const uint4 val = *reinterpret_cast<const uint4 *>(ystg + fb_ystg_off(r, 4 * ch));
+            const uint32_t o = r < rows && 8 * ch < span ? (uint32_t)(((int64_t)r * L + 8 * ch) * 2) : kOob;
+            yo.st16<kStreaming>(val, o);
         }
+    };
+
+    f32x4_t acc[NST][2], db[2];
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt) {
+        db[nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int st = 0; st < NST; ++st) acc[st][nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     }
     const bf16x8_t ones = as_bf16x8(make_uint4(0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u));
     const bool odd = (l16 & 1) != 0;
 
-    // dY stores of the wave's units: LPR lanes per staged row (16 bytes each), RPS rows per store
-    constexpr int LPR = UPW * 4;
-    constexpr int RPS = 64 / LPR;
-    constexpr int SPT = 32 / RPS;
-    const int sr = lane / LPR, sc = lane % LPR;
-    const int width = col[UPW - 1] + nl[UPW - 1];
-    const int64_t labw = lab0 + off[0];
-    const bool sok = 8 * sc < width;
-
-    for (int i = tid; i < 2 * kFbMaxSpan; i += kFbWaves * 64) bm[i] = 0u;
+    for (int i = tid; i < 2 * kFbMaxSpan; i += NT) bm[i] = 0u;
     const int nblk = Bp / 32;
     load(0);
     for (int blk = 0; blk < nblk; ++blk) {
-        __syncthreads();   // the previous slab is no longer read
-        store(blk);
+        __syncthreads();   // the previous slab is no longer read, and its dY block is staged
+        if (blk > 0) store_slab(blk - 1);
+        stage_slab(blk);
         __syncthreads();
         if (blk + 1 < nblk) load(blk + 1);
         const uint32_t *cur = bm + (blk & 1) * kFbMaxSpan;
-        const int b0 = blk * 32;
-        const int rows = B - b0 < 32 ? B - b0 : 32;
+        const int rows = B - blk * 32 < 32 ? B - blk * 32 : 32;
+        // forward: z^T tile [32 rows][32 labels] of the unit
+        f32x4_t z[2][2];
 #pragma unroll
-        for (int j = 0; j < UPW; ++j) {
-            // forward: z^T tile [32 rows][32 labels] of unit j
-            f32x4_t z[2][2];
+        for (int m = 0; m < 2; ++m)
 #pragma unroll
-            for (int m = 0; m < 2; ++m)
+            for (int nt = 0; nt < 2; ++nt) z[m][nt] = f32x4_t{bl[nt], bl[nt], bl[nt], bl[nt]};
 #pragma unroll
-                for (int nt = 0; nt < 2; ++nt) z[m][nt] = f32x4_t{bl[j][nt], bl[j][nt], bl[j][nt], bl[j][nt]};
+        for (int s = 0; s < KS; ++s) {
 #pragma unroll
-            for (int s = 0; s < KS; ++s) {
+            for (int m = 0; m < 2; ++m) {
+                const uint2 lo = lds_read_tr(xs + fa[s][0] * kBw2XRow + 16 * aq + 8 * m);
+                const uint2 hi = lds_read_tr(xs + fa[s][1] * kBw2XRow + 16 * aq + 8 * m);
+                const bf16x8_t av = as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y));
 #pragma unroll
-                for (int m = 0; m < 2; ++m) {
-                    const uint2 lo = lds_read_tr(xs + fa[j][s][0] * kBw2XRow + 16 * aq + 8 * m);
-                    const uint2 hi = lds_read_tr(xs + fa[j][s][1] * kBw2XRow + 16 * aq + 8 * m);
-                    const bf16x8_t av = as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y));
-#pragma unroll
-                    for (int nt = 0; nt < 2; ++nt) z[m][nt] = mfma16x16x32(av, as_bf16x8(wop[j][nt][s]), z[m][nt]);
-                }
-            }
-            // epilogue: dY = sigmoid(z) - T for rows 8q .. 8q+7 of label 16 nt + l16 (zero on rows past B)
-            uint4 yb[2];
-#pragma unroll
-            for (int nt = 0; nt < 2; ++nt) {
-                const int t = 16 * nt + l16;
-                const uint32_t tw = t < nl[j] ? cur[off[j] + t] >> (8 * q) : 0u;
-                float d[8];
-#pragma unroll
-                for (int r = 0; r < 8; ++r) {
-                    const float zz = z[r >> 2][nt][r & 3];
-                    d[r] = 8 * q + r < rows ? bce_grad_f32(zz, (tw >> r) & 1u) : 0.0f;
-                }
-                yb[nt] = make_uint4(pack_bf16(d[0], d[1]), pack_bf16(d[2], d[3]), pack_bf16(d[4], d[5]),
-                                    pack_bf16(d[6], d[7]));
-            }
-            // stage: even lanes write rows 8q .. 8q+3 of labels (t, t+1), odd lanes rows 8q+4 .. +7 of (t-1, t)
-#pragma unroll
-            for (int nt = 0; nt < 2; ++nt) {
-                if (16 * nt >= nl[j]) continue;   // wave-uniform: groups are whole 16-label tiles
-                const uint4 v = yb[nt];
-                const uint32_t r0 = dpp_swap_pairs(odd ? v.x : v.z);
-                const uint32_t r1 = dpp_swap_pairs(odd ? v.y : v.w);
-                const uint32_t L0 = odd ? r0 : v.x, H0 = odd ? v.z : r0;
-                const uint32_t L1 = odd ? r1 : v.y, H1 = odd ? v.w : r1;
-                char *p = ystg + (8 * q + (odd ? 4 : 0)) * YS + (col[j] + 16 * nt + (l16 & ~1)) * 2;
-                *reinterpret_cast<uint32_t *>(p) = (L0 & 0xffffu) | (H0 << 16);
-                *reinterpret_cast<uint32_t *>(p + YS) = (L0 >> 16) | (H0 & 0xffff0000u);
-                *reinterpret_cast<uint32_t *>(p + 2 * YS) = (L1 & 0xffffu) | (H1 << 16);
-                *reinterpret_cast<uint32_t *>(p + 3 * YS) = (L1 >> 16) | (H1 & 0xffff0000u);
-            }
-            if constexpr (WITH_DW) {
-#pragma unroll
-                for (int st = 0; st < NST; ++st) {
-                    const uint4 xv = *reinterpret_cast<const uint4 *>(xs + fw[j][st] * kBw2XRow + q * 16);
-#pragma unroll
-                    for (int nt = 0; nt < 2; ++nt)
-                        acc[j][st][nt] = mfma16x16x32(as_bf16x8(xv), as_bf16x8(yb[nt]), acc[j][st][nt]);
-                }
-                if (dbias) {
-#pragma unroll
-                    for (int nt = 0; nt < 2; ++nt) db[j][nt] = mfma16x16x32(ones, as_bf16x8(yb[nt]), db[j][nt]);
-                }
+                for (int nt = 0; nt < 2; ++nt) z[m][nt] = mfma16x16x32(av, as_bf16x8(wop[nt][s]), z[m][nt]);
             }
         }
-        // the wave's [32 rows][width] dY block leaves as 16-byte pieces, LPR lanes per row
-        const Buf yo(dY + (int64_t)b0 * L + labw, (uint32_t)(rows * L * 2));
+        // epilogue: dY = sigmoid(z) - T for rows 8q .. 8q+7 of label 16 nt + l16, zero on rows past B.
+        // Branch-free per element (so that the exp / rcp chains of the 16 values interleave); the
+        // row mask is needed only in a last, partial slab and the targets only where a positive
+        // falls in the tile, both wave-uniform tests.  The bitmap word of a label past the unit
+        // lies inside the 512-word bitmap and is never used.
+        uint4 yb[2];
 #pragma unroll
-        for (int p = 0; p < SPT; ++p) {
-            const int r = RPS * p + sr;
-            const uint4 v = *reinterpret_cast<const uint4 *>(ystg + r * YS + sc * 16);
-            const uint32_t o = sok && r < rows ? (uint32_t)(((int64_t)r * L + 8 * sc) * 2) : kOob;
-            yo.st16<kStreaming>(v, o);
+        for (int nt = 0; nt < 2; ++nt) {
+            const uint32_t tw = cur[off + 16 * nt + l16] >> (8 * q);
+            float d[8];
+#pragma unroll
+            for (int r = 0; r < 8; ++r) d[r] = sigmoid_f32(z[r >> 2][nt][r & 3]);
+            if (rows < 32) {
+#pragma unroll
+                for (int r = 0; r < 8; ++r) d[r] = 8 * q + r < rows ? d[r] : 0.0f;
+            }
+            if (__builtin_amdgcn_ballot_w64((tw & 0xffu) != 0u) != 0) {
+#pragma unroll
+                for (int r = 0; r < 8; ++r) d[r] -= (float)((tw >> r) & 1u);
+            }
+            yb[nt] = make_uint4(pack_bf16(d[0], d[1]), pack_bf16(d[2], d[3]), pack_bf16(d[4], d[5]),
+                                pack_bf16(d[6], d[7]));
+        }
+        // stage: even lanes write rows 8q .. 8q+3 of labels (t, t+1), odd lanes rows 8q+4 .. +7 of (t-1, t)
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt) {
+            if (16 * nt >= nl) continue;   // wave-uniform: groups are whole 16-label tiles
+            const uint4 y = yb[nt];
+            const uint32_t r0 = dpp_swap_pairs(odd ? y.x : y.z);
+            const uint32_t r1 = dpp_swap_pairs(odd ? y.y : y.w);
+            const uint32_t L0 = odd ? r0 : y.x, H0 = odd ? y.z : r0;
+            const uint32_t L1 = odd ? r1 : y.y, H1 = odd ? y.w : r1;
+            const int row = 8 * q + (odd ? 4 : 0);
+            const int dw = (off + 16 * nt + (l16 & ~1)) >> 1;
+            char *p = ystg + fb_ystg_off(row, dw);   // rows row .. row+3 share the column permutation
+            // low halves of (L, H), then high halves: one byte permute each
+            *reinterpret_cast<uint32_t *>(p) = __builtin_amdgcn_perm(H0, L0, 0x05040100u);
+            *reinterpret_cast<uint32_t *>(p + kFbYRow) = __builtin_amdgcn_perm(H0, L0, 0x07060302u);
+            *reinterpret_cast<uint32_t *>(p + 2 * kFbYRow) = __builtin_amdgcn_perm(H1, L1, 0x05040100u);
+            *reinterpret_cast<uint32_t *>(p + 3 * kFbYRow) = __builtin_amdgcn_perm(H1, L1, 0x07060302u);
+        }
+        if constexpr (WITH_DW) {
+#pragma unroll
+            for (int st = 0; st < NST; ++st) {
+                const uint4 xv = *reinterpret_cast<const uint4 *>(xs + fw[st] * kBw2XRow + q * 16);
+#pragma unroll
+                for (int nt = 0; nt < 2; ++nt) acc[st][nt] = mfma16x16x32(as_bf16x8(xv), as_bf16x8(yb[nt]), acc[st][nt]);
+            }
+            if constexpr (WITH_DB) {
+#pragma unroll
+                for (int nt = 0; nt < 2; ++nt) db[nt] = mfma16x16x32(ones, as_bf16x8(yb[nt]), db[nt]);
+            }
         }
     }
+    __syncthreads();   // the last slab's dY block is staged
+    store_slab(nblk - 1);
 
     if constexpr (WITH_DW) {
-        // dW: as in the backward-weight kernel, each wave stages its unit's [32 labels][F_IN] fp32
-        // block in LDS and writes it as whole contiguous runs; dbias from the q = 0 lanes.
-        __syncthreads();   // every wave is done with the staged slabs
+        // dW: as in the backward-weight kernel, a wave stages its unit's [32 labels][F_IN] fp32 block
+        // in LDS and writes it as whole contiguous runs; half the waves at a time.  dbias from the
+        // q = 0 lanes.
         constexpr int OS = F_IN + 4;
-        float *ostg = reinterpret_cast<float *>(fbs) + wave * 32 * OS;
+        float *ostg = reinterpret_cast<float *>(fbs) + (wave % (NW / 2)) * 32 * OS;
+        const Buf ob(dW + lb * F_IN, (uint32_t)(nl * F_IN * 4));   // this unit's labels only
 #pragma unroll
-        for (int j = 0; j < UPW; ++j) {
-            const int64_t lb = lab_of(vu[j]);
+        for (int half = 0; half < 2; ++half) {
+            __syncthreads();   // every wave is done with the staged slabs / the previous half's staging
+            if (wave / (NW / 2) == half) {
 #pragma unroll
-            for (int nt = 0; nt < 2; ++nt)
+                for (int nt = 0; nt < 2; ++nt)
 #pragma unroll
-                for (int st = 0; st < NST; ++st)
-                    *reinterpret_cast<float4 *>(ostg + (16 * nt + l16) * OS + 16 * st + 4 * q) =
-                        make_float4(acc[j][st][nt][0], acc[j][st][nt][1], acc[j][st][nt][2], acc[j][st][nt][3]);
-            const Buf ob(dW + lb * F_IN, (uint32_t)(nl[j] * F_IN * 4));   // this unit's labels only
+                    for (int st = 0; st < NST; ++st)
+                        *reinterpret_cast<float4 *>(ostg + (16 * nt + l16) * OS + 16 * st + 4 * q) =
+                            make_float4(acc[st][nt][0], acc[st][nt][1], acc[st][nt][2], acc[st][nt][3]);
 #pragma unroll
-            for (int i = 0; i < F_IN / 8; ++i) {
-                const int e = 64 * i + lane;
-                const int r = e / (F_IN / 4), c = (e % (F_IN / 4)) * 4;
-                float4 v = *reinterpret_cast<const float4 *>(ostg + r * OS + c);
-                if (beta) {
-                    const float4 o = __builtin_bit_cast(float4, ob.ld16((uint32_t)(e * 16)));
-                    v.x += o.x; v.y += o.y; v.z += o.z; v.w += o.w;
+                for (int i = 0; i < F_IN / 8; ++i) {
+                    const int e = 64 * i + lane;
+                    const int r = e / (F_IN / 4), c = (e % (F_IN / 4)) * 4;
+                    float4 val = *reinterpret_cast<const float4 *>(ostg + r * OS + c);
+                    if (beta) {
+                        const float4 o = __builtin_bit_cast(float4, ob.ld16((uint32_t)(e * 16)));
+                        val.x += o.x; val.y += o.y; val.z += o.z; val.w += o.w;
+                    }
+                    ob.st16<kStreaming>(__builtin_bit_cast(uint4, val), (uint32_t)(e * 16));
                 }
-                ob.st16<kStreaming>(__builtin_bit_cast(uint4, v), (uint32_t)(e * 16));
             }
-            if (dbias && q == 0) {
+        }
+        if constexpr (WITH_DB) {
+            if (q == 0) {
 #pragma unroll
                 for (int nt = 0; nt < 2; ++nt) {
                     const int t = 16 * nt + l16;
-                    if (t < nl[j]) dbias[lb + t] = (beta ? dbias[lb + t] : 0.0f) + db[j][nt][0];
+                    if (t < nl) dbias[lb + t] = (beta ? dbias[lb + t] : 0.0f) + db[nt][0];
                 }
             }
         }
@@ -1369,16 +1378,24 @@ static hipError_t launch_fwd_bce(const TailArgs &a, const bf16_t *Xb, const int3
     const int64_t K = a.L / a.G;
     const int64_t units = K * cdiv(a.G, 32);
     const size_t lds = fb_lds((int)a.F_s, F_IN);
-    const dim3 grid((unsigned)cdiv(units, kFbWaves * fb_upw(F_IN)));
+    const dim3 grid((unsigned)cdiv(units, fb_waves(F_IN)));
     auto go = [&](auto kern) {
         hipError_t e = allow_lds(kern, lds);
         if (e != hipSuccess) return e;
-        hipLaunchKernelGGL(kern, grid, dim3(kFbWaves * 64), lds, s, Xb, idx, (const bf16_t *)W, bias, pos, P,
+        hipLaunchKernelGGL(kern, grid, dim3(fb_waves(F_IN) * 64), lds, s, Xb, idx, (const bf16_t *)W, bias, pos, P,
                            (bf16_t *)dY, dW, dbias, beta, (int)a.B, Bp, (int)a.F_s, a.L, (int)a.G, K);
         return hipGetLastError();
     };
-    if (dW) return bias ? go(k_fwd_bce<F_IN, true, true>) : go(k_fwd_bce<F_IN, false, true>);
-    return bias ? go(k_fwd_bce<F_IN, true, false>) : go(k_fwd_bce<F_IN, false, false>);
+    // (bias, dW, dbias, small F_s): the common shapes of a training step get their own variants
+    const bool xs = a.F_s <= kFbSmallFs;
+    if (dW && dbias)
+        return bias ? (xs ? go(k_fwd_bce<F_IN, true, true, true, true>) : go(k_fwd_bce<F_IN, true, true, true, false>))
+                    : (xs ? go(k_fwd_bce<F_IN, false, true, true, true>) : go(k_fwd_bce<F_IN, false, true, true, false>));
+    if (dW)
+        return bias ? (xs ? go(k_fwd_bce<F_IN, true, true, false, true>) : go(k_fwd_bce<F_IN, true, true, false, false>))
+                    : (xs ? go(k_fwd_bce<F_IN, false, true, false, true>) : go(k_fwd_bce<F_IN, false, true, false, false>));
+    return bias ? (xs ? go(k_fwd_bce<F_IN, true, false, false, true>) : go(k_fwd_bce<F_IN, true, false, false, false>))
+                : (xs ? go(k_fwd_bce<F_IN, false, false, false, true>) : go(k_fwd_bce<F_IN, false, false, false, false>));
 }
 
 hipError_t fwd_bce_mfma(const TailArgs &a, const void *X, const int32_t *idx, const void *W, const float *bias,
