@@ -542,7 +542,10 @@ __global__ __launch_bounds__(512) void k_bwd_w2(const bf16_t *__restrict__ Xb, c
 // words into the slab's [32 rows][512 labels] LDS block.  The block's 32-byte column blocks are
 // XOR-permuted by row / 8 (the lanes of one write instruction then hit distinct banks), and the
 // whole block leaves as 1 KB row runs, cooperatively, in the next slab's barrier window: one row
-// per store instruction, the pattern the DRAM pages serve fastest.
+// per store instruction, the pattern the DRAM pages serve fastest.  (Double-buffering the block so
+// that its stores run during the next slab's products measured the same time.)
+// Rows past B (a last, partial slab) meet zero X^T rows in the backward-weight product and are
+// never stored, so their dY is zeroed only where dbias sums it.
 // Targets: the slab's positives that fall in the workgroup's span are set as bits of an LDS
 // bitmap, one 32-bit word of rows per label.  Two bitmaps alternate by slab parity: in one
 // barrier interval each thread clears its word of the previous slab's bitmap and sets the
@@ -737,7 +740,7 @@ __global__ __launch_bounds__(64 * fb_waves(F_IN)) void k_fwd_bce(
             float d[8];
 #pragma unroll
             for (int r = 0; r < 8; ++r) d[r] = sigmoid_f32(z[r >> 2][nt][r & 3]);
-            if (rows < 32) {
+            if (WITH_DB && rows < 32) {
 #pragma unroll
                 for (int r = 0; r < 8; ++r) d[r] = 8 * q + r < rows ? d[r] : 0.0f;
             }
