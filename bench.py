@@ -50,6 +50,10 @@ CALL_KERNELS = {
 }
 
 
+# calls whose kernel another call of a different size also launches: which dispatches are theirs
+SHARED_KERNEL_PICK = {"bce": max, "head_bce": min}
+
+
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
@@ -154,33 +158,40 @@ def summarize_trace(db, workload, command):
 def summarize_traffic(fetch_db, write_db, workload, command):
     """HBM bytes per kernel launch from FETCH_SIZE and WRITE_SIZE (KiB per dispatch), each scaled by what
     the same counter reads for the plain COPY_BYTES device copy run in the same process."""
-    def per_kernel(db, counter):
+    def per_dispatch(db, counter):
         rows = _db_rows(db, f"select name, dispatch_id, sum(counter_value) from pmc_events "
                             f"where counter_name = '{counter}' group by name, dispatch_id")
         acc = {}
         for name, _, v in rows:
-            k = _short(name)
-            s, n = acc.get(k, (0.0, 0))
-            acc[k] = (s + v * 1024.0, n + 1)
-        return {k: s / n for k, (s, n) in acc.items()}
-    fetch, write = per_kernel(fetch_db, "FETCH_SIZE"), per_kernel(write_db, "WRITE_SIZE")
+            acc.setdefault(_short(name), []).append(v * 1024.0)
+        return acc
+    fetch_d, write_d = per_dispatch(fetch_db, "FETCH_SIZE"), per_dispatch(write_db, "WRITE_SIZE")
+    fetch = {k: sum(v) / len(v) for k, v in fetch_d.items()}
+    write = {k: sum(v) / len(v) for k, v in write_d.items()}
     copy_keys = [k for k in fetch if "copy" in k.lower()]
     if not copy_keys:
         raise SystemExit("no copy kernel in the counter runs (run bench.py with --copy-calibration)")
-    ck = max(copy_keys, key=lambda k: fetch[k])
-    f_fetch = COPY_BYTES / fetch[ck]
-    f_write = COPY_BYTES / write[ck] if write.get(ck) else None
+    ck = max(copy_keys, key=lambda k: max(fetch_d[k]))
+    # the calibration copies are the largest dispatches of the copy kernel (the same kernel also
+    # moves the inputs from the host, in smaller pieces)
+    f_fetch = COPY_BYTES / max(fetch_d[ck])
+    f_write = COPY_BYTES / max(write_d[ck]) if write_d.get(ck) else None
     calls = {}
     for call, prefixes in CALL_KERNELS.items():
         ks = [k for k in fetch if any(k.startswith(p) for p in prefixes)]
         if not ks or f_write is None:
             continue
-        calls[call] = round(sum(fetch[k] * f_fetch + write.get(k, 0.0) * f_write for k in ks))
+        # the tail's and the head's BCE gradient run one kernel: the tail's are its largest dispatches
+        pick = SHARED_KERNEL_PICK.get(call)
+        fv = (lambda k: pick(fetch_d[k])) if pick else (lambda k: fetch[k])
+        wv = (lambda k: pick(write_d[k]) if k in write_d else 0.0) if pick else (lambda k: write.get(k, 0.0))
+        calls[call] = round(sum(fv(k) * f_fetch + wv(k) * f_write for k in ks))
     rec = {"workload": workload, "kernel_source_hash": kernel_source_hash(), "copy_kernel": ck,
            "fetch_factor": round(f_fetch, 4), "write_factor": round(f_write, 4), "calls": calls}
     lines = [f"HBM traffic per launch, workload {workload}",
              "rocprofv3 --pmc FETCH_SIZE, then --pmc WRITE_SIZE (KiB per dispatch), each scaled by the factor",
-             f"that maps the same counter to the {COPY_BYTES} bytes a plain device copy ({ck}) reads or writes.",
+             f"that maps the same counter to the {COPY_BYTES} bytes a plain device copy ({ck}, its largest",
+             "dispatches) reads or writes.",
              f"Command: {command}", "",
              "kernel | FETCH bytes (raw) | WRITE bytes (raw) | scaled HBM bytes"]
     for k in sorted(fetch, key=lambda k: -fetch[k]):
