@@ -296,6 +296,8 @@ def main():
         dYht = torch.empty((wl.B, wl.H), dtype=odt, device=dev)
     torch.cuda.synchronize()
 
+    stream = torch.cuda.current_stream()
+
     def head_train():
         return [("head_fwd", lambda: hs.haste_head_fwd(wl.B, wl.F_s, wl.H, wl.dtype, Xd, Whd, None, Yh)),
                 ("head_bce", lambda: hs.haste_bce_grad(wl.B, wl.H, wl.dtype, Yh, posh, dYht))] if wl.H else []
@@ -318,8 +320,6 @@ def main():
     separate.append(("bwd_w", lambda: hs.haste_bwd_w(desc, Xd, idxd, dYd, dW, None, 0, ws_w)))
     separate.append(("bwd_x", lambda: hs.haste_bwd_x(desc, idxd, Wd, dYd, dX, 0, ws_x)))
     separate += head_back(dYhd) if wl.H else []
-
-    stream = torch.cuda.current_stream()
 
     def timed(calls):
         """K steps after W warm-up steps; events between the calls on the launch stream."""

@@ -557,17 +557,20 @@ __global__ __launch_bounds__(256) void k_gemm_f32(const float *__restrict__ A, i
 }
 
 // split of the H contraction of dX for output tiles of tm x tn: enough workgroups to cover the
-// chip (about `target`), never below 256 head labels per chunk
-int64_t head_splits(int64_t B, int64_t F_s, int64_t H, int64_t tm, int64_t tn, int64_t target) {
-    const int64_t tiles = haste::cdiv(B, tm) * haste::cdiv(F_s, tn);
-    int64_t S = haste::cdiv(target, tiles < 1 ? 1 : tiles);
+// chip (about `target`), never below 256 head labels per chunk.  at_most: never more than
+// `target` workgroups, for the 256x256 kernel, which holds a whole CU (its LDS allows one
+// workgroup per CU): one workgroup past the CU count would run in a second round on its own.
+int64_t head_splits(int64_t B, int64_t F_s, int64_t H, int64_t tm, int64_t tn, int64_t target, bool at_most) {
+    const int64_t tiles = haste::cdiv(B, tm) * haste::cdiv(F_s, tn) < 1 ? 1 : haste::cdiv(B, tm) * haste::cdiv(F_s, tn);
+    int64_t S = at_most ? target / tiles : haste::cdiv(target, tiles);
     const int64_t maxS = haste::cdiv(H, 256);
     if (S > maxS) S = maxS;
     return S < 1 ? 1 : S;
 }
 int64_t head_splits_for(int64_t B, int64_t F_s, int64_t H, int32_t dtype, bool big) {
-    if (dtype != HASTE_DTYPE_BF16) return head_splits(B, F_s, H, 64, 64, 512);
-    return big ? head_splits(B, F_s, H, G4T, G4T, 256) : head_splits(B, F_s, H, TM, TN, 512);
+    if (dtype != HASTE_DTYPE_BF16) return head_splits(B, F_s, H, 64, 64, 512, false);
+    return big ? head_splits(B, F_s, H, G4T, G4T, kXcds * kCusPerXcd, true)
+               : head_splits(B, F_s, H, TM, TN, 512, false);
 }
 
 // The double-buffered kernel needs 16-byte aligned rows along every operand's contiguous
