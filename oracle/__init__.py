@@ -61,8 +61,10 @@ class Oracle:
         L.haste_oracle_head_bwd_x.argtypes = sig_head + [_P, _P, _I64, _I64, _P]
         L.haste_oracle_bce_grad.argtypes = [_I64, _I64, _P, _P, _I64, _P]
         L.haste_oracle_bce_grad_at.argtypes = [_I64, _I64, _P, _I64, _I64, _P, _P, _P, _P]
+        _D = ctypes.c_double
+        L.haste_oracle_sgd_momentum.argtypes = [_I64, ctypes.c_int, _P, _P, _P, _D, _D, _D, _P]
         for f in ("fwd", "fwd_at", "bwd_w", "bwd_x", "head_fwd", "head_bwd_w", "head_bwd_x", "bce_grad",
-                  "bce_grad_at"):
+                  "bce_grad_at", "sgd_momentum"):
             getattr(L, "haste_oracle_" + f).restype = ctypes.c_int
 
     # ---- helpers --------------------------------------------------------------------------
@@ -152,6 +154,17 @@ class Oracle:
                                                _ptr(bs), _ptr(ns), _ptr(z), _ptr(out))
         self._check(rc, "bce_grad_at")
         return out
+
+    def sgd_momentum(self, W, grad, m, lr, momentum, weight_decay, dtype):
+        """One momentum step: returns (W_next, m_next) in fp64; W in its storage dtype."""
+        W = self._store(W, dtype)
+        g = np.ascontiguousarray(grad, dtype=np.float64).reshape(-1)
+        mm = np.array(m, dtype=np.float64).reshape(-1)
+        out = np.empty(W.size, dtype=np.float64)
+        rc = self.lib.haste_oracle_sgd_momentum(W.size, dtype, _ptr(W), _ptr(g), _ptr(mm), lr, momentum,
+                                                weight_decay, _ptr(out))
+        self._check(rc, "sgd_momentum")
+        return out.reshape(W.shape), mm.reshape(W.shape)
 
     def bwd_x(self, idx, W, dY, G, F_s, dtype, b0=0, b1=None):
         """dX[b1-b0, F_s] in fp64 for rows [b0, b1)."""

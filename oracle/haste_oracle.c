@@ -15,6 +15,7 @@
  *   - dX      grad h_{:, I_k} += grad Z_k W_k, summed over k     (Section 3.2, backward-feature)
  *   - head    a^H = W_head h_head                                (Section 3.3)
  *   - BCE     d/dz of the binary cross-entropy of sigmoid(z)      (Section 3.3 objective)
+ *   - SGD     momentum step of the classification layer's optimizer (Section 4)
  *
  * Arithmetic: inputs are decoded exactly to double (bf16 -> fp64 and fp32 -> fp64 are exact);
  * every sum is accumulated in double in the order the definition states (no blocking, no
@@ -230,6 +231,25 @@ int haste_oracle_bce_grad_at(int64_t B, int64_t N, const int32_t *pos, int64_t P
         for (int64_t p = 0; p < P; ++p)
             if (pos[bs[i] * P + p] == ns[i]) y = 1.0;
         out[i] = sigmoid(z[i]) - y;
+    }
+    return 0;
+}
+
+/* ---------------------------------------------------------------------------------------------
+ * SGD with momentum, the optimizer the paper trains the classification layer with (Section 4,
+ * implementation details), in the common form without dampening or look-ahead:
+ *   velocity  m <- momentum * m + (grad + weight_decay * W)
+ *   weights   W_next = W - lr * m
+ * W is read in its storage dtype; grad, m (in/out) and W_next are doubles.
+ * ------------------------------------------------------------------------------------------- */
+int haste_oracle_sgd_momentum(int64_t n, int dtype, const void *W, const double *grad, double *m, double lr,
+                              double momentum, double weight_decay, double *W_next) {
+    if (n < 0 || (dtype != DT_F32 && dtype != DT_BF16)) return 1;
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < n; ++i) {
+        const double w = ld(W, i, dtype);
+        m[i] = momentum * m[i] + (grad[i] + weight_decay * w);
+        W_next[i] = w - lr * m[i];
     }
     return 0;
 }

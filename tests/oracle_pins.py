@@ -10,6 +10,8 @@ raises AssertionError when the oracle disagrees with:
   G = 1 is standard per-label fixed fan-in; G = L is one gathered GEMM);
 * finite differences of the Section 3.3 BCE objective and of the bilinear pairing, and of the
   objective with respect to the logits for the BCE-gradient function;
+* closed forms of the momentum step (constant gradient, weight decay alone) and its convergence on a
+  quadratic;
 * the adjoint identity <dY, Y - bias> = <dX, X> = <dW, W> (bilinearity);
 * exact one-hot gathers/scatters and the group-permutation invariance.
 """
@@ -354,6 +356,38 @@ def pin_bce_grad(o):
     assert np.abs(zero - 1.0 / (1.0 + np.exp(-Z))).max() <= 1e-15, "no positives: gradient is sigmoid(z)"
 
 
+def pin_sgd_momentum(o):
+    """The momentum step against closed forms that do not restate it: a constant gradient g from rest
+    gives m_T = g (1 - mu^T) / (1 - mu) and moves W by lr g sum_t (1 - mu^t) / (1 - mu); weight
+    decay alone shrinks W geometrically by (1 - lr wd) per step (mu = 0); and heavy-ball steps on
+    the quadratic |W - W*|^2 / 2 (gradient W - W*) converge to W*."""
+    rng = np.random.default_rng(31)
+    n = 37
+    W0 = rng.standard_normal(n)
+    g = rng.standard_normal(n)
+    lr, mu, T = 0.05, 0.9, 6
+    W, m = W0.copy(), np.zeros(n)
+    for _ in range(T):
+        W, m = o.sgd_momentum(W, g, m, lr, mu, 0.0, F32)
+    geo = lambda t: (1 - mu ** t) / (1 - mu)
+    m_ref = g * geo(T)
+    W_ref = W0.astype(np.float32).astype(np.float64) - lr * g * sum(geo(t) for t in range(1, T + 1))
+    # W passes through fp32 storage between steps in this loop: compare within that rounding
+    assert np.abs(m - m_ref).max() <= 1e-12 * max(1.0, np.abs(m_ref).max()), "momentum of a constant gradient"
+    assert np.abs(W - W_ref).max() <= 1e-5 * max(1.0, np.abs(W_ref).max()), "weights under a constant gradient"
+    Wd = W0.copy()
+    for _ in range(T):
+        Wd, _m = o.sgd_momentum(Wd, np.zeros(n), np.zeros(n), lr, 0.0, 0.3, F32)
+    Wd_ref = W0.astype(np.float32).astype(np.float64) * (1 - lr * 0.3) ** T
+    assert np.abs(Wd - Wd_ref).max() <= 1e-6, "weight decay alone is a geometric shrink"
+    Wstar = rng.standard_normal(n)
+    Wq, mq = np.zeros(n), np.zeros(n)
+    for _ in range(400):
+        Wq, mq = o.sgd_momentum(Wq, Wq.astype(np.float32).astype(np.float64) - Wstar, mq, 0.1, 0.8, 0.0, F32)
+    assert np.abs(Wq - Wstar).max() <= 1e-5, "heavy-ball steps on a quadratic must converge to its minimum"
+
+
 ALL_PINS = [pin_fig2_gs, pin_fig2_ffi, pin_bruteforce, pin_duplicate_indices, pin_dense_special_case,
             pin_group_equals_expanded_ffi, pin_finite_differences, pin_adjoint_identity, pin_one_hot,
-            pin_group_permutation, pin_label_ranges, pin_head, pin_bce_grad]
+            pin_group_permutation, pin_label_ranges, pin_head, pin_bce_grad,
+            pin_sgd_momentum]

@@ -44,6 +44,11 @@ MUTANTS = {
     "bce_sigmoid_sign": ("static double sigmoid(double z) { return 1.0 / (1.0 + exp(-z)); }",
                          "static double sigmoid(double z) { return 1.0 / (1.0 + exp(z)); }"),
     "bce_at_target_ignored": ("if (pos[bs[i] * P + p] == ns[i]) y = 1.0;", "if (pos[bs[i] * P + p] == ns[i]) y = 0.0;"),
+    "sgd_momentum_dropped": ("m[i] = momentum * m[i] + (grad[i] + weight_decay * w);",
+                             "m[i] = (grad[i] + weight_decay * w);"),
+    "sgd_decay_sign": ("m[i] = momentum * m[i] + (grad[i] + weight_decay * w);",
+                       "m[i] = momentum * m[i] + (grad[i] - weight_decay * w);"),
+    "sgd_step_uses_grad": ("W_next[i] = w - lr * m[i];", "W_next[i] = w - lr * grad[i];"),
     "bf16_decode_shift": ("uint32_t u = ((uint32_t)((const uint16_t *)p)[i]) << 16;",
                           "uint32_t u = ((uint32_t)((const uint16_t *)p)[i]) << 15;"),
 }
