@@ -8,6 +8,8 @@ sigmoid(z) - y of the Section 3.3 objective (the workload's definition of dY):
   -> tail backward-feature (haste_bwd_x) -> head backward (haste_head_bwd, adds its dX onto the tail's).
 Timed beside it, on the same inputs:
   - the same training pass unfused: haste_fwd, haste_bce_grad, haste_bwd_w instead of haste_fwd_bce;
+  - the training pass plus one SGD-with-momentum step on W and W_h, fused (haste_fwd_bce_sgd, dW
+    never stored) and unfused (haste_bwd_w + haste_sgd_momentum);
   - the five separate calls on a fixed dY (haste_fwd, haste_head_fwd, haste_bwd_w, haste_bwd_x,
     haste_head_bwd), i.e. without the loss gradient.
 Default workload: the 2.95M-label tail (G = 32, F_in = 64) with a 65,536-label dense head, B = 512,
@@ -38,6 +40,9 @@ COPY_BYTES = 1 << 30            # plain device copy used to calibrate the HBM by
 CALL_KERNELS = {
     "fwd": ["k_fwd<"],
     "fwd_bce": ["k_transpose_x", "k_fwd_bce"],
+    "fwd_bce_sgd": ["k_transpose_x", "k_fwd_bce"],
+    "sgd": ["k_sgd_momentum"],
+    "head_sgd": ["k_sgd_momentum"],
     "bce": ["k_bce_grad"],
     "head_bce": ["k_bce_grad"],
     "bwd_w": ["k_transpose_x", "k_bwd_w"],
@@ -51,7 +56,7 @@ CALL_KERNELS = {
 
 
 # calls whose kernel another call of a different size also launches: which dispatches are theirs
-SHARED_KERNEL_PICK = {"bce": max, "head_bce": min}
+SHARED_KERNEL_PICK = {"bce": max, "head_bce": min, "sgd": max, "head_sgd": min}
 
 
 def parse():
@@ -88,6 +93,9 @@ def call_cost(wl, dt_bytes=2, n_pos=0):
     c = {
         "fwd": (X + idx + W + Y, tail_flops),
         "fwd_bce": (X + idx + W + pos + Y + dW, 2 * tail_flops),   # writes dY (Y's size) and dW
+        # reads W and the fp32 velocity, writes dY, the velocity and the next W
+        "fwd_bce_sgd": (X + idx + 2 * W + pos + Y + 2 * dW, 2 * tail_flops),
+        "sgd": (2 * W + 3 * dW, 0),
         "bce": (2 * Y + pos, 0),
         "bwd_w": (X + idx + Y + dW, tail_flops),
         "bwd_x": (idx + W + Y + dX, tail_flops),
@@ -95,6 +103,7 @@ def call_cost(wl, dt_bytes=2, n_pos=0):
     if H:
         c["head_fwd"] = (X + Wh + Yh, head_flops)
         c["head_bce"] = (2 * Yh + pos, 0)
+        c["head_sgd"] = (2 * Wh + 3 * dWh, 0)
         c["head_bwd"] = (X + Wh + Yh + dWh + 2 * dX, 2 * head_flops)
     return c
 
@@ -314,6 +323,23 @@ def main():
                [("bwd_w", lambda: hs.haste_bwd_w(desc, Xd, idxd, dYt, dW, None, 0, ws_w)),
                 ("bwd_x", lambda: hs.haste_bwd_x(desc, idxd, Wd, dYt, dX, 0, ws_x))] +
                (head_back(dYht) if wl.H else []))
+    # the training pass with the optimizer (SGD with momentum on W and W_h): fused, the tail's step is
+    # applied inside haste_fwd_bce_sgd and dW never reaches memory; unfused, dW is stored and stepped
+    opt = hs.sgd_opts(0.01, 0.9, 0.0)
+    mom = torch.zeros((wl.L, wl.F_in), dtype=torch.float32, device=dev)
+    Wnext = torch.empty_like(Wd)
+    ws_s = hs.workspace(hs.haste_workspace_bytes(desc, hs.HASTE_OP_FWD_BCE_SGD))
+    if wl.H:
+        mom_h = torch.zeros((wl.H, wl.F_s), dtype=torch.float32, device=dev)
+        Whnext = torch.empty_like(Whd)
+    head_step = ([("head_sgd", lambda: hs.haste_sgd_momentum(wl.H * wl.F_s, wl.dtype, Whd, dWh, mom_h, opt,
+                                                             Whnext))] if wl.H else [])
+    fused_opt = ([("fwd_bce_sgd", lambda: hs.haste_fwd_bce_sgd(desc, Xd, idxd, Wd, None, posd, dYt, opt, mom, Wnext,
+                                                               None, ws_s))] +
+                 head_train() + [("bwd_x", lambda: hs.haste_bwd_x(desc, idxd, Wd, dYt, dX, 0, ws_x))] +
+                 (head_back(dYht) if wl.H else []) + head_step)
+    unfused_opt = unfused + [("sgd", lambda: hs.haste_sgd_momentum(wl.L * wl.F_in, wl.dtype, Wd, dW, mom, opt,
+                                                                   Wnext))] + head_step
     separate = [("fwd", lambda: hs.haste_fwd(desc, Xd, idxd, Wd, None, Y))]
     if wl.H:
         separate.append(("head_fwd", lambda: hs.haste_head_fwd(wl.B, wl.F_s, wl.H, wl.dtype, Xd, Whd, None, Yh)))
@@ -358,6 +384,8 @@ def main():
     sep_ms, sep_per, _ = timed(separate)
     unf_ms, unf_per, _ = timed(unfused)
     step_ms, per_call, wall_ms = timed(fused)
+    fo_ms, fo_per, _ = timed(fused_opt)
+    uo_ms, uo_per, _ = timed(unfused_opt)
 
     step_bytes = sum(cost[k][0] for k in per_call)
     step_flops = sum(cost[k][1] for k in per_call)
@@ -388,6 +416,13 @@ def main():
         "roofline": roof,
         "unfused_training_step": {"ms": round(unf_ms, 4), "per_call": detail(unf_per),
                                   "what": "haste_fwd + haste_bce_grad + haste_bwd_w in place of haste_fwd_bce"},
+        "training_step_with_optimizer": {
+            "fused_ms": round(fo_ms, 4), "unfused_ms": round(uo_ms, 4),
+            "fused_per_call_ms": {k: round(v, 4) for k, v in fo_per.items()},
+            "unfused_per_call_ms": {k: round(v, 4) for k, v in uo_per.items()},
+            "what": "the training pass plus one SGD-with-momentum step on W and W_h: fused, the tail's step runs "
+                    "inside haste_fwd_bce_sgd (dW never stored); unfused, haste_fwd + haste_bce_grad + haste_bwd_w "
+                    "+ haste_sgd_momentum"},
         "separate_calls_step": {
             "ms": round(sep_ms, 4), "per_call": detail(sep_per),
             "step_alg_bytes": sum(cost[k][0] for k in sep_per),

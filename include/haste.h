@@ -49,7 +49,17 @@ enum haste_status {
 };
 
 /* Workspace-query operation codes. */
-enum haste_op { HASTE_OP_FWD = 0, HASTE_OP_BWD_W = 1, HASTE_OP_BWD_X = 2, HASTE_OP_FWD_BCE = 3 };
+enum haste_op {
+    HASTE_OP_FWD = 0, HASTE_OP_BWD_W = 1, HASTE_OP_BWD_X = 2, HASTE_OP_FWD_BCE = 3, HASTE_OP_FWD_BCE_SGD = 4
+};
+
+/* Hyper-parameters of one step of SGD with momentum (see haste_sgd_momentum). */
+typedef struct haste_sgd {
+    float lr;            /* learning rate                                               */
+    float momentum;      /* velocity decay, in [0, 1)                                   */
+    float weight_decay;  /* L2 coefficient added to the gradient (0 = none)             */
+    int32_t reserved;    /* must be 0                                                   */
+} haste_sgd_t;
 
 /* Shape of one sparse tail layer. */
 typedef struct haste_desc {
@@ -106,14 +116,48 @@ int haste_bwd_x(const haste_desc_t *desc, const int32_t *idx, const void *W, con
  * pos[B, P] int32 holds each row's positive tail labels as column ids; entries outside [0, L)
  * (e.g. -1 padding) are ignored and a repeated id counts once.  P >= 0; pos may be NULL when
  * P == 0.  bias as in haste_fwd; beta is 0 (overwrite) or 1 (accumulate).
- * bf16 layers whose groups are whole 16-label tiles, with P <= 64, run one fused kernel (the
- * logits never reach memory).  Other layers run haste_fwd into dY, the gradient in place (for
- * bf16 the sigmoid then sees the logits rounded to bf16), and haste_bwd_w.
+ * bf16 layers whose groups are whole 16-label tiles, with F_s <= 768 and P <= 64, run one fused
+ * kernel (the logits never reach memory).  Other layers run haste_fwd into dY, the gradient in
+ * place (for bf16 the sigmoid then sees the logits rounded to bf16), and haste_bwd_w.
  * ws: haste_workspace_bytes(desc, HASTE_OP_FWD_BCE) bytes.
  */
 int haste_fwd_bce(const haste_desc_t *desc, const void *X, const int32_t *idx, const void *W,
                   const float *bias, const int32_t *pos, int32_t P, void *dY, float *dW,
                   float *dbias, int beta, void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * haste_fwd_bce followed by one step of SGD with momentum on W (the classification layer's
+ * optimizer, Section 4), with the step applied where the backward-weight product is formed, so
+ * that dW never reaches memory:
+ *   dY as in haste_fwd_bce;  dW as in haste_fwd_bce (not stored);
+ *   m[l, t]      = momentum * m[l, t] + (dW[l, t] + weight_decay * W[l, t])     (fp32, updated)
+ *   W_next[l, t] = W[l, t] - lr * m[l, t]                                         (dtype)
+ * m[L, F_in] fp32 (zeros before the first step); W_next[L, F_in] in the dtype of W, and it must
+ * not overlap W (the backward-feature call of the same step still reads W).  dbias: optional
+ * gradient output as in haste_fwd_bce (the bias's own step is a haste_sgd_momentum call).
+ * The fp32 arithmetic of the step is that of haste_sgd_momentum, so the result equals
+ * haste_fwd_bce + haste_sgd_momentum bit for bit.  Layers outside the fused kernel's shapes (those
+ * of haste_fwd_bce, with F_s <= 768) run exactly that composition, with dW in ws; on the fused
+ * shapes more than 64 positives per row is HASTE_ERR_UNSUPPORTED (compose the two calls instead).
+ * B == 0 applies the step with a zero gradient.
+ * ws: haste_workspace_bytes(desc, HASTE_OP_FWD_BCE_SGD) bytes.
+ */
+int haste_fwd_bce_sgd(const haste_desc_t *desc, const void *X, const int32_t *idx, const void *W,
+                      const float *bias, const int32_t *pos, int32_t P, void *dY, float *dbias,
+                      const haste_sgd_t *opt, float *m, void *W_next, void *ws, size_t ws_bytes,
+                      void *stream);
+
+/*
+ * One step of SGD with momentum (Section 4: the classification layer is trained with SGD and
+ * momentum), in the common form without dampening or look-ahead, over n weights:
+ *   m[i]      = momentum * m[i] + (grad[i] + weight_decay * W[i])
+ *   W_next[i] = W[i] - lr * m[i]
+ * W, W_next [n] in dtype (W_next may be W: an in-place step); grad [n] (NULL: a zero gradient) and
+ * m [n] fp32, m updated.  momentum must lie in [0, 1).
+ * Arithmetic: fp32 fused multiply-adds; a bf16 W_next is rounded to nearest even.
+ */
+int haste_sgd_momentum(int64_t n, int32_t dtype, const void *W, const float *grad, float *m,
+                       const haste_sgd_t *opt, void *W_next, void *stream);
 
 /*
  * Gradient of the binary cross-entropy objective at stored logits (Section 3.3), for the dense

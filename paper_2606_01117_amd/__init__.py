@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(PKG, "libhaste.so")
 
 HASTE_DTYPE_F32 = 0
 HASTE_DTYPE_BF16 = 1
-HASTE_OP_FWD, HASTE_OP_BWD_W, HASTE_OP_BWD_X, HASTE_OP_FWD_BCE = 0, 1, 2, 3
+HASTE_OP_FWD, HASTE_OP_BWD_W, HASTE_OP_BWD_X, HASTE_OP_FWD_BCE, HASTE_OP_FWD_BCE_SGD = 0, 1, 2, 3, 4
 STATUS = {0: "ok", 1: "invalid argument", 2: "unsupported", 3: "workspace too small", 4: "HIP error"}
 
 
@@ -34,6 +34,11 @@ class haste_desc_t(ctypes.Structure):
                 ("F_in", ctypes.c_int64), ("dtype", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
+class haste_sgd_t(ctypes.Structure):
+    _fields_ = [("lr", ctypes.c_float), ("momentum", ctypes.c_float), ("weight_decay", ctypes.c_float),
+                ("reserved", ctypes.c_int32)]
+
+
 def _load() -> ctypes.CDLL:
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"libhaste.so is not built ({LIB_PATH}); run paper_2606_01117_amd.build.build()")
@@ -46,6 +51,8 @@ def _load() -> ctypes.CDLL:
         "haste_bwd_x": [D, P, P, P, P, ctypes.c_int, P, SZ, P],
         "haste_fwd_bce": [D, P, P, P, P, P, I32, P, P, P, ctypes.c_int, P, SZ, P],
         "haste_bce_grad": [I64, I64, I32, P, P, I32, P, P],
+        "haste_fwd_bce_sgd": [D, P, P, P, P, P, I32, P, P, ctypes.POINTER(haste_sgd_t), P, P, P, SZ, P],
+        "haste_sgd_momentum": [I64, I32, P, P, P, ctypes.POINTER(haste_sgd_t), P, P],
         "haste_head_fwd": [I64, I64, I64, I32, P, P, P, P, P],
         "haste_head_bwd": [I64, I64, I64, I32, P, P, P, P, P, ctypes.c_int, P, SZ, P],
         "haste_validate_idx": [D, P, P, P],
@@ -68,7 +75,8 @@ def _load() -> ctypes.CDLL:
 lib = _load()
 
 # every symbol the header declares
-EXPORTS = ("haste_fwd", "haste_bwd_w", "haste_bwd_x", "haste_fwd_bce", "haste_bce_grad", "haste_head_fwd", "haste_head_bwd", "haste_workspace_bytes",
+EXPORTS = ("haste_fwd", "haste_bwd_w", "haste_bwd_x", "haste_fwd_bce", "haste_fwd_bce_sgd", "haste_sgd_momentum",
+           "haste_bce_grad", "haste_head_fwd", "haste_head_bwd", "haste_workspace_bytes",
            "haste_head_workspace_bytes", "haste_validate_idx", "haste_debug_gather", "haste_status_str",
            "haste_last_error", "haste_version")
 
@@ -165,6 +173,22 @@ def haste_fwd_bce(desc, X, idx, W, bias, pos, dY, dW=None, dbias=None, beta=0, w
     p, n = _ws(ws)
     _check(lib.haste_fwd_bce(ctypes.byref(desc), _ptr(X), _ptr(idx), _ptr(W), _ptr(bias), _ptr(pos), _npos(pos),
                              _ptr(dY), _ptr(dW), _ptr(dbias), int(beta), p, n, _stream(stream)))
+
+
+def sgd_opts(lr: float, momentum: float, weight_decay: float = 0.0) -> haste_sgd_t:
+    return haste_sgd_t(lr, momentum, weight_decay, 0)
+
+
+def haste_fwd_bce_sgd(desc, X, idx, W, bias, pos, dY, opt, m, W_next, dbias=None, ws=None, stream=None):
+    p, n = _ws(ws)
+    _check(lib.haste_fwd_bce_sgd(ctypes.byref(desc), _ptr(X), _ptr(idx), _ptr(W), _ptr(bias), _ptr(pos), _npos(pos),
+                                 _ptr(dY), _ptr(dbias), ctypes.byref(opt), _ptr(m), _ptr(W_next), p, n,
+                                 _stream(stream)))
+
+
+def haste_sgd_momentum(n, dtype, W, grad, m, opt, W_next, stream=None):
+    _check(lib.haste_sgd_momentum(int(n), dtype, _ptr(W), _ptr(grad), _ptr(m), ctypes.byref(opt), _ptr(W_next),
+                                  _stream(stream)))
 
 
 def haste_bce_grad(B, N, dtype, Y, pos, dY, stream=None):

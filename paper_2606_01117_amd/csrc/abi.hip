@@ -92,6 +92,10 @@ size_t haste_workspace_bytes(const haste_desc_t *d, int op) {
         case HASTE_OP_BWD_X: return haste::bwd_x_mfma_supported(a) ? haste::bwd_x_mfma_ws(a) : haste::bwd_x_valu_ws(a);
         // the fused kernel and the backward-weight kernel stage the same X^T copy
         case HASTE_OP_FWD_BCE: return haste::bwd_w_mfma_supported(a) ? haste::bwd_w_mfma_ws(a) : 0;
+        // the composed form also keeps dW in the workspace (after the X^T copy)
+        case HASTE_OP_FWD_BCE_SGD:
+            return (haste::bwd_w_mfma_supported(a) ? haste::bwd_w_mfma_ws(a) : 0) +
+                   (haste::fwd_bce_mfma_supported(a, 0) ? 0 : (size_t)haste::round_up(a.L * a.F_in * 4, 256));
     }
     return 0;
 }
@@ -215,6 +219,83 @@ int haste_fwd_bce(const haste_desc_t *d, const void *X, const int32_t *idx, cons
         e = bw_mfma ? haste::bwd_w_mfma(a, X, idx, dY, dW, dbias, beta, ws, s)
                     : haste::bwd_w_valu(a, X, idx, dY, dW, dbias, beta, s);
     return hip_status(e, "haste_fwd_bce");
+}
+
+static int check_sgd(const haste_sgd_t *o) {
+    if (!o) return fail(HASTE_ERR_INVALID, "opt is NULL");
+    if (o->reserved != 0) return fail(HASTE_ERR_INVALID, "opt.reserved must be 0");
+    if (!(o->momentum >= 0.0f && o->momentum < 1.0f)) return fail(HASTE_ERR_INVALID, "momentum must be in [0, 1)");
+    if (!(o->lr == o->lr) || !(o->weight_decay == o->weight_decay))
+        return fail(HASTE_ERR_INVALID, "lr and weight_decay must be numbers");
+    return HASTE_OK;
+}
+
+int haste_sgd_momentum(int64_t n, int32_t dtype, const void *W, const float *grad, float *m, const haste_sgd_t *opt,
+                       void *W_next, void *stream) {
+    if (dtype != HASTE_DTYPE_F32 && dtype != HASTE_DTYPE_BF16) return fail(HASTE_ERR_INVALID, "bad dtype %d", dtype);
+    if (n < 0) return fail(HASTE_ERR_INVALID, "n must be >= 0");
+    TRY(check_sgd(opt));
+    if (n == 0) return ok();
+    TRY(need_ptr(W, "W"));
+    if (grad) TRY(need_ptr(grad, "grad"));
+    TRY(need_ptr(m, "m"));
+    TRY(need_ptr(W_next, "W_next"));
+    if (haste::cdiv(n, 256) >= ((int64_t)1 << 31)) return fail(HASTE_ERR_UNSUPPORTED, "n too large");
+    return hip_status(haste::sgd_momentum(n, dtype, W, grad, m, *opt, W_next, as_stream(stream)), "haste_sgd_momentum");
+}
+
+int haste_fwd_bce_sgd(const haste_desc_t *d, const void *X, const int32_t *idx, const void *W, const float *bias,
+                      const int32_t *pos, int32_t P, void *dY, float *dbias, const haste_sgd_t *opt, float *m,
+                      void *W_next, void *ws, size_t ws_bytes, void *stream) {
+    TRY(check_desc(d));
+    TRY(check_sgd(opt));
+    if (P < 0) return fail(HASTE_ERR_INVALID, "P must be >= 0");
+    const haste::TailArgs a = targs(d);
+    hipStream_t s = as_stream(stream);
+    if (a.L == 0) return ok();
+    TRY(need_ptr(W, "W"));
+    TRY(need_ptr(m, "m"));
+    TRY(need_ptr(W_next, "W_next"));
+    if (dbias && !aligned16(dbias)) return fail(HASTE_ERR_INVALID, "dbias is not 16-byte aligned");
+    const int64_t wbytes = a.L * a.F_in * (a.dtype == HASTE_DTYPE_BF16 ? 2 : 4);
+    {
+        const char *w0 = static_cast<const char *>(W), *n0 = static_cast<const char *>(W_next);
+        if (n0 < w0 + wbytes && w0 < n0 + wbytes)
+            return fail(HASTE_ERR_INVALID, "W_next overlaps W (the backward-feature call still reads W)");
+    }
+    if (a.B > 0) {
+        TRY(need_ptr(X, "X"));
+        TRY(need_ptr(idx, "idx"));
+        TRY(need_ptr(dY, "dY"));
+        if (P > 0) TRY(need_ptr(pos, "pos"));
+    }
+    if (bias && !aligned16(bias)) return fail(HASTE_ERR_INVALID, "bias is not 16-byte aligned");
+    if (a.B * haste::cdiv(a.L, 2048) >= ((int64_t)1 << 31))
+        return fail(HASTE_ERR_UNSUPPORTED, "B * L too large for the gradient kernel's grid");
+    // the fused kernel's shapes need only the X^T copy; others keep dW in the workspace too
+    const bool fused_shape = haste::fwd_bce_mfma_supported(a, 0);
+    const size_t xws = haste::bwd_w_mfma_supported(a) ? haste::bwd_w_mfma_ws(a) : 0;
+    const size_t need = xws + (fused_shape ? 0 : (size_t)haste::round_up(a.L * a.F_in * 4, 256));
+    if (a.B == 0) {  // no rows: a zero gradient, the step still decays the velocity and the weights
+        if (dbias) TRY(hip_status(haste::fill_f32(dbias, a.L, 0.0f, s), "haste_fwd_bce_sgd"));
+        return hip_status(haste::sgd_momentum(a.L * a.F_in, a.dtype, W, nullptr, m, *opt, W_next, s),
+                          "haste_fwd_bce_sgd");
+    }
+    if (need && (!ws || ws_bytes < need))
+        return fail(HASTE_ERR_WORKSPACE, "haste_fwd_bce_sgd needs %zu workspace bytes, got %zu", need, ws ? ws_bytes : 0);
+    if (need) TRY(need_ptr(ws, "ws"));
+    if (fused_shape) {
+        if (!haste::fwd_bce_mfma_supported(a, P))
+            return fail(HASTE_ERR_UNSUPPORTED, "more than 64 positives per row; use haste_fwd_bce and haste_sgd_momentum");
+        return hip_status(haste::fwd_bce_sgd_mfma(a, X, idx, W, bias, P > 0 ? pos : nullptr, P, dY, dbias, *opt, m,
+                                                  W_next, ws, s),
+                          "haste_fwd_bce_sgd");
+    }
+    // composed: dW into the workspace after the X^T copy, then the momentum step
+    float *dW = reinterpret_cast<float *>(static_cast<char *>(ws) + xws);
+    const int rc = haste_fwd_bce(d, X, idx, W, bias, pos, P, dY, dW, dbias, 0, ws, xws, stream);
+    if (rc != HASTE_OK) return rc;
+    return hip_status(haste::sgd_momentum(a.L * a.F_in, a.dtype, W, dW, m, *opt, W_next, s), "haste_fwd_bce_sgd");
 }
 
 int haste_bce_grad(int64_t B, int64_t N, int32_t dtype, const void *Y, const int32_t *pos, int32_t P, void *dY,

@@ -113,6 +113,15 @@ __device__ __forceinline__ float bce_grad_f32(float z, bool positive) {
     return positive ? sg - 1.0f : sg;
 }
 
+// One step of SGD with momentum on one weight (the classification layer's optimizer, Section 4):
+// velocity m <- momentum * m + (g + weight_decay * w), then w_next = w - lr * m.  Explicit fused
+// multiply-adds, so that every kernel that applies the step rounds it the same way.
+__device__ __forceinline__ void sgd_step(float w, float g, float &m, float &w_next, float lr, float momentum,
+                                         float weight_decay) {
+    m = __fmaf_rn(momentum, m, __fmaf_rn(weight_decay, w, g));
+    w_next = __fmaf_rn(-lr, m, w);
+}
+
 // ---- host-side launchers (one translation unit each) -----------------------------------------
 namespace haste {
 
@@ -140,6 +149,13 @@ size_t fwd_bce_mfma_ws(const TailArgs &a);
 hipError_t fwd_bce_mfma(const TailArgs &a, const void *X, const int32_t *idx, const void *W, const float *bias,
                         const int32_t *pos, int P, void *dY, float *dW, float *dbias, int beta, void *ws,
                         hipStream_t s);
+// forward + BCE gradient + backward-weight with the momentum step applied to W in place of storing dW
+hipError_t fwd_bce_sgd_mfma(const TailArgs &a, const void *X, const int32_t *idx, const void *W, const float *bias,
+                            const int32_t *pos, int P, void *dY, float *dbias, const haste_sgd_t &opt, float *m,
+                            void *W_next, void *ws, hipStream_t s);
+// momentum step over n weights: m and W_next updated (W_next may alias W)
+hipError_t sgd_momentum(int64_t n, int32_t dtype, const void *W, const float *g, float *m, const haste_sgd_t &opt,
+                        void *W_next, hipStream_t s);
 // dY[b, n] = sigmoid(Y[b, n]) - T[b, n] elementwise (Y and dY may alias)
 hipError_t bce_grad(int64_t B, int64_t N, int32_t dtype, const void *Y, const int32_t *pos, int P, void *dY,
                     hipStream_t s);

@@ -573,21 +573,26 @@ __device__ __forceinline__ uint32_t dpp_swap_pairs(uint32_t v) {   // lane l rec
 // byte offset of dword d of staged dY row r (32-byte column blocks permuted by r / 8)
 __device__ __forceinline__ int fb_ystg_off(int r, int d) { return r * kFbYRow + 4 * (d ^ (8 * (r >> 3))); }
 
-// XS: F_s <= kFbSmallFs (fewer X^T prefetch registers)
-constexpr int kFbSmallFs = 768;
+// widest input the kernel stages (its X^T prefetch registers are sized for it)
+constexpr int kFbMaxFs = 768;
 
-template <int F_IN, bool HAS_BIAS, bool WITH_DW, bool WITH_DB, bool XS>
+// what the kernel does with the backward-weight product: nothing, store dW, or apply the
+// momentum step to W with it (dW never stored)
+constexpr int kFbOutNone = 0, kFbOutDW = 1, kFbOutSGD = 2;
+
+template <int F_IN, bool HAS_BIAS, int OUT, bool WITH_DB>
 __global__ __launch_bounds__(64 * fb_waves(F_IN)) void k_fwd_bce(
     const bf16_t *__restrict__ Xb, const int32_t *__restrict__ idx, const bf16_t *__restrict__ W,
     const float *__restrict__ bias, const int32_t *__restrict__ pos, int P, bf16_t *__restrict__ dY,
-    float *__restrict__ dW, float *__restrict__ dbias, int beta, int B, int Bp, int F_s, int64_t L, int G,
-    int64_t K) {
+    float *__restrict__ dW, float *__restrict__ dbias, int beta, float lr, float momentum, float weight_decay,
+    float *__restrict__ mom, bf16_t *__restrict__ W_next, int B, int Bp, int F_s, int64_t L, int G, int64_t K) {
+    constexpr bool WITH_DW = OUT != kFbOutNone;
     extern __shared__ __align__(16) char fbs[];
     constexpr int NW = fb_waves(F_IN);
     constexpr int NT = NW * 64;                 // threads
     constexpr int KS = F_IN / 32;               // forward K-steps (32 slots)
     constexpr int NST = F_IN / 16;              // backward-weight M-tiles (16 slots)
-    constexpr int XL = (XS ? kFbSmallFs : kMaxFs) * 4 / NT;   // 16-byte X^T loads per thread and slab
+    constexpr int XL = kFbMaxFs * 4 / NT;       // 16-byte X^T loads per thread and slab
     constexpr int PL = 32 * kFbMaxPos / NT;     // positives per thread and slab
     constexpr int YL = 32 * 64 / NT;            // 16-byte dY stores per thread and slab
     char *xs = fbs;
@@ -787,11 +792,15 @@ __global__ __launch_bounds__(64 * fb_waves(F_IN)) void k_fwd_bce(
 
     if constexpr (WITH_DW) {
         // dW: as in the backward-weight kernel, a wave stages its unit's [32 labels][F_IN] fp32 block
-        // in LDS and writes it as whole contiguous runs; half the waves at a time.  dbias from the
-        // q = 0 lanes.
+        // in LDS and writes it as whole contiguous runs; half the waves at a time.  With the
+        // momentum step, the same runs read the unit's W and velocity and write the velocity and
+        // the next weights instead.  dbias from the q = 0 lanes.
         constexpr int OS = F_IN + 4;
         float *ostg = reinterpret_cast<float *>(fbs) + (wave % (NW / 2)) * 32 * OS;
-        const Buf ob(dW + lb * F_IN, (uint32_t)(nl * F_IN * 4));   // this unit's labels only
+        const Buf ob(OUT == kFbOutSGD ? (void *)(mom + lb * F_IN) : (void *)(dW + lb * F_IN),
+                     (uint32_t)(nl * F_IN * 4));   // this unit's labels only
+        const Buf wb(W + lb * F_IN, (uint32_t)(nl * F_IN * 2));
+        const Buf nb(W_next + lb * F_IN, (uint32_t)(OUT == kFbOutSGD ? nl * F_IN * 2 : 0));
 #pragma unroll
         for (int half = 0; half < 2; ++half) {
             __syncthreads();   // every wave is done with the staged slabs / the previous half's staging
@@ -807,11 +816,24 @@ __global__ __launch_bounds__(64 * fb_waves(F_IN)) void k_fwd_bce(
                     const int e = 64 * i + lane;
                     const int r = e / (F_IN / 4), c = (e % (F_IN / 4)) * 4;
                     float4 val = *reinterpret_cast<const float4 *>(ostg + r * OS + c);
-                    if (beta) {
-                        const float4 o = __builtin_bit_cast(float4, ob.ld16((uint32_t)(e * 16)));
-                        val.x += o.x; val.y += o.y; val.z += o.z; val.w += o.w;
+                    if constexpr (OUT == kFbOutSGD) {
+                        // slots 4e .. 4e+3 of the unit's block: W (4 bf16) and velocity (4 fp32)
+                        const uint2 wv = wb.ld8((uint32_t)(e * 8));
+                        float4 mv = __builtin_bit_cast(float4, ob.ld16((uint32_t)(e * 16)));
+                        float n0, n1, n2, n3;
+                        sgd_step(bf16_to_f32((bf16_t)(wv.x & 0xffffu)), val.x, mv.x, n0, lr, momentum, weight_decay);
+                        sgd_step(bf16_to_f32((bf16_t)(wv.x >> 16)), val.y, mv.y, n1, lr, momentum, weight_decay);
+                        sgd_step(bf16_to_f32((bf16_t)(wv.y & 0xffffu)), val.z, mv.z, n2, lr, momentum, weight_decay);
+                        sgd_step(bf16_to_f32((bf16_t)(wv.y >> 16)), val.w, mv.w, n3, lr, momentum, weight_decay);
+                        ob.st16<kStreaming>(__builtin_bit_cast(uint4, mv), (uint32_t)(e * 16));
+                        nb.st8<kStreaming>(make_uint2(pack_bf16(n0, n1), pack_bf16(n2, n3)), (uint32_t)(e * 8));
+                    } else {
+                        if (beta) {
+                            const float4 o = __builtin_bit_cast(float4, ob.ld16((uint32_t)(e * 16)));
+                            val.x += o.x; val.y += o.y; val.z += o.z; val.w += o.w;
+                        }
+                        ob.st16<kStreaming>(__builtin_bit_cast(uint4, val), (uint32_t)(e * 16));
                     }
-                    ob.st16<kStreaming>(__builtin_bit_cast(uint4, val), (uint32_t)(e * 16));
                 }
             }
         }
@@ -1365,19 +1387,33 @@ hipError_t bwd_w_mfma(const TailArgs &a, const void *X, const int32_t *idx, cons
 }
 
 // ---- forward with the BCE-gradient epilogue, fused with backward-weight -------------------------
-// Groups of whole 16-label tiles (the staged dY columns of a wave's units stay contiguous), and at
-// most kFbMaxPos positives per row (the slab prefetch).
+// Groups of whole 16-label tiles (the staged dY columns of a wave's units stay contiguous), inputs
+// of at most kFbMaxFs features, and at most kFbMaxPos positives per row (the slab prefetch).
 bool fwd_bce_mfma_supported(const TailArgs &a, int P) {
-    return bwd_w_mfma_supported(a) && (a.G % 16) == 0 && P >= 0 && P <= kFbMaxPos &&
+    return bwd_w_mfma_supported(a) && (a.G % 16) == 0 && a.F_s <= kFbMaxFs && P >= 0 && P <= kFbMaxPos &&
            fb_lds((int)a.F_s, (int)a.F_in) <= kLdsBudget;
 }
 
 size_t fwd_bce_mfma_ws(const TailArgs &a) { return bwd_w_mfma_ws(a); }
 
-template <int F_IN>
-static hipError_t launch_fwd_bce(const TailArgs &a, const bf16_t *Xb, const int32_t *idx, const void *W,
-                                 const float *bias, const int32_t *pos, int P, void *dY, float *dW, float *dbias,
-                                 int beta, int Bp, hipStream_t s) {
+struct FbArgs {
+    const bf16_t *Xb;
+    const int32_t *idx;
+    const void *W;
+    const float *bias;
+    const int32_t *pos;
+    int P;
+    void *dY;
+    float *dW, *dbias;
+    int beta;
+    haste_sgd_t opt;
+    float *m;
+    void *W_next;
+    int Bp;
+};
+
+template <int F_IN, int OUT>
+static hipError_t launch_fwd_bce(const TailArgs &a, const FbArgs &f, hipStream_t s) {
     const int64_t K = a.L / a.G;
     const int64_t units = K * cdiv(a.G, 32);
     const size_t lds = fb_lds((int)a.F_s, F_IN);
@@ -1385,37 +1421,46 @@ static hipError_t launch_fwd_bce(const TailArgs &a, const bf16_t *Xb, const int3
     auto go = [&](auto kern) {
         hipError_t e = allow_lds(kern, lds);
         if (e != hipSuccess) return e;
-        hipLaunchKernelGGL(kern, grid, dim3(fb_waves(F_IN) * 64), lds, s, Xb, idx, (const bf16_t *)W, bias, pos, P,
-                           (bf16_t *)dY, dW, dbias, beta, (int)a.B, Bp, (int)a.F_s, a.L, (int)a.G, K);
+        hipLaunchKernelGGL(kern, grid, dim3(fb_waves(F_IN) * 64), lds, s, f.Xb, f.idx, (const bf16_t *)f.W, f.bias,
+                           f.pos, f.P, (bf16_t *)f.dY, f.dW, f.dbias, f.beta, f.opt.lr, f.opt.momentum,
+                           f.opt.weight_decay, f.m, (bf16_t *)f.W_next, (int)a.B, f.Bp, (int)a.F_s, a.L, (int)a.G, K);
         return hipGetLastError();
     };
-    // (bias, dW, dbias, small F_s): the common shapes of a training step get their own variants
-    const bool xs = a.F_s <= kFbSmallFs;
-    if (dW && dbias)
-        return bias ? (xs ? go(k_fwd_bce<F_IN, true, true, true, true>) : go(k_fwd_bce<F_IN, true, true, true, false>))
-                    : (xs ? go(k_fwd_bce<F_IN, false, true, true, true>) : go(k_fwd_bce<F_IN, false, true, true, false>));
-    if (dW)
-        return bias ? (xs ? go(k_fwd_bce<F_IN, true, true, false, true>) : go(k_fwd_bce<F_IN, true, true, false, false>))
-                    : (xs ? go(k_fwd_bce<F_IN, false, true, false, true>) : go(k_fwd_bce<F_IN, false, true, false, false>));
-    return bias ? (xs ? go(k_fwd_bce<F_IN, true, false, false, true>) : go(k_fwd_bce<F_IN, true, false, false, false>))
-                : (xs ? go(k_fwd_bce<F_IN, false, false, false, true>) : go(k_fwd_bce<F_IN, false, false, false, false>));
+    if constexpr (OUT == kFbOutNone)
+        return f.bias ? go(k_fwd_bce<F_IN, true, OUT, false>) : go(k_fwd_bce<F_IN, false, OUT, false>);
+    if (f.dbias) return f.bias ? go(k_fwd_bce<F_IN, true, OUT, true>) : go(k_fwd_bce<F_IN, false, OUT, true>);
+    return f.bias ? go(k_fwd_bce<F_IN, true, OUT, false>) : go(k_fwd_bce<F_IN, false, OUT, false>);
+}
+
+template <int OUT>
+static hipError_t fwd_bce_dispatch(const TailArgs &a, const void *X, FbArgs &f, void *ws, hipStream_t s) {
+    f.Bp = (int)round_up(a.B, 32);
+    bf16_t *Xb = reinterpret_cast<bf16_t *>(ws);
+    f.Xb = Xb;
+    hipLaunchKernelGGL(k_transpose_x, dim3((unsigned)cdiv(a.F_s, 32), (unsigned)cdiv(f.Bp, 32)), dim3(256), 0, s,
+                       (const bf16_t *)X, Xb, (int)a.B, (int)a.F_s);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    switch (a.F_in) {
+        case 32: return launch_fwd_bce<32, OUT>(a, f, s);
+        case 64: return launch_fwd_bce<64, OUT>(a, f, s);
+        case 128: return launch_fwd_bce<128, OUT>(a, f, s);
+    }
+    return hipErrorInvalidValue;
 }
 
 hipError_t fwd_bce_mfma(const TailArgs &a, const void *X, const int32_t *idx, const void *W, const float *bias,
                         const int32_t *pos, int P, void *dY, float *dW, float *dbias, int beta, void *ws,
                         hipStream_t s) {
-    const int Bp = (int)round_up(a.B, 32);
-    bf16_t *Xb = reinterpret_cast<bf16_t *>(ws);
-    hipLaunchKernelGGL(k_transpose_x, dim3((unsigned)cdiv(a.F_s, 32), (unsigned)cdiv(Bp, 32)), dim3(256), 0, s,
-                       (const bf16_t *)X, Xb, (int)a.B, (int)a.F_s);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    switch (a.F_in) {
-        case 32: return launch_fwd_bce<32>(a, Xb, idx, W, bias, pos, P, dY, dW, dbias, beta, Bp, s);
-        case 64: return launch_fwd_bce<64>(a, Xb, idx, W, bias, pos, P, dY, dW, dbias, beta, Bp, s);
-        case 128: return launch_fwd_bce<128>(a, Xb, idx, W, bias, pos, P, dY, dW, dbias, beta, Bp, s);
-    }
-    return hipErrorInvalidValue;
+    FbArgs f{nullptr, idx, W, bias, pos, P, dY, dW, dbias, beta, haste_sgd_t{0.f, 0.f, 0.f, 0}, nullptr, nullptr, 0};
+    return dW ? fwd_bce_dispatch<kFbOutDW>(a, X, f, ws, s) : fwd_bce_dispatch<kFbOutNone>(a, X, f, ws, s);
+}
+
+hipError_t fwd_bce_sgd_mfma(const TailArgs &a, const void *X, const int32_t *idx, const void *W, const float *bias,
+                            const int32_t *pos, int P, void *dY, float *dbias, const haste_sgd_t &opt, float *m,
+                            void *W_next, void *ws, hipStream_t s) {
+    FbArgs f{nullptr, idx, W, bias, pos, P, dY, nullptr, dbias, 0, opt, m, W_next, 0};
+    return fwd_bce_dispatch<kFbOutSGD>(a, X, f, ws, s);
 }
 
 // ---- backward-feature ---------------------------------------------------------------------------

@@ -144,6 +144,39 @@ __global__ __launch_bounds__(256) void k_bce_grad(const T *Y, const int32_t *__r
         for (int i = 0; i < n; ++i) store_out(o, i, bce_grad_f32(load_f32(y, i), (t >> i) & 1));
     }
 }
+
+// One momentum step per weight (sgd_step), four consecutive weights per thread: 16-byte velocity and
+// gradient accesses and 8- or 16-byte weight accesses when n is a multiple of 4 and the buffers are
+// aligned (VEC), else one weight per thread.  W_next may be W: each weight is read before it is
+// written, by the same thread.  g == NULL: a zero gradient.
+template <typename T, bool VEC>
+__global__ __launch_bounds__(256) void k_sgd_momentum(const T *W, const float *__restrict__ g, float *__restrict__ m,
+                                                      T *W_next, int64_t n, float lr, float momentum,
+                                                      float weight_decay) {
+    const int64_t i0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * (VEC ? 4 : 1);
+    if (i0 >= n) return;
+    if constexpr (VEC) {
+        const float4 gv = g ? *reinterpret_cast<const float4 *>(g + i0) : make_float4(0.f, 0.f, 0.f, 0.f);
+        float4 mv = *reinterpret_cast<const float4 *>(m + i0);
+        float w[4], o[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) w[j] = load_f32(W, i0 + j);
+        sgd_step(w[0], gv.x, mv.x, o[0], lr, momentum, weight_decay);
+        sgd_step(w[1], gv.y, mv.y, o[1], lr, momentum, weight_decay);
+        sgd_step(w[2], gv.z, mv.z, o[2], lr, momentum, weight_decay);
+        sgd_step(w[3], gv.w, mv.w, o[3], lr, momentum, weight_decay);
+        *reinterpret_cast<float4 *>(m + i0) = mv;
+        if constexpr (sizeof(T) == 2)
+            *reinterpret_cast<uint2 *>(W_next + i0) = make_uint2(pack_bf16(o[0], o[1]), pack_bf16(o[2], o[3]));
+        else
+            *reinterpret_cast<float4 *>(W_next + i0) = make_float4(o[0], o[1], o[2], o[3]);
+    } else {
+        float mm = m[i0], o;
+        sgd_step(load_f32(W, i0), g ? g[i0] : 0.0f, mm, o, lr, momentum, weight_decay);
+        m[i0] = mm;
+        store_out(W_next, i0, o);
+    }
+}
 }  // namespace
 
 namespace haste {
@@ -202,6 +235,31 @@ hipError_t bce_grad(int64_t B, int64_t N, int32_t dtype, const void *Y, const in
             hipLaunchKernelGGL((k_bce_grad<bf16_t, false>), grid, block, 0, s, (const bf16_t *)Y, pos, P, (bf16_t *)dY, N, nchunk);
     } else {
         hipLaunchKernelGGL((k_bce_grad<float, false>), grid, block, 0, s, (const float *)Y, pos, P, (float *)dY, N, nchunk);
+    }
+    return hipGetLastError();
+}
+
+
+hipError_t sgd_momentum(int64_t n, int32_t dtype, const void *W, const float *g, float *m, const haste_sgd_t &opt,
+                        void *W_next, hipStream_t s) {
+    const uintptr_t al = reinterpret_cast<uintptr_t>(W) | reinterpret_cast<uintptr_t>(g) |
+                         reinterpret_cast<uintptr_t>(m) | reinterpret_cast<uintptr_t>(W_next);
+    const bool vec = (n % 4) == 0 && (al & 15) == 0;
+    const dim3 grid((unsigned)cdiv(n, vec ? 1024 : 256)), block(256);
+    if (dtype == HASTE_DTYPE_BF16) {
+        if (vec)
+            hipLaunchKernelGGL((k_sgd_momentum<bf16_t, true>), grid, block, 0, s, (const bf16_t *)W, g, m,
+                               (bf16_t *)W_next, n, opt.lr, opt.momentum, opt.weight_decay);
+        else
+            hipLaunchKernelGGL((k_sgd_momentum<bf16_t, false>), grid, block, 0, s, (const bf16_t *)W, g, m,
+                               (bf16_t *)W_next, n, opt.lr, opt.momentum, opt.weight_decay);
+    } else {
+        if (vec)
+            hipLaunchKernelGGL((k_sgd_momentum<float, true>), grid, block, 0, s, (const float *)W, g, m,
+                               (float *)W_next, n, opt.lr, opt.momentum, opt.weight_decay);
+        else
+            hipLaunchKernelGGL((k_sgd_momentum<float, false>), grid, block, 0, s, (const float *)W, g, m,
+                               (float *)W_next, n, opt.lr, opt.momentum, opt.weight_decay);
     }
     return hipGetLastError();
 }

@@ -13,7 +13,7 @@ import pytest
 
 import oracle
 import synth
-from gpu_helpers import TOL, host_f32, out_tensor, rel_err, say, to_dev
+from gpu_helpers import TOL, host_f32, oracle_fwd_bce, out_tensor, rand_pos, rel_err, say, targets, to_dev
 
 pytestmark = pytest.mark.gpu
 F32, BF16 = synth.DT_F32, synth.DT_BF16
@@ -41,45 +41,6 @@ def _check(name, got, ref, dtype):
     e = rel_err(got, ref)
     say(f"    {name:<10s} rel_inf_err={e:.3e} (tol {TOL[dtype]:.0e})")
     assert e <= TOL[dtype], f"{name}: {e:.3e} > {TOL[dtype]:.0e}"
-
-
-def rand_pos(rng, B, L, P):
-    """[B, P] positives with the awkward entries: repeats, -1 padding, ids past L and below -1,
-    and ids on 512-label span edges and at both ends of the layer."""
-    if P == 0:
-        return np.zeros((B, 0), np.int32)
-    pos = rng.integers(0, L, size=(B, P)).astype(np.int32)
-    edges = [0, L - 1, min(511, L - 1), min(512, L - 1), L // 2]
-    for b in range(B):
-        r = rng.random()
-        if r < 0.2:
-            pos[b, -1] = -1
-        elif r < 0.3:
-            pos[b, -1] = L + int(rng.integers(0, 100))
-        elif r < 0.4:
-            pos[b, -1] = -int(rng.integers(2, 100))
-        elif r < 0.6 and P > 1:
-            pos[b, -1] = pos[b, 0]       # a repeat counts once
-        pos[b, 0] = edges[b % len(edges)] if b % 3 == 0 else pos[b, 0]
-    return pos
-
-
-def targets(pos, B, L):
-    T = np.zeros((B, L), bool)
-    for b in range(B):
-        for c in pos[b]:
-            if 0 <= c < L:
-                T[b, c] = True
-    return T
-
-
-def oracle_fwd_bce(orc, X, idx, W, bias, pos, G, F_in, dt):
-    """fp64 composition: logits, BCE gradient, backward-weight (dY passed at fp32 precision)."""
-    z = orc.fwd(X, idx, W, bias, G, dt)
-    dY = orc.bce_grad(z, pos)
-    Xf = synth.to_f64(X, dt).astype(np.float32)   # exact for bf16 and fp32 storage
-    dW, db = orc.bwd_w(Xf, idx, dY.astype(np.float32), G, F_in, F32, with_dbias=True)
-    return dY, dW, db
 
 
 CASES = [
