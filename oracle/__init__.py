@@ -63,6 +63,11 @@ class Oracle:
         L.haste_oracle_bce_grad_at.argtypes = [_I64, _I64, _P, _I64, _I64, _P, _P, _P, _P]
         _D = ctypes.c_double
         L.haste_oracle_sgd_momentum.argtypes = [_I64, ctypes.c_int, _P, _P, _P, _D, _D, _D, _P]
+        L.haste_oracle_splitmix64.argtypes = [ctypes.c_uint64, ctypes.c_uint64]
+        L.haste_oracle_splitmix64.restype = ctypes.c_uint64
+        L.haste_oracle_rewire.argtypes = [_I64, _I64, _I64, _I64, ctypes.c_int, _P, _P, _P, _D, ctypes.c_int,
+                                          ctypes.c_uint64, _P, _P]
+        L.haste_oracle_rewire.restype = ctypes.c_int
         for f in ("fwd", "fwd_at", "bwd_w", "bwd_x", "head_fwd", "head_bwd_w", "head_bwd_x", "bce_grad",
                   "bce_grad_at", "sgd_momentum"):
             getattr(L, "haste_oracle_" + f).restype = ctypes.c_int
@@ -165,6 +170,22 @@ class Oracle:
                                                 weight_decay, _ptr(out))
         self._check(rc, "sgd_momentum")
         return out.reshape(W.shape), mm.reshape(W.shape)
+
+    def splitmix64(self, seed: int, i: int) -> int:
+        return int(self.lib.haste_oracle_splitmix64(seed, i))
+
+    def rewire(self, idx, W, m, G, H, dtype, rho, init_random, seed):
+        """Returns (idx', W' in storage dtype, m' (fp64) or None, n_pruned, mask[K, F] by old slot)."""
+        idx = np.array(idx, dtype=np.int32, order="C")
+        W = np.array(self._store(W, dtype), order="C")
+        K, F = idx.shape
+        mm = None if m is None else np.array(m, dtype=np.float64, order="C")
+        mask = np.empty(K * F, dtype=np.uint8)
+        n = ctypes.c_int64(0)
+        rc = self.lib.haste_oracle_rewire(K, G, F, H, dtype, _ptr(idx), _ptr(W), _ptr(mm), rho, int(init_random),
+                                          seed, ctypes.byref(n), _ptr(mask))
+        self._check(rc, "rewire")
+        return idx, W, mm, int(n.value), mask.reshape(K, F).astype(bool)
 
     def bwd_x(self, idx, W, dY, G, F_s, dtype, b0=0, b1=None):
         """dX[b1-b0, F_s] in fp64 for rows [b0, b1)."""

@@ -16,6 +16,7 @@
  *   - head    a^H = W_head h_head                                (Section 3.3)
  *   - BCE     d/dz of the binary cross-entropy of sigmoid(z)      (Section 3.3 objective)
  *   - SGD     momentum step of the classification layer's optimizer (Section 4)
+ *   - rewire  group-shared rewiring of the supports (Alg. 3)
  *
  * Arithmetic: inputs are decoded exactly to double (bf16 -> fp64 and fp32 -> fp64 are exact);
  * every sum is accumulated in double in the order the definition states (no blocking, no
@@ -26,6 +27,7 @@
  */
 #include <math.h>
 #include <stdint.h>
+#include <stdlib.h>
 #include <string.h>
 #include <omp.h>
 
@@ -251,5 +253,142 @@ int haste_oracle_sgd_momentum(int64_t n, int dtype, const void *W, const double 
         m[i] = momentum * m[i] + (grad[i] + weight_decay * w);
         W_next[i] = w - lr * m[i];
     }
+    return 0;
+}
+
+/* ---------------------------------------------------------------------------------------------
+ * Group-shared rewiring (Alg. 3, the discrete phase of the training loop in Section 3.4):
+ *   1. score every (group k, slot j) by the |w| of the group's labels at that slot;
+ *   2. mark the m = floor(K F rho) smallest scores over all groups;
+ *   3. give each marked slot a new feature;
+ *   4. reinitialise the marked slots' weights (zero, or uniform in [-1/sqrt(F), 1/sqrt(F)]).
+ * Readings where the algorithm is silent or leaves the layout's invariants open:
+ *   - the score is the sum over the G labels, accumulated in fp32 in label order (the mean of the
+ *     algorithm divides every score by the same G, which orders them identically); both this and
+ *     the GPU take the selection decision in that fp32 arithmetic;
+ *   - ties in the selection go to the lower flat index k F + j;
+ *   - a marked slot draws its feature uniformly from those not kept by its group and not drawn
+ *     before it (slots in ascending j), so every support stays a set; the row is then re-sorted,
+ *     carrying each slot's weight column (and velocity) with it;
+ *   - randomness: SplitMix64 (Steele, Lea and Flood, 2014) in counter form, output i of the stream
+ *     seeded with `seed`: draw r = out(k F + j) picks the (r mod n_free)-th free feature in
+ *     ascending order; label l's reinitialised slot j takes n = out(K F + l F + j) >> 40 (24 bits)
+ *     and the value ((2 n - 2^24) as fp32) * (a 2^-24), a = fp32(1 / sqrt(F)), stored in the
+ *     weights' dtype (bf16 rounded to nearest even);
+ *   - a velocity array, if given, moves with its weights and is zero on reinitialised slots.
+ * idx [K, F] (strictly increasing rows, in/out), W [K G, F] in its storage dtype (in/out), m
+ * [K G, F] doubles or NULL (in/out); mask [K F] receives the marked slots by their old position.
+ * ------------------------------------------------------------------------------------------- */
+static uint64_t splitmix64_at(uint64_t s, uint64_t i) {
+    uint64_t z = s + (i + 1) * 0x9E3779B97F4A7C15ull;
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+}
+
+uint64_t haste_oracle_splitmix64(uint64_t seed, uint64_t i) { return splitmix64_at(seed, i); }
+
+static uint16_t bf16_rne(float f) {
+    uint32_t u;
+    memcpy(&u, &f, sizeof u);
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+typedef struct { float s; int64_t i; } score_t;
+
+static int by_score(const void *a, const void *b) {
+    const score_t *x = (const score_t *)a, *y = (const score_t *)b;
+    if (x->s < y->s) return -1;
+    if (x->s > y->s) return 1;
+    return (x->i > y->i) - (x->i < y->i);
+}
+
+typedef struct { int32_t f; int32_t src; } slot_t;
+
+static int by_feature(const void *a, const void *b) {
+    const slot_t *x = (const slot_t *)a, *y = (const slot_t *)b;
+    return (x->f > y->f) - (x->f < y->f);
+}
+
+int haste_oracle_rewire(int64_t K, int64_t G, int64_t F, int64_t H, int dtype, int32_t *idx, void *W, double *m,
+                        double rho, int init_random, uint64_t seed, int64_t *n_pruned, uint8_t *mask) {
+    if (K < 0 || G <= 0 || F <= 0 || H < F || rho < 0.0 || rho >= 1.0) return 1;
+    if (dtype != DT_F32 && dtype != DT_BF16) return 1;
+    const int64_t KF = K * F;
+    const int64_t npr = (int64_t)floor((double)K * (double)F * rho);
+    *n_pruned = npr;
+    memset(mask, 0, (size_t)KF);
+    if (npr == 0) return 0;
+    /* 1. scores, fp32, labels in order */
+    score_t *sc = (score_t *)malloc((size_t)KF * sizeof(score_t));
+    if (!sc) return 2;
+    for (int64_t k = 0; k < K; ++k)
+        for (int64_t j = 0; j < F; ++j) {
+            float s = 0.0f;
+            for (int64_t g = 0; g < G; ++g) s += fabsf((float)ld(W, (k * G + g) * F + j, dtype));
+            sc[k * F + j].s = s;
+            sc[k * F + j].i = k * F + j;
+        }
+    /* 2. the npr smallest, ties to the lower index */
+    qsort(sc, (size_t)KF, sizeof(score_t), by_score);
+    for (int64_t r = 0; r < npr; ++r) mask[sc[r].i] = 1;
+    free(sc);
+    /* 3-4. per group: draws, re-sort, weights */
+    const float a = (float)(1.0 / sqrt((double)F));
+    const float scale = a * 5.9604644775390625e-08f; /* a * 2^-24, exact */
+    uint8_t *used = (uint8_t *)malloc((size_t)H);
+    slot_t *row = (slot_t *)malloc((size_t)F * sizeof(slot_t));
+    double *tmp = (double *)malloc((size_t)F * sizeof(double));
+    if (!used || !row || !tmp) { free(used); free(row); free(tmp); return 2; }
+    for (int64_t k = 0; k < K; ++k) {
+        int any = 0;
+        for (int64_t j = 0; j < F; ++j) any |= mask[k * F + j];
+        if (!any) continue;
+        memset(used, 0, (size_t)H);
+        int64_t n_used = 0;
+        for (int64_t j = 0; j < F; ++j)
+            if (!mask[k * F + j]) { used[idx[k * F + j]] = 1; ++n_used; }
+        for (int64_t j = 0; j < F; ++j) {
+            int32_t f = idx[k * F + j];
+            if (mask[k * F + j]) {
+                const int64_t t = (int64_t)(splitmix64_at(seed, (uint64_t)(k * F + j)) % (uint64_t)(H - n_used));
+                int64_t c = -1;
+                for (f = 0; f < H; ++f)
+                    if (!used[f] && ++c == t) break;
+                used[f] = 1;
+                ++n_used;
+            }
+            row[j].f = f;
+            row[j].src = (int32_t)j;
+        }
+        qsort(row, (size_t)F, sizeof(slot_t), by_feature);
+        for (int64_t p = 0; p < F; ++p) idx[k * F + p] = row[p].f;
+        for (int64_t g = 0; g < G; ++g) {
+            const int64_t l = k * G + g;
+            for (int64_t p = 0; p < F; ++p) {
+                const int64_t j = row[p].src;
+                if (mask[k * F + j]) {
+                    double v = 0.0;
+                    if (init_random) {
+                        const uint64_t n = splitmix64_at(seed, (uint64_t)(KF + l * F + j)) >> 40;
+                        v = (double)((float)((int64_t)(2 * n) - (1LL << 24)) * scale);
+                    }
+                    tmp[p] = v;
+                } else {
+                    tmp[p] = ld(W, l * F + j, dtype);
+                }
+            }
+            for (int64_t p = 0; p < F; ++p) {
+                if (dtype == DT_BF16) ((uint16_t *)W)[l * F + p] = bf16_rne((float)tmp[p]);
+                else ((float *)W)[l * F + p] = (float)tmp[p];
+            }
+            if (m) {
+                for (int64_t p = 0; p < F; ++p) tmp[p] = mask[k * F + row[p].src] ? 0.0 : m[l * F + row[p].src];
+                for (int64_t p = 0; p < F; ++p) m[l * F + p] = tmp[p];
+            }
+        }
+    }
+    free(used); free(row); free(tmp);
     return 0;
 }

@@ -12,6 +12,8 @@ raises AssertionError when the oracle disagrees with:
   objective with respect to the logits for the BCE-gradient function;
 * closed forms of the momentum step (constant gradient, weight decay alone) and its convergence on a
   quadratic;
+* the rewiring of Alg. 3 on a hand-checked layer, its tie rule, its invariants on random layers,
+  the uniformity of its draws, and the published outputs of its generator;
 * the adjoint identity <dY, Y - bias> = <dX, X> = <dW, W> (bilinearity);
 * exact one-hot gathers/scatters and the group-permutation invariance.
 """
@@ -387,7 +389,110 @@ def pin_sgd_momentum(o):
     assert np.abs(Wq - Wstar).max() <= 1e-5, "heavy-ball steps on a quadratic must converge to its minimum"
 
 
+def pin_splitmix64(o):
+    """The counter-based generator of the rewiring draws is SplitMix64 (Steele, Lea and Flood, 2014):
+    its first three outputs for seed 0, as published with the reference implementation."""
+    assert [o.splitmix64(0, i) for i in range(3)] == [0xE220A8397B1DCDAF, 0x6E789E6AA1B965F4, 0x06C45D188009454F]
+
+
+def _scores_f32(W, G, F, dtype):
+    """Per-(group, slot) sums of |w| over the group's labels, fp32, labels in order (independent)."""
+    Wf = np.abs(synth.to_f64(W, dtype).astype(np.float32)).reshape(-1, G, F)
+    s = np.zeros((Wf.shape[0], F), np.float32)
+    for g in range(G):
+        s += Wf[:, g, :]
+    return s
+
+
+def pin_rewire_hand(o):
+    """Alg. 3 on a hand-checked layer: scores [[0.1, 5, 3], [2, 0.05, 7]], rho = 0.34 gives
+    m = floor(6 * 0.34) = 2, so slot 0 of group 0 and slot 1 of group 1 are pruned; kept features
+    keep their weights, the new features are outside the kept ones, zero init gives zero weights."""
+    idx = np.array([[1, 4, 6], [0, 2, 7]], np.int32)
+    W = np.array([[0.05, 2.0, 1.0], [0.05, 3.0, 2.0], [1.0, 0.02, 3.0], [1.0, 0.03, 4.0]], np.float32)
+    idx2, W2, _, n, mask = o.rewire(idx, W, None, 2, 8, F32, 0.34, False, 7)
+    assert n == 2
+    assert np.array_equal(mask, np.array([[1, 0, 0], [0, 1, 0]], bool)), f"pruned slots {mask}"
+    for k, kept in ((0, {4: (2.0, 3.0), 6: (1.0, 2.0)}), (1, {0: (1.0, 1.0), 7: (3.0, 4.0)})):
+        row = list(idx2[k])
+        assert row == sorted(set(row)) and len(row) == 3
+        new = [f for f in row if f not in kept]
+        assert len(new) == 1, f"group {k} must gain exactly one feature outside its kept ones: {row}"
+        for f, ws in kept.items():
+            p = row.index(f)
+            assert (W2[2 * k, p], W2[2 * k + 1, p]) == ws, f"kept weight of feature {f} moved wrongly"
+        p = row.index(new[0])
+        assert W2[2 * k, p] == 0.0 and W2[2 * k + 1, p] == 0.0
+
+
+def pin_rewire_ties_and_noop(o):
+    """Equal scores (all-zero weights) prune the lowest flat indices first; rho = 0 changes nothing."""
+    rng = np.random.default_rng(41)
+    K, F, G, H = 5, 4, 2, 20
+    idx = np.stack([np.sort(rng.choice(H, F, replace=False)) for _ in range(K)]).astype(np.int32)
+    _, _, _, n, mask = o.rewire(idx, np.zeros((K * G, F), np.float32), None, G, H, F32, 0.5, False, 1)
+    assert n == 10 and np.array_equal(mask.reshape(-1), np.arange(K * F) < 10), "ties must go to the lower index"
+    W = rng.standard_normal((K * G, F)).astype(np.float32)
+    idx2, W2, _, n, mask = o.rewire(idx, W, None, G, H, F32, 0.0, True, 1)
+    assert n == 0 and not mask.any() and np.array_equal(idx2, idx) and np.array_equal(W2, W)
+
+
+def pin_rewire_invariants(o):
+    """On random layers: exactly m slots pruned, none scoring above a kept one; rows stay strictly
+    increasing; every kept (feature, weight column, velocity) survives; new features are outside the
+    kept set, with weights within 1/sqrt(F) (random init) and zero velocity."""
+    rng = np.random.default_rng(43)
+    for dtype, init in ((BF16, True), (F32, False)):
+        K, G, F, H, rho = 50, 4, 16, 64, 0.3
+        idx = np.stack([np.sort(rng.choice(H, F, replace=False)) for _ in range(K)]).astype(np.int32)
+        W = (rng.standard_normal((K * G, F)) * rng.random((K * G, 1))).astype(np.float32)
+        W = synth.bf16_bits(W) if dtype == BF16 else W
+        m = rng.standard_normal((K * G, F))
+        idx2, W2, m2, n, mask = o.rewire(idx, W, m, G, H, dtype, rho, init, 123)
+        assert n == int(np.floor(K * F * rho)) and mask.sum() == n
+        S = _scores_f32(W, G, F, dtype)
+        assert S[mask].max() <= S[~mask].min(), "a pruned slot scores above a kept one"
+        Wv, W2v = synth.to_f64(W, dtype), synth.to_f64(W2, dtype)
+        for k in range(K):
+            row = list(idx2[k])
+            assert all(0 <= f < H for f in row) and all(a < b for a, b in zip(row, row[1:]))
+            kept = {int(idx[k, j]): j for j in range(F) if not mask[k, j]}
+            new = [p for p, f in enumerate(row) if f not in kept]
+            assert len(new) == int(mask[k].sum())
+            for f, j in kept.items():
+                p = row.index(f)
+                for g in range(G):
+                    l = k * G + g
+                    assert W2v[l, p] == Wv[l, j] and m2[l, p] == m[l, j], "kept slot lost its weight or velocity"
+            for p in new:
+                for g in range(G):
+                    l = k * G + g
+                    assert m2[l, p] == 0.0
+                    assert (abs(W2v[l, p]) <= 1.0 / np.sqrt(F) * (1 + 2 ** -8)) if init else W2v[l, p] == 0.0
+
+
+def pin_rewire_uniform(o):
+    """A pruned slot's new feature is uniform over the features its group does not keep: with F = 2
+    and one slot pruned, the new feature's rank among the H - 1 free features is uniform."""
+    rng = np.random.default_rng(47)
+    K, F, H = 4000, 2, 6
+    idx = np.stack([np.sort(rng.choice(H, F, replace=False)) for _ in range(K)]).astype(np.int32)
+    W = rng.random((K, F)).astype(np.float32) + 0.5
+    idx2, _, _, _, mask = o.rewire(idx, W, None, 1, H, F32, 0.5, False, 99)
+    counts = np.zeros(H - 1)
+    for k in np.nonzero(mask.sum(axis=1) == 1)[0]:
+        kept = int(idx[k][~mask[k]][0])
+        others = [int(f) for f in idx2[k] if f != kept]
+        assert len(others) == 1 and kept in idx2[k], f"group {k}: {idx2[k]} must keep {kept} and add one feature"
+        free = [f for f in range(H) if f != kept]
+        counts[free.index(others[0])] += 1
+    exp = counts.sum() / (H - 1)
+    chi2 = float(((counts - exp) ** 2 / exp).sum())
+    assert counts.sum() > 1000 and chi2 < 25.0, f"new-feature ranks not uniform: {counts}, chi2 {chi2:.1f}"
+
+
 ALL_PINS = [pin_fig2_gs, pin_fig2_ffi, pin_bruteforce, pin_duplicate_indices, pin_dense_special_case,
             pin_group_equals_expanded_ffi, pin_finite_differences, pin_adjoint_identity, pin_one_hot,
             pin_group_permutation, pin_label_ranges, pin_head, pin_bce_grad,
-            pin_sgd_momentum]
+            pin_sgd_momentum, pin_splitmix64, pin_rewire_hand, pin_rewire_ties_and_noop, pin_rewire_invariants,
+            pin_rewire_uniform]

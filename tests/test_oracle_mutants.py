@@ -49,6 +49,13 @@ MUTANTS = {
     "sgd_decay_sign": ("m[i] = momentum * m[i] + (grad[i] + weight_decay * w);",
                        "m[i] = momentum * m[i] + (grad[i] - weight_decay * w);"),
     "sgd_step_uses_grad": ("W_next[i] = w - lr * m[i];", "W_next[i] = w - lr * grad[i];"),
+    "rewire_ties_reversed": ("return (x->i > y->i) - (x->i < y->i);", "return (x->i < y->i) - (x->i > y->i);"),
+    "rewire_largest": ("if (x->s < y->s) return -1;\n    if (x->s > y->s) return 1;",
+                       "if (x->s > y->s) return -1;\n    if (x->s < y->s) return 1;"),
+    "rewire_m_ceil": ("(int64_t)floor((double)K * (double)F * rho)", "(int64_t)ceil((double)K * (double)F * rho)"),
+    "rewire_kept_not_excluded": ("if (!mask[k * F + j]) { used[idx[k * F + j]] = 1; ++n_used; }",
+                                 "if (!mask[k * F + j]) { ++n_used; }"),
+    "rewire_column_not_moved": ("tmp[p] = ld(W, l * F + j, dtype);", "tmp[p] = ld(W, l * F + p, dtype);"),
     "bf16_decode_shift": ("uint32_t u = ((uint32_t)((const uint16_t *)p)[i]) << 16;",
                           "uint32_t u = ((uint32_t)((const uint16_t *)p)[i]) << 15;"),
 }
