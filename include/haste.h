@@ -50,7 +50,8 @@ enum haste_status {
 
 /* Workspace-query operation codes. */
 enum haste_op {
-    HASTE_OP_FWD = 0, HASTE_OP_BWD_W = 1, HASTE_OP_BWD_X = 2, HASTE_OP_FWD_BCE = 3, HASTE_OP_FWD_BCE_SGD = 4
+    HASTE_OP_FWD = 0, HASTE_OP_BWD_W = 1, HASTE_OP_BWD_X = 2, HASTE_OP_FWD_BCE = 3, HASTE_OP_FWD_BCE_SGD = 4,
+    HASTE_OP_REWIRE = 5
 };
 
 /* Hyper-parameters of one step of SGD with momentum (see haste_sgd_momentum). */
@@ -158,6 +159,30 @@ int haste_fwd_bce_sgd(const haste_desc_t *desc, const void *X, const int32_t *id
  */
 int haste_sgd_momentum(int64_t n, int32_t dtype, const void *W, const float *grad, float *m,
                        const haste_sgd_t *opt, void *W_next, void *stream);
+
+/*
+ * Group-shared rewiring (Alg. 3; the discrete phase of the training loop, Section 3.4), in place:
+ *   1. score[k, j] = sum over the G labels l of group k of |W[l, j]|, fp32, labels in order (the
+ *      algorithm's mean, scaled by the common factor G, which orders the scores identically);
+ *   2. prune the m = floor(K * F_in * rho) smallest scores over all groups, ties to the lower
+ *      flat index k * F_in + j;
+ *   3. each pruned slot of group k, in ascending slot order, takes a feature drawn uniformly from
+ *      [0, F_s) minus the features the group keeps and those drawn before it (rows stay sets);
+ *      then row k is re-sorted, each slot carrying its weight column W[kG .. kG+G-1, j] and its
+ *      velocity m[.., j] with it;
+ *   4. pruned slots' weights: 0 (init_random = 0) or uniform in [-1/sqrt(F_in), 1/sqrt(F_in)]
+ *      (init_random = 1), stored in the dtype of W; their velocity is set to 0.
+ * Draws: SplitMix64 (Steele, Lea and Flood, 2014) in counter form, output i of the stream seeded
+ * with `seed`: the new feature of slot j of group k is the (out(k F + j) mod n_free)-th free
+ * feature in ascending order; label l's new weight at slot j is ((2 n - 2^24) as fp32) *
+ * (fp32(1/sqrt(F_in)) * 2^-24) with n = out(K F + l F + j) >> 40.
+ * idx [K, F_in] int32 (strictly increasing rows, precondition), W [L, F_in] (dtype) and m
+ * [L, F_in] fp32 (or NULL) are updated in place.  rho in [0, 1); *n_pruned (host, or NULL)
+ * receives m.  F_in <= 128.  ws: haste_workspace_bytes(desc, HASTE_OP_REWIRE) bytes; desc->B is
+ * not used.
+ */
+int haste_rewire(const haste_desc_t *desc, int32_t *idx, void *W, float *m, double rho, int32_t init_random,
+                 uint64_t seed, int64_t *n_pruned, void *ws, size_t ws_bytes, void *stream);
 
 /*
  * Gradient of the binary cross-entropy objective at stored logits (Section 3.3), for the dense

@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(PKG, "libhaste.so")
 
 HASTE_DTYPE_F32 = 0
 HASTE_DTYPE_BF16 = 1
-HASTE_OP_FWD, HASTE_OP_BWD_W, HASTE_OP_BWD_X, HASTE_OP_FWD_BCE, HASTE_OP_FWD_BCE_SGD = 0, 1, 2, 3, 4
+HASTE_OP_FWD, HASTE_OP_BWD_W, HASTE_OP_BWD_X, HASTE_OP_FWD_BCE, HASTE_OP_FWD_BCE_SGD, HASTE_OP_REWIRE = range(6)
 STATUS = {0: "ok", 1: "invalid argument", 2: "unsupported", 3: "workspace too small", 4: "HIP error"}
 
 
@@ -53,6 +53,7 @@ def _load() -> ctypes.CDLL:
         "haste_bce_grad": [I64, I64, I32, P, P, I32, P, P],
         "haste_fwd_bce_sgd": [D, P, P, P, P, P, I32, P, P, ctypes.POINTER(haste_sgd_t), P, P, P, SZ, P],
         "haste_sgd_momentum": [I64, I32, P, P, P, ctypes.POINTER(haste_sgd_t), P, P],
+        "haste_rewire": [D, P, P, P, ctypes.c_double, I32, ctypes.c_uint64, P, P, SZ, P],
         "haste_head_fwd": [I64, I64, I64, I32, P, P, P, P, P],
         "haste_head_bwd": [I64, I64, I64, I32, P, P, P, P, P, ctypes.c_int, P, SZ, P],
         "haste_validate_idx": [D, P, P, P],
@@ -76,7 +77,7 @@ lib = _load()
 
 # every symbol the header declares
 EXPORTS = ("haste_fwd", "haste_bwd_w", "haste_bwd_x", "haste_fwd_bce", "haste_fwd_bce_sgd", "haste_sgd_momentum",
-           "haste_bce_grad", "haste_head_fwd", "haste_head_bwd", "haste_workspace_bytes",
+           "haste_rewire", "haste_bce_grad", "haste_head_fwd", "haste_head_bwd", "haste_workspace_bytes",
            "haste_head_workspace_bytes", "haste_validate_idx", "haste_debug_gather", "haste_status_str",
            "haste_last_error", "haste_version")
 
@@ -189,6 +190,15 @@ def haste_fwd_bce_sgd(desc, X, idx, W, bias, pos, dY, opt, m, W_next, dbias=None
 def haste_sgd_momentum(n, dtype, W, grad, m, opt, W_next, stream=None):
     _check(lib.haste_sgd_momentum(int(n), dtype, _ptr(W), _ptr(grad), _ptr(m), ctypes.byref(opt), _ptr(W_next),
                                   _stream(stream)))
+
+
+def haste_rewire(desc, idx, W, m, rho, init_random, seed, ws=None, stream=None) -> int:
+    """Rewires in place; returns the number of pruned slots."""
+    p, n = _ws(ws)
+    npr = ctypes.c_int64(0)
+    _check(lib.haste_rewire(ctypes.byref(desc), _ptr(idx), _ptr(W), _ptr(m), float(rho), int(init_random),
+                            int(seed) & ((1 << 64) - 1), ctypes.byref(npr), p, n, _stream(stream)))
+    return int(npr.value)
 
 
 def haste_bce_grad(B, N, dtype, Y, pos, dY, stream=None):

@@ -1,5 +1,6 @@
 // C ABI of libhaste.so: argument validation, kernel selection and launch on the caller's stream.
 // Nothing here allocates, frees or synchronises; scratch comes only from the caller's workspace.
+#include <math.h>
 #include <stdarg.h>
 #include <stdio.h>
 #include <string.h>
@@ -85,6 +86,7 @@ const char *haste_last_error(void) { return g_err; }
 size_t haste_workspace_bytes(const haste_desc_t *d, int op) {
     if (check_desc(d) != HASTE_OK) return 0;
     const haste::TailArgs a = targs(d);
+    if (op == HASTE_OP_REWIRE) return a.L > 0 && haste::rewire_supported(a) ? haste::rewire_ws(a) : 0;
     if (a.B == 0 || a.L == 0) return 0;
     switch (op) {
         case HASTE_OP_FWD: return 0;
@@ -93,6 +95,7 @@ size_t haste_workspace_bytes(const haste_desc_t *d, int op) {
         // the fused kernel and the backward-weight kernel stage the same X^T copy
         case HASTE_OP_FWD_BCE: return haste::bwd_w_mfma_supported(a) ? haste::bwd_w_mfma_ws(a) : 0;
         // the composed form also keeps dW in the workspace (after the X^T copy)
+        case HASTE_OP_REWIRE: return haste::rewire_supported(a) ? haste::rewire_ws(a) : 0;
         case HASTE_OP_FWD_BCE_SGD:
             return (haste::bwd_w_mfma_supported(a) ? haste::bwd_w_mfma_ws(a) : 0) +
                    (haste::fwd_bce_mfma_supported(a, 0) ? 0 : (size_t)haste::round_up(a.L * a.F_in * 4, 256));
@@ -296,6 +299,28 @@ int haste_fwd_bce_sgd(const haste_desc_t *d, const void *X, const int32_t *idx, 
     const int rc = haste_fwd_bce(d, X, idx, W, bias, pos, P, dY, dW, dbias, 0, ws, xws, stream);
     if (rc != HASTE_OK) return rc;
     return hip_status(haste::sgd_momentum(a.L * a.F_in, a.dtype, W, dW, m, *opt, W_next, s), "haste_fwd_bce_sgd");
+}
+
+int haste_rewire(const haste_desc_t *d, int32_t *idx, void *W, float *m, double rho, int32_t init_random,
+                 uint64_t seed, int64_t *n_pruned, void *ws, size_t ws_bytes, void *stream) {
+    TRY(check_desc(d));
+    if (!(rho >= 0.0 && rho < 1.0)) return fail(HASTE_ERR_INVALID, "rho must be in [0, 1)");
+    if (init_random != 0 && init_random != 1) return fail(HASTE_ERR_INVALID, "init_random must be 0 or 1");
+    const haste::TailArgs a = targs(d);
+    if (!haste::rewire_supported(a)) return fail(HASTE_ERR_UNSUPPORTED, "rewiring takes at most 128 slots per group");
+    const int64_t K = a.L / a.G;
+    const int64_t npr = (int64_t)floor((double)K * (double)a.F_in * rho);
+    if (n_pruned) *n_pruned = npr;
+    if (npr == 0) return ok();
+    TRY(need_ptr(idx, "idx"));
+    TRY(need_ptr(W, "W"));
+    if (m) TRY(need_ptr(m, "m"));
+    const size_t need = haste::rewire_ws(a);
+    if (!ws || ws_bytes < need)
+        return fail(HASTE_ERR_WORKSPACE, "haste_rewire needs %zu workspace bytes, got %zu", need, ws ? ws_bytes : 0);
+    TRY(need_ptr(ws, "ws"));
+    if (K * a.F_in >= ((int64_t)1 << 31) / 4) return fail(HASTE_ERR_UNSUPPORTED, "K * F_in too large");
+    return hip_status(haste::rewire(a, idx, W, m, npr, init_random, seed, ws, as_stream(stream)), "haste_rewire");
 }
 
 int haste_bce_grad(int64_t B, int64_t N, int32_t dtype, const void *Y, const int32_t *pos, int32_t P, void *dY,

@@ -156,6 +156,11 @@ hipError_t fwd_bce_sgd_mfma(const TailArgs &a, const void *X, const int32_t *idx
 // momentum step over n weights: m and W_next updated (W_next may alias W)
 hipError_t sgd_momentum(int64_t n, int32_t dtype, const void *W, const float *g, float *m, const haste_sgd_t &opt,
                         void *W_next, hipStream_t s);
+// group-shared rewiring (Alg. 3); n_prune >= 1
+bool rewire_supported(const TailArgs &a);
+size_t rewire_ws(const TailArgs &a);
+hipError_t rewire(const TailArgs &a, int32_t *idx, void *W, float *m, int64_t n_prune, int init_random, uint64_t seed,
+                  void *ws, hipStream_t s);
 // dY[b, n] = sigmoid(Y[b, n]) - T[b, n] elementwise (Y and dY may alias)
 hipError_t bce_grad(int64_t B, int64_t N, int32_t dtype, const void *Y, const int32_t *pos, int P, void *dY,
                     hipStream_t s);
