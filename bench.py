@@ -43,6 +43,7 @@ CALL_KERNELS = {
     "fwd_bce_sgd": ["k_transpose_x", "k_fwd_bce"],
     "sgd": ["k_sgd_momentum"],
     "head_sgd": ["k_sgd_momentum"],
+    "rewire": ["k_rw_"],
     "bce": ["k_bce_grad"],
     "head_bce": ["k_bce_grad"],
     "bwd_w": ["k_transpose_x", "k_bwd_w"],
@@ -436,6 +437,30 @@ def main():
                                           out["dense_bottleneck"]["ms"], 3)
         out["separate_calls_step"]["tail_vs_bottleneck"] = round(
             sum(sep_per[k] for k in ("fwd", "bwd_w", "bwd_x")) / out["dense_bottleneck"]["ms"], 3)
+    # rewiring (Alg. 3) at rho = 0.1 on copies of the supports and weights, timed alone (it runs
+    # every few hundred steps, not in the step)
+    if wl.dtype == synth.DT_BF16 or wl.dtype == synth.DT_F32:
+        idx_r, W_r = idxd.clone(), Wd.clone()
+        ws_r = hs.workspace(hs.haste_workspace_bytes(desc, hs.HASTE_OP_REWIRE))
+        n_r = 0
+        for _ in range(2):
+            idx_r.copy_(idxd)
+            W_r.copy_(Wd)
+            n_r = hs.haste_rewire(desc, idx_r, W_r, None, 0.1, 1, 7, ws_r)
+        torch.cuda.synchronize()
+        r_ms = 0.0
+        for it in range(5):
+            idx_r.copy_(idxd)
+            W_r.copy_(Wd)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            hs.haste_rewire(desc, idx_r, W_r, None, 0.1, 1, 7 + it, ws_r)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            r_ms += e0.elapsed_time(e1) / 5
+        out["rewire"] = {"ms": round(r_ms, 4), "rho": 0.1, "pruned_slots": n_r,
+                         "what": "haste_rewire (Alg. 3) on the layer's supports and weights, random reinit"}
+        del idx_r, W_r, ws_r
     if args.copy_calibration:
         src = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device=dev).fill_(1.0)
         dst = torch.empty_like(src)
