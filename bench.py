@@ -109,10 +109,21 @@ def call_cost(wl, dt_bytes=2, n_pos=0):
     return c
 
 
-def kernel_source_hash():
+# source files of each call's kernels (the shared header is part of every call)
+CALL_FILES = {
+    "head_fwd": ["head.hip"], "head_bwd": ["head.hip", "util.hip"],
+    "bce": ["util.hip"], "head_bce": ["util.hip"], "sgd": ["util.hip"], "head_sgd": ["util.hip"],
+    "rewire": ["rewire.hip"],
+}
+
+
+def kernel_source_hash(call=None):
+    """Hash of the kernel sources: those of one call (default: the tail file), or all of them."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2606_01117_amd", "csrc")
-    for f in sorted(os.listdir(csrc)):
+    files = sorted(os.listdir(csrc)) if call is None else sorted(
+        CALL_FILES.get(call, ["tail_mfma.hip"]) + ["common.hpp"])
+    for f in files:
         with open(os.path.join(csrc, f), "rb") as fh:
             h.update(f.encode() + fh.read())
     return h.hexdigest()[:16]
@@ -131,7 +142,7 @@ def measured_traffic(workload, call):
         t = json.loads(line)
     except (OSError, ValueError, StopIteration):
         return None
-    if t.get("kernel_source_hash") != kernel_source_hash():
+    if t.get("call_source_hash", {}).get(call) != kernel_source_hash(call):
         return None
     return t.get("calls", {}).get(call)
 
@@ -196,7 +207,8 @@ def summarize_traffic(fetch_db, write_db, workload, command):
         fv = (lambda k: pick(fetch_d[k])) if pick else (lambda k: fetch[k])
         wv = (lambda k: pick(write_d[k]) if k in write_d else 0.0) if pick else (lambda k: write.get(k, 0.0))
         calls[call] = round(sum(fv(k) * f_fetch + wv(k) * f_write for k in ks))
-    rec = {"workload": workload, "kernel_source_hash": kernel_source_hash(), "copy_kernel": ck,
+    rec = {"workload": workload, "kernel_source_hash": kernel_source_hash(),
+           "call_source_hash": {c: kernel_source_hash(c) for c in calls}, "copy_kernel": ck,
            "fetch_factor": round(f_fetch, 4), "write_factor": round(f_write, 4), "calls": calls}
     lines = [f"HBM traffic per launch, workload {workload}",
              "rocprofv3 --pmc FETCH_SIZE, then --pmc WRITE_SIZE (KiB per dispatch), each scaled by the factor",
