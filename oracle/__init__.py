@@ -68,6 +68,8 @@ class Oracle:
         L.haste_oracle_rewire.argtypes = [_I64, _I64, _I64, _I64, ctypes.c_int, _P, _P, _P, _D, ctypes.c_int,
                                           ctypes.c_uint64, _P, _P]
         L.haste_oracle_rewire.restype = ctypes.c_int
+        L.haste_oracle_group_labels.argtypes = [_I64, _I64, _P, _I64, _I64, _I64, ctypes.c_uint64, _P, _P, _P, _P]
+        L.haste_oracle_group_labels.restype = ctypes.c_int
         for f in ("fwd", "fwd_at", "bwd_w", "bwd_x", "head_fwd", "head_bwd_w", "head_bwd_x", "bce_grad",
                   "bce_grad_at", "sgd_momentum"):
             getattr(L, "haste_oracle_" + f).restype = ctypes.c_int
@@ -186,6 +188,19 @@ class Oracle:
                                           seed, ctypes.byref(n), _ptr(mask))
         self._check(rc, "rewire")
         return idx, W, mm, int(n.value), mask.reshape(K, F).astype(bool)
+
+    def group_labels(self, E, G, beta, iters, seed):
+        """Alg. 2 on int8 embeddings E [N, D]: (order [N], group sizes, cluster [N])."""
+        E = np.ascontiguousarray(E, dtype=np.int8)
+        N, D = E.shape
+        order = np.empty(N, dtype=np.int32)
+        gsize = np.empty(N, dtype=np.int32)
+        cl = np.empty(N, dtype=np.int32)
+        ng = ctypes.c_int64(0)
+        rc = self.lib.haste_oracle_group_labels(N, D, _ptr(E), G, beta, iters, seed, _ptr(order), _ptr(gsize),
+                                                ctypes.byref(ng), _ptr(cl))
+        self._check(rc, "group_labels")
+        return order, gsize[:ng.value].copy(), cl
 
     def bwd_x(self, idx, W, dY, G, F_s, dtype, b0=0, b1=None):
         """dX[b1-b0, F_s] in fp64 for rows [b0, b1)."""

@@ -17,6 +17,7 @@
  *   - BCE     d/dz of the binary cross-entropy of sigmoid(z)      (Section 3.3 objective)
  *   - SGD     momentum step of the classification layer's optimizer (Section 4)
  *   - rewire  group-shared rewiring of the supports (Alg. 3)
+ *   - group   semantic grouping of labels (Alg. 2)
  *
  * Arithmetic: inputs are decoded exactly to double (bf16 -> fp64 and fp32 -> fp64 are exact);
  * every sum is accumulated in double in the order the definition states (no blocking, no
@@ -390,5 +391,118 @@ int haste_oracle_rewire(int64_t K, int64_t G, int64_t F, int64_t H, int dtype, i
         }
     }
     free(used); free(row); free(tmp);
+    return 0;
+}
+
+/* ---------------------------------------------------------------------------------------------
+ * Semantic label grouping (Alg. 2): coarse spherical k-means into C = max(1, floor(N / (beta G)))
+ * clusters, then, inside each cluster, greedy groups of G: a random unassigned seed and its
+ * top-G unassigned labels by similarity (the seed included).
+ * Readings:
+ *   - embeddings are unit vectors stored as int8 (x 127), so every similarity is an exact integer
+ *     dot product and every assignment, seed and top-G decision is exact;
+ *   - k-means runs `iters` full Lloyd iterations (assign all labels, then move each non-empty
+ *     cluster's centre to the int8-quantised direction of its members' sum: round-half-even of
+ *     127 s / |s|, |s| in fp64), then a final assignment; the paper's mini-batch variant is a CPU
+ *     economy.  Assignment ties go to the lower cluster index;
+ *   - initial centres: the first C entries of a partial Fisher-Yates shuffle of [0, N) whose i-th
+ *     swap partner is i + out(i) mod (N - i); the t-th seed of cluster c is the
+ *     (out(N + c N + t) mod n_unassigned)-th unassigned member in ascending label order
+ *     (out = SplitMix64 in counter form, as for rewiring);
+ *   - top-G ties go to the lower label; a group lists its labels in ascending order; groups are
+ *     emitted cluster by cluster, in the order they are formed.
+ * E [N, D] int8; order [N] receives the labels group after group, gsize the group sizes,
+ * *n_groups their count, cluster [N] (or NULL) the final cluster of each label.
+ * ------------------------------------------------------------------------------------------- */
+static int64_t dot8(const int8_t *a, const int8_t *b, int64_t D) {
+    int64_t s = 0;
+    for (int64_t d = 0; d < D; ++d) s += (int64_t)a[d] * (int64_t)b[d];
+    return s;
+}
+
+static void assign_all(int64_t N, int64_t D, int64_t C, const int8_t *E, const int8_t *cen, int32_t *cl) {
+#pragma omp parallel for schedule(static)
+    for (int64_t l = 0; l < N; ++l) {
+        int64_t best = 0, bv = dot8(E + l * D, cen, D);
+        for (int64_t c = 1; c < C; ++c) {
+            const int64_t v = dot8(E + l * D, cen + c * D, D);
+            if (v > bv) { bv = v; best = c; }
+        }
+        cl[l] = (int32_t)best;
+    }
+}
+
+typedef struct { int64_t sim; int32_t id; } cand_t;
+
+static int by_sim(const void *a, const void *b) {
+    const cand_t *x = (const cand_t *)a, *y = (const cand_t *)b;
+    if (x->sim != y->sim) return x->sim > y->sim ? -1 : 1;
+    return (x->id > y->id) - (x->id < y->id);
+}
+
+static int by_id(const void *a, const void *b) {
+    const int32_t x = *(const int32_t *)a, y = *(const int32_t *)b;
+    return (x > y) - (x < y);
+}
+
+int haste_oracle_group_labels(int64_t N, int64_t D, const int8_t *E, int64_t G, int64_t beta, int64_t iters,
+                              uint64_t seed, int32_t *order, int32_t *gsize, int64_t *n_groups, int32_t *cluster) {
+    if (N <= 0 || D <= 0 || G <= 0 || beta <= 0 || iters < 0) return 1;
+    int64_t C = N / (beta * G);
+    if (C < 1) C = 1;
+    int32_t *a = (int32_t *)malloc((size_t)N * sizeof(int32_t));
+    int8_t *cen = (int8_t *)malloc((size_t)(C * D));
+    int32_t *cl = (int32_t *)malloc((size_t)N * sizeof(int32_t));
+    int64_t *sum = (int64_t *)malloc((size_t)D * sizeof(int64_t));
+    cand_t *cand = (cand_t *)malloc((size_t)N * sizeof(cand_t));
+    if (!a || !cen || !cl || !sum || !cand) { free(a); free(cen); free(cl); free(sum); free(cand); return 2; }
+    for (int64_t i = 0; i < N; ++i) a[i] = (int32_t)i;
+    for (int64_t i = 0; i < C; ++i) {
+        const int64_t j = i + (int64_t)(splitmix64_at(seed, (uint64_t)i) % (uint64_t)(N - i));
+        const int32_t t = a[i]; a[i] = a[j]; a[j] = t;
+        memcpy(cen + i * D, E + (int64_t)a[i] * D, (size_t)D);
+    }
+    for (int64_t it = 0; it < iters; ++it) {
+        assign_all(N, D, C, E, cen, cl);
+        for (int64_t c = 0; c < C; ++c) {
+            memset(sum, 0, (size_t)D * sizeof(int64_t));
+            int64_t cnt = 0;
+            for (int64_t l = 0; l < N; ++l)
+                if (cl[l] == c) { ++cnt; for (int64_t d = 0; d < D; ++d) sum[d] += E[l * D + d]; }
+            int64_t ss = 0;
+            for (int64_t d = 0; d < D; ++d) ss += sum[d] * sum[d];
+            if (cnt == 0 || ss == 0) continue;   /* an empty cluster keeps its centre */
+            const double norm = sqrt((double)ss);
+            for (int64_t d = 0; d < D; ++d) {
+                double q = rint(127.0 * (double)sum[d] / norm);
+                cen[c * D + d] = (int8_t)(q > 127.0 ? 127.0 : (q < -127.0 ? -127.0 : q));
+            }
+        }
+    }
+    assign_all(N, D, C, E, cen, cl);
+    if (cluster) memcpy(cluster, cl, (size_t)N * sizeof(int32_t));
+    int64_t pos = 0, ng = 0;
+    for (int64_t c = 0; c < C; ++c) {
+        int64_t nu = 0;   /* unassigned members, ascending */
+        for (int64_t l = 0; l < N; ++l)
+            if (cl[l] == c) a[nu++] = (int32_t)l;
+        for (int64_t t = 0; nu > 0; ++t) {
+            const int64_t s = a[(int64_t)(splitmix64_at(seed, (uint64_t)(N + c * N + t)) % (uint64_t)nu)];
+            for (int64_t i = 0; i < nu; ++i) { cand[i].sim = dot8(E + (int64_t)a[i] * D, E + s * D, D); cand[i].id = a[i]; }
+            qsort(cand, (size_t)nu, sizeof(cand_t), by_sim);
+            const int64_t k = nu < G ? nu : G;
+            for (int64_t i = 0; i < k; ++i) order[pos + i] = cand[i].id;
+            qsort(order + pos, (size_t)k, sizeof(int32_t), by_id);
+            gsize[ng++] = (int32_t)k;
+            pos += k;
+            /* the rest stay unassigned, ascending */
+            int64_t r = 0;
+            for (int64_t i = k; i < nu; ++i) a[r++] = cand[i].id;
+            qsort(a, (size_t)r, sizeof(int32_t), by_id);
+            nu = r;
+        }
+    }
+    *n_groups = ng;
+    free(a); free(cen); free(cl); free(sum); free(cand);
     return 0;
 }

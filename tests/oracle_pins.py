@@ -14,6 +14,7 @@ raises AssertionError when the oracle disagrees with:
   quadratic;
 * the rewiring of Alg. 3 on a hand-checked layer, its tie rule, its invariants on random layers,
   the uniformity of its draws, and the published outputs of its generator;
+* the grouping of Alg. 2 on planted directions (exact groups) and planted clusters (recovered);
 * the adjoint identity <dY, Y - bias> = <dX, X> = <dW, W> (bilinearity);
 * exact one-hot gathers/scatters and the group-permutation invariance.
 """
@@ -491,8 +492,64 @@ def pin_rewire_uniform(o):
     assert counts.sum() > 1000 and chi2 < 25.0, f"new-feature ranks not uniform: {counts}, chi2 {chi2:.1f}"
 
 
+def _unit_int8(X):
+    X = np.asarray(X, np.float64)
+    return np.rint(127 * X / np.linalg.norm(X, axis=1, keepdims=True)).astype(np.int8)
+
+
+def pin_group_greedy(o):
+    """Alg. 2's greedy stage on one coarse cluster (beta G >= N): three planted directions of four
+    labels each (labels interleaved) come back as exactly those three groups, whatever the seed."""
+    rng = np.random.default_rng(51)
+    N, D = 12, 8
+    X = np.zeros((N, D))
+    for l in range(N):
+        X[l, l % 3] = 10.0
+        X[l, 3:] = rng.standard_normal(D - 3)
+    E = _unit_int8(X)
+    want = {frozenset(l for l in range(N) if l % 3 == g) for g in range(3)}
+    for seed in (0, 1, 2, 12345):
+        order, gs, cl = o.group_labels(E, 4, 3, 3, seed)
+        assert list(gs) == [4, 4, 4] and not cl.any()
+        groups = [order[4 * i: 4 * i + 4] for i in range(3)]
+        assert all(list(g) == sorted(g) for g in groups)
+        assert {frozenset(int(x) for x in g) for g in groups} == want, f"seed {seed}: {groups}"
+
+
+def pin_group_planted(o):
+    """On embeddings with eight planted clusters of 256, the coarse k-means recovers the clusters
+    (each k-means cluster dominated by one planted cluster), at least 90% of the groups are pure,
+    and the output is a partition into groups of G (the last of a cluster may be short)."""
+    rng = np.random.default_rng(53)
+    N, D, P, G, beta = 2048, 64, 8, 16, 16
+    mu = rng.standard_normal((P, D))
+    planted = rng.permutation(np.repeat(np.arange(P), N // P))
+    E = _unit_int8(mu[planted] / np.linalg.norm(mu[planted], axis=1, keepdims=True) * 4 + rng.standard_normal((N, D)) * 0.15)
+    order, gs, cl = o.group_labels(E, G, beta, 8, 77)
+    assert sorted(order.tolist()) == list(range(N)), "groups must partition the labels"
+    C = N // (beta * G)
+    assert cl.min() >= 0 and cl.max() < C
+    dominated = 0
+    for c in range(C):
+        members = planted[cl == c]
+        if members.size and np.bincount(members, minlength=P).max() >= 0.8 * members.size:
+            dominated += 1
+    assert dominated >= C - 2, f"only {dominated} of {C} k-means clusters follow the planted ones"
+    starts = np.concatenate([[0], np.cumsum(gs)])
+    pure = 0
+    for i in range(gs.size):
+        g = order[starts[i]:starts[i + 1]]
+        assert len(set(cl[g])) == 1, "a group spans two coarse clusters"
+        pure += len(set(planted[g])) == 1
+    assert pure >= 0.9 * gs.size, f"only {pure} of {gs.size} groups are pure"
+    for c in range(C):
+        n_c = int((cl == c).sum())
+        assert sum(1 for i in range(gs.size) if cl[order[starts[i]]] == c) == -(-n_c // G), "groups per cluster"
+    assert gs.max() <= G
+
+
 ALL_PINS = [pin_fig2_gs, pin_fig2_ffi, pin_bruteforce, pin_duplicate_indices, pin_dense_special_case,
             pin_group_equals_expanded_ffi, pin_finite_differences, pin_adjoint_identity, pin_one_hot,
             pin_group_permutation, pin_label_ranges, pin_head, pin_bce_grad,
             pin_sgd_momentum, pin_splitmix64, pin_rewire_hand, pin_rewire_ties_and_noop, pin_rewire_invariants,
-            pin_rewire_uniform]
+            pin_rewire_uniform, pin_group_greedy, pin_group_planted]

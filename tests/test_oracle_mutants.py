@@ -56,6 +56,11 @@ MUTANTS = {
     "rewire_kept_not_excluded": ("if (!mask[k * F + j]) { used[idx[k * F + j]] = 1; ++n_used; }",
                                  "if (!mask[k * F + j]) { ++n_used; }"),
     "rewire_column_not_moved": ("tmp[p] = ld(W, l * F + j, dtype);", "tmp[p] = ld(W, l * F + p, dtype);"),
+    "group_least_similar": ("if (x->sim != y->sim) return x->sim > y->sim ? -1 : 1;",
+                            "if (x->sim != y->sim) return x->sim < y->sim ? -1 : 1;"),
+    "group_assign_argmin": ("if (v > bv) { bv = v; best = c; }", "if (v < bv) { bv = v; best = c; }"),
+    "group_centre_negated": ("for (int64_t d = 0; d < D; ++d) sum[d] += E[l * D + d]; }",
+                             "for (int64_t d = 0; d < D; ++d) sum[d] -= E[l * D + d]; }"),
     "bf16_decode_shift": ("uint32_t u = ((uint32_t)((const uint16_t *)p)[i]) << 16;",
                           "uint32_t u = ((uint32_t)((const uint16_t *)p)[i]) << 15;"),
 }
