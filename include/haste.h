@@ -184,6 +184,43 @@ int haste_sgd_momentum(int64_t n, int32_t dtype, const void *W, const float *gra
 int haste_rewire(const haste_desc_t *desc, int32_t *idx, void *W, float *m, double rho, int32_t init_random,
                  uint64_t seed, int64_t *n_pruned, void *ws, size_t ws_bytes, void *stream);
 
+/* Options of haste_group_labels. */
+typedef struct haste_group_opts {
+    int64_t G;       /* group size (1 .. 256)                                         */
+    int64_t beta;    /* bucket factor: C = max(1, floor(N / (beta * G))) clusters      */
+    int64_t iters;   /* k-means iterations (>= 0)                                      */
+    uint64_t seed;   /* SplitMix64 seed of the initial centres and the group seeds      */
+} haste_group_opts_t;
+
+/*
+ * Semantic grouping of labels (Alg. 2), before training: coarse spherical k-means into C clusters,
+ * then, inside each cluster, greedy groups of G: a random unassigned seed and its top-G
+ * unassigned labels by similarity (the seed included), until the cluster is used up.
+ *   - E [N, D] int8: unit label embeddings scaled by 127 (round(127 e / |e|)); similarities are
+ *     exact integer dot products, so every decision below is exact.
+ *   - k-means: centres start as the first C labels of a partial Fisher-Yates shuffle of [0, N)
+ *     (swap partner of i: i + out(i) mod (N - i)); `iters` full Lloyd iterations follow (assign
+ *     every label to its most similar centre, ties to the lower centre; move each non-empty
+ *     cluster's centre to round-half-even(127 s / |s|) of its members' sum s, |s| in fp64), then a
+ *     final assignment.  (The paper runs mini-batch k-means, a CPU economy; full passes of the
+ *     [N, D] x [D, C] product are cheap on the GPU.)
+ *   - groups: cluster by cluster; the t-th seed of cluster c is the (out(N + c N + t) mod
+ *     n_unassigned)-th unassigned member in ascending label order; top-G ties go to the lower
+ *     label; a group lists its labels in ascending order.  The last group of a cluster may have
+ *     fewer than G labels (the layout needs L % G == 0: pad with zero-weight labels).
+ *   out(i) is SplitMix64 (Steele, Lea and Flood, 2014) output i of the stream seeded with seed.
+ * order [N] int32 receives the labels group after group; gsize [N] int32 the group sizes (first
+ * *n_groups entries); n_groups is a DEVICE int64; cluster [N] int32 (device, or NULL) the final
+ * cluster of each label.  D % 16 == 0, D <= 1024, N < 2^24.
+ * ws: haste_group_workspace_bytes(N, D, opts) bytes.
+ */
+int haste_group_labels(int64_t N, int64_t D, const int8_t *E, const haste_group_opts_t *opts, int32_t *order,
+                       int32_t *gsize, int64_t *n_groups, int32_t *cluster, void *ws, size_t ws_bytes,
+                       void *stream);
+
+/* Bytes of workspace haste_group_labels needs (0 for invalid arguments). */
+size_t haste_group_workspace_bytes(int64_t N, int64_t D, const haste_group_opts_t *opts);
+
 /*
  * Gradient of the binary cross-entropy objective at stored logits (Section 3.3), for the dense
  * head or any [B, N] logit block:

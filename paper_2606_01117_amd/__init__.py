@@ -39,6 +39,10 @@ class haste_sgd_t(ctypes.Structure):
                 ("reserved", ctypes.c_int32)]
 
 
+class haste_group_opts_t(ctypes.Structure):
+    _fields_ = [("G", ctypes.c_int64), ("beta", ctypes.c_int64), ("iters", ctypes.c_int64), ("seed", ctypes.c_uint64)]
+
+
 def _load() -> ctypes.CDLL:
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"libhaste.so is not built ({LIB_PATH}); run paper_2606_01117_amd.build.build()")
@@ -54,6 +58,7 @@ def _load() -> ctypes.CDLL:
         "haste_fwd_bce_sgd": [D, P, P, P, P, P, I32, P, P, ctypes.POINTER(haste_sgd_t), P, P, P, SZ, P],
         "haste_sgd_momentum": [I64, I32, P, P, P, ctypes.POINTER(haste_sgd_t), P, P],
         "haste_rewire": [D, P, P, P, ctypes.c_double, I32, ctypes.c_uint64, P, P, SZ, P],
+        "haste_group_labels": [I64, I64, P, ctypes.POINTER(haste_group_opts_t), P, P, P, P, P, SZ, P],
         "haste_head_fwd": [I64, I64, I64, I32, P, P, P, P, P],
         "haste_head_bwd": [I64, I64, I64, I32, P, P, P, P, P, ctypes.c_int, P, SZ, P],
         "haste_validate_idx": [D, P, P, P],
@@ -67,6 +72,8 @@ def _load() -> ctypes.CDLL:
     lib.haste_workspace_bytes.restype = SZ
     lib.haste_head_workspace_bytes.argtypes = [I64, I64, I64, I32]
     lib.haste_head_workspace_bytes.restype = SZ
+    lib.haste_group_workspace_bytes.argtypes = [I64, I64, ctypes.POINTER(haste_group_opts_t)]
+    lib.haste_group_workspace_bytes.restype = SZ
     for name in ("haste_status_str", "haste_last_error", "haste_version"):
         getattr(lib, name).restype = ctypes.c_char_p
     lib.haste_status_str.argtypes = [ctypes.c_int]
@@ -77,7 +84,7 @@ lib = _load()
 
 # every symbol the header declares
 EXPORTS = ("haste_fwd", "haste_bwd_w", "haste_bwd_x", "haste_fwd_bce", "haste_fwd_bce_sgd", "haste_sgd_momentum",
-           "haste_rewire", "haste_bce_grad", "haste_head_fwd", "haste_head_bwd", "haste_workspace_bytes",
+           "haste_rewire", "haste_group_labels", "haste_group_workspace_bytes", "haste_bce_grad", "haste_head_fwd", "haste_head_bwd", "haste_workspace_bytes",
            "haste_head_workspace_bytes", "haste_validate_idx", "haste_debug_gather", "haste_status_str",
            "haste_last_error", "haste_version")
 
@@ -199,6 +206,22 @@ def haste_rewire(desc, idx, W, m, rho, init_random, seed, ws=None, stream=None) 
     _check(lib.haste_rewire(ctypes.byref(desc), _ptr(idx), _ptr(W), _ptr(m), float(rho), int(init_random),
                             int(seed) & ((1 << 64) - 1), ctypes.byref(npr), p, n, _stream(stream)))
     return int(npr.value)
+
+
+def group_opts(G: int, beta: int, iters: int, seed: int) -> haste_group_opts_t:
+    return haste_group_opts_t(G, beta, iters, seed & ((1 << 64) - 1))
+
+
+def haste_group_workspace_bytes(N, D, opts) -> int:
+    return int(lib.haste_group_workspace_bytes(N, D, ctypes.byref(opts)))
+
+
+def haste_group_labels(E, opts, order, gsize, n_groups, cluster=None, ws=None, stream=None):
+    """E: [N, D] int8 device tensor; n_groups: a 1-element int64 device tensor."""
+    p, n = _ws(ws)
+    N, D = E.shape
+    _check(lib.haste_group_labels(N, D, _ptr(E), ctypes.byref(opts), _ptr(order), _ptr(gsize), _ptr(n_groups),
+                                  _ptr(cluster), p, n, _stream(stream)))
 
 
 def haste_bce_grad(B, N, dtype, Y, pos, dY, stream=None):

@@ -323,6 +323,36 @@ int haste_rewire(const haste_desc_t *d, int32_t *idx, void *W, float *m, double 
     return hip_status(haste::rewire(a, idx, W, m, npr, init_random, seed, ws, as_stream(stream)), "haste_rewire");
 }
 
+static int check_group(int64_t N, int64_t D, const haste_group_opts_t *o) {
+    if (!o) return fail(HASTE_ERR_INVALID, "opts is NULL");
+    if (o->beta < 1 || o->iters < 0) return fail(HASTE_ERR_INVALID, "beta must be >= 1 and iters >= 0");
+    if (!haste::group_supported(N, D, o->G))
+        return fail(HASTE_ERR_UNSUPPORTED, "grouping needs 0 < N < 2^24, D a multiple of 16 up to 1024, 1 <= G <= 256");
+    return HASTE_OK;
+}
+
+size_t haste_group_workspace_bytes(int64_t N, int64_t D, const haste_group_opts_t *o) {
+    if (check_group(N, D, o) != HASTE_OK) return 0;
+    return haste::group_ws(N, D, o->G, o->beta);
+}
+
+int haste_group_labels(int64_t N, int64_t D, const int8_t *E, const haste_group_opts_t *o, int32_t *order,
+                       int32_t *gsize, int64_t *n_groups, int32_t *cluster, void *ws, size_t ws_bytes, void *stream) {
+    TRY(check_group(N, D, o));
+    TRY(need_ptr(E, "E"));
+    TRY(need_ptr(order, "order"));
+    TRY(need_ptr(gsize, "gsize"));
+    if (!n_groups) return fail(HASTE_ERR_INVALID, "n_groups is NULL");
+    if (cluster) TRY(need_ptr(cluster, "cluster"));
+    const size_t need = haste::group_ws(N, D, o->G, o->beta);
+    if (!ws || ws_bytes < need)
+        return fail(HASTE_ERR_WORKSPACE, "haste_group_labels needs %zu workspace bytes, got %zu", need, ws ? ws_bytes : 0);
+    TRY(need_ptr(ws, "ws"));
+    return hip_status(haste::group_labels(N, D, E, o->G, o->beta, o->iters, o->seed, order, gsize, n_groups, cluster,
+                                          ws, as_stream(stream)),
+                      "haste_group_labels");
+}
+
 int haste_bce_grad(int64_t B, int64_t N, int32_t dtype, const void *Y, const int32_t *pos, int32_t P, void *dY,
                    void *stream) {
     if (dtype != HASTE_DTYPE_F32 && dtype != HASTE_DTYPE_BF16) return fail(HASTE_ERR_INVALID, "bad dtype %d", dtype);

@@ -161,6 +161,11 @@ bool rewire_supported(const TailArgs &a);
 size_t rewire_ws(const TailArgs &a);
 hipError_t rewire(const TailArgs &a, int32_t *idx, void *W, float *m, int64_t n_prune, int init_random, uint64_t seed,
                   void *ws, hipStream_t s);
+// semantic grouping of labels (Alg. 2) on int8 unit embeddings
+bool group_supported(int64_t N, int64_t D, int64_t G);
+size_t group_ws(int64_t N, int64_t D, int64_t G, int64_t beta);
+hipError_t group_labels(int64_t N, int64_t D, const int8_t *E, int64_t G, int64_t beta, int64_t iters, uint64_t seed,
+                        int32_t *order, int32_t *gsize, int64_t *n_groups, int32_t *cluster, void *ws, hipStream_t s);
 // dY[b, n] = sigmoid(Y[b, n]) - T[b, n] elementwise (Y and dY may alias)
 hipError_t bce_grad(int64_t B, int64_t N, int32_t dtype, const void *Y, const int32_t *pos, int P, void *dY,
                     hipStream_t s);
