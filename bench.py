@@ -44,6 +44,7 @@ CALL_KERNELS = {
     "sgd": ["k_sgd_momentum"],
     "head_sgd": ["k_sgd_momentum"],
     "rewire": ["k_rw_"],
+    "grouping": ["k_gl_"],
     "bce": ["k_bce_grad"],
     "head_bce": ["k_bce_grad"],
     "bwd_w": ["k_transpose_x", "k_bwd_w"],
@@ -68,6 +69,7 @@ def parse():
     p.add_argument("--workload", default="l2949k_g32_h65k")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-bottleneck", action="store_true")
+    p.add_argument("--grouping", action="store_true", help="also time the label grouping of Alg. 2 (655K labels)")
     p.add_argument("--copy-calibration", action="store_true",
                    help="after the timed steps, run a plain %d-byte device copy (for counter calibration)" % COPY_BYTES)
     p.add_argument("--summarize-trace", metavar="DB",
@@ -113,7 +115,7 @@ def call_cost(wl, dt_bytes=2, n_pos=0):
 CALL_FILES = {
     "head_fwd": ["head.hip"], "head_bwd": ["head.hip", "util.hip"],
     "bce": ["util.hip"], "head_bce": ["util.hip"], "sgd": ["util.hip"], "head_sgd": ["util.hip"],
-    "rewire": ["rewire.hip"],
+    "rewire": ["rewire.hip"], "grouping": ["group.hip"],
 }
 
 
@@ -473,6 +475,34 @@ def main():
         out["rewire"] = {"ms": round(r_ms, 4), "rho": 0.1, "pruned_slots": n_r,
                          "what": "haste_rewire (Alg. 3) on the layer's supports and weights, random reinit"}
         del idx_r, W_r, ws_r
+    # grouping (Alg. 2), done once before training: the tail's labels as 768-dimensional int8 unit
+    # embeddings around planted directions (drawn on the device from a seeded generator), at the
+    # tail size of the 655K-label layer, bucket factor 16
+    if args.grouping:
+        gN, gD, gG, gbeta, giters = 655360, 768, 32, 16, 10
+        gen = torch.Generator(device=dev).manual_seed(17)
+        mu = torch.randn((4096, gD), device=dev, generator=gen)
+        lab = torch.randint(0, 4096, (gN,), device=dev, generator=gen)
+        Xg = mu[lab] / mu[lab].norm(dim=1, keepdim=True) + 0.3 / gD ** 0.5 * torch.randn((gN, gD), device=dev,
+                                                                                     generator=gen)
+        Eg = torch.round(127 * Xg / Xg.norm(dim=1, keepdim=True)).to(torch.int8)
+        del mu, lab, Xg
+        gopts = hs.group_opts(gG, gbeta, giters, 5)
+        g_order = torch.empty(gN, dtype=torch.int32, device=dev)
+        g_size = torch.empty(gN, dtype=torch.int32, device=dev)
+        g_n = torch.empty(1, dtype=torch.int64, device=dev)
+        ws_g = hs.workspace(hs.haste_group_workspace_bytes(gN, gD, gopts))
+        hs.haste_group_labels(Eg, gopts, g_order, g_size, g_n, None, ws_g)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        hs.haste_group_labels(Eg, gopts, g_order, g_size, g_n, None, ws_g)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        out["grouping"] = {"ms": round(e0.elapsed_time(e1), 3), "N": gN, "D": gD, "G": gG, "beta": gbeta,
+                           "iters": giters, "groups": int(g_n.item()),
+                           "what": "haste_group_labels (Alg. 2) on planted int8 unit embeddings"}
+        del Eg, g_order, g_size, ws_g
     if args.copy_calibration:
         src = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device=dev).fill_(1.0)
         dst = torch.empty_like(src)
