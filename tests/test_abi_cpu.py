@@ -118,3 +118,45 @@ def test_debug_gather_range_checked(hs):
     d = _desc(hs)
     assert hs.lib.haste_debug_gather(ctypes.byref(d), FAKE, FAKE, 7, 2, FAKE, None) == 1
     assert "group range" in hs.haste_last_error()
+
+
+def test_loss_optimizer_rewire_group_arguments_checked(hs):
+    """The entry points added beside the layer calls reject bad arguments before any launch."""
+    d = hs.make_desc(128, 768, 4096, 32, 64, hs.HASTE_DTYPE_BF16)
+    # loss gradient: negative P, dbias without dW, missing workspace
+    assert hs.lib.haste_fwd_bce(ctypes.byref(d), FAKE, FAKE, FAKE, None, FAKE, -1, FAKE, FAKE, None, 0, FAKE,
+                                1 << 30, None) == 1
+    assert hs.lib.haste_fwd_bce(ctypes.byref(d), FAKE, FAKE, FAKE, None, None, 0, FAKE, None, FAKE, 0, FAKE,
+                                1 << 30, None) == 1
+    assert "dbias needs dW" in hs.haste_last_error()
+    assert hs.lib.haste_fwd_bce(ctypes.byref(d), FAKE, FAKE, FAKE, None, None, 0, FAKE, FAKE, None, 0, None, 0,
+                                None) == 3
+    assert hs.lib.haste_bce_grad(4, 8, 9, FAKE, None, 0, FAKE, None) == 1
+    # optimizer: momentum outside [0, 1), W_next overlapping W
+    bad = hs.sgd_opts(0.1, 1.0)
+    assert hs.lib.haste_sgd_momentum(16, 1, FAKE, FAKE, FAKE, ctypes.byref(bad), FAKE, None) == 1
+    assert "momentum" in hs.haste_last_error()
+    ok = hs.sgd_opts(0.1, 0.9)
+    ws = hs.haste_workspace_bytes(d, hs.HASTE_OP_FWD_BCE_SGD)
+    assert ws > 0
+    assert hs.lib.haste_fwd_bce_sgd(ctypes.byref(d), FAKE, FAKE, FAKE, None, None, 0, FAKE, None, ctypes.byref(ok),
+                                    FAKE, FAKE + 64, FAKE, ws, None) == 1
+    assert "overlaps" in hs.haste_last_error()
+    # rewiring: rho outside [0, 1), init mode, width
+    ws_r = hs.haste_workspace_bytes(d, hs.HASTE_OP_REWIRE)
+    assert ws_r > 0
+    assert hs.lib.haste_rewire(ctypes.byref(d), FAKE, FAKE, None, 1.0, 1, 0, None, FAKE, ws_r, None) == 1
+    assert hs.lib.haste_rewire(ctypes.byref(d), FAKE, FAKE, None, 0.1, 2, 0, None, FAKE, ws_r, None) == 1
+    wide = hs.make_desc(8, 1024, 4096, 16, 256, hs.HASTE_DTYPE_BF16)
+    assert hs.lib.haste_rewire(ctypes.byref(wide), FAKE, FAKE, None, 0.1, 1, 0, None, FAKE, 1 << 30, None) == 2
+    # rho = 0 prunes nothing: no launch, no workspace needed
+    n = ctypes.c_int64(-1)
+    assert hs.lib.haste_rewire(ctypes.byref(d), FAKE, FAKE, None, 0.0, 1, 0, ctypes.byref(n), None, 0, None) == 0
+    assert n.value == 0
+    # grouping: dimensions must be a multiple of 16; G within 1 .. 256
+    g = hs.group_opts(32, 16, 5, 1)
+    assert hs.haste_group_workspace_bytes(1000, 100, g) == 0
+    assert hs.lib.haste_group_labels(1000, 100, FAKE, ctypes.byref(g), FAKE, FAKE, FAKE, None, FAKE, 1 << 30,
+                                     None) == 2
+    assert hs.haste_group_workspace_bytes(1000, 128, hs.group_opts(300, 16, 5, 1)) == 0
+    assert hs.haste_group_workspace_bytes(1000, 128, g) > 0
