@@ -25,6 +25,7 @@ import argparse
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -36,11 +37,12 @@ MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16 MFMA
 PROFILES = os.path.join(ROOT, "profiles")
 COPY_BYTES = 1 << 30            # plain device copy used to calibrate the HBM byte counters
 
-# kernels launched by each call (symbol prefixes in rocprofv3 output)
+# kernels launched by each call (patterns matched at the start of rocprofv3's kernel names; the
+# fused kernel's third template argument is its output: 1 stores dW, 2 applies the momentum step)
 CALL_KERNELS = {
     "fwd": ["k_fwd<"],
-    "fwd_bce": ["k_transpose_x", "k_fwd_bce"],
-    "fwd_bce_sgd": ["k_transpose_x", "k_fwd_bce"],
+    "fwd_bce": ["k_transpose_x", r"k_fwd_bce<\d+, \w+, 1,"],
+    "fwd_bce_sgd": ["k_transpose_x", r"k_fwd_bce<\d+, \w+, 2,"],
     "sgd": ["k_sgd_momentum"],
     "head_sgd": ["k_sgd_momentum"],
     "rewire": ["k_rw_"],
@@ -201,7 +203,7 @@ def summarize_traffic(fetch_db, write_db, workload, command):
     f_write = COPY_BYTES / max(write_d[ck]) if write_d.get(ck) else None
     calls = {}
     for call, prefixes in CALL_KERNELS.items():
-        ks = [k for k in fetch if any(k.startswith(p) for p in prefixes)]
+        ks = [k for k in fetch if any(re.match(p, k) for p in prefixes)]
         if not ks or f_write is None:
             continue
         # the tail's and the head's BCE gradient run one kernel: the tail's are its largest dispatches
