@@ -4,10 +4,11 @@ One step = one training pass of the layer on one batch of seeded synthetic input
 in HBM, with the upstream gradient formed from the step's own logits as the BCE gradient
 sigmoid(z) - y of the Section 3.3 objective (the workload's definition of dY):
   tail forward + BCE gradient + backward-weight, fused (haste_fwd_bce)
-  -> head forward (haste_head_fwd) -> head BCE gradient in place (haste_bce_grad)
+  -> head forward + BCE gradient, fused (haste_head_fwd_bce)
   -> tail backward-feature (haste_bwd_x) -> head backward (haste_head_bwd, adds its dX onto the tail's).
 Timed beside it, on the same inputs:
-  - the same training pass unfused: haste_fwd, haste_bce_grad, haste_bwd_w instead of haste_fwd_bce;
+  - the same training pass unfused: haste_fwd, haste_bce_grad, haste_bwd_w instead of haste_fwd_bce,
+    and haste_head_fwd + haste_bce_grad instead of haste_head_fwd_bce;
   - the training pass plus one SGD-with-momentum step on W and W_h, fused (haste_fwd_bce_sgd, dW
     never stored) and unfused (haste_bwd_w + haste_sgd_momentum);
   - the five separate calls on a fixed dY (haste_fwd, haste_head_fwd, haste_bwd_w, haste_bwd_x,
@@ -53,6 +54,8 @@ CALL_KERNELS = {
     "bwd_x": ["k_transpose_w", "k_bwd_x", "k_reduce_fmajor"],
     # the head's GEMM kernels by operand layout and epilogue (three tile sizes: 256, 128, fallback)
     "head_fwd": ["k_gemm4<true, true, 0>", "k_gemm2<true, true, 0>", "k_gemm_bf16<true, true, 0>"],
+    # the 256 kernel with the loss gradient in its epilogue (other shapes run head_fwd's kernels)
+    "head_fwd_bce": ["k_gemm4<true, true, 3>"],
     "head_bwd": ["k_gemm4<false, false, 1>", "k_gemm4<true, false, 2>", "k_gemm2<false, false, 1>",
                  "k_gemm2<true, false, 2>", "k_gemm_bf16<false, false, 1>", "k_gemm_bf16<true, false, 2>",
                  "k_reduce_rmajor"],
@@ -108,6 +111,7 @@ def call_cost(wl, dt_bytes=2, n_pos=0):
     if H:
         c["head_fwd"] = (X + Wh + Yh, head_flops)
         c["head_bce"] = (2 * Yh + pos, 0)
+        c["head_fwd_bce"] = (X + Wh + pos + Yh, head_flops)   # writes dY_h (Y_h's size)
         c["head_sgd"] = (2 * Wh + 3 * dWh, 0)
         c["head_bwd"] = (X + Wh + Yh + dWh + 2 * dX, 2 * head_flops)
     return c
@@ -115,7 +119,7 @@ def call_cost(wl, dt_bytes=2, n_pos=0):
 
 # source files of each call's kernels (the shared header is part of every call)
 CALL_FILES = {
-    "head_fwd": ["head.hip"], "head_bwd": ["head.hip", "util.hip"],
+    "head_fwd": ["head.hip"], "head_fwd_bce": ["head.hip"], "head_bwd": ["head.hip", "util.hip"],
     "bce": ["util.hip"], "head_bce": ["util.hip"], "sgd": ["util.hip"], "head_sgd": ["util.hip"],
     "rewire": ["rewire.hip"], "grouping": ["group.hip"],
 }
@@ -324,9 +328,14 @@ def main():
 
     stream = torch.cuda.current_stream()
 
-    def head_train():
+    def head_train(fused=True):
+        if not wl.H:
+            return []
+        if fused:
+            return [("head_fwd_bce", lambda: hs.haste_head_fwd_bce(wl.B, wl.F_s, wl.H, wl.dtype, Xd, Whd, None, posh,
+                                                                   dYht))]
         return [("head_fwd", lambda: hs.haste_head_fwd(wl.B, wl.F_s, wl.H, wl.dtype, Xd, Whd, None, Yh)),
-                ("head_bce", lambda: hs.haste_bce_grad(wl.B, wl.H, wl.dtype, Yh, posh, dYht))] if wl.H else []
+                ("head_bce", lambda: hs.haste_bce_grad(wl.B, wl.H, wl.dtype, Yh, posh, dYht))]
 
     def head_back(dyh):
         return [("head_bwd", lambda: hs.haste_head_bwd(wl.B, wl.F_s, wl.H, wl.dtype, Xd, Whd, dyh, dWh, dX, 1,
@@ -336,7 +345,7 @@ def main():
              head_train() + [("bwd_x", lambda: hs.haste_bwd_x(desc, idxd, Wd, dYt, dX, 0, ws_x))] +
              (head_back(dYht) if wl.H else []))
     unfused = ([("fwd", lambda: hs.haste_fwd(desc, Xd, idxd, Wd, None, Y)),
-                ("bce", lambda: hs.haste_bce_grad(wl.B, wl.L, wl.dtype, Y, posd, dYt))] + head_train() +
+                ("bce", lambda: hs.haste_bce_grad(wl.B, wl.L, wl.dtype, Y, posd, dYt))] + head_train(False) +
                [("bwd_w", lambda: hs.haste_bwd_w(desc, Xd, idxd, dYt, dW, None, 0, ws_w)),
                 ("bwd_x", lambda: hs.haste_bwd_x(desc, idxd, Wd, dYt, dX, 0, ws_x))] +
                (head_back(dYht) if wl.H else []))
@@ -432,14 +441,14 @@ def main():
         "per_call": detail(per_call),
         "roofline": roof,
         "unfused_training_step": {"ms": round(unf_ms, 4), "per_call": detail(unf_per),
-                                  "what": "haste_fwd + haste_bce_grad + haste_bwd_w in place of haste_fwd_bce"},
+                                  "what": "haste_fwd + haste_bce_grad + haste_bwd_w in place of haste_fwd_bce, haste_head_fwd + haste_bce_grad in place of haste_head_fwd_bce"},
         "training_step_with_optimizer": {
             "fused_ms": round(fo_ms, 4), "unfused_ms": round(uo_ms, 4),
             "fused_per_call_ms": {k: round(v, 4) for k, v in fo_per.items()},
             "unfused_per_call_ms": {k: round(v, 4) for k, v in uo_per.items()},
             "what": "the training pass plus one SGD-with-momentum step on W and W_h: fused, the tail's step runs "
-                    "inside haste_fwd_bce_sgd (dW never stored); unfused, haste_fwd + haste_bce_grad + haste_bwd_w "
-                    "+ haste_sgd_momentum"},
+                    "inside haste_fwd_bce_sgd (dW never stored) and the head's loss gradient inside "
+                    "haste_head_fwd_bce; unfused, the unfused training step + haste_sgd_momentum"},
         "separate_calls_step": {
             "ms": round(sep_ms, 4), "per_call": detail(sep_per),
             "step_alg_bytes": sum(cost[k][0] for k in sep_per),

@@ -239,6 +239,23 @@ int haste_head_fwd(int64_t B, int64_t F_s, int64_t H, int32_t dtype, const void 
                    const void *W_head, const float *bias_h, void *Y_h, void *stream);
 
 /*
+ * Dense head forward fused with the gradient of the binary cross-entropy objective (Section 3.3,
+ * head branch):
+ *   dY_h[b, h] = sigmoid(bias_h[h] + sum_f X[b, f] * W_head[h, f]) - T[b, h]
+ * with T from pos[B, P] as in haste_bce_grad (ids in [0, H); -1 padding and repeats allowed).
+ * The logits are not stored.  On bf16 layers whose pointers are 16-byte aligned and whose F_s
+ * and H are multiples of 8 the sigmoid is taken of the fp32 logit inside the GEMM's epilogue and
+ * sigmoid - T is rounded once to bf16; otherwise the logits are written into dY_h (rounded to
+ * dtype) and the gradient is formed there in place, as haste_head_fwd + haste_bce_grad would.
+ * X[B, F_s], W_head[H, F_s] (dtype), bias_h[H] fp32 (16-byte aligned) or NULL, dY_h[B, H] (dtype)
+ * overwritten.  Errors: HASTE_ERR_INVALID for a bad dtype, negative sizes or P, a NULL pointer
+ * that is needed, or an unaligned bias_h; nothing is launched then.
+ */
+int haste_head_fwd_bce(int64_t B, int64_t F_s, int64_t H, int32_t dtype, const void *X,
+                       const void *W_head, const float *bias_h, const int32_t *pos, int32_t P,
+                       void *dY_h, void *stream);
+
+/*
  * Dense head backward (Section 3.3 objective, head branch):
  *   dW_h[h, f] = sum_b dY_h[b, h] * X[b, f]                        (overwritten, fp32)
  *   dX[b, f]   = beta_dx * dX[b, f] + sum_h dY_h[b, h] * W_head[h, f]

@@ -60,6 +60,7 @@ def _load() -> ctypes.CDLL:
         "haste_rewire": [D, P, P, P, ctypes.c_double, I32, ctypes.c_uint64, P, P, SZ, P],
         "haste_group_labels": [I64, I64, P, ctypes.POINTER(haste_group_opts_t), P, P, P, P, P, SZ, P],
         "haste_head_fwd": [I64, I64, I64, I32, P, P, P, P, P],
+        "haste_head_fwd_bce": [I64, I64, I64, I32, P, P, P, P, I32, P, P],
         "haste_head_bwd": [I64, I64, I64, I32, P, P, P, P, P, ctypes.c_int, P, SZ, P],
         "haste_validate_idx": [D, P, P, P],
         "haste_debug_gather": [D, P, P, I64, I64, P, P],
@@ -84,8 +85,8 @@ lib = _load()
 
 # every symbol the header declares
 EXPORTS = ("haste_fwd", "haste_bwd_w", "haste_bwd_x", "haste_fwd_bce", "haste_fwd_bce_sgd", "haste_sgd_momentum",
-           "haste_rewire", "haste_group_labels", "haste_group_workspace_bytes", "haste_bce_grad", "haste_head_fwd", "haste_head_bwd", "haste_workspace_bytes",
-           "haste_head_workspace_bytes", "haste_validate_idx", "haste_debug_gather", "haste_status_str",
+           "haste_rewire", "haste_group_labels", "haste_group_workspace_bytes", "haste_bce_grad", "haste_head_fwd",
+           "haste_head_fwd_bce", "haste_head_bwd", "haste_workspace_bytes", "haste_head_workspace_bytes", "haste_validate_idx", "haste_debug_gather", "haste_status_str",
            "haste_last_error", "haste_version")
 
 
@@ -230,6 +231,11 @@ def haste_bce_grad(B, N, dtype, Y, pos, dY, stream=None):
 
 def haste_head_fwd(B, F_s, H, dtype, X, W_head, bias_h, Y_h, stream=None):
     _check(lib.haste_head_fwd(B, F_s, H, dtype, _ptr(X), _ptr(W_head), _ptr(bias_h), _ptr(Y_h), _stream(stream)))
+
+
+def haste_head_fwd_bce(B, F_s, H, dtype, X, W_head, bias_h, pos, dY_h, stream=None):
+    _check(lib.haste_head_fwd_bce(B, F_s, H, dtype, _ptr(X), _ptr(W_head), _ptr(bias_h), _ptr(pos), _npos(pos),
+                                  _ptr(dY_h), _stream(stream)))
 
 
 def haste_head_bwd(B, F_s, H, dtype, X, W_head, dY_h, dW_h, dX, beta_dx=0, ws=None, stream=None):

@@ -384,6 +384,22 @@ int haste_head_fwd(int64_t B, int64_t F_s, int64_t H, int32_t dtype, const void 
     return hip_status(haste::head_fwd(B, F_s, H, dtype, X, W_head, bias_h, Y_h, as_stream(stream)), "haste_head_fwd");
 }
 
+int haste_head_fwd_bce(int64_t B, int64_t F_s, int64_t H, int32_t dtype, const void *X, const void *W_head,
+                       const float *bias_h, const int32_t *pos, int32_t P, void *dY_h, void *stream) {
+    TRY(check_head(B, F_s, H, dtype));
+    if (P < 0) return fail(HASTE_ERR_INVALID, "P must be >= 0");
+    if (B == 0 || H == 0) return ok();
+    TRY(need_ptr(X, "X"));
+    TRY(need_ptr(W_head, "W_head"));
+    TRY(need_ptr(dY_h, "dY_h"));
+    if (P > 0) TRY(need_ptr(pos, "pos"));
+    if (bias_h && !aligned16(bias_h)) return fail(HASTE_ERR_INVALID, "bias_h is not 16-byte aligned");
+    if (B * haste::cdiv(H, 2048) >= ((int64_t)1 << 31)) return fail(HASTE_ERR_UNSUPPORTED, "B * H too large");
+    return hip_status(haste::head_fwd_bce(B, F_s, H, dtype, X, W_head, bias_h, P > 0 ? pos : nullptr, P, dY_h,
+                                          as_stream(stream)),
+                      "haste_head_fwd_bce");
+}
+
 int haste_head_bwd(int64_t B, int64_t F_s, int64_t H, int32_t dtype, const void *X, const void *W_head,
                    const void *dY_h, float *dW_h, float *dX, int beta_dx, void *ws, size_t ws_bytes, void *stream) {
     TRY(check_head(B, F_s, H, dtype));

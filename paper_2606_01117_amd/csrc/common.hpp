@@ -184,6 +184,9 @@ hipError_t bwd_x_valu(const TailArgs &a, const int32_t *idx, const void *W, cons
 size_t head_ws(int64_t B, int64_t F_s, int64_t H, int32_t dtype);
 hipError_t head_fwd(int64_t B, int64_t F_s, int64_t H, int32_t dtype, const void *X, const void *Wh,
                     const float *bias_h, void *Yh, hipStream_t s);
+// dY_h = sigmoid(X W_head^T + bias_h) - T (T from pos[B, P] as in bce_grad)
+hipError_t head_fwd_bce(int64_t B, int64_t F_s, int64_t H, int32_t dtype, const void *X, const void *Wh,
+                        const float *bias_h, const int32_t *pos, int P, void *dYh, hipStream_t s);
 hipError_t head_bwd(int64_t B, int64_t F_s, int64_t H, int32_t dtype, const void *X, const void *Wh,
                     const void *dYh, float *dWh, float *dX, int beta_dx, void *ws, hipStream_t s);
 

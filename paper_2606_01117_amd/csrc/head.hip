@@ -15,7 +15,8 @@
 
 namespace {
 
-enum { EPI_BF16_BIAS = 0, EPI_F32 = 1, EPI_F32_PART = 2 };
+// EPI_BF16_BCE: the loss gradient sigmoid(logit) - T of the bias-added logits, in bf16 (256 kernel)
+enum { EPI_BF16_BIAS = 0, EPI_F32 = 1, EPI_F32_PART = 2, EPI_BF16_BCE = 3 };
 
 constexpr int TM = 128, TN = 128, TK = 32;
 constexpr int LS = TK + 8;  // LDS row stride (bf16): 80 bytes keeps 16-byte rows aligned
@@ -309,7 +310,10 @@ struct G4Operand {
     int64_t klim;       // end of this workgroup's K range
     __device__ __forceinline__ void issue(int64_t k0, uint32_t lds_stage, int wave, int lane) const {
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
+        for (int t = 0; t < 4; ++t) issue1(k0, lds_stage, wave, lane, t);
+    }
+    __device__ __forceinline__ void issue1(int64_t k0, uint32_t lds_stage, int wave, int lane, int t) const {
+        {
             const int i = 4 * wave + t;
             uint32_t off;
             if (KC) {
@@ -348,7 +352,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm4(const bf16_t *__restrict__ A, 
                                                   const bf16_t *__restrict__ Bm, int64_t sb, uint32_t b_bytes,
                                                   void *__restrict__ C, int64_t ldc, const float *__restrict__ bias,
                                                   int64_t M, int64_t N, int64_t K, int64_t kchunk, int MT, int NT,
-                                                  int Z) {
+                                                  int Z, const int32_t *__restrict__ pos, int P) {
     extern __shared__ __align__(16) char g4s[];   // [stage][A tile, B tile]
     // tile order: the workgroups that share an operand tile run on one XCD back to back
     const int w = blockIdx.x, xcd = w % kXcds, local = w / kXcds;
@@ -403,8 +407,11 @@ __global__ __launch_bounds__(256, 1) void k_gemm4(const bf16_t *__restrict__ A, 
     };
     // Software pipeline over K steps of two 16-deep halves (h0, h1).  Iteration j: read h1 of step
     // j while h0's products run; wait for step j + 1 and barrier (stage j % 4 is then fully read
-    // into registers by every wave); refill stage j % 4 with step j + 4; read h0 of step j + 1
-    // while h1's products run.  Steps past the end are loaded out of range into stages that are
+    // into registers by every wave); then h1's 16 products, with the 8 loads that refill stage
+    // j % 4 with step j + 4 between the first 8 and the reads of h0 of step j + 1 between the
+    // last 8.  Issued as one burst after the barrier, the four waves' 32 loads queue at the
+    // texture unit and hold up the products behind them; spread out, they overlap (12% on the
+    // head's three products).  Steps past the end are loaded out of range into stages that are
     // never read.
 #pragma unroll
     for (int s = 0; s < G4S; ++s) {
@@ -423,21 +430,70 @@ __global__ __launch_bounds__(256, 1) void k_gemm4(const bf16_t *__restrict__ A, 
         __builtin_amdgcn_sched_barrier(0);
         wait_vmcnt<8 * (G4S - 2)>();   // this wave's loads of step j + 1 have landed
         __syncthreads();               // everyone's have; stage j % 4 is read out
-        oa.issue(kb + (int64_t)(j + G4S) * G4K, stA(st), wave, lane);
-        ob.issue(kb + (int64_t)(j + G4S) * G4K, stB(st), wave, lane);
-        frags((j + 1) % G4S, 0, a0, b0);   // past the last step: never used
-        __builtin_amdgcn_sched_barrier(0);
-        products(a1, b1);
-        __builtin_amdgcn_sched_barrier(0);
+        const char *ta = g4s + ((j + 1) % G4S) * 2 * G4OP * 2, *tb = ta + G4OP * 2;
+        const int64_t kn = kb + (int64_t)(j + G4S) * G4K;
+#pragma unroll
+        for (int s = 0; s < 16; ++s) {
+            const int jn = s >> 2, i = s & 3;
+            acc[jn][i] = mfma32x32x16(as_bf16x8(b1[jn]), as_bf16x8(a1[i]), acc[jn][i]);
+            if (s < 4) oa.issue1(kn, stA(st), wave, lane, s);
+            else if (s < 8) ob.issue1(kn, stB(st), wave, lane, s - 4);
+            else if (s < 12) a0[s - 8] = oa.frag(ta, wm * 128 + (s - 8) * 32, 0, lane);   // past the last
+            else b0[s - 12] = ob.frag(tb, wn * 128 + (s - 12) * 32, 0, lane);               // step: unused
+            __builtin_amdgcn_sched_barrier(0);
+        }
     }
     wait_vmcnt<0>();   // no load may still be writing LDS
     __syncthreads();   // and no wave still reads a stage: the LDS now stages the output
+
+    // Loss gradient (EPI_BF16_BCE): the tile's targets as a bitmap [256 rows][8 words] behind the
+    // staged half-tile (ids outside [n0, n0 + 256) or [0, N) ignored, repeats set the same bit),
+    // and the sigmoid of every bias-added logit in registers, in all four waves at once.
+    uint32_t *tbits = reinterpret_cast<uint32_t *>(g4s + 128 * G4T * 2);
+    if constexpr (EPI == EPI_BF16_BCE) {
+        for (int e = threadIdx.x; e < G4T * 8; e += 256) tbits[e] = 0u;
+        __syncthreads();
+        // one row per thread; its ids 8 at a time, all 8 loads in flight before any is used
+        const int r = threadIdx.x;
+        const bool live = m0 + r < M;
+        const int32_t *pr = pos + (live ? (m0 + r) * P : 0);
+        for (int p0 = 0; p0 < P; p0 += 8) {
+            int id[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) id[u] = live && p0 + u < P ? pr[p0 + u] : -1;
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+                if (id[u] >= n0 && id[u] < n0 + G4T && id[u] < N) {
+                    const int c = (int)(id[u] - n0);
+                    atomicOr(&tbits[r * 8 + (c >> 5)], 1u << (c & 31));
+                }
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int nl = wn * 128 + j * 32 + 8 * r + 4 * hh;
+                float4 b = make_float4(0.f, 0.f, 0.f, 0.f);
+                if (bias && n0 + nl < N) b = *reinterpret_cast<const float4 *>(bias + n0 + nl);   // 16-byte aligned
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    f32x16_t &d = acc[j][i];
+                    d[4 * r + 0] = sigmoid_f32(d[4 * r + 0] + b.x);
+                    d[4 * r + 1] = sigmoid_f32(d[4 * r + 1] + b.y);
+                    d[4 * r + 2] = sigmoid_f32(d[4 * r + 2] + b.z);
+                    d[4 * r + 3] = sigmoid_f32(d[4 * r + 3] + b.w);
+                }
+                __builtin_amdgcn_sched_barrier(0);   // one block of registers at a time
+            }
+        __syncthreads();   // the bitmap is complete
+    }
 
     // Output: one 128-row half of the tile at a time goes through LDS as [128 rows][256 columns]
     // (16-byte chunk c of row r at c ^ (r % 32): the 32 rows one store-to-LDS instruction touches
     // fall in distinct banks), then leaves as whole row pieces of 512 B (bf16) or 1 KB (fp32),
     // 1 KB per store instruction.
-    constexpr int OB = EPI == EPI_BF16_BIAS ? 2 : 4;    // output bytes per element
+    constexpr bool BF = EPI == EPI_BF16_BIAS || EPI == EPI_BF16_BCE;   // bf16 output
+    constexpr int OB = BF ? 2 : 4;                      // output bytes per element
     constexpr int RB = G4T * OB;                        // bytes per staged row
     constexpr int RPI = 1024 / RB;                      // rows per store instruction
     char *eb = g4s;
@@ -462,9 +518,16 @@ __global__ __launch_bounds__(256, 1) void k_gemm4(const bf16_t *__restrict__ A, 
                         const int ml = i * 32 + ln;
                         const f32x16_t &d = acc[j][i];
                         char *p = eb + ml * RB + ((((byte >> 4) ^ (ml & 31)) << 4) | (byte & 15));
-                        const float4 v = make_float4(d[4 * r + 0] + b.x, d[4 * r + 1] + b.y, d[4 * r + 2] + b.z,
-                                                     d[4 * r + 3] + b.w);
-                        if (EPI == EPI_BF16_BIAS)
+                        float4 v = make_float4(d[4 * r + 0] + b.x, d[4 * r + 1] + b.y, d[4 * r + 2] + b.z,
+                                               d[4 * r + 3] + b.w);
+                        if constexpr (EPI == EPI_BF16_BCE) {   // minus the targets of these 4 columns
+                            const uint32_t tb = tbits[(128 * h + ml) * 8 + (nl >> 5)] >> (nl & 31);
+                            v.x -= (float)(tb & 1u);
+                            v.y -= (float)((tb >> 1) & 1u);
+                            v.z -= (float)((tb >> 2) & 1u);
+                            v.w -= (float)((tb >> 3) & 1u);
+                        }
+                        if (BF)
                             *reinterpret_cast<uint2 *>(p) = make_uint2(pack_bf16(v.x, v.y), pack_bf16(v.z, v.w));
                         else
                             *reinterpret_cast<float4 *>(p) = v;
@@ -492,7 +555,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm4(const bf16_t *__restrict__ A, 
                 if (m < M && n < N) {
                     // outputs written once and not read again soon: streaming stores
                     const u32x4_t w = __builtin_bit_cast(u32x4_t, v[t]);
-                    if (EPI == EPI_BF16_BIAS)
+                    if (BF)
                         __builtin_nontemporal_store(w, reinterpret_cast<u32x4_t *>(Cb + m * ldo + n));
                     else if (EPI == EPI_F32)
                         __builtin_nontemporal_store(w, reinterpret_cast<u32x4_t *>(Cf + m * ldo + n));
@@ -594,7 +657,7 @@ bool gemm4_ok(int64_t B, int64_t F_s, int64_t H, std::initializer_list<const voi
 template <bool AK, bool BK, int EPI>
 hipError_t launch_gemm4(hipStream_t s, const bf16_t *A, int64_t sa, int64_t a_elems, const bf16_t *Bm, int64_t sb,
                         int64_t b_elems, void *C, int64_t ldc, const float *bias, int64_t M, int64_t N, int64_t K,
-                        int64_t kchunk, int Z) {
+                        int64_t kchunk, int Z, const int32_t *pos = nullptr, int P = 0) {
     const int MT = (int)haste::cdiv(M, G4T), NT = (int)haste::cdiv(N, G4T);
     const int64_t grid = Z > 1 ? haste::round_up(Z, kXcds) * MT * NT
                                : (MT <= NT ? haste::round_up(NT, kXcds) * MT : haste::round_up(MT, kXcds) * NT);
@@ -603,7 +666,7 @@ hipError_t launch_gemm4(hipStream_t s, const bf16_t *A, int64_t sa, int64_t a_el
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)kG4Lds);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(256), kG4Lds, s, A, sa, (uint32_t)(a_elems * 2), Bm, sb,
-                       (uint32_t)(b_elems * 2), C, ldc, bias, M, N, K, kchunk, MT, NT, Z);
+                       (uint32_t)(b_elems * 2), C, ldc, bias, M, N, K, kchunk, MT, NT, Z, pos, P);
     return hipGetLastError();
 }
 
@@ -650,6 +713,19 @@ hipError_t head_fwd(int64_t B, int64_t F_s, int64_t H, int32_t dtype, const void
                            (const float *)Wh, (int64_t)1, F_s, Yh, H, bias_h, B, H, F_s, F_s);
     }
     return hipGetLastError();
+}
+
+// dY_h = sigmoid(X W_head^T + bias_h) - T: the 256 kernel with the loss gradient in its epilogue
+// where it applies (the logits never reach memory), else the logits into dY_h and the gradient in
+// place
+hipError_t head_fwd_bce(int64_t B, int64_t F_s, int64_t H, int32_t dtype, const void *X, const void *Wh,
+                        const float *bias_h, const int32_t *pos, int P, void *dYh, hipStream_t s) {
+    if (dtype == HASTE_DTYPE_BF16 && gemm4_ok(B, F_s, H, {X, Wh, dYh, bias_h}))
+        return launch_gemm4<true, true, EPI_BF16_BCE>(s, (const bf16_t *)X, F_s, B * F_s, (const bf16_t *)Wh, F_s,
+                                                      H * F_s, dYh, H, bias_h, B, H, F_s, F_s, 1, pos, P);
+    const hipError_t e = head_fwd(B, F_s, H, dtype, X, Wh, bias_h, dYh, s);
+    if (e != hipSuccess) return e;
+    return bce_grad(B, H, dtype, dYh, pos, P, dYh, s);
 }
 
 hipError_t head_bwd(int64_t B, int64_t F_s, int64_t H, int32_t dtype, const void *X, const void *Wh,

@@ -132,6 +132,12 @@ def test_loss_optimizer_rewire_group_arguments_checked(hs):
     assert hs.lib.haste_fwd_bce(ctypes.byref(d), FAKE, FAKE, FAKE, None, None, 0, FAKE, FAKE, None, 0, None, 0,
                                 None) == 3
     assert hs.lib.haste_bce_grad(4, 8, 9, FAKE, None, 0, FAKE, None) == 1
+    # head forward with the loss gradient: negative P, positives named but missing, unaligned bias
+    assert hs.lib.haste_head_fwd_bce(4, 768, 1024, 1, FAKE, FAKE, None, FAKE, -1, FAKE, None) == 1
+    assert hs.lib.haste_head_fwd_bce(4, 768, 1024, 1, FAKE, FAKE, None, None, 3, FAKE, None) == 1
+    assert "pos" in hs.haste_last_error()
+    assert hs.lib.haste_head_fwd_bce(4, 768, 1024, 1, FAKE, FAKE, FAKE + 4, None, 0, FAKE, None) == 1
+    assert hs.lib.haste_head_fwd_bce(0, 768, 1024, 1, None, None, None, None, 0, None, None) == 0
     # optimizer: momentum outside [0, 1), W_next overlapping W
     bad = hs.sgd_opts(0.1, 1.0)
     assert hs.lib.haste_sgd_momentum(16, 1, FAKE, FAKE, FAKE, ctypes.byref(bad), FAKE, None) == 1

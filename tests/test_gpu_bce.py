@@ -192,3 +192,67 @@ def test_fwd_bce_large_sampled(hs, orc, name):
     hs.haste_bwd_w(desc, Xd, idxd, dY, dW2, None, 0, hs.workspace(hs.haste_workspace_bytes(desc, hs.HASTE_OP_BWD_W)))
     _sync()
     assert bool((dW2 == dW).all()), "fused dW differs from haste_bwd_w on its dY"
+
+
+# ------------------------------------------------------------------------------------------
+# dense head forward fused with the loss gradient
+# ------------------------------------------------------------------------------------------
+HEAD_BCE = [
+    # B, F_s, H, dtype, P, bias   (the GEMM epilogue forms the gradient where the 256-tile kernel
+    # runs: bf16, F_s and H multiples of 8; the other cases compose the forward and haste_bce_grad)
+    (33, 200, 304, BF16, 6, True),
+    (256, 768, 1024, BF16, 8, False),
+    (300, 520, 2056, BF16, 64, True),
+    (1, 64, 24, BF16, 3, False),
+    (64, 256, 512, BF16, 0, True),
+    (130, 768, 4100, BF16, 5, True),
+    (33, 200, 300, F32, 6, True),
+]
+
+
+@pytest.mark.parametrize("case", HEAD_BCE, ids=[f"B{c[0]}_F{c[1]}_H{c[2]}_{'bf16' if c[3] else 'f32'}_P{c[4]}"
+                                                for c in HEAD_BCE])
+def test_head_fwd_bce(hs, orc, case):
+    B, F_s, H, dt, P, with_bias = case
+    say(f"[head_fwd_bce] B={B} F_s={F_s} H={H} dtype={dt} P={P}")
+    wl = synth.small("head_bce", B=B, F_s=F_s, L=0, G=1, F_in=1, H=H, dtype=dt, wid=700 + HEAD_BCE.index(case))
+    X, Wh = synth.draw_X(wl), synth.draw_W_head(wl)
+    rng = np.random.default_rng(wl.wid)
+    bh = rng.standard_normal(H).astype(np.float32) if with_bias else None
+    pos = rand_pos(rng, B, H, P)
+    dY = out_tensor((B, H), dt)
+    hs.haste_head_fwd_bce(B, F_s, H, dt, to_dev(X), to_dev(Wh), to_dev(bh), to_dev(pos) if P else None, dY)
+    _sync()
+    got = host_f32(dY, dt)
+    _check("head dY", got, orc.bce_grad(orc.head_fwd(X, Wh, bh, dt), pos), dt)
+    T = targets(pos, B, H)
+    assert np.array_equal(got < 0, T) and np.all(got[~T] > 0), "targets are not applied exactly where pos names them"
+
+
+def test_head_fwd_bce_large_sampled(hs, orc):
+    """The 65,536-label head of the 3M-label layer (B = 512), its own positives; column slices
+    at both ends and across a tile edge against the oracle."""
+    wl = synth.WORKLOADS["l2949k_g32_h65k"]
+    say(f"[head_fwd_bce workload] {wl.name}")
+    X, Wh = synth.draw_X(wl), synth.draw_W_head(wl)
+    rng = np.random.default_rng(17)
+    pos = rand_pos(rng, wl.B, wl.H, 8)
+    pos[:, 0] = rng.integers(0, 300, wl.B)             # frequent labels first, as the head's are
+    dY = out_tensor((wl.B, wl.H), wl.dtype)
+    hs.haste_head_fwd_bce(wl.B, wl.F_s, wl.H, wl.dtype, to_dev(X), to_dev(Wh), None, to_dev(pos), dY)
+    _sync()
+    got = host_f32(dY, wl.dtype)
+    T = targets(pos, wl.B, wl.H)
+    assert np.array_equal(got < 0, T), "targets are not applied exactly where pos names them"
+    for h0, h1 in [(0, 400), (32640, 33024), (wl.H - 300, wl.H)]:
+        ref = orc.bce_grad(orc.head_fwd(X, Wh, None, wl.dtype, h0, h1), pos - h0)
+        _check(f"[{h0},{h1})", got[:, h0:h1], ref, wl.dtype)
+
+
+def test_head_fwd_bce_errors(hs):
+    import torch
+    dummy = torch.zeros(16, dtype=torch.int32, device="cuda")
+    hs.haste_head_fwd_bce(0, 768, 1024, BF16, dummy, dummy, None, None, dummy)   # B = 0: nothing to do
+    with pytest.raises(hs.HasteError):   # positives named but missing
+        hs._check(hs.lib.haste_head_fwd_bce(4, 768, 1024, BF16, hs._ptr(dummy), hs._ptr(dummy), None, None, 3,
+                                            hs._ptr(dummy), None))
