@@ -447,8 +447,8 @@ __global__ __launch_bounds__(256, 1) void k_gemm4(const bf16_t *__restrict__ A, 
     __syncthreads();   // and no wave still reads a stage: the LDS now stages the output
 
     // Loss gradient (EPI_BF16_BCE): the tile's targets as a bitmap [256 rows][8 words] behind the
-    // staged half-tile (ids outside [n0, n0 + 256) or [0, N) ignored, repeats set the same bit),
-    // and the sigmoid of every bias-added logit in registers, in all four waves at once.
+    // staged half-tile (ids outside [n0, n0 + 256) or [0, N) ignored, repeats set the same bit);
+    // the sigmoid is taken while staging.
     uint32_t *tbits = reinterpret_cast<uint32_t *>(g4s + 128 * G4T * 2);
     if constexpr (EPI == EPI_BF16_BCE) {
         for (int e = threadIdx.x; e < G4T * 8; e += 256) tbits[e] = 0u;
@@ -468,23 +468,6 @@ __global__ __launch_bounds__(256, 1) void k_gemm4(const bf16_t *__restrict__ A, 
                     atomicOr(&tbits[r * 8 + (c >> 5)], 1u << (c & 31));
                 }
         }
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int nl = wn * 128 + j * 32 + 8 * r + 4 * hh;
-                float4 b = make_float4(0.f, 0.f, 0.f, 0.f);
-                if (bias && n0 + nl < N) b = *reinterpret_cast<const float4 *>(bias + n0 + nl);   // 16-byte aligned
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    f32x16_t &d = acc[j][i];
-                    d[4 * r + 0] = sigmoid_f32(d[4 * r + 0] + b.x);
-                    d[4 * r + 1] = sigmoid_f32(d[4 * r + 1] + b.y);
-                    d[4 * r + 2] = sigmoid_f32(d[4 * r + 2] + b.z);
-                    d[4 * r + 3] = sigmoid_f32(d[4 * r + 3] + b.w);
-                }
-                __builtin_amdgcn_sched_barrier(0);   // one block of registers at a time
-            }
         __syncthreads();   // the bitmap is complete
     }
 
@@ -510,7 +493,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm4(const bf16_t *__restrict__ A, 
                 for (int r = 0; r < 4; ++r) {
                     const int nl = wn * 128 + j * 32 + 8 * r + 4 * hh;
                     float4 b = make_float4(0.f, 0.f, 0.f, 0.f);
-                    if (EPI == EPI_BF16_BIAS && bias && n0 + nl < N)
+                    if (BF && bias && n0 + nl < N)
                         b = *reinterpret_cast<const float4 *>(bias + n0 + nl);   // 16-byte aligned
                     const int byte = nl * OB;
 #pragma unroll
@@ -520,8 +503,9 @@ __global__ __launch_bounds__(256, 1) void k_gemm4(const bf16_t *__restrict__ A, 
                         char *p = eb + ml * RB + ((((byte >> 4) ^ (ml & 31)) << 4) | (byte & 15));
                         float4 v = make_float4(d[4 * r + 0] + b.x, d[4 * r + 1] + b.y, d[4 * r + 2] + b.z,
                                                d[4 * r + 3] + b.w);
-                        if constexpr (EPI == EPI_BF16_BCE) {   // minus the targets of these 4 columns
+                        if constexpr (EPI == EPI_BF16_BCE) {   // sigmoid, minus the targets of these 4 columns
                             const uint32_t tb = tbits[(128 * h + ml) * 8 + (nl >> 5)] >> (nl & 31);
+                            v = make_float4(sigmoid_f32(v.x), sigmoid_f32(v.y), sigmoid_f32(v.z), sigmoid_f32(v.w));
                             v.x -= (float)(tb & 1u);
                             v.y -= (float)((tb >> 1) & 1u);
                             v.z -= (float)((tb >> 2) & 1u);
