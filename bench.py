@@ -3,9 +3,10 @@
 One step = one training pass of the layer on one batch of seeded synthetic input already resident
 in HBM, with the upstream gradient formed from the step's own logits as the BCE gradient
 sigmoid(z) - y of the Section 3.3 objective (the workload's definition of dY):
-  tail forward + BCE gradient + backward-weight, fused (haste_fwd_bce)
+  the tail's pass in one call (haste_tail_step): forward + BCE gradient + backward-weight, fused,
+  then backward-feature on the transposed weights the fused kernel wrote
   -> head forward + BCE gradient, fused (haste_head_fwd_bce)
-  -> tail backward-feature (haste_bwd_x) -> head backward (haste_head_bwd, adds its dX onto the tail's).
+  -> head backward (haste_head_bwd, adds its dX onto the tail's).
 Timed beside it, on the same inputs:
   - the same training pass unfused: haste_fwd, haste_bce_grad, haste_bwd_w instead of haste_fwd_bce,
     and haste_head_fwd + haste_bce_grad instead of haste_head_fwd_bce;
@@ -44,6 +45,7 @@ CALL_KERNELS = {
     "fwd": ["k_fwd<"],
     "fwd_bce": ["k_transpose_x", r"k_fwd_bce<\d+, \w+, 1,"],
     "fwd_bce_sgd": ["k_transpose_x", r"k_fwd_bce<\d+, \w+, 2,"],
+    "tail_step": ["k_transpose_x", r"k_fwd_bce<\d+, \w+, 1,", "k_bwd_x", "k_reduce_fmajor"],
     "sgd": ["k_sgd_momentum"],
     "head_sgd": ["k_sgd_momentum"],
     "rewire": ["k_rw_"],
@@ -108,6 +110,7 @@ def call_cost(wl, dt_bytes=2, n_pos=0):
         "bwd_w": (X + idx + Y + dW, tail_flops),
         "bwd_x": (idx + W + Y + dX, tail_flops),
     }
+    c["tail_step"] = (c["fwd_bce"][0] + c["bwd_x"][0], c["fwd_bce"][1] + c["bwd_x"][1])   # both passes' operands
     if H:
         c["head_fwd"] = (X + Wh + Yh, head_flops)
         c["head_bce"] = (2 * Yh + pos, 0)
@@ -320,7 +323,7 @@ def main():
     n_pos = pos.shape[1]
     posd = up(synth.pos_matrix(tail_pairs, wl.B, n_pos))
     dYt = torch.empty((wl.B, wl.L), dtype=odt, device=dev)   # the training step's own dY
-    ws_f = hs.workspace(hs.haste_workspace_bytes(desc, hs.HASTE_OP_FWD_BCE))
+    ws_t = hs.workspace(hs.haste_workspace_bytes(desc, hs.HASTE_OP_TAIL_STEP))
     if wl.H:
         posh = up(synth.pos_matrix(head_pairs, wl.B, n_pos))
         dYht = torch.empty((wl.B, wl.H), dtype=odt, device=dev)
@@ -341,9 +344,9 @@ def main():
         return [("head_bwd", lambda: hs.haste_head_bwd(wl.B, wl.F_s, wl.H, wl.dtype, Xd, Whd, dyh, dWh, dX, 1,
                                                        ws_h))] if wl.H else []
 
-    fused = ([("fwd_bce", lambda: hs.haste_fwd_bce(desc, Xd, idxd, Wd, None, posd, dYt, dW, None, 0, ws_f))] +
-             head_train() + [("bwd_x", lambda: hs.haste_bwd_x(desc, idxd, Wd, dYt, dX, 0, ws_x))] +
-             (head_back(dYht) if wl.H else []))
+    fused = ([("tail_step", lambda: hs.haste_tail_step(desc, Xd, idxd, Wd, None, posd, dYt, dW, None, 0, dX, 0,
+                                                        ws_t))] +
+             head_train() + (head_back(dYht) if wl.H else []))
     unfused = ([("fwd", lambda: hs.haste_fwd(desc, Xd, idxd, Wd, None, Y)),
                 ("bce", lambda: hs.haste_bce_grad(wl.B, wl.L, wl.dtype, Y, posd, dYt))] + head_train(False) +
                [("bwd_w", lambda: hs.haste_bwd_w(desc, Xd, idxd, dYt, dW, None, 0, ws_w)),
@@ -458,7 +461,7 @@ def main():
 
     if not args.no_bottleneck and is_bf:
         out["dense_bottleneck"] = bottleneck(wl, Xd, Wd, dYd, args)
-        out["tail_vs_bottleneck"] = round(sum(per_call[k] for k in ("fwd_bce", "bwd_x")) /
+        out["tail_vs_bottleneck"] = round(sum(per_call[k] for k in ("tail_step", "fwd_bce", "bwd_x") if k in per_call) /
                                           out["dense_bottleneck"]["ms"], 3)
         out["separate_calls_step"]["tail_vs_bottleneck"] = round(
             sum(sep_per[k] for k in ("fwd", "bwd_w", "bwd_x")) / out["dense_bottleneck"]["ms"], 3)

@@ -51,7 +51,7 @@ enum haste_status {
 /* Workspace-query operation codes. */
 enum haste_op {
     HASTE_OP_FWD = 0, HASTE_OP_BWD_W = 1, HASTE_OP_BWD_X = 2, HASTE_OP_FWD_BCE = 3, HASTE_OP_FWD_BCE_SGD = 4,
-    HASTE_OP_REWIRE = 5
+    HASTE_OP_REWIRE = 5, HASTE_OP_TAIL_STEP = 6
 };
 
 /* Hyper-parameters of one step of SGD with momentum (see haste_sgd_momentum). */
@@ -217,6 +217,22 @@ typedef struct haste_group_opts {
 int haste_group_labels(int64_t N, int64_t D, const int8_t *E, const haste_group_opts_t *opts, int32_t *order,
                        int32_t *gsize, int64_t *n_groups, int32_t *cluster, void *ws, size_t ws_bytes,
                        void *stream);
+
+/*
+ * The tail's training pass (Section 3.2 forward and both backward products, with the gradient of
+ * the Section 3.3 objective): haste_fwd_bce (dY, dW, dbias as documented there) followed by
+ *   dX = beta_dx * dX + scatter(dY W)        as haste_bwd_x, on the dY just formed.
+ * Same arguments and rules as those two calls; beta applies to dW and dbias, beta_dx to dX.
+ * Results equal the two calls' bit for bit.  For groups of 32 labels on the fused path the
+ * forward kernel also writes the transposed weights and lane-ordered supports the backward-feature
+ * kernel reads, into the workspace, so that pass skips its own transposition of W.  dX NULL runs
+ * haste_fwd_bce alone.  ws: haste_workspace_bytes(desc, HASTE_OP_TAIL_STEP) bytes (holds both
+ * calls' workspaces side by side); too small gives HASTE_ERR_WORKSPACE and launches nothing.
+ */
+int haste_tail_step(const haste_desc_t *desc, const void *X, const int32_t *idx, const void *W,
+                    const float *bias, const int32_t *pos, int32_t P, void *dY, float *dW,
+                    float *dbias, int beta, float *dX, int beta_dx, void *ws, size_t ws_bytes,
+                    void *stream);
 
 /* Bytes of workspace haste_group_labels needs (0 for invalid arguments). */
 size_t haste_group_workspace_bytes(int64_t N, int64_t D, const haste_group_opts_t *opts);

@@ -96,6 +96,10 @@ size_t haste_workspace_bytes(const haste_desc_t *d, int op) {
         case HASTE_OP_FWD_BCE: return haste::bwd_w_mfma_supported(a) ? haste::bwd_w_mfma_ws(a) : 0;
         // the composed form also keeps dW in the workspace (after the X^T copy)
         case HASTE_OP_REWIRE: return haste::rewire_supported(a) ? haste::rewire_ws(a) : 0;
+        // backward-feature's region (partials, transposed weights, supports), then the fused kernel's
+        case HASTE_OP_TAIL_STEP:
+            return (size_t)haste::round_up((int64_t)haste_workspace_bytes(d, HASTE_OP_BWD_X), 256) +
+                   haste_workspace_bytes(d, HASTE_OP_FWD_BCE);
         case HASTE_OP_FWD_BCE_SGD:
             return (haste::bwd_w_mfma_supported(a) ? haste::bwd_w_mfma_ws(a) : 0) +
                    (haste::fwd_bce_mfma_supported(a, 0) ? 0 : (size_t)haste::round_up(a.L * a.F_in * 4, 256));
@@ -177,6 +181,42 @@ int haste_bwd_x(const haste_desc_t *d, const int32_t *idx, const void *W, const 
     TRY(need_ptr(ws, "ws"));
     if (mf) return hip_status(haste::bwd_x_mfma(a, idx, W, dY, dX, beta, ws, s), "haste_bwd_x");
     return hip_status(haste::bwd_x_valu(a, idx, W, dY, dX, beta, ws, s), "haste_bwd_x");
+}
+
+int haste_tail_step(const haste_desc_t *d, const void *X, const int32_t *idx, const void *W, const float *bias,
+                    const int32_t *pos, int32_t P, void *dY, float *dW, float *dbias, int beta, float *dX, int beta_dx,
+                    void *ws, size_t ws_bytes, void *stream) {
+    TRY(check_desc(d));
+    if (beta != 0 && beta != 1) return fail(HASTE_ERR_INVALID, "beta must be 0 or 1");
+    if (beta_dx != 0 && beta_dx != 1) return fail(HASTE_ERR_INVALID, "beta_dx must be 0 or 1");
+    if (P < 0) return fail(HASTE_ERR_INVALID, "P must be >= 0");
+    const haste::TailArgs a = targs(d);
+    const size_t need = haste_workspace_bytes(d, HASTE_OP_TAIL_STEP);
+    if (need && (!ws || ws_bytes < need))
+        return fail(HASTE_ERR_WORKSPACE, "haste_tail_step needs %zu workspace bytes, got %zu", need, ws ? ws_bytes : 0);
+    const size_t xoff = (size_t)haste::round_up((int64_t)haste_workspace_bytes(d, HASTE_OP_BWD_X), 256);
+    if (a.L > 0 && a.B > 0 && dW && dX && haste::tail_step_fused(a, P)) {
+        TRY(need_ptr(X, "X"));
+        TRY(need_ptr(idx, "idx"));
+        TRY(need_ptr(W, "W"));
+        TRY(need_ptr(dY, "dY"));
+        TRY(need_ptr(dW, "dW"));
+        TRY(need_ptr(dX, "dX"));
+        TRY(need_ptr(ws, "ws"));
+        if (P > 0) TRY(need_ptr(pos, "pos"));
+        if (bias && !aligned16(bias)) return fail(HASTE_ERR_INVALID, "bias is not 16-byte aligned");
+        if (dbias && !aligned16(dbias)) return fail(HASTE_ERR_INVALID, "dbias is not 16-byte aligned");
+        if (a.B * haste::cdiv(a.L, 2048) >= ((int64_t)1 << 31))
+            return fail(HASTE_ERR_UNSUPPORTED, "B * L too large for the gradient kernel's grid");
+        return hip_status(haste::tail_step_mfma(a, X, idx, W, bias, P > 0 ? pos : nullptr, P, dY, dW, dbias, beta, dX,
+                                                beta_dx, ws, as_stream(stream)),
+                          "haste_tail_step");
+    }
+    // composed: the two calls, each in its own part of the workspace
+    TRY(haste_fwd_bce(d, X, idx, W, bias, pos, P, dY, dW, dbias, beta, ws ? (char *)ws + xoff : nullptr,
+                      ws ? ws_bytes - xoff : 0, stream));
+    if (!dX) return ok();
+    return haste_bwd_x(d, idx, W, dY, dX, beta_dx, ws, xoff, stream);
 }
 
 int haste_fwd_bce(const haste_desc_t *d, const void *X, const int32_t *idx, const void *W, const float *bias,

@@ -558,6 +558,9 @@ constexpr int kFbYRow = 1056;                   // bytes per staged dY row: 512 
 // waves per workgroup: one 32-label unit each; 128-slot supports need twice the registers
 __host__ __device__ constexpr int fb_waves(int F_in) { return F_in == 128 ? 8 : 16; }
 
+// a wave's LDS region for the transposed weights of its group (32 labels) and the slot positions
+__host__ __device__ constexpr int fb_wt_region(int f_in) { return 32 * f_in * 2 + 128; }
+
 // X^T block, both bitmaps and the staged dY block, or at the end the dW staging of half the waves
 static size_t fb_lds(int F_s, int F_in) {
     const size_t main = (size_t)haste::round_up((int64_t)F_s * kBw2XRow, 16) + 2 * kFbMaxSpan * 4 +
@@ -585,7 +588,8 @@ __global__ __launch_bounds__(64 * fb_waves(F_IN)) void k_fwd_bce(
     const bf16_t *__restrict__ Xb, const int32_t *__restrict__ idx, const bf16_t *__restrict__ W,
     const float *__restrict__ bias, const int32_t *__restrict__ pos, int P, bf16_t *__restrict__ dY,
     float *__restrict__ dW, float *__restrict__ dbias, int beta, float lr, float momentum, float weight_decay,
-    float *__restrict__ mom, bf16_t *__restrict__ W_next, int B, int Bp, int F_s, int64_t L, int G, int64_t K) {
+    float *__restrict__ mom, bf16_t *__restrict__ W_next, int B, int Bp, int F_s, int64_t L, int G, int64_t K,
+    bf16_t *__restrict__ WT, int32_t *__restrict__ idxl) {
     constexpr bool WITH_DW = OUT != kFbOutNone;
     extern __shared__ __align__(16) char fbs[];
     constexpr int NW = fb_waves(F_IN);
@@ -705,6 +709,69 @@ __global__ __launch_bounds__(64 * fb_waves(F_IN)) void k_fwd_bce(
     const bf16x8_t ones = as_bf16x8(make_uint4(0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u));
     const bool odd = (l16 & 1) != 0;
 
+    // For the backward-feature pass of the same step (groups of 32 labels, so a wave's unit is one
+    // group): the group's weights transposed and its supports in lane order, in that pass's layout
+    // (W^T label-octet major [4][F_IN positions][8 labels]; positions dealt by residue mod 8, as its
+    // accumulator banks need).  Staged through this wave's LDS region before the slabs use the LDS.
+    if constexpr (WITH_DW) {
+        if (WT) {
+            constexpr int RB = 32 * F_IN * 2;                         // bytes of a group's W^T
+            char *tw = fbs + wave * fb_wt_region(F_IN);
+            uint8_t *sp = reinterpret_cast<uint8_t *>(tw + RB);        // position of each slot
+            const int32_t *ik = idx + vu * F_IN;
+            int f[2], cls[2], occ[2] = {0, 0};
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                const int t = lane + 64 * i;
+                f[i] = t < F_IN ? ik[t] : -1;
+                cls[i] = f[i] >= 0 ? (f[i] & 7) : -1;
+            }
+            const uint64_t lt = __lanemask_lt();
+            int cnt[8];
+#pragma unroll
+            for (int c = 0; c < 8; ++c) {
+                const uint64_t m0 = __ballot(cls[0] == c), m1 = __ballot(cls[1] == c);
+                if (cls[0] == c) occ[0] = __popcll(m0 & lt);
+                if (cls[1] == c) occ[1] = __popcll(m0) + __popcll(m1 & lt);
+                cnt[c] = __popcll(m0) + __popcll(m1);
+            }
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                if (cls[i] < 0) continue;
+                const int r = cls[i], o = occ[i];
+                int rank = 0;                     // slots with a smaller (occurrence, residue)
+#pragma unroll
+                for (int c = 0; c < 8; ++c) rank += (cnt[c] < o ? cnt[c] : o) + (c < r && cnt[c] > o ? 1 : 0);
+                sp[lane + 64 * i] = (uint8_t)rank;
+                if (v < nunits) idxl[vu * F_IN + (rank & 15) * NST + (rank >> 4)] = f[i];
+            }
+            __builtin_amdgcn_wave_barrier();
+#pragma unroll
+            for (int s = 0; s < KS; ++s) {
+                const uint2 pp = *reinterpret_cast<const uint2 *>(sp + 32 * s + 8 * q);   // positions of 8 slots
+#pragma unroll
+                for (int nt = 0; nt < 2; ++nt) {
+                    const int lam = 16 * nt + l16;
+                    const uint32_t u[4] = {wop[nt][s].x, wop[nt][s].y, wop[nt][s].z, wop[nt][s].w};
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const int ps = (int)(((e < 4 ? pp.x : pp.y) >> (8 * (e & 3))) & 0xffu);
+                        *reinterpret_cast<bf16_t *>(tw + (((lam >> 3) * F_IN + ps) * 8 + (lam & 7)) * 2) =
+                            (bf16_t)((e & 1) ? (u[e >> 1] >> 16) : (u[e >> 1] & 0xffffu));
+                    }
+                }
+            }
+            __builtin_amdgcn_wave_barrier();
+            if (v < nunits) {
+                char *dst = reinterpret_cast<char *>(WT) + vu * RB;
+#pragma unroll
+                for (int i = 0; i < RB / 1024; ++i)
+                    *reinterpret_cast<uint4 *>(dst + (i * 64 + lane) * 16) =
+                        *reinterpret_cast<const uint4 *>(tw + (i * 64 + lane) * 16);
+            }
+            __syncthreads();   // every wave's region is read out before the bitmaps and slabs use the LDS
+        }
+    }
     for (int i = tid; i < 2 * kFbMaxSpan; i += NT) bm[i] = 0u;
     const int nblk = Bp / 32;
     load(0);
@@ -1410,20 +1477,24 @@ struct FbArgs {
     float *m;
     void *W_next;
     int Bp;
+    bf16_t *WT;       // transposed weights and lane-ordered supports for backward-feature, or null
+    int32_t *idxl;
 };
 
 template <int F_IN, int OUT>
 static hipError_t launch_fwd_bce(const TailArgs &a, const FbArgs &f, hipStream_t s) {
     const int64_t K = a.L / a.G;
     const int64_t units = K * cdiv(a.G, 32);
-    const size_t lds = fb_lds((int)a.F_s, F_IN);
+    size_t lds = fb_lds((int)a.F_s, F_IN);
+    if (f.WT && lds < (size_t)fb_waves(F_IN) * fb_wt_region(F_IN)) lds = (size_t)fb_waves(F_IN) * fb_wt_region(F_IN);
     const dim3 grid((unsigned)cdiv(units, fb_waves(F_IN)));
     auto go = [&](auto kern) {
         hipError_t e = allow_lds(kern, lds);
         if (e != hipSuccess) return e;
         hipLaunchKernelGGL(kern, grid, dim3(fb_waves(F_IN) * 64), lds, s, f.Xb, f.idx, (const bf16_t *)f.W, f.bias,
                            f.pos, f.P, (bf16_t *)f.dY, f.dW, f.dbias, f.beta, f.opt.lr, f.opt.momentum,
-                           f.opt.weight_decay, f.m, (bf16_t *)f.W_next, (int)a.B, f.Bp, (int)a.F_s, a.L, (int)a.G, K);
+                           f.opt.weight_decay, f.m, (bf16_t *)f.W_next, (int)a.B, f.Bp, (int)a.F_s, a.L, (int)a.G, K,
+                           f.WT, f.idxl);
         return hipGetLastError();
     };
     if constexpr (OUT == kFbOutNone)
@@ -1452,14 +1523,15 @@ static hipError_t fwd_bce_dispatch(const TailArgs &a, const void *X, FbArgs &f, 
 hipError_t fwd_bce_mfma(const TailArgs &a, const void *X, const int32_t *idx, const void *W, const float *bias,
                         const int32_t *pos, int P, void *dY, float *dW, float *dbias, int beta, void *ws,
                         hipStream_t s) {
-    FbArgs f{nullptr, idx, W, bias, pos, P, dY, dW, dbias, beta, haste_sgd_t{0.f, 0.f, 0.f, 0}, nullptr, nullptr, 0};
+    FbArgs f{nullptr, idx, W, bias, pos, P, dY, dW, dbias, beta, haste_sgd_t{0.f, 0.f, 0.f, 0}, nullptr, nullptr, 0,
+             nullptr, nullptr};
     return dW ? fwd_bce_dispatch<kFbOutDW>(a, X, f, ws, s) : fwd_bce_dispatch<kFbOutNone>(a, X, f, ws, s);
 }
 
 hipError_t fwd_bce_sgd_mfma(const TailArgs &a, const void *X, const int32_t *idx, const void *W, const float *bias,
                             const int32_t *pos, int P, void *dY, float *dbias, const haste_sgd_t &opt, float *m,
                             void *W_next, void *ws, hipStream_t s) {
-    FbArgs f{nullptr, idx, W, bias, pos, P, dY, nullptr, dbias, 0, opt, m, W_next, 0};
+    FbArgs f{nullptr, idx, W, bias, pos, P, dY, nullptr, dbias, 0, opt, m, W_next, 0, nullptr, nullptr};
     return fwd_bce_dispatch<kFbOutSGD>(a, X, f, ws, s);
 }
 
@@ -1513,6 +1585,9 @@ static hipError_t launch_bwd_x_g(const TailArgs &a, const BwdXGeom &g, const int
     return hipErrorInvalidValue;
 }
 
+static hipError_t bwd_x_main(const TailArgs &a, const BwdXGeom &g, const int32_t *idxl, const bf16_t *WT,
+                             const void *dY, float *part, float *dX, int beta, hipStream_t s);
+
 hipError_t bwd_x_mfma(const TailArgs &a, const int32_t *idx, const void *W, const void *dY, float *dX, int beta,
                       void *ws, hipStream_t s) {
     const BwdXGeom g = bwd_x_geom(a);
@@ -1529,6 +1604,13 @@ hipError_t bwd_x_mfma(const TailArgs &a, const int32_t *idx, const void *W, cons
                        WT, idxl, K, (int)a.G, Gp, (int)a.F_in);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
+    return bwd_x_main(a, g, idxl, WT, dY, part, dX, beta, s);
+}
+
+// the main kernel and the reduction, on transposed weights and lane-ordered supports already built
+static hipError_t bwd_x_main(const TailArgs &a, const BwdXGeom &g, const int32_t *idxl, const bf16_t *WT,
+                             const void *dY, float *part, float *dX, int beta, hipStream_t s) {
+    hipError_t e = hipSuccess;
     switch (a.F_in) {
         case 32: e = launch_bwd_x_g<32>(a, g, idxl, WT, dY, part, s); break;
         case 64: e = launch_bwd_x_g<64>(a, g, idxl, WT, dY, part, s); break;
@@ -1537,6 +1619,30 @@ hipError_t bwd_x_mfma(const TailArgs &a, const int32_t *idx, const void *W, cons
     }
     if (e != hipSuccess) return e;
     return reduce_fmajor(part, (int)g.nseg, g.nbt * 32, a.B, a.F_s, dX, beta, s);
+}
+
+// ---- the tail's training pass: fused forward + loss gradient + dW, then backward-feature ----------
+// Groups of 32 labels, where a fused-kernel wave's unit is one group: that kernel also writes the
+// transposed weights and lane-ordered supports backward-feature reads (the pre-pass is skipped).
+bool tail_step_fused(const TailArgs &a, int P) {
+    return a.G == 32 && fwd_bce_mfma_supported(a, P) && bwd_x_mfma_supported(a);
+}
+
+size_t tail_step_ws(const TailArgs &a) { return round_up(bwd_x_mfma_ws(a), 256) + fwd_bce_mfma_ws(a); }
+
+hipError_t tail_step_mfma(const TailArgs &a, const void *X, const int32_t *idx, const void *W, const float *bias,
+                          const int32_t *pos, int P, void *dY, float *dW, float *dbias, int beta, float *dX,
+                          int beta_dx, void *ws, hipStream_t s) {
+    const BwdXGeom g = bwd_x_geom(a);
+    char *wb = reinterpret_cast<char *>(ws);
+    float *part = reinterpret_cast<float *>(wb);
+    bf16_t *WT = reinterpret_cast<bf16_t *>(wb + bwd_x_part_bytes(a, g));
+    int32_t *idxl = reinterpret_cast<int32_t *>(reinterpret_cast<char *>(WT) + bwd_x_wt_bytes(a));
+    FbArgs f{nullptr, idx, W, bias, pos, P, dY, dW, dbias, beta, haste_sgd_t{0.f, 0.f, 0.f, 0}, nullptr, nullptr, 0,
+             WT, idxl};
+    hipError_t e = fwd_bce_dispatch<kFbOutDW>(a, X, f, wb + round_up(bwd_x_mfma_ws(a), 256), s);
+    if (e != hipSuccess) return e;
+    return bwd_x_main(a, g, idxl, WT, dY, part, dX, beta_dx, s);
 }
 
 }  // namespace haste

@@ -28,14 +28,15 @@ def test_algorithmic_bytes_of_the_3m_layer():
     assert c["fwd_bce"][0] == X + idx + W + B * 8 * 4 + Y + dW
     assert round(c["bwd_x"][0] / 1e9, 2) == 3.42 and round(c["fwd_bce"][0] / 1e9, 2) == 4.18
     assert c["head_fwd_bce"] == (c["head_fwd"][0] + B * 8 * 4, 2 * B * H * F_s)
+    assert c["tail_step"][0] == c["fwd_bce"][0] + c["bwd_x"][0]
 
 
 def test_profiled_kernels_are_charged_to_their_calls():
     def owners(kernel):
         return {c for c, pats in bench.CALL_KERNELS.items() if any(re.match(p, kernel) for p in pats)}
-    assert owners("k_fwd_bce<64, false, 1, false>") == {"fwd_bce"}
+    assert owners("k_fwd_bce<64, false, 1, false>") == {"fwd_bce", "tail_step"}
     assert owners("k_fwd_bce<128, true, 2, true>") == {"fwd_bce_sgd"}
     assert owners("k_gemm4<true, true, 3>") == {"head_fwd_bce"}
     assert owners("k_gemm4<true, true, 0>") == {"head_fwd"}
-    assert owners("k_bwd_x<64, 1>") == {"bwd_x"} and owners("k_transpose_w") == {"bwd_x"}
+    assert owners("k_bwd_x<64, 1>") == {"bwd_x", "tail_step"} and owners("k_transpose_w") == {"bwd_x"}
     assert "head_bwd" in owners("k_reduce_rmajor") and "bwd_x" in owners("k_reduce_fmajor")
