@@ -46,6 +46,7 @@ CALL_KERNELS = {
     "fwd_bce": ["k_transpose_x", r"k_fwd_bce<\d+, \w+, 1,"],
     "fwd_bce_sgd": ["k_transpose_x", r"k_fwd_bce<\d+, \w+, 2,"],
     "tail_step": ["k_transpose_x", r"k_fwd_bce<\d+, \w+, 1,", "k_bwd_x", "k_reduce_fmajor"],
+    "tail_step_sgd": ["k_transpose_x", r"k_fwd_bce<\d+, \w+, 2,", "k_bwd_x", "k_reduce_fmajor"],
     "sgd": ["k_sgd_momentum"],
     "head_sgd": ["k_sgd_momentum"],
     "rewire": ["k_rw_"],
@@ -111,6 +112,7 @@ def call_cost(wl, dt_bytes=2, n_pos=0):
         "bwd_x": (idx + W + Y + dX, tail_flops),
     }
     c["tail_step"] = (c["fwd_bce"][0] + c["bwd_x"][0], c["fwd_bce"][1] + c["bwd_x"][1])   # both passes' operands
+    c["tail_step_sgd"] = (c["fwd_bce_sgd"][0] + c["bwd_x"][0], c["fwd_bce_sgd"][1] + c["bwd_x"][1])
     if H:
         c["head_fwd"] = (X + Wh + Yh, head_flops)
         c["head_bce"] = (2 * Yh + pos, 0)
@@ -357,16 +359,15 @@ def main():
     opt = hs.sgd_opts(0.01, 0.9, 0.0)
     mom = torch.zeros((wl.L, wl.F_in), dtype=torch.float32, device=dev)
     Wnext = torch.empty_like(Wd)
-    ws_s = hs.workspace(hs.haste_workspace_bytes(desc, hs.HASTE_OP_FWD_BCE_SGD))
     if wl.H:
         mom_h = torch.zeros((wl.H, wl.F_s), dtype=torch.float32, device=dev)
         Whnext = torch.empty_like(Whd)
     head_step = ([("head_sgd", lambda: hs.haste_sgd_momentum(wl.H * wl.F_s, wl.dtype, Whd, dWh, mom_h, opt,
                                                              Whnext))] if wl.H else [])
-    fused_opt = ([("fwd_bce_sgd", lambda: hs.haste_fwd_bce_sgd(desc, Xd, idxd, Wd, None, posd, dYt, opt, mom, Wnext,
-                                                               None, ws_s))] +
-                 head_train() + [("bwd_x", lambda: hs.haste_bwd_x(desc, idxd, Wd, dYt, dX, 0, ws_x))] +
-                 (head_back(dYht) if wl.H else []) + head_step)
+    ws_ts = hs.workspace(hs.haste_workspace_bytes(desc, hs.HASTE_OP_TAIL_STEP_SGD))
+    fused_opt = ([("tail_step_sgd", lambda: hs.haste_tail_step_sgd(desc, Xd, idxd, Wd, None, posd, dYt, None, opt, mom,
+                                                                   Wnext, dX, 0, ws_ts))] +
+                 head_train() + (head_back(dYht) if wl.H else []) + head_step)
     unfused_opt = unfused + [("sgd", lambda: hs.haste_sgd_momentum(wl.L * wl.F_in, wl.dtype, Wd, dW, mom, opt,
                                                                    Wnext))] + head_step
     separate = [("fwd", lambda: hs.haste_fwd(desc, Xd, idxd, Wd, None, Y))]
@@ -450,7 +451,7 @@ def main():
             "fused_per_call_ms": {k: round(v, 4) for k, v in fo_per.items()},
             "unfused_per_call_ms": {k: round(v, 4) for k, v in uo_per.items()},
             "what": "the training pass plus one SGD-with-momentum step on W and W_h: fused, the tail's step runs "
-                    "inside haste_fwd_bce_sgd (dW never stored) and the head's loss gradient inside "
+                    "inside haste_tail_step_sgd (dW never stored) and the head's loss gradient inside "
                     "haste_head_fwd_bce; unfused, the unfused training step + haste_sgd_momentum"},
         "separate_calls_step": {
             "ms": round(sep_ms, 4), "per_call": detail(sep_per),

@@ -51,7 +51,7 @@ enum haste_status {
 /* Workspace-query operation codes. */
 enum haste_op {
     HASTE_OP_FWD = 0, HASTE_OP_BWD_W = 1, HASTE_OP_BWD_X = 2, HASTE_OP_FWD_BCE = 3, HASTE_OP_FWD_BCE_SGD = 4,
-    HASTE_OP_REWIRE = 5, HASTE_OP_TAIL_STEP = 6
+    HASTE_OP_REWIRE = 5, HASTE_OP_TAIL_STEP = 6, HASTE_OP_TAIL_STEP_SGD = 7
 };
 
 /* Hyper-parameters of one step of SGD with momentum (see haste_sgd_momentum). */
@@ -233,6 +233,17 @@ int haste_tail_step(const haste_desc_t *desc, const void *X, const int32_t *idx,
                     const float *bias, const int32_t *pos, int32_t P, void *dY, float *dW,
                     float *dbias, int beta, float *dX, int beta_dx, void *ws, size_t ws_bytes,
                     void *stream);
+
+/*
+ * The same pass with the optimizer step (Section 4: SGD with momentum): haste_fwd_bce_sgd (dY, m,
+ * W_next, dbias as documented there; dW never stored) followed by haste_bwd_x on its dY with the
+ * step's W (not W_next), bit-identical to the two calls.  W_next must not overlap W.
+ * ws: haste_workspace_bytes(desc, HASTE_OP_TAIL_STEP_SGD) bytes.
+ */
+int haste_tail_step_sgd(const haste_desc_t *desc, const void *X, const int32_t *idx, const void *W,
+                        const float *bias, const int32_t *pos, int32_t P, void *dY, float *dbias,
+                        const haste_sgd_t *opt, float *m, void *W_next, float *dX, int beta_dx,
+                        void *ws, size_t ws_bytes, void *stream);
 
 /* Bytes of workspace haste_group_labels needs (0 for invalid arguments). */
 size_t haste_group_workspace_bytes(int64_t N, int64_t D, const haste_group_opts_t *opts);

@@ -20,7 +20,7 @@ LIB_PATH = os.path.join(PKG, "libhaste.so")
 HASTE_DTYPE_F32 = 0
 HASTE_DTYPE_BF16 = 1
 (HASTE_OP_FWD, HASTE_OP_BWD_W, HASTE_OP_BWD_X, HASTE_OP_FWD_BCE, HASTE_OP_FWD_BCE_SGD, HASTE_OP_REWIRE,
- HASTE_OP_TAIL_STEP) = range(7)
+ HASTE_OP_TAIL_STEP, HASTE_OP_TAIL_STEP_SGD) = range(8)
 STATUS = {0: "ok", 1: "invalid argument", 2: "unsupported", 3: "workspace too small", 4: "HIP error"}
 
 
@@ -62,6 +62,8 @@ def _load() -> ctypes.CDLL:
         "haste_group_labels": [I64, I64, P, ctypes.POINTER(haste_group_opts_t), P, P, P, P, P, SZ, P],
         "haste_head_fwd": [I64, I64, I64, I32, P, P, P, P, P],
         "haste_tail_step": [D, P, P, P, P, P, I32, P, P, P, ctypes.c_int, P, ctypes.c_int, P, SZ, P],
+        "haste_tail_step_sgd": [D, P, P, P, P, P, I32, P, P, ctypes.POINTER(haste_sgd_t), P, P, P, ctypes.c_int, P, SZ,
+                                P],
         "haste_head_fwd_bce": [I64, I64, I64, I32, P, P, P, P, I32, P, P],
         "haste_head_bwd": [I64, I64, I64, I32, P, P, P, P, P, ctypes.c_int, P, SZ, P],
         "haste_validate_idx": [D, P, P, P],
@@ -88,7 +90,7 @@ lib = _load()
 # every symbol the header declares
 EXPORTS = ("haste_fwd", "haste_bwd_w", "haste_bwd_x", "haste_fwd_bce", "haste_fwd_bce_sgd", "haste_sgd_momentum",
            "haste_rewire", "haste_group_labels", "haste_group_workspace_bytes", "haste_bce_grad", "haste_head_fwd",
-           "haste_head_fwd_bce", "haste_head_bwd", "haste_tail_step", "haste_workspace_bytes", "haste_head_workspace_bytes", "haste_validate_idx", "haste_debug_gather", "haste_status_str",
+           "haste_head_fwd_bce", "haste_head_bwd", "haste_tail_step", "haste_tail_step_sgd", "haste_workspace_bytes", "haste_head_workspace_bytes", "haste_validate_idx", "haste_debug_gather", "haste_status_str",
            "haste_last_error", "haste_version")
 
 
@@ -192,6 +194,14 @@ def haste_tail_step(desc, X, idx, W, bias, pos, dY, dW, dbias, beta, dX, beta_dx
     _check(lib.haste_tail_step(ctypes.byref(desc), _ptr(X), _ptr(idx), _ptr(W), _ptr(bias), _ptr(pos), _npos(pos),
                                _ptr(dY), _ptr(dW), _ptr(dbias), int(beta), _ptr(dX), int(beta_dx), p, n,
                                _stream(stream)))
+
+
+def haste_tail_step_sgd(desc, X, idx, W, bias, pos, dY, dbias, opt, m, W_next, dX, beta_dx, ws=None, stream=None):
+    """haste_fwd_bce_sgd followed by haste_bwd_x on its dY with the step's W."""
+    p, n = _ws(ws)
+    _check(lib.haste_tail_step_sgd(ctypes.byref(desc), _ptr(X), _ptr(idx), _ptr(W), _ptr(bias), _ptr(pos), _npos(pos),
+                                   _ptr(dY), _ptr(dbias), ctypes.byref(opt), _ptr(m), _ptr(W_next), _ptr(dX),
+                                   int(beta_dx), p, n, _stream(stream)))
 
 
 def sgd_opts(lr: float, momentum: float, weight_decay: float = 0.0) -> haste_sgd_t:

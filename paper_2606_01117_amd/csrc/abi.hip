@@ -100,6 +100,9 @@ size_t haste_workspace_bytes(const haste_desc_t *d, int op) {
         case HASTE_OP_TAIL_STEP:
             return (size_t)haste::round_up((int64_t)haste_workspace_bytes(d, HASTE_OP_BWD_X), 256) +
                    haste_workspace_bytes(d, HASTE_OP_FWD_BCE);
+        case HASTE_OP_TAIL_STEP_SGD:
+            return (size_t)haste::round_up((int64_t)haste_workspace_bytes(d, HASTE_OP_BWD_X), 256) +
+                   haste_workspace_bytes(d, HASTE_OP_FWD_BCE_SGD);
         case HASTE_OP_FWD_BCE_SGD:
             return (haste::bwd_w_mfma_supported(a) ? haste::bwd_w_mfma_ws(a) : 0) +
                    (haste::fwd_bce_mfma_supported(a, 0) ? 0 : (size_t)haste::round_up(a.L * a.F_in * 4, 256));
@@ -490,3 +493,44 @@ int haste_debug_gather(const haste_desc_t *d, const void *X, const int32_t *idx,
 }
 
 }  // extern "C"
+
+int haste_tail_step_sgd(const haste_desc_t *d, const void *X, const int32_t *idx, const void *W, const float *bias,
+                        const int32_t *pos, int32_t P, void *dY, float *dbias, const haste_sgd_t *opt, float *m,
+                        void *W_next, float *dX, int beta_dx, void *ws, size_t ws_bytes, void *stream) {
+    TRY(check_desc(d));
+    TRY(check_sgd(opt));
+    if (beta_dx != 0 && beta_dx != 1) return fail(HASTE_ERR_INVALID, "beta_dx must be 0 or 1");
+    if (P < 0) return fail(HASTE_ERR_INVALID, "P must be >= 0");
+    const haste::TailArgs a = targs(d);
+    const size_t need = haste_workspace_bytes(d, HASTE_OP_TAIL_STEP_SGD);
+    if (need && (!ws || ws_bytes < need))
+        return fail(HASTE_ERR_WORKSPACE, "haste_tail_step_sgd needs %zu workspace bytes, got %zu", need,
+                    ws ? ws_bytes : 0);
+    const size_t xoff = (size_t)haste::round_up((int64_t)haste_workspace_bytes(d, HASTE_OP_BWD_X), 256);
+    if (a.L > 0 && a.B > 0 && dX && haste::tail_step_fused(a, P)) {
+        TRY(need_ptr(X, "X"));
+        TRY(need_ptr(idx, "idx"));
+        TRY(need_ptr(W, "W"));
+        TRY(need_ptr(dY, "dY"));
+        TRY(need_ptr(m, "m"));
+        TRY(need_ptr(W_next, "W_next"));
+        TRY(need_ptr(dX, "dX"));
+        TRY(need_ptr(ws, "ws"));
+        if (P > 0) TRY(need_ptr(pos, "pos"));
+        if (bias && !aligned16(bias)) return fail(HASTE_ERR_INVALID, "bias is not 16-byte aligned");
+        if (dbias && !aligned16(dbias)) return fail(HASTE_ERR_INVALID, "dbias is not 16-byte aligned");
+        const uintptr_t wb = (uintptr_t)W, nb = (uintptr_t)W_next, len = (uintptr_t)(a.L * a.F_in * 2);
+        if (wb < nb + len && nb < wb + len)
+            return fail(HASTE_ERR_INVALID, "W_next overlaps W (the backward-feature pass still reads W)");
+        if (a.B * haste::cdiv(a.L, 2048) >= ((int64_t)1 << 31))
+            return fail(HASTE_ERR_UNSUPPORTED, "B * L too large for the gradient kernel's grid");
+        return hip_status(haste::tail_step_sgd_mfma(a, X, idx, W, bias, P > 0 ? pos : nullptr, P, dY, dbias, *opt, m,
+                                                    W_next, dX, beta_dx, ws, ws_bytes - xoff, as_stream(stream)),
+                          "haste_tail_step_sgd");
+    }
+    // composed: the two calls, each in its own part of the workspace
+    TRY(haste_fwd_bce_sgd(d, X, idx, W, bias, pos, P, dY, dbias, opt, m, W_next, ws ? (char *)ws + xoff : nullptr,
+                          ws ? ws_bytes - xoff : 0, stream));
+    if (!dX) return ok();
+    return haste_bwd_x(d, idx, W, dY, dX, beta_dx, ws, xoff, stream);
+}

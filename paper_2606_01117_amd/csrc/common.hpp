@@ -145,6 +145,9 @@ size_t tail_step_ws(const TailArgs &a);
 hipError_t tail_step_mfma(const TailArgs &a, const void *X, const int32_t *idx, const void *W, const float *bias,
                           const int32_t *pos, int P, void *dY, float *dW, float *dbias, int beta, float *dX,
                           int beta_dx, void *ws, hipStream_t s);
+hipError_t tail_step_sgd_mfma(const TailArgs &a, const void *X, const int32_t *idx, const void *W, const float *bias,
+                              const int32_t *pos, int P, void *dY, float *dbias, const haste_sgd_t &opt, float *m,
+                              void *W_next, float *dX, int beta_dx, void *ws, size_t fb_ws_bytes, hipStream_t s);
 bool bwd_x_mfma_supported(const TailArgs &a);
 size_t bwd_x_mfma_ws(const TailArgs &a);
 hipError_t bwd_x_mfma(const TailArgs &a, const int32_t *idx, const void *W, const void *dY, float *dX, int beta,

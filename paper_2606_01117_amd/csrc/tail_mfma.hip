@@ -1645,4 +1645,21 @@ hipError_t tail_step_mfma(const TailArgs &a, const void *X, const int32_t *idx, 
     return bwd_x_main(a, g, idxl, WT, dY, part, dX, beta_dx, s);
 }
 
+// the same pass with the momentum step in the fused kernel (dW never stored); the transposed
+// weights it hands over are those of the step's W, read before the update
+hipError_t tail_step_sgd_mfma(const TailArgs &a, const void *X, const int32_t *idx, const void *W, const float *bias,
+                              const int32_t *pos, int P, void *dY, float *dbias, const haste_sgd_t &opt, float *m,
+                              void *W_next, float *dX, int beta_dx, void *ws, size_t fb_ws_bytes, hipStream_t s) {
+    (void)fb_ws_bytes;
+    const BwdXGeom g = bwd_x_geom(a);
+    char *wb = reinterpret_cast<char *>(ws);
+    float *part = reinterpret_cast<float *>(wb);
+    bf16_t *WT = reinterpret_cast<bf16_t *>(wb + bwd_x_part_bytes(a, g));
+    int32_t *idxl = reinterpret_cast<int32_t *>(reinterpret_cast<char *>(WT) + bwd_x_wt_bytes(a));
+    FbArgs f{nullptr, idx, W, bias, pos, P, dY, nullptr, dbias, 0, opt, m, W_next, 0, WT, idxl};
+    hipError_t e = fwd_bce_dispatch<kFbOutSGD>(a, X, f, wb + round_up(bwd_x_mfma_ws(a), 256), s);
+    if (e != hipSuccess) return e;
+    return bwd_x_main(a, g, idxl, WT, dY, part, dX, beta_dx, s);
+}
+
 }  // namespace haste

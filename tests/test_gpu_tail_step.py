@@ -90,3 +90,40 @@ def test_tail_step_workspace_checked(hs):
     with pytest.raises(hs.HasteError):
         hs.haste_tail_step(d, dummy, dummy, dummy, None, None, dummy, dummy, None, 0, dummy, 0,
                            hs.workspace(need - 256))
+
+
+@pytest.mark.parametrize("case", [("g32_f64", 64, 768, 4096, 32, 64, 8, True), ("g32_f128", 70, 768, 4096, 32, 128, 5, False),
+                                  ("composed_g16", 48, 512, 4096, 16, 64, 4, False)], ids=lambda c: c[0])
+def test_tail_step_sgd_equals_the_two_calls(hs, case):
+    import torch
+    name, B, F_s, L, G, F_in, P, with_bias = case
+    say(f"[tail_step_sgd] {name}: B={B} F_s={F_s} L={L} G={G} F_in={F_in} P={P}")
+    wl = synth.small(name, B=B, F_s=F_s, L=L, G=G, F_in=F_in, dtype=BF16, wid=950 + F_in + G)
+    X, W, idx = synth.draw_X(wl), synth.draw_W(wl), synth.draw_idx(wl)
+    rng = np.random.default_rng(wl.wid)
+    bias = rng.standard_normal(L).astype(np.float32) if with_bias else None
+    m0 = rng.standard_normal((L, F_in)).astype(np.float32)
+    pos = rand_pos(rng, B, L, P)
+    desc = hs.make_desc(B, F_s, L, G, F_in, BF16)
+    Xd, idxd, Wd, bd, posd = to_dev(X), to_dev(idx), to_dev(W), to_dev(bias), to_dev(pos)
+    opt = hs.sgd_opts(0.05, 0.9, 1e-4)
+    outs = []
+    for fused in (True, False):
+        dY = out_tensor((B, L), BF16)
+        m = to_dev(m0)
+        Wn = torch.empty_like(Wd)
+        db = torch.empty((L,), dtype=torch.float32, device="cuda") if with_bias else None
+        dX = torch.zeros((B, F_s), dtype=torch.float32, device="cuda")
+        if fused:
+            hs.haste_tail_step_sgd(desc, Xd, idxd, Wd, bd, posd, dY, db, opt, m, Wn, dX, 0,
+                                   hs.workspace(hs.haste_workspace_bytes(desc, hs.HASTE_OP_TAIL_STEP_SGD)))
+        else:
+            hs.haste_fwd_bce_sgd(desc, Xd, idxd, Wd, bd, posd, dY, opt, m, Wn, db,
+                                 hs.workspace(hs.haste_workspace_bytes(desc, hs.HASTE_OP_FWD_BCE_SGD)))
+            hs.haste_bwd_x(desc, idxd, Wd, dY, dX, 0, hs.workspace(hs.haste_workspace_bytes(desc, hs.HASTE_OP_BWD_X)))
+        torch.cuda.synchronize()
+        outs.append((dY.view(torch.int16), m, Wn.view(torch.int16), db, dX))
+    a, b = outs
+    for i, what in enumerate(("dY", "velocity", "W_next", "dbias", "dX")):
+        if a[i] is not None:
+            assert bool((a[i] == b[i]).all()), what
