@@ -258,7 +258,7 @@ int haste_oracle_sgd_momentum(int64_t n, int dtype, const void *W, const double 
 }
 
 /* ---------------------------------------------------------------------------------------------
- * Group-shared rewiring (Alg. 3, the discrete phase of the training loop in Section 3.4):
+ * Group-shared rewiring (Alg. 3, the discrete phase of the alternating training loop in Section 3.3):
  *   1. score every (group k, slot j) by the |w| of the group's labels at that slot;
  *   2. mark the m = floor(K F rho) smallest scores over all groups;
  *   3. give each marked slot a new feature;
@@ -396,21 +396,30 @@ int haste_oracle_rewire(int64_t K, int64_t G, int64_t F, int64_t H, int dtype, i
 
 /* ---------------------------------------------------------------------------------------------
  * Semantic label grouping (Alg. 2): coarse spherical k-means into C = max(1, floor(N / (beta G)))
- * clusters, then, inside each cluster, greedy groups of G: a random unassigned seed and its
- * top-G unassigned labels by similarity (the seed included).
+ * clusters, then, inside each cluster, greedy groups: a random unassigned seed together with its
+ * top-(G - 1) unassigned neighbours by cosine similarity (Section 3.1, "Label Grouping").
  * Readings:
- *   - embeddings are unit vectors stored as int8 (x 127), so every similarity is an exact integer
- *     dot product and every assignment, seed and top-G decision is exact;
- *   - k-means runs `iters` full Lloyd iterations (assign all labels, then move each non-empty
- *     cluster's centre to the int8-quantised direction of its members' sum: round-half-even of
- *     127 s / |s|, |s| in fp64), then a final assignment; the paper's mini-batch variant is a CPU
- *     economy.  Assignment ties go to the lower cluster index;
+ *   - embeddings are stored as int8 (unit vectors x 127, rounded); similarity is the cosine of the
+ *     stored vectors, cos(u, v) = u.v / (|u| |v|) (Eq. grouping-objective's sim);
+ *   - spherical k-means: a centre is the normalised mean of its members, i.e. the direction of
+ *     their sum s (an exact integer vector).  The cosine of e with that centre is e.s / (|e| |s|);
+ *     |e| is the same for every centre and does not change the argmax, so a label goes to the
+ *     centre maximising e.s / |s|.  e.s is an exact integer, |s|^2 an exact integer rounded once to
+ *     double, and the quotient takes one correctly rounded square root and one correctly rounded
+ *     division in fp64: the decision is taken in fp64 on the exact inputs.  Ties go to the lower
+ *     centre.  Initial centres are single labels (s = e); an empty cluster, or one whose members
+ *     sum to zero, keeps its centre;
+ *   - k-means runs `iters` full Lloyd iterations (assign every label, then move every centre),
+ *     then a final assignment; the paper's mini-batch variant is a CPU economy;
+ *   - the greedy stage: the seed always belongs to its own group; the other k - 1 members are the
+ *     unassigned labels of largest cos(e_i, e_s) = (e_i.e_s) / sqrt(|e_i|^2 |e_s|^2), formed in
+ *     fp64 the same way (|e_i|^2 |e_s|^2 < 2^53 is exact), ties to the lower label;
  *   - initial centres: the first C entries of a partial Fisher-Yates shuffle of [0, N) whose i-th
  *     swap partner is i + out(i) mod (N - i); the t-th seed of cluster c is the
  *     (out(N + c N + t) mod n_unassigned)-th unassigned member in ascending label order
  *     (out = SplitMix64 in counter form, as for rewiring);
- *   - top-G ties go to the lower label; a group lists its labels in ascending order; groups are
- *     emitted cluster by cluster, in the order they are formed.
+ *   - a group lists its labels in ascending order; groups are emitted cluster by cluster, in the
+ *     order they are formed.
  * E [N, D] int8; order [N] receives the labels group after group, gsize the group sizes,
  * *n_groups their count, cluster [N] (or NULL) the final cluster of each label.
  * ------------------------------------------------------------------------------------------- */
@@ -420,19 +429,31 @@ static int64_t dot8(const int8_t *a, const int8_t *b, int64_t D) {
     return s;
 }
 
-static void assign_all(int64_t N, int64_t D, int64_t C, const int8_t *E, const int8_t *cen, int32_t *cl) {
+/* |s| of an integer vector: the exact sum of squares (128-bit), rounded once to double, then a
+ * correctly rounded square root */
+static double exact_norm(const int64_t *s, int64_t D) {
+    unsigned __int128 q = 0;
+    for (int64_t d = 0; d < D; ++d) q += (unsigned __int128)((__int128)s[d] * (__int128)s[d]);
+    return sqrt((double)q);
+}
+
+static void assign_all(int64_t N, int64_t D, int64_t C, const int8_t *E, const int64_t *cs, const double *cn,
+                       int32_t *cl) {
 #pragma omp parallel for schedule(static)
     for (int64_t l = 0; l < N; ++l) {
-        int64_t best = 0, bv = dot8(E + l * D, cen, D);
-        for (int64_t c = 1; c < C; ++c) {
-            const int64_t v = dot8(E + l * D, cen + c * D, D);
-            if (v > bv) { bv = v; best = c; }
+        int64_t best = -1;
+        double bv = 0.0;
+        for (int64_t c = 0; c < C; ++c) {
+            int64_t dot = 0;
+            for (int64_t d = 0; d < D; ++d) dot += (int64_t)E[l * D + d] * cs[c * D + d];
+            const double v = (double)dot / cn[c];
+            if (best < 0 || v > bv) { bv = v; best = c; }
         }
         cl[l] = (int32_t)best;
     }
 }
 
-typedef struct { int64_t sim; int32_t id; } cand_t;
+typedef struct { double sim; int32_t id; } cand_t;
 
 static int by_sim(const void *a, const void *b) {
     const cand_t *x = (const cand_t *)a, *y = (const cand_t *)b;
@@ -451,35 +472,36 @@ int haste_oracle_group_labels(int64_t N, int64_t D, const int8_t *E, int64_t G, 
     int64_t C = N / (beta * G);
     if (C < 1) C = 1;
     int32_t *a = (int32_t *)malloc((size_t)N * sizeof(int32_t));
-    int8_t *cen = (int8_t *)malloc((size_t)(C * D));
+    int64_t *cs = (int64_t *)malloc((size_t)(C * D) * sizeof(int64_t));   /* centre directions (sums) */
+    double *cn = (double *)malloc((size_t)C * sizeof(double));            /* their norms */
     int32_t *cl = (int32_t *)malloc((size_t)N * sizeof(int32_t));
     int64_t *sum = (int64_t *)malloc((size_t)D * sizeof(int64_t));
     cand_t *cand = (cand_t *)malloc((size_t)N * sizeof(cand_t));
-    if (!a || !cen || !cl || !sum || !cand) { free(a); free(cen); free(cl); free(sum); free(cand); return 2; }
+    if (!a || !cs || !cn || !cl || !sum || !cand) {
+        free(a); free(cs); free(cn); free(cl); free(sum); free(cand);
+        return 2;
+    }
     for (int64_t i = 0; i < N; ++i) a[i] = (int32_t)i;
     for (int64_t i = 0; i < C; ++i) {
         const int64_t j = i + (int64_t)(splitmix64_at(seed, (uint64_t)i) % (uint64_t)(N - i));
         const int32_t t = a[i]; a[i] = a[j]; a[j] = t;
-        memcpy(cen + i * D, E + (int64_t)a[i] * D, (size_t)D);
+        for (int64_t d = 0; d < D; ++d) cs[i * D + d] = E[(int64_t)a[i] * D + d];
+        cn[i] = exact_norm(cs + i * D, D);
     }
     for (int64_t it = 0; it < iters; ++it) {
-        assign_all(N, D, C, E, cen, cl);
+        assign_all(N, D, C, E, cs, cn, cl);
         for (int64_t c = 0; c < C; ++c) {
             memset(sum, 0, (size_t)D * sizeof(int64_t));
             int64_t cnt = 0;
             for (int64_t l = 0; l < N; ++l)
                 if (cl[l] == c) { ++cnt; for (int64_t d = 0; d < D; ++d) sum[d] += E[l * D + d]; }
-            int64_t ss = 0;
-            for (int64_t d = 0; d < D; ++d) ss += sum[d] * sum[d];
-            if (cnt == 0 || ss == 0) continue;   /* an empty cluster keeps its centre */
-            const double norm = sqrt((double)ss);
-            for (int64_t d = 0; d < D; ++d) {
-                double q = rint(127.0 * (double)sum[d] / norm);
-                cen[c * D + d] = (int8_t)(q > 127.0 ? 127.0 : (q < -127.0 ? -127.0 : q));
-            }
+            const double nrm = exact_norm(sum, D);
+            if (cnt == 0 || nrm == 0.0) continue;   /* the centre stays where it was */
+            memcpy(cs + c * D, sum, (size_t)D * sizeof(int64_t));
+            cn[c] = nrm;
         }
     }
-    assign_all(N, D, C, E, cen, cl);
+    assign_all(N, D, C, E, cs, cn, cl);
     if (cluster) memcpy(cluster, cl, (size_t)N * sizeof(int32_t));
     int64_t pos = 0, ng = 0;
     for (int64_t c = 0; c < C; ++c) {
@@ -487,22 +509,33 @@ int haste_oracle_group_labels(int64_t N, int64_t D, const int8_t *E, int64_t G, 
         for (int64_t l = 0; l < N; ++l)
             if (cl[l] == c) a[nu++] = (int32_t)l;
         for (int64_t t = 0; nu > 0; ++t) {
-            const int64_t s = a[(int64_t)(splitmix64_at(seed, (uint64_t)(N + c * N + t)) % (uint64_t)nu)];
-            for (int64_t i = 0; i < nu; ++i) { cand[i].sim = dot8(E + (int64_t)a[i] * D, E + s * D, D); cand[i].id = a[i]; }
-            qsort(cand, (size_t)nu, sizeof(cand_t), by_sim);
+            const int64_t r = (int64_t)(splitmix64_at(seed, (uint64_t)(N + c * N + t)) % (uint64_t)nu);
+            const int32_t s = a[r];
+            const int64_t ns = dot8(E + (int64_t)s * D, E + (int64_t)s * D, D);
+            int64_t nc = 0;   /* the other unassigned members, by cosine to the seed */
+            for (int64_t i = 0; i < nu; ++i) {
+                if (i == r) continue;
+                const int8_t *e = E + (int64_t)a[i] * D;
+                const int64_t ni = dot8(e, e, D);
+                cand[nc].sim = (double)dot8(e, E + (int64_t)s * D, D) / sqrt((double)(ni * ns));
+                cand[nc].id = a[i];
+                ++nc;
+            }
+            qsort(cand, (size_t)nc, sizeof(cand_t), by_sim);
             const int64_t k = nu < G ? nu : G;
-            for (int64_t i = 0; i < k; ++i) order[pos + i] = cand[i].id;
+            order[pos] = s;
+            for (int64_t i = 0; i + 1 < k; ++i) order[pos + 1 + i] = cand[i].id;
             qsort(order + pos, (size_t)k, sizeof(int32_t), by_id);
             gsize[ng++] = (int32_t)k;
             pos += k;
             /* the rest stay unassigned, ascending */
-            int64_t r = 0;
-            for (int64_t i = k; i < nu; ++i) a[r++] = cand[i].id;
-            qsort(a, (size_t)r, sizeof(int32_t), by_id);
-            nu = r;
+            int64_t rr = 0;
+            for (int64_t i = k - 1; i < nc; ++i) a[rr++] = cand[i].id;
+            qsort(a, (size_t)rr, sizeof(int32_t), by_id);
+            nu = rr;
         }
     }
     *n_groups = ng;
-    free(a); free(cen); free(cl); free(sum); free(cand);
+    free(a); free(cs); free(cn); free(cl); free(sum); free(cand);
     return 0;
 }

@@ -14,7 +14,9 @@ raises AssertionError when the oracle disagrees with:
   quadratic;
 * the rewiring of Alg. 3 on a hand-checked layer, its tie rule, its invariants on random layers,
   the uniformity of its draws, and the published outputs of its generator;
-* the grouping of Alg. 2 on planted directions (exact groups) and planted clusters (recovered);
+* the grouping of Alg. 2 on planted directions (exact groups) and planted clusters (recovered),
+  against its brute-force statement with NumPy cosines, and its seed rule on near-duplicates;
+* the moments and bins of rewiring's random reinitialisation (Alg. 3's uniform law);
 * the adjoint identity <dY, Y - bias> = <dX, X> = <dW, W> (bilinearity);
 * exact one-hot gathers/scatters and the group-permutation invariance.
 """
@@ -492,6 +494,125 @@ def pin_rewire_uniform(o):
     assert counts.sum() > 1000 and chi2 < 25.0, f"new-feature ranks not uniform: {counts}, chi2 {chi2:.1f}"
 
 
+def pin_rewire_reinit_distribution(o):
+    """Alg. 3's random mode draws each reinitialised weight from Unif(-1/sqrt(F), 1/sqrt(F)): over
+    many pruned slots the values stay inside that interval, take both signs, reach both ends, have
+    mean 0 and variance 1/(3F) (the moments of that uniform law), and fill ten equal bins evenly."""
+    rng = np.random.default_rng(59)
+    K, G, F, H, rho = 400, 8, 16, 64, 0.5
+    idx = np.stack([np.sort(rng.choice(H, F, replace=False)) for _ in range(K)]).astype(np.int32)
+    W = (rng.random((K * G, F)) + 1.0).astype(np.float32)   # kept weights lie in [1, 2): not draws
+    idx2, W2, _, n, mask = o.rewire(idx, W, None, G, H, F32, rho, True, 2024)
+    vals = []
+    for k in range(K):
+        kept = set(int(idx[k, j]) for j in range(F) if not mask[k, j])
+        new = [p for p, f in enumerate(idx2[k]) if int(f) not in kept]
+        vals.append(W2[k * G:(k + 1) * G][:, new].reshape(-1))
+    v = np.concatenate(vals).astype(np.float64)
+    a = 1.0 / np.sqrt(F)
+    assert v.size == n * G and v.size > 20000
+    assert np.all(np.abs(v) <= a), "a reinitialised weight lies outside [-1/sqrt(F), 1/sqrt(F)]"
+    assert (v > 0).mean() > 0.45 and (v < 0).mean() > 0.45, "reinitialised weights must take both signs"
+    assert v.max() > 0.99 * a and v.min() < -0.99 * a, "draws must reach both ends of the interval"
+    sd_mean = np.sqrt(a * a / 3 / v.size)
+    assert abs(v.mean()) < 5 * sd_mean, f"mean {v.mean():.3g} is not 0"
+    assert abs(v.var() / (a * a / 3) - 1) < 0.05, f"variance {v.var():.4g} is not 1/(3F) = {a * a / 3:.4g}"
+    counts = np.histogram(v, bins=10, range=(-a, a))[0]
+    exp = v.size / 10
+    chi2 = float(((counts - exp) ** 2 / exp).sum())
+    assert chi2 < 30.0, f"reinitialised weights not uniform over ten bins: {counts}, chi2 {chi2:.1f}"
+
+
+def _cos_rows(E, s):
+    """fp64 cosine of every row of E with vector s (NumPy; independent of the oracle)."""
+    Ef = E.astype(np.float64)
+    sf = np.asarray(s, np.float64)
+    return (Ef @ sf) / (np.linalg.norm(Ef, axis=1) * np.linalg.norm(sf))
+
+
+def _brute_group(o, E, G, beta, iters, seed):
+    """Alg. 2 written out with NumPy cosines: spherical k-means whose centres are the normalised
+    means of their members (ties to the lower centre; an empty cluster keeps its centre), then per
+    cluster a seed plus its top-(G - 1) unassigned neighbours by cosine (ties to the lower label).
+    Random choices follow the documented counter draws of the generator (pinned separately)."""
+    E = np.asarray(E, np.int8)
+    N, D = E.shape
+    C = max(1, N // (beta * G))
+    perm = list(range(N))
+    for i in range(C):
+        j = i + o.splitmix64(seed, i) % (N - i)
+        perm[i], perm[j] = perm[j], perm[i]
+    mu = np.stack([E[perm[c]].astype(np.float64) for c in range(C)])
+    mu /= np.linalg.norm(mu, axis=1, keepdims=True)
+    Ef = E.astype(np.float64)
+
+    def assign():
+        return np.argmax(Ef @ mu.T, axis=1)   # the first maximum: the lower centre
+
+    for _ in range(iters):
+        cl = assign()
+        for c in range(C):
+            s = Ef[cl == c].sum(axis=0)
+            if (cl == c).any() and np.linalg.norm(s) > 0:
+                mu[c] = s / np.linalg.norm(s)
+    cl = assign()
+    order, gsize = [], []
+    for c in range(C):
+        un = [l for l in range(N) if cl[l] == c]
+        t = 0
+        while un:
+            s = un[o.splitmix64(seed, N + c * N + t) % len(un)]
+            t += 1
+            rest = [l for l in un if l != s]
+            cs = _cos_rows(E[rest], E[s]) if rest else np.zeros(0)
+            ranked = sorted(range(len(rest)), key=lambda i: (-cs[i], rest[i]))
+            grp = sorted([s] + [rest[i] for i in ranked[:G - 1]])
+            order += grp
+            gsize.append(len(grp))
+            un = sorted(set(un) - set(grp))
+    return np.array(order), np.array(gsize), cl
+
+
+def pin_group_bruteforce(o):
+    """Alg. 2 on small random int8 embeddings of uneven norms (so that a dot product and a cosine
+    rank differently) against its brute-force statement with NumPy cosines: identical clusters,
+    groups and group order, for several seeds and iteration counts, with exact duplicate rows."""
+    rng = np.random.default_rng(61)
+    for N, D, G, beta in ((40, 8, 4, 20), (240, 16, 4, 10), (300, 8, 8, 6)):
+        E = (rng.integers(-127, 128, (N, D)) * (0.1 + 0.9 * rng.random((N, 1)))).astype(np.int8)
+        E[np.abs(E).sum(axis=1) == 0, 0] = 1   # cosines need non-zero rows
+        E[5] = E[17]                        # an exact tie of cosines, broken by the lower label
+        for iters, seed in ((0, 3), (1, 0), (4, 11)):
+            order, gs, cl = o.group_labels(E, G, beta, iters, seed)
+            order_b, gs_b, cl_b = _brute_group(o, E, G, beta, iters, seed)
+            assert np.array_equal(cl, cl_b), f"N={N} iters={iters}: clusters differ from spherical k-means"
+            assert np.array_equal(gs, gs_b) and np.array_equal(order, order_b), \
+                f"N={N} iters={iters} seed={seed}: groups differ from the greedy cosine stage"
+
+
+def pin_group_seed_in_group(o):
+    """The seed always belongs to its own group (Section 3.1: a seed and its top-(G - 1) neighbours),
+    also for near-duplicate labels a, b whose int8 rounding makes a.b exceed b.b: with labels
+    {a, b, a} and G = 2, a seed b gives the group {b, the lower a}, a seed a gives {a, a}."""
+    rng = np.random.default_rng(67)
+    while True:
+        u = rng.standard_normal(16)
+        a = np.rint(127 * u / np.linalg.norm(u)).astype(np.int64)
+        w = u + rng.standard_normal(16) * 0.01
+        b = np.rint(127 * w / np.linalg.norm(w)).astype(np.int64)
+        if a @ b > b @ b and not np.array_equal(a, b):
+            break
+    E = np.stack([a, b, a]).astype(np.int8)
+    seen = set()
+    for seed in range(12):
+        order, gs, _ = o.group_labels(E, 2, 8, 0, seed)
+        first_seed = [0, 1, 2][o.splitmix64(seed, 3) % 3]
+        want = [0, 1] if first_seed == 1 else [0, 2]
+        assert list(gs) == [2, 1] and list(order[:2]) == want, f"seed {seed} (label {first_seed}): {order}"
+        seen.add(first_seed)
+    assert 1 in seen, "no draw picked the seed b"
+
+
 def _unit_int8(X):
     X = np.asarray(X, np.float64)
     return np.rint(127 * X / np.linalg.norm(X, axis=1, keepdims=True)).astype(np.int8)
@@ -552,4 +673,5 @@ ALL_PINS = [pin_fig2_gs, pin_fig2_ffi, pin_bruteforce, pin_duplicate_indices, pi
             pin_group_equals_expanded_ffi, pin_finite_differences, pin_adjoint_identity, pin_one_hot,
             pin_group_permutation, pin_label_ranges, pin_head, pin_bce_grad,
             pin_sgd_momentum, pin_splitmix64, pin_rewire_hand, pin_rewire_ties_and_noop, pin_rewire_invariants,
-            pin_rewire_uniform, pin_group_greedy, pin_group_planted]
+            pin_rewire_uniform, pin_rewire_reinit_distribution, pin_group_greedy, pin_group_planted,
+            pin_group_bruteforce, pin_group_seed_in_group]

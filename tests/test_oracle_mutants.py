@@ -58,7 +58,19 @@ MUTANTS = {
     "rewire_column_not_moved": ("tmp[p] = ld(W, l * F + j, dtype);", "tmp[p] = ld(W, l * F + p, dtype);"),
     "group_least_similar": ("if (x->sim != y->sim) return x->sim > y->sim ? -1 : 1;",
                             "if (x->sim != y->sim) return x->sim < y->sim ? -1 : 1;"),
-    "group_assign_argmin": ("if (v > bv) { bv = v; best = c; }", "if (v < bv) { bv = v; best = c; }"),
+    "group_assign_argmin": ("if (best < 0 || v > bv) { bv = v; best = c; }", "if (best < 0 || v < bv) { bv = v; best = c; }"),
+    "group_assign_raw_dot": ("const double v = (double)dot / cn[c];", "const double v = (double)dot;"),
+    "group_centre_int8": ("memcpy(cs + c * D, sum, (size_t)D * sizeof(int64_t));\n            cn[c] = nrm;",
+                          "for (int64_t d = 0; d < D; ++d) cs[c * D + d] = (int64_t)rint(127.0 * (double)sum[d] / nrm);\n"
+                          "            cn[c] = exact_norm(cs + c * D, D);"),
+    "group_sim_raw_dot": ("cand[nc].sim = (double)dot8(e, E + (int64_t)s * D, D) / sqrt((double)(ni * ns));",
+                          "cand[nc].sim = (double)dot8(e, E + (int64_t)s * D, D) + 0.0 * (double)(ni * ns);"),
+    "group_seed_index": ("const int32_t s = a[r];", "const int32_t s = a[nu - 1 - r];"),
+    "group_seed_tie_not_lower": ("return (x->id > y->id) - (x->id < y->id);\n}\n\nstatic int by_id",
+                                 "return (x->id < y->id) - (x->id > y->id);\n}\n\nstatic int by_id"),
+    "rewire_reinit_zero": ("v = (double)((float)((int64_t)(2 * n) - (1LL << 24)) * scale);", "v = 0.0 * (double)n;"),
+    "rewire_reinit_one_sided": ("(float)((int64_t)(2 * n) - (1LL << 24)) * scale", "(float)((int64_t)n) * scale"),
+    "rewire_reinit_scale_1_over_F": ("const float a = (float)(1.0 / sqrt((double)F));", "const float a = (float)(1.0 / (double)F);"),
     "group_centre_negated": ("for (int64_t d = 0; d < D; ++d) sum[d] += E[l * D + d]; }",
                              "for (int64_t d = 0; d < D; ++d) sum[d] -= E[l * D + d]; }"),
     "bf16_decode_shift": ("uint32_t u = ((uint32_t)((const uint16_t *)p)[i]) << 16;",
