@@ -161,7 +161,7 @@ int haste_sgd_momentum(int64_t n, int32_t dtype, const void *W, const float *gra
                        const haste_sgd_t *opt, void *W_next, void *stream);
 
 /*
- * Group-shared rewiring (Alg. 3; the discrete phase of the training loop, Section 3.4), in place:
+ * Group-shared rewiring (Alg. 3; the discrete phase of the alternating training loop, Section 3.3), in place:
  *   1. score[k, j] = sum over the G labels l of group k of |W[l, j]|, fp32, labels in order (the
  *      algorithm's mean, scaled by the common factor G, which orders the scores identically);
  *   2. prune the m = floor(K * F_in * rho) smallest scores over all groups, ties to the lower
@@ -193,25 +193,31 @@ typedef struct haste_group_opts {
 } haste_group_opts_t;
 
 /*
- * Semantic grouping of labels (Alg. 2), before training: coarse spherical k-means into C clusters,
- * then, inside each cluster, greedy groups of G: a random unassigned seed and its top-G
- * unassigned labels by similarity (the seed included), until the cluster is used up.
- *   - E [N, D] int8: unit label embeddings scaled by 127 (round(127 e / |e|)); similarities are
- *     exact integer dot products, so every decision below is exact.
- *   - k-means: centres start as the first C labels of a partial Fisher-Yates shuffle of [0, N)
- *     (swap partner of i: i + out(i) mod (N - i)); `iters` full Lloyd iterations follow (assign
- *     every label to its most similar centre, ties to the lower centre; move each non-empty
- *     cluster's centre to round-half-even(127 s / |s|) of its members' sum s, |s| in fp64), then a
- *     final assignment.  (The paper runs mini-batch k-means, a CPU economy; full passes of the
- *     [N, D] x [D, C] product are cheap on the GPU.)
+ * Semantic grouping of labels (Alg. 2; Section 3.1, "Label Grouping"), before training: coarse
+ * spherical k-means into C clusters, then, inside each cluster, greedy groups: a random unassigned
+ * seed together with its top-(G - 1) unassigned neighbours by cosine similarity, until the cluster
+ * is used up.  The seed always belongs to its own group.
+ *   - E [N, D] int8: label embeddings (unit vectors scaled by 127 and rounded); every row must be
+ *     non-zero (a precondition).  Similarity is the cosine of the stored rows.
+ *   - k-means: a centre is the normalised mean of its members, held exactly as the integer sum s
+ *     of their rows; a label e goes to the centre maximising e.s / |s| (its cosine up to the
+ *     label's own norm), formed in fp64 from the exact integer e.s and |s| = sqrt of the exact
+ *     |s|^2 rounded once, ties to the lower centre.  Centres start as the first C labels of a
+ *     partial Fisher-Yates shuffle of [0, N) (swap partner of i: i + out(i) mod (N - i)); `iters`
+ *     full Lloyd iterations follow (assign every label, then move every non-empty cluster's centre
+ *     to its members' sum; a zero sum keeps the centre), then a final assignment.  (The paper runs
+ *     mini-batch k-means, a CPU economy; full passes of the [N, D] x [D, C] product are cheap on
+ *     the GPU.)
  *   - groups: cluster by cluster; the t-th seed of cluster c is the (out(N + c N + t) mod
- *     n_unassigned)-th unassigned member in ascending label order; top-G ties go to the lower
- *     label; a group lists its labels in ascending order.  The last group of a cluster may have
- *     fewer than G labels (the layout needs L % G == 0: pad with zero-weight labels).
+ *     n_unassigned)-th unassigned member in ascending label order; the other members are the
+ *     unassigned labels of largest cosine (e_i.e_s) / sqrt(|e_i|^2 |e_s|^2) in fp64, ties to the
+ *     lower label; a group lists its labels in ascending order.  The last group of a cluster may
+ *     have fewer than G labels (the layout needs L % G == 0: pad with zero-weight labels).
  *   out(i) is SplitMix64 (Steele, Lea and Flood, 2014) output i of the stream seeded with seed.
  * order [N] int32 receives the labels group after group; gsize [N] int32 the group sizes (first
  * *n_groups entries); n_groups is a DEVICE int64; cluster [N] int32 (device, or NULL) the final
- * cluster of each label.  D % 16 == 0, D <= 1024, N < 2^24.
+ * cluster of each label.  D % 16 == 0, D <= 1024, N < 2^24, N D < 2^31, 4 C D < 2^31; otherwise
+ * HASTE_ERR_UNSUPPORTED.
  * ws: haste_group_workspace_bytes(N, D, opts) bytes.
  */
 int haste_group_labels(int64_t N, int64_t D, const int8_t *E, const haste_group_opts_t *opts, int32_t *order,
@@ -302,8 +308,10 @@ size_t haste_workspace_bytes(const haste_desc_t *desc, int op);
 size_t haste_head_workspace_bytes(int64_t B, int64_t F_s, int64_t H, int32_t dtype);
 
 /*
- * Debug check of the idx precondition: *n_bad_rows (device int32, overwritten) receives the
- * number of rows of idx[n_rows, F_in] that are not strictly increasing within [0, F_s).
+ * Debug check of the idx precondition (Section 3.1: each group's support I_k is a set of exactly
+ * F_in input features, a subset of the F_s features of h; stored sorted, a set is a strictly
+ * increasing row): *n_bad_rows (device int32, overwritten) receives the number of rows of
+ * idx[n_rows, F_in] that are not strictly increasing within [0, F_s).
  * n_rows = L/G (or L when G = 1).
  */
 int haste_validate_idx(const haste_desc_t *desc, const int32_t *idx, int32_t *n_bad_rows,

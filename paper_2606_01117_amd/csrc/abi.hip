@@ -58,6 +58,20 @@ haste::TailArgs targs(const haste_desc_t *d) { return haste::TailArgs{d->B, d->F
 
 hipStream_t as_stream(void *s) { return reinterpret_cast<hipStream_t>(s); }
 
+}  // namespace
+
+namespace haste {
+int report(int code, const char *fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof g_err, fmt, ap);
+    va_end(ap);
+    return code;
+}
+}  // namespace haste
+
+namespace {
+
 #define TRY(x)                      \
     do {                            \
         int _rc = (x);              \
@@ -369,8 +383,9 @@ int haste_rewire(const haste_desc_t *d, int32_t *idx, void *W, float *m, double 
 static int check_group(int64_t N, int64_t D, const haste_group_opts_t *o) {
     if (!o) return fail(HASTE_ERR_INVALID, "opts is NULL");
     if (o->beta < 1 || o->iters < 0) return fail(HASTE_ERR_INVALID, "beta must be >= 1 and iters >= 0");
-    if (!haste::group_supported(N, D, o->G))
-        return fail(HASTE_ERR_UNSUPPORTED, "grouping needs 0 < N < 2^24, D a multiple of 16 up to 1024, 1 <= G <= 256");
+    if (!haste::group_supported(N, D, o->G, o->beta))
+        return fail(HASTE_ERR_UNSUPPORTED, "grouping needs 0 < N < 2^24, D a multiple of 16 up to 1024, 1 <= G <= 256, "
+                                           "N D < 2^31 and 4 C D < 2^31");
     return HASTE_OK;
 }
 

@@ -130,6 +130,9 @@ struct TailArgs {
     int32_t dtype;
 };
 
+// records the calling thread's haste_last_error() message and returns code (abi.hip)
+int report(int code, const char *fmt, ...);
+
 // tail, MFMA (bf16)
 bool fwd_mfma_supported(const TailArgs &a);
 hipError_t fwd_mfma(const TailArgs &a, const void *X, const int32_t *idx, const void *W, const float *bias,
@@ -172,7 +175,7 @@ size_t rewire_ws(const TailArgs &a);
 hipError_t rewire(const TailArgs &a, int32_t *idx, void *W, float *m, int64_t n_prune, int init_random, uint64_t seed,
                   void *ws, hipStream_t s);
 // semantic grouping of labels (Alg. 2) on int8 unit embeddings
-bool group_supported(int64_t N, int64_t D, int64_t G);
+bool group_supported(int64_t N, int64_t D, int64_t G, int64_t beta);
 size_t group_ws(int64_t N, int64_t D, int64_t G, int64_t beta);
 hipError_t group_labels(int64_t N, int64_t D, const int8_t *E, int64_t G, int64_t beta, int64_t iters, uint64_t seed,
                         int32_t *order, int32_t *gsize, int64_t *n_groups, int32_t *cluster, void *ws, hipStream_t s);

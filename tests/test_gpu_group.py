@@ -1,8 +1,11 @@
 """GPU parity of haste_group_labels (Alg. 2, through the C ABI) against the CPU oracle.
 
-Similarities are exact integer dot products of int8 unit embeddings, and the draws come from the
-same counter-based generator on both sides, so the clusters, the groups and their order must
-match the oracle exactly.  At the size of the 655K-label tail (too slow for the oracle) the
+Both sides take every decision in fp64 from exact integers (a centre is its members' exact sum;
+a label's score for a centre is e.s / |s|; a greedy similarity is the cosine of two int8 rows),
+and the draws come from the same counter-based generator on both sides, so the clusters, the
+groups and their order must match the oracle exactly.  The cases include rows of uneven norm
+(where a dot product and a cosine rank differently), near-duplicate rows, and clusters large
+enough that their sums need all four digit planes of the int8 products.  At the size of the 655K-label tail (too slow for the oracle) the
 output is checked for what holds at any size: a partition into groups of G (the last of each
 cluster may be short), each group inside one cluster.
 """
@@ -56,13 +59,39 @@ def _run(hs, E, G, beta, iters, seed):
     return order.cpu().numpy(), gsize.cpu().numpy()[:n], cl.cpu().numpy()
 
 
+def uneven(N, D, rng):
+    """int8 rows of uneven norm with exact and near duplicates (non-zero rows)."""
+    E = (rng.integers(-127, 128, (N, D)) * (0.1 + 0.9 * rng.random((N, 1)))).astype(np.int8)
+    E[np.abs(E).astype(np.int32).sum(axis=1) == 0, 0] = 1
+    E[1::7] = E[0:-1:7]                                                  # exact duplicates
+    E[3::11] = np.clip(E[2:-1:11].astype(np.int32) + rng.integers(-1, 2, E[2:-1:11].shape), -127, 127)
+    return E
+
+
+def two_axes(n, D, n_mid, rng):
+    """Two clusters of n labels near the axes e_0 and e_1, plus n_mid labels between them: the
+    clusters' sums reach 127 n (four digit planes from n = 66,052) and the labels in between are
+    decided by the exact scores."""
+    E = np.zeros((2 * n + n_mid, D), np.int64)
+    E[:n, 0] = 127
+    E[n:2 * n, 1] = 127
+    E[:2 * n, 2:] = rng.integers(-3, 4, (2 * n, D - 2))
+    t = rng.random(n_mid) * 0.2 + 0.4
+    E[2 * n:, 0] = np.rint(127 * np.cos(t * np.pi / 2))
+    E[2 * n:, 1] = np.rint(127 * np.sin(t * np.pi / 2))
+    E[2 * n:, 2:] = rng.integers(-2, 3, (n_mid, D - 2))
+    return E[rng.permutation(E.shape[0])].astype(np.int8)
+
+
 CASES = [
-    # name, N, D, planted clusters (0: isotropic), G, beta, iters
+    # name, N, D, planted clusters (0: isotropic, -1: uneven norms, -2: two axes), G, beta, iters
     ("planted_2048_d64", 2048, 64, 8, 16, 16, 8),
     ("random_5000_d128", 5000, 128, 0, 32, 4, 4),
     ("d48_tail_chunk", 3000, 48, 20, 16, 8, 5),
     ("one_cluster", 300, 32, 5, 8, 64, 3),
     ("planted_50k_d256", 50000, 256, 200, 32, 16, 5),
+    ("uneven_norms_3000_d32", 3000, 32, -1, 8, 8, 4),
+    ("two_axes_141k_d16", 141000, 16, -2, 256, 275, 2),
 ]
 
 
@@ -71,7 +100,11 @@ def test_group_exact(hs, orc, case):
     name, N, D, P, G, beta, iters = case
     say(f"[group] {name}: N={N} D={D} G={G} beta={beta} iters={iters}")
     rng = np.random.default_rng(N + D)
-    if P:
+    if P == -1:
+        E = uneven(N, D, rng)
+    elif P == -2:
+        E = two_axes(70000, D, N - 140000, rng)
+    elif P:
         E = planted(N, D, P, rng)
     else:
         X = rng.standard_normal((N, D))
