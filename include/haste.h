@@ -127,6 +127,27 @@ int haste_fwd_bce(const haste_desc_t *desc, const void *X, const int32_t *idx, c
                   float *dbias, int beta, void *ws, size_t ws_bytes, void *stream);
 
 /*
+ * For callers that cannot allocate (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid allocation): haste_fwd_bce with its scratch in a device array the library owns, so
+ * the call takes no workspace and allocates nothing.  Arguments, results and errors are those of
+ * haste_fwd_bce, bit for bit, without ws / ws_bytes.
+ * Limit: the layer's scratch, haste_workspace_bytes(desc, HASTE_OP_FWD_BCE) (2 F_s round_up(B, 32)
+ * + 256 bytes on the matrix-core path), must not exceed haste_fwd_bce_static_max_bytes() (8 MiB);
+ * a larger layer gives HASTE_ERR_UNSUPPORTED and launches nothing.
+ * Each GPU holds one such array for the life of the process, shared by every call on that GPU and
+ * left holding the last call's data (each call writes all it reads): calls that overlap on one GPU
+ * (other streams or threads) race on it, and the caller must serialise them.  The array's device
+ * address is looked up on the first call on each device; the current device must be the one the
+ * stream belongs to.
+ */
+int haste_fwd_bce_static(const haste_desc_t *desc, const void *X, const int32_t *idx, const void *W,
+                         const float *bias, const int32_t *pos, int32_t P, void *dY, float *dW,
+                         float *dbias, int beta, void *stream);
+
+/* Bytes of scratch haste_fwd_bce_static holds per device (its limit). */
+size_t haste_fwd_bce_static_max_bytes(void);
+
+/*
  * haste_fwd_bce followed by one step of SGD with momentum on W (the classification layer's
  * optimizer, Section 4), with the step applied where the backward-weight product is formed, so
  * that dW never reaches memory:

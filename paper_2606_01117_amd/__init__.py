@@ -55,6 +55,7 @@ def _load() -> ctypes.CDLL:
         "haste_bwd_w": [D, P, P, P, P, P, ctypes.c_int, P, SZ, P],
         "haste_bwd_x": [D, P, P, P, P, ctypes.c_int, P, SZ, P],
         "haste_fwd_bce": [D, P, P, P, P, P, I32, P, P, P, ctypes.c_int, P, SZ, P],
+        "haste_fwd_bce_static": [D, P, P, P, P, P, I32, P, P, P, ctypes.c_int, P],
         "haste_bce_grad": [I64, I64, I32, P, P, I32, P, P],
         "haste_fwd_bce_sgd": [D, P, P, P, P, P, I32, P, P, ctypes.POINTER(haste_sgd_t), P, P, P, SZ, P],
         "haste_sgd_momentum": [I64, I32, P, P, P, ctypes.POINTER(haste_sgd_t), P, P],
@@ -79,6 +80,8 @@ def _load() -> ctypes.CDLL:
     lib.haste_head_workspace_bytes.restype = SZ
     lib.haste_group_workspace_bytes.argtypes = [I64, I64, ctypes.POINTER(haste_group_opts_t)]
     lib.haste_group_workspace_bytes.restype = SZ
+    lib.haste_fwd_bce_static_max_bytes.argtypes = []
+    lib.haste_fwd_bce_static_max_bytes.restype = SZ
     for name in ("haste_status_str", "haste_last_error", "haste_version"):
         getattr(lib, name).restype = ctypes.c_char_p
     lib.haste_status_str.argtypes = [ctypes.c_int]
@@ -88,7 +91,8 @@ def _load() -> ctypes.CDLL:
 lib = _load()
 
 # every symbol the header declares
-EXPORTS = ("haste_fwd", "haste_bwd_w", "haste_bwd_x", "haste_fwd_bce", "haste_fwd_bce_sgd", "haste_sgd_momentum",
+EXPORTS = ("haste_fwd", "haste_bwd_w", "haste_bwd_x", "haste_fwd_bce", "haste_fwd_bce_static",
+           "haste_fwd_bce_static_max_bytes", "haste_fwd_bce_sgd", "haste_sgd_momentum",
            "haste_rewire", "haste_group_labels", "haste_group_workspace_bytes", "haste_bce_grad", "haste_head_fwd",
            "haste_head_fwd_bce", "haste_head_bwd", "haste_tail_step", "haste_tail_step_sgd", "haste_workspace_bytes", "haste_head_workspace_bytes", "haste_validate_idx", "haste_debug_gather", "haste_status_str",
            "haste_last_error", "haste_version")
@@ -186,6 +190,16 @@ def haste_fwd_bce(desc, X, idx, W, bias, pos, dY, dW=None, dbias=None, beta=0, w
     p, n = _ws(ws)
     _check(lib.haste_fwd_bce(ctypes.byref(desc), _ptr(X), _ptr(idx), _ptr(W), _ptr(bias), _ptr(pos), _npos(pos),
                              _ptr(dY), _ptr(dW), _ptr(dbias), int(beta), p, n, _stream(stream)))
+
+
+def haste_fwd_bce_static(desc, X, idx, W, bias, pos, dY, dW=None, dbias=None, beta=0, stream=None):
+    """haste_fwd_bce with the library's own per-device scratch (no workspace, allocates nothing)."""
+    _check(lib.haste_fwd_bce_static(ctypes.byref(desc), _ptr(X), _ptr(idx), _ptr(W), _ptr(bias), _ptr(pos),
+                                    _npos(pos), _ptr(dY), _ptr(dW), _ptr(dbias), int(beta), _stream(stream)))
+
+
+def haste_fwd_bce_static_max_bytes() -> int:
+    return int(lib.haste_fwd_bce_static_max_bytes())
 
 
 def haste_tail_step(desc, X, idx, W, bias, pos, dY, dW, dbias, beta, dX, beta_dx, ws=None, stream=None):

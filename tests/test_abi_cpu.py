@@ -166,3 +166,16 @@ def test_loss_optimizer_rewire_group_arguments_checked(hs):
                                      None) == 2
     assert hs.haste_group_workspace_bytes(1000, 128, hs.group_opts(300, 16, 5, 1)) == 0
     assert hs.haste_group_workspace_bytes(1000, 128, g) > 0
+
+
+def test_fwd_bce_static_limits(hs):
+    """The no-workspace variant refuses a layer whose scratch exceeds its per-device array, and
+    reports invalid descriptors as haste_fwd_bce does, before any device call."""
+    assert hs.haste_fwd_bce_static_max_bytes() == 8 << 20
+    big = hs.make_desc(8192, 768, 4096, 32, 64, hs.HASTE_DTYPE_BF16)     # 2 * 768 * 8192 + 256 > 8 MiB
+    assert hs.haste_workspace_bytes(big, hs.HASTE_OP_FWD_BCE) > 8 << 20
+    rc = hs.lib.haste_fwd_bce_static(ctypes.byref(big), FAKE, FAKE, FAKE, None, None, 0, FAKE, FAKE, None, 0, None)
+    assert rc == 2 and b"8388608" in hs.lib.haste_last_error()
+    bad = _desc(hs, L=30)                                               # L % G != 0
+    rc = hs.lib.haste_fwd_bce_static(ctypes.byref(bad), FAKE, FAKE, FAKE, None, None, 0, FAKE, FAKE, None, 0, None)
+    assert rc == 1
