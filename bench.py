@@ -38,6 +38,7 @@ HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16 MFMA
 PROFILES = os.path.join(ROOT, "profiles")
 COPY_BYTES = 1 << 30            # plain device copy used to calibrate the HBM byte counters
+FLUSH_BYTES = 512 << 20         # written before each timed step of a working set the MALL could hold
 
 # kernels launched by each call (patterns matched at the start of rocprofv3's kernel names; the
 # fused kernel's third template argument is its output: 1 stores dW, 2 applies the momentum step)
@@ -78,6 +79,8 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-bottleneck", action="store_true")
     p.add_argument("--grouping", action="store_true", help="also time the label grouping of Alg. 2 (655K labels)")
+    p.add_argument("--no-gsweep", action="store_true",
+                   help="skip the group-size sweep (G = 1, 4, 16, 64 on the 655K-label layer, with its bottleneck)")
     p.add_argument("--copy-calibration", action="store_true",
                    help="after the timed steps, run a plain %d-byte device copy (for counter calibration)" % COPY_BYTES)
     p.add_argument("--summarize-trace", metavar="DB",
@@ -377,6 +380,11 @@ def main():
     separate.append(("bwd_x", lambda: hs.haste_bwd_x(desc, idxd, Wd, dYd, dX, 0, ws_x)))
     separate += head_back(dYhd) if wl.H else []
 
+    # a working set that fits the 256 MB MALL would be timed warm: flush it before every timed step
+    # by writing a 512 MB buffer (outside the events that time the step)
+    mall_flush = call_cost(wl, 2 if is_bf else 4, 0)["fwd"][0] + wl.B * wl.L * (2 if is_bf else 4) < (512 << 20)
+    flush_buf = torch.empty(FLUSH_BYTES // 4, dtype=torch.float32, device=dev) if mall_flush else None
+
     def timed(calls):
         """K steps after W warm-up steps; events between the calls on the launch stream."""
         for _ in range(args.warmup):
@@ -387,6 +395,8 @@ def main():
         torch.cuda.synchronize()
         w0 = time.perf_counter()
         for s in range(args.steps):
+            if flush_buf is not None:
+                flush_buf.fill_(float(s))
             evs[s][0].record(stream)
             for i, (_, fn) in enumerate(calls):
                 fn()
@@ -442,6 +452,7 @@ def main():
         "step_hbm_frac": round(step_bytes / step_ms / 1e6 / HBM_PEAK_GBPS, 4),
         "step_mfma_pct": round(100 * step_flops / (step_ms / 1e3) / (MFMA_BF16_PEAK_TFLOPS * 1e12), 2),
         "wall_ms_per_step": round(wall_ms, 4),
+        "mall_flush": bool(mall_flush),
         "per_call": detail(per_call),
         "roofline": roof,
         "unfused_training_step": {"ms": round(unf_ms, 4), "per_call": detail(unf_per),
@@ -518,6 +529,9 @@ def main():
                            "iters": giters, "groups": int(g_n.item()),
                            "what": "haste_group_labels (Alg. 2) on planted int8 unit embeddings"}
         del Eg, g_order, g_size, ws_g
+    if not args.no_gsweep and wl.name == "l2949k_g32_h65k":
+        print("[bench] group-size sweep", file=sys.stderr, flush=True)
+        out["gsweep"] = gsweep(args, hs, synth, torch, np)
     if args.copy_calibration:
         src = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device=dev).fill_(1.0)
         dst = torch.empty_like(src)
@@ -529,6 +543,69 @@ def main():
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(wl, X, idx, W, dY, Wh, dYh, synth.pos_matrix(tail_pairs, wl.B, n_pos))
     print(json.dumps(out), flush=True)
+
+
+def gsweep(args, hs, synth, torch, np):
+    """The group-size sweep (Fig. 4's axis) on the 655K-label layer (B = 256, F_s = 768, F_in = 64):
+    for G = 1 (standard fixed fan-in), 4, 16 and 64 the training pass of the tail (haste_tail_step)
+    and the separate calls on a fixed dY, with the FLOPs-matched dense bottleneck timed beside them.
+    X, W and dY are shared by every G; each G has its own supports."""
+    dev = torch.device("cuda:0")
+    base = synth.WORKLOADS["gsweep_g16"]
+    up = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16) if a.dtype == np.uint16 else
+                                    np.ascontiguousarray(a)).to(dev)
+    Xd, Wd = up(synth.draw_X(base)), up(synth.draw_W(base))
+    pos = synth.draw_positives(base)
+    perm = synth.draw_perm(base)
+    dYd = up(synth.draw_dY(base, positives=pos, perm=perm))
+    tail_pairs, _ = synth.positive_neurons(base, pos, perm)
+    posd = up(synth.pos_matrix(tail_pairs, base.B, pos.shape[1]))
+    B, F_s, L, F_in = base.B, base.F_s, base.L, base.F_in
+    Y = torch.empty((B, L), dtype=torch.int16, device=dev)
+    dYt = torch.empty((B, L), dtype=torch.int16, device=dev)
+    dW = torch.empty((L, F_in), dtype=torch.float32, device=dev)
+    dX = torch.empty((B, F_s), dtype=torch.float32, device=dev)
+    st = torch.cuda.current_stream()
+
+    def time_it(fns, n):
+        for _ in range(max(1, args.warmup)):
+            for f in fns:
+                f()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(st)
+        for _ in range(n):
+            for f in fns:
+                f()
+        e1.record(st)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n
+
+    n = max(3, min(args.steps, 10))
+    res = {}
+    for G in (1, 4, 16, 64):
+        wl = synth.WORKLOADS[f"gsweep_g{G}"]
+        idxd = up(synth.draw_idx(wl))
+        desc = hs.make_desc(B, F_s, L, G, F_in, hs.HASTE_DTYPE_BF16)
+        ws_t = hs.workspace(hs.haste_workspace_bytes(desc, hs.HASTE_OP_TAIL_STEP))
+        ws_w = hs.workspace(hs.haste_workspace_bytes(desc, hs.HASTE_OP_BWD_W))
+        ws_x = hs.workspace(hs.haste_workspace_bytes(desc, hs.HASTE_OP_BWD_X))
+        step = time_it([lambda: hs.haste_tail_step(desc, Xd, idxd, Wd, None, posd, dYt, dW, None, 0, dX, 0, ws_t)], n)
+        f = time_it([lambda: hs.haste_fwd(desc, Xd, idxd, Wd, None, Y)], n)
+        w = time_it([lambda: hs.haste_bwd_w(desc, Xd, idxd, dYd, dW, None, 0, ws_w)], n)
+        x = time_it([lambda: hs.haste_bwd_x(desc, idxd, Wd, dYd, dX, 0, ws_x)], n)
+        res[f"G{G}"] = {"tail_step_ms": round(step, 4), "fwd_ms": round(f, 4), "bwd_w_ms": round(w, 4),
+                        "bwd_x_ms": round(x, 4), "separate_ms": round(f + w + x, 4)}
+        del idxd, ws_t, ws_w, ws_x
+    bn = bottleneck(base, Xd, Wd, dYd, args)
+    res["dense_bottleneck_ms"] = bn["ms"]
+    for G in (1, 4, 16, 64):
+        res[f"G{G}"]["separate_vs_bottleneck"] = round(res[f"G{G}"]["separate_ms"] / bn["ms"], 3)
+    res["what"] = ("655K-label layer, B=256, F_s=768, F_in=64, bf16: haste_tail_step (forward + BCE gradient + "
+                   "backward-weight + backward-feature) and the separate fwd / bwd_w / bwd_x calls on a fixed dY "
+                   "per group size (G=1 is standard fixed fan-in); the dense bottleneck is [256,64]x[64,655360] "
+                   "fwd + dW + dX with torch.matmul")
+    return res
 
 
 def bottleneck(wl, Xd, Wd, dYd, args):
