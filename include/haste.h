@@ -117,9 +117,12 @@ int haste_bwd_x(const haste_desc_t *desc, const int32_t *idx, const void *W, con
  * pos[B, P] int32 holds each row's positive tail labels as column ids; entries outside [0, L)
  * (e.g. -1 padding) are ignored and a repeated id counts once.  P >= 0; pos may be NULL when
  * P == 0.  bias as in haste_fwd; beta is 0 (overwrite) or 1 (accumulate).
- * bf16 layers whose groups are whole 16-label tiles, with F_s <= 768 and P <= 64, run one fused
- * kernel (the logits never reach memory).  Other layers run haste_fwd into dY, the gradient in
- * place (for bf16 the sigmoid then sees the logits rounded to bf16), and haste_bwd_w.
+ * bf16 layers whose groups are whole 16-label tiles, with F_s <= 1024, run one fused kernel (the
+ * logits never reach memory), for any number of positives per row: rows of more than 64 are first
+ * bucketed by workgroup and batch slab in the workspace, whose queried size provides for up to
+ * 1024 per row (2 F_s round_up(B, 32) + 8 (L B / 512) + 4 B P bytes about; a larger P fuses when
+ * ws holds that much, else composes).  Other layers run haste_fwd into dY, the gradient in place
+ * (for bf16 the sigmoid then sees the logits rounded to bf16), and haste_bwd_w.
  * ws: haste_workspace_bytes(desc, HASTE_OP_FWD_BCE) bytes.
  */
 int haste_fwd_bce(const haste_desc_t *desc, const void *X, const int32_t *idx, const void *W,
@@ -131,9 +134,10 @@ int haste_fwd_bce(const haste_desc_t *desc, const void *X, const int32_t *idx, c
  * that forbid allocation): haste_fwd_bce with its scratch in a device array the library owns, so
  * the call takes no workspace and allocates nothing.  Arguments, results and errors are those of
  * haste_fwd_bce, bit for bit, without ws / ws_bytes.
- * Limit: the layer's scratch, haste_workspace_bytes(desc, HASTE_OP_FWD_BCE) (2 F_s round_up(B, 32)
- * + 256 bytes on the matrix-core path), must not exceed haste_fwd_bce_static_max_bytes() (8 MiB);
- * a larger layer gives HASTE_ERR_UNSUPPORTED and launches nothing.
+ * Limit: the call's scratch (the X^T copy, 2 F_s round_up(B, 32) + 256 bytes on the matrix-core
+ * path, plus on the fused kernel's shapes the bucketed positives of rows of more than 64) must not
+ * exceed haste_fwd_bce_static_max_bytes() (8 MiB); a larger call gives HASTE_ERR_UNSUPPORTED and
+ * launches nothing.
  * Each GPU holds one such array for the life of the process, shared by every call on that GPU and
  * left holding the last call's data (each call writes all it reads): calls that overlap on one GPU
  * (other streams or threads) race on it, and the caller must serialise them.  The array's device
@@ -159,8 +163,8 @@ size_t haste_fwd_bce_static_max_bytes(void);
  * gradient output as in haste_fwd_bce (the bias's own step is a haste_sgd_momentum call).
  * The fp32 arithmetic of the step is that of haste_sgd_momentum, so the result equals
  * haste_fwd_bce + haste_sgd_momentum bit for bit.  Layers outside the fused kernel's shapes (those
- * of haste_fwd_bce, with F_s <= 768) run exactly that composition, with dW in ws; on the fused
- * shapes more than 64 positives per row is HASTE_ERR_UNSUPPORTED (compose the two calls instead).
+ * of haste_fwd_bce) run exactly that composition, with dW in ws.  On the fused shapes rows of more
+ * than 1024 positives need more workspace than the query gives (HASTE_ERR_WORKSPACE names it).
  * B == 0 applies the step with a zero gradient.
  * ws: haste_workspace_bytes(desc, HASTE_OP_FWD_BCE_SGD) bytes.
  */

@@ -106,8 +106,11 @@ size_t haste_workspace_bytes(const haste_desc_t *d, int op) {
         case HASTE_OP_FWD: return 0;
         case HASTE_OP_BWD_W: return haste::bwd_w_mfma_supported(a) ? haste::bwd_w_mfma_ws(a) : 0;
         case HASTE_OP_BWD_X: return haste::bwd_x_mfma_supported(a) ? haste::bwd_x_mfma_ws(a) : haste::bwd_x_valu_ws(a);
-        // the fused kernel and the backward-weight kernel stage the same X^T copy
-        case HASTE_OP_FWD_BCE: return haste::bwd_w_mfma_supported(a) ? haste::bwd_w_mfma_ws(a) : 0;
+        // the fused kernel and the backward-weight kernel stage the same X^T copy; the fused kernel
+        // also buckets rows of many positives (provided for up to kFusedPosWs per row)
+        case HASTE_OP_FWD_BCE:
+            if (haste::fwd_bce_mfma_supported(a, haste::kFusedPosWs)) return haste::fwd_bce_mfma_ws(a, haste::kFusedPosWs);
+            return haste::bwd_w_mfma_supported(a) ? haste::bwd_w_mfma_ws(a) : 0;
         // the composed form also keeps dW in the workspace (after the X^T copy)
         case HASTE_OP_REWIRE: return haste::rewire_supported(a) ? haste::rewire_ws(a) : 0;
         // backward-feature's region (partials, transposed weights, supports), then the fused kernel's
@@ -118,8 +121,9 @@ size_t haste_workspace_bytes(const haste_desc_t *d, int op) {
             return (size_t)haste::round_up((int64_t)haste_workspace_bytes(d, HASTE_OP_BWD_X), 256) +
                    haste_workspace_bytes(d, HASTE_OP_FWD_BCE_SGD);
         case HASTE_OP_FWD_BCE_SGD:
+            if (haste::fwd_bce_mfma_supported(a, haste::kFusedPosWs)) return haste::fwd_bce_mfma_ws(a, haste::kFusedPosWs);
             return (haste::bwd_w_mfma_supported(a) ? haste::bwd_w_mfma_ws(a) : 0) +
-                   (haste::fwd_bce_mfma_supported(a, 0) ? 0 : (size_t)haste::round_up(a.L * a.F_in * 4, 256));
+                   (size_t)haste::round_up(a.L * a.F_in * 4, 256);
     }
     return 0;
 }
@@ -212,7 +216,7 @@ int haste_tail_step(const haste_desc_t *d, const void *X, const int32_t *idx, co
     if (need && (!ws || ws_bytes < need))
         return fail(HASTE_ERR_WORKSPACE, "haste_tail_step needs %zu workspace bytes, got %zu", need, ws ? ws_bytes : 0);
     const size_t xoff = (size_t)haste::round_up((int64_t)haste_workspace_bytes(d, HASTE_OP_BWD_X), 256);
-    if (a.L > 0 && a.B > 0 && dW && dX && haste::tail_step_fused(a, P)) {
+    if (a.L > 0 && a.B > 0 && dW && dX && haste::tail_step_fused(a, P) && ws_bytes >= haste::tail_step_ws(a, P)) {
         TRY(need_ptr(X, "X"));
         TRY(need_ptr(idx, "idx"));
         TRY(need_ptr(W, "W"));
@@ -267,7 +271,9 @@ int haste_fwd_bce(const haste_desc_t *d, const void *X, const int32_t *idx, cons
     if (need && (!ws || ws_bytes < need))
         return fail(HASTE_ERR_WORKSPACE, "haste_fwd_bce needs %zu workspace bytes, got %zu", need, ws ? ws_bytes : 0);
     if (need) TRY(need_ptr(ws, "ws"));
-    if (haste::fwd_bce_mfma_supported(a, P))
+    // fused where the shape allows it and the workspace also holds the bucketed positives of long
+    // rows (the query's size does for up to kFusedPosWs per row)
+    if (haste::fwd_bce_mfma_supported(a, P) && ws_bytes >= haste::fwd_bce_mfma_ws(a, P))
         return hip_status(haste::fwd_bce_mfma(a, X, idx, W, bias, P > 0 ? pos : nullptr, P, dY, dW, dbias, beta, ws, s),
                           "haste_fwd_bce");
     // composed: logits into dY, the gradient in place, then the backward-weight product
@@ -332,21 +338,21 @@ int haste_fwd_bce_sgd(const haste_desc_t *d, const void *X, const int32_t *idx, 
     if (bias && !aligned16(bias)) return fail(HASTE_ERR_INVALID, "bias is not 16-byte aligned");
     if (a.B * haste::cdiv(a.L, 2048) >= ((int64_t)1 << 31))
         return fail(HASTE_ERR_UNSUPPORTED, "B * L too large for the gradient kernel's grid");
-    // the fused kernel's shapes need only the X^T copy; others keep dW in the workspace too
-    const bool fused_shape = haste::fwd_bce_mfma_supported(a, 0);
+    // the fused kernel's shapes need the X^T copy (and the bucketed positives of rows of more than
+    // 64); others keep dW in the workspace too
+    const bool fused_shape = haste::fwd_bce_mfma_supported(a, P);
     const size_t xws = haste::bwd_w_mfma_supported(a) ? haste::bwd_w_mfma_ws(a) : 0;
-    const size_t need = xws + (fused_shape ? 0 : (size_t)haste::round_up(a.L * a.F_in * 4, 256));
+    const size_t need = fused_shape ? haste::fwd_bce_mfma_ws(a, P) : xws + (size_t)haste::round_up(a.L * a.F_in * 4, 256);
     if (a.B == 0) {  // no rows: a zero gradient, the step still decays the velocity and the weights
         if (dbias) TRY(hip_status(haste::fill_f32(dbias, a.L, 0.0f, s), "haste_fwd_bce_sgd"));
         return hip_status(haste::sgd_momentum(a.L * a.F_in, a.dtype, W, nullptr, m, *opt, W_next, s),
                           "haste_fwd_bce_sgd");
     }
     if (need && (!ws || ws_bytes < need))
-        return fail(HASTE_ERR_WORKSPACE, "haste_fwd_bce_sgd needs %zu workspace bytes, got %zu", need, ws ? ws_bytes : 0);
+        return fail(HASTE_ERR_WORKSPACE, "haste_fwd_bce_sgd needs %zu workspace bytes for rows of %d positives, got %zu",
+                    need, (int)P, ws ? ws_bytes : 0);
     if (need) TRY(need_ptr(ws, "ws"));
     if (fused_shape) {
-        if (!haste::fwd_bce_mfma_supported(a, P))
-            return fail(HASTE_ERR_UNSUPPORTED, "more than 64 positives per row; use haste_fwd_bce and haste_sgd_momentum");
         return hip_status(haste::fwd_bce_sgd_mfma(a, X, idx, W, bias, P > 0 ? pos : nullptr, P, dY, dbias, *opt, m,
                                                   W_next, ws, s),
                           "haste_fwd_bce_sgd");
@@ -522,7 +528,7 @@ int haste_tail_step_sgd(const haste_desc_t *d, const void *X, const int32_t *idx
         return fail(HASTE_ERR_WORKSPACE, "haste_tail_step_sgd needs %zu workspace bytes, got %zu", need,
                     ws ? ws_bytes : 0);
     const size_t xoff = (size_t)haste::round_up((int64_t)haste_workspace_bytes(d, HASTE_OP_BWD_X), 256);
-    if (a.L > 0 && a.B > 0 && dX && haste::tail_step_fused(a, P)) {
+    if (a.L > 0 && a.B > 0 && dX && haste::tail_step_fused(a, P) && ws_bytes >= haste::tail_step_ws(a, P)) {
         TRY(need_ptr(X, "X"));
         TRY(need_ptr(idx, "idx"));
         TRY(need_ptr(W, "W"));

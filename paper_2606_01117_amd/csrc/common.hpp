@@ -144,7 +144,7 @@ hipError_t bwd_w_mfma(const TailArgs &a, const void *X, const int32_t *idx, cons
 // the tail's training pass in two kernels' worth of work: fused forward + loss gradient + dW, then
 // backward-feature reading the transposed weights the first one wrote (groups of 32 labels)
 bool tail_step_fused(const TailArgs &a, int P);
-size_t tail_step_ws(const TailArgs &a);
+size_t tail_step_ws(const TailArgs &a, int P);
 hipError_t tail_step_mfma(const TailArgs &a, const void *X, const int32_t *idx, const void *W, const float *bias,
                           const int32_t *pos, int P, void *dY, float *dW, float *dbias, int beta, float *dX,
                           int beta_dx, void *ws, hipStream_t s);
@@ -156,9 +156,11 @@ size_t bwd_x_mfma_ws(const TailArgs &a);
 hipError_t bwd_x_mfma(const TailArgs &a, const int32_t *idx, const void *W, const void *dY, float *dX, int beta,
                       void *ws, hipStream_t s);
 
-// forward with the BCE-gradient epilogue, optionally fused with backward-weight (bf16, MFMA)
+// forward with the BCE-gradient epilogue, optionally fused with backward-weight (bf16, MFMA); the
+// workspace query provides for rows of up to kFusedPosWs positives
+constexpr int kFusedPosWs = 1024;
 bool fwd_bce_mfma_supported(const TailArgs &a, int P);
-size_t fwd_bce_mfma_ws(const TailArgs &a);
+size_t fwd_bce_mfma_ws(const TailArgs &a, int P);   // P: positives per row
 hipError_t fwd_bce_mfma(const TailArgs &a, const void *X, const int32_t *idx, const void *W, const float *bias,
                         const int32_t *pos, int P, void *dY, float *dW, float *dbias, int beta, void *ws,
                         hipStream_t s);

@@ -45,7 +45,13 @@ size_t haste_fwd_bce_static_max_bytes(void) { return kStaticScratchBytes; }
 
 int haste_fwd_bce_static(const haste_desc_t *d, const void *X, const int32_t *idx, const void *W, const float *bias,
                          const int32_t *pos, int32_t P, void *dY, float *dW, float *dbias, int beta, void *stream) {
-    const size_t need = haste_workspace_bytes(d, HASTE_OP_FWD_BCE);   // 0 for an invalid descriptor
+    // the scratch this call needs: the X^T copy, and on the fused kernel's shapes the bucketed
+    // positives of rows of more than 64 (0 for an invalid descriptor: haste_fwd_bce reports it)
+    size_t need = haste_workspace_bytes(d, HASTE_OP_BWD_W);
+    if (need) {
+        const haste::TailArgs a{d->B, d->F_s, d->L, d->G, d->F_in, d->dtype};
+        if (haste::fwd_bce_mfma_supported(a, P)) need = haste::fwd_bce_mfma_ws(a, P);
+    }
     if (need > kStaticScratchBytes)
         return haste::report(HASTE_ERR_UNSUPPORTED,
                             "haste_fwd_bce_static: this layer needs %zu bytes of scratch, more than the %zu the "

@@ -549,7 +549,11 @@ __global__ __launch_bounds__(512) void k_bwd_w2(const bf16_t *__restrict__ Xb, c
 // Targets: the slab's positives that fall in the workgroup's span are set as bits of an LDS
 // bitmap, one 32-bit word of rows per label.  Two bitmaps alternate by slab parity: in one
 // barrier interval each thread clears its word of the previous slab's bitmap and sets the
-// current slab's bits, and the bitmap is read only after the next barrier.
+// current slab's bits, and the bitmap is read only after the next barrier.  Rows of at most
+// kFbMaxPos positives: every workgroup prefetches all of the slab's positives (two per thread)
+// and keeps those in its span.  Longer rows: a pre-pass buckets the positives by (workgroup,
+// slab) cell (counting sort), and a workgroup prefetches only its own cell's entries, one per
+// thread (a cell of more than one entry per thread finishes with direct loads).
 // --------------------------------------------------------------------------------------------
 constexpr int kFbMaxSpan = 512;                 // labels per workgroup at most
 constexpr int kFbMaxPos = 64;                   // positives per row the slab prefetch holds
@@ -576,8 +580,10 @@ __device__ __forceinline__ uint32_t dpp_swap_pairs(uint32_t v) {   // lane l rec
 // byte offset of dword d of staged dY row r (32-byte column blocks permuted by r / 8)
 __device__ __forceinline__ int fb_ystg_off(int r, int d) { return r * kFbYRow + 4 * (d ^ (8 * (r >> 3))); }
 
-// widest input the kernel stages (its X^T prefetch registers are sized for it)
-constexpr int kFbMaxFs = 768;
+// widest input the kernel takes; its X^T prefetch registers cover the first kFbPrefetchFs features
+// of a slab's block, and wider inputs load the rest while staging
+constexpr int kFbMaxFs = 1024;
+constexpr int kFbPrefetchFs = 768;
 
 // what the kernel does with the backward-weight product: nothing, store dW, or apply the
 // momentum step to W with it (dW never stored)
@@ -589,14 +595,15 @@ __global__ __launch_bounds__(64 * fb_waves(F_IN)) void k_fwd_bce(
     const float *__restrict__ bias, const int32_t *__restrict__ pos, int P, bf16_t *__restrict__ dY,
     float *__restrict__ dW, float *__restrict__ dbias, int beta, float lr, float momentum, float weight_decay,
     float *__restrict__ mom, bf16_t *__restrict__ W_next, int B, int Bp, int F_s, int64_t L, int G, int64_t K,
-    bf16_t *__restrict__ WT, int32_t *__restrict__ idxl) {
+    bf16_t *__restrict__ WT, int32_t *__restrict__ idxl, const int32_t *__restrict__ cofs,
+    const uint32_t *__restrict__ cent, int64_t n_ent) {
     constexpr bool WITH_DW = OUT != kFbOutNone;
     extern __shared__ __align__(16) char fbs[];
     constexpr int NW = fb_waves(F_IN);
     constexpr int NT = NW * 64;                 // threads
     constexpr int KS = F_IN / 32;               // forward K-steps (32 slots)
     constexpr int NST = F_IN / 16;              // backward-weight M-tiles (16 slots)
-    constexpr int XL = kFbMaxFs * 4 / NT;       // 16-byte X^T loads per thread and slab
+    constexpr int XL = kFbPrefetchFs * 4 / NT;  // prefetched 16-byte X^T loads per thread and slab
     constexpr int PL = 32 * kFbMaxPos / NT;     // positives per thread and slab
     constexpr int YL = 32 * 64 / NT;            // 16-byte dY stores per thread and slab
     char *xs = fbs;
@@ -653,13 +660,25 @@ __global__ __launch_bounds__(64 * fb_waves(F_IN)) void k_fwd_bce(
     }
 
     // cooperative slab loads: the X^T block (4 F_s chunks of 16 bytes) and the slab's positives
+    // (all of them, or this workgroup's bucket: entries (row in slab) << 16 | (label - lab0))
     const int nxc = 4 * F_s;
+    const int nslab = Bp / 32;
+    const bool bucketed = cofs != nullptr;
+    const Buf eb(cent, (uint32_t)(bucketed ? n_ent * 4 : 0));
     uint4 xr[XL];
     uint32_t pr[PL];
+    int pc0 = 0, pc1 = 0;   // the current bucket's entries (bucketed)
     auto load = [&](int blk) {
         const Buf xb(Xb + (int64_t)blk * F_s * 32, (uint32_t)(nxc * 16));
 #pragma unroll
         for (int i = 0; i < XL; ++i) xr[i] = xb.ld16((uint32_t)(tid + NT * i) * 16);   // past the block: zero
+        if (bucketed) {
+            const int64_t cell = (int64_t)blockIdx.x * nslab + blk;
+            pc0 = cofs[cell];
+            pc1 = cofs[cell + 1];
+            pr[0] = eb.ld4(tid < pc1 - pc0 ? (uint32_t)(pc0 + tid) * 4 : kOob);
+            return;
+        }
         const int b0 = blk * 32;
         const int rows = B - b0 < 32 ? B - b0 : 32;
         const Buf pb(pos + (int64_t)b0 * P, (uint32_t)(rows > 0 ? rows * P * 4 : 0));
@@ -672,9 +691,24 @@ __global__ __launch_bounds__(64 * fb_waves(F_IN)) void k_fwd_bce(
             const int c = tid + NT * i;
             if (c < nxc) *reinterpret_cast<uint4 *>(xs + (c >> 2) * kBw2XRow + (c & 3) * 16) = xr[i];
         }
+        if (nxc > XL * NT) {   // an input wider than the prefetch: the rest of the block, loaded here
+            const Buf xb(Xb + (int64_t)blk * F_s * 32, (uint32_t)(nxc * 16));
+            for (int c = XL * NT + tid; c < nxc; c += NT)
+                *reinterpret_cast<uint4 *>(xs + (c >> 2) * kBw2XRow + (c & 3) * 16) = xb.ld16((uint32_t)c * 16);
+        }
         // clear this thread's word of the previous slab's bitmap, set the current slab's targets
         uint32_t *cur = bm + (blk & 1) * kFbMaxSpan;
         if (tid < kFbMaxSpan) bm[((blk + 1) & 1) * kFbMaxSpan + tid] = 0u;
+        if (bucketed) {
+            // entries lie in this workgroup's span by construction; the masks only keep a corrupt
+            // entry inside the bitmap
+            if (tid < pc1 - pc0) atomicOr(cur + (pr[0] & (kFbMaxSpan - 1)), 1u << ((pr[0] >> 16) & 31));
+            for (int e = pc0 + NT + tid; e < pc1; e += NT) {
+                const uint32_t v = eb.ld4((uint32_t)e * 4);
+                atomicOr(cur + (v & (kFbMaxSpan - 1)), 1u << ((v >> 16) & 31));
+            }
+            return;
+        }
         const int rows = B - blk * 32 < 32 ? B - blk * 32 : 32;
 #pragma unroll
         for (int i = 0; i < PL; ++i) {
@@ -1454,14 +1488,103 @@ hipError_t bwd_w_mfma(const TailArgs &a, const void *X, const int32_t *idx, cons
 }
 
 // ---- forward with the BCE-gradient epilogue, fused with backward-weight -------------------------
-// Groups of whole 16-label tiles (the staged dY columns of a wave's units stay contiguous), inputs
-// of at most kFbMaxFs features, and at most kFbMaxPos positives per row (the slab prefetch).
+// Groups of whole 16-label tiles (the staged dY columns of a wave's units stay contiguous) and
+// inputs of at most kFbMaxFs features; any number of positives per row (more than kFbMaxPos are
+// bucketed by a pre-pass, in the workspace).
 bool fwd_bce_mfma_supported(const TailArgs &a, int P) {
-    return bwd_w_mfma_supported(a) && (a.G % 16) == 0 && a.F_s <= kFbMaxFs && P >= 0 && P <= kFbMaxPos &&
-           fb_lds((int)a.F_s, (int)a.F_in) <= kLdsBudget;
+    return bwd_w_mfma_supported(a) && (a.G % 16) == 0 && a.F_s <= kFbMaxFs && P >= 0 &&
+           a.B * (int64_t)P < ((int64_t)1 << 29) && fb_lds((int)a.F_s, (int)a.F_in) <= kLdsBudget;
 }
 
-size_t fwd_bce_mfma_ws(const TailArgs &a) { return bwd_w_mfma_ws(a); }
+// the fused kernel's (workgroup, slab) cells: workgroups of fb_waves units, slabs of 32 rows
+struct FbCells {
+    int ntn, nw, nslab;
+    int64_t nwg, ncell;
+};
+
+static FbCells fb_cells(const TailArgs &a) {
+    FbCells c;
+    c.ntn = (int)cdiv(a.G, 32);
+    c.nw = fb_waves((int)a.F_in);
+    c.nslab = (int)(round_up(a.B, 32) / 32);
+    c.nwg = cdiv((a.L / a.G) * c.ntn, c.nw);
+    c.ncell = c.nwg * c.nslab;
+    return c;
+}
+
+// workspace of the bucketed positives (rows of more than kFbMaxPos): per-cell counts, offsets and
+// the entries
+static size_t fb_pos_ws(const TailArgs &a, int P) {
+    if (P <= kFbMaxPos) return 0;
+    const FbCells c = fb_cells(a);
+    return (size_t)(round_up(c.ncell * 4, 256) + round_up((c.ncell + 1) * 4, 256) + round_up(a.B * (int64_t)P * 4, 256));
+}
+
+size_t fwd_bce_mfma_ws(const TailArgs &a, int P) { return bwd_w_mfma_ws(a) + fb_pos_ws(a, P); }
+
+// cell of the positive (row b, label col), and the first label of a workgroup's span
+__device__ __forceinline__ int64_t fb_cell_of(int64_t col, int b, int G, int ntn, int nw, int nslab) {
+    const int64_t k = col / G;
+    const int64_t unit = k * ntn + (col - k * G) / 32;
+    return (unit / nw) * nslab + (b >> 5);
+}
+
+__device__ __forceinline__ int64_t fb_span_start(int64_t w, int G, int ntn, int nw) {
+    const int64_t v = w * nw, k = v / ntn;
+    return k * G + 32 * (v - k * ntn);
+}
+
+__global__ void k_fb_pos_count(const int32_t *__restrict__ pos, int B, int P, int64_t L, int G, int ntn, int nw,
+                               int nslab, int32_t *__restrict__ cnt) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= (int64_t)B * P) return;
+    const int64_t col = pos[i];
+    if (col < 0 || col >= L) return;   // outside the layer: ignored
+    atomicAdd(&cnt[fb_cell_of(col, (int)(i / P), G, ntn, nw, nslab)], 1);
+}
+
+// cofs = exclusive prefix sums of cnt (cofs[ncell] = total), and cnt cleared for use as cursors
+// (one workgroup of 1024 threads, each over a contiguous run of cells)
+__global__ __launch_bounds__(1024) void k_fb_pos_scan(int32_t *__restrict__ cnt, int64_t ncell,
+                                                      int32_t *__restrict__ cofs) {
+    __shared__ int32_t s[1024];
+    const int64_t per = (ncell + 1023) / 1024;
+    const int64_t c0 = threadIdx.x * per, c1 = c0 + per < ncell ? c0 + per : ncell;
+    int32_t tot = 0;
+    for (int64_t c = c0; c < c1; ++c) tot += cnt[c];
+    s[threadIdx.x] = tot;
+    __syncthreads();
+    for (int off = 1; off < 1024; off <<= 1) {
+        const int32_t v = threadIdx.x >= off ? s[threadIdx.x - off] : 0;
+        __syncthreads();
+        s[threadIdx.x] += v;
+        __syncthreads();
+    }
+    int32_t run = s[threadIdx.x] - tot;
+    for (int64_t c = c0; c < c1; ++c) {
+        const int32_t n = cnt[c];
+        cofs[c] = run;
+        cnt[c] = 0;
+        run += n;
+    }
+    if (threadIdx.x == 1023) cofs[ncell] = s[1023];
+}
+
+// entries (row in slab) << 16 | (label - span start), in cell order (order within a cell is free:
+// the kernel only ORs them into a bitmap)
+__global__ void k_fb_pos_fill(const int32_t *__restrict__ pos, int B, int P, int64_t L, int G, int ntn, int nw,
+                              int nslab, const int32_t *__restrict__ cofs, int32_t *__restrict__ cur,
+                              uint32_t *__restrict__ cent) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= (int64_t)B * P) return;
+    const int64_t col = pos[i];
+    if (col < 0 || col >= L) return;
+    const int b = (int)(i / P);
+    const int64_t cell = fb_cell_of(col, b, G, ntn, nw, nslab);
+    const int slot = atomicAdd(&cur[cell], 1);
+    const int64_t o = col - fb_span_start(cell / nslab, G, ntn, nw);
+    cent[cofs[cell] + slot] = ((uint32_t)(b & 31) << 16) | (uint32_t)o;
+}
 
 struct FbArgs {
     const bf16_t *Xb;
@@ -1479,6 +1602,9 @@ struct FbArgs {
     int Bp;
     bf16_t *WT;       // transposed weights and lane-ordered supports for backward-feature, or null
     int32_t *idxl;
+    const int32_t *cofs = nullptr;   // bucketed positives (rows of more than kFbMaxPos), or null
+    const uint32_t *cent = nullptr;
+    int64_t n_ent = 0;
 };
 
 template <int F_IN, int OUT>
@@ -1494,7 +1620,7 @@ static hipError_t launch_fwd_bce(const TailArgs &a, const FbArgs &f, hipStream_t
         hipLaunchKernelGGL(kern, grid, dim3(fb_waves(F_IN) * 64), lds, s, f.Xb, f.idx, (const bf16_t *)f.W, f.bias,
                            f.pos, f.P, (bf16_t *)f.dY, f.dW, f.dbias, f.beta, f.opt.lr, f.opt.momentum,
                            f.opt.weight_decay, f.m, (bf16_t *)f.W_next, (int)a.B, f.Bp, (int)a.F_s, a.L, (int)a.G, K,
-                           f.WT, f.idxl);
+                           f.WT, f.idxl, f.cofs, f.cent, f.n_ent);
         return hipGetLastError();
     };
     if constexpr (OUT == kFbOutNone)
@@ -1512,6 +1638,26 @@ static hipError_t fwd_bce_dispatch(const TailArgs &a, const void *X, FbArgs &f, 
                        (const bf16_t *)X, Xb, (int)a.B, (int)a.F_s);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
+    if (f.P > kFbMaxPos) {   // bucket the positives by (workgroup, slab) cell
+        const FbCells c = fb_cells(a);
+        char *pw = reinterpret_cast<char *>(ws) + bwd_w_mfma_ws(a);
+        int32_t *cnt = reinterpret_cast<int32_t *>(pw);
+        int32_t *cofs = reinterpret_cast<int32_t *>(pw + round_up(c.ncell * 4, 256));
+        uint32_t *cent = reinterpret_cast<uint32_t *>(pw + round_up(c.ncell * 4, 256) + round_up((c.ncell + 1) * 4, 256));
+        const int64_t n = a.B * (int64_t)f.P;
+        e = fill_f32(reinterpret_cast<float *>(cnt), c.ncell, 0.0f, s);   // all-zero bits: integer zeros
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(k_fb_pos_count, dim3((unsigned)cdiv(n, 256)), dim3(256), 0, s, f.pos, (int)a.B, f.P, a.L,
+                           (int)a.G, c.ntn, c.nw, c.nslab, cnt);
+        hipLaunchKernelGGL(k_fb_pos_scan, dim3(1), dim3(1024), 0, s, cnt, c.ncell, cofs);
+        hipLaunchKernelGGL(k_fb_pos_fill, dim3((unsigned)cdiv(n, 256)), dim3(256), 0, s, f.pos, (int)a.B, f.P, a.L,
+                           (int)a.G, c.ntn, c.nw, c.nslab, cofs, cnt, cent);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        f.cofs = cofs;
+        f.cent = cent;
+        f.n_ent = n;
+    }
     switch (a.F_in) {
         case 32: return launch_fwd_bce<32, OUT>(a, f, s);
         case 64: return launch_fwd_bce<64, OUT>(a, f, s);
@@ -1628,7 +1774,7 @@ bool tail_step_fused(const TailArgs &a, int P) {
     return a.G == 32 && fwd_bce_mfma_supported(a, P) && bwd_x_mfma_supported(a);
 }
 
-size_t tail_step_ws(const TailArgs &a) { return round_up(bwd_x_mfma_ws(a), 256) + fwd_bce_mfma_ws(a); }
+size_t tail_step_ws(const TailArgs &a, int P) { return round_up(bwd_x_mfma_ws(a), 256) + fwd_bce_mfma_ws(a, P); }
 
 hipError_t tail_step_mfma(const TailArgs &a, const void *X, const int32_t *idx, const void *W, const float *bias,
                           const int32_t *pos, int P, void *dY, float *dW, float *dbias, int beta, float *dX,

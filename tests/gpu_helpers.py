@@ -114,6 +114,23 @@ def rand_pos(rng, B, L, P):
     return pos
 
 
+def skewed_pos(rng, B, L, P, hot=512):
+    """[B, P] positives with rows of very different lengths (-1 padded): up to half of a row in the
+    first `hot` labels (one workgroup's span, so that its cells hold many entries), the rest
+    anywhere, some repeats, ids out of range."""
+    pos = np.full((B, P), -1, np.int32)
+    for b in range(B):
+        n = P if b % 3 == 0 else int(rng.integers(0, P + 1))
+        nh = min(n // 2, hot)
+        row = list(rng.choice(hot, nh, replace=False)) + list(rng.integers(0, L, n - nh))
+        if n > 2 and b % 5 == 0:
+            row[-1] = row[0]              # a repeat counts once
+        if n > 3 and b % 7 == 0:
+            row[-2] = L + 5               # outside the layer: ignored
+        pos[b, :n] = row
+    return pos
+
+
 def targets(pos, B, L):
     T = np.zeros((B, L), bool)
     for b in range(B):

@@ -13,7 +13,8 @@ import pytest
 
 import oracle
 import synth
-from gpu_helpers import TOL, host_f32, oracle_fwd_bce, out_tensor, rand_pos, rel_err, say, targets, to_dev
+from gpu_helpers import (TOL, host_f32, oracle_fwd_bce, out_tensor, rand_pos, rel_err, say, skewed_pos, targets,
+                         to_dev)
 
 pytestmark = pytest.mark.gpu
 F32, BF16 = synth.DT_F32, synth.DT_BF16
@@ -44,7 +45,8 @@ def _check(name, got, ref, dtype):
 
 
 CASES = [
-    # name, B, F_s, L, G, F_in, dtype, P, bias   (fused: bf16, G % 16 == 0, P <= 64)
+    # name, B, F_s, L, G, F_in, dtype, P, bias   (fused: bf16, G % 16 == 0, F_s <= 1024; rows of more
+    # than 64 positives are bucketed by a pre-pass)
     ("fused_g32_f64", 40, 256, 2048, 32, 64, BF16, 6, False),
     ("fused_g32_f64_bias", 64, 768, 4096, 32, 64, BF16, 8, True),
     ("fused_g16_ragged_b33", 33, 768, 4096, 16, 64, BF16, 5, False),
@@ -53,7 +55,14 @@ CASES = [
     ("fused_b300_f32", 300, 768, 8192, 32, 32, BF16, 64, True),
     ("fused_b1", 1, 768, 1024, 32, 64, BF16, 2, False),
     ("fused_p0", 50, 512, 2048, 32, 64, BF16, 0, False),
-    ("composed_p80", 40, 256, 2048, 32, 64, BF16, 80, False),
+    ("fused_p80_bucketed", 40, 256, 2048, 32, 64, BF16, 80, False),
+    ("fused_p200_skewed", 96, 768, 8192, 32, 64, BF16, -200, True),
+    ("fused_p130_skewed_f128", 70, 768, 4096, 64, 128, BF16, -130, False),
+    ("fused_p90_skewed_g16_f32", 65, 512, 4096, 16, 32, BF16, -90, True),
+    # 32 rows of 80 with half in one 512-label span: a cell of about 1280 entries, over one per thread
+    ("fused_p80_full_cell", 32, 768, 4096, 32, 64, BF16, -80, False),
+    ("fused_fs1024", 70, 1024, 4096, 32, 64, BF16, 8, True),
+    ("fused_fs1024_f128_p100", 45, 1024, 2048, 32, 128, BF16, -100, False),
     ("composed_g8", 70, 768, 3072, 8, 32, BF16, 5, True),
     ("composed_g4", 64, 512, 1536, 4, 64, BF16, 5, False),
     ("composed_g1_ffi", 37, 768, 1024, 1, 64, BF16, 4, False),
@@ -70,7 +79,14 @@ def test_fwd_bce(hs, orc, case):
     X, W, idx = synth.draw_X(wl), synth.draw_W(wl), synth.draw_idx(wl)
     rng = np.random.default_rng(wl.wid)
     bias = rng.standard_normal(L).astype(np.float32) if with_bias else None
-    pos = rand_pos(rng, B, L, P)
+    if P < 0:
+        P = -P
+        pos = skewed_pos(rng, B, L, P)
+        if name == "fused_p80_full_cell":
+            pos[:, :40] = np.stack([rng.choice(512, 40, replace=False) for _ in range(B)])
+            pos[:, 40:] = rng.integers(512, L, (B, 40))
+    else:
+        pos = rand_pos(rng, B, L, P)
     desc = hs.make_desc(B, F_s, L, G, F_in, dt)
     Xd, idxd, Wd, bd = to_dev(X), to_dev(idx), to_dev(W), to_dev(bias)
     posd = to_dev(pos) if P else None

@@ -11,7 +11,7 @@ import pytest
 
 import oracle
 import synth
-from gpu_helpers import TOL, host_f32, oracle_fwd_bce, out_tensor, rand_pos, rel_err, say, to_dev
+from gpu_helpers import TOL, host_f32, oracle_fwd_bce, out_tensor, rand_pos, rel_err, say, skewed_pos, to_dev
 
 pytestmark = pytest.mark.gpu
 F32, BF16 = synth.DT_F32, synth.DT_BF16
@@ -63,12 +63,15 @@ def test_sgd_momentum_elementwise(hs, orc, n, dt, inplace, wd, zero_grad):
 
 
 CASES = [
-    # name, B, F_s, L, G, F_in, dtype, P, bias, dbias   (fused: bf16, G % 16 == 0, F_s <= 768, P <= 64)
+    # name, B, F_s, L, G, F_in, dtype, P, bias, dbias   (fused: bf16, G % 16 == 0, F_s <= 1024; P < 0:
+    # skewed rows of up to -P positives, bucketed by the pre-pass)
     ("fused_g32_f64", 40, 256, 2048, 32, 64, BF16, 6, False, False),
     ("fused_g16_ragged_b33", 33, 768, 4096, 16, 64, BF16, 5, True, True),
     ("fused_g64_f128", 70, 768, 4096, 64, 128, BF16, 8, True, True),
     ("fused_g32_f32_b300", 300, 512, 8192, 32, 32, BF16, 8, False, True),
-    ("composed_fs1024", 40, 1024, 2048, 32, 64, BF16, 4, False, False),
+    ("fused_fs1024", 40, 1024, 2048, 32, 64, BF16, 4, False, False),
+    ("fused_p150_skewed", 64, 768, 4096, 32, 64, BF16, -150, True, True),
+    ("fused_p200_skewed_f128", 48, 512, 4096, 32, 128, BF16, -200, False, True),
     ("composed_g8", 70, 768, 3072, 8, 32, BF16, 5, True, True),
     ("composed_f32_g8", 32, 256, 4096, 8, 32, F32, 5, False, False),
 ]
@@ -83,7 +86,7 @@ def test_fwd_bce_sgd(hs, orc, case):
     X, W, idx = synth.draw_X(wl), synth.draw_W(wl), synth.draw_idx(wl)
     rng = np.random.default_rng(wl.wid)
     bias = rng.standard_normal(L).astype(np.float32) if with_bias else None
-    pos = rand_pos(rng, B, L, P)
+    pos = skewed_pos(rng, B, L, -P) if P < 0 else rand_pos(rng, B, L, P)
     m0 = (0.01 * rng.standard_normal((L, F_in))).astype(np.float32)
     lr, mu, wd = 0.1, 0.9, 1e-4
     desc = hs.make_desc(B, F_s, L, G, F_in, dt)
@@ -139,8 +142,8 @@ def test_fwd_bce_sgd_edges(hs):
         hs.haste_fwd_bce_sgd(d, dummy, dummy, W, None, None, dummy, opt, m, W, None, ws)
     with pytest.raises(hs.HasteError):   # momentum out of range
         hs.haste_fwd_bce_sgd(d, dummy, dummy, W, None, None, dummy, hs.sgd_opts(0.1, 1.0), m, Wn, None, ws)
-    with pytest.raises(hs.HasteError):   # more positives per row than the fused kernel takes
-        pos = torch.zeros((8, 65), dtype=torch.int32, device="cuda")
+    with pytest.raises(hs.HasteError):   # rows of more positives than the queried workspace provides for
+        pos = torch.zeros((8, 2000), dtype=torch.int32, device="cuda")
         hs.haste_fwd_bce_sgd(d, dummy, dummy, W, None, pos, dummy, opt, m, Wn, None, ws)
 
 

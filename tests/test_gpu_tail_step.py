@@ -57,6 +57,8 @@ CASES = [
     ("g32_f32_ragged_b33", 33, 256, 2048, 32, 32, BF16, 3, False, 0),
     ("g32_f128", 70, 768, 4096, 32, 128, BF16, 8, True, 0),
     ("g32_small_fs", 96, 128, 4096, 32, 64, BF16, 4, False, 1),
+    ("g32_f64_p150_bucketed", 64, 768, 8192, 32, 64, BF16, 150, True, 1),
+    ("g32_fs896", 40, 896, 4096, 32, 64, BF16, 6, False, 0),   # X^T past the prefetch; bwd_x takes F_s <= 910
     ("composed_g16", 64, 768, 4096, 16, 64, BF16, 8, False, 0),
     ("composed_f32", 32, 256, 4096, 8, 32, F32, 5, True, 1),
 ]
@@ -93,6 +95,7 @@ def test_tail_step_workspace_checked(hs):
 
 
 @pytest.mark.parametrize("case", [("g32_f64", 64, 768, 4096, 32, 64, 8, True), ("g32_f128", 70, 768, 4096, 32, 128, 5, False),
+                                  ("g32_f64_p120_bucketed", 50, 512, 4096, 32, 64, 120, True),
                                   ("composed_g16", 48, 512, 4096, 16, 64, 4, False)], ids=lambda c: c[0])
 def test_tail_step_sgd_equals_the_two_calls(hs, case):
     import torch

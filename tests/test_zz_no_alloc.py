@@ -24,6 +24,7 @@ CALLS = [
     ("fused_b300_g32", 300, 768, 8192, 32, 64, 8, True, 0),
     ("fused_smaller_b40_g16", 40, 256, 2048, 16, 32, 3, False, 1),
     ("composed_b33_g4", 33, 512, 1024, 4, 64, 5, True, 0),
+    ("fused_bucketed_b64_p150", 64, 768, 4096, 32, 64, 150, False, 0),
 ]
 
 
