@@ -589,7 +589,7 @@ constexpr int kFbPrefetchFs = 768;
 // momentum step to W with it (dW never stored)
 constexpr int kFbOutNone = 0, kFbOutDW = 1, kFbOutSGD = 2;
 
-template <int F_IN, bool HAS_BIAS, int OUT, bool WITH_DB>
+template <int F_IN, bool HAS_BIAS, int OUT, bool WITH_DB, bool BUCKETED>
 __global__ __launch_bounds__(64 * fb_waves(F_IN)) void k_fwd_bce(
     const bf16_t *__restrict__ Xb, const int32_t *__restrict__ idx, const bf16_t *__restrict__ W,
     const float *__restrict__ bias, const int32_t *__restrict__ pos, int P, bf16_t *__restrict__ dY,
@@ -604,6 +604,7 @@ __global__ __launch_bounds__(64 * fb_waves(F_IN)) void k_fwd_bce(
     constexpr int KS = F_IN / 32;               // forward K-steps (32 slots)
     constexpr int NST = F_IN / 16;              // backward-weight M-tiles (16 slots)
     constexpr int XL = kFbPrefetchFs * 4 / NT;  // prefetched 16-byte X^T loads per thread and slab
+    constexpr int XW = (kFbMaxFs - kFbPrefetchFs) * 4 / NT;   // and the rest of the widest input
     constexpr int PL = 32 * kFbMaxPos / NT;     // positives per thread and slab
     constexpr int YL = 32 * 64 / NT;            // 16-byte dY stores per thread and slab
     char *xs = fbs;
@@ -663,7 +664,7 @@ __global__ __launch_bounds__(64 * fb_waves(F_IN)) void k_fwd_bce(
     // (all of them, or this workgroup's bucket: entries (row in slab) << 16 | (label - lab0))
     const int nxc = 4 * F_s;
     const int nslab = Bp / 32;
-    const bool bucketed = cofs != nullptr;
+    constexpr bool bucketed = BUCKETED;   // positives bucketed by cell (rows of more than kFbMaxPos)
     const Buf eb(cent, (uint32_t)(bucketed ? n_ent * 4 : 0));
     uint4 xr[XL];
     uint32_t pr[PL];
@@ -672,18 +673,18 @@ __global__ __launch_bounds__(64 * fb_waves(F_IN)) void k_fwd_bce(
         const Buf xb(Xb + (int64_t)blk * F_s * 32, (uint32_t)(nxc * 16));
 #pragma unroll
         for (int i = 0; i < XL; ++i) xr[i] = xb.ld16((uint32_t)(tid + NT * i) * 16);   // past the block: zero
-        if (bucketed) {
+        if constexpr (bucketed) {
             const int64_t cell = (int64_t)blockIdx.x * nslab + blk;
-            pc0 = cofs[cell];
-            pc1 = cofs[cell + 1];
+            pc0 = __builtin_amdgcn_readfirstlane(cofs[cell]);   // workgroup-uniform: scalar registers
+            pc1 = __builtin_amdgcn_readfirstlane(cofs[cell + 1]);
             pr[0] = eb.ld4(tid < pc1 - pc0 ? (uint32_t)(pc0 + tid) * 4 : kOob);
-            return;
-        }
-        const int b0 = blk * 32;
-        const int rows = B - b0 < 32 ? B - b0 : 32;
-        const Buf pb(pos + (int64_t)b0 * P, (uint32_t)(rows > 0 ? rows * P * 4 : 0));
+        } else {
+            const int b0 = blk * 32;
+            const int rows = B - b0 < 32 ? B - b0 : 32;
+            const Buf pb(pos + (int64_t)b0 * P, (uint32_t)(rows > 0 ? rows * P * 4 : 0));
 #pragma unroll
-        for (int i = 0; i < PL; ++i) pr[i] = pb.ld4((uint32_t)(tid + NT * i) * 4);   // validity checked at use
+            for (int i = 0; i < PL; ++i) pr[i] = pb.ld4((uint32_t)(tid + NT * i) * 4);   // validity checked at use
+        }
     };
     auto stage_slab = [&](int blk) {
 #pragma unroll
@@ -691,15 +692,10 @@ __global__ __launch_bounds__(64 * fb_waves(F_IN)) void k_fwd_bce(
             const int c = tid + NT * i;
             if (c < nxc) *reinterpret_cast<uint4 *>(xs + (c >> 2) * kBw2XRow + (c & 3) * 16) = xr[i];
         }
-        if (nxc > XL * NT) {   // an input wider than the prefetch: the rest of the block, loaded here
-            const Buf xb(Xb + (int64_t)blk * F_s * 32, (uint32_t)(nxc * 16));
-            for (int c = XL * NT + tid; c < nxc; c += NT)
-                *reinterpret_cast<uint4 *>(xs + (c >> 2) * kBw2XRow + (c & 3) * 16) = xb.ld16((uint32_t)c * 16);
-        }
         // clear this thread's word of the previous slab's bitmap, set the current slab's targets
         uint32_t *cur = bm + (blk & 1) * kFbMaxSpan;
         if (tid < kFbMaxSpan) bm[((blk + 1) & 1) * kFbMaxSpan + tid] = 0u;
-        if (bucketed) {
+        if constexpr (bucketed) {
             // entries lie in this workgroup's span by construction; the masks only keep a corrupt
             // entry inside the bitmap
             if (tid < pc1 - pc0) atomicOr(cur + (pr[0] & (kFbMaxSpan - 1)), 1u << ((pr[0] >> 16) & 31));
@@ -707,15 +703,23 @@ __global__ __launch_bounds__(64 * fb_waves(F_IN)) void k_fwd_bce(
                 const uint32_t v = eb.ld4((uint32_t)e * 4);
                 atomicOr(cur + (v & (kFbMaxSpan - 1)), 1u << ((v >> 16) & 31));
             }
-            return;
-        }
-        const int rows = B - blk * 32 < 32 ? B - blk * 32 : 32;
+        } else {
+            const int rows = B - blk * 32 < 32 ? B - blk * 32 : 32;
 #pragma unroll
-        for (int i = 0; i < PL; ++i) {
-            const int e = tid + NT * i;
-            if (e < rows * P) {
-                const int64_t o = (int64_t)(int32_t)pr[i] - lab0;
-                if (o >= 0 && o < span) atomicOr(cur + o, 1u << (e / P));
+            for (int i = 0; i < PL; ++i) {
+                const int e = tid + NT * i;
+                if (e < rows * P) {
+                    const int64_t o = (int64_t)(int32_t)pr[i] - lab0;
+                    if (o >= 0 && o < span) atomicOr(cur + o, 1u << (e / P));
+                }
+            }
+        }
+        if (nxc > XL * NT) {   // an input wider than the prefetch: the rest of the block, loaded here
+            const Buf xb(Xb + (int64_t)blk * F_s * 32, (uint32_t)(nxc * 16));
+#pragma unroll
+            for (int i = 0; i < XW; ++i) {
+                const int c = XL * NT + tid + NT * i;
+                if (c < nxc) *reinterpret_cast<uint4 *>(xs + (c >> 2) * kBw2XRow + (c & 3) * 16) = xb.ld16((uint32_t)c * 16);
             }
         }
     };
@@ -1607,6 +1611,14 @@ struct FbArgs {
     int64_t n_ent = 0;
 };
 
+template <int F_IN, int OUT, bool BK, class Go>
+static hipError_t launch_fwd_bce_k(const FbArgs &f, Go &go) {
+    if constexpr (OUT == kFbOutNone)
+        return f.bias ? go(k_fwd_bce<F_IN, true, OUT, false, BK>) : go(k_fwd_bce<F_IN, false, OUT, false, BK>);
+    if (f.dbias) return f.bias ? go(k_fwd_bce<F_IN, true, OUT, true, BK>) : go(k_fwd_bce<F_IN, false, OUT, true, BK>);
+    return f.bias ? go(k_fwd_bce<F_IN, true, OUT, false, BK>) : go(k_fwd_bce<F_IN, false, OUT, false, BK>);
+}
+
 template <int F_IN, int OUT>
 static hipError_t launch_fwd_bce(const TailArgs &a, const FbArgs &f, hipStream_t s) {
     const int64_t K = a.L / a.G;
@@ -1623,10 +1635,7 @@ static hipError_t launch_fwd_bce(const TailArgs &a, const FbArgs &f, hipStream_t
                            f.WT, f.idxl, f.cofs, f.cent, f.n_ent);
         return hipGetLastError();
     };
-    if constexpr (OUT == kFbOutNone)
-        return f.bias ? go(k_fwd_bce<F_IN, true, OUT, false>) : go(k_fwd_bce<F_IN, false, OUT, false>);
-    if (f.dbias) return f.bias ? go(k_fwd_bce<F_IN, true, OUT, true>) : go(k_fwd_bce<F_IN, false, OUT, true>);
-    return f.bias ? go(k_fwd_bce<F_IN, true, OUT, false>) : go(k_fwd_bce<F_IN, false, OUT, false>);
+    return f.cofs ? launch_fwd_bce_k<F_IN, OUT, true>(f, go) : launch_fwd_bce_k<F_IN, OUT, false>(f, go);
 }
 
 template <int OUT>
