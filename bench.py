@@ -57,10 +57,10 @@ CALL_KERNELS = {
     "bwd_w": ["k_transpose_x", "k_bwd_w"],
     "bwd_x": ["k_transpose_w", "k_bwd_x", "k_reduce_fmajor"],
     # the head's GEMM kernels by operand layout and epilogue (three tile sizes: 256, 128, fallback)
-    "head_fwd": ["k_gemm4<true, true, 0>", "k_gemm2<true, true, 0>", "k_gemm_bf16<true, true, 0>"],
-    # the 256 kernel with the loss gradient in its epilogue (other shapes run head_fwd's kernels)
-    "head_fwd_bce": ["k_gemm4<true, true, 3>"],
-    "head_bwd": ["k_gemm4<false, false, 1>", "k_gemm4<true, false, 2>", "k_gemm2<false, false, 1>",
+    "head_fwd": [r"k_gemm4<\d+, true, true, 0>", "k_gemm2<true, true, 0>", "k_gemm_bf16<true, true, 0>"],
+    # the large-tile kernel with the loss gradient in its epilogue (other shapes run head_fwd's kernels)
+    "head_fwd_bce": [r"k_gemm4<\d+, true, true, 3>"],
+    "head_bwd": [r"k_gemm4<\d+, false, false, 1>", r"k_gemm4<\d+, true, false, 2>", "k_gemm2<false, false, 1>",
                  "k_gemm2<true, false, 2>", "k_gemm_bf16<false, false, 1>", "k_gemm_bf16<true, false, 2>",
                  "k_reduce_rmajor"],
 }

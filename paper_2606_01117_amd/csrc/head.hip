@@ -281,11 +281,15 @@ constexpr size_t kG2Lds = (size_t)4 * G2TILE * 2;   // two stages of two operand
 // ---------------------------------------------------------------------------------------------
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
-constexpr int G4T = 256;                  // output tile (rows and columns)
+constexpr int G4T = 256;                  // output tile rows (M)
+constexpr int kHeadBN = 128;              // output tile columns (N) of the head's products
 constexpr int G4K = 32;                   // K step
-constexpr int G4S = 4;                    // LDS stages
-constexpr int G4OP = G4T * G4K;           // bf16 per operand and stage (16 KB)
-constexpr size_t kG4Lds = (size_t)G4S * 2 * G4OP * 2;   // 128 KB
+
+// the tile's column count BN (256 or 128) fixes the rest: LDS stages (one workgroup per CU at 256,
+// two at 128), bytes of the two operands' stage tiles, and the LDS the kernel takes
+__host__ __device__ constexpr int g4_stages(int bn) { return bn == 256 ? 4 : 3; }
+__host__ __device__ constexpr int g4_stage_bytes(int bn) { return (G4T + bn) * G4K * 2; }
+__host__ __device__ constexpr size_t g4_lds(int bn) { return (size_t)g4_stages(bn) * g4_stage_bytes(bn); }
 
 // one direct global-to-LDS load: this lane's 16 bytes at byte offset voff of the buffer land at
 // LDS address lds + 16 * lane
@@ -299,36 +303,36 @@ __device__ __forceinline__ void wait_vmcnt() {
     asm volatile("s_waitcnt vmcnt(%0)" :: "n"(N) : "memory");
 }
 
-// One operand's loads: wave w issues instructions i = 4w + t (t = 0..3), each filling 1 KB of
-// the stage: K-contiguous: rows 16i .. 16i+15 (4 lanes per 64-byte row); M/N-contiguous: k-rows
-// 2i, 2i+1 (32 lanes per 512-byte k-row).
-template <bool KC>
+// One operand tile of R rows (R = 256 or 128) and 32 k per stage, R / 16 load instructions of
+// 1 KB, R / 64 per wave: wave w issues instructions i = (R / 64) w + t.  K-contiguous: rows 16i ..
+// 16i+15 (4 lanes per 64-byte row); M/N-contiguous: 512 / R k-rows of 2R bytes per instruction.
+template <bool KC, int R>
 struct G4Operand {
+    static constexpr int NI = R / 64;    // load instructions per wave and stage
+    static constexpr int LPK = R / 8;    // lanes per k-row (M/N-contiguous)
     Buf buf;
     int64_t ld;         // elements between consecutive rows (KC) or k-rows (M/N contiguous)
     int64_t r0, rlim;   // tile rows and the operand's row count (M or N)
     int64_t klim;       // end of this workgroup's K range
     __device__ __forceinline__ void issue(int64_t k0, uint32_t lds_stage, int wave, int lane) const {
 #pragma unroll
-        for (int t = 0; t < 4; ++t) issue1(k0, lds_stage, wave, lane, t);
+        for (int t = 0; t < NI; ++t) issue1(k0, lds_stage, wave, lane, t);
     }
     __device__ __forceinline__ void issue1(int64_t k0, uint32_t lds_stage, int wave, int lane, int t) const {
-        {
-            const int i = 4 * wave + t;
-            uint32_t off;
-            if (KC) {
-                const int row = 16 * i + (lane >> 2), c = (lane & 3) ^ ((row >> 1) & 3);
-                const int64_t k = k0 + 8 * c;
-                const bool ok = r0 + row < rlim && k < klim;   // klim is a multiple of 8
-                off = ok ? (uint32_t)(((r0 + row) * ld + k) * 2) : kOob;
-            } else {
-                const int kr = 2 * i + (lane >> 5), c = (lane & 31) ^ ((kr & 3) << 1);
-                const int64_t r = r0 + 8 * c;
-                const bool ok = k0 + kr < klim && r < rlim;    // rlim is a multiple of 8
-                off = ok ? (uint32_t)(((k0 + kr) * ld + r) * 2) : kOob;
-            }
-            lds_dma16(buf, off, __builtin_amdgcn_readfirstlane(lds_stage + i * 1024));
+        const int i = NI * wave + t;
+        uint32_t off;
+        if (KC) {
+            const int row = 16 * i + (lane >> 2), c = (lane & 3) ^ ((row >> 1) & 3);
+            const int64_t k = k0 + 8 * c;
+            const bool ok = r0 + row < rlim && k < klim;   // klim is a multiple of 8
+            off = ok ? (uint32_t)(((r0 + row) * ld + k) * 2) : kOob;
+        } else {
+            const int kr = (512 / R) * i + lane / LPK, c = (lane % LPK) ^ ((kr & 3) << 1);
+            const int64_t r = r0 + 8 * c;
+            const bool ok = k0 + kr < klim && r < rlim;    // rlim is a multiple of 8
+            off = ok ? (uint32_t)(((k0 + kr) * ld + r) * 2) : kOob;
         }
+        lds_dma16(buf, off, __builtin_amdgcn_readfirstlane(lds_stage + i * 1024));
     }
     // MFMA operand fragment: rows rb .. rb+31 (lane ln), k = ks*16 + 8hh .. +7 of the stage
     __device__ __forceinline__ uint4 frag(const char *stage, int rb, int ks, int lane) const {
@@ -340,19 +344,22 @@ struct G4Operand {
         const int g = lane >> 4, i = lane & 15;                 // 16-lane group, lane in group
         const int rr = rb + 16 * (g & 1) + 4 * (i & 3);          // rows of this source lane
         const int kk = ks * 16 + 8 * (g >> 1) + (i >> 2);        // k-row of this source lane
-        const char *p = stage + kk * 512 + (((rr >> 3) ^ ((kk & 3) << 1)) * 16) + (rr & 7) * 2;
+        const char *p = stage + kk * (2 * R) + (((rr >> 3) ^ ((kk & 3) << 1)) * 16) + (rr & 7) * 2;
         const uint2 lo = lds_read_tr(p);
-        const uint2 hi = lds_read_tr(p + 4 * 512);               // k-row kk + 4: same swizzle
+        const uint2 hi = lds_read_tr(p + 4 * (2 * R));           // k-row kk + 4: same swizzle
         return make_uint4(lo.x, lo.y, hi.x, hi.y);
     }
 };
 
-template <bool AK, bool BK, int EPI>
-__global__ __launch_bounds__(256, 1) void k_gemm4(const bf16_t *__restrict__ A, int64_t sa, uint32_t a_bytes,
-                                                  const bf16_t *__restrict__ Bm, int64_t sb, uint32_t b_bytes,
-                                                  void *__restrict__ C, int64_t ldc, const float *__restrict__ bias,
-                                                  int64_t M, int64_t N, int64_t K, int64_t kchunk, int MT, int NT,
-                                                  int Z, const int32_t *__restrict__ pos, int P) {
+template <int BN, bool AK, bool BK, int EPI>
+__global__ __launch_bounds__(256, BN == 128 ? 2 : 1) void k_gemm4(
+    const bf16_t *__restrict__ A, int64_t sa, uint32_t a_bytes, const bf16_t *__restrict__ Bm, int64_t sb,
+    uint32_t b_bytes, void *__restrict__ C, int64_t ldc, const float *__restrict__ bias, int64_t M, int64_t N,
+    int64_t K, int64_t kchunk, int MT, int NT, int Z, const int32_t *__restrict__ pos, int P) {
+    constexpr int S = g4_stages(BN);
+    constexpr int NB = BN / 64;                  // 32-column blocks per wave
+    constexpr int LPW = 4 + NB;                  // loads per wave and stage (A: 4, B: NB)
+    constexpr int SB = g4_stage_bytes(BN);
     extern __shared__ __align__(16) char g4s[];   // [stage][A tile, B tile]
     // tile order: the workgroups that share an operand tile run on one XCD back to back
     const int w = blockIdx.x, xcd = w % kXcds, local = w / kXcds;
@@ -372,86 +379,91 @@ __global__ __launch_bounds__(256, 1) void k_gemm4(const bf16_t *__restrict__ A, 
         nt = local % NT;
         if (mt >= MT) return;
     }
-    const int64_t m0 = (int64_t)mt * G4T, n0 = (int64_t)nt * G4T;
+    const int64_t m0 = (int64_t)mt * G4T, n0 = (int64_t)nt * BN;
     const int64_t kb = (int64_t)z * kchunk;
     const int64_t ke = kb + kchunk < K ? kb + kchunk : K;
     const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int ln = lane & 31, hh = lane >> 5;
     const int wm = wave >> 1, wn = wave & 1;
 
-    const G4Operand<AK> oa{Buf(A, a_bytes), sa, m0, M, ke};
-    const G4Operand<BK> ob{Buf(Bm, b_bytes), sb, n0, N, ke};
+    const G4Operand<AK, G4T> oa{Buf(A, a_bytes), sa, m0, M, ke};
+    const G4Operand<BK, BN> ob{Buf(Bm, b_bytes), sb, n0, N, ke};
     const uint32_t lds0 = (uint32_t)reinterpret_cast<uintptr_t>(g4s);
-    auto stA = [&](int st) { return lds0 + (uint32_t)(st * 2 * G4OP * 2); };
-    auto stB = [&](int st) { return lds0 + (uint32_t)(st * 2 * G4OP * 2 + G4OP * 2); };
+    auto stA = [&](int st) { return lds0 + (uint32_t)(st * SB); };
+    auto stB = [&](int st) { return lds0 + (uint32_t)(st * SB + G4T * G4K * 2); };
 
-    f32x16_t acc[4][4];   // [n block j][m block i]: D^T[n][m]
+    f32x16_t acc[NB][4];   // [n block j][m block i]: D^T[n][m]
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < NB; ++j)
 #pragma unroll
         for (int i = 0; i < 4; ++i) acc[j][i] = f32x16_t{0};
 
     const int nsteps = (int)((ke - kb + G4K - 1) / G4K);
-    auto frags = [&](int st, int ks, uint4 (&av)[4], uint4 (&bv)[4]) {
-        const char *ta = g4s + st * 2 * G4OP * 2, *tb = ta + G4OP * 2;
+    auto frags = [&](int st, int ks, uint4 (&av)[4], uint4 (&bv)[NB]) {
+        const char *ta = g4s + st * SB, *tb = ta + G4T * G4K * 2;
 #pragma unroll
         for (int i = 0; i < 4; ++i) av[i] = oa.frag(ta, wm * 128 + i * 32, ks, lane);
 #pragma unroll
-        for (int jn = 0; jn < 4; ++jn) bv[jn] = ob.frag(tb, wn * 128 + jn * 32, ks, lane);
+        for (int jn = 0; jn < NB; ++jn) bv[jn] = ob.frag(tb, wn * (BN / 2) + jn * 32, ks, lane);
     };
-    auto products = [&](const uint4 (&av)[4], const uint4 (&bv)[4]) {
+    auto products = [&](const uint4 (&av)[4], const uint4 (&bv)[NB]) {
 #pragma unroll
-        for (int jn = 0; jn < 4; ++jn)
+        for (int jn = 0; jn < NB; ++jn)
 #pragma unroll
             for (int i = 0; i < 4; ++i) acc[jn][i] = mfma32x32x16(as_bf16x8(bv[jn]), as_bf16x8(av[i]), acc[jn][i]);
     };
     // Software pipeline over K steps of two 16-deep halves (h0, h1).  Iteration j: read h1 of step
-    // j while h0's products run; wait for step j + 1 and barrier (stage j % 4 is then fully read
-    // into registers by every wave); then h1's 16 products, with the 8 loads that refill stage
-    // j % 4 with step j + 4 between the first 8 and the reads of h0 of step j + 1 between the
-    // last 8.  Issued as one burst after the barrier, the four waves' 32 loads queue at the
-    // texture unit and hold up the products behind them; spread out, they overlap (12% on the
-    // head's three products).  Steps past the end are loaded out of range into stages that are
-    // never read.
+    // j while h0's products run; wait for step j + 1 and barrier (stage j % S is then fully read
+    // into registers by every wave); then h1's products, with the loads that refill stage j % S
+    // with step j + S and the reads of h0 of step j + 1 spread between them.  Issued as one burst
+    // after the barrier, the four waves' loads queue at the texture unit and hold up the products
+    // behind them; spread out, they overlap.  Steps past the end are loaded out of range into
+    // stages that are never read.
 #pragma unroll
-    for (int s = 0; s < G4S; ++s) {
+    for (int s = 0; s < S; ++s) {
         oa.issue(kb + (int64_t)s * G4K, stA(s), wave, lane);
         ob.issue(kb + (int64_t)s * G4K, stB(s), wave, lane);
     }
-    uint4 a0[4], b0[4], a1[4], b1[4];
-    wait_vmcnt<8 * (G4S - 1)>();   // this wave's loads of step 0 have landed
+    uint4 a0[4], b0[NB], a1[4], b1[NB];
+    wait_vmcnt<LPW * (S - 1)>();   // this wave's loads of step 0 have landed
     __syncthreads();               // everyone's have
     frags(0, 0, a0, b0);
+    constexpr int NP = 4 * NB;                   // products of a half step
+    constexpr int NA = 8 + 2 * NB;               // loads and fragment reads to spread over them
     for (int j = 0; j < nsteps; ++j) {
-        const int st = j % G4S;
+        const int st = j % S;
         frags(st, 1, a1, b1);
         __builtin_amdgcn_sched_barrier(0);   // the reads go ahead of the products they overlap
         products(a0, b0);
         __builtin_amdgcn_sched_barrier(0);
-        wait_vmcnt<8 * (G4S - 2)>();   // this wave's loads of step j + 1 have landed
-        __syncthreads();               // everyone's have; stage j % 4 is read out
-        const char *ta = g4s + ((j + 1) % G4S) * 2 * G4OP * 2, *tb = ta + G4OP * 2;
-        const int64_t kn = kb + (int64_t)(j + G4S) * G4K;
+        wait_vmcnt<LPW * (S - 2)>();   // this wave's loads of step j + 1 have landed
+        __syncthreads();               // everyone's have; stage j % S is read out
+        const char *ta = g4s + ((j + 1) % S) * SB, *tb = ta + G4T * G4K * 2;
+        const int64_t kn = kb + (int64_t)(j + S) * G4K;
 #pragma unroll
-        for (int s = 0; s < 16; ++s) {
-            const int jn = s >> 2, i = s & 3;
+        for (int s = 0; s < NP; ++s) {
+            const int jn = s / 4, i = s % 4;
             acc[jn][i] = mfma32x32x16(as_bf16x8(b1[jn]), as_bf16x8(a1[i]), acc[jn][i]);
-            if (s < 4) oa.issue1(kn, stA(st), wave, lane, s);
-            else if (s < 8) ob.issue1(kn, stB(st), wave, lane, s - 4);
-            else if (s < 12) a0[s - 8] = oa.frag(ta, wm * 128 + (s - 8) * 32, 0, lane);   // past the last
-            else b0[s - 12] = ob.frag(tb, wn * 128 + (s - 12) * 32, 0, lane);               // step: unused
+#pragma unroll
+            for (int a = s * NA / NP; a < (s + 1) * NA / NP; ++a) {
+                if (a < 4) oa.issue1(kn, stA(st), wave, lane, a);
+                else if (a < 4 + NB) ob.issue1(kn, stB(st), wave, lane, a - 4);
+                else if (a < 8 + NB) a0[a - 4 - NB] = oa.frag(ta, wm * 128 + (a - 4 - NB) * 32, 0, lane);   // past the
+                else b0[a - 8 - NB] = ob.frag(tb, wn * (BN / 2) + (a - 8 - NB) * 32, 0, lane);          // last: unused
+            }
             __builtin_amdgcn_sched_barrier(0);
         }
     }
     wait_vmcnt<0>();   // no load may still be writing LDS
     __syncthreads();   // and no wave still reads a stage: the LDS now stages the output
 
-    // Loss gradient (EPI_BF16_BCE): the tile's targets as a bitmap [256 rows][8 words] behind the
-    // staged half-tile (ids outside [n0, n0 + 256) or [0, N) ignored, repeats set the same bit);
-    // the sigmoid is taken while staging.
-    uint32_t *tbits = reinterpret_cast<uint32_t *>(g4s + 128 * G4T * 2);
+    // Loss gradient (EPI_BF16_BCE): the tile's targets as a bitmap [256 rows][BN / 32 words]
+    // behind the staged half-tile (ids outside [n0, n0 + BN) or [0, N) ignored, repeats set the
+    // same bit); the sigmoid is taken while staging.
+    constexpr int TW = BN / 32;                          // target words per row
+    uint32_t *tbits = reinterpret_cast<uint32_t *>(g4s + 128 * BN * 2);
     if constexpr (EPI == EPI_BF16_BCE) {
-        for (int e = threadIdx.x; e < G4T * 8; e += 256) tbits[e] = 0u;
+        for (int e = threadIdx.x; e < G4T * TW; e += 256) tbits[e] = 0u;
         __syncthreads();
         // one row per thread; its ids 8 at a time, all 8 loads in flight before any is used
         const int r = threadIdx.x;
@@ -463,21 +475,22 @@ __global__ __launch_bounds__(256, 1) void k_gemm4(const bf16_t *__restrict__ A, 
             for (int u = 0; u < 8; ++u) id[u] = live && p0 + u < P ? pr[p0 + u] : -1;
 #pragma unroll
             for (int u = 0; u < 8; ++u)
-                if (id[u] >= n0 && id[u] < n0 + G4T && id[u] < N) {
+                if (id[u] >= n0 && id[u] < n0 + BN && id[u] < N) {
                     const int c = (int)(id[u] - n0);
-                    atomicOr(&tbits[r * 8 + (c >> 5)], 1u << (c & 31));
+                    atomicOr(&tbits[r * TW + (c >> 5)], 1u << (c & 31));
                 }
         }
         __syncthreads();   // the bitmap is complete
     }
 
-    // Output: one 128-row half of the tile at a time goes through LDS as [128 rows][256 columns]
-    // (16-byte chunk c of row r at c ^ (r % 32): the 32 rows one store-to-LDS instruction touches
-    // fall in distinct banks), then leaves as whole row pieces of 512 B (bf16) or 1 KB (fp32),
-    // 1 KB per store instruction.
+    // Output: one 128-row half of the tile at a time goes through LDS as [128 rows][BN columns]
+    // (16-byte chunk c of row r at c ^ (r % XM + 1): the rows one store-to-LDS instruction touches
+    // spread over the banks), then leaves as whole row pieces of BN elements, 1 KB per store
+    // instruction.
     constexpr bool BF = EPI == EPI_BF16_BIAS || EPI == EPI_BF16_BCE;   // bf16 output
     constexpr int OB = BF ? 2 : 4;                      // output bytes per element
-    constexpr int RB = G4T * OB;                        // bytes per staged row
+    constexpr int RB = BN * OB;                         // bytes per staged row
+    constexpr int XM = RB / 16 - 1 < 31 ? RB / 16 - 1 : 31;   // chunk swizzle mask
     constexpr int RPI = 1024 / RB;                      // rows per store instruction
     char *eb = g4s;
     float *Cf = reinterpret_cast<float *>(C) + (EPI == EPI_F32_PART ? (int64_t)z * M * N : 0);
@@ -488,10 +501,10 @@ __global__ __launch_bounds__(256, 1) void k_gemm4(const bf16_t *__restrict__ A, 
         if (wm == h) {
             // D^T[n = 8r + 4hh + q][m = ln] per 32x32 block: 4 consecutive columns per lane and r
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
+            for (int j = 0; j < NB; ++j)
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                    const int nl = wn * 128 + j * 32 + 8 * r + 4 * hh;
+                    const int nl = wn * (BN / 2) + j * 32 + 8 * r + 4 * hh;
                     float4 b = make_float4(0.f, 0.f, 0.f, 0.f);
                     if (BF && bias && n0 + nl < N)
                         b = *reinterpret_cast<const float4 *>(bias + n0 + nl);   // 16-byte aligned
@@ -500,11 +513,11 @@ __global__ __launch_bounds__(256, 1) void k_gemm4(const bf16_t *__restrict__ A, 
                     for (int i = 0; i < 4; ++i) {
                         const int ml = i * 32 + ln;
                         const f32x16_t &d = acc[j][i];
-                        char *p = eb + ml * RB + ((((byte >> 4) ^ (ml & 31)) << 4) | (byte & 15));
+                        char *p = eb + ml * RB + ((((byte >> 4) ^ (ml & XM)) << 4) | (byte & 15));
                         float4 v = make_float4(d[4 * r + 0] + b.x, d[4 * r + 1] + b.y, d[4 * r + 2] + b.z,
                                                d[4 * r + 3] + b.w);
                         if constexpr (EPI == EPI_BF16_BCE) {   // sigmoid, minus the targets of these 4 columns
-                            const uint32_t tb = tbits[(128 * h + ml) * 8 + (nl >> 5)] >> (nl & 31);
+                            const uint32_t tb = tbits[(128 * h + ml) * TW + (nl >> 5)] >> (nl & 31);
                             v = make_float4(sigmoid_f32(v.x), sigmoid_f32(v.y), sigmoid_f32(v.z), sigmoid_f32(v.w));
                             v.x -= (float)(tb & 1u);
                             v.y -= (float)((tb >> 1) & 1u);
@@ -524,25 +537,25 @@ __global__ __launch_bounds__(256, 1) void k_gemm4(const bf16_t *__restrict__ A, 
         const int rl = lane / (64 / RPI), c = lane % (64 / RPI);
         const int64_t n = n0 + (int64_t)c * (16 / OB);
         constexpr int NI = 128 / RPI / 4;                   // store instructions per wave
-        constexpr int NB = 8;                               // issued in batches: reads, then stores
+        constexpr int NBAT = NI < 8 ? NI : 8;               // issued in batches: reads, then stores
 #pragma unroll
-        for (int t0 = 0; t0 < NI; t0 += NB) {
-            uint4 v[NB];
+        for (int t0 = 0; t0 < NI; t0 += NBAT) {
+            uint4 v[NBAT];
 #pragma unroll
-            for (int t = 0; t < NB; ++t) {
+            for (int t = 0; t < NBAT; ++t) {
                 const int row = RPI * (4 * (t0 + t) + wave) + rl;
-                v[t] = *reinterpret_cast<const uint4 *>(eb + row * RB + ((c ^ (row & 31)) << 4));
+                v[t] = *reinterpret_cast<const uint4 *>(eb + row * RB + ((c ^ (row & XM)) << 4));
             }
 #pragma unroll
-            for (int t = 0; t < NB; ++t) {
+            for (int t = 0; t < NBAT; ++t) {
                 const int64_t m = m0 + 128 * h + RPI * (4 * (t0 + t) + wave) + rl;
                 if (m < M && n < N) {
                     // outputs written once and not read again soon: streaming stores
-                    const u32x4_t w = __builtin_bit_cast(u32x4_t, v[t]);
+                    const u32x4_t wv = __builtin_bit_cast(u32x4_t, v[t]);
                     if (BF)
-                        __builtin_nontemporal_store(w, reinterpret_cast<u32x4_t *>(Cb + m * ldo + n));
+                        __builtin_nontemporal_store(wv, reinterpret_cast<u32x4_t *>(Cb + m * ldo + n));
                     else if (EPI == EPI_F32)
-                        __builtin_nontemporal_store(w, reinterpret_cast<u32x4_t *>(Cf + m * ldo + n));
+                        __builtin_nontemporal_store(wv, reinterpret_cast<u32x4_t *>(Cf + m * ldo + n));
                     else
                         *reinterpret_cast<uint4 *>(Cf + m * ldo + n) = v[t];
                 }
@@ -616,7 +629,7 @@ int64_t head_splits(int64_t B, int64_t F_s, int64_t H, int64_t tm, int64_t tn, i
 }
 int64_t head_splits_for(int64_t B, int64_t F_s, int64_t H, int32_t dtype, bool big) {
     if (dtype != HASTE_DTYPE_BF16) return head_splits(B, F_s, H, 64, 64, 512, false);
-    return big ? head_splits(B, F_s, H, G4T, G4T, kXcds * kCusPerXcd, true)
+    return big ? head_splits(B, F_s, H, G4T, kHeadBN, kXcds * kCusPerXcd * (kHeadBN == 128 ? 2 : 1), true)
                : head_splits(B, F_s, H, TM, TN, 512, false);
 }
 
@@ -637,19 +650,20 @@ bool gemm4_ok(int64_t B, int64_t F_s, int64_t H, std::initializer_list<const voi
 }
 
 // C[M, N] (+)= A B over K, split into Z chunks of kchunk (a multiple of the K step); sa, sb are
-// the operands' row strides (elements)
+// the operands' row strides (elements).  256 x kHeadBN output tiles.
 template <bool AK, bool BK, int EPI>
 hipError_t launch_gemm4(hipStream_t s, const bf16_t *A, int64_t sa, int64_t a_elems, const bf16_t *Bm, int64_t sb,
                         int64_t b_elems, void *C, int64_t ldc, const float *bias, int64_t M, int64_t N, int64_t K,
                         int64_t kchunk, int Z, const int32_t *pos = nullptr, int P = 0) {
-    const int MT = (int)haste::cdiv(M, G4T), NT = (int)haste::cdiv(N, G4T);
+    constexpr int BN = kHeadBN;
+    const int MT = (int)haste::cdiv(M, G4T), NT = (int)haste::cdiv(N, BN);
     const int64_t grid = Z > 1 ? haste::round_up(Z, kXcds) * MT * NT
                                : (MT <= NT ? haste::round_up(NT, kXcds) * MT : haste::round_up(MT, kXcds) * NT);
-    auto kern = k_gemm4<AK, BK, EPI>;
+    auto kern = k_gemm4<BN, AK, BK, EPI>;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)kG4Lds);
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)g4_lds(BN));
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(256), kG4Lds, s, A, sa, (uint32_t)(a_elems * 2), Bm, sb,
+    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(256), g4_lds(BN), s, A, sa, (uint32_t)(a_elems * 2), Bm, sb,
                        (uint32_t)(b_elems * 2), C, ldc, bias, M, N, K, kchunk, MT, NT, Z, pos, P);
     return hipGetLastError();
 }

@@ -36,7 +36,8 @@ def test_profiled_kernels_are_charged_to_their_calls():
         return {c for c, pats in bench.CALL_KERNELS.items() if any(re.match(p, kernel) for p in pats)}
     assert owners("k_fwd_bce<64, false, 1, false>") == {"fwd_bce", "tail_step"}
     assert owners("k_fwd_bce<128, true, 2, true>") == {"fwd_bce_sgd", "tail_step_sgd"}
-    assert owners("k_gemm4<true, true, 3>") == {"head_fwd_bce"}
-    assert owners("k_gemm4<true, true, 0>") == {"head_fwd"}
+    assert owners("k_gemm4<128, true, true, 3>") == {"head_fwd_bce"}
+    assert owners("k_gemm4<128, true, true, 0>") == {"head_fwd"}
+    assert owners("k_gemm4<128, true, false, 2>") == {"head_bwd"}
     assert owners("k_bwd_x<64, 1>") == {"bwd_x", "tail_step", "tail_step_sgd"} and owners("k_transpose_w") == {"bwd_x"}
     assert "head_bwd" in owners("k_reduce_rmajor") and "bwd_x" in owners("k_reduce_fmajor")
