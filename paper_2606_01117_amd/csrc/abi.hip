@@ -72,6 +72,19 @@ int report(int code, const char *fmt, ...) {
 
 namespace {
 
+// the forward kernel for a layer: small groups (G = 1, 2, 4, 8) on their own matrix-core kernel,
+// larger ones on the gather-once kernel, the rest (fp32, other G) on the vector ALUs
+bool fwd_kernel_exists(const haste::TailArgs &a) {
+    return haste::fwd_sg_supported(a) || haste::fwd_mfma_supported(a) || haste::valu_supported(a);
+}
+
+hipError_t fwd_any(const haste::TailArgs &a, const void *X, const int32_t *idx, const void *W, const float *bias,
+                   void *Y, hipStream_t s) {
+    if (haste::fwd_sg_supported(a)) return haste::fwd_sg(a, X, idx, W, bias, Y, s);
+    if (haste::fwd_mfma_supported(a)) return haste::fwd_mfma(a, X, idx, W, bias, Y, s);
+    return haste::fwd_valu(a, X, idx, W, bias, Y, s);
+}
+
 #define TRY(x)                      \
     do {                            \
         int _rc = (x);              \
@@ -145,9 +158,8 @@ int haste_fwd(const haste_desc_t *d, const void *X, const int32_t *idx, const vo
     TRY(need_ptr(W, "W"));
     TRY(need_ptr(Y, "Y"));
     if (bias && !aligned16(bias)) return fail(HASTE_ERR_INVALID, "bias is not 16-byte aligned");
-    if (haste::fwd_mfma_supported(a)) return hip_status(haste::fwd_mfma(a, X, idx, W, bias, Y, as_stream(stream)), "haste_fwd");
-    if (!haste::valu_supported(a)) return fail(HASTE_ERR_UNSUPPORTED, "no forward kernel for this shape");
-    return hip_status(haste::fwd_valu(a, X, idx, W, bias, Y, as_stream(stream)), "haste_fwd");
+    if (!fwd_kernel_exists(a)) return fail(HASTE_ERR_UNSUPPORTED, "no forward kernel for this shape");
+    return hip_status(fwd_any(a, X, idx, W, bias, Y, as_stream(stream)), "haste_fwd");
 }
 
 int haste_bwd_w(const haste_desc_t *d, const void *X, const int32_t *idx, const void *dY, float *dW, float *dbias,
@@ -277,9 +289,8 @@ int haste_fwd_bce(const haste_desc_t *d, const void *X, const int32_t *idx, cons
         return hip_status(haste::fwd_bce_mfma(a, X, idx, W, bias, P > 0 ? pos : nullptr, P, dY, dW, dbias, beta, ws, s),
                           "haste_fwd_bce");
     // composed: logits into dY, the gradient in place, then the backward-weight product
-    const bool fm = haste::fwd_mfma_supported(a);
-    if (!fm && !haste::valu_supported(a)) return fail(HASTE_ERR_UNSUPPORTED, "no forward kernel for this shape");
-    hipError_t e = fm ? haste::fwd_mfma(a, X, idx, W, bias, dY, s) : haste::fwd_valu(a, X, idx, W, bias, dY, s);
+    if (!fwd_kernel_exists(a)) return fail(HASTE_ERR_UNSUPPORTED, "no forward kernel for this shape");
+    hipError_t e = fwd_any(a, X, idx, W, bias, dY, s);
     if (e == hipSuccess) e = haste::bce_grad(a.B, a.L, a.dtype, dY, P > 0 ? pos : nullptr, P, dY, s);
     if (e == hipSuccess && dW)
         e = bw_mfma ? haste::bwd_w_mfma(a, X, idx, dY, dW, dbias, beta, ws, s)

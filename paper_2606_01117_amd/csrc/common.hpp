@@ -137,6 +137,10 @@ int report(int code, const char *fmt, ...);
 bool fwd_mfma_supported(const TailArgs &a);
 hipError_t fwd_mfma(const TailArgs &a, const void *X, const int32_t *idx, const void *W, const float *bias,
                     void *Y, hipStream_t s);
+// forward for small groups (G = 1, 2, 4, 8), 16 / G groups per matrix tile
+bool fwd_sg_supported(const TailArgs &a);
+hipError_t fwd_sg(const TailArgs &a, const void *X, const int32_t *idx, const void *W, const float *bias, void *Y,
+                  hipStream_t s);
 bool bwd_w_mfma_supported(const TailArgs &a);
 size_t bwd_w_mfma_ws(const TailArgs &a);
 hipError_t bwd_w_mfma(const TailArgs &a, const void *X, const int32_t *idx, const void *dY, float *dW,

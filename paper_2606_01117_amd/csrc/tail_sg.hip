@@ -1,0 +1,254 @@
+// Forward logits of the tail for small groups (G = 1, 2, 4, 8; bf16), on the matrix cores.
+//
+// Section 3.2's gather-once pays off in proportion to G: with a few labels per group, the work is
+// the gather of X[:, I_k] for every group, and a 16- or 32-label matrix tile would sit mostly on
+// one group's few labels.  Here one v_mfma_f32_16x16x32_bf16 tile covers 16 labels = 16 / G whole
+// groups: its K = 32 positions are 2G slots of each of those groups, and the weight operand is
+// block-diagonal (label n's weights sit only in the K positions of its own group; zeros
+// elsewhere).  So each (group, slot, row) value is gathered exactly once, and the matrix core's
+// extra zero products cost nothing that matters next to the gather.
+//   M = 16 batch rows, N = 16 labels, K = 32 (group-slot pairs).
+//   A (rows x K): gathered with ds_read_b64_tr_b16 from an X^T slab [F_s][32 rows] in LDS: source
+//     lane 4j + a of each 16-lane group names K position 8q + j (and 8q + 4 + j) at rows 4a .. 4a+3,
+//     so result lane (row l16, q) holds row l16 at K positions 8q .. 8q+7.
+//   B (K x labels): lane (label n, q) holds K positions 8q .. 8q+7; the ones of n's group carry
+//     W[n, slot], the others are zero.
+//   D: lane (label n, q) holds rows 4q .. 4q+3 of label n.
+// A workgroup of 8 waves keeps one 32-row slab of X^T for its whole segment of labels and sweeps it
+// in passes of 128 labels (one 16-label tile per wave): the pass's supports and weights are staged
+// in LDS (prefetched into registers during the previous pass), and its logits leave through LDS
+// as 256-byte row runs.  The batch slabs of a segment run on one XCD, sharing W through its L2.
+#include "common.hpp"
+
+namespace {
+
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+constexpr int kSgWaves = 8;
+constexpr int kSgThreads = 64 * kSgWaves;
+constexpr int kSgRows = 32;                     // batch rows per slab
+constexpr int kSgXRow = 80;                     // bytes per staged X^T feature row (32 rows + pad)
+constexpr int kSgPass = 16 * kSgWaves;          // labels per pass
+constexpr int kSgOutRow = kSgPass * 2 + 16;     // bytes per staged output row (bf16 + pad)
+
+__device__ __forceinline__ uint2 tr_read(const char *p) {
+    return lds_read_tr(p);
+}
+
+template <int G, int F_IN>
+struct SgGeom {
+    static constexpr int PG = kSgPass / G;                      // groups per pass
+    static constexpr int NS = F_IN / (2 * G);                   // K steps per tile
+    static constexpr int IDX_BYTES = PG * F_IN * 4;             // staged supports per pass
+    static constexpr int W_BYTES = kSgPass * F_IN * 2;          // staged weights per pass
+    static constexpr int IC = IDX_BYTES / 16, WC = W_BYTES / 16;   // 16-byte chunks
+    static constexpr int IL = (IC + kSgThreads - 1) / kSgThreads;  // prefetch loads per thread
+    static constexpr int WL = (WC + kSgThreads - 1) / kSgThreads;
+};
+
+template <int G, int F_IN>
+static size_t sg_lds(int F_s) {
+    using S = SgGeom<G, F_IN>;
+    return (size_t)F_s * kSgXRow + S::IDX_BYTES + S::W_BYTES + (size_t)kSgRows * kSgOutRow;
+}
+
+template <int G, int F_IN, bool HAS_BIAS>
+__global__ __launch_bounds__(kSgThreads) void k_fwd_sg(const bf16_t *__restrict__ X, const int32_t *__restrict__ idx,
+                                                       const bf16_t *__restrict__ W, const float *__restrict__ bias,
+                                                       bf16_t *__restrict__ Y, int B, int F_s, int64_t L, int nbt,
+                                                       int64_t pps, int64_t npass) {
+    using S = SgGeom<G, F_IN>;
+    extern __shared__ __align__(16) char sgs[];
+    char *xs = sgs;                                               // [F_s][kSgXRow]
+    int32_t *sidx = reinterpret_cast<int32_t *>(sgs + (size_t)F_s * kSgXRow);   // [PG][F_IN]
+    char *sw = reinterpret_cast<char *>(sidx) + S::IDX_BYTES;    // [128 labels][F_IN] bf16
+    char *so = sw + S::W_BYTES;                                   // [32 rows][kSgOutRow]
+    const int w = blockIdx.x, xcd = w % kXcds, jj = w / kXcds;
+    const int bt = jj % nbt;
+    const int64_t seg = (int64_t)(jj / nbt) * kXcds + xcd;
+    const int64_t p_begin = seg * pps, p_end = p_begin + pps < npass ? p_begin + pps : npass;
+    if (p_begin >= p_end) return;   // workgroup-uniform
+    const int b0 = bt * kSgRows;
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int l16 = lane & 15, q = lane >> 4;
+
+    // the slab's X^T: 16-byte row pieces of X, scattered into feature rows (zero past B)
+    {
+        const int cpr = F_s / 8;   // 16-byte chunks per X row
+        for (int c = tid; c < kSgRows * cpr; c += kSgThreads) {
+            const int r = c / cpr, f8 = (c - r * cpr) * 8;
+            uint4 v = make_uint4(0u, 0u, 0u, 0u);
+            if (b0 + r < B) v = *reinterpret_cast<const uint4 *>(X + (int64_t)(b0 + r) * F_s + f8);
+            const uint32_t u[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                *reinterpret_cast<bf16_t *>(xs + (f8 + e) * kSgXRow + r * 2) =
+                    (bf16_t)((e & 1) ? (u[e >> 1] >> 16) : (u[e >> 1] & 0xffffu));
+        }
+    }
+
+    // pass staging, prefetched into registers: supports of the pass's groups, weights of its labels
+    uint4 pi[S::IL], pw[S::WL];
+    auto fetch = [&](int64_t p) {
+        const int64_t l0 = p * kSgPass;
+        const int64_t g0 = l0 / G;
+        const int64_t ng = (L - l0 < kSgPass ? L - l0 : kSgPass) / G;   // groups of the pass in the layer
+        const Buf ib(idx + g0 * F_IN, (uint32_t)(ng * F_IN * 4));
+        const Buf wb(W + l0 * F_IN, (uint32_t)(ng * G * F_IN * 2));
+#pragma unroll
+        for (int i = 0; i < S::IL; ++i) pi[i] = ib.ld16((uint32_t)(tid + kSgThreads * i) * 16);   // past: zero
+#pragma unroll
+        for (int i = 0; i < S::WL; ++i) pw[i] = wb.ld16((uint32_t)(tid + kSgThreads * i) * 16);
+    };
+    auto stage = [&]() {
+#pragma unroll
+        for (int i = 0; i < S::IL; ++i)
+            if (tid + kSgThreads * i < S::IC)
+                *reinterpret_cast<uint4 *>(reinterpret_cast<char *>(sidx) + (tid + kSgThreads * i) * 16) = pi[i];
+#pragma unroll
+        for (int i = 0; i < S::WL; ++i)
+            if (tid + kSgThreads * i < S::WC) *reinterpret_cast<uint4 *>(sw + (tid + kSgThreads * i) * 16) = pw[i];
+    };
+
+    // this lane's roles: gather source (K position 8q + j, rows 4a ..) and weight operand window
+    const int j = l16 >> 2, a = l16 & 3;
+    const int klo = 8 * q + j, khi = klo + 4;
+    const int n_grp = l16 / G;                       // this label's group within the tile
+    // K positions of the label's group: [2G n_grp, 2G n_grp + 2G); this lane's octet [8q, 8q + 8)
+    const int kg0 = 2 * G * n_grp;
+    const bool wact = kg0 < 8 * q + 8 && kg0 + 2 * G > 8 * q;
+
+    fetch(p_begin);
+    for (int64_t p = p_begin; p < p_end; ++p) {
+        __syncthreads();   // the previous pass's staging and output are no longer read
+        stage();
+        __syncthreads();
+        if (p + 1 < p_end) fetch(p + 1);
+        const int64_t l0 = p * kSgPass + 16 * wave;     // this wave's tile
+        f32x4_t acc[2];
+        {
+            const float bv = HAS_BIAS && l0 + l16 < L ? bias[l0 + l16] : 0.0f;
+            acc[0] = acc[1] = f32x4_t{bv, bv, bv, bv};
+        }
+        if (l0 < L) {   // wave-uniform
+            const int32_t *ti = sidx + (16 * wave / G) * F_IN;    // the tile's groups' supports
+            const char *tw = sw + (16 * wave + l16) * F_IN * 2;   // this lane's label's weights
+#pragma unroll
+            for (int s = 0; s < S::NS; ++s) {
+                const int flo = ti[(klo / (2 * G)) * F_IN + s * 2 * G + klo % (2 * G)];
+                const int fhi = ti[(khi / (2 * G)) * F_IN + s * 2 * G + khi % (2 * G)];
+                uint4 bw = make_uint4(0u, 0u, 0u, 0u);
+                if constexpr (G >= 4) {
+                    // the whole octet is one group's: 8 consecutive slots
+                    if (wact) bw = *reinterpret_cast<const uint4 *>(tw + (s * 2 * G + (8 * q) % (2 * G)) * 2);
+                } else if constexpr (G == 2) {
+                    // 4 slots of the label's group at octet position 0 or 4
+                    if (wact) {
+                        const uint2 v = *reinterpret_cast<const uint2 *>(tw + s * 4 * 2);
+                        if (kg0 == 8 * q) bw = make_uint4(v.x, v.y, 0u, 0u);
+                        else bw = make_uint4(0u, 0u, v.x, v.y);
+                    }
+                } else {
+                    // 2 slots at octet position 0, 2, 4 or 6
+                    if (wact) {
+                        const uint32_t v = *reinterpret_cast<const uint32_t *>(tw + s * 2 * 2);
+                        const int pos = (kg0 - 8 * q) >> 1;
+                        bw = make_uint4(pos == 0 ? v : 0u, pos == 1 ? v : 0u, pos == 2 ? v : 0u, pos == 3 ? v : 0u);
+                    }
+                }
+#pragma unroll
+                for (int m = 0; m < 2; ++m) {
+                    const uint2 lo = tr_read(xs + flo * kSgXRow + (16 * m + 4 * a) * 2);
+                    const uint2 hi = tr_read(xs + fhi * kSgXRow + (16 * m + 4 * a) * 2);
+                    acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y)),
+                                                                     as_bf16x8(bw), acc[m], 0, 0, 0);
+                }
+            }
+        }
+        // logits of rows 16m + 4q + r, label 16 wave + l16, into the pass's output block
+#pragma unroll
+        for (int m = 0; m < 2; ++m)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+                *reinterpret_cast<bf16_t *>(so + (16 * m + 4 * q + r) * kSgOutRow + (16 * wave + l16) * 2) =
+                    f32_to_bf16(acc[m][r]);
+        __syncthreads();
+        // 32 rows x 256 bytes: one 16-byte chunk per thread (16 chunks per row)
+        {
+            const int r = tid >> 4, c = tid & 15;
+            const int64_t lb = p * kSgPass + 8 * c;
+            if (b0 + r < B && lb < L) {
+                const uint4 v = *reinterpret_cast<const uint4 *>(so + r * kSgOutRow + c * 16);
+                bf16_t *dst = Y + (int64_t)(b0 + r) * L + lb;
+                if (lb + 8 <= L) {
+                    __builtin_nontemporal_store(__builtin_bit_cast(u32x4_t, v), reinterpret_cast<u32x4_t *>(dst));
+                } else {
+                    const uint32_t u[4] = {v.x, v.y, v.z, v.w};
+                    for (int e = 0; lb + e < L; ++e) dst[e] = (bf16_t)((e & 1) ? (u[e >> 1] >> 16) : (u[e >> 1] & 0xffffu));
+                }
+            }
+        }
+    }
+}
+
+template <int G, int F_IN>
+static hipError_t launch_fwd_sg(const haste::TailArgs &a, const void *X, const int32_t *idx, const void *W,
+                                const float *bias, void *Y, hipStream_t s) {
+    const size_t lds = sg_lds<G, F_IN>((int)a.F_s);
+    const int nbt = (int)haste::cdiv(a.B, kSgRows);
+    const int64_t npass = haste::cdiv(a.L, kSgPass);
+    // one workgroup per CU (the slab and the pass staging take most of the LDS), each sweeping a
+    // segment of passes; segments a multiple of the XCD count
+    int64_t nseg = haste::round_up(haste::cdiv(kXcds * kCusPerXcd, nbt), kXcds);
+    const int64_t max_seg = haste::round_up(npass, kXcds);
+    if (nseg > max_seg) nseg = max_seg;
+    const int64_t pps = haste::cdiv(npass, nseg);
+    auto go = [&](auto kern) {
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(kern, dim3((unsigned)(nseg * nbt)), dim3(kSgThreads), lds, s, (const bf16_t *)X, idx,
+                           (const bf16_t *)W, bias, (bf16_t *)Y, (int)a.B, (int)a.F_s, a.L, nbt, pps, npass);
+        return hipGetLastError();
+    };
+    return bias ? go(k_fwd_sg<G, F_IN, true>) : go(k_fwd_sg<G, F_IN, false>);
+}
+
+template <int G>
+static hipError_t fwd_sg_g(const haste::TailArgs &a, const void *X, const int32_t *idx, const void *W,
+                           const float *bias, void *Y, hipStream_t s) {
+    switch (a.F_in) {
+        case 32: return launch_fwd_sg<G, 32>(a, X, idx, W, bias, Y, s);
+        case 64: return launch_fwd_sg<G, 64>(a, X, idx, W, bias, Y, s);
+        case 128:
+            if constexpr (G >= 2) return launch_fwd_sg<G, 128>(a, X, idx, W, bias, Y, s);
+            break;
+    }
+    return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+namespace haste {
+
+// bf16, G in {1, 2, 4, 8}, F_in in {32, 64} (and 128 for G >= 2: the pass's staged supports and
+// weights then still fit the LDS beside the slab), F_s a multiple of 8 up to kMaxFs, and the
+// logits' row offsets within the 31-bit range of a row pointer.
+bool fwd_sg_supported(const TailArgs &a) {
+    if (a.dtype != HASTE_DTYPE_BF16 || !(a.G == 1 || a.G == 2 || a.G == 4 || a.G == 8)) return false;
+    if (!(a.F_in == 32 || a.F_in == 64 || (a.F_in == 128 && a.G >= 2))) return false;
+    return a.F_s % 8 == 0 && a.F_s <= kMaxFs && a.L < ((int64_t)1 << 40);
+}
+
+hipError_t fwd_sg(const TailArgs &a, const void *X, const int32_t *idx, const void *W, const float *bias, void *Y,
+                  hipStream_t s) {
+    switch (a.G) {
+        case 1: return fwd_sg_g<1>(a, X, idx, W, bias, Y, s);
+        case 2: return fwd_sg_g<2>(a, X, idx, W, bias, Y, s);
+        case 4: return fwd_sg_g<4>(a, X, idx, W, bias, Y, s);
+        case 8: return fwd_sg_g<8>(a, X, idx, W, bias, Y, s);
+    }
+    return hipErrorInvalidValue;
+}
+
+}  // namespace haste

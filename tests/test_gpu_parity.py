@@ -59,6 +59,13 @@ SMALL = [
     ("bf16_g72_f32", 48, 384, 72 * 29, 72, 32, BF16),
     # 12-label groups (4-label stores) with a 128-slot support
     ("bf16_g12_f128", 45, 512, 12 * 37, 12, 128, BF16),
+    # small groups (16 / G groups per matrix tile), ragged label counts and batch tails
+    ("bf16_g2_f128", 50, 768, 2048, 2, 128, BF16),
+    ("bf16_g4_f128_fs896", 70, 896, 4096, 4, 128, BF16),
+    ("bf16_g1_f32_l1003", 33, 256, 1003, 1, 32, BF16),
+    ("bf16_g8_f64_l2056", 100, 768, 2056, 8, 64, BF16),
+    ("bf16_g2_f32_l1030", 40, 512, 1030, 2, 32, BF16),
+    ("bf16_g4_b1", 1, 768, 1024, 4, 64, BF16),
     ("f32_g8", 32, 256, 4096, 8, 32, F32),
     ("f32_g1", 9, 100, 300, 1, 7, F32),
     ("f32_g32_f64", 50, 768, 2048, 32, 64, F32),
