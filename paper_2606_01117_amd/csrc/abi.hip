@@ -85,6 +85,17 @@ hipError_t fwd_any(const haste::TailArgs &a, const void *X, const int32_t *idx, 
     return haste::fwd_valu(a, X, idx, W, bias, Y, s);
 }
 
+// the backward-weight kernel for a layer: small groups (G = 2, 4, 8) and larger ones on the matrix
+// cores (both on the workspace's X^T copy), the rest on the vector ALUs
+bool bwd_w_uses_xt(const haste::TailArgs &a) { return haste::bwd_w_sg_supported(a) || haste::bwd_w_mfma_supported(a); }
+
+hipError_t bwd_w_any(const haste::TailArgs &a, const void *X, const int32_t *idx, const void *dY, float *dW,
+                     float *dbias, int beta, void *ws, hipStream_t s) {
+    if (haste::bwd_w_sg_supported(a)) return haste::bwd_w_sg(a, X, idx, dY, dW, dbias, beta, ws, s);
+    if (haste::bwd_w_mfma_supported(a)) return haste::bwd_w_mfma(a, X, idx, dY, dW, dbias, beta, ws, s);
+    return haste::bwd_w_valu(a, X, idx, dY, dW, dbias, beta, s);
+}
+
 #define TRY(x)                      \
     do {                            \
         int _rc = (x);              \
@@ -117,13 +128,13 @@ size_t haste_workspace_bytes(const haste_desc_t *d, int op) {
     if (a.B == 0 || a.L == 0) return 0;
     switch (op) {
         case HASTE_OP_FWD: return 0;
-        case HASTE_OP_BWD_W: return haste::bwd_w_mfma_supported(a) ? haste::bwd_w_mfma_ws(a) : 0;
+        case HASTE_OP_BWD_W: return bwd_w_uses_xt(a) ? haste::bwd_w_mfma_ws(a) : 0;
         case HASTE_OP_BWD_X: return haste::bwd_x_mfma_supported(a) ? haste::bwd_x_mfma_ws(a) : haste::bwd_x_valu_ws(a);
         // the fused kernel and the backward-weight kernel stage the same X^T copy; the fused kernel
         // also buckets rows of many positives (provided for up to kFusedPosWs per row)
         case HASTE_OP_FWD_BCE:
             if (haste::fwd_bce_mfma_supported(a, haste::kFusedPosWs)) return haste::fwd_bce_mfma_ws(a, haste::kFusedPosWs);
-            return haste::bwd_w_mfma_supported(a) ? haste::bwd_w_mfma_ws(a) : 0;
+            return bwd_w_uses_xt(a) ? haste::bwd_w_mfma_ws(a) : 0;
         // the composed form also keeps dW in the workspace (after the X^T copy)
         case HASTE_OP_REWIRE: return haste::rewire_supported(a) ? haste::rewire_ws(a) : 0;
         // backward-feature's region (partials, transposed weights, supports), then the fused kernel's
@@ -135,7 +146,7 @@ size_t haste_workspace_bytes(const haste_desc_t *d, int op) {
                    haste_workspace_bytes(d, HASTE_OP_FWD_BCE_SGD);
         case HASTE_OP_FWD_BCE_SGD:
             if (haste::fwd_bce_mfma_supported(a, haste::kFusedPosWs)) return haste::fwd_bce_mfma_ws(a, haste::kFusedPosWs);
-            return (haste::bwd_w_mfma_supported(a) ? haste::bwd_w_mfma_ws(a) : 0) +
+            return (bwd_w_uses_xt(a) ? haste::bwd_w_mfma_ws(a) : 0) +
                    (size_t)haste::round_up(a.L * a.F_in * 4, 256);
     }
     return 0;
@@ -180,12 +191,12 @@ int haste_bwd_w(const haste_desc_t *d, const void *X, const int32_t *idx, const 
     TRY(need_ptr(X, "X"));
     TRY(need_ptr(idx, "idx"));
     TRY(need_ptr(dY, "dY"));
-    if (haste::bwd_w_mfma_supported(a)) {
+    if (bwd_w_uses_xt(a)) {
         const size_t need = haste::bwd_w_mfma_ws(a);
         if (!ws || ws_bytes < need)
             return fail(HASTE_ERR_WORKSPACE, "haste_bwd_w needs %zu workspace bytes, got %zu", need, ws ? ws_bytes : 0);
         TRY(need_ptr(ws, "ws"));
-        return hip_status(haste::bwd_w_mfma(a, X, idx, dY, dW, dbias, beta, ws, s), "haste_bwd_w");
+        return hip_status(bwd_w_any(a, X, idx, dY, dW, dbias, beta, ws, s), "haste_bwd_w");
     }
     if (!haste::valu_supported(a)) return fail(HASTE_ERR_UNSUPPORTED, "no backward-weight kernel for this shape");
     return hip_status(haste::bwd_w_valu(a, X, idx, dY, dW, dbias, beta, s), "haste_bwd_w");
@@ -278,7 +289,7 @@ int haste_fwd_bce(const haste_desc_t *d, const void *X, const int32_t *idx, cons
     if (bias && !aligned16(bias)) return fail(HASTE_ERR_INVALID, "bias is not 16-byte aligned");
     if (a.B * haste::cdiv(a.L, 2048) >= ((int64_t)1 << 31))
         return fail(HASTE_ERR_UNSUPPORTED, "B * L too large for the gradient kernel's grid");
-    const bool bw_mfma = haste::bwd_w_mfma_supported(a);
+    const bool bw_mfma = bwd_w_uses_xt(a);
     const size_t need = bw_mfma ? haste::bwd_w_mfma_ws(a) : 0;
     if (need && (!ws || ws_bytes < need))
         return fail(HASTE_ERR_WORKSPACE, "haste_fwd_bce needs %zu workspace bytes, got %zu", need, ws ? ws_bytes : 0);
@@ -293,8 +304,7 @@ int haste_fwd_bce(const haste_desc_t *d, const void *X, const int32_t *idx, cons
     hipError_t e = fwd_any(a, X, idx, W, bias, dY, s);
     if (e == hipSuccess) e = haste::bce_grad(a.B, a.L, a.dtype, dY, P > 0 ? pos : nullptr, P, dY, s);
     if (e == hipSuccess && dW)
-        e = bw_mfma ? haste::bwd_w_mfma(a, X, idx, dY, dW, dbias, beta, ws, s)
-                    : haste::bwd_w_valu(a, X, idx, dY, dW, dbias, beta, s);
+        e = bwd_w_any(a, X, idx, dY, dW, dbias, beta, ws, s);
     return hip_status(e, "haste_fwd_bce");
 }
 
@@ -352,7 +362,7 @@ int haste_fwd_bce_sgd(const haste_desc_t *d, const void *X, const int32_t *idx, 
     // the fused kernel's shapes need the X^T copy (and the bucketed positives of rows of more than
     // 64); others keep dW in the workspace too
     const bool fused_shape = haste::fwd_bce_mfma_supported(a, P);
-    const size_t xws = haste::bwd_w_mfma_supported(a) ? haste::bwd_w_mfma_ws(a) : 0;
+    const size_t xws = bwd_w_uses_xt(a) ? haste::bwd_w_mfma_ws(a) : 0;
     const size_t need = fused_shape ? haste::fwd_bce_mfma_ws(a, P) : xws + (size_t)haste::round_up(a.L * a.F_in * 4, 256);
     if (a.B == 0) {  // no rows: a zero gradient, the step still decays the velocity and the weights
         if (dbias) TRY(hip_status(haste::fill_f32(dbias, a.L, 0.0f, s), "haste_fwd_bce_sgd"));

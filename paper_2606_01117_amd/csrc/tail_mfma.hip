@@ -1461,6 +1461,14 @@ bool bwd_w_mfma_supported(const TailArgs &a) { return fwd_mfma_supported(a); }
 // X^T staged in 32-row batch blocks (the batch padded to whole blocks)
 size_t bwd_w_mfma_ws(const TailArgs &a) { return (size_t)a.F_s * (size_t)round_up(a.B, 32) * 2 + 256; }
 
+// X^T in 32-row batch blocks, [B/32][F_s][32] (rows past B zero), into the workspace
+hipError_t transpose_x(const TailArgs &a, const void *X, void *ws, hipStream_t s) {
+    const int Bp = (int)round_up(a.B, 32);
+    hipLaunchKernelGGL(k_transpose_x, dim3((unsigned)cdiv(a.F_s, 32), (unsigned)cdiv(Bp, 32)), dim3(256), 0, s,
+                       (const bf16_t *)X, reinterpret_cast<bf16_t *>(ws), (int)a.B, (int)a.F_s);
+    return hipGetLastError();
+}
+
 hipError_t bwd_w_mfma(const TailArgs &a, const void *X, const int32_t *idx, const void *dY, float *dW,
                       float *dbias, int beta, void *ws, hipStream_t s) {
     const int Bp = (int)round_up(a.B, 32);

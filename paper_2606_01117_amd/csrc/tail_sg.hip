@@ -227,6 +227,196 @@ static hipError_t fwd_sg_g(const haste::TailArgs &a, const void *X, const int32_
     return hipErrorInvalidValue;
 }
 
+// ---------------------------------------------------------------------------------------------
+// Backward-weight for small groups (G = 2, 4, 8), the same block-diagonal packing with K = rows:
+// per tile of 16 labels (16 / G groups) and K step s, the M = 16 "slot lines" are slots
+// s G .. s G + G - 1 of each of the tile's groups, and D[line][label] is kept where the line's
+// group is the label's (the rest is the zero-weight side of the packing).
+//   A (lines x rows) = X^T rows of the line's feature, rows 8q .. 8q+7: one 16-byte LDS read;
+//   B (rows x labels) = dY, two ds_read_b64_tr_b16 per tile and slab (shared by every K step);
+//   D: lane (label n, q) holds lines 4q .. 4q+3; for G >= 4 they are slots of n's group exactly
+//     when 4q / G = n / G (4 consecutive slots), for G = 2 two of them are.
+// A workgroup of 8 waves owns a span of 16 TPW * 8 labels (TPW tiles per wave, whose accumulators
+// stay in registers for the whole batch) and sweeps the batch in 32-row slabs: per slab the X^T
+// block (contiguous in the workspace copy) and the span's dY rows are staged in LDS, the next
+// slab's arriving in registers meanwhile.  dbias is the same B operand against all-ones A.
+// ---------------------------------------------------------------------------------------------
+constexpr int kSwYPad = 32;                     // staged dY row padding (bytes)
+
+__host__ __device__ constexpr int sw_tpw(int G, int F_in) {
+    return 32 * G / F_in < 4 ? 32 * G / F_in : 4;   // accumulators: TPW * (F_in / G) * 4 <= 128 registers
+}
+__host__ __device__ constexpr int sw_span(int G, int F_in) { return 16 * kSgWaves * sw_tpw(G, F_in); }
+
+template <int G, int F_IN>
+static size_t sw_lds(int F_s) {
+    return (size_t)haste::round_up((int64_t)F_s * kSgXRow, 16) + (size_t)kSgRows * (sw_span(G, F_IN) * 2 + kSwYPad);
+}
+
+template <int G, int F_IN, bool WITH_DB>
+__global__ __launch_bounds__(kSgThreads) void k_bwd_w_sg(const bf16_t *__restrict__ Xb, const int32_t *__restrict__ idx,
+                                                         const bf16_t *__restrict__ dY, float *__restrict__ dW,
+                                                         float *__restrict__ dbias, int beta, int B, int Bp, int F_s,
+                                                         int64_t L) {
+    constexpr int TPW = sw_tpw(G, F_IN);
+    constexpr int SPAN = sw_span(G, F_IN);
+    constexpr int NSW = F_IN / G;                  // K steps (slot-line tiles) per label tile
+    constexpr int YR = SPAN * 2 + kSwYPad;         // staged dY row bytes
+    constexpr int XL = kMaxFs * 4 / kSgThreads;    // 16-byte X^T loads per thread and slab (at most)
+    constexpr int YC = SPAN / 8;                   // 16-byte dY chunks per row
+    constexpr int YL = (kSgRows * YC + kSgThreads - 1) / kSgThreads;
+    static_assert(TPW >= 1, "a wave needs a whole tile");
+    extern __shared__ __align__(16) char sws[];
+    char *xs = sws;
+    char *ys = sws + ((F_s * kSgXRow + 15) & ~15);
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int l16 = lane & 15, q = lane >> 4;
+    const int64_t K = L / G;
+    const int64_t lab0 = (int64_t)blockIdx.x * SPAN;
+    const int span = L - lab0 < SPAN ? (int)(L - lab0) : SPAN;
+
+    // this lane's slot-line features, per tile and K step (groups past the layer: the last one)
+    int f[TPW][NSW];
+#pragma unroll
+    for (int t = 0; t < TPW; ++t) {
+        const int64_t l0 = lab0 + 16 * (TPW * wave + t);
+        int64_t g = l0 / G + l16 / G;
+        g = g < K ? g : K - 1;
+#pragma unroll
+        for (int s = 0; s < NSW; ++s) f[t][s] = idx[g * F_IN + s * G + l16 % G];
+    }
+
+    const int nxc = 4 * F_s;
+    uint4 xr[XL], yr[YL];
+    auto load = [&](int blk) {
+        const Buf xb(Xb + (int64_t)blk * F_s * 32, (uint32_t)(nxc * 16));
+#pragma unroll
+        for (int i = 0; i < XL; ++i) xr[i] = xb.ld16((uint32_t)(tid + kSgThreads * i) * 16);   // past the block: zero
+        const int b0 = blk * kSgRows;
+        const int rows = B - b0 < kSgRows ? B - b0 : kSgRows;
+        const Buf db(dY + (int64_t)b0 * L + lab0, (uint32_t)(rows > 0 ? ((int64_t)(rows - 1) * L + span) * 2 : 0));
+#pragma unroll
+        for (int i = 0; i < YL; ++i) {
+            const int c = tid + kSgThreads * i, row = c / YC, part = c % YC;
+            const bool ok = c < kSgRows * YC && row < rows && 8 * part < span;
+            yr[i] = db.ld16(ok ? (uint32_t)(((int64_t)row * L + 8 * part) * 2) : kOob);
+        }
+    };
+    auto store = [&]() {
+#pragma unroll
+        for (int i = 0; i < XL; ++i) {
+            const int c = tid + kSgThreads * i;
+            if (c < nxc) *reinterpret_cast<uint4 *>(xs + (c >> 2) * kSgXRow + (c & 3) * 16) = xr[i];
+        }
+#pragma unroll
+        for (int i = 0; i < YL; ++i) {
+            const int c = tid + kSgThreads * i;
+            if (c < kSgRows * YC) *reinterpret_cast<uint4 *>(ys + (c / YC) * YR + (c % YC) * 16) = yr[i];
+        }
+    };
+
+    f32x4_t acc[TPW][NSW], db[TPW];
+#pragma unroll
+    for (int t = 0; t < TPW; ++t) {
+        db[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < NSW; ++s) acc[t][s] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    }
+    const bf16x8_t ones = as_bf16x8(make_uint4(0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u));
+    // B-operand source lanes: 16-lane group q names rows 8q + (l16 >> 2) (+ 4), labels 4 (l16 & 3) ..
+    const char *ysrc = ys + (8 * q + (l16 >> 2)) * YR + (l16 & 3) * 8;
+
+    const int nblk = Bp / kSgRows;
+    load(0);
+    for (int blk = 0; blk < nblk; ++blk) {
+        __syncthreads();   // the previous slab is no longer read
+        store();
+        __syncthreads();
+        if (blk + 1 < nblk) load(blk + 1);
+#pragma unroll
+        for (int t = 0; t < TPW; ++t) {
+            const char *p = ysrc + 16 * (TPW * wave + t) * 2;
+            const uint2 lo = lds_read_tr(p);
+            const uint2 hi = lds_read_tr(p + 4 * YR);
+            const bf16x8_t bv = as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y));
+#pragma unroll
+            for (int s = 0; s < NSW; ++s) {
+                const uint4 av = *reinterpret_cast<const uint4 *>(xs + f[t][s] * kSgXRow + 16 * q);
+                acc[t][s] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(av), bv, acc[t][s], 0, 0, 0);
+            }
+            if constexpr (WITH_DB) db[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, bv, db[t], 0, 0, 0);
+        }
+    }
+    // the kept lines: G >= 4: lines 4q .. 4q+3 are slots (4q mod G) .. +3 of the K step when 4q / G
+    // is the label's group; G = 2: lines r0, r0 + 1 (r0 = 2 (n / 2) - 4q) when that lies in [0, 4)
+#pragma unroll
+    for (int t = 0; t < TPW; ++t) {
+        const int64_t l = lab0 + 16 * (TPW * wave + t) + l16;
+        if (l >= L) continue;
+        float *wr = dW + l * F_IN;
+        if constexpr (G >= 4) {
+            if ((4 * q) / G == l16 / G) {
+#pragma unroll
+                for (int s = 0; s < NSW; ++s) {
+                    float4 *p = reinterpret_cast<float4 *>(wr + s * G + (4 * q) % G);
+                    float4 v = make_float4(acc[t][s][0], acc[t][s][1], acc[t][s][2], acc[t][s][3]);
+                    if (beta) {
+                        const float4 o = *p;
+                        v.x += o.x; v.y += o.y; v.z += o.z; v.w += o.w;
+                    }
+                    *p = v;
+                }
+            }
+        } else {
+            const int r0 = 2 * (l16 / 2) - 4 * q;
+            if (r0 >= 0 && r0 < 4) {
+#pragma unroll
+                for (int s = 0; s < NSW; ++s) {
+                    float2 *p = reinterpret_cast<float2 *>(wr + 2 * s);
+                    float2 v = r0 == 0 ? make_float2(acc[t][s][0], acc[t][s][1]) : make_float2(acc[t][s][2], acc[t][s][3]);
+                    if (beta) {
+                        const float2 o = *p;
+                        v.x += o.x; v.y += o.y;
+                    }
+                    *p = v;
+                }
+            }
+        }
+        if constexpr (WITH_DB) {
+            if (q == 0) dbias[l] = (beta ? dbias[l] : 0.0f) + db[t][0];
+        }
+    }
+}
+
+template <int G, int F_IN>
+static hipError_t launch_bwd_w_sg(const haste::TailArgs &a, const void *Xb, const int32_t *idx, const void *dY,
+                                  float *dW, float *dbias, int beta, int Bp, hipStream_t s) {
+    const size_t lds = sw_lds<G, F_IN>((int)a.F_s);
+    const dim3 grid((unsigned)haste::cdiv(a.L, sw_span(G, F_IN)));
+    auto go = [&](auto kern) {
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(kern, grid, dim3(kSgThreads), lds, s, (const bf16_t *)Xb, idx, (const bf16_t *)dY, dW,
+                           dbias, beta, (int)a.B, Bp, (int)a.F_s, a.L);
+        return hipGetLastError();
+    };
+    return dbias ? go(k_bwd_w_sg<G, F_IN, true>) : go(k_bwd_w_sg<G, F_IN, false>);
+}
+
+template <int G>
+static hipError_t bwd_w_sg_g(const haste::TailArgs &a, const void *Xb, const int32_t *idx, const void *dY, float *dW,
+                             float *dbias, int beta, int Bp, hipStream_t s) {
+    switch (a.F_in) {
+        case 32: return launch_bwd_w_sg<G, 32>(a, Xb, idx, dY, dW, dbias, beta, Bp, s);
+        case 64: return launch_bwd_w_sg<G, 64>(a, Xb, idx, dY, dW, dbias, beta, Bp, s);
+        case 128:
+            if constexpr (G >= 4) return launch_bwd_w_sg<G, 128>(a, Xb, idx, dY, dW, dbias, beta, Bp, s);
+            break;
+    }
+    return hipErrorInvalidValue;
+}
+
 }  // namespace
 
 namespace haste {
@@ -238,6 +428,28 @@ bool fwd_sg_supported(const TailArgs &a) {
     if (a.dtype != HASTE_DTYPE_BF16 || !(a.G == 1 || a.G == 2 || a.G == 4 || a.G == 8)) return false;
     if (!(a.F_in == 32 || a.F_in == 64 || (a.F_in == 128 && a.G >= 2))) return false;
     return a.F_s % 8 == 0 && a.F_s <= kMaxFs && a.L < ((int64_t)1 << 40);
+}
+
+// backward-weight: bf16, G in {2, 4, 8}, F_in in {32, 64} (and 128 for G >= 4), F_s a multiple of
+// 8 up to kMaxFs; the X^T copy of the workspace (bwd_w_mfma_ws) is shared with the other kernels.
+bool bwd_w_sg_supported(const TailArgs &a) {
+    if (a.dtype != HASTE_DTYPE_BF16 || !(a.G == 2 || a.G == 4 || a.G == 8)) return false;
+    if (!(a.F_in == 32 || a.F_in == 64 || (a.F_in == 128 && a.G >= 4))) return false;
+    // a slab's dY rows are addressed from its first row with 31-bit byte offsets
+    return a.F_s % 8 == 0 && a.F_s <= kMaxFs && (a.L * 32 + 1024) * 2 < ((int64_t)1 << 31);
+}
+
+hipError_t bwd_w_sg(const TailArgs &a, const void *X, const int32_t *idx, const void *dY, float *dW, float *dbias,
+                    int beta, void *ws, hipStream_t s) {
+    const int Bp = (int)round_up(a.B, 32);
+    hipError_t e = transpose_x(a, X, ws, s);
+    if (e != hipSuccess) return e;
+    switch (a.G) {
+        case 2: return bwd_w_sg_g<2>(a, ws, idx, dY, dW, dbias, beta, Bp, s);
+        case 4: return bwd_w_sg_g<4>(a, ws, idx, dY, dW, dbias, beta, Bp, s);
+        case 8: return bwd_w_sg_g<8>(a, ws, idx, dY, dW, dbias, beta, Bp, s);
+    }
+    return hipErrorInvalidValue;
 }
 
 hipError_t fwd_sg(const TailArgs &a, const void *X, const int32_t *idx, const void *W, const float *bias, void *Y,
