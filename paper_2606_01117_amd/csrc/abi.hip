@@ -85,7 +85,7 @@ hipError_t fwd_any(const haste::TailArgs &a, const void *X, const int32_t *idx, 
     return haste::fwd_valu(a, X, idx, W, bias, Y, s);
 }
 
-// the backward-weight kernel for a layer: small groups (G = 2, 4, 8) and larger ones on the matrix
+// the backward-weight kernel for a layer: small groups (G = 1, 2, 4, 8) and larger ones on the matrix
 // cores (both on the workspace's X^T copy), the rest on the vector ALUs
 bool bwd_w_uses_xt(const haste::TailArgs &a) { return haste::bwd_w_sg_supported(a) || haste::bwd_w_mfma_supported(a); }
 

@@ -141,7 +141,7 @@ hipError_t fwd_mfma(const TailArgs &a, const void *X, const int32_t *idx, const 
 bool fwd_sg_supported(const TailArgs &a);
 hipError_t fwd_sg(const TailArgs &a, const void *X, const int32_t *idx, const void *W, const float *bias, void *Y,
                   hipStream_t s);
-// backward-weight for small groups (G = 2, 4, 8), on the workspace's X^T copy (bwd_w_mfma_ws)
+// backward-weight for small groups (G = 1, 2, 4, 8), on the workspace's X^T copy (bwd_w_mfma_ws)
 bool bwd_w_sg_supported(const TailArgs &a);
 hipError_t bwd_w_sg(const TailArgs &a, const void *X, const int32_t *idx, const void *dY, float *dW, float *dbias,
                     int beta, void *ws, hipStream_t s);

@@ -228,23 +228,29 @@ static hipError_t fwd_sg_g(const haste::TailArgs &a, const void *X, const int32_
 }
 
 // ---------------------------------------------------------------------------------------------
-// Backward-weight for small groups (G = 2, 4, 8), the same block-diagonal packing with K = rows:
+// Backward-weight for small groups (G = 1, 2, 4, 8), the same block-diagonal packing with K = rows:
 // per tile of 16 labels (16 / G groups) and K step s, the M = 16 "slot lines" are slots
 // s G .. s G + G - 1 of each of the tile's groups, and D[line][label] is kept where the line's
 // group is the label's (the rest is the zero-weight side of the packing).
 //   A (lines x rows) = X^T rows of the line's feature, rows 8q .. 8q+7: one 16-byte LDS read;
 //   B (rows x labels) = dY, two ds_read_b64_tr_b16 per tile and slab (shared by every K step);
 //   D: lane (label n, q) holds lines 4q .. 4q+3; for G >= 4 they are slots of n's group exactly
-//     when 4q / G = n / G (4 consecutive slots), for G = 2 two of them are.
+//     when 4q / G = n / G (4 consecutive slots), for G = 2 two of them are, for G = 1 one.
 // A workgroup of 8 waves owns a span of 16 TPW * 8 labels (TPW tiles per wave, whose accumulators
-// stay in registers for the whole batch) and sweeps the batch in 32-row slabs: per slab the X^T
+// stay in registers for the whole batch; for G = 1 a pass covers 16 slots and the batch is swept
+// once per pass) and sweeps the batch in 32-row slabs: per slab the X^T
 // block (contiguous in the workspace copy) and the span's dY rows are staged in LDS, the next
 // slab's arriving in registers meanwhile.  dbias is the same B operand against all-ones A.
 // ---------------------------------------------------------------------------------------------
 constexpr int kSwYPad = 32;                     // staged dY row padding (bytes)
 
+// label tiles per wave, and K steps per pass over the batch: accumulators TPW * NSC * 4 <= 128
+// registers (G = 1 sweeps the batch F_in / 16 times, 16 slots at a time)
 __host__ __device__ constexpr int sw_tpw(int G, int F_in) {
-    return 32 * G / F_in < 4 ? 32 * G / F_in : 4;   // accumulators: TPW * (F_in / G) * 4 <= 128 registers
+    return G == 1 ? 2 : (32 * G / F_in < 4 ? 32 * G / F_in : 4);
+}
+__host__ __device__ constexpr int sw_nsc(int G, int F_in) {
+    return F_in / G < 32 / sw_tpw(G, F_in) ? F_in / G : 32 / sw_tpw(G, F_in);
 }
 __host__ __device__ constexpr int sw_span(int G, int F_in) { return 16 * kSgWaves * sw_tpw(G, F_in); }
 
@@ -260,7 +266,8 @@ __global__ __launch_bounds__(kSgThreads) void k_bwd_w_sg(const bf16_t *__restric
                                                          int64_t L) {
     constexpr int TPW = sw_tpw(G, F_IN);
     constexpr int SPAN = sw_span(G, F_IN);
-    constexpr int NSW = F_IN / G;                  // K steps (slot-line tiles) per label tile
+    constexpr int NSW = sw_nsc(G, F_IN);           // K steps (slot-line tiles) per pass over the batch
+    constexpr int NPASS = F_IN / G / NSW;          // passes (1 unless G = 1)
     constexpr int YR = SPAN * 2 + kSwYPad;         // staged dY row bytes
     constexpr int XL = kMaxFs * 4 / kSgThreads;    // 16-byte X^T loads per thread and slab (at most)
     constexpr int YC = SPAN / 8;                   // 16-byte dY chunks per row
@@ -275,16 +282,18 @@ __global__ __launch_bounds__(kSgThreads) void k_bwd_w_sg(const bf16_t *__restric
     const int64_t lab0 = (int64_t)blockIdx.x * SPAN;
     const int span = L - lab0 < SPAN ? (int)(L - lab0) : SPAN;
 
-    // this lane's slot-line features, per tile and K step (groups past the layer: the last one)
     int f[TPW][NSW];
+    // this lane's slot-line features, per tile and K step of pass ps (groups past the layer: the last)
+    auto features = [&](int ps) {
 #pragma unroll
-    for (int t = 0; t < TPW; ++t) {
-        const int64_t l0 = lab0 + 16 * (TPW * wave + t);
-        int64_t g = l0 / G + l16 / G;
-        g = g < K ? g : K - 1;
+        for (int t = 0; t < TPW; ++t) {
+            const int64_t l0 = lab0 + 16 * (TPW * wave + t);
+            int64_t g = l0 / G + l16 / G;
+            g = g < K ? g : K - 1;
 #pragma unroll
-        for (int s = 0; s < NSW; ++s) f[t][s] = idx[g * F_IN + s * G + l16 % G];
-    }
+            for (int s = 0; s < NSW; ++s) f[t][s] = idx[g * F_IN + (ps * NSW + s) * G + l16 % G];
+        }
+    };
 
     const int nxc = 4 * F_s;
     uint4 xr[XL], yr[YL];
@@ -316,17 +325,20 @@ __global__ __launch_bounds__(kSgThreads) void k_bwd_w_sg(const bf16_t *__restric
     };
 
     f32x4_t acc[TPW][NSW], db[TPW];
+    const bf16x8_t ones = as_bf16x8(make_uint4(0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u));
+    // B-operand source lanes: 16-lane group q names rows 8q + (l16 >> 2) (+ 4), labels 4 (l16 & 3) ..
+    const char *ysrc = ys + (8 * q + (l16 >> 2)) * YR + (l16 & 3) * 8;
+    const int nblk = Bp / kSgRows;
+
+    for (int ps = 0; ps < NPASS; ++ps) {
+    features(ps);
 #pragma unroll
     for (int t = 0; t < TPW; ++t) {
         db[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int s = 0; s < NSW; ++s) acc[t][s] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     }
-    const bf16x8_t ones = as_bf16x8(make_uint4(0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u));
-    // B-operand source lanes: 16-lane group q names rows 8q + (l16 >> 2) (+ 4), labels 4 (l16 & 3) ..
-    const char *ysrc = ys + (8 * q + (l16 >> 2)) * YR + (l16 & 3) * 8;
-
-    const int nblk = Bp / kSgRows;
+    if (ps > 0) __syncthreads();   // the previous pass's last slab is no longer read
     load(0);
     for (int blk = 0; blk < nblk; ++blk) {
         __syncthreads();   // the previous slab is no longer read
@@ -344,7 +356,9 @@ __global__ __launch_bounds__(kSgThreads) void k_bwd_w_sg(const bf16_t *__restric
                 const uint4 av = *reinterpret_cast<const uint4 *>(xs + f[t][s] * kSgXRow + 16 * q);
                 acc[t][s] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(av), bv, acc[t][s], 0, 0, 0);
             }
-            if constexpr (WITH_DB) db[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, bv, db[t], 0, 0, 0);
+            if constexpr (WITH_DB) {
+                if (ps == 0) db[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, bv, db[t], 0, 0, 0);
+            }
         }
     }
     // the kept lines: G >= 4: lines 4q .. 4q+3 are slots (4q mod G) .. +3 of the K step when 4q / G
@@ -367,7 +381,7 @@ __global__ __launch_bounds__(kSgThreads) void k_bwd_w_sg(const bf16_t *__restric
                     *p = v;
                 }
             }
-        } else {
+        } else if constexpr (G == 2) {
             const int r0 = 2 * (l16 / 2) - 4 * q;
             if (r0 >= 0 && r0 < 4) {
 #pragma unroll
@@ -381,11 +395,23 @@ __global__ __launch_bounds__(kSgThreads) void k_bwd_w_sg(const bf16_t *__restric
                     *p = v;
                 }
             }
+        } else {
+            // G = 1: line l16 is label l16's slot of the K step, held by lane (l16, l16 / 4) at l16 % 4
+            if (q == l16 / 4) {
+                const int r0 = l16 & 3;
+#pragma unroll
+                for (int s = 0; s < NSW; ++s) {
+                    float *p = wr + ps * NSW + s;
+                    const float v = r0 == 0 ? acc[t][s][0] : r0 == 1 ? acc[t][s][1] : r0 == 2 ? acc[t][s][2] : acc[t][s][3];
+                    *p = beta ? *p + v : v;
+                }
+            }
         }
         if constexpr (WITH_DB) {
-            if (q == 0) dbias[l] = (beta ? dbias[l] : 0.0f) + db[t][0];
+            if (ps == 0 && q == 0) dbias[l] = (beta ? dbias[l] : 0.0f) + db[t][0];
         }
     }
+    }   // passes
 }
 
 template <int G, int F_IN>
@@ -411,7 +437,7 @@ static hipError_t bwd_w_sg_g(const haste::TailArgs &a, const void *Xb, const int
         case 32: return launch_bwd_w_sg<G, 32>(a, Xb, idx, dY, dW, dbias, beta, Bp, s);
         case 64: return launch_bwd_w_sg<G, 64>(a, Xb, idx, dY, dW, dbias, beta, Bp, s);
         case 128:
-            if constexpr (G >= 4) return launch_bwd_w_sg<G, 128>(a, Xb, idx, dY, dW, dbias, beta, Bp, s);
+            if constexpr (G == 1 || G >= 4) return launch_bwd_w_sg<G, 128>(a, Xb, idx, dY, dW, dbias, beta, Bp, s);
             break;
     }
     return hipErrorInvalidValue;
@@ -433,10 +459,11 @@ bool fwd_sg_supported(const TailArgs &a) {
 // backward-weight: bf16, G in {2, 4, 8}, F_in in {32, 64} (and 128 for G >= 4), F_s a multiple of
 // 8 up to kMaxFs; the X^T copy of the workspace (bwd_w_mfma_ws) is shared with the other kernels.
 bool bwd_w_sg_supported(const TailArgs &a) {
-    if (a.dtype != HASTE_DTYPE_BF16 || !(a.G == 2 || a.G == 4 || a.G == 8)) return false;
-    if (!(a.F_in == 32 || a.F_in == 64 || (a.F_in == 128 && a.G >= 4))) return false;
-    // a slab's dY rows are addressed from its first row with 31-bit byte offsets
-    return a.F_s % 8 == 0 && a.F_s <= kMaxFs && (a.L * 32 + 1024) * 2 < ((int64_t)1 << 31);
+    if (a.dtype != HASTE_DTYPE_BF16 || !(a.G == 1 || a.G == 2 || a.G == 4 || a.G == 8)) return false;
+    if (!(a.F_in == 32 || a.F_in == 64 || (a.F_in == 128 && (a.G == 1 || a.G >= 4)))) return false;
+    // a slab's dY rows are addressed from its first row with 31-bit byte offsets, and read with
+    // buffer loads that need dword-aligned rows (L even)
+    return a.F_s % 8 == 0 && a.F_s <= kMaxFs && (a.L * 32 + 1024) * 2 < ((int64_t)1 << 31) && a.L % 2 == 0;
 }
 
 hipError_t bwd_w_sg(const TailArgs &a, const void *X, const int32_t *idx, const void *dY, float *dW, float *dbias,
@@ -445,6 +472,7 @@ hipError_t bwd_w_sg(const TailArgs &a, const void *X, const int32_t *idx, const 
     hipError_t e = transpose_x(a, X, ws, s);
     if (e != hipSuccess) return e;
     switch (a.G) {
+        case 1: return bwd_w_sg_g<1>(a, ws, idx, dY, dW, dbias, beta, Bp, s);
         case 2: return bwd_w_sg_g<2>(a, ws, idx, dY, dW, dbias, beta, Bp, s);
         case 4: return bwd_w_sg_g<4>(a, ws, idx, dY, dW, dbias, beta, Bp, s);
         case 8: return bwd_w_sg_g<8>(a, ws, idx, dY, dW, dbias, beta, Bp, s);

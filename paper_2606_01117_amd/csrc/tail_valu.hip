@@ -79,6 +79,10 @@ __global__ __launch_bounds__(256) void k_bwd_w_valu(const T *__restrict__ X, con
         for (int t = 0; t < TC; ++t) acc[t] = 0.0f;
         float db = 0.0f;
         const int nt = F_in - tc < TC ? F_in - tc : TC;
+        // the pass's supports, once for the whole batch (lanes sit a label's support apart)
+        int fs[TC];
+#pragma unroll
+        for (int t = 0; t < TC; ++t) fs[t] = valid && t < nt ? idx[g * F_in + tc + t] : 0;
         for (int b0 = 0; b0 < B; b0 += TB) {
             __syncthreads();
             load_slab(xs, X, b0, B, F_s);
@@ -94,8 +98,7 @@ __global__ __launch_bounds__(256) void k_bwd_w_valu(const T *__restrict__ X, con
 #pragma unroll
                 for (int t = 0; t < TC; ++t) {
                     if (t < nt) {
-                        const int f = idx[g * F_in + tc + t];
-                        const float4 *xr = reinterpret_cast<const float4 *>(xs + f * XS);
+                        const float4 *xr = reinterpret_cast<const float4 *>(xs + fs[t] * XS);
                         float s = 0.0f;
 #pragma unroll
                         for (int q = 0; q < TB / 4; ++q) {
@@ -141,8 +144,7 @@ __global__ __launch_bounds__(kOwnWaves * 64) void k_bwd_x_valu(const int32_t *__
                                                                 int64_t L, int G, int F_in, int64_t lps) {
     extern __shared__ __align__(16) float accs[];   // [F_s][kOwnAS], then the staged block
     const int LB = 4096 / F_in;                      // labels per staged block
-    int *sf = reinterpret_cast<int *>(accs + F_s * kOwnAS);   // [LB][F_in] supports
-    float *sw = reinterpret_cast<float *>(sf + LB * F_in);    // [LB][F_in] weights
+    int2 *sfw = reinterpret_cast<int2 *>(accs + F_s * kOwnAS);   // [LB][F_in] (support, weight bits)
     const int64_t seg = blockIdx.x;
     const int b0 = blockIdx.y * 32;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -157,8 +159,7 @@ __global__ __launch_bounds__(kOwnWaves * 64) void k_bwd_x_valu(const int32_t *__
         for (int e = tid; e < nl * F_in; e += nthr) {
             const int j = e / F_in, t = e - j * F_in;
             const int64_t l = lb + j;
-            sf[e] = idx[(l / G) * F_in + t];
-            sw[e] = load_f32(W, l * F_in + t);
+            sfw[e] = make_int2(idx[(l / G) * F_in + t], __float_as_int(load_f32(W, l * F_in + t)));
         }
         __syncthreads();
         // dY of this wave's 4 rows for labels lb + 64c + lane (c < LB / 64 chunks of the block)
@@ -177,8 +178,9 @@ __global__ __launch_bounds__(kOwnWaves * 64) void k_bwd_x_valu(const int32_t *__
 #pragma unroll
                 for (int i = 0; i < 4; ++i) dy[i] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(dyr[i]), jj));
                 for (int t = lane; t < F_in; t += 64) {
-                    const int f = sf[j * F_in + t];
-                    const float wv = sw[j * F_in + t];
+                    const int2 fw = sfw[j * F_in + t];   // one 8-byte read: the slot's feature and weight
+                    const int f = fw.x;
+                    const float wv = __int_as_float(fw.y);
                     float4 *p = reinterpret_cast<float4 *>(accw + f * kOwnAS);
                     float4 v = *p;
                     v.x = fmaf(dy[0], wv, v.x);
