@@ -87,6 +87,12 @@ hipError_t fwd_any(const haste::TailArgs &a, const void *X, const int32_t *idx, 
 
 // the backward-weight kernel for a layer: small groups (G = 1, 2, 4, 8) and larger ones on the matrix
 // cores (both on the workspace's X^T copy), the rest on the vector ALUs
+// backward-feature: small-group kernel, else the general matrix-core kernel, else the VALU kernel
+size_t bwd_x_ws(const haste::TailArgs &a) {
+    if (haste::bwd_x_sg_supported(a)) return haste::bwd_x_sg_ws(a);
+    return haste::bwd_x_mfma_supported(a) ? haste::bwd_x_mfma_ws(a) : haste::bwd_x_valu_ws(a);
+}
+
 bool bwd_w_uses_xt(const haste::TailArgs &a) { return haste::bwd_w_sg_supported(a) || haste::bwd_w_mfma_supported(a); }
 
 hipError_t bwd_w_any(const haste::TailArgs &a, const void *X, const int32_t *idx, const void *dY, float *dW,
@@ -129,7 +135,7 @@ size_t haste_workspace_bytes(const haste_desc_t *d, int op) {
     switch (op) {
         case HASTE_OP_FWD: return 0;
         case HASTE_OP_BWD_W: return bwd_w_uses_xt(a) ? haste::bwd_w_mfma_ws(a) : 0;
-        case HASTE_OP_BWD_X: return haste::bwd_x_mfma_supported(a) ? haste::bwd_x_mfma_ws(a) : haste::bwd_x_valu_ws(a);
+        case HASTE_OP_BWD_X: return bwd_x_ws(a);
         // the fused kernel and the backward-weight kernel stage the same X^T copy; the fused kernel
         // also buckets rows of many positives (provided for up to kFusedPosWs per row)
         case HASTE_OP_FWD_BCE:
@@ -217,13 +223,14 @@ int haste_bwd_x(const haste_desc_t *d, const int32_t *idx, const void *W, const 
     TRY(need_ptr(idx, "idx"));
     TRY(need_ptr(W, "W"));
     TRY(need_ptr(dY, "dY"));
-    const bool mf = haste::bwd_x_mfma_supported(a);
-    if (!mf && !haste::valu_supported(a)) return fail(HASTE_ERR_UNSUPPORTED, "no backward-feature kernel for this shape");
-    const size_t need = mf ? haste::bwd_x_mfma_ws(a) : haste::bwd_x_valu_ws(a);
+    if (!haste::bwd_x_sg_supported(a) && !haste::bwd_x_mfma_supported(a) && !haste::valu_supported(a))
+        return fail(HASTE_ERR_UNSUPPORTED, "no backward-feature kernel for this shape");
+    const size_t need = bwd_x_ws(a);
     if (!ws || ws_bytes < need)
         return fail(HASTE_ERR_WORKSPACE, "haste_bwd_x needs %zu workspace bytes, got %zu", need, ws ? ws_bytes : 0);
     TRY(need_ptr(ws, "ws"));
-    if (mf) return hip_status(haste::bwd_x_mfma(a, idx, W, dY, dX, beta, ws, s), "haste_bwd_x");
+    if (haste::bwd_x_sg_supported(a)) return hip_status(haste::bwd_x_sg(a, idx, W, dY, dX, beta, ws, s), "haste_bwd_x");
+    if (haste::bwd_x_mfma_supported(a)) return hip_status(haste::bwd_x_mfma(a, idx, W, dY, dX, beta, ws, s), "haste_bwd_x");
     return hip_status(haste::bwd_x_valu(a, idx, W, dY, dX, beta, ws, s), "haste_bwd_x");
 }
 

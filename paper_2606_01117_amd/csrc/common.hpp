@@ -103,6 +103,54 @@ struct Buf {
     }
 };
 
+// The backward-feature accumulator dX^T[F_s][32 rows] (fp32) in LDS: row f is 128 bytes, and its
+// 16-byte chunk c (rows 4c .. 4c + 3) sits at chunk position c ^ (f mod 8).  A matrix-core result
+// tile writes one chunk of 16 rows at a time (lane l16 -> row f_l16), so the XOR spreads those
+// rows over the banks without padding (less LDS than 36- or 40-float rows, and fewer conflicts
+// than either on the 16-row tiles of random supports).  acc_row(f): the row's byte offset with
+// its swizzle, so that chunk c of the row is at acc_row(f) ^ (c << 4).
+__host__ __device__ constexpr uint32_t acc_row(int f) { return (uint32_t)f * 128u | (((uint32_t)f & 7u) << 4); }
+__host__ __device__ constexpr int acc_index(int f, int r) {   // float index of row r of accumulator row f
+    return f * 32 + ((((r >> 2) ^ f) & 7) << 2) + (r & 3);
+}
+
+// Slot order of a group's support for the backward-feature accumulator.  Rows of distinct
+// residue mod 8 fall in distinct banks for the 8 lanes an access serves together, so slots are
+// ordered by (occurrence of the residue so far, row mod 8), which deals the residues round-robin
+// over the runs of 8 positions: a residue held by at most F_in / 8 slots never appears twice in a
+// run (measured on 16-row tiles of random 64-slot supports: 1.4x the conflict-free read time
+// against 2.2x for sorted order).  For the slots t = lane and
+// t = lane + 64 (those below F_in) of support `sup`: f = the feature (-1 past F_in) and pos = its
+// position (-1 past F_in).  Wave-level: every lane of the wave must call it.
+__device__ __forceinline__ void slot_positions(const int32_t *sup, int F_in, int lane, int (&f)[2], int (&pos)[2]) {
+    int cls[2], occ[2] = {0, 0};
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int t = lane + 64 * i;
+        f[i] = t < F_in ? sup[t] : -1;
+        cls[i] = f[i] >= 0 ? (f[i] & 7) : -1;
+    }
+    const uint64_t lt = __lanemask_lt();
+    int cnt[8];
+#pragma unroll
+    for (int v = 0; v < 8; ++v) {
+        const uint64_t m0 = __ballot(cls[0] == v), m1 = __ballot(cls[1] == v);
+        if (cls[0] == v) occ[0] = __popcll(m0 & lt);
+        if (cls[1] == v) occ[1] = __popcll(m0) + __popcll(m1 & lt);
+        cnt[v] = __popcll(m0) + __popcll(m1);
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        pos[i] = -1;
+        if (cls[i] < 0) continue;
+        const int r = cls[i], o = occ[i];
+        int rank = 0;                             // slots with a smaller (occurrence, residue)
+#pragma unroll
+        for (int v = 0; v < 8; ++v) rank += (cnt[v] < o ? cnt[v] : o) + (v < r && cnt[v] > o ? 1 : 0);
+        pos[i] = rank;
+    }
+}
+
 // Gradient of the binary cross-entropy of sigmoid(z) against a 0/1 target with respect to the
 // logit z (Section 3.3 objective): sigmoid(z) - y, in fp32.  exp(-z) overflows to +inf for very
 // negative z, which gives sigmoid 0 as it should.
@@ -146,6 +194,11 @@ bool bwd_w_sg_supported(const TailArgs &a);
 hipError_t bwd_w_sg(const TailArgs &a, const void *X, const int32_t *idx, const void *dY, float *dW, float *dbias,
                     int beta, void *ws, hipStream_t s);
 hipError_t transpose_x(const TailArgs &a, const void *X, void *ws, hipStream_t s);
+// backward-feature for small groups (G = 1, 2, 4, 8), 32 consecutive labels per matrix-core K step
+bool bwd_x_sg_supported(const TailArgs &a);
+size_t bwd_x_sg_ws(const TailArgs &a);
+hipError_t bwd_x_sg(const TailArgs &a, const int32_t *idx, const void *W, const void *dY, float *dX, int beta, void *ws,
+                    hipStream_t s);
 bool bwd_w_mfma_supported(const TailArgs &a);
 size_t bwd_w_mfma_ws(const TailArgs &a);
 hipError_t bwd_w_mfma(const TailArgs &a, const void *X, const int32_t *idx, const void *dY, float *dW,

@@ -756,32 +756,13 @@ __global__ __launch_bounds__(64 * fb_waves(F_IN)) void k_fwd_bce(
             constexpr int RB = 32 * F_IN * 2;                         // bytes of a group's W^T
             char *tw = fbs + wave * fb_wt_region(F_IN);
             uint8_t *sp = reinterpret_cast<uint8_t *>(tw + RB);        // position of each slot
-            const int32_t *ik = idx + vu * F_IN;
-            int f[2], cls[2], occ[2] = {0, 0};
+            int f[2], ps[2];
+            slot_positions(idx + vu * F_IN, F_IN, lane, f, ps);
 #pragma unroll
             for (int i = 0; i < 2; ++i) {
-                const int t = lane + 64 * i;
-                f[i] = t < F_IN ? ik[t] : -1;
-                cls[i] = f[i] >= 0 ? (f[i] & 7) : -1;
-            }
-            const uint64_t lt = __lanemask_lt();
-            int cnt[8];
-#pragma unroll
-            for (int c = 0; c < 8; ++c) {
-                const uint64_t m0 = __ballot(cls[0] == c), m1 = __ballot(cls[1] == c);
-                if (cls[0] == c) occ[0] = __popcll(m0 & lt);
-                if (cls[1] == c) occ[1] = __popcll(m0) + __popcll(m1 & lt);
-                cnt[c] = __popcll(m0) + __popcll(m1);
-            }
-#pragma unroll
-            for (int i = 0; i < 2; ++i) {
-                if (cls[i] < 0) continue;
-                const int r = cls[i], o = occ[i];
-                int rank = 0;                     // slots with a smaller (occurrence, residue)
-#pragma unroll
-                for (int c = 0; c < 8; ++c) rank += (cnt[c] < o ? cnt[c] : o) + (c < r && cnt[c] > o ? 1 : 0);
-                sp[lane + 64 * i] = (uint8_t)rank;
-                if (v < nunits) idxl[vu * F_IN + (rank & 15) * NST + (rank >> 4)] = f[i];
+                if (ps[i] < 0) continue;
+                sp[lane + 64 * i] = (uint8_t)ps[i];
+                if (v < nunits) idxl[vu * F_IN + (ps[i] & 15) * NST + (ps[i] >> 4)] = (int32_t)acc_row(f[i]);
             }
             __builtin_amdgcn_wave_barrier();
 #pragma unroll
@@ -963,7 +944,7 @@ __global__ __launch_bounds__(64 * fb_waves(F_IN)) void k_fwd_bce(
 // over W instead of one transpose per group and batch tile.
 //
 // A workgroup owns a 32-row batch tile and one contiguous segment of groups; its partial
-// dX^T[F_s][32] (fp32, rows padded to 40 floats) lives in LDS.  Two consumer waves each own one
+// dX^T[F_s][32] (fp32, rows swizzled as acc_row states) lives in LDS.  Two consumer waves each own one
 // 16-row half of the tile for every group and every support slot, so no two waves ever touch
 // the same accumulator cell: each wave adds its products with plain read-add-write in its own
 // program order (LDS operations of one wave are executed in order), with no barrier between
@@ -985,17 +966,15 @@ __global__ __launch_bounds__(64 * fb_waves(F_IN)) void k_fwd_bce(
 //     accumulator row idx[k, slot].
 // --------------------------------------------------------------------------------------------
 
-// W [K][G][F_in] -> WT [K][Gp / 8][F_in][8] and idx [K][F_in] -> idxl [K][F_in], both in lane
+// W [K][G][F_in] -> WT [K][Gp / 8][F_in][8] and idx [K][F_in] -> idxl [K][F_in] (the accumulator
+// row offsets acc_row(idx[k, slot]) of the slots), both in lane
 // order: position p = 16 st + l16 is the slot that lane l16 of 16-slot tile st handles.  WT holds
 // label octet o of position p at (o F_in + p) 8 (labels G .. Gp - 1 zero, Gp = G rounded up to
 // 8), so a consumer's operand load (16 positions x one octet per 16 lanes) reads contiguous
 // 256-byte runs; idxl keeps the supports of lanes l16, 16 + l16, ... side by side (one vector load
 // per lane).
 //
-// Slot order.  An accumulator read or write of a tile is served 8 lanes at a time, and 8 rows of
-// distinct residue mod 8 fall in distinct LDS banks (40-float rows).  Slots are therefore ordered
-// by (occurrence of the residue so far, row mod 8), which deals the residues round-robin over the
-// runs of 8 positions: a residue held by at most F_in / 8 slots never appears twice in a run.
+// Slot order: slot_positions (the residues of the rows mod 8 dealt round-robin, for the banks).
 // One group per wave step (the four waves of a workgroup work independently, each in its own LDS
 // region: the positions and the transposed block).
 constexpr int kTwWaves = 4;
@@ -1015,33 +994,15 @@ __global__ __launch_bounds__(kTwWaves * 64) void k_transpose_w(const bf16_t *__r
     const int TS = Gp + 4;
     const int nq = F_in / 4;                      // slot quads per label
     const int nst = F_in / 16;
-    const uint64_t lt = __lanemask_lt();
     for (int64_t k = (int64_t)blockIdx.x * kTwWaves + wv; k < K; k += (int64_t)gridDim.x * kTwWaves) {
         // slots t = lane and t = lane + 64 (F_in = 128)
-        int f[2], cls[2], occ[2] = {0, 0};
+        int f[2], ps[2];
+        slot_positions(idx + k * F_in, F_in, lane, f, ps);
 #pragma unroll
         for (int i = 0; i < 2; ++i) {
-            const int t = lane + 64 * i;
-            f[i] = t < F_in ? idx[k * F_in + t] : -1;
-            cls[i] = f[i] >= 0 ? (f[i] & 7) : -1;  // row mod 8
-        }
-        int cnt[8];
-#pragma unroll
-        for (int v = 0; v < 8; ++v) {
-            const uint64_t m0 = __ballot(cls[0] == v), m1 = __ballot(cls[1] == v);
-            if (cls[0] == v) occ[0] = __popcll(m0 & lt);
-            if (cls[1] == v) occ[1] = __popcll(m0) + __popcll(m1 & lt);
-            cnt[v] = __popcll(m0) + __popcll(m1);
-        }
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            if (cls[i] < 0) continue;
-            const int r = cls[i], o = occ[i];
-            int rank = 0;                         // slots with a smaller (occurrence, residue)
-#pragma unroll
-            for (int v = 0; v < 8; ++v) rank += (cnt[v] < o ? cnt[v] : o) + (v < r && cnt[v] > o ? 1 : 0);
-            spos[lane + 64 * i] = rank;
-            idxl[k * F_in + (rank & 15) * nst + (rank >> 4)] = f[i];
+            if (ps[i] < 0) continue;
+            spos[lane + 64 * i] = ps[i];
+            idxl[k * F_in + (ps[i] & 15) * nst + (ps[i] >> 4)] = (int32_t)acc_row(f[i]);
         }
         __builtin_amdgcn_wave_barrier();
         const uint2 *src = reinterpret_cast<const uint2 *>(W + k * G * F_in);
@@ -1073,11 +1034,9 @@ __global__ __launch_bounds__(kTwWaves * 64) void k_transpose_w(const bf16_t *__r
 template <int F_IN, int NLB>
 struct BwdXGroup {
     uint4 w[NLB][F_IN / 16];  // W_k^T[16st + l16][32c + 8q .. +7]
-    int f[F_IN / 16];         // accumulator rows idx[k, 16st + l16]
+    int f[F_IN / 16];         // accumulator row offsets acc_row(idx[k, 16st + l16])
 };
 
-constexpr int kBxAS = 40;          // accumulator row stride (floats): 32 rows + 8 pad (bank spread)
-constexpr int kBxASMin = 36;       // where the LDS does not hold the wide rows
 constexpr int kBxConsumers = 2;    // consumer waves (one per 16-row half)
 constexpr int kBxProducers = 4;    // producer waves
 constexpr int kBxProdDepth = 4;    // staged dY chunks in flight per producer wave
@@ -1102,15 +1061,15 @@ __host__ __device__ constexpr int bx_stage_row_bytes(int nlb, int ch) { return 6
 template <int F_IN, int NLB>
 __global__ __launch_bounds__((kBxConsumers + kBxProducers) * 64) void k_bwd_x(
     const int32_t *__restrict__ idx, const bf16_t *__restrict__ WT, const bf16_t *__restrict__ dY, float *__restrict__ part, int B, int Bp, int F_s, int64_t L, int G, int Gp,
-    int64_t K, int nbt, int64_t gps, int CH, int AS) {
-    extern __shared__ __align__(16) float accs[];  // [F_s][AS], then the staged dY
+    int64_t K, int nbt, int64_t gps, int CH) {
+    extern __shared__ __align__(16) float accs[];  // [F_s][32] (swizzled, acc_row), then the staged dY
     constexpr int NST = F_IN / 16;                 // 16-slot tiles
     constexpr int NP = kBxProducers;
     constexpr int NJ = 32 / NP;                    // rows per producer wave and chunk
     constexpr int NB = bx_depth_for(F_IN, NLB);
     constexpr int GB = 64 * NLB;                   // staged bytes per group and row
     const int RS = bx_stage_row_bytes(NLB, CH);    // staged row stride
-    char *ys = reinterpret_cast<char *>(accs + F_s * AS);   // [2][32][RS]
+    char *ys = reinterpret_cast<char *>(accs + F_s * 32);   // [2][32][RS]
     const int cbytes = 32 * RS;
     const int w = blockIdx.x;
     const int xcd = w % kXcds;
@@ -1134,7 +1093,7 @@ __global__ __launch_bounds__((kBxConsumers + kBxProducers) * 64) void k_bwd_x(
     // accumulator and the whole staging area (its zero label padding is never written again)
     {
         uint32_t *z = reinterpret_cast<uint32_t *>(accs);
-        const int nz = F_s * AS + (2 * cbytes) / 4;
+        const int nz = F_s * 32 + (2 * cbytes) / 4;
         for (int e = tid; e < nz; e += nthr) z[e] = 0u;
     }
     __syncthreads();
@@ -1258,17 +1217,17 @@ __global__ __launch_bounds__((kBxConsumers + kBxProducers) * 64) void k_bwd_x(
 
         // this lane's dY operand: row 16 bh + l16 of a group, labels 32c + 8q .. +7
         const char *ylane = ys + (16 * bh + l16) * RS + 16 * q;
-        // this lane's accumulator column: rows 16 bh + 4q .. +3 of an accumulator row
+        // this lane's accumulator chunk: rows 16 bh + 4q .. +3 of an accumulator row
         typedef __attribute__((address_space(3))) f32x4_t lds_f32x4_t;
-        const uint32_t acol = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) float *)accs +
-                              (uint32_t)((16 * bh + 4 * q) * 4);   // LDS byte address
+        const uint32_t abase = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) float *)accs;
+        const uint32_t achunk = (uint32_t)((4 * bh + q) << 4);
         auto read_dy = [&](uint4 (&ay)[NLB], const char *yp) {
 #pragma unroll
             for (int c = 0; c < NLB; ++c) ay[c] = *reinterpret_cast<const uint4 *>(yp + 64 * c);
         };
 
-        auto acc_addr = [&](int f) {
-            uint32_t ao = __umul24((uint32_t)f, (uint32_t)(AS * 4)) + acol;
+        auto acc_addr = [&](int f) {   // f: acc_row of the accumulator row
+            uint32_t ao = ((uint32_t)f ^ achunk) + abase;
             asm volatile("" : "+v"(ao));   // computed once, kept for the write
             return ao;
         };
@@ -1341,7 +1300,7 @@ __global__ __launch_bounds__((kBxConsumers + kBxProducers) * 64) void k_bwd_x(
     __syncthreads();
     for (int e = tid; e < F_s * 32; e += nthr) {
         const int f = e >> 5, b = e & 31;
-        pp[(size_t)f * Bp + b] = accs[f * AS + b];
+        pp[(size_t)f * Bp + b] = accs[acc_index(f, b)];
     }
 }
 
@@ -1358,7 +1317,7 @@ hipError_t allow_lds(Kern k, size_t bytes) {
 }
 
 struct BwdXGeom {
-    int nbt, nwaves, ch, as;
+    int nbt, nwaves, ch;
     int64_t nseg, gps;
     size_t lds;
 };
@@ -1373,11 +1332,9 @@ BwdXGeom bwd_x_geom(const haste::TailArgs &a) {
     int ch = (int)(256 / a.G) < kBxChunkBytes / gb ? (int)(256 / a.G) : kBxChunkBytes / gb;
     const int nb = bx_depth_for(a.F_in, nlb);
     auto stage = [&](int c) { return (int64_t)2 * 32 * bx_stage_row_bytes(nlb, c); };   // both buffers
-    // the wide accumulator rows where the LDS still holds chunks of at least one pass
-    g.as = (int64_t)a.F_s * kBxAS * 4 + stage(nb) <= (int64_t)kLdsBudget ? kBxAS : kBxASMin;
-    while (ch > 0 && (int64_t)a.F_s * g.as * 4 + stage(ch) > (int64_t)kLdsBudget) --ch;
+    while (ch > 0 && (int64_t)a.F_s * 128 + stage(ch) > (int64_t)kLdsBudget) --ch;
     g.ch = ch / nb * nb;
-    g.lds = (size_t)a.F_s * g.as * 4 + (size_t)stage(g.ch);
+    g.lds = (size_t)a.F_s * 128 + (size_t)stage(g.ch);
     const int64_t K = a.L / a.G;
     int64_t spx = kCusPerXcd / g.nbt;  // one workgroup per CU: the accumulator takes most of the LDS
     if (spx < 1) spx = 1;
@@ -1732,7 +1689,7 @@ static hipError_t launch_bwd_x(const TailArgs &a, const BwdXGeom &g, const int32
     const int64_t K = a.L / a.G;
     hipLaunchKernelGGL(kern, dim3((unsigned)(g.nseg * g.nbt)), dim3(g.nwaves * 64), g.lds, s, idx, WT,
                        (const bf16_t *)dY, part, (int)a.B, g.nbt * 32, (int)a.F_s, a.L, (int)a.G,
-                       (int)round_up(a.G, 8), K, g.nbt, g.gps, g.ch, g.as);
+                       (int)round_up(a.G, 8), K, g.nbt, g.gps, g.ch);
     return hipGetLastError();
 }
 

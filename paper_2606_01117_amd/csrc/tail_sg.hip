@@ -18,6 +18,8 @@
 // in passes of 128 labels (one 16-label tile per wave): the pass's supports and weights are staged
 // in LDS (prefetched into registers during the previous pass), and its logits leave through LDS
 // as 256-byte row runs.  The batch slabs of a segment run on one XCD, sharing W through its L2.
+#include <utility>
+
 #include "common.hpp"
 
 namespace {
@@ -443,6 +445,367 @@ static hipError_t bwd_w_sg_g(const haste::TailArgs &a, const void *Xb, const int
     return hipErrorInvalidValue;
 }
 
+
+// ---------------------------------------------------------------------------------------------
+// Backward-feature for small groups (G = 1, 2, 4, 8; bf16):
+//   dX^T[f][rows] = sum over groups k and slots t with idx[k, t] = f of
+//                   sum over the labels l of group k of W[l, t] dY[rows, l]   (Section 3.2),
+// as the general kernel computes it (per-segment partial dX^T in LDS, fixed-order reduction), but
+// with 32 consecutive labels (a "super-group" of 32 / G groups) per matrix-core K step.
+//   M = 16 rows, N = 16 slots of one group, K = the super-group's 32 labels in natural order.
+//   A (rows x labels): the staged dY block, one 16-byte LDS read per super-group, shared by the
+//     tiles of all of its groups.
+//   B (labels x slots): group gi's labels are K positions G gi .. G gi + G - 1, inside the 8-label
+//     octet q = G gi / 8; lane (slot l16, octet q) holds W[G gi + u][slot] (u < G) there and zeros
+//     elsewhere, and every other lane holds zeros.  The pre-pass lays W out per super-group so
+//     that the non-zero values one lane contributes over all of its tiles are F_in contiguous
+//     bytes: per super-group a consumer wave reads the 32-label block exactly once.
+//   D: lane (slot, q) holds rows 4q .. 4q + 3 of the slot, added into accumulator row idx[k, slot].
+// The slots of one group are distinct features, so the 16 accumulator rows of a tile are distinct;
+// the groups of a super-group can share features, so each group's accumulator reads follow the
+// previous group's writes in the wave's LDS program order.
+// ---------------------------------------------------------------------------------------------
+// f(integral_constant<int, I>) for I = 0 .. N - 1, unrolled at compile time
+template <typename F, int... I>
+__device__ __forceinline__ void static_for_impl(F &&f, std::integer_sequence<int, I...>) {
+    (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F &&f) {
+    static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+constexpr int kBsConsumers = 2;                  // consumer waves (one per 16-row half)
+constexpr int kBsProducers = 2;                  // producer waves (staging dY)
+constexpr int kBsThreads = 64 * (kBsConsumers + kBsProducers);
+// groups' supports in flight per consumer lane (16, at most 64 registers), and the weight blocks
+// of the next two super-groups: the loads come from HBM for the first batch tile of a segment
+__host__ __device__ constexpr int bs_idx_depth(int f_in) { return f_in <= 64 ? 16 : 8; }
+
+__host__ __device__ constexpr int bs_row_bytes(int ch) { return ch * 64 + 32; }   // staged dY row
+__host__ __device__ constexpr int bs_stage_bytes(int ch) { return 2 * 32 * bs_row_bytes(ch); }
+
+// Pre-pass: per group (one wave each), its supports in lane order as accumulator row offsets
+// (idxl, as the general kernel's)
+// and its weights into the super-group block WS: lane (l16, q) of super-group n owns the F_in bytes
+// at ((n 4 + q) 16 + l16) F_in, holding for each group gi of octet q (local index j = gi mod 8/G)
+// and slot tile st the G weights of position 16 st + l16 at byte (j F_in / 16 + st) 2G.  Groups
+// from K to the end of the last super-group are written as zeros.
+constexpr int kBtWaves = 8;
+
+__global__ __launch_bounds__(kBtWaves * 64) void k_transpose_w_sg(const bf16_t *__restrict__ W,
+                                                                  const int32_t *__restrict__ idx,
+                                                                  bf16_t *__restrict__ WS, int32_t *__restrict__ idxl,
+                                                                  int64_t K, int64_t Kp, int G, int F_in) {
+    __shared__ int pslot[kBtWaves][128];          // slot at each position
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int nst = F_in / 16, sg = 32 / G;
+    for (int64_t k = (int64_t)blockIdx.x * kBtWaves + wv; k < Kp; k += (int64_t)gridDim.x * kBtWaves) {
+        if (k < K) {   // wave-uniform
+            int f[2], ps[2];
+            slot_positions(idx + k * F_in, F_in, lane, f, ps);
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                if (ps[i] < 0) continue;
+                pslot[wv][ps[i]] = lane + 64 * i;
+                idxl[k * F_in + (ps[i] & 15) * nst + (ps[i] >> 4)] = (int32_t)acc_row(f[i]);
+            }
+        }
+        __builtin_amdgcn_wave_barrier();
+        const int64_t n = k / sg;
+        const int gi = (int)(k - n * sg);
+        const int q = G * gi / 8, j = gi % (8 / G);
+        for (int p = lane; p < F_in; p += 64) {
+            const int l16 = p & 15, st = p >> 4;
+            char *dst = reinterpret_cast<char *>(WS) + ((n * 4 + q) * 16 + l16) * F_in + (j * nst + st) * 2 * G;
+            uint32_t v[4] = {0u, 0u, 0u, 0u};
+            if (k < K) {
+                const int t = pslot[wv][p];
+                for (int u = 0; u < G; ++u) {
+                    const uint32_t w = W[(k * G + u) * F_in + t];
+                    v[u >> 1] |= (u & 1) ? w << 16 : w;
+                }
+            }
+            if (G == 8) *reinterpret_cast<uint4 *>(dst) = make_uint4(v[0], v[1], v[2], v[3]);
+            else if (G == 4) *reinterpret_cast<uint2 *>(dst) = make_uint2(v[0], v[1]);
+            else if (G == 2) *reinterpret_cast<uint32_t *>(dst) = v[0];
+            else *reinterpret_cast<bf16_t *>(dst) = (bf16_t)v[0];
+        }
+        __builtin_amdgcn_wave_barrier();
+    }
+}
+
+// The B operand of tile (group gi of the super-group, slot tile st) from the lane's F_in bytes wc.
+template <int G, int NST, int GI, int ST>
+__device__ __forceinline__ uint4 bs_operand(const uint32_t *wc, bool act) {
+    constexpr int J = GI % (8 / G);
+    uint32_t o[4] = {0u, 0u, 0u, 0u};
+    if constexpr (G >= 2) {
+        constexpr int DW = G / 2;                         // dwords per tile
+        constexpr int D0 = (J * NST + ST) * DW;           // first source dword
+        constexpr int P0 = ((G * GI) % 8) / 2;            // first destination dword
+#pragma unroll
+        for (int t = 0; t < DW; ++t) o[P0 + t] = act ? wc[D0 + t] : 0u;
+    } else {
+        constexpr int E = J * NST + ST;                   // source bf16
+        const uint32_t x = (E & 1) ? (wc[E >> 1] >> 16) : (wc[E >> 1] & 0xffffu);
+        o[(GI % 8) / 2] = act ? ((GI & 1) ? x << 16 : x) : 0u;
+    }
+    return make_uint4(o[0], o[1], o[2], o[3]);
+}
+
+template <int G, int F_IN, int CH>
+__global__ __launch_bounds__(kBsThreads) void k_bwd_x_sg(const int32_t *__restrict__ idxl, const bf16_t *__restrict__ WS,
+                                                         const bf16_t *__restrict__ dY, float *__restrict__ part, int B,
+                                                         int Bp, int F_s, int64_t L, int64_t K, int nbt, int64_t sps,
+                                                         int64_t nsg) {
+    constexpr int SG = 32 / G;                    // groups per super-group
+    constexpr int NST = F_IN / 16;                // slot tiles per group
+    constexpr int NWD = F_IN / 4;                 // dwords of W per lane and super-group
+    constexpr int D = bs_idx_depth(F_IN);
+    // weight blocks: a ring of NWR super-groups, loaded WD ahead
+    constexpr int NWR = SG >= 16 ? 2 : 4;
+    constexpr int WD = NWR - 1;
+    // super-groups per unrolled period: every ring slot index is then a compile-time constant, so
+    // no register is copied while its load is in flight (which would cost a wait for all loads)
+    constexpr int P = (D > SG ? D / SG : 1) > NWR ? (D > SG ? D / SG : 1) : NWR;
+    static_assert(P % NWR == 0 && (P * SG) % D == 0, "ring periods");
+    constexpr int RS = bs_row_bytes(CH);
+    constexpr int CB = 32 * RS;                   // bytes per chunk buffer
+    static_assert((D > SG ? D % SG : SG % D) == 0, "the supports' ring must wrap at super-group boundaries");
+    extern __shared__ __align__(16) float bsa[];  // [F_s][32] accumulator (acc_row), then [2][32][RS] staged dY
+    char *ys = reinterpret_cast<char *>(bsa + (size_t)F_s * 32);
+    const int w = blockIdx.x, xcd = w % kXcds, jj = w / kXcds;
+    const int bt = jj % nbt;
+    const int64_t seg = (int64_t)(jj / nbt) * kXcds + xcd;
+    const int b0 = bt * 32;
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int l16 = lane & 15, q = lane >> 4;
+    float *pp = part + (size_t)seg * F_s * Bp + b0;
+    const int64_t s_begin = seg * sps;
+    const int64_t s_end = s_begin + sps < nsg ? s_begin + sps : nsg;
+    if (s_begin >= s_end) {   // empty segment: the partial is zero (workgroup-uniform)
+        for (int e = tid; e < F_s * 32; e += kBsThreads) pp[(size_t)(e >> 5) * Bp + (e & 31)] = 0.0f;
+        return;
+    }
+    for (int e = tid; e < F_s * 32; e += kBsThreads) bsa[e] = 0.0f;
+    __syncthreads();
+    const int n = (int)(s_end - s_begin);         // super-groups of this segment
+    const int nch = (n + CH - 1) / CH;            // staged chunks
+
+    if (wave >= kBsConsumers) {
+        // ---- producers: chunk c = super-groups c CH .. of the segment, 32 rows x CH 64 bytes ----
+        // Lane i of instruction r of wave p: row 2 (p + kBsProducers r) + i / 32, 16-byte piece
+        // i mod 32 (8 labels) of the chunk; labels past the layer (and rows past B) stage zeros.
+        constexpr int PPR = 4 * CH;               // pieces per row
+        constexpr int RPI = 64 / PPR;             // rows per instruction
+        constexpr int NI = 32 / (RPI * kBsProducers);
+        static_assert(NI * RPI * kBsProducers == 32, "producer rows");
+        const int p = wave - kBsConsumers;
+        const int rows = B - b0 < 32 ? B - b0 : 32;
+        const int pr = lane / PPR, pc = lane % PPR;
+        const Buf db(dY + (int64_t)b0 * L, (uint32_t)((int64_t)rows * L * 2));
+        uint4 v[2][NI];
+        auto load = [&](int c, uint4 (&vv)[NI]) {
+            const int64_t lab = (s_begin + (int64_t)c * CH) * 32 + 8 * pc;
+            const int nvalid = lab >= L ? 0 : (L - lab >= 8 ? 8 : (int)(L - lab));   // even (L even)
+#pragma unroll
+            for (int i = 0; i < NI; ++i) {
+                const int r = RPI * (p + kBsProducers * i) + pr;
+                const uint32_t off = (nvalid > 0 && r < rows) ? (uint32_t)(((int64_t)r * L + lab) * 2) : kOob;
+                if (nvalid == 8 || nvalid == 0) {
+                    vv[i] = db.ld16(off);
+                } else {
+                    // the row's last piece when L is not a multiple of 8: dword by dword, so that
+                    // nothing past the row (the next row, or past the end of dY) is read
+                    vv[i] = make_uint4(db.ld4(off), db.ld4(nvalid > 2 ? off + 4 : kOob),
+                                       db.ld4(nvalid > 4 ? off + 8 : kOob), db.ld4(nvalid > 6 ? off + 12 : kOob));
+                }
+            }
+        };
+        auto store = [&](int c, const uint4 (&vv)[NI]) {
+            char *yb = ys + (c & 1) * CB + pc * 16;
+#pragma unroll
+            for (int i = 0; i < NI; ++i) *reinterpret_cast<uint4 *>(yb + (RPI * (p + kBsProducers * i) + pr) * RS) = vv[i];
+        };
+        load(0, v[0]);
+        if (nch > 1) load(1, v[1]);
+        // chunk c into buffer c % 2 (free: its previous chunk, c - 2, was consumed before barrier
+        // c - 1), then barrier c hands it over; the registers then take chunk c + 2
+        for (int c = 0; c < nch; c += 2) {
+            store(c, v[0]);
+            if (c + 2 < nch) load(c + 2, v[0]);
+            __syncthreads();
+            if (c + 1 < nch) {
+                store(c + 1, v[1]);
+                if (c + 3 < nch) load(c + 3, v[1]);
+                __syncthreads();
+            }
+        }
+    } else {
+        // ---- consumers: rows 16 bh .. 16 bh + 15 of the tile ----
+        const int bh = wave;
+        const int64_t g_begin = s_begin * SG;
+        const int64_t g_end = s_end * SG < K ? s_end * SG : K;
+        // the segment's weight blocks and lane-ordered supports
+        const Buf wseg(WS + s_begin * 32 * F_IN, (uint32_t)(n * 64 * F_IN));
+        const Buf iseg(idxl + g_begin * F_IN, (uint32_t)((g_end - g_begin) * F_IN * 4));
+        const uint32_t wlane = (uint32_t)((q * 16 + l16) * F_IN);
+        auto load_w = [&](int s, uint32_t (&wv)[NWD]) __attribute__((always_inline)) {
+            const int sc = s < n ? s : n - 1;
+#pragma unroll
+            for (int i = 0; i < NWD / 4; ++i) {
+                const uint4 x = __builtin_bit_cast(
+                    uint4, __builtin_amdgcn_raw_buffer_load_b128(wseg.r, (int)(wlane + 16 * i), sc * 64 * F_IN, 0));
+                wv[4 * i] = x.x;
+                wv[4 * i + 1] = x.y;
+                wv[4 * i + 2] = x.z;
+                wv[4 * i + 3] = x.w;
+            }
+        };
+        const int ng = (int)(g_end - g_begin);   // at least 1
+        // g: group index within the segment, clamped to its last (the padding groups of the last
+        // super-group then repeat a real group's rows with zero weights, adding zeros)
+        auto load_f = [&](int gu, int (&f)[NST]) __attribute__((always_inline)) {
+            const int g = gu < ng ? gu : ng - 1;
+            const uint32_t o = (uint32_t)(l16 * NST * 4);
+            if constexpr (NST == 2) {
+                const uint2 x = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(iseg.r, (int)o, g * F_IN * 4, 0));
+                f[0] = (int)x.x;
+                f[1] = (int)x.y;
+            } else {
+#pragma unroll
+                for (int h = 0; h < NST / 4; ++h) {
+                    const uint4 x = __builtin_bit_cast(
+                        uint4, __builtin_amdgcn_raw_buffer_load_b128(iseg.r, (int)(o + 16 * h), g * F_IN * 4, 0));
+                    f[4 * h] = (int)x.x;
+                    f[4 * h + 1] = (int)x.y;
+                    f[4 * h + 2] = (int)x.z;
+                    f[4 * h + 3] = (int)x.w;
+                }
+            }
+        };
+        typedef __attribute__((address_space(3))) f32x4_t lds_f32x4_t;
+        const uint32_t abase = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) float *)bsa;
+        const uint32_t achunk = (uint32_t)((4 * bh + q) << 4);   // rows 16 bh + 4q .. +3
+        const char *ylane = ys + (16 * bh + l16) * RS + 16 * q;
+
+        uint32_t wr[NWR][NWD];                    // super-group s in slot s % NWR
+        int fr[D][NST];                           // group g of the segment in slot g % D
+#pragma unroll
+        for (int i = 0; i < WD; ++i) load_w(i, wr[i]);
+#pragma unroll
+        for (int d = 0; d < D; ++d) load_f(d, fr[d]);
+        // super-group s = s0 + UU (s0 a multiple of P)
+        auto step = [&](int s, auto uc) __attribute__((always_inline)) {
+            constexpr int UU = decltype(uc)::value;
+            if (s > 0 && s % CH == 0) __syncthreads();   // chunk s / CH staged (workgroup-uniform)
+            load_w(s + WD, wr[(UU + WD) % NWR]);          // the slot super-group s - 1 used
+            __builtin_amdgcn_sched_barrier(0);
+            const uint32_t *wc = wr[UU % NWR];
+            const uint4 ay = *reinterpret_cast<const uint4 *>(ylane + ((s / CH) & 1) * CB + (s % CH) * 64);
+            const bf16x8_t a = as_bf16x8(ay);
+            // the SG groups of the super-group, in order
+            static_for<SG>([&](auto gic) __attribute__((always_inline)) {
+                constexpr int GI = decltype(gic)::value;
+                constexpr int R = (UU * SG + GI) % D;     // ring slot of this group's supports
+                const bool act = q == (G * GI) / 8;
+                uint32_t ao[NST];
+#pragma unroll
+                for (int st = 0; st < NST; ++st) ao[st] = ((uint32_t)fr[R][st] ^ achunk) + abase;
+                load_f(s * SG + GI + D, fr[R]);
+                __builtin_amdgcn_sched_barrier(0);   // keep the prefetch where it is issued
+                f32x4_t acc[NST];
+#pragma unroll
+                for (int st = 0; st < NST; ++st) acc[st] = *(lds_f32x4_t *)(uintptr_t)ao[st];
+                // D = dY_s W_gi + old through the matrix core's accumulator input
+                static_for<NST>([&](auto stc) __attribute__((always_inline)) {
+                    constexpr int ST = decltype(stc)::value;
+                    acc[ST] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        a, as_bf16x8(bs_operand<G, NST, GI, ST>(wc, act)), acc[ST], 0, 0, 0);
+                });
+#pragma unroll
+                for (int st = 0; st < NST; ++st) *(lds_f32x4_t *)(uintptr_t)ao[st] = acc[st];
+            });
+        };
+        __syncthreads();                          // chunk 0 staged
+        // whole periods (no exit inside one, so the loads' waits keep their depth across the loop's
+        // back edge), then the rest
+        int s0 = 0;
+        for (; s0 + P <= n; s0 += P)
+            static_for<P>([&](auto uc) __attribute__((always_inline)) { step(s0 + decltype(uc)::value, uc); });
+        static_for<P>([&](auto uc) __attribute__((always_inline)) {
+            if (s0 + decltype(uc)::value < n) step(s0 + decltype(uc)::value, uc);
+        });
+    }
+    __syncthreads();
+    for (int e = tid; e < F_s * 32; e += kBsThreads) {
+        const int f = e >> 5, b = e & 31;
+        pp[(size_t)f * Bp + b] = bsa[acc_index(f, b)];
+    }
+}
+
+struct BsGeom {
+    int nbt, ch;
+    int64_t nsg, nseg, sps;
+    size_t lds;
+};
+
+static BsGeom bs_geom(const haste::TailArgs &a) {
+    BsGeom g;
+    g.nbt = (int)haste::cdiv(a.B, 32);
+    g.nsg = haste::cdiv(a.L, 32);
+    constexpr int64_t budget = 160 * 1024;
+    // 8 super-groups per chunk where they fit beside the accumulator, else 2
+    g.ch = (int64_t)a.F_s * 128 + bs_stage_bytes(8) <= budget ? 8 : 2;
+    g.lds = (size_t)a.F_s * 128 + (size_t)bs_stage_bytes(g.ch);
+    int64_t spx = kCusPerXcd / g.nbt;   // one workgroup per CU: the accumulator takes most of the LDS
+    if (spx < 1) spx = 1;
+    const int64_t max_spx = haste::cdiv(g.nsg, kXcds);
+    if (spx > max_spx) spx = max_spx;
+    g.nseg = spx * kXcds;
+    g.sps = haste::cdiv(g.nsg, g.nseg);
+    return g;
+}
+
+template <int G, int F_IN, int CH>
+static hipError_t launch_bwd_x_sg(const haste::TailArgs &a, const BsGeom &g, const int32_t *idxl, const bf16_t *WS,
+                                  const void *dY, float *part, hipStream_t s) {
+    auto kern = k_bwd_x_sg<G, F_IN, CH>;
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       (int)g.lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(kern, dim3((unsigned)(g.nseg * g.nbt)), dim3(kBsThreads), g.lds, s, idxl, WS,
+                       (const bf16_t *)dY, part, (int)a.B, g.nbt * 32, (int)a.F_s, a.L, a.L / a.G, g.nbt, g.sps, g.nsg);
+    return hipGetLastError();
+}
+
+template <int G, int F_IN>
+static hipError_t bwd_x_sg_f(const haste::TailArgs &a, const BsGeom &g, const int32_t *idxl, const bf16_t *WS,
+                             const void *dY, float *part, hipStream_t s) {
+    return g.ch == 8 ? launch_bwd_x_sg<G, F_IN, 8>(a, g, idxl, WS, dY, part, s)
+                     : launch_bwd_x_sg<G, F_IN, 2>(a, g, idxl, WS, dY, part, s);
+}
+
+template <int G>
+static hipError_t bwd_x_sg_g(const haste::TailArgs &a, const BsGeom &g, const int32_t *idxl, const bf16_t *WS,
+                             const void *dY, float *part, hipStream_t s) {
+    switch (a.F_in) {
+        case 32: return bwd_x_sg_f<G, 32>(a, g, idxl, WS, dY, part, s);
+        case 64: return bwd_x_sg_f<G, 64>(a, g, idxl, WS, dY, part, s);
+        case 128: return bwd_x_sg_f<G, 128>(a, g, idxl, WS, dY, part, s);
+    }
+    return hipErrorInvalidValue;
+}
+
+// workspace: the per-segment partials, the super-group weight blocks, the lane-ordered supports
+static size_t bs_part_bytes(const haste::TailArgs &a, const BsGeom &g) {
+    return (size_t)haste::round_up(g.nseg * a.F_s * (g.nbt * 32) * 4, 256);
+}
+static size_t bs_ws_bytes(const haste::TailArgs &a, const BsGeom &g) {
+    return (size_t)haste::round_up(g.nsg * 32 * a.F_in * 2, 256);
+}
+
 }  // namespace
 
 namespace haste {
@@ -478,6 +841,44 @@ hipError_t bwd_w_sg(const TailArgs &a, const void *X, const int32_t *idx, const 
         case 8: return bwd_w_sg_g<8>(a, ws, idx, dY, dW, dbias, beta, Bp, s);
     }
     return hipErrorInvalidValue;
+}
+
+// backward-feature: bf16, G in {1, 2, 4, 8}, F_in in {32, 64, 128}, even F_s up to kMaxFs; dY rows
+// dword-aligned (L even) and 32 rows of them within the 31-bit range of a buffer offset.
+bool bwd_x_sg_supported(const TailArgs &a) {
+    if (a.dtype != HASTE_DTYPE_BF16 || !(a.G == 1 || a.G == 2 || a.G == 4 || a.G == 8)) return false;
+    if (!(a.F_in == 32 || a.F_in == 64 || a.F_in == 128)) return false;
+    if (a.F_s % 2 != 0 || a.F_s > kMaxFs || a.L % 2 != 0 || a.L * 32 * 2 >= ((int64_t)1 << 31)) return false;
+    const BsGeom g = bs_geom(a);
+    return g.lds <= 160 * 1024 && g.sps * 64 * a.F_in < ((int64_t)1 << 31);
+}
+
+size_t bwd_x_sg_ws(const TailArgs &a) {
+    const BsGeom g = bs_geom(a);
+    return bs_part_bytes(a, g) + bs_ws_bytes(a, g) + (size_t)round_up((a.L / a.G) * a.F_in * 4, 256);
+}
+
+hipError_t bwd_x_sg(const TailArgs &a, const int32_t *idx, const void *W, const void *dY, float *dX, int beta, void *ws,
+                    hipStream_t s) {
+    const BsGeom g = bs_geom(a);
+    float *part = reinterpret_cast<float *>(ws);
+    bf16_t *WS = reinterpret_cast<bf16_t *>(reinterpret_cast<char *>(ws) + bs_part_bytes(a, g));
+    int32_t *idxl = reinterpret_cast<int32_t *>(reinterpret_cast<char *>(WS) + bs_ws_bytes(a, g));
+    const int64_t K = a.L / a.G, Kp = g.nsg * (32 / a.G);
+    const int64_t tgrid = cdiv(Kp, kBtWaves) < 8192 ? cdiv(Kp, kBtWaves) : 8192;
+    hipLaunchKernelGGL(k_transpose_w_sg, dim3((unsigned)tgrid), dim3(kBtWaves * 64), 0, s, (const bf16_t *)W, idx, WS,
+                       idxl, K, Kp, (int)a.G, (int)a.F_in);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    switch (a.G) {
+        case 1: e = bwd_x_sg_g<1>(a, g, idxl, WS, dY, part, s); break;
+        case 2: e = bwd_x_sg_g<2>(a, g, idxl, WS, dY, part, s); break;
+        case 4: e = bwd_x_sg_g<4>(a, g, idxl, WS, dY, part, s); break;
+        case 8: e = bwd_x_sg_g<8>(a, g, idxl, WS, dY, part, s); break;
+        default: return hipErrorInvalidValue;
+    }
+    if (e != hipSuccess) return e;
+    return reduce_fmajor(part, (int)g.nseg, g.nbt * 32, a.B, a.F_s, dX, beta, s);
 }
 
 hipError_t fwd_sg(const TailArgs &a, const void *X, const int32_t *idx, const void *W, const float *bias, void *Y,

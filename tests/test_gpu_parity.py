@@ -66,6 +66,11 @@ SMALL = [
     ("bf16_g8_f64_l2056", 100, 768, 2056, 8, 64, BF16),
     ("bf16_g2_f32_l1030", 40, 512, 1030, 2, 32, BF16),
     ("bf16_g4_b1", 1, 768, 1024, 4, 64, BF16),
+    # backward-feature's small-group kernel: 32-label super-groups cut short at the end of the layer
+    # (and rows ending inside a 16-byte piece), the narrow staging of the widest feature dimension
+    ("bf16_g1_f128_l1062", 45, 512, 1062, 1, 128, BF16),
+    ("bf16_g8_f128", 33, 768, 1024, 8, 128, BF16),
+    ("bf16_g4_fs1024", 40, 1024, 2048, 4, 64, BF16),
     ("f32_g8", 32, 256, 4096, 8, 32, F32),
     ("f32_g1", 9, 100, 300, 1, 7, F32),
     ("f32_g32_f64", 50, 768, 2048, 32, 64, F32),
@@ -266,8 +271,9 @@ def test_empty_batch_and_labels(hs):
     assert float(dX.abs().max()) == 0.0
 
 
-def test_repeatable(hs):
-    wl = synth.small("repeat", B=256, F_s=768, L=65536, G=32, F_in=64, dtype=BF16, wid=503, dy_normal=True)
+@pytest.mark.parametrize("G", [32, 4])
+def test_repeatable(hs, G):
+    wl = synth.small("repeat", B=256, F_s=768, L=65536, G=G, F_in=64, dtype=BF16, wid=503, dy_normal=True)
     X, idx, W, _, dY = make_inputs(wl)
     lay = Layer(hs, wl, X, idx, W, None, dY)
     lay.fwd(); lay.bwd_w(); lay.bwd_x()
