@@ -203,7 +203,7 @@ int haste_sgd_momentum(int64_t n, int32_t dtype, const void *W, const float *gra
  * (fp32(1/sqrt(F_in)) * 2^-24) with n = out(K F + l F + j) >> 40.
  * idx [K, F_in] int32 (strictly increasing rows, precondition), W [L, F_in] (dtype) and m
  * [L, F_in] fp32 (or NULL) are updated in place.  rho in [0, 1); *n_pruned (host, or NULL)
- * receives m.  F_in <= 128.  ws: haste_workspace_bytes(desc, HASTE_OP_REWIRE) bytes; desc->B is
+ * receives m.  F_in <= 256.  ws: haste_workspace_bytes(desc, HASTE_OP_REWIRE) bytes; desc->B is
  * not used.
  */
 int haste_rewire(const haste_desc_t *desc, int32_t *idx, void *W, float *m, double rho, int32_t init_random,

@@ -398,7 +398,7 @@ int haste_rewire(const haste_desc_t *d, int32_t *idx, void *W, float *m, double 
     if (!(rho >= 0.0 && rho < 1.0)) return fail(HASTE_ERR_INVALID, "rho must be in [0, 1)");
     if (init_random != 0 && init_random != 1) return fail(HASTE_ERR_INVALID, "init_random must be 0 or 1");
     const haste::TailArgs a = targs(d);
-    if (!haste::rewire_supported(a)) return fail(HASTE_ERR_UNSUPPORTED, "rewiring takes at most 128 slots per group");
+    if (!haste::rewire_supported(a)) return fail(HASTE_ERR_UNSUPPORTED, "rewiring takes at most 256 slots per group and 1024 features");
     const int64_t K = a.L / a.G;
     const int64_t npr = (int64_t)floor((double)K * (double)a.F_in * rho);
     if (n_pruned) *n_pruned = npr;

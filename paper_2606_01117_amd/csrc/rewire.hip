@@ -158,10 +158,10 @@ __global__ __launch_bounds__(256) void k_rw_mark(const uint32_t *__restrict__ ke
     }
 }
 
-// Regrowth, one wave per group with a pruned slot.  F <= 128 slots (two per lane), H <= 1024
+// Regrowth, one wave per group with a pruned slot.  F <= 256 slots (up to four per lane), H <= 1024
 // features (one 32-bit word of the wave's used-feature bitmap per lane).
 constexpr int kRwWaves = 4;
-constexpr int kRwMaxF = 128;
+constexpr int kRwMaxF = 256;
 
 template <typename T>
 __global__ __launch_bounds__(64 * kRwWaves) void k_rw_regrow(int32_t *__restrict__ idx, T *__restrict__ W,

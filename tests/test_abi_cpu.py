@@ -153,7 +153,7 @@ def test_loss_optimizer_rewire_group_arguments_checked(hs):
     assert ws_r > 0
     assert hs.lib.haste_rewire(ctypes.byref(d), FAKE, FAKE, None, 1.0, 1, 0, None, FAKE, ws_r, None) == 1
     assert hs.lib.haste_rewire(ctypes.byref(d), FAKE, FAKE, None, 0.1, 2, 0, None, FAKE, ws_r, None) == 1
-    wide = hs.make_desc(8, 1024, 4096, 16, 256, hs.HASTE_DTYPE_BF16)
+    wide = hs.make_desc(8, 1024, 4096, 16, 512, hs.HASTE_DTYPE_BF16)
     assert hs.lib.haste_rewire(ctypes.byref(wide), FAKE, FAKE, None, 0.1, 1, 0, None, FAKE, 1 << 30, None) == 2
     # rho = 0 prunes nothing: no launch, no workspace needed
     n = ctypes.c_int64(-1)

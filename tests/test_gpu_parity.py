@@ -71,6 +71,8 @@ SMALL = [
     ("bf16_g1_f128_l1062", 45, 512, 1062, 1, 128, BF16),
     ("bf16_g8_f128", 33, 768, 1024, 8, 128, BF16),
     ("bf16_g4_fs1024", 40, 1024, 2048, 4, 64, BF16),
+    # 256-slot supports (the VALU kernels)
+    ("bf16_g32_f256", 40, 768, 2048, 32, 256, BF16),
     ("f32_g8", 32, 256, 4096, 8, 32, F32),
     ("f32_g1", 9, 100, 300, 1, 7, F32),
     ("f32_g32_f64", 50, 768, 2048, 32, 64, F32),

@@ -50,6 +50,8 @@ CASES = [
     ("bf16_g1_ffi", 2000, 1, 16, 100, BF16, 0.05, 1, False),
     ("bf16_h_eq_f_plus_1", 64, 4, 63, 64, BF16, 0.5, 1, True),
     ("bf16_many_blocks", 4096, 2, 64, 1024, BF16, 0.02, 1, False),
+    # the widest support the regrowth takes (four slots per lane)
+    ("bf16_g8_f256", 400, 8, 256, 768, BF16, 0.1, 1, True),
 ]
 
 
