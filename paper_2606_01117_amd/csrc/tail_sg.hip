@@ -498,10 +498,15 @@ __global__ __launch_bounds__(kBtWaves * 64) void k_transpose_w_sg(const bf16_t *
                                                                   bf16_t *__restrict__ WS, int32_t *__restrict__ idxl,
                                                                   int64_t K, int64_t Kp, int G, int F_in) {
     __shared__ int pslot[kBtWaves][128];          // slot at each position
+    __shared__ uint32_t wrow[kBtWaves][8 * 128 / 2];   // the group's weights [G][F_in] bf16
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
     const int nst = F_in / 16, sg = 32 / G;
+    const uint16_t *wr16 = reinterpret_cast<const uint16_t *>(wrow[wv]);
     for (int64_t k = (int64_t)blockIdx.x * kBtWaves + wv; k < Kp; k += (int64_t)gridDim.x * kBtWaves) {
         if (k < K) {   // wave-uniform
+            // the group's G weight rows (contiguous), whole dwords, into LDS
+            const uint32_t *src = reinterpret_cast<const uint32_t *>(W + k * G * F_in);
+            for (int e = lane; e < G * F_in / 2; e += 64) wrow[wv][e] = src[e];
             int f[2], ps[2];
             slot_positions(idx + k * F_in, F_in, lane, f, ps);
 #pragma unroll
@@ -522,7 +527,7 @@ __global__ __launch_bounds__(kBtWaves * 64) void k_transpose_w_sg(const bf16_t *
             if (k < K) {
                 const int t = pslot[wv][p];
                 for (int u = 0; u < G; ++u) {
-                    const uint32_t w = W[(k * G + u) * F_in + t];
+                    const uint32_t w = wr16[u * F_in + t];
                     v[u >> 1] |= (u & 1) ? w << 16 : w;
                 }
             }
