@@ -263,11 +263,13 @@ __global__ __launch_bounds__(256, 2) void k_gemm2(const bf16_t *__restrict__ A, 
 constexpr size_t kG2Lds = (size_t)4 * G2TILE * 2;   // two stages of two operand tiles
 
 // ---------------------------------------------------------------------------------------------
-// bf16 GEMM for large tiles: 256x256 output tile, 4 waves in a 2x2 grid each owning a 128x128
-// block (4x4 v_mfma_f32_32x32x16_bf16 accumulators, 256 registers per lane).  K advances in
-// steps of 32 through a ring of 4 LDS stages filled by direct global-to-LDS loads
+// bf16 GEMM for large tiles: 256 x BN output tile (BN = 256 or 128), 4 waves in a 2x2 grid each
+// owning a 128 x BN/2 block (4 x BN/64 v_mfma_f32_32x32x16_bf16 accumulators).  K advances in
+// steps of 32 through a ring of LDS stages filled by direct global-to-LDS loads
 // (buffer_load_dwordx4 ... lds: 64 lanes x 16 bytes land contiguously at the address in M0), so
-// three steps are in flight while one is multiplied, without staging registers.  The loads are
+// the next steps are in flight while one is multiplied, without staging registers: 4 stages and
+// one workgroup per CU at BN = 256; 3 stages and two workgroups per CU at BN = 128 (the head's
+// products use 128), so that one workgroup's epilogue overlaps the other's products.  The loads are
 // issued from inline assembly and waited for explicitly (s_waitcnt vmcnt): issued through the
 // compiler's builtin, every LDS read would first wait for all of them.
 // Stage layouts carry an XOR swizzle of their 16-byte chunks instead of padding, so that a load
