@@ -13,7 +13,7 @@ INCLUDE = os.path.join(ROOT, "include")
 OBJDIR = os.path.join(ROOT, "_build", "haste")
 LIB = os.path.join(PKG, "libhaste.so")
 
-SOURCES = ["abi.hip", "tail_mfma.hip", "tail_valu.hip", "head.hip", "util.hip", "rewire.hip", "group.hip", "static_ws.hip", "tail_sg.hip"]
+SOURCES = ["abi.hip", "tail_mfma.hip", "tail_valu.hip", "head.hip", "util.hip", "rewire.hip", "group.hip", "static_ws.hip", "tail_sg.hip", "tail_dense.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

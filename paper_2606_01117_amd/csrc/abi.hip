@@ -89,6 +89,7 @@ hipError_t fwd_any(const haste::TailArgs &a, const void *X, const int32_t *idx, 
 // cores (both on the workspace's X^T copy), the rest on the vector ALUs
 // backward-feature: small-group kernel, else the general matrix-core kernel, else the VALU kernel
 size_t bwd_x_ws(const haste::TailArgs &a) {
+    if (haste::bwd_x_dn_supported(a)) return haste::bwd_x_dn_ws(a);
     if (haste::bwd_x_sg_supported(a)) return haste::bwd_x_sg_ws(a);
     return haste::bwd_x_mfma_supported(a) ? haste::bwd_x_mfma_ws(a) : haste::bwd_x_valu_ws(a);
 }
@@ -223,12 +224,14 @@ int haste_bwd_x(const haste_desc_t *d, const int32_t *idx, const void *W, const 
     TRY(need_ptr(idx, "idx"));
     TRY(need_ptr(W, "W"));
     TRY(need_ptr(dY, "dY"));
-    if (!haste::bwd_x_sg_supported(a) && !haste::bwd_x_mfma_supported(a) && !haste::valu_supported(a))
+    if (!haste::bwd_x_dn_supported(a) && !haste::bwd_x_sg_supported(a) && !haste::bwd_x_mfma_supported(a) &&
+        !haste::valu_supported(a))
         return fail(HASTE_ERR_UNSUPPORTED, "no backward-feature kernel for this shape");
     const size_t need = bwd_x_ws(a);
     if (!ws || ws_bytes < need)
         return fail(HASTE_ERR_WORKSPACE, "haste_bwd_x needs %zu workspace bytes, got %zu", need, ws ? ws_bytes : 0);
     TRY(need_ptr(ws, "ws"));
+    if (haste::bwd_x_dn_supported(a)) return hip_status(haste::bwd_x_dn(a, idx, W, dY, dX, beta, ws, s), "haste_bwd_x");
     if (haste::bwd_x_sg_supported(a)) return hip_status(haste::bwd_x_sg(a, idx, W, dY, dX, beta, ws, s), "haste_bwd_x");
     if (haste::bwd_x_mfma_supported(a)) return hip_status(haste::bwd_x_mfma(a, idx, W, dY, dX, beta, ws, s), "haste_bwd_x");
     return hip_status(haste::bwd_x_valu(a, idx, W, dY, dX, beta, ws, s), "haste_bwd_x");

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <utility>
+
 #include "haste.h"
 
 typedef uint16_t bf16_t;  // bf16 bit pattern
@@ -46,6 +48,16 @@ __device__ __forceinline__ uint2 lds_read_tr(const void *p) {
 // D[8*i + 4*(l/32) + j][l % 32] in register 4*i + j.
 __device__ __forceinline__ f32x16_t mfma32x32x16(const bf16x8_t &a, const bf16x8_t &b, const f32x16_t &c) {
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// f(integral_constant<int, I>) for I = 0 .. N - 1, unrolled at compile time
+template <typename F, int... I>
+__device__ __forceinline__ void static_for_impl(F &&f, std::integer_sequence<int, I...>) {
+    (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F &&f) {
+    static_for_impl(f, std::make_integer_sequence<int, N>{});
 }
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8_t, v); }
@@ -198,6 +210,12 @@ hipError_t transpose_x(const TailArgs &a, const void *X, void *ws, hipStream_t s
 bool bwd_x_sg_supported(const TailArgs &a);
 size_t bwd_x_sg_ws(const TailArgs &a);
 hipError_t bwd_x_sg(const TailArgs &a, const int32_t *idx, const void *W, const void *dY, float *dX, int beta, void *ws,
+                    hipStream_t s);
+// backward-feature for small groups (G = 1, 2, 4, 8, F_s <= 800) as a dense product over each
+// 32-label step's weights scattered into an LDS tile
+bool bwd_x_dn_supported(const TailArgs &a);
+size_t bwd_x_dn_ws(const TailArgs &a);
+hipError_t bwd_x_dn(const TailArgs &a, const int32_t *idx, const void *W, const void *dY, float *dX, int beta, void *ws,
                     hipStream_t s);
 bool bwd_w_mfma_supported(const TailArgs &a);
 size_t bwd_w_mfma_ws(const TailArgs &a);

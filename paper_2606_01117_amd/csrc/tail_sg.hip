@@ -18,7 +18,6 @@
 // in passes of 128 labels (one 16-label tile per wave): the pass's supports and weights are staged
 // in LDS (prefetched into registers during the previous pass), and its logits leave through LDS
 // as 256-byte row runs.  The batch slabs of a segment run on one XCD, sharing W through its L2.
-#include <utility>
 
 #include "common.hpp"
 
@@ -465,16 +464,6 @@ static hipError_t bwd_w_sg_g(const haste::TailArgs &a, const void *Xb, const int
 // the groups of a super-group can share features, so each group's accumulator reads follow the
 // previous group's writes in the wave's LDS program order.
 // ---------------------------------------------------------------------------------------------
-// f(integral_constant<int, I>) for I = 0 .. N - 1, unrolled at compile time
-template <typename F, int... I>
-__device__ __forceinline__ void static_for_impl(F &&f, std::integer_sequence<int, I...>) {
-    (f(std::integral_constant<int, I>{}), ...);
-}
-template <int N, typename F>
-__device__ __forceinline__ void static_for(F &&f) {
-    static_for_impl(f, std::make_integer_sequence<int, N>{});
-}
-
 constexpr int kBsConsumers = 2;                  // consumer waves (one per 16-row half)
 constexpr int kBsProducers = 2;                  // producer waves (staging dY)
 constexpr int kBsThreads = 64 * (kBsConsumers + kBsProducers);
