@@ -7,33 +7,32 @@
 //
 // With G <= 8 a group's tile of the segmented-accumulator kernels is mostly padding, and their
 // LDS traffic per (label, slot, row) is a 4-byte read and a 4-byte write of the accumulator.  Here
-// the accumulator never leaves the registers: a workgroup owns 32 batch rows and all F_s features
-// (dX^T [F_s][32] fp32 spread over its 8 waves' matrix-core accumulators) for a segment of
-// labels.  Per step of 32 labels:
+// the accumulator never leaves the registers: a workgroup owns 16 MT batch rows and all F_s
+// features (dX^T [F_s][16 MT] fp32 spread over its 8 waves' matrix-core accumulators) for a
+// segment of labels.  Per step of 32 labels:
 //   - the step's weights are scattered into a zeroed [F_s][32] bf16 tile in LDS (one 2-byte write
 //     per (label, slot): W'[l, idx[g(l), t]] = W[l, t]), and cleared with the same writes after use;
-//   - D += A B with A = dY[32 rows][32 labels] (staged in LDS) and B = the tile, F_s / 16 tiles
-//     of v_mfma_f32_16x16x32_bf16 per row half: K = the step's labels, in natural order.
-// Three tiles rotate: step t + 1 is scattered and step t - 1 cleared while step t is multiplied,
-// with one barrier per step.  Each 32-label half of a 64-label round is scattered by one half of
-// the waves (a lane: one label, F_in / 8 consecutive slots), which also clears what it wrote two
-// steps earlier, so a clear and a later write of the same cell are ordered by that barrier.
-// Segments of labels are summed by the fixed-order reduction over segment partials; the result is
-// bit-reproducible and uses no atomics.
+//   - D += A B with A = dY[16 MT rows][32 labels] (staged in LDS) and B = the tile, F_s / 16 tiles
+//     of v_mfma_f32_16x16x32_bf16 per 16 rows: K = the step's labels, in natural order.
+// The scatter costs the same for every row of the workgroup, so more rows per workgroup (MT = 4)
+// halve it per row.  Three tiles rotate: step t + 1 is scattered and step t - 1 cleared while
+// step t is multiplied, with one barrier per step.  Each 32-label half of a 64-label round is
+// scattered by one half of the waves (a lane: one label, F_in / 8 consecutive slots), which also
+// clears what it wrote two steps earlier, so a clear and a later write of the same cell are
+// ordered by that barrier.  Segments of labels are summed by the fixed-order reduction over
+// segment partials; the result is bit-reproducible and uses no atomics.
 #include "common.hpp"
 
 namespace {
 
-constexpr int kDnWaves = 8;
-constexpr int kDnThreads = 64 * kDnWaves;
-constexpr int kDnStageRow = 160;                 // bytes per staged dY row: 64 labels + pad
-constexpr int kDnStage = 32 * kDnStageRow;       // one round's staged dY block [32 rows][64 labels]
+constexpr int kDnStageRow = 80;                  // bytes per staged dY row: 32 labels + pad
 
 // the [FR][32] bf16 weight tile: row f is 64 bytes, and its 16-byte chunk c (labels 8c .. 8c+7)
 // sits at chunk position c ^ ((f >> 2) mod 4), which spreads a step's scattered writes over all
 // 64 banks (the matrix-core operand reads, 16 whole rows at a time, stay conflict-free)
 __host__ __device__ constexpr int dn_tile_bytes(int fr) { return fr * 64; }
-__host__ __device__ constexpr int dn_lds(int fr) { return 3 * dn_tile_bytes(fr) + 2 * kDnStage + 64; }
+__host__ __device__ constexpr int dn_stage_bytes(int mt) { return 16 * mt * kDnStageRow; }   // one step's dY
+__host__ __device__ constexpr int dn_lds(int fr, int mt) { return 3 * dn_tile_bytes(fr) + 2 * dn_stage_bytes(mt) + 64; }
 
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
@@ -42,232 +41,320 @@ typedef __attribute__((address_space(3))) u32x2_t lds_u32x2_t;
 typedef __attribute__((address_space(3))) u32x4_t lds_u32x4_t;
 typedef __attribute__((address_space(3))) bf16x8_t lds_bf16x8_t;
 
-// NFT: 16-feature tiles per wave (wave w owns tiles w, w + 8, ...), so F_s <= 128 NFT.
-// TAIL2: L = 2 mod 4 (the last dY piece of a row holds two labels).
-template <int F_IN, int NFT, bool TAIL2>
-__global__ __launch_bounds__(kDnThreads) void k_bwd_x_dn(const int32_t *__restrict__ idx, const bf16_t *__restrict__ W,
-                                                         const bf16_t *__restrict__ dY, float *__restrict__ part, int B,
-                                                         int Bp, int F_s, int FR, int64_t L, int gshift, int nbt,
-                                                         int64_t lps) {
-    constexpr int E = F_IN / 8;                   // slots per lane and round
-    constexpr int NW = E / 2;                     // dwords of weights per lane and round
-    static_assert(E % 4 == 0, "whole 16-byte support loads");
-    extern __shared__ __align__(16) char dn[];    // 3 tiles, then [2] staged rounds, then a dummy cell
+// NWV: waves (8: two per SIMD; 4: one per SIMD, whose 512 registers then hold the accumulators of
+// 64 rows).  MT: 16-row tiles per workgroup.  NFT: 16-feature tiles per wave (wave w owns tiles
+// w, w + NWV, ...); the tiles have FR = 16 NWV NFT >= F_s rows.  TAILP: L is not a multiple of the
+// PL labels of a staged dY piece (the last piece of a row is then read dword by dword).
+template <int NWV, int MT, int F_IN, int NFT, bool TAILP>
+__global__ __attribute__((amdgpu_flat_work_group_size(64 * NWV, 64 * NWV), amdgpu_waves_per_eu(NWV / 4, NWV / 4)))
+void k_bwd_x_dn(const int32_t *__restrict__ idx, const bf16_t *__restrict__ W, const bf16_t *__restrict__ dY,
+                float *__restrict__ part, int B, int Bp, int F_s, int FR, int64_t L, int gshift, int nbt,
+                int64_t lps) {
+    constexpr int T = 64 * NWV;                   // threads
+    constexpr int RW = 16 * MT;                   // batch rows of the workgroup
+    constexpr int LPL = T / 32;                   // lanes per label of a step
+    constexpr int E = F_IN / LPL;                 // slots per lane and step
+    constexpr int NW = E / 2;                     // dwords of weights per lane and step
+    constexpr int PL = 16 * MT * 32 / T;          // labels per staged dY piece (2 or 8)
+    constexpr int PPR = 32 / PL;                  // pieces per row and step
+    constexpr int SB = dn_stage_bytes(MT);
+    constexpr int RSL = 4;                        // steps whose loads are in flight (ring slots)
+    constexpr int PER = 12;                       // unrolled period: multiple of RSL, 3 tiles, 2 parities
+    constexpr int NMF = MT * NFT;                 // products per wave and step
+    static_assert(E == 2 || E % 4 == 0, "support loads of 8 or 16 bytes");
+    static_assert(RW * PPR == T, "one dY piece per thread and step");
+    static_assert(PER % RSL == 0 && PER % 6 == 0, "ring period");
+    extern __shared__ __align__(16) char dn[];    // 3 tiles, then [2] staged steps, then a dummy cell
     const int w = blockIdx.x, xcd = w % kXcds, jj = w / kXcds;
     const int bt = jj % nbt;
     const int64_t seg = (int64_t)(jj / nbt) * kXcds + xcd;
-    const int b0 = bt * 32;
+    const int b0 = bt * RW;
     const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int l16 = lane & 15, q = lane >> 4;
-    const int NT = FR / 16;                       // feature tiles
     float *pp = part + (size_t)seg * F_s * Bp + b0;
     const int64_t l_begin = seg * lps;
     const int64_t l_end = l_begin + lps < L ? l_begin + lps : L;
     if (l_begin >= l_end) {   // empty segment: the partial is zero (workgroup-uniform)
-        for (int e = tid; e < F_s * 32; e += kDnThreads) pp[(size_t)(e >> 5) * Bp + (e & 31)] = 0.0f;
+        for (int e = tid; e < F_s * RW; e += T) pp[(size_t)(e / RW) * Bp + (e % RW)] = 0.0f;
         return;
     }
-    const int nr = (int)((l_end - l_begin + 63) / 64);   // rounds of 64 labels; 2 nr steps
+    const int n = (int)((l_end - l_begin + 31) / 32);   // steps of 32 labels
     const int TB = dn_tile_bytes(FR);
     const uint32_t lbase = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char *)dn;
     const uint32_t sbase = lbase + 3 * TB;        // staged dY
-    const uint32_t dummy = sbase + 2 * kDnStage;  // written by the first clear, never read
+    const uint32_t dummy = sbase + 2 * SB;        // written by the first clears, never read
 
-    for (int e = tid; e < 3 * TB / 16; e += kDnThreads)
-        *(lds_u32x4_t *)(uintptr_t)(lbase + 16 * e) = u32x4_t{0u, 0u, 0u, 0u};
+    for (int e = tid; e < 3 * TB / 16; e += T) *(lds_u32x4_t *)(uintptr_t)(lbase + 16 * e) = u32x4_t{0u, 0u, 0u, 0u};
 
     // ---- per-lane roles ----
-    // scatter: half h of the waves takes the round's labels 32 h .. 32 h + 31, i.e. step 2R + h;
-    // lane -> label 8 (wave mod 4) + lane / 8 of the step, slots E (lane mod 8) .. + E - 1
-    const int h = wave >> 2;
-    const int ls = 8 * (wave & 3) + (lane >> 3);  // label within its step
-    const int o = lane & 7;
+    // scatter: lane -> label ls of the step, slots E (tid mod LPL) .. + E - 1.  The labels of one
+    // wave should cover the four 4-byte label pairs of a chunk, which with random features spreads
+    // an instruction's 2-byte writes over all 64 banks: 8 lanes per label, 8 consecutive labels a
+    // wave; 16 lanes per label, labels 2k + j of the chunk (k = 0 .. 3) per wave
+    const int gl0 = tid / LPL;
+    const int ls = LPL == 8 ? gl0 : 8 * (gl0 >> 3) + 2 * (gl0 & 3) + ((gl0 >> 2) & 1);
+    const int o = tid % LPL;
     const uint32_t lpos = (uint32_t)(((ls >> 3) << 4) | ((ls & 7) << 1));   // chunk and label bits
     const Buf wseg(W + l_begin * F_IN, (uint32_t)((l_end - l_begin) * F_IN * 2));
     const int64_t g_begin = l_begin >> gshift;
     const Buf iseg(idx + g_begin * F_IN, (uint32_t)(((l_end >> gshift) - g_begin) * F_IN * 4));
-    // dY: lane -> row tid / 16, labels 4 (tid mod 16) .. + 3 of the round (8 bytes)
-    const int rows = B - b0 < 32 ? B - b0 : 32;
-    const int dr = tid >> 4, dp = tid & 15;
+    // dY: lane -> row tid / PPR, labels PL (tid mod PPR) .. + PL - 1 of the step
+    const int rows = B - b0 < RW ? B - b0 : RW;
+    const int dr = tid / PPR, dp = tid % PPR;
     const Buf dseg(dY + (int64_t)b0 * L, (uint32_t)((int64_t)rows * L * 2));
 
-    struct Round {
+    struct Slot {
         uint32_t wv[NW];   // W[l, E o .. E o + E - 1] (bf16 pairs)
         int32_t f[E];      // the same slots' features
-        uint2 y;           // dY piece
+        uint32_t y[PL / 2];
     };
-    Round rg[3];           // round R in slot R mod 3
-    auto load_round = [&](int R, Round &r) __attribute__((always_inline)) {
-        const int64_t lr = (int64_t)R * 64 + 32 * h + ls;     // label offset within the segment
+    Slot rg[RSL];          // step s in slot s mod RSL
+    auto load_step = [&](int st, Slot &r) __attribute__((always_inline)) {
+        const int64_t lr = (int64_t)st * 32 + ls;             // label offset within the segment
         const uint32_t wo = (uint32_t)(lr * F_IN * 2 + E * 2 * o);
-#pragma unroll
-        for (int i = 0; i < NW / 4; ++i) {
-            const uint4 x = wseg.ld16(wo + 16 * i);
-            r.wv[4 * i] = x.x;
-            r.wv[4 * i + 1] = x.y;
-            r.wv[4 * i + 2] = x.z;
-            r.wv[4 * i + 3] = x.w;
-        }
-        if constexpr (NW == 2) {
+        if constexpr (NW == 1) {
+            r.wv[0] = wseg.ld4(wo);
+        } else if constexpr (NW == 2) {
             const uint2 x = wseg.ld8(wo);
             r.wv[0] = x.x;
             r.wv[1] = x.y;
+        } else {
+#pragma unroll
+            for (int i = 0; i < NW / 4; ++i) {
+                const uint4 x = wseg.ld16(wo + 16 * i);
+                r.wv[4 * i] = x.x;
+                r.wv[4 * i + 1] = x.y;
+                r.wv[4 * i + 2] = x.z;
+                r.wv[4 * i + 3] = x.w;
+            }
         }
         const int64_t gl = ((l_begin + lr) >> gshift) - g_begin;
         const uint32_t io = (uint32_t)(gl * F_IN * 4 + E * 4 * o);
+        if constexpr (E == 2) {
+            const uint2 x = iseg.ld8(io);
+            r.f[0] = (int32_t)x.x;
+            r.f[1] = (int32_t)x.y;
+        } else {
 #pragma unroll
-        for (int i = 0; i < E / 4; ++i) {
-            const uint4 x = iseg.ld16(io + 16 * i);
-            r.f[4 * i] = (int32_t)x.x;
-            r.f[4 * i + 1] = (int32_t)x.y;
-            r.f[4 * i + 2] = (int32_t)x.z;
-            r.f[4 * i + 3] = (int32_t)x.w;
+            for (int i = 0; i < E / 4; ++i) {
+                const uint4 x = iseg.ld16(io + 16 * i);
+                r.f[4 * i] = (int32_t)x.x;
+                r.f[4 * i + 1] = (int32_t)x.y;
+                r.f[4 * i + 2] = (int32_t)x.z;
+                r.f[4 * i + 3] = (int32_t)x.w;
+            }
         }
-        // dY piece: 4 labels of row dr.  Segments start and end at multiples of 64 labels, except
-        // the layer's end, so with L even a piece is whole, past the end, or (L = 2 mod 4) the
-        // layer's last two labels, read as one dword so that nothing past the row is read
-        const int64_t lab = l_begin + (int64_t)R * 64 + 4 * dp;
+        // dY piece: PL labels of row dr.  Segments start and end at multiples of 64 labels, except
+        // the layer's end, so a piece is whole or past the end unless L is not a multiple of PL;
+        // then the layer's last piece of a row is read dword by dword (L is even), so that
+        // nothing past the row is read
+        const int64_t lab = l_begin + (int64_t)st * 32 + PL * dp;
         const int64_t nv = l_end - lab;
         const uint32_t yo = dr < rows && nv > 0 ? (uint32_t)(((int64_t)dr * L + lab) * 2) : kOob;
-        r.y = dseg.ld8(nv >= 4 ? yo : kOob);
-        if constexpr (TAIL2) r.y.x |= dseg.ld4(nv == 2 ? yo : kOob);
-    };
-    // scatter of a step's lane entries into tile buffer tb; the addresses are kept for the clear
-    uint32_t ca[E];
+        if constexpr (PL == 2) {
+            r.y[0] = dseg.ld4(yo);
+        } else if constexpr (!TAILP) {
+            const uint4 v = dseg.ld16(yo);
+            r.y[0] = v.x;
+            r.y[1] = v.y;
+            r.y[2] = v.z;
+            r.y[3] = v.w;
+        } else {
 #pragma unroll
-    for (int j = 0; j < E; ++j) ca[j] = dummy;
-    auto scatter = [&](const Round &r, int tb) __attribute__((always_inline)) {
+            for (int k = 0; k < PL / 2; ++k) r.y[k] = dseg.ld4(nv > 2 * k ? yo + 4 * k : kOob);
+        }
+    };
+    // a step's lane entries are written into tile buffer tb, and their addresses kept in ca[] so
+    // that the same lanes clear them two steps later
+    uint32_t ca[2][E];
+#pragma unroll
+    for (int j = 0; j < E; ++j) ca[0][j] = ca[1][j] = dummy;
+    auto scatter = [&](const Slot &r, int tb, uint32_t (&c)[E]) __attribute__((always_inline)) {
         const uint32_t base = lbase + (uint32_t)(tb * TB);
 #pragma unroll
         for (int j = 0; j < E; ++j) {
             const uint32_t f = (uint32_t)r.f[j];
-            ca[j] = base + (f << 6) + (lpos ^ ((f << 2) & 0x30u));
+            c[j] = base + (f << 6) + (lpos ^ ((f << 2) & 0x30u));
             const uint32_t v = r.wv[j >> 1];
-            *(lds_u16_t *)(uintptr_t)ca[j] = (uint16_t)((j & 1) ? (v >> 16) : v);
+            *(lds_u16_t *)(uintptr_t)c[j] = (uint16_t)((j & 1) ? (v >> 16) : v);
         }
     };
-    auto clear = [&]() __attribute__((always_inline)) {
+    auto clear = [&](const uint32_t (&c)[E]) __attribute__((always_inline)) {
 #pragma unroll
-        for (int j = 0; j < E; ++j) *(lds_u16_t *)(uintptr_t)ca[j] = (uint16_t)0;
+        for (int j = 0; j < E; ++j) *(lds_u16_t *)(uintptr_t)c[j] = (uint16_t)0;
     };
-    auto store_y = [&](const Round &r, int sb) __attribute__((always_inline)) {
-        *(lds_u32x2_t *)(uintptr_t)(sbase + (uint32_t)(sb * kDnStage + dr * kDnStageRow + 8 * dp)) = u32x2_t{r.y.x, r.y.y};
+    const uint32_t yst = sbase + (uint32_t)(dr * kDnStageRow + PL * 2 * dp);
+    auto store_y = [&](const Slot &r, int sb) __attribute__((always_inline)) {
+        if constexpr (PL == 2) *(__attribute__((address_space(3))) uint32_t *)(uintptr_t)(yst + sb * SB) = r.y[0];
+        else *(lds_u32x4_t *)(uintptr_t)(yst + sb * SB) = u32x4_t{r.y[0], r.y[1], r.y[2], r.y[3]};
     };
 
-    f32x4_t acc[2][NFT];
+    f32x4_t acc[MT][NFT];
 #pragma unroll
-    for (int hh = 0; hh < 2; ++hh)
+    for (int m = 0; m < MT; ++m)
 #pragma unroll
-        for (int i = 0; i < NFT; ++i) acc[hh][i] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
-    // operand addresses: A rows 16 hh + l16, labels 8q .. of the step; B rows 16 ft + l16, chunk q
+        for (int i = 0; i < NFT; ++i) acc[m][i] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+    // operand addresses: A rows 16 m + l16, labels 8q .. 8q + 7 of the step; B rows 16 ft + l16,
+    // chunk q
     const uint32_t aoff = sbase + (uint32_t)(l16 * kDnStageRow + 16 * q);
-    uint32_t boff[NFT];
-#pragma unroll
-    for (int i = 0; i < NFT; ++i) {
-        const int ft = wave + 8 * i < NT ? wave + 8 * i : NT - 1;   // past the last tile: a repeat, not stored
-        boff[i] = lbase + (uint32_t)(ft * 1024 + l16 * 64 + ((q ^ ((l16 >> 2) & 3)) << 4));
-    }
+    const uint32_t boff = lbase + (uint32_t)(wave * 1024 + l16 * 64 + ((q ^ ((l16 >> 2) & 3)) << 4));
 
-    load_round(0, rg[0]);
-    load_round(1, rg[1]);
+#pragma unroll
+    for (int i = 0; i < RSL; ++i) load_step(i, rg[i]);
     __syncthreads();                              // tiles zeroed
-    if (h == 0) scatter(rg[0], 0);                // step 0
+    scatter(rg[0], 0, ca[0]);                     // step 0
     store_y(rg[0], 0);
     __syncthreads();
 
-    // step t = t0 + U of the unrolled period (U = t mod 6): round t / 2 in ring slot U / 2, tile t mod 3
+    // step t = t0 + U of the unrolled period: its loads in slot U mod RSL, tile t mod 3, staged dY
+    // and clear addresses t mod 2
+    // Step t's operands are read into register set t mod 2 right after the barrier that completes
+    // its tile, and its products are split in two halves: the first runs beside the scatter of
+    // step t + 1, the second at the start of step t + 1, where it covers the latency of that step's
+    // operand reads (the matrix cores would otherwise wait at every barrier).
+    bf16x8_t oa[2][MT], ob[2][NFT];
+#pragma unroll
+    for (int m = 0; m < MT; ++m) oa[1][m] = bf16x8_t{};
+#pragma unroll
+    for (int i = 0; i < NFT; ++i) ob[1][i] = bf16x8_t{};   // "step -1": zero products
+    constexpr int H1 = NFT / 2;                   // feature tiles of the first half
+    static_assert(NFT % 2 == 0, "two halves");
     auto step = [&](int t, auto uc) __attribute__((always_inline)) {
         constexpr int U = decltype(uc)::value;
-        constexpr int PAR = U % 2, RS = U / 2, TBI = U % 3;
-        const int R = t >> 1;
-        if constexpr (PAR == 0) load_round(R + 2, rg[(RS + 2) % 3]);
-        __builtin_amdgcn_sched_barrier(0);
-        // step t's operands, all issued before anything else touches the LDS
-        const uint32_t ab = aoff + (uint32_t)((R & 1) * kDnStage + PAR * 64);
-        const bf16x8_t a0 = *(lds_bf16x8_t *)(uintptr_t)ab;
-        const bf16x8_t a1 = *(lds_bf16x8_t *)(uintptr_t)(ab + 16 * kDnStageRow);
-        bf16x8_t b[NFT];
+        constexpr int TBI = U % 3, PAR = U % 2;
+        constexpr int SN = (U + 1) % RSL;         // slot of step t + 1
+        const uint32_t ab = aoff + (uint32_t)(PAR * SB);
 #pragma unroll
-        for (int i = 0; i < NFT; ++i) b[i] = *(lds_bf16x8_t *)(uintptr_t)(boff[i] + TBI * TB);
-        __builtin_amdgcn_sched_barrier(0);
-        // scatter step t + 1 (its half), after clearing that half's step t - 1
-        if (h != PAR) {
-            clear();
-            scatter(rg[PAR == 0 ? RS : (RS + 1) % 3], (TBI + 1) % 3);
-        }
-        if constexpr (PAR == 1) store_y(rg[(RS + 1) % 3], (R + 1) & 1);
-        // products of step t
+        for (int m = 0; m < MT; ++m) oa[PAR][m] = *(lds_bf16x8_t *)(uintptr_t)(ab + 16 * m * kDnStageRow);
 #pragma unroll
-        for (int i = 0; i < NFT; ++i) {
-            acc[0][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, b[i], acc[0][i], 0, 0, 0);
-            acc[1][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, b[i], acc[1][i], 0, 0, 0);
-        }
+        for (int i = 0; i < NFT; ++i) ob[PAR][i] = *(lds_bf16x8_t *)(uintptr_t)(boff + TBI * TB + NWV * 1024 * i);
+        __builtin_amdgcn_sched_barrier(0);
+        // second half of step t - 1
+#pragma unroll
+        for (int i = H1; i < NFT; ++i)
+#pragma unroll
+            for (int m = 0; m < MT; ++m)
+                acc[m][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(oa[1 - PAR][m], ob[1 - PAR][i], acc[m][i], 0, 0, 0);
+        // step t + 1: clear step t - 1's cells (tile (t + 2) mod 3, read before the last barrier),
+        // write step t + 1's weights into tile (t + 1) mod 3 (cleared before the last barrier) and
+        // stage its dY
+        clear(ca[1 - PAR]);
+        scatter(rg[SN], (TBI + 1) % 3, ca[1 - PAR]);
+        store_y(rg[SN], 1 - PAR);
+        // first half of step t
+#pragma unroll
+        for (int i = 0; i < H1; ++i)
+#pragma unroll
+            for (int m = 0; m < MT; ++m)
+                acc[m][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(oa[PAR][m], ob[PAR][i], acc[m][i], 0, 0, 0);
+        // the products of step t - 1 beside the scatter's address arithmetic, then those of step t
+        // beside its LDS writes
+        static_for<MT * (NFT - H1)>([&](auto) __attribute__((always_inline)) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x002, 1, 0);
+        });
+        static_for<MT * H1>([&](auto) __attribute__((always_inline)) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x002, 1, 0);
+        });
+        __builtin_amdgcn_sched_barrier(0);
+        // the slot of step t is free (step t was written into its tile during the previous step):
+        // it takes step t + RSL
+        load_step(t + RSL, rg[U % RSL]);
+        __builtin_amdgcn_sched_barrier(0);
         __syncthreads();
     };
-    const int n = 2 * nr;
-    int t0 = 0;
-    for (; t0 + 6 <= n; t0 += 6)
-        static_for<6>([&](auto uc) __attribute__((always_inline)) { step(t0 + decltype(uc)::value, uc); });
-    static_for<6>([&](auto uc) __attribute__((always_inline)) {
-        if (t0 + decltype(uc)::value < n) step(t0 + decltype(uc)::value, uc);
-    });
+    // whole periods only (steps past the segment's end add zeros): a conditional step would give the
+    // accumulators a second path, and the compiler would then copy them between register files
+    for (int t0 = 0; t0 < n; t0 += PER)
+        static_for<PER>([&](auto uc) __attribute__((always_inline)) { step(t0 + decltype(uc)::value, uc); });
+    // second half of the last step (odd: the step count is a multiple of PER)
+#pragma unroll
+    for (int i = H1; i < NFT; ++i)
+#pragma unroll
+        for (int m = 0; m < MT; ++m)
+            acc[m][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(oa[1][m], ob[1][i], acc[m][i], 0, 0, 0);
 
     // partial dX^T of the segment: lane (l16, q) of tile ft holds feature 16 ft + l16, rows
-    // 16 hh + 4q .. + 3
+    // 16 m + 4q .. + 3
 #pragma unroll
     for (int i = 0; i < NFT; ++i) {
-        const int f = 16 * (wave + 8 * i) + l16;
-        if (wave + 8 * i < NT && f < F_s) {
+        const int f = 16 * (wave + NWV * i) + l16;
+        if (f < F_s) {
 #pragma unroll
-            for (int hh = 0; hh < 2; ++hh)
-                *reinterpret_cast<float4 *>(pp + (size_t)f * Bp + 16 * hh + 4 * q) =
-                    make_float4(acc[hh][i][0], acc[hh][i][1], acc[hh][i][2], acc[hh][i][3]);
+            for (int m = 0; m < MT; ++m)
+                *reinterpret_cast<float4 *>(pp + (size_t)f * Bp + 16 * m + 4 * q) =
+                    make_float4(acc[m][i][0], acc[m][i][1], acc[m][i][2], acc[m][i][3]);
         }
     }
 }
 
 struct DnGeom {
-    int nbt, FR, nft;
+    int nwv, mt, nbt, FR, nft;
     int64_t nseg, lps;
     size_t lds;
 };
 
+// Batches of more than 32 rows take 64-row workgroups of 4 waves (one per SIMD, so that the 64 x F_s
+// accumulators fit the registers), smaller ones, and 128-slot supports (whose lanes carry twice the
+// entries), 32-row workgroups of 8 waves.
 static DnGeom dn_geom(const haste::TailArgs &a) {
     DnGeom g;
-    g.nbt = (int)haste::cdiv(a.B, 32);
-    g.FR = (int)haste::round_up(a.F_s, 16);
-    const int per_wave = (int)haste::cdiv(g.FR / 16, kDnWaves);
-    g.nft = per_wave <= 2 ? 2 : per_wave <= 4 ? 4 : per_wave <= 6 ? 6 : per_wave <= 7 ? 7 : 0;
+    g.nwv = a.B > 32 && a.F_in <= 64 ? 4 : 8;
+    g.mt = g.nwv == 4 ? 4 : 2;
+    g.nbt = (int)haste::cdiv(a.B, 16 * g.mt);
+    const int per_wave = (int)haste::cdiv(haste::cdiv(a.F_s, 16), g.nwv);
+    // the instantiated tile counts per wave (0: F_s too wide)
+    static const int k4[] = {2, 4, 8, 12}, k8[] = {2, 4, 6};
+    g.nft = 0;
+    if (g.nwv == 4) {
+        for (int c : k4)
+            if (g.nft == 0 && per_wave <= c) g.nft = c;
+    } else {
+        for (int c : k8)
+            if (g.nft == 0 && per_wave <= c) g.nft = c;
+    }
+    g.FR = 16 * g.nwv * g.nft;
     // one workgroup per CU (the tiles take most of the LDS): segments x batch tiles ~ 256
     int64_t nseg = haste::round_up(haste::cdiv(kXcds * kCusPerXcd, g.nbt), kXcds);
     const int64_t max_seg = haste::round_up(haste::cdiv(a.L, 64), kXcds);
     g.nseg = nseg < max_seg ? nseg : max_seg;
     g.lps = haste::round_up(haste::cdiv(a.L, g.nseg), 64);
-    g.lds = (size_t)dn_lds(g.FR);
+    g.lds = (size_t)dn_lds(g.FR, g.mt);
     return g;
 }
 
-template <int F_IN, int NFT>
+template <int NWV, int MT, int F_IN, int NFT>
 static hipError_t launch_dn(const haste::TailArgs &a, const DnGeom &g, const int32_t *idx, const void *W,
                             const void *dY, float *part, hipStream_t s) {
-    auto kern = a.L % 4 == 2 ? k_bwd_x_dn<F_IN, NFT, true> : k_bwd_x_dn<F_IN, NFT, false>;
+    constexpr int PL = 16 * MT * 32 / (64 * NWV);
+    auto kern = a.L % PL != 0 ? k_bwd_x_dn<NWV, MT, F_IN, NFT, true> : k_bwd_x_dn<NWV, MT, F_IN, NFT, false>;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
                                        (int)g.lds);
     if (e != hipSuccess) return e;
     const int gshift = a.G == 1 ? 0 : a.G == 2 ? 1 : a.G == 4 ? 2 : 3;
-    hipLaunchKernelGGL(kern, dim3((unsigned)(g.nseg * g.nbt)), dim3(kDnThreads), g.lds, s, idx, (const bf16_t *)W,
-                       (const bf16_t *)dY, part, (int)a.B, g.nbt * 32, (int)a.F_s, g.FR, a.L, gshift, g.nbt, g.lps);
+    hipLaunchKernelGGL(kern, dim3((unsigned)(g.nseg * g.nbt)), dim3(64 * NWV), g.lds, s, idx, (const bf16_t *)W,
+                       (const bf16_t *)dY, part, (int)a.B, g.nbt * 16 * MT, (int)a.F_s, g.FR, a.L, gshift, g.nbt, g.lps);
     return hipGetLastError();
 }
 
 template <int F_IN>
 static hipError_t dn_f(const haste::TailArgs &a, const DnGeom &g, const int32_t *idx, const void *W, const void *dY,
                        float *part, hipStream_t s) {
-    switch (g.nft) {
-        case 2: return launch_dn<F_IN, 2>(a, g, idx, W, dY, part, s);
-        case 4: return launch_dn<F_IN, 4>(a, g, idx, W, dY, part, s);
-        case 6: return launch_dn<F_IN, 6>(a, g, idx, W, dY, part, s);
-        case 7: return launch_dn<F_IN, 7>(a, g, idx, W, dY, part, s);
+    if (g.nwv == 4) {
+        switch (g.nft) {
+            case 2: return launch_dn<4, 4, F_IN, 2>(a, g, idx, W, dY, part, s);
+            case 4: return launch_dn<4, 4, F_IN, 4>(a, g, idx, W, dY, part, s);
+            case 8: return launch_dn<4, 4, F_IN, 8>(a, g, idx, W, dY, part, s);
+            case 12: return launch_dn<4, 4, F_IN, 12>(a, g, idx, W, dY, part, s);
+        }
+    } else {
+        switch (g.nft) {
+            case 2: return launch_dn<8, 2, F_IN, 2>(a, g, idx, W, dY, part, s);
+            case 4: return launch_dn<8, 2, F_IN, 4>(a, g, idx, W, dY, part, s);
+            case 6: return launch_dn<8, 2, F_IN, 6>(a, g, idx, W, dY, part, s);
+        }
     }
     return hipErrorInvalidValue;
 }
@@ -276,20 +363,20 @@ static hipError_t dn_f(const haste::TailArgs &a, const DnGeom &g, const int32_t 
 
 namespace haste {
 
-// bf16, G in {1, 2, 4, 8}, F_in in {32, 64, 128}; F_s up to the three [F_s][32] tiles the LDS holds
-// (800); dY rows dword-aligned (L even) and 32 of them within the 31-bit range of a buffer offset;
+// bf16, G in {1, 2, 4, 8}, F_in in {32, 64, 128}; F_s up to 768 (three [768][32] tiles fill the
+// LDS); dY rows dword-aligned (L even) and a workgroup's rows within the 31-bit range of a buffer offset;
 // a segment's weight and support offsets within that range too.
 bool bwd_x_dn_supported(const TailArgs &a) {
     if (a.dtype != HASTE_DTYPE_BF16 || !(a.G == 1 || a.G == 2 || a.G == 4 || a.G == 8)) return false;
     if (!(a.F_in == 32 || a.F_in == 64 || a.F_in == 128)) return false;
-    if (a.F_s <= 0 || a.L % 2 != 0 || a.L * 32 * 2 >= ((int64_t)1 << 31)) return false;
+    if (a.F_s <= 0 || a.L % 2 != 0 || a.L * 64 * 2 >= ((int64_t)1 << 31)) return false;
     const DnGeom g = dn_geom(a);
-    return g.nft != 0 && g.lds <= 160 * 1024 && (g.lps + 256) * a.F_in * 4 < ((int64_t)1 << 31);
+    return g.nft != 0 && g.lds <= 160 * 1024 && (g.lps + 1024) * a.F_in * 4 < ((int64_t)1 << 31);
 }
 
 size_t bwd_x_dn_ws(const TailArgs &a) {
     const DnGeom g = dn_geom(a);
-    return (size_t)round_up(g.nseg * a.F_s * (g.nbt * 32) * 4, 256);
+    return (size_t)round_up(g.nseg * a.F_s * (g.nbt * 16 * g.mt) * 4, 256);
 }
 
 hipError_t bwd_x_dn(const TailArgs &a, const int32_t *idx, const void *W, const void *dY, float *dX, int beta, void *ws,
@@ -304,7 +391,7 @@ hipError_t bwd_x_dn(const TailArgs &a, const int32_t *idx, const void *W, const 
         default: return hipErrorInvalidValue;
     }
     if (e != hipSuccess) return e;
-    return reduce_fmajor(part, (int)g.nseg, g.nbt * 32, a.B, a.F_s, dX, beta, s);
+    return reduce_fmajor(part, (int)g.nseg, g.nbt * 16 * g.mt, a.B, a.F_s, dX, beta, s);
 }
 
 }  // namespace haste
