@@ -75,11 +75,13 @@ namespace {
 // the forward kernel for a layer: small groups (G = 1, 2, 4, 8) on their own matrix-core kernel,
 // larger ones on the gather-once kernel, the rest (fp32, other G) on the vector ALUs
 bool fwd_kernel_exists(const haste::TailArgs &a) {
-    return haste::fwd_sg_supported(a) || haste::fwd_mfma_supported(a) || haste::valu_supported(a);
+    return haste::fwd_dn_supported(a) || haste::fwd_sg_supported(a) || haste::fwd_mfma_supported(a) ||
+           haste::valu_supported(a);
 }
 
 hipError_t fwd_any(const haste::TailArgs &a, const void *X, const int32_t *idx, const void *W, const float *bias,
                    void *Y, hipStream_t s) {
+    if (haste::fwd_dn_supported(a)) return haste::fwd_dn(a, X, idx, W, bias, Y, s);
     if (haste::fwd_sg_supported(a)) return haste::fwd_sg(a, X, idx, W, bias, Y, s);
     if (haste::fwd_mfma_supported(a)) return haste::fwd_mfma(a, X, idx, W, bias, Y, s);
     return haste::fwd_valu(a, X, idx, W, bias, Y, s);

@@ -217,6 +217,11 @@ bool bwd_x_dn_supported(const TailArgs &a);
 size_t bwd_x_dn_ws(const TailArgs &a);
 hipError_t bwd_x_dn(const TailArgs &a, const int32_t *idx, const void *W, const void *dY, float *dX, int beta, void *ws,
                     hipStream_t s);
+// forward for groups of 1 or 2 labels (F_s <= 768) as a dense product over each 32-label step's
+// weights scattered into an LDS tile
+bool fwd_dn_supported(const TailArgs &a);
+hipError_t fwd_dn(const TailArgs &a, const void *X, const int32_t *idx, const void *W, const float *bias, void *Y,
+                  hipStream_t s);
 bool bwd_w_mfma_supported(const TailArgs &a);
 size_t bwd_w_mfma_ws(const TailArgs &a);
 hipError_t bwd_w_mfma(const TailArgs &a, const void *X, const int32_t *idx, const void *dY, float *dW,

@@ -290,6 +290,216 @@ void k_bwd_x_dn(const int32_t *__restrict__ idx, const bf16_t *__restrict__ W, c
     }
 }
 
+// ---------------------------------------------------------------------------------------------
+// Forward for small groups as a dense product over scattered weight tiles (bf16):
+//   Y[rows, l] = bias[l] + sum over f of X[rows, f] W'[l, f]   (Section 3.2, the forward product;
+//   W' as above, here stored label-major).
+// The gathers of the small-group forward cost one LDS read per (label's group, slot, row); here a
+// step of 32 labels costs one 2-byte write per (label, slot), independent of the rows.  A
+// workgroup of 8 waves owns 32 batch rows and a segment of labels; wave (mt, nt, kh) keeps X for
+// rows 16 mt .. 16 mt + 15 and the features of K half kh in its registers for the whole segment.
+// Per step:
+//   - the step's weights are scattered into a zeroed [32 labels][FR] bf16 tile and cleared after
+//     use (FR = F_s rounded up to 128);
+//   - wave (mt, nt, kh) forms D[labels 16 nt ..][rows 16 mt ..] over its K half with
+//     v_mfma_f32_16x16x32_bf16: A = 16-byte reads of the tile's label rows, B = X from registers;
+//   - in the next step the two K halves are summed through LDS (in fixed order), the bias is added,
+//     and the bf16 result goes into a staged [32 rows][64 labels] block that leaves as 128-byte row
+//     runs every second step.
+// Two tiles alternate, with two barriers per step: one between a tile's clear and its next scatter,
+// one between the scatter and the products that read it.
+// ---------------------------------------------------------------------------------------------
+constexpr int kFdStageRow = 144;                 // bytes per staged output row: 64 labels + pad
+constexpr int kFdStage = 32 * kFdStageRow;
+constexpr int kFdRed = 8 * 1024;                 // one step's partial sums: 8 waves x 64 lanes x 16 B
+__host__ __device__ constexpr int fd_lds(int fr) { return 2 * 64 * fr + 2 * kFdRed + 2 * kFdStage + 64; }
+
+// KCH: 32-feature K chunks per half (FR = 64 KCH).
+template <int KCH, int F_IN, bool HAS_BIAS>
+__global__ __launch_bounds__(512) void k_fwd_dn(const bf16_t *__restrict__ X, const int32_t *__restrict__ idx,
+                                                const bf16_t *__restrict__ W, const float *__restrict__ bias,
+                                                bf16_t *__restrict__ Y, int B, int F_s, int64_t L, int gshift, int nbt,
+                                                int64_t lps) {
+    constexpr int FR = 64 * KCH;                  // tile columns (features)
+    constexpr int TB = 64 * FR;                   // tile bytes: [32 labels][FR] bf16
+    constexpr int LPL = 16;                       // lanes per label of a step
+    constexpr int E = F_IN / LPL;                 // slots per lane and step
+    constexpr int NW = E / 2;                     // dwords of weights per lane and step
+    constexpr int RSL = 4;                        // steps whose loads are in flight (ring slots)
+    constexpr int PER = 4;                        // unrolled period: RSL, 2 tiles, 2 staged blocks
+    static_assert(FR % 128 == 0, "a tile row is whole 16-chunk blocks");
+    static_assert(E == 2 || E % 4 == 0, "support loads of 8 or 16 bytes");
+    extern __shared__ __align__(16) char fd[];    // 2 tiles, [2] partial sums, [2] staged blocks, dummy
+    const int w = blockIdx.x, xcd = w % kXcds, jj = w / kXcds;
+    const int bt = jj % nbt;
+    const int64_t seg = (int64_t)(jj / nbt) * kXcds + xcd;
+    const int b0 = bt * 32;
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int l16 = lane & 15, q = lane >> 4;
+    const int64_t l_begin = seg * lps;
+    const int64_t l_end = l_begin + lps < L ? l_begin + lps : L;
+    if (l_begin >= l_end) return;                 // workgroup-uniform
+    const int n = (int)(((l_end - l_begin + 31) / 32 + PER - 1) / PER * PER);   // steps, whole periods
+    const uint32_t lbase = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char *)fd;
+    const uint32_t rbase = lbase + 2 * TB;        // partial sums
+    const uint32_t sbase = rbase + 2 * kFdRed;    // staged output
+    const uint32_t dummy = sbase + 2 * kFdStage;  // written by the first clear, never read
+    for (int e = tid; e < 2 * TB / 16; e += 512) *(lds_u32x4_t *)(uintptr_t)(lbase + 16 * e) = u32x4_t{0u, 0u, 0u, 0u};
+
+    // ---- X for this wave's rows and K half, in registers for the whole segment ----
+    const int mt = wave & 1, nt = (wave >> 1) & 1, kh = wave >> 2;
+    const int rows = B - b0 < 32 ? B - b0 : 32;
+    bf16x8_t xa[KCH];
+    {
+        const Buf xb(X + (int64_t)b0 * F_s, (uint32_t)((int64_t)rows * F_s * 2));
+        const int r = 16 * mt + l16;
+#pragma unroll
+        for (int c = 0; c < KCH; ++c) {
+            const int f0 = 32 * (kh * KCH + c) + 8 * q;
+            const uint32_t off = r < rows && f0 < F_s ? (uint32_t)(((int64_t)r * F_s + f0) * 2) : kOob;
+            xa[c] = as_bf16x8(xb.ld16(off));
+        }
+    }
+
+    // ---- scatter roles (as in backward-feature: 16 lanes per label, 4 labels of distinct 4-byte
+    // pairs per wave) ----
+    const int gl0 = tid / LPL;
+    const int ls = 8 * (gl0 >> 3) + 2 * (gl0 & 3) + ((gl0 >> 2) & 1);
+    const int o = tid % LPL;
+    const uint32_t lrow = (uint32_t)(ls * FR * 2);
+    const uint32_t lsw = (uint32_t)(ls & 15);
+    const Buf wseg(W + l_begin * F_IN, (uint32_t)((l_end - l_begin) * F_IN * 2));
+    const int64_t g_begin = l_begin >> gshift;
+    const Buf iseg(idx + g_begin * F_IN, (uint32_t)(((l_end >> gshift) - g_begin) * F_IN * 4));
+    struct Slot {
+        uint32_t wv[NW];
+        int32_t f[E];
+    };
+    Slot rg[RSL];
+    auto load_step = [&](int st, Slot &r) __attribute__((always_inline)) {
+        const int64_t lr = (int64_t)st * 32 + ls;
+        const uint32_t wo = (uint32_t)(lr * F_IN * 2 + E * 2 * o);
+        if constexpr (NW == 1) {
+            r.wv[0] = wseg.ld4(wo);
+        } else if constexpr (NW == 2) {
+            const uint2 x = wseg.ld8(wo);
+            r.wv[0] = x.x;
+            r.wv[1] = x.y;
+        } else {
+#pragma unroll
+            for (int i = 0; i < NW / 4; ++i) {
+                const uint4 x = wseg.ld16(wo + 16 * i);
+                r.wv[4 * i] = x.x;
+                r.wv[4 * i + 1] = x.y;
+                r.wv[4 * i + 2] = x.z;
+                r.wv[4 * i + 3] = x.w;
+            }
+        }
+        const int64_t gl = ((l_begin + lr) >> gshift) - g_begin;
+        const uint32_t io = (uint32_t)(gl * F_IN * 4 + E * 4 * o);
+        if constexpr (E == 2) {
+            const uint2 x = iseg.ld8(io);
+            r.f[0] = (int32_t)x.x;
+            r.f[1] = (int32_t)x.y;
+        } else {
+#pragma unroll
+            for (int i = 0; i < E / 4; ++i) {
+                const uint4 x = iseg.ld16(io + 16 * i);
+                r.f[4 * i] = (int32_t)x.x;
+                r.f[4 * i + 1] = (int32_t)x.y;
+                r.f[4 * i + 2] = (int32_t)x.z;
+                r.f[4 * i + 3] = (int32_t)x.w;
+            }
+        }
+    };
+    // tile row ls: the 16-byte chunk k (features 8k .. 8k + 7) at chunk position k ^ (ls mod 16)
+    uint32_t ca[2][E];
+#pragma unroll
+    for (int j = 0; j < E; ++j) ca[0][j] = ca[1][j] = dummy;
+    auto scatter = [&](const Slot &r, int tb, uint32_t (&c)[E]) __attribute__((always_inline)) {
+        const uint32_t base = lbase + (uint32_t)(tb * TB) + lrow;
+#pragma unroll
+        for (int j = 0; j < E; ++j) {
+            const uint32_t f = (uint32_t)r.f[j];
+            c[j] = base + ((((f >> 3) ^ lsw) << 4) | ((f & 7u) << 1));
+            const uint32_t v = r.wv[j >> 1];
+            *(lds_u16_t *)(uintptr_t)c[j] = (uint16_t)((j & 1) ? (v >> 16) : v);
+        }
+    };
+    auto clear = [&](const uint32_t (&c)[E]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int j = 0; j < E; ++j) *(lds_u16_t *)(uintptr_t)c[j] = (uint16_t)0;
+    };
+    // A operand: tile row 16 nt + l16, chunk 4 (kh KCH + c) + q at position chunk ^ l16
+    const uint32_t arow = lbase + (uint32_t)((16 * nt + l16) * FR * 2);
+    const uint32_t ql = (uint32_t)(q ^ l16);
+    // partial sums: wave w's lane l at w 1024 + 16 l; combine roles (threads < 256): row cr, label
+    // quad cq of the step
+    const uint32_t rslot = rbase + (uint32_t)(wave * 1024 + lane * 16);
+    const int cr = (tid >> 3) & 31, cq = tid & 7;
+    const uint32_t rsrc = rbase + (uint32_t)(((cr >> 4) + 2 * (cq >> 2)) * 1024 + (16 * (cq & 3) + (cr & 15)) * 16);
+    auto combine = [&](int st, int par) __attribute__((always_inline)) {   // step st, partials par
+        if (tid < 256) {
+            const f32x4_t p0 = *(__attribute__((address_space(3))) f32x4_t *)(uintptr_t)(rsrc + par * kFdRed);
+            const f32x4_t p1 = *(__attribute__((address_space(3))) f32x4_t *)(uintptr_t)(rsrc + par * kFdRed + 4 * 1024);
+            f32x4_t v = p0 + p1;
+            if constexpr (HAS_BIAS) {
+                const int64_t lab = l_begin + (int64_t)st * 32 + 4 * cq;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) v[e] += lab + e < l_end ? bias[lab + e] : 0.0f;
+            }
+            const uint32_t sb = sbase + (uint32_t)(((st >> 1) & 1) * kFdStage + cr * kFdStageRow + (st & 1) * 64 + 8 * cq);
+            *(lds_u32x2_t *)(uintptr_t)sb = u32x2_t{pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3])};
+        }
+    };
+    // flush of steps 2k, 2k + 1: thread -> row tid / 16, labels 4 (tid mod 16) .. + 3 (8 bytes)
+    const int fr_ = tid >> 4, fp = tid & 15;
+    auto flush = [&](int k) __attribute__((always_inline)) {
+        const int64_t lab = l_begin + (int64_t)k * 64 + 4 * fp;
+        const int64_t nv = l_end - lab;
+        if (fr_ < rows && nv > 0) {
+            const u32x2_t v =
+                *(lds_u32x2_t *)(uintptr_t)(sbase + (uint32_t)((k & 1) * kFdStage + fr_ * kFdStageRow + 8 * fp));
+            bf16_t *dst = Y + (int64_t)(b0 + fr_) * L + lab;
+            if (nv >= 4) *reinterpret_cast<uint2 *>(dst) = make_uint2(v[0], v[1]);
+            else *reinterpret_cast<uint32_t *>(dst) = v[0];   // L even: the row's last two labels
+        }
+    };
+
+#pragma unroll
+    for (int i = 0; i < RSL; ++i) load_step(i, rg[i]);
+    __syncthreads();                              // tiles zeroed
+    scatter(rg[0], 0, ca[0]);                     // step 0
+    __syncthreads();
+
+    auto step = [&](int t, auto uc) __attribute__((always_inline)) {
+        constexpr int U = decltype(uc)::value;
+        constexpr int PAR = U % 2;
+        bf16x8_t ob[KCH];
+#pragma unroll
+        for (int c = 0; c < KCH; ++c)
+            ob[c] = *(lds_bf16x8_t *)(uintptr_t)(arow + (uint32_t)(PAR * TB) +
+                                                 ((((uint32_t)(4 * (kh * KCH + c))) ^ ql) << 4));
+        __builtin_amdgcn_sched_barrier(0);
+        clear(ca[1 - PAR]);                       // step t - 1's cells (its tile was read before the last barrier)
+        f32x4_t d = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int c = 0; c < KCH; ++c) d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ob[c], xa[c], d, 0, 0, 0);
+        *(__attribute__((address_space(3))) f32x4_t *)(uintptr_t)(rslot + PAR * kFdRed) = d;
+        if (t >= 1) combine(t - 1, 1 - PAR);
+        if (PAR == 1 && t >= 3) flush((t - 3) >> 1);
+        __syncthreads();                          // clears done: the tile takes step t + 1
+        scatter(rg[(U + 1) % RSL], 1 - PAR, ca[1 - PAR]);
+        load_step(t + RSL, rg[U % RSL]);          // step t's slot is free (scattered in the last step)
+        __syncthreads();
+    };
+    for (int t0 = 0; t0 < n; t0 += PER)
+        static_for<PER>([&](auto uc) __attribute__((always_inline)) { step(t0 + decltype(uc)::value, uc); });
+    combine(n - 1, (n - 1) & 1);
+    __syncthreads();
+    flush((n - 2) >> 1);
+}
+
 struct DnGeom {
     int nwv, mt, nbt, FR, nft;
     int64_t nseg, lps;
@@ -359,6 +569,53 @@ static hipError_t dn_f(const haste::TailArgs &a, const DnGeom &g, const int32_t 
     return hipErrorInvalidValue;
 }
 
+
+struct FdGeom {
+    int nbt, kch;
+    int64_t nseg, lps;
+    size_t lds;
+};
+
+static FdGeom fd_geom(const haste::TailArgs &a) {
+    FdGeom g;
+    g.nbt = (int)haste::cdiv(a.B, 32);
+    const int fr = (int)haste::round_up(a.F_s, 128);
+    g.kch = fr / 64;
+    int64_t nseg = haste::round_up(haste::cdiv(kXcds * kCusPerXcd, g.nbt), kXcds);
+    const int64_t max_seg = haste::round_up(haste::cdiv(a.L, 64), kXcds);
+    g.nseg = nseg < max_seg ? nseg : max_seg;
+    g.lps = haste::round_up(haste::cdiv(a.L, g.nseg), 64);
+    g.lds = (size_t)fd_lds(fr);
+    return g;
+}
+
+template <int KCH, int F_IN>
+static hipError_t launch_fd(const haste::TailArgs &a, const FdGeom &g, const void *X, const int32_t *idx, const void *W,
+                            const float *bias, void *Y, hipStream_t s) {
+    auto kern = bias ? k_fwd_dn<KCH, F_IN, true> : k_fwd_dn<KCH, F_IN, false>;
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       (int)g.lds);
+    if (e != hipSuccess) return e;
+    const int gshift = a.G == 1 ? 0 : a.G == 2 ? 1 : a.G == 4 ? 2 : 3;
+    hipLaunchKernelGGL(kern, dim3((unsigned)(g.nseg * g.nbt)), dim3(512), g.lds, s, (const bf16_t *)X, idx,
+                       (const bf16_t *)W, bias, (bf16_t *)Y, (int)a.B, (int)a.F_s, a.L, gshift, g.nbt, g.lps);
+    return hipGetLastError();
+}
+
+template <int F_IN>
+static hipError_t fd_f(const haste::TailArgs &a, const FdGeom &g, const void *X, const int32_t *idx, const void *W,
+                       const float *bias, void *Y, hipStream_t s) {
+    switch (g.kch) {
+        case 2: return launch_fd<2, F_IN>(a, g, X, idx, W, bias, Y, s);
+        case 4: return launch_fd<4, F_IN>(a, g, X, idx, W, bias, Y, s);
+        case 6: return launch_fd<6, F_IN>(a, g, X, idx, W, bias, Y, s);
+        case 8: return launch_fd<8, F_IN>(a, g, X, idx, W, bias, Y, s);
+        case 10: return launch_fd<10, F_IN>(a, g, X, idx, W, bias, Y, s);
+        case 12: return launch_fd<12, F_IN>(a, g, X, idx, W, bias, Y, s);
+    }
+    return hipErrorInvalidValue;
+}
+
 }  // namespace
 
 namespace haste {
@@ -392,6 +649,28 @@ hipError_t bwd_x_dn(const TailArgs &a, const int32_t *idx, const void *W, const 
     }
     if (e != hipSuccess) return e;
     return reduce_fmajor(part, (int)g.nseg, g.nbt * 16 * g.mt, a.B, a.F_s, dX, beta, s);
+}
+
+// forward: bf16, G in {1, 2} (larger groups share their gathers, which the small-group kernel then
+// does more cheaply), F_in in {32, 64, 128}, F_s a multiple of 8 up to 768 (X rows read 16 bytes at
+// a time; two [32][768] tiles beside the staging), L even (the output leaves in label pairs).
+bool fwd_dn_supported(const TailArgs &a) {
+    if (a.dtype != HASTE_DTYPE_BF16 || !(a.G == 1 || a.G == 2)) return false;
+    if (!(a.F_in == 32 || a.F_in == 64 || a.F_in == 128)) return false;
+    if (a.F_s <= 0 || a.F_s % 8 != 0 || a.F_s > 768 || a.L % 2 != 0) return false;
+    const FdGeom g = fd_geom(a);
+    return g.lds <= 160 * 1024 && (g.lps + 1024) * a.F_in * 4 < ((int64_t)1 << 31);
+}
+
+hipError_t fwd_dn(const TailArgs &a, const void *X, const int32_t *idx, const void *W, const float *bias, void *Y,
+                  hipStream_t s) {
+    const FdGeom g = fd_geom(a);
+    switch (a.F_in) {
+        case 32: return fd_f<32>(a, g, X, idx, W, bias, Y, s);
+        case 64: return fd_f<64>(a, g, X, idx, W, bias, Y, s);
+        case 128: return fd_f<128>(a, g, X, idx, W, bias, Y, s);
+    }
+    return hipErrorInvalidValue;
 }
 
 }  // namespace haste
