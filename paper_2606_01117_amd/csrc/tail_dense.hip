@@ -303,16 +303,16 @@ void k_bwd_x_dn(const int32_t *__restrict__ idx, const bf16_t *__restrict__ W, c
 //     use (FR = F_s rounded up to 128);
 //   - wave (mt, nt, kh) forms D[labels 16 nt ..][rows 16 mt ..] over its K half with
 //     v_mfma_f32_16x16x32_bf16: A = 16-byte reads of the tile's label rows, B = X from registers;
-//   - in the next step the two K halves are summed through LDS (in fixed order), the bias is added,
-//     and the bf16 result goes into a staged [32 rows][64 labels] block that leaves as 128-byte row
-//     runs every second step.
-// Two tiles alternate, with two barriers per step: one between a tile's clear and its next scatter,
-// one between the scatter and the products that read it.
+//   - in the next step the K-half-1 wave's partial sums reach its K-half-0 partner through LDS, which
+//     adds them to its own (in fixed order) with the bias and puts the bf16 result into a staged
+//     [32 rows][64 labels] block that leaves as 128-byte row runs every second step.
+// Three tiles rotate (the step's, the next one being written, the previous one being cleared), with
+// one barrier per step; at F_s = 768 they and the staging fill the 160 KB of LDS.
 // ---------------------------------------------------------------------------------------------
-constexpr int kFdStageRow = 144;                 // bytes per staged output row: 64 labels + pad
-constexpr int kFdStage = 32 * kFdStageRow;
-constexpr int kFdRed = 8 * 1024;                 // one step's partial sums: 8 waves x 64 lanes x 16 B
-__host__ __device__ constexpr int fd_lds(int fr) { return 2 * 64 * fr + 2 * kFdRed + 2 * kFdStage + 64; }
+// staged output: [32 rows][64 labels] bf16, 8-byte piece p of row r at piece position p ^ (r mod 16)
+constexpr int kFdStage = 32 * 128;
+constexpr int kFdRed = 4 * 1024;                 // one step's K-half-1 partial sums: 4 waves x 64 lanes x 16 B
+__host__ __device__ constexpr int fd_lds(int fr) { return 3 * 64 * fr + 2 * kFdRed + 2 * kFdStage; }
 
 // KCH: 32-feature K chunks per half (FR = 64 KCH).
 template <int KCH, int F_IN, bool HAS_BIAS>
@@ -326,10 +326,10 @@ __global__ __launch_bounds__(512) void k_fwd_dn(const bf16_t *__restrict__ X, co
     constexpr int E = F_IN / LPL;                 // slots per lane and step
     constexpr int NW = E / 2;                     // dwords of weights per lane and step
     constexpr int RSL = 4;                        // steps whose loads are in flight (ring slots)
-    constexpr int PER = 4;                        // unrolled period: RSL, 2 tiles, 2 staged blocks
+    constexpr int PER = 12;                       // unrolled period: RSL, 3 tiles, 2 staged blocks
     static_assert(FR % 128 == 0, "a tile row is whole 16-chunk blocks");
     static_assert(E == 2 || E % 4 == 0, "support loads of 8 or 16 bytes");
-    extern __shared__ __align__(16) char fd[];    // 2 tiles, [2] partial sums, [2] staged blocks, dummy
+    extern __shared__ __align__(16) char fd[];    // 3 tiles, [2] partial sums, [2] staged blocks
     const int w = blockIdx.x, xcd = w % kXcds, jj = w / kXcds;
     const int bt = jj % nbt;
     const int64_t seg = (int64_t)(jj / nbt) * kXcds + xcd;
@@ -341,10 +341,11 @@ __global__ __launch_bounds__(512) void k_fwd_dn(const bf16_t *__restrict__ X, co
     if (l_begin >= l_end) return;                 // workgroup-uniform
     const int n = (int)(((l_end - l_begin + 31) / 32 + PER - 1) / PER * PER);   // steps, whole periods
     const uint32_t lbase = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char *)fd;
-    const uint32_t rbase = lbase + 2 * TB;        // partial sums
+    const uint32_t rbase = lbase + 3 * TB;        // partial sums
     const uint32_t sbase = rbase + 2 * kFdRed;    // staged output
-    const uint32_t dummy = sbase + 2 * kFdStage;  // written by the first clear, never read
-    for (int e = tid; e < 2 * TB / 16; e += 512) *(lds_u32x4_t *)(uintptr_t)(lbase + 16 * e) = u32x4_t{0u, 0u, 0u, 0u};
+    // the first clear writes here: staged block 1, which is first written in step 3
+    const uint32_t dummy = sbase + kFdStage;
+    for (int e = tid; e < 3 * TB / 16; e += 512) *(lds_u32x4_t *)(uintptr_t)(lbase + 16 * e) = u32x4_t{0u, 0u, 0u, 0u};
 
     // ---- X for this wave's rows and K half, in registers for the whole segment ----
     const int mt = wave & 1, nt = (wave >> 1) & 1, kh = wave >> 2;
@@ -433,24 +434,22 @@ __global__ __launch_bounds__(512) void k_fwd_dn(const bf16_t *__restrict__ X, co
     // A operand: tile row 16 nt + l16, chunk 4 (kh KCH + c) + q at position chunk ^ l16
     const uint32_t arow = lbase + (uint32_t)((16 * nt + l16) * FR * 2);
     const uint32_t ql = (uint32_t)(q ^ l16);
-    // partial sums: wave w's lane l at w 1024 + 16 l; combine roles (threads < 256): row cr, label
-    // quad cq of the step
-    const uint32_t rslot = rbase + (uint32_t)(wave * 1024 + lane * 16);
-    const int cr = (tid >> 3) & 31, cq = tid & 7;
-    const uint32_t rsrc = rbase + (uint32_t)(((cr >> 4) + 2 * (cq >> 2)) * 1024 + (16 * (cq & 3) + (cr & 15)) * 16);
-    auto combine = [&](int st, int par) __attribute__((always_inline)) {   // step st, partials par
-        if (tid < 256) {
-            const f32x4_t p0 = *(__attribute__((address_space(3))) f32x4_t *)(uintptr_t)(rsrc + par * kFdRed);
-            const f32x4_t p1 = *(__attribute__((address_space(3))) f32x4_t *)(uintptr_t)(rsrc + par * kFdRed + 4 * 1024);
-            f32x4_t v = p0 + p1;
-            if constexpr (HAS_BIAS) {
-                const int64_t lab = l_begin + (int64_t)st * 32 + 4 * cq;
+    // K-half-1 partial sums: wave 4 + j's lane l at j 1024 + 16 l, read by its partner wave j
+    const uint32_t rslot = rbase + (uint32_t)((wave & 3) * 1024 + lane * 16);
+    f32x4_t dprev = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};   // a K-half-0 wave's partial sums of the last step
+    // the partner pair's result of step st: rows 16 mt + l16, labels 16 nt + 4q .. + 3 of the step
+    const int srow = 16 * mt + l16;
+    auto combine = [&](int st, int par) __attribute__((always_inline)) {
+        const f32x4_t p1 = *(__attribute__((address_space(3))) f32x4_t *)(uintptr_t)(rslot + par * kFdRed);
+        f32x4_t v = dprev + p1;
+        if constexpr (HAS_BIAS) {
+            const int64_t lab = l_begin + (int64_t)st * 32 + 16 * nt + 4 * q;
 #pragma unroll
-                for (int e = 0; e < 4; ++e) v[e] += lab + e < l_end ? bias[lab + e] : 0.0f;
-            }
-            const uint32_t sb = sbase + (uint32_t)(((st >> 1) & 1) * kFdStage + cr * kFdStageRow + (st & 1) * 64 + 8 * cq);
-            *(lds_u32x2_t *)(uintptr_t)sb = u32x2_t{pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3])};
+            for (int e = 0; e < 4; ++e) v[e] += lab + e < l_end ? bias[lab + e] : 0.0f;
         }
+        const int piece = (st & 1) * 8 + 4 * nt + q;
+        const uint32_t sb = sbase + (uint32_t)(((st >> 1) & 1) * kFdStage + srow * 128 + ((piece ^ (srow & 15)) << 3));
+        *(lds_u32x2_t *)(uintptr_t)sb = u32x2_t{pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3])};
     };
     // flush of steps 2k, 2k + 1: thread -> row tid / 16, labels 4 (tid mod 16) .. + 3 (8 bytes)
     const int fr_ = tid >> 4, fp = tid & 15;
@@ -458,8 +457,8 @@ __global__ __launch_bounds__(512) void k_fwd_dn(const bf16_t *__restrict__ X, co
         const int64_t lab = l_begin + (int64_t)k * 64 + 4 * fp;
         const int64_t nv = l_end - lab;
         if (fr_ < rows && nv > 0) {
-            const u32x2_t v =
-                *(lds_u32x2_t *)(uintptr_t)(sbase + (uint32_t)((k & 1) * kFdStage + fr_ * kFdStageRow + 8 * fp));
+            const u32x2_t v = *(lds_u32x2_t *)(uintptr_t)(sbase + (uint32_t)((k & 1) * kFdStage + fr_ * 128 +
+                                                                             ((fp ^ (fr_ & 15)) << 3)));
             bf16_t *dst = Y + (int64_t)(b0 + fr_) * L + lab;
             if (nv >= 4) *reinterpret_cast<uint2 *>(dst) = make_uint2(v[0], v[1]);
             else *reinterpret_cast<uint32_t *>(dst) = v[0];   // L even: the row's last two labels
@@ -472,30 +471,37 @@ __global__ __launch_bounds__(512) void k_fwd_dn(const bf16_t *__restrict__ X, co
     scatter(rg[0], 0, ca[0]);                     // step 0
     __syncthreads();
 
+    // step t = t0 + U: tile t mod 3, partial sums t mod 2, ring slot t mod RSL, clear addresses t mod 2
     auto step = [&](int t, auto uc) __attribute__((always_inline)) {
         constexpr int U = decltype(uc)::value;
-        constexpr int PAR = U % 2;
+        constexpr int PAR = U % 2, TBI = U % 3;
         bf16x8_t ob[KCH];
 #pragma unroll
         for (int c = 0; c < KCH; ++c)
-            ob[c] = *(lds_bf16x8_t *)(uintptr_t)(arow + (uint32_t)(PAR * TB) +
+            ob[c] = *(lds_bf16x8_t *)(uintptr_t)(arow + (uint32_t)(TBI * TB) +
                                                  ((((uint32_t)(4 * (kh * KCH + c))) ^ ql) << 4));
         __builtin_amdgcn_sched_barrier(0);
-        clear(ca[1 - PAR]);                       // step t - 1's cells (its tile was read before the last barrier)
-        f32x4_t d = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+        // step t - 1's cells (tile (t + 2) mod 3, read before the last barrier) are cleared and step
+        // t + 1 is written into tile (t + 1) mod 3 (cleared before the last barrier)
+        clear(ca[1 - PAR]);
+        scatter(rg[(U + 1) % RSL], (TBI + 1) % 3, ca[1 - PAR]);
+        // two independent chains of products (even and odd chunks), so that one's latency is covered
+        f32x4_t d[2] = {f32x4_t{0.0f, 0.0f, 0.0f, 0.0f}, f32x4_t{0.0f, 0.0f, 0.0f, 0.0f}};
 #pragma unroll
-        for (int c = 0; c < KCH; ++c) d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ob[c], xa[c], d, 0, 0, 0);
-        *(__attribute__((address_space(3))) f32x4_t *)(uintptr_t)(rslot + PAR * kFdRed) = d;
-        if (t >= 1) combine(t - 1, 1 - PAR);
+        for (int c = 0; c < KCH; ++c) d[c & 1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ob[c], xa[c], d[c & 1], 0, 0, 0);
+        if (kh == 1) {
+            *(__attribute__((address_space(3))) f32x4_t *)(uintptr_t)(rslot + PAR * kFdRed) = d[0] + d[1];
+        } else {
+            if (t >= 1) combine(t - 1, 1 - PAR);
+            dprev = d[0] + d[1];
+        }
         if (PAR == 1 && t >= 3) flush((t - 3) >> 1);
-        __syncthreads();                          // clears done: the tile takes step t + 1
-        scatter(rg[(U + 1) % RSL], 1 - PAR, ca[1 - PAR]);
         load_step(t + RSL, rg[U % RSL]);          // step t's slot is free (scattered in the last step)
         __syncthreads();
     };
     for (int t0 = 0; t0 < n; t0 += PER)
         static_for<PER>([&](auto uc) __attribute__((always_inline)) { step(t0 + decltype(uc)::value, uc); });
-    combine(n - 1, (n - 1) & 1);
+    if (kh == 0) combine(n - 1, (n - 1) & 1);
     __syncthreads();
     flush((n - 2) >> 1);
 }
