@@ -133,12 +133,17 @@ CALL_FILES = {
 }
 
 
+# a tail call runs, depending on the layer's shape, kernels of any of the tail files, and the
+# fixed-order reductions of util.hip
+TAIL_FILES = ["tail_mfma.hip", "tail_sg.hip", "tail_dense.hip", "tail_valu.hip", "util.hip"]
+
+
 def kernel_source_hash(call=None):
-    """Hash of the kernel sources: those of one call (default: the tail file), or all of them."""
+    """Hash of the kernel sources: those of one call (default: the tail files), or all of them."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2606_01117_amd", "csrc")
     files = sorted(os.listdir(csrc)) if call is None else sorted(
-        CALL_FILES.get(call, ["tail_mfma.hip"]) + ["common.hpp"])
+        CALL_FILES.get(call, TAIL_FILES) + ["common.hpp"])
     for f in files:
         with open(os.path.join(csrc, f), "rb") as fh:
             h.update(f.encode() + fh.read())
