@@ -71,6 +71,13 @@ SMALL = [
     ("bf16_g1_f128_l1062", 45, 512, 1062, 1, 128, BF16),
     ("bf16_g8_f128", 33, 768, 1024, 8, 128, BF16),
     ("bf16_g4_fs1024", 40, 1024, 2048, 4, 64, BF16),
+    # the scattered-tile kernels: feature counts that are not whole tiles, 64-row workgroups with a
+    # mostly empty row tile, 2-label row tails, a layer shorter than the segments it is cut into,
+    # feature counts between the tile-count steps
+    ("bf16_g2_fs104_l1030", 33, 104, 1030, 2, 32, BF16),
+    ("bf16_g1_fs200_b31", 31, 200, 2050, 1, 64, BF16),
+    ("bf16_g2_l130", 40, 256, 130, 2, 64, BF16),
+    ("bf16_g8_fs520", 64, 520, 2048, 8, 64, BF16),
     # 256-slot supports (the VALU kernels)
     ("bf16_g32_f256", 40, 768, 2048, 32, 256, BF16),
     ("f32_g8", 32, 256, 4096, 8, 32, F32),
