@@ -122,7 +122,10 @@ int haste_bwd_x(const haste_desc_t *desc, const int32_t *idx, const void *W, con
  * bucketed by workgroup and batch slab in the workspace, whose queried size provides for up to
  * 1024 per row (2 F_s round_up(B, 32) + 8 (L B / 512) + 4 B P bytes about; a larger P fuses when
  * ws holds that much, else composes).  Other layers run haste_fwd into dY, the gradient in place
- * (for bf16 the sigmoid then sees the logits rounded to bf16), and haste_bwd_w.
+ * (for bf16 the sigmoid then sees the logits rounded to bf16), and haste_bwd_w; for bf16 groups of
+ * 1, 2, 4 or 8 labels with rows of up to 256 positives the forward kernel itself stores that same
+ * gradient (bit for bit), after sorting each row's positives into the workspace (B * P * 4 bytes
+ * after the X^T copy; the queried size provides for 256 per row).
  * ws: haste_workspace_bytes(desc, HASTE_OP_FWD_BCE) bytes.
  */
 int haste_fwd_bce(const haste_desc_t *desc, const void *X, const int32_t *idx, const void *W,

@@ -79,6 +79,17 @@ bool fwd_kernel_exists(const haste::TailArgs &a) {
            haste::valu_supported(a);
 }
 
+// the small-group forward kernels form the loss gradient as they store (given the sorted positives)
+bool fwd_small_bce(const haste::TailArgs &a, int P) {
+    return P <= haste::kSortPosMax && (haste::fwd_dn_supported(a) || haste::fwd_sg_supported(a));
+}
+
+hipError_t fwd_small(const haste::TailArgs &a, const void *X, const int32_t *idx, const void *W, const float *bias,
+                     void *Y, hipStream_t s, const int32_t *spos, int P) {
+    if (haste::fwd_dn_supported(a)) return haste::fwd_dn(a, X, idx, W, bias, Y, s, spos, P);
+    return haste::fwd_sg(a, X, idx, W, bias, Y, s, spos, P);
+}
+
 hipError_t fwd_any(const haste::TailArgs &a, const void *X, const int32_t *idx, const void *W, const float *bias,
                    void *Y, hipStream_t s) {
     if (haste::fwd_dn_supported(a)) return haste::fwd_dn(a, X, idx, W, bias, Y, s);
@@ -141,9 +152,14 @@ size_t haste_workspace_bytes(const haste_desc_t *d, int op) {
         case HASTE_OP_BWD_X: return bwd_x_ws(a);
         // the fused kernel and the backward-weight kernel stage the same X^T copy; the fused kernel
         // also buckets rows of many positives (provided for up to kFusedPosWs per row)
-        case HASTE_OP_FWD_BCE:
+        // small groups: the sorted positives (for rows of up to kSortPosMax) after the X^T copy
+        case HASTE_OP_FWD_BCE: {
             if (haste::fwd_bce_mfma_supported(a, haste::kFusedPosWs)) return haste::fwd_bce_mfma_ws(a, haste::kFusedPosWs);
-            return bwd_w_uses_xt(a) ? haste::bwd_w_mfma_ws(a) : 0;
+            const size_t xws = bwd_w_uses_xt(a) ? haste::bwd_w_mfma_ws(a) : 0;
+            if (!fwd_small_bce(a, 0)) return xws;
+            return (size_t)haste::round_up((int64_t)xws, 256) +
+                   (size_t)haste::round_up(a.B * haste::kSortPosMax * 4, 256);
+        }
         // the composed form also keeps dW in the workspace (after the X^T copy)
         case HASTE_OP_REWIRE: return haste::rewire_supported(a) ? haste::rewire_ws(a) : 0;
         // backward-feature's region (partials, transposed weights, supports), then the fused kernel's
@@ -153,9 +169,10 @@ size_t haste_workspace_bytes(const haste_desc_t *d, int op) {
         case HASTE_OP_TAIL_STEP_SGD:
             return (size_t)haste::round_up((int64_t)haste_workspace_bytes(d, HASTE_OP_BWD_X), 256) +
                    haste_workspace_bytes(d, HASTE_OP_FWD_BCE_SGD);
+        // composed: haste_fwd_bce's region, then dW
         case HASTE_OP_FWD_BCE_SGD:
             if (haste::fwd_bce_mfma_supported(a, haste::kFusedPosWs)) return haste::fwd_bce_mfma_ws(a, haste::kFusedPosWs);
-            return (bwd_w_uses_xt(a) ? haste::bwd_w_mfma_ws(a) : 0) +
+            return (size_t)haste::round_up((int64_t)haste_workspace_bytes(d, HASTE_OP_FWD_BCE), 256) +
                    (size_t)haste::round_up(a.L * a.F_in * 4, 256);
     }
     return 0;
@@ -311,10 +328,21 @@ int haste_fwd_bce(const haste_desc_t *d, const void *X, const int32_t *idx, cons
     if (haste::fwd_bce_mfma_supported(a, P) && ws_bytes >= haste::fwd_bce_mfma_ws(a, P))
         return hip_status(haste::fwd_bce_mfma(a, X, idx, W, bias, P > 0 ? pos : nullptr, P, dY, dW, dbias, beta, ws, s),
                           "haste_fwd_bce");
-    // composed: logits into dY, the gradient in place, then the backward-weight product
-    if (!fwd_kernel_exists(a)) return fail(HASTE_ERR_UNSUPPORTED, "no forward kernel for this shape");
-    hipError_t e = fwd_any(a, X, idx, W, bias, dY, s);
-    if (e == hipSuccess) e = haste::bce_grad(a.B, a.L, a.dtype, dY, P > 0 ? pos : nullptr, P, dY, s);
+    // small groups: the forward stores the gradient of its rounded logits (bit for bit what the
+    // separate gradient pass computes), given each row's positives sorted after the X^T copy
+    const size_t spos_at = (size_t)haste::round_up((int64_t)need, 256);
+    hipError_t e = hipSuccess;
+    if (fwd_small_bce(a, P) && ws && ws_bytes >= spos_at + (size_t)a.B * P * 4) {
+        int32_t *spos = reinterpret_cast<int32_t *>(static_cast<char *>(ws) + spos_at);
+        if (P > 0) e = haste::sort_positives(a.B, a.L, pos, P, spos, s);
+        // with no positives the kernels never read the list, but need a non-null one to form the gradient
+        if (e == hipSuccess) e = fwd_small(a, X, idx, W, bias, dY, s, P > 0 ? spos : reinterpret_cast<int32_t *>(dY), P);
+    } else {
+        // composed: logits into dY, the gradient in place
+        if (!fwd_kernel_exists(a)) return fail(HASTE_ERR_UNSUPPORTED, "no forward kernel for this shape");
+        e = fwd_any(a, X, idx, W, bias, dY, s);
+        if (e == hipSuccess) e = haste::bce_grad(a.B, a.L, a.dtype, dY, P > 0 ? pos : nullptr, P, dY, s);
+    }
     if (e == hipSuccess && dW)
         e = bwd_w_any(a, X, idx, dY, dW, dbias, beta, ws, s);
     return hip_status(e, "haste_fwd_bce");
@@ -374,7 +402,8 @@ int haste_fwd_bce_sgd(const haste_desc_t *d, const void *X, const int32_t *idx, 
     // the fused kernel's shapes need the X^T copy (and the bucketed positives of rows of more than
     // 64); others keep dW in the workspace too
     const bool fused_shape = haste::fwd_bce_mfma_supported(a, P);
-    const size_t xws = bwd_w_uses_xt(a) ? haste::bwd_w_mfma_ws(a) : 0;
+    // composed: haste_fwd_bce's region (the X^T copy and sorted positives), then dW
+    const size_t xws = (size_t)haste::round_up((int64_t)haste_workspace_bytes(d, HASTE_OP_FWD_BCE), 256);
     const size_t need = fused_shape ? haste::fwd_bce_mfma_ws(a, P) : xws + (size_t)haste::round_up(a.L * a.F_in * 4, 256);
     if (a.B == 0) {  // no rows: a zero gradient, the step still decays the velocity and the weights
         if (dbias) TRY(hip_status(haste::fill_f32(dbias, a.L, 0.0f, s), "haste_fwd_bce_sgd"));

@@ -173,6 +173,43 @@ __device__ __forceinline__ float bce_grad_f32(float z, bool positive) {
     return positive ? sg - 1.0f : sg;
 }
 
+// The loss-gradient targets of one batch row over an increasing sequence of label windows, read
+// from the row's positives sorted ascending (INT32_MAX past the last; sort_positives): `cur` is
+// the first positive not yet passed.  Windows must not go back.
+struct PosCursor {
+    const int32_t *p;
+    int P, cur;
+    int32_t nxt;
+    // start at the first positive >= first (binary search)
+    __device__ __forceinline__ void init(const int32_t *row, int P_, int64_t first) {
+        p = row;
+        P = P_;
+        int lo = 0, hi = P_;
+        while (lo < hi) {
+            const int mid = (lo + hi) >> 1;
+            if ((int64_t)row[mid] < first) lo = mid + 1;
+            else hi = mid;
+        }
+        cur = lo;
+        nxt = cur < P ? p[cur] : INT32_MAX;
+    }
+    // bit e set where label lab + e (e < n <= 32) is a positive of the row
+    __device__ __forceinline__ uint32_t bits(int64_t lab, int n) {
+        uint32_t t = 0;
+        while (nxt != INT32_MAX && (int64_t)nxt < lab + n) {
+            if ((int64_t)nxt >= lab) t |= 1u << (uint32_t)(nxt - lab);
+            ++cur;
+            nxt = cur < P ? p[cur] : INT32_MAX;
+        }
+        return t;
+    }
+};
+
+// bf16 pair -> the loss gradients of both logits (targets bit 0 and bit 1 of t), as a bf16 pair
+__device__ __forceinline__ uint32_t bce_pair(uint32_t w, uint32_t t) {
+    return pack_bf16(bce_grad_f32(__uint_as_float(w << 16), t & 1u), bce_grad_f32(__uint_as_float(w & 0xffff0000u), (t >> 1) & 1u));
+}
+
 // One step of SGD with momentum on one weight (the classification layer's optimizer, Section 4):
 // velocity m <- momentum * m + (g + weight_decay * w), then w_next = w - lr * m.  Explicit fused
 // multiply-adds, so that every kernel that applies the step rounds it the same way.
@@ -199,8 +236,10 @@ hipError_t fwd_mfma(const TailArgs &a, const void *X, const int32_t *idx, const 
                     void *Y, hipStream_t s);
 // forward for small groups (G = 1, 2, 4, 8), 16 / G groups per matrix tile
 bool fwd_sg_supported(const TailArgs &a);
+// spos (optional): the rows' positives sorted by sort_positives; the output is then the loss
+// gradient sigmoid(Y) - T of the bf16 logits, bit for bit as bce_grad computes it
 hipError_t fwd_sg(const TailArgs &a, const void *X, const int32_t *idx, const void *W, const float *bias, void *Y,
-                  hipStream_t s);
+                  hipStream_t s, const int32_t *spos = nullptr, int P = 0);
 // backward-weight for small groups (G = 1, 2, 4, 8), on the workspace's X^T copy (bwd_w_mfma_ws)
 bool bwd_w_sg_supported(const TailArgs &a);
 hipError_t bwd_w_sg(const TailArgs &a, const void *X, const int32_t *idx, const void *dY, float *dW, float *dbias,
@@ -221,7 +260,7 @@ hipError_t bwd_x_dn(const TailArgs &a, const int32_t *idx, const void *W, const 
 // weights scattered into an LDS tile
 bool fwd_dn_supported(const TailArgs &a);
 hipError_t fwd_dn(const TailArgs &a, const void *X, const int32_t *idx, const void *W, const float *bias, void *Y,
-                  hipStream_t s);
+                  hipStream_t s, const int32_t *spos = nullptr, int P = 0);
 bool bwd_w_mfma_supported(const TailArgs &a);
 size_t bwd_w_mfma_ws(const TailArgs &a);
 hipError_t bwd_w_mfma(const TailArgs &a, const void *X, const int32_t *idx, const void *dY, float *dW,
@@ -266,6 +305,9 @@ bool group_supported(int64_t N, int64_t D, int64_t G, int64_t beta);
 size_t group_ws(int64_t N, int64_t D, int64_t G, int64_t beta);
 hipError_t group_labels(int64_t N, int64_t D, const int8_t *E, int64_t G, int64_t beta, int64_t iters, uint64_t seed,
                         int32_t *order, int32_t *gsize, int64_t *n_groups, int32_t *cluster, void *ws, hipStream_t s);
+// spos[b][0..P): row b's positives in [0, N) sorted ascending, the rest INT32_MAX (P <= kSortPosMax)
+constexpr int kSortPosMax = 256;
+hipError_t sort_positives(int64_t B, int64_t N, const int32_t *pos, int P, int32_t *spos, hipStream_t s);
 // dY[b, n] = sigmoid(Y[b, n]) - T[b, n] elementwise (Y and dY may alias)
 hipError_t bce_grad(int64_t B, int64_t N, int32_t dtype, const void *Y, const int32_t *pos, int P, void *dY,
                     hipStream_t s);

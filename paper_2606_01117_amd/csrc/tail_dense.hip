@@ -319,7 +319,7 @@ template <int KCH, int F_IN, bool HAS_BIAS>
 __global__ __launch_bounds__(512) void k_fwd_dn(const bf16_t *__restrict__ X, const int32_t *__restrict__ idx,
                                                 const bf16_t *__restrict__ W, const float *__restrict__ bias,
                                                 bf16_t *__restrict__ Y, int B, int F_s, int64_t L, int gshift, int nbt,
-                                                int64_t lps) {
+                                                int64_t lps, const int32_t *__restrict__ spos, int P) {
     constexpr int FR = 64 * KCH;                  // tile columns (features)
     constexpr int TB = 64 * FR;                   // tile bytes: [32 labels][FR] bf16
     constexpr int LPL = 16;                       // lanes per label of a step
@@ -451,14 +451,21 @@ __global__ __launch_bounds__(512) void k_fwd_dn(const bf16_t *__restrict__ X, co
         const uint32_t sb = sbase + (uint32_t)(((st >> 1) & 1) * kFdStage + srow * 128 + ((piece ^ (srow & 15)) << 3));
         *(lds_u32x2_t *)(uintptr_t)sb = u32x2_t{pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3])};
     };
-    // flush of steps 2k, 2k + 1: thread -> row tid / 16, labels 4 (tid mod 16) .. + 3 (8 bytes)
+    // flush of steps 2k, 2k + 1: thread -> row tid / 16, labels 4 (tid mod 16) .. + 3 (8 bytes);
+    // with the positives, the loss gradient of the rounded logits
     const int fr_ = tid >> 4, fp = tid & 15;
+    PosCursor tgt;
+    if (spos && fr_ < rows) tgt.init(spos + (int64_t)(b0 + fr_) * P, P, l_begin + 4 * fp);
     auto flush = [&](int k) __attribute__((always_inline)) {
         const int64_t lab = l_begin + (int64_t)k * 64 + 4 * fp;
         const int64_t nv = l_end - lab;
         if (fr_ < rows && nv > 0) {
-            const u32x2_t v = *(lds_u32x2_t *)(uintptr_t)(sbase + (uint32_t)((k & 1) * kFdStage + fr_ * 128 +
-                                                                             ((fp ^ (fr_ & 15)) << 3)));
+            u32x2_t v = *(lds_u32x2_t *)(uintptr_t)(sbase + (uint32_t)((k & 1) * kFdStage + fr_ * 128 +
+                                                                       ((fp ^ (fr_ & 15)) << 3)));
+            if (spos) {   // kernel-uniform
+                const uint32_t t = tgt.bits(lab, 4);
+                v = u32x2_t{bce_pair(v[0], t), bce_pair(v[1], t >> 2)};
+            }
             bf16_t *dst = Y + (int64_t)(b0 + fr_) * L + lab;
             if (nv >= 4) *reinterpret_cast<uint2 *>(dst) = make_uint2(v[0], v[1]);
             else *reinterpret_cast<uint32_t *>(dst) = v[0];   // L even: the row's last two labels
@@ -597,27 +604,27 @@ static FdGeom fd_geom(const haste::TailArgs &a) {
 
 template <int KCH, int F_IN>
 static hipError_t launch_fd(const haste::TailArgs &a, const FdGeom &g, const void *X, const int32_t *idx, const void *W,
-                            const float *bias, void *Y, hipStream_t s) {
+                            const float *bias, void *Y, hipStream_t s, const int32_t *spos, int P) {
     auto kern = bias ? k_fwd_dn<KCH, F_IN, true> : k_fwd_dn<KCH, F_IN, false>;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
                                        (int)g.lds);
     if (e != hipSuccess) return e;
     const int gshift = a.G == 1 ? 0 : a.G == 2 ? 1 : a.G == 4 ? 2 : 3;
     hipLaunchKernelGGL(kern, dim3((unsigned)(g.nseg * g.nbt)), dim3(512), g.lds, s, (const bf16_t *)X, idx,
-                       (const bf16_t *)W, bias, (bf16_t *)Y, (int)a.B, (int)a.F_s, a.L, gshift, g.nbt, g.lps);
+                       (const bf16_t *)W, bias, (bf16_t *)Y, (int)a.B, (int)a.F_s, a.L, gshift, g.nbt, g.lps, spos, P);
     return hipGetLastError();
 }
 
 template <int F_IN>
 static hipError_t fd_f(const haste::TailArgs &a, const FdGeom &g, const void *X, const int32_t *idx, const void *W,
-                       const float *bias, void *Y, hipStream_t s) {
+                       const float *bias, void *Y, hipStream_t s, const int32_t *spos, int P) {
     switch (g.kch) {
-        case 2: return launch_fd<2, F_IN>(a, g, X, idx, W, bias, Y, s);
-        case 4: return launch_fd<4, F_IN>(a, g, X, idx, W, bias, Y, s);
-        case 6: return launch_fd<6, F_IN>(a, g, X, idx, W, bias, Y, s);
-        case 8: return launch_fd<8, F_IN>(a, g, X, idx, W, bias, Y, s);
-        case 10: return launch_fd<10, F_IN>(a, g, X, idx, W, bias, Y, s);
-        case 12: return launch_fd<12, F_IN>(a, g, X, idx, W, bias, Y, s);
+        case 2: return launch_fd<2, F_IN>(a, g, X, idx, W, bias, Y, s, spos, P);
+        case 4: return launch_fd<4, F_IN>(a, g, X, idx, W, bias, Y, s, spos, P);
+        case 6: return launch_fd<6, F_IN>(a, g, X, idx, W, bias, Y, s, spos, P);
+        case 8: return launch_fd<8, F_IN>(a, g, X, idx, W, bias, Y, s, spos, P);
+        case 10: return launch_fd<10, F_IN>(a, g, X, idx, W, bias, Y, s, spos, P);
+        case 12: return launch_fd<12, F_IN>(a, g, X, idx, W, bias, Y, s, spos, P);
     }
     return hipErrorInvalidValue;
 }
@@ -669,12 +676,12 @@ bool fwd_dn_supported(const TailArgs &a) {
 }
 
 hipError_t fwd_dn(const TailArgs &a, const void *X, const int32_t *idx, const void *W, const float *bias, void *Y,
-                  hipStream_t s) {
+                  hipStream_t s, const int32_t *spos, int P) {
     const FdGeom g = fd_geom(a);
     switch (a.F_in) {
-        case 32: return fd_f<32>(a, g, X, idx, W, bias, Y, s);
-        case 64: return fd_f<64>(a, g, X, idx, W, bias, Y, s);
-        case 128: return fd_f<128>(a, g, X, idx, W, bias, Y, s);
+        case 32: return fd_f<32>(a, g, X, idx, W, bias, Y, s, spos, P);
+        case 64: return fd_f<64>(a, g, X, idx, W, bias, Y, s, spos, P);
+        case 128: return fd_f<128>(a, g, X, idx, W, bias, Y, s, spos, P);
     }
     return hipErrorInvalidValue;
 }

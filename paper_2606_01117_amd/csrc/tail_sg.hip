@@ -57,7 +57,8 @@ template <int G, int F_IN, bool HAS_BIAS>
 __global__ __launch_bounds__(kSgThreads) void k_fwd_sg(const bf16_t *__restrict__ X, const int32_t *__restrict__ idx,
                                                        const bf16_t *__restrict__ W, const float *__restrict__ bias,
                                                        bf16_t *__restrict__ Y, int B, int F_s, int64_t L, int nbt,
-                                                       int64_t pps, int64_t npass) {
+                                                       int64_t pps, int64_t npass, const int32_t *__restrict__ spos,
+                                                       int P) {
     using S = SgGeom<G, F_IN>;
     extern __shared__ __align__(16) char sgs[];
     char *xs = sgs;                                               // [F_s][kSgXRow]
@@ -119,6 +120,9 @@ __global__ __launch_bounds__(kSgThreads) void k_fwd_sg(const bf16_t *__restrict_
     const int kg0 = 2 * G * n_grp;
     const bool wact = kg0 < 8 * q + 8 && kg0 + 2 * G > 8 * q;
 
+    // the loss-gradient targets of this thread's output row, from the first window it stores
+    PosCursor tgt;
+    if (spos && b0 + (tid >> 4) < B) tgt.init(spos + (int64_t)(b0 + (tid >> 4)) * P, P, p_begin * kSgPass + 8 * (tid & 15));
     fetch(p_begin);
     for (int64_t p = p_begin; p < p_end; ++p) {
         __syncthreads();   // the previous pass's staging and output are no longer read
@@ -174,12 +178,17 @@ __global__ __launch_bounds__(kSgThreads) void k_fwd_sg(const bf16_t *__restrict_
                 *reinterpret_cast<bf16_t *>(so + (16 * m + 4 * q + r) * kSgOutRow + (16 * wave + l16) * 2) =
                     f32_to_bf16(acc[m][r]);
         __syncthreads();
-        // 32 rows x 256 bytes: one 16-byte chunk per thread (16 chunks per row)
+        // 32 rows x 256 bytes: one 16-byte chunk per thread (16 chunks per row); with the positives,
+        // the loss gradient of the rounded logits
         {
             const int r = tid >> 4, c = tid & 15;
             const int64_t lb = p * kSgPass + 8 * c;
             if (b0 + r < B && lb < L) {
-                const uint4 v = *reinterpret_cast<const uint4 *>(so + r * kSgOutRow + c * 16);
+                uint4 v = *reinterpret_cast<const uint4 *>(so + r * kSgOutRow + c * 16);
+                if (spos) {   // kernel-uniform
+                    const uint32_t t = tgt.bits(lb, 8);
+                    v = make_uint4(bce_pair(v.x, t), bce_pair(v.y, t >> 2), bce_pair(v.z, t >> 4), bce_pair(v.w, t >> 6));
+                }
                 bf16_t *dst = Y + (int64_t)(b0 + r) * L + lb;
                 if (lb + 8 <= L) {
                     __builtin_nontemporal_store(__builtin_bit_cast(u32x4_t, v), reinterpret_cast<u32x4_t *>(dst));
@@ -194,7 +203,7 @@ __global__ __launch_bounds__(kSgThreads) void k_fwd_sg(const bf16_t *__restrict_
 
 template <int G, int F_IN>
 static hipError_t launch_fwd_sg(const haste::TailArgs &a, const void *X, const int32_t *idx, const void *W,
-                                const float *bias, void *Y, hipStream_t s) {
+                                const float *bias, void *Y, hipStream_t s, const int32_t *spos, int P) {
     const size_t lds = sg_lds<G, F_IN>((int)a.F_s);
     const int nbt = (int)haste::cdiv(a.B, kSgRows);
     const int64_t npass = haste::cdiv(a.L, kSgPass);
@@ -209,7 +218,7 @@ static hipError_t launch_fwd_sg(const haste::TailArgs &a, const void *X, const i
                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
         if (e != hipSuccess) return e;
         hipLaunchKernelGGL(kern, dim3((unsigned)(nseg * nbt)), dim3(kSgThreads), lds, s, (const bf16_t *)X, idx,
-                           (const bf16_t *)W, bias, (bf16_t *)Y, (int)a.B, (int)a.F_s, a.L, nbt, pps, npass);
+                           (const bf16_t *)W, bias, (bf16_t *)Y, (int)a.B, (int)a.F_s, a.L, nbt, pps, npass, spos, P);
         return hipGetLastError();
     };
     return bias ? go(k_fwd_sg<G, F_IN, true>) : go(k_fwd_sg<G, F_IN, false>);
@@ -217,12 +226,12 @@ static hipError_t launch_fwd_sg(const haste::TailArgs &a, const void *X, const i
 
 template <int G>
 static hipError_t fwd_sg_g(const haste::TailArgs &a, const void *X, const int32_t *idx, const void *W,
-                           const float *bias, void *Y, hipStream_t s) {
+                           const float *bias, void *Y, hipStream_t s, const int32_t *spos, int P) {
     switch (a.F_in) {
-        case 32: return launch_fwd_sg<G, 32>(a, X, idx, W, bias, Y, s);
-        case 64: return launch_fwd_sg<G, 64>(a, X, idx, W, bias, Y, s);
+        case 32: return launch_fwd_sg<G, 32>(a, X, idx, W, bias, Y, s, spos, P);
+        case 64: return launch_fwd_sg<G, 64>(a, X, idx, W, bias, Y, s, spos, P);
         case 128:
-            if constexpr (G >= 2) return launch_fwd_sg<G, 128>(a, X, idx, W, bias, Y, s);
+            if constexpr (G >= 2) return launch_fwd_sg<G, 128>(a, X, idx, W, bias, Y, s, spos, P);
             break;
     }
     return hipErrorInvalidValue;
@@ -876,12 +885,12 @@ hipError_t bwd_x_sg(const TailArgs &a, const int32_t *idx, const void *W, const 
 }
 
 hipError_t fwd_sg(const TailArgs &a, const void *X, const int32_t *idx, const void *W, const float *bias, void *Y,
-                  hipStream_t s) {
+                  hipStream_t s, const int32_t *spos, int P) {
     switch (a.G) {
-        case 1: return fwd_sg_g<1>(a, X, idx, W, bias, Y, s);
-        case 2: return fwd_sg_g<2>(a, X, idx, W, bias, Y, s);
-        case 4: return fwd_sg_g<4>(a, X, idx, W, bias, Y, s);
-        case 8: return fwd_sg_g<8>(a, X, idx, W, bias, Y, s);
+        case 1: return fwd_sg_g<1>(a, X, idx, W, bias, Y, s, spos, P);
+        case 2: return fwd_sg_g<2>(a, X, idx, W, bias, Y, s, spos, P);
+        case 4: return fwd_sg_g<4>(a, X, idx, W, bias, Y, s, spos, P);
+        case 8: return fwd_sg_g<8>(a, X, idx, W, bias, Y, s, spos, P);
     }
     return hipErrorInvalidValue;
 }

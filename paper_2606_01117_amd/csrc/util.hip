@@ -184,6 +184,31 @@ __global__ __launch_bounds__(256) void k_bce_grad(const T *Y, const int32_t *__r
     }
 }
 
+// Each batch row's positives sorted ascending (one wave per row): element i goes to its rank
+// #{j : v_j < v_i, or v_j == v_i and j < i}; ids outside [0, N) (the -1 padding) sort last as
+// INT32_MAX.
+__global__ __launch_bounds__(256) void k_sort_pos(const int32_t *__restrict__ pos, int P, int64_t B, int64_t N,
+                                                  int32_t *__restrict__ spos) {
+    __shared__ int32_t v[4][haste::kSortPosMax];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int64_t b = (int64_t)blockIdx.x * 4 + w;
+    if (b >= B) return;   // wave-uniform; no barrier follows
+    for (int i = lane; i < P; i += 64) {
+        const int32_t x = pos[b * P + i];
+        v[w][i] = x >= 0 && x < N ? x : INT32_MAX;
+    }
+    __builtin_amdgcn_wave_barrier();
+    for (int i = lane; i < P; i += 64) {
+        const int32_t x = v[w][i];
+        int r = 0;
+        for (int j = 0; j < P; ++j) {
+            const int32_t y = v[w][j];
+            r += (y < x) || (y == x && j < i);
+        }
+        spos[b * P + r] = x;
+    }
+}
+
 // One momentum step per weight (sgd_step), four consecutive weights per thread: 16-byte velocity and
 // gradient accesses and 8- or 16-byte weight accesses when n is a multiple of 4 and the buffers are
 // aligned (VEC), else one weight per thread.  W_next may be W: each weight is read before it is
@@ -283,6 +308,12 @@ hipError_t bce_grad(int64_t B, int64_t N, int32_t dtype, const void *Y, const in
     return hipGetLastError();
 }
 
+
+hipError_t sort_positives(int64_t B, int64_t N, const int32_t *pos, int P, int32_t *spos, hipStream_t s) {
+    if (B <= 0 || P <= 0) return hipSuccess;
+    hipLaunchKernelGGL(k_sort_pos, dim3((unsigned)cdiv(B, 4)), dim3(256), 0, s, pos, P, B, N, spos);
+    return hipGetLastError();
+}
 
 hipError_t sgd_momentum(int64_t n, int32_t dtype, const void *W, const float *g, float *m, const haste_sgd_t &opt,
                         void *W_next, hipStream_t s) {

@@ -63,9 +63,16 @@ CASES = [
     ("fused_p80_full_cell", 32, 768, 4096, 32, 64, BF16, -80, False),
     ("fused_fs1024", 70, 1024, 4096, 32, 64, BF16, 8, True),
     ("fused_fs1024_f128_p100", 45, 1024, 2048, 32, 128, BF16, -100, False),
+    # small groups: the forward kernel stores the gradient (rows of up to 256 positives, sorted
+    # first), else the forward, the gradient pass and backward-weight
     ("composed_g8", 70, 768, 3072, 8, 32, BF16, 5, True),
     ("composed_g4", 64, 512, 1536, 4, 64, BF16, 5, False),
     ("composed_g1_ffi", 37, 768, 1024, 1, 64, BF16, 4, False),
+    ("small_g4_p100_skewed", 64, 512, 2048, 4, 64, BF16, -100, True),
+    ("small_g1_p40_l1030", 40, 256, 1030, 1, 32, BF16, 40, False),
+    ("small_g2_p0", 33, 256, 1024, 2, 64, BF16, 0, True),
+    ("small_g8_p256_skewed", 36, 768, 4096, 8, 64, BF16, -256, False),
+    ("small_g2_p300_composed", 36, 256, 2048, 2, 64, BF16, 300, False),
     ("composed_f32_g8", 32, 256, 4096, 8, 32, F32, 5, True),
 ]
 
@@ -109,6 +116,14 @@ def test_fwd_bce(hs, orc, case):
     hs.haste_bwd_w(desc, Xd, idxd, dY, dW2, db2, 0, hs.workspace(hs.haste_workspace_bytes(desc, hs.HASTE_OP_BWD_W)))
     _sync()
     assert bool((dW2 == dW).all()) and bool((db2 == db).all()), "fused dW differs from haste_bwd_w on its dY"
+    if dt == BF16 and G in (1, 2, 4, 8):
+        # small groups: the gradient the forward stores is the gradient pass's on its logits, bit for bit
+        Y = out_tensor((B, L), dt)
+        hs.haste_fwd(desc, Xd, idxd, Wd, bd, Y)
+        dY3 = out_tensor((B, L), dt)
+        hs.haste_bce_grad(B, L, dt, Y, posd, dY3)
+        _sync()
+        assert bool((dY3 == dY).all()), "the forward's gradient store differs from haste_bce_grad on its logits"
     # beta = 1 accumulates; without dW only dY is written
     hs.haste_fwd_bce(desc, Xd, idxd, Wd, bd, posd, dY, dW, db, 1, ws)
     dY2 = out_tensor((B, L), dt)
