@@ -354,7 +354,7 @@ struct G4Operand {
 };
 
 template <int BN, bool AK, bool BK, int EPI>
-__global__ __launch_bounds__(256, BN == 128 ? 2 : 1) void k_gemm4(
+__global__ __launch_bounds__(256, BN <= 128 ? 2 : 1) void k_gemm4(
     const bf16_t *__restrict__ A, int64_t sa, uint32_t a_bytes, const bf16_t *__restrict__ Bm, int64_t sb,
     uint32_t b_bytes, void *__restrict__ C, int64_t ldc, const float *__restrict__ bias, int64_t M, int64_t N,
     int64_t K, int64_t kchunk, int MT, int NT, int Z, const int32_t *__restrict__ pos, int P) {
@@ -652,12 +652,12 @@ bool gemm4_ok(int64_t B, int64_t F_s, int64_t H, std::initializer_list<const voi
 }
 
 // C[M, N] (+)= A B over K, split into Z chunks of kchunk (a multiple of the K step); sa, sb are
-// the operands' row strides (elements).  256 x kHeadBN output tiles.
-template <bool AK, bool BK, int EPI>
-hipError_t launch_gemm4(hipStream_t s, const bf16_t *A, int64_t sa, int64_t a_elems, const bf16_t *Bm, int64_t sb,
-                        int64_t b_elems, void *C, int64_t ldc, const float *bias, int64_t M, int64_t N, int64_t K,
-                        int64_t kchunk, int Z, const int32_t *pos = nullptr, int P = 0) {
-    constexpr int BN = kHeadBN;
+// the operands' row strides (elements).  256 x kHeadBN output tiles, or 256 x 64 where the wider
+// ones would leave CUs idle (a 16K-label head over 256 rows: 128 tiles against 256 CUs).
+template <int BN, bool AK, bool BK, int EPI>
+hipError_t launch_gemm4_bn(hipStream_t s, const bf16_t *A, int64_t sa, int64_t a_elems, const bf16_t *Bm, int64_t sb,
+                           int64_t b_elems, void *C, int64_t ldc, const float *bias, int64_t M, int64_t N, int64_t K,
+                           int64_t kchunk, int Z, const int32_t *pos, int P) {
     const int MT = (int)haste::cdiv(M, G4T), NT = (int)haste::cdiv(N, BN);
     const int64_t grid = Z > 1 ? haste::round_up(Z, kXcds) * MT * NT
                                : (MT <= NT ? haste::round_up(NT, kXcds) * MT : haste::round_up(MT, kXcds) * NT);
@@ -668,6 +668,18 @@ hipError_t launch_gemm4(hipStream_t s, const bf16_t *A, int64_t sa, int64_t a_el
     hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(256), g4_lds(BN), s, A, sa, (uint32_t)(a_elems * 2), Bm, sb,
                        (uint32_t)(b_elems * 2), C, ldc, bias, M, N, K, kchunk, MT, NT, Z, pos, P);
     return hipGetLastError();
+}
+
+template <bool AK, bool BK, int EPI>
+hipError_t launch_gemm4(hipStream_t s, const bf16_t *A, int64_t sa, int64_t a_elems, const bf16_t *Bm, int64_t sb,
+                        int64_t b_elems, void *C, int64_t ldc, const float *bias, int64_t M, int64_t N, int64_t K,
+                        int64_t kchunk, int Z, const int32_t *pos = nullptr, int P = 0) {
+    const int64_t tiles = haste::cdiv(M, G4T) * haste::cdiv(N, kHeadBN) * Z;
+    if (tiles < kXcds * kCusPerXcd && N % 64 == 0)
+        return launch_gemm4_bn<64, AK, BK, EPI>(s, A, sa, a_elems, Bm, sb, b_elems, C, ldc, bias, M, N, K, kchunk, Z,
+                                                pos, P);
+    return launch_gemm4_bn<kHeadBN, AK, BK, EPI>(s, A, sa, a_elems, Bm, sb, b_elems, C, ldc, bias, M, N, K, kchunk, Z,
+                                                 pos, P);
 }
 
 template <bool AK, bool BK, int EPI>
