@@ -565,10 +565,12 @@ __host__ __device__ constexpr int fb_waves(int F_in) { return F_in == 128 ? 8 : 
 // a wave's LDS region for the transposed weights of its group (32 labels) and the slot positions
 __host__ __device__ constexpr int fb_wt_region(int f_in) { return 32 * f_in * 2 + 128; }
 
-// X^T block, both bitmaps and the staged dY block, or at the end the dW staging of half the waves
-static size_t fb_lds(int F_s, int F_in) {
-    const size_t main = (size_t)haste::round_up((int64_t)F_s * kBw2XRow, 16) + 2 * kFbMaxSpan * 4 +
-                        (size_t)32 * kFbYRow;
+// The X^T block (two with dbx: the next slab's is staged while the current one is in use), the
+// target bitmaps (two, or three with dbx) and the staged dY block; or at the end the dW staging of
+// half the waves
+static size_t fb_lds(int F_s, int F_in, bool dbx) {
+    const size_t main = (size_t)(dbx ? 2 : 1) * haste::round_up((int64_t)F_s * kBw2XRow, 16) +
+                        (size_t)(dbx ? 3 : 2) * kFbMaxSpan * 4 + (size_t)32 * kFbYRow;
     const size_t out = (size_t)(fb_waves(F_in) / 2) * 32 * (F_in + 4) * 4;
     return main > out ? main : out;
 }
@@ -589,7 +591,7 @@ constexpr int kFbPrefetchFs = 768;
 // momentum step to W with it (dW never stored)
 constexpr int kFbOutNone = 0, kFbOutDW = 1, kFbOutSGD = 2;
 
-template <int F_IN, bool HAS_BIAS, int OUT, bool WITH_DB, bool BUCKETED>
+template <int F_IN, bool HAS_BIAS, int OUT, bool WITH_DB, bool BUCKETED, bool DBX>
 __global__ __launch_bounds__(64 * fb_waves(F_IN)) void k_fwd_bce(
     const bf16_t *__restrict__ Xb, const int32_t *__restrict__ idx, const bf16_t *__restrict__ W,
     const float *__restrict__ bias, const int32_t *__restrict__ pos, int P, bf16_t *__restrict__ dY,
@@ -607,9 +609,11 @@ __global__ __launch_bounds__(64 * fb_waves(F_IN)) void k_fwd_bce(
     constexpr int XW = (kFbMaxFs - kFbPrefetchFs) * 4 / NT;   // and the rest of the widest input
     constexpr int PL = 32 * kFbMaxPos / NT;     // positives per thread and slab
     constexpr int YL = 32 * 64 / NT;            // 16-byte dY stores per thread and slab
+    constexpr int NBM = DBX ? 3 : 2;            // target bitmaps in rotation
+    const int xsb = (F_s * kBw2XRow + 15) & ~15;   // bytes of one X^T block
     char *xs = fbs;
-    uint32_t *bm = reinterpret_cast<uint32_t *>(fbs + ((F_s * kBw2XRow + 15) & ~15));
-    char *ystg = reinterpret_cast<char *>(bm + 2 * kFbMaxSpan);
+    uint32_t *bm = reinterpret_cast<uint32_t *>(fbs + (DBX ? 2 : 1) * xsb);
+    char *ystg = reinterpret_cast<char *>(bm + NBM * kFbMaxSpan);
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int l16 = lane & 15, q = lane >> 4;
@@ -687,14 +691,16 @@ __global__ __launch_bounds__(64 * fb_waves(F_IN)) void k_fwd_bce(
         }
     };
     auto stage_slab = [&](int blk) {
+        char *xd = xs + (DBX ? (blk & 1) * xsb : 0);
 #pragma unroll
         for (int i = 0; i < XL; ++i) {
             const int c = tid + NT * i;
-            if (c < nxc) *reinterpret_cast<uint4 *>(xs + (c >> 2) * kBw2XRow + (c & 3) * 16) = xr[i];
+            if (c < nxc) *reinterpret_cast<uint4 *>(xd + (c >> 2) * kBw2XRow + (c & 3) * 16) = xr[i];
         }
-        // clear this thread's word of the previous slab's bitmap, set the current slab's targets
-        uint32_t *cur = bm + (blk & 1) * kFbMaxSpan;
-        if (tid < kFbMaxSpan) bm[((blk + 1) & 1) * kFbMaxSpan + tid] = 0u;
+        // clear this thread's word of the bitmap that comes next in the rotation (the slab that
+        // used it is done), set this slab's targets
+        uint32_t *cur = bm + (blk % NBM) * kFbMaxSpan;
+        if (tid < kFbMaxSpan) bm[((blk + 1) % NBM) * kFbMaxSpan + tid] = 0u;
         if constexpr (bucketed) {
             // entries lie in this workgroup's span by construction; the masks only keep a corrupt
             // entry inside the bitmap
@@ -719,22 +725,33 @@ __global__ __launch_bounds__(64 * fb_waves(F_IN)) void k_fwd_bce(
 #pragma unroll
             for (int i = 0; i < XW; ++i) {
                 const int c = XL * NT + tid + NT * i;
-                if (c < nxc) *reinterpret_cast<uint4 *>(xs + (c >> 2) * kBw2XRow + (c & 3) * 16) = xb.ld16((uint32_t)c * 16);
+                if (c < nxc) *reinterpret_cast<uint4 *>(xd + (c >> 2) * kBw2XRow + (c & 3) * 16) = xb.ld16((uint32_t)c * 16);
             }
         }
     };
     // the staged dY block of slab blk leaves as 1 KB row runs: 64 chunks of 16 bytes per row
-    auto store_slab = [&](int blk) {
+    auto read_ystg = [&](uint4 (&yv)[YL]) {
+#pragma unroll
+        for (int i = 0; i < YL; ++i) {
+            const int c = tid + NT * i;
+            yv[i] = *reinterpret_cast<const uint4 *>(ystg + fb_ystg_off(c >> 6, 4 * (c & 63)));
+        }
+    };
+    auto store_y = [&](int blk, const uint4 (&yv)[YL]) {
         const int b0 = blk * 32;
         const int rows = B - b0 < 32 ? B - b0 : 32;
         const Buf yo(dY + (int64_t)b0 * L + lab0, (uint32_t)(rows * L * 2));
 #pragma unroll
         for (int i = 0; i < YL; ++i) {
             const int c = tid + NT * i, r = c >> 6, ch = c & 63;
-            const uint4 val = *reinterpret_cast<const uint4 *>(ystg + fb_ystg_off(r, 4 * ch));
             const uint32_t o = r < rows && 8 * ch < span ? (uint32_t)(((int64_t)r * L + 8 * ch) * 2) : kOob;
-            yo.st16<kStreaming>(val, o);
+            yo.st16<kStreaming>(yv[i], o);
         }
+    };
+    auto store_slab = [&](int blk) {
+        uint4 yv[YL];
+        read_ystg(yv);
+        store_y(blk, yv);
     };
 
     f32x4_t acc[NST][2], db[2];
@@ -791,16 +808,34 @@ __global__ __launch_bounds__(64 * fb_waves(F_IN)) void k_fwd_bce(
             __syncthreads();   // every wave's region is read out before the bitmaps and slabs use the LDS
         }
     }
-    for (int i = tid; i < 2 * kFbMaxSpan; i += NT) bm[i] = 0u;
+    for (int i = tid; i < NBM * kFbMaxSpan; i += NT) bm[i] = 0u;
     const int nblk = Bp / 32;
     load(0);
+    if constexpr (DBX) {
+        __syncthreads();   // bitmaps cleared
+        stage_slab(0);
+        if (nblk > 1) load(1);
+    }
     for (int blk = 0; blk < nblk; ++blk) {
-        __syncthreads();   // the previous slab is no longer read, and its dY block is staged
-        if (blk > 0) store_slab(blk - 1);
-        stage_slab(blk);
-        __syncthreads();
-        if (blk + 1 < nblk) load(blk + 1);
-        const uint32_t *cur = bm + (blk & 1) * kFbMaxSpan;
+        if constexpr (DBX) {
+            // Two X^T blocks: slab blk + 1 is staged while slab blk is in use, and the barrier pair
+            // brackets only the reads of the staged dY block.
+            __syncthreads();   // slab blk is staged; the previous slab is done and its dY block staged
+            uint4 yv[YL];
+            if (blk > 0) read_ystg(yv);
+            __syncthreads();   // the dY block has been read out
+            if (blk > 0) store_y(blk - 1, yv);
+            if (blk + 1 < nblk) stage_slab(blk + 1);
+            if (blk + 2 < nblk) load(blk + 2);
+        } else {
+            __syncthreads();   // the previous slab is no longer read, and its dY block is staged
+            if (blk > 0) store_slab(blk - 1);
+            stage_slab(blk);
+            __syncthreads();
+            if (blk + 1 < nblk) load(blk + 1);
+        }
+        const char *xsc = xs + (DBX ? (blk & 1) * xsb : 0);   // this slab's X^T block
+        const uint32_t *cur = bm + (blk % NBM) * kFbMaxSpan;
         const int rows = B - blk * 32 < 32 ? B - blk * 32 : 32;
         // forward: z^T tile [32 rows][32 labels] of the unit
         f32x4_t z[2][2];
@@ -812,8 +847,8 @@ __global__ __launch_bounds__(64 * fb_waves(F_IN)) void k_fwd_bce(
         for (int s = 0; s < KS; ++s) {
 #pragma unroll
             for (int m = 0; m < 2; ++m) {
-                const uint2 lo = lds_read_tr(xs + fa[s][0] * kBw2XRow + 16 * aq + 8 * m);
-                const uint2 hi = lds_read_tr(xs + fa[s][1] * kBw2XRow + 16 * aq + 8 * m);
+                const uint2 lo = lds_read_tr(xsc + fa[s][0] * kBw2XRow + 16 * aq + 8 * m);
+                const uint2 hi = lds_read_tr(xsc + fa[s][1] * kBw2XRow + 16 * aq + 8 * m);
                 const bf16x8_t av = as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y));
 #pragma unroll
                 for (int nt = 0; nt < 2; ++nt) z[m][nt] = mfma16x16x32(av, as_bf16x8(wop[nt][s]), z[m][nt]);
@@ -863,7 +898,7 @@ __global__ __launch_bounds__(64 * fb_waves(F_IN)) void k_fwd_bce(
         if constexpr (WITH_DW) {
 #pragma unroll
             for (int st = 0; st < NST; ++st) {
-                const uint4 xv = *reinterpret_cast<const uint4 *>(xs + fw[st] * kBw2XRow + q * 16);
+                const uint4 xv = *reinterpret_cast<const uint4 *>(xsc + fw[st] * kBw2XRow + q * 16);
 #pragma unroll
                 for (int nt = 0; nt < 2; ++nt) acc[st][nt] = mfma16x16x32(as_bf16x8(xv), as_bf16x8(yb[nt]), acc[st][nt]);
             }
@@ -1462,7 +1497,7 @@ hipError_t bwd_w_mfma(const TailArgs &a, const void *X, const int32_t *idx, cons
 // bucketed by a pre-pass, in the workspace).
 bool fwd_bce_mfma_supported(const TailArgs &a, int P) {
     return bwd_w_mfma_supported(a) && (a.G % 16) == 0 && a.F_s <= kFbMaxFs && P >= 0 &&
-           a.B * (int64_t)P < ((int64_t)1 << 29) && fb_lds((int)a.F_s, (int)a.F_in) <= kLdsBudget;
+           a.B * (int64_t)P < ((int64_t)1 << 29) && fb_lds((int)a.F_s, (int)a.F_in, false) <= kLdsBudget;
 }
 
 // the fused kernel's (workgroup, slab) cells: workgroups of fb_waves units, slabs of 32 rows
@@ -1576,19 +1611,22 @@ struct FbArgs {
     int64_t n_ent = 0;
 };
 
-template <int F_IN, int OUT, bool BK, class Go>
+template <int F_IN, int OUT, bool BK, bool DBX, class Go>
 static hipError_t launch_fwd_bce_k(const FbArgs &f, Go &go) {
     if constexpr (OUT == kFbOutNone)
-        return f.bias ? go(k_fwd_bce<F_IN, true, OUT, false, BK>) : go(k_fwd_bce<F_IN, false, OUT, false, BK>);
-    if (f.dbias) return f.bias ? go(k_fwd_bce<F_IN, true, OUT, true, BK>) : go(k_fwd_bce<F_IN, false, OUT, true, BK>);
-    return f.bias ? go(k_fwd_bce<F_IN, true, OUT, false, BK>) : go(k_fwd_bce<F_IN, false, OUT, false, BK>);
+        return f.bias ? go(k_fwd_bce<F_IN, true, OUT, false, BK, DBX>) : go(k_fwd_bce<F_IN, false, OUT, false, BK, DBX>);
+    if (f.dbias)
+        return f.bias ? go(k_fwd_bce<F_IN, true, OUT, true, BK, DBX>) : go(k_fwd_bce<F_IN, false, OUT, true, BK, DBX>);
+    return f.bias ? go(k_fwd_bce<F_IN, true, OUT, false, BK, DBX>) : go(k_fwd_bce<F_IN, false, OUT, false, BK, DBX>);
 }
 
 template <int F_IN, int OUT>
 static hipError_t launch_fwd_bce(const TailArgs &a, const FbArgs &f, hipStream_t s) {
     const int64_t K = a.L / a.G;
     const int64_t units = K * cdiv(a.G, 32);
-    size_t lds = fb_lds((int)a.F_s, F_IN);
+    // a second X^T block where the LDS holds it (inputs of up to 768 features)
+    const bool dbx = fb_lds((int)a.F_s, F_IN, true) <= kLdsBudget;
+    size_t lds = fb_lds((int)a.F_s, F_IN, dbx);
     if (f.WT && lds < (size_t)fb_waves(F_IN) * fb_wt_region(F_IN)) lds = (size_t)fb_waves(F_IN) * fb_wt_region(F_IN);
     const dim3 grid((unsigned)cdiv(units, fb_waves(F_IN)));
     auto go = [&](auto kern) {
@@ -1600,7 +1638,8 @@ static hipError_t launch_fwd_bce(const TailArgs &a, const FbArgs &f, hipStream_t
                            f.WT, f.idxl, f.cofs, f.cent, f.n_ent);
         return hipGetLastError();
     };
-    return f.cofs ? launch_fwd_bce_k<F_IN, OUT, true>(f, go) : launch_fwd_bce_k<F_IN, OUT, false>(f, go);
+    if (dbx) return f.cofs ? launch_fwd_bce_k<F_IN, OUT, true, true>(f, go) : launch_fwd_bce_k<F_IN, OUT, false, true>(f, go);
+    return f.cofs ? launch_fwd_bce_k<F_IN, OUT, true, false>(f, go) : launch_fwd_bce_k<F_IN, OUT, false, false>(f, go);
 }
 
 template <int OUT>
