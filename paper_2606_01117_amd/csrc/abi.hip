@@ -107,10 +107,13 @@ size_t bwd_x_ws(const haste::TailArgs &a) {
     return haste::bwd_x_mfma_supported(a) ? haste::bwd_x_mfma_ws(a) : haste::bwd_x_valu_ws(a);
 }
 
-bool bwd_w_uses_xt(const haste::TailArgs &a) { return haste::bwd_w_sg_supported(a) || haste::bwd_w_mfma_supported(a); }
+bool bwd_w_uses_xt(const haste::TailArgs &a) {
+    return haste::bwd_w_dn_supported(a) || haste::bwd_w_sg_supported(a) || haste::bwd_w_mfma_supported(a);
+}
 
 hipError_t bwd_w_any(const haste::TailArgs &a, const void *X, const int32_t *idx, const void *dY, float *dW,
                      float *dbias, int beta, void *ws, hipStream_t s) {
+    if (haste::bwd_w_dn_supported(a)) return haste::bwd_w_dn(a, X, idx, dY, dW, dbias, beta, ws, s);
     if (haste::bwd_w_sg_supported(a)) return haste::bwd_w_sg(a, X, idx, dY, dW, dbias, beta, ws, s);
     if (haste::bwd_w_mfma_supported(a)) return haste::bwd_w_mfma(a, X, idx, dY, dW, dbias, beta, ws, s);
     return haste::bwd_w_valu(a, X, idx, dY, dW, dbias, beta, s);

@@ -261,6 +261,11 @@ hipError_t bwd_x_dn(const TailArgs &a, const int32_t *idx, const void *W, const 
 bool fwd_dn_supported(const TailArgs &a);
 hipError_t fwd_dn(const TailArgs &a, const void *X, const int32_t *idx, const void *W, const float *bias, void *Y,
                   hipStream_t s, const int32_t *spos = nullptr, int P = 0);
+// backward-weight for groups of 1 or 2 labels (F_s <= 768) as the dense product dY^T X of 64-label
+// blocks, the supports' entries picked out of it (X^T copy in the workspace)
+bool bwd_w_dn_supported(const TailArgs &a);
+hipError_t bwd_w_dn(const TailArgs &a, const void *X, const int32_t *idx, const void *dY, float *dW, float *dbias,
+                    int beta, void *ws, hipStream_t s);
 bool bwd_w_mfma_supported(const TailArgs &a);
 size_t bwd_w_mfma_ws(const TailArgs &a);
 hipError_t bwd_w_mfma(const TailArgs &a, const void *X, const int32_t *idx, const void *dY, float *dW,

@@ -629,6 +629,293 @@ static hipError_t fd_f(const haste::TailArgs &a, const FdGeom &g, const void *X,
     return hipErrorInvalidValue;
 }
 
+
+// ---------------------------------------------------------------------------------------------
+// Backward-weight for groups of 1 or 2 labels as a dense matrix-core product (bf16):
+//   dW[l, t] = sum over rows b of dY[b, l] X[b, idx[g(l), t]]   (Section 3.2, the backward-weight
+//   product): the entries of D = dY^T X [labels][F_s] at each label's support.
+// With one or two labels per group a gather kernel shares a gathered X column among at most two
+// labels, and its cost is an LDS gather per (label, slot, row).  Here a workgroup of 4 waves (one
+// per SIMD) owns 64 labels and forms D for all F_s features over the whole batch: wave w keeps
+// D[64 labels][features 16 NFT w ..] in its matrix-core accumulators (192 registers at NFT = 12,
+// in the AGPRs).  Per K step of 32 rows, with v_mfma_f32_16x16x32_bf16 (M = labels, N = features,
+// K = rows):
+//   A = dY^T: the step's [32 rows][64 labels] block, staged in LDS and read transposed with
+//       ds_read_b64_tr_b16 (lane (label l16, q) receives rows 8q .. 8q+7 of its label);
+//   B = X^T from the block-major copy (16 bytes per lane: rows 8q .. 8q+7 of one feature; 1 KiB
+//       of 16 whole features per wave instruction, L2-resident).
+// The product does F_s / F_in times the multiply-adds the layer needs (12x at 64 slots of 768),
+// which the matrix cores absorb; X^T is read once per 64 labels.  After the batch, the D slices
+// are staged in LDS as [feature][64 labels] fp32 (rows of 272 bytes: the 16 lanes of one write
+// land on distinct banks), a round of WPR waves at a time, and each thread picks out its dW cells
+// (label, slot) whose feature lies in the round's range; the cells leave as contiguous rows.
+// Rows past B meet zero X^T rows (and are loaded as zeros), and the K steps run in whole periods
+// of four (a padded step reads past the X^T copy, i.e. zeros), so the accumulators have one path.
+// ---------------------------------------------------------------------------------------------
+constexpr int kWdLabels = 64;                     // labels per workgroup
+constexpr int kWdYRow = 160;                      // staged dY row: 64 labels + 32 bytes of pad
+constexpr int kWdDRow = 272;                      // staged D^T row: 64 labels fp32 + 16 bytes of pad
+// waves per extraction round: their D^T slices (NWV waves x 16 NFT features) within 104 KB
+__host__ __device__ constexpr int wd_wpr(int nwv, int nft) { return nwv * nft <= 24 ? nwv : nwv * nft <= 48 ? nwv / 2 : nwv / 4; }
+__host__ __device__ constexpr int wd_stage(int nwv, int nft) {   // dY staging, then the D^T rounds
+    return wd_wpr(nwv, nft) * 16 * nft * kWdDRow > 2 * 32 * kWdYRow ? wd_wpr(nwv, nft) * 16 * nft * kWdDRow : 2 * 32 * kWdYRow;
+}
+__host__ __device__ constexpr int wd_lds(int nwv, int nft, int f_in) { return wd_stage(nwv, nft) + kWdLabels * f_in * 4; }   // + supports
+
+// NWV: waves (4: one per SIMD; 8: two).  NFT: 16-feature tiles per wave (NWV x 16 NFT >= F_s).
+// TAILP: L is not a multiple of 8, so the last block's last 8-label piece of a row is read dword by
+// dword (nothing past the row).
+template <int NWV, int NFT, int F_IN, bool WITH_DB, bool TAILP>
+__global__ __attribute__((amdgpu_flat_work_group_size(64 * NWV, 64 * NWV), amdgpu_waves_per_eu(NWV / 4, NWV / 4)))
+void k_bwd_w_dn(const bf16_t *__restrict__ Xb, const int32_t *__restrict__ idx, const bf16_t *__restrict__ dY,
+                float *__restrict__ dW, float *__restrict__ dbias, int beta, int B, int Bp, int F_s, int64_t L,
+                int gshift, int64_t nblk) {
+    constexpr int T = 64 * NWV;                   // threads
+    constexpr int NC = kWdLabels * F_IN / T;       // dW cells per thread
+    constexpr int WPR = wd_wpr(NWV, NFT);
+    constexpr int FPW = 16 * NFT;                  // features per wave
+    extern __shared__ __align__(16) char wd[];
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int l16 = lane & 15, q = lane >> 4;
+    const uint32_t lbase = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char *)wd;
+    typedef __attribute__((address_space(3))) int lds_i32_t;
+    typedef __attribute__((address_space(3))) float lds_f32_t;
+
+    // this thread's dW cells of a block: label e / F_IN, slot e mod F_IN (e = tid + 256 i); their
+    // features wait in LDS (behind the staging area) until the extraction
+    const uint32_t fbase = lbase + (uint32_t)wd_stage(NWV, NFT);
+    auto load_fe = [&](int64_t lab0, int nlab, int (&fe)[NC]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int i = 0; i < NC; ++i) {
+            const int e = tid + T * i, l = e / F_IN;
+            fe[i] = l < nlab ? idx[((lab0 + l) >> gshift) * F_IN + e % F_IN] : -1;
+        }
+    };
+    auto store_fe = [&](const int (&fe)[NC]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int i = 0; i < NC; ++i) *(lds_i32_t *)(uintptr_t)(fbase + 4 * (tid + T * i)) = fe[i];
+    };
+
+    // dY of K step k of a block: thread -> row tid / 8, labels 8 (tid mod 8) .. + 7 (a block of no
+    // labels reads nothing); with 8 waves, waves 4 .. 7 stage nothing
+    const bool ystage = NWV == 4 || tid < 256;
+    const int yr = (tid >> 3) & 31, yc = tid & 7;
+    const uint32_t yst = lbase + (uint32_t)(yr * kWdYRow + 16 * yc);
+    auto load_y = [&](int64_t lab0, int nlab, int k) __attribute__((always_inline)) -> u32x4_t {
+        const int b0 = 32 * k;
+        const int rows = B - b0 < 32 ? B - b0 : 32;   // none past the batch (and past the padded step)
+        const Buf yb(dY + (int64_t)(rows > 0 ? b0 : 0) * L + lab0,
+                     rows > 0 ? (uint32_t)(((int64_t)(rows - 1) * L + nlab) * 2) : 0u);
+        const int nv = nlab - 8 * yc;                  // labels of this piece in the block
+        const uint32_t o = ystage && yr < rows && nv > 0 ? (uint32_t)(((int64_t)yr * L + 8 * yc) * 2) : kOob;
+        if constexpr (!TAILP) {
+            const uint4 v = yb.ld16(o);
+            return u32x4_t{v.x, v.y, v.z, v.w};
+        } else {
+            u32x4_t v;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) v[j] = yb.ld4(nv > 2 * j ? o + 4 * j : kOob);
+            return v;
+        }
+    };
+    // X^T of K step k: lane -> feature FPW wave + 16 nt + l16, rows 8q .. 8q + 7 (a lane offset plus
+    // a scalar one per tile and step).  Features past F_s read the next block's rows or, past the
+    // copy, zeros: finite values in columns of D that no support names.
+    const Buf xb(Xb, (uint32_t)((int64_t)Bp * F_s * 2));
+    const int xo = ((FPW * wave + l16) * 32 + 8 * q) * 2;
+    auto load_x = [&](int k, bf16x8_t (&bo)[NFT]) __attribute__((always_inline)) {
+        const int kb = k * F_s * 64;
+#pragma unroll
+        for (int nt = 0; nt < NFT; ++nt)
+            bo[nt] = as_bf16x8(__builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(xb.r, xo, kb + 1024 * nt, 0)));
+    };
+    // A operand source lanes (ds_read_b64_tr_b16): 16-lane group q names rows 8q + (l16 >> 2) (+ 4),
+    // labels 16 m + 4 (l16 & 3) .. + 3
+    const uint32_t asrc = lbase + (uint32_t)((8 * q + (l16 >> 2)) * kWdYRow + (l16 & 3) * 8);
+    // (the LDS byte address becomes an LDS pointer directly: through a generic pointer, address 0
+    // would turn into the LDS null value)
+    auto read_a = [&](uint32_t slot, int m) __attribute__((always_inline)) -> bf16x8_t {
+        const uint32_t p = asrc + slot + 32 * m;
+        const bf16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t *)(uintptr_t)p);
+        const bf16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t *)(uintptr_t)(p + 4 * kWdYRow));
+        const uint2 l2 = __builtin_bit_cast(uint2, lo), h2 = __builtin_bit_cast(uint2, hi);
+        return as_bf16x8(make_uint4(l2.x, l2.y, h2.x, h2.y));
+    };
+
+    f32x4_t acc[4][NFT];
+    f32x4_t db;                                    // dbias of M tile `wave` (ones as B)
+    const bf16x8_t ones = as_bf16x8(make_uint4(0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u));
+    constexpr uint32_t SB = 32 * kWdYRow;          // one staged step
+    // K steps in whole periods of four (the dY ring below; a padded step reads zeros)
+    const int nk = Bp / 32;
+    const int nkp = (nk + 3) & ~3;
+    bf16x8_t bo[2][NFT];   // X^T of steps k (parity) and k + 1
+    u32x4_t yv[4];         // dY of steps k + 1 .. k + 4, step s in yv[s mod 4]
+    int fe[NC];
+
+    // The workgroup runs blocks blockIdx.x, + gridDim.x, ... (one workgroup per CU).  A block's
+    // first loads (supports, dY of steps 0 .. 4, X^T of step 0) are issued before the previous
+    // block's extraction, so that their latency is hidden behind it.
+    int64_t blk = blockIdx.x;
+    int64_t lab0 = blk * kWdLabels;
+    int nlab = L - lab0 < kWdLabels ? (int)(L - lab0) : kWdLabels;
+    {
+        load_fe(lab0, nlab, fe);
+        const u32x4_t y0 = load_y(lab0, nlab, 0);
+#pragma unroll
+        for (int j = 1; j <= 4; ++j) yv[j & 3] = load_y(lab0, nlab, j);
+        load_x(0, bo[0]);
+        if (ystage) *(lds_u32x4_t *)(uintptr_t)yst = y0;
+        store_fe(fe);
+        __syncthreads();                           // step 0 and the supports staged
+    }
+    for (;;) {
+#pragma unroll
+        for (int m = 0; m < 4; ++m)
+#pragma unroll
+            for (int nt = 0; nt < NFT; ++nt) acc[m][nt] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+        db = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+        // Step k (U = k mod 4): its dY is in staging slot k mod 2 and its X^T in bo[k mod 2].  It
+        // stages step k + 1's dY (loaded four steps earlier) into the other slot, whose step k - 1
+        // was read before the last barrier, and loads step k + 5's dY in its place; step k + 1's X^T
+        // loads are issued one per feature tile between the products (issued together, the four
+        // waves' 48 loads queue at the texture unit and each wave waits there before its first
+        // product).
+        auto step = [&](int k, auto uc) __attribute__((always_inline)) {
+            constexpr int U = decltype(uc)::value;
+            constexpr int PAR = U & 1, J = (U + 1) & 3;
+            bf16x8_t a[4];
+#pragma unroll
+            for (int m = 0; m < 4; ++m) a[m] = read_a(PAR * SB, m);
+            bf16x8_t ad;
+            if constexpr (WITH_DB) ad = read_a(PAR * SB, wave & 3);
+            if (ystage) *(lds_u32x4_t *)(uintptr_t)(yst + (1 - PAR) * SB) = yv[J];
+            yv[J] = load_y(lab0, nlab, k + 5);
+            __builtin_amdgcn_sched_barrier(0);
+            const int kb = (k + 1) * F_s * 64;
+#pragma unroll
+            for (int nt = 0; nt < NFT; ++nt) {
+                bo[1 - PAR][nt] = as_bf16x8(__builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(xb.r, xo, kb + 1024 * nt, 0)));
+#pragma unroll
+                for (int m = 0; m < 4; ++m) acc[m][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[m], bo[PAR][nt], acc[m][nt], 0, 0, 0);
+            }
+            if constexpr (WITH_DB) db = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ad, ones, db, 0, 0, 0);
+            static_for<NFT>([&](auto) __attribute__((always_inline)) {
+                __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // one X^T load
+                __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);   // four products
+            });
+            __builtin_amdgcn_sched_barrier(0);
+            __syncthreads();
+        };
+        for (int k0 = 0; k0 < nkp; k0 += 4)
+            static_for<4>([&](auto uc) __attribute__((always_inline)) { step(k0 + decltype(uc)::value, uc); });
+
+        // the next block's first loads (none past the last block: a block of no labels)
+        const int64_t nb = blk + gridDim.x;
+        const int64_t lab0n = nb < nblk ? nb * kWdLabels : lab0;
+        const int nlabn = nb < nblk ? (L - lab0n < kWdLabels ? (int)(L - lab0n) : kWdLabels) : 0;
+        // (128-slot supports: the next block's support ids are loaded after the extraction, whose
+        // registers they would otherwise crowd)
+        constexpr bool PRE_FE = F_IN <= 64;
+        int fen[NC];
+        if constexpr (PRE_FE) load_fe(lab0n, nlabn, fen);
+        const u32x4_t y0 = load_y(lab0n, nlabn, 0);
+#pragma unroll
+        for (int j = 1; j <= 4; ++j) yv[j & 3] = load_y(lab0n, nlabn, j);
+        load_x(0, bo[0]);
+
+        // extraction: round r stages the slices of waves WPR r .. WPR r + WPR - 1 (features
+        // FPW WPR r .. + FPW WPR - 1) as D^T [feature][label]; lane (l16, q) of tile (m, nt) holds
+        // feature 16 nt + l16 of its wave, labels 16 m + 4q .. + 3
+        constexpr int NR = NWV / WPR;
+        float dv[NC];
+#pragma unroll
+        for (int i = 0; i < NC; ++i) {
+            fe[i] = *(lds_i32_t *)(uintptr_t)(fbase + 4 * (tid + T * i));
+            dv[i] = 0.0f;
+        }
+#pragma unroll
+        for (int r = 0; r < NR; ++r) {
+            if (r > 0) __syncthreads();            // the previous round's picks are done
+            if (wave / WPR == r) {
+                const uint32_t drow = lbase + (uint32_t)(((wave % WPR) * FPW + l16) * kWdDRow + 16 * q);
+#pragma unroll
+                for (int nt = 0; nt < NFT; ++nt)
+#pragma unroll
+                    for (int m = 0; m < 4; ++m)
+                        *(lds_u32x4_t *)(uintptr_t)(drow + 16 * nt * kWdDRow + 64 * m) =
+                            __builtin_bit_cast(u32x4_t, acc[m][nt]);
+            }
+            __syncthreads();
+            const int lo = FPW * WPR * r;
+#pragma unroll
+            for (int i = 0; i < NC; ++i) {
+                const int fr = fe[i] - lo;
+                if (fr >= 0 && fr < FPW * WPR) {
+                    const int l = (tid + T * i) / F_IN;
+                    dv[i] = *(lds_f32_t *)(uintptr_t)(lbase + (uint32_t)(fr * kWdDRow + 4 * l));
+                }
+            }
+        }
+        float *wrow = dW + lab0 * F_IN;
+#pragma unroll
+        for (int i = 0; i < NC; ++i) {
+            const int e = tid + T * i;
+            if (e / F_IN < nlab) wrow[e] = beta ? wrow[e] + dv[i] : dv[i];
+        }
+        if constexpr (WITH_DB) {
+            if (l16 == 0 && wave < 4) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int l = 16 * wave + 4 * q + i;
+                    if (l < nlab) dbias[lab0 + l] = (beta ? dbias[lab0 + l] : 0.0f) + db[i];
+                }
+            }
+        }
+        if (nb >= nblk) break;                     // workgroup-uniform
+        if constexpr (!PRE_FE) load_fe(lab0n, nlabn, fen);
+        __syncthreads();                           // the picks are done: the LDS takes the next block
+        if (ystage) *(lds_u32x4_t *)(uintptr_t)yst = y0;
+        store_fe(fen);
+        __syncthreads();
+        blk = nb;
+        lab0 = lab0n;
+        nlab = nlabn;
+    }
+}
+
+static int wd_nft(int F_s) { return F_s <= 256 ? 4 : F_s <= 512 ? 8 : F_s <= 768 ? 12 : 0; }
+
+template <int NWV, int NFT, int F_IN>
+static hipError_t launch_wd(const haste::TailArgs &a, const void *Xb, const int32_t *idx, const void *dY, float *dW,
+                            float *dbias, int beta, int Bp, hipStream_t s) {
+    const bool tailp = a.L % 8 != 0;
+    auto go = [&](auto kern) {
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, wd_lds(NWV, NFT, F_IN));
+        if (e != hipSuccess) return e;
+        const int gshift = a.G == 1 ? 0 : 1;
+        const int64_t nblk = haste::cdiv(a.L, kWdLabels);
+        const int64_t grid = nblk < kXcds * kCusPerXcd ? nblk : kXcds * kCusPerXcd;   // one workgroup per CU
+        hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(64 * NWV), wd_lds(NWV, NFT, F_IN), s, (const bf16_t *)Xb, idx,
+                           (const bf16_t *)dY, dW, dbias, beta, (int)a.B, Bp, (int)a.F_s, a.L, gshift, nblk);
+        return hipGetLastError();
+    };
+    if (dbias) return tailp ? go(k_bwd_w_dn<NWV, NFT, F_IN, true, true>) : go(k_bwd_w_dn<NWV, NFT, F_IN, true, false>);
+    return tailp ? go(k_bwd_w_dn<NWV, NFT, F_IN, false, true>) : go(k_bwd_w_dn<NWV, NFT, F_IN, false, false>);
+}
+
+template <int F_IN>
+static hipError_t wd_f(const haste::TailArgs &a, const void *Xb, const int32_t *idx, const void *dY, float *dW,
+                       float *dbias, int beta, int Bp, hipStream_t s) {
+    switch (wd_nft((int)a.F_s)) {
+        case 4: return launch_wd<8, 2, F_IN>(a, Xb, idx, dY, dW, dbias, beta, Bp, s);
+        case 8: return launch_wd<8, 4, F_IN>(a, Xb, idx, dY, dW, dbias, beta, Bp, s);
+        case 12: return launch_wd<8, 6, F_IN>(a, Xb, idx, dY, dW, dbias, beta, Bp, s);
+    }
+    return hipErrorInvalidValue;
+}
+
 }  // namespace
 
 namespace haste {
@@ -682,6 +969,28 @@ hipError_t fwd_dn(const TailArgs &a, const void *X, const int32_t *idx, const vo
         case 32: return fd_f<32>(a, g, X, idx, W, bias, Y, s, spos, P);
         case 64: return fd_f<64>(a, g, X, idx, W, bias, Y, s, spos, P);
         case 128: return fd_f<128>(a, g, X, idx, W, bias, Y, s, spos, P);
+    }
+    return hipErrorInvalidValue;
+}
+
+// backward-weight: bf16, G in {1, 2}, F_in in {32, 64, 128}, F_s a multiple of 8 up to 768 (the
+// four waves' accumulators); dY rows dword-aligned (L even) and 32 rows of them within the 31-bit
+// range of a buffer offset.  The X^T copy of the workspace is the other backward-weight kernels'.
+bool bwd_w_dn_supported(const TailArgs &a) {
+    if (a.dtype != HASTE_DTYPE_BF16 || !(a.G == 1 || a.G == 2)) return false;
+    if (!(a.F_in == 32 || a.F_in == 64 || a.F_in == 128)) return false;
+    return a.F_s > 0 && a.F_s % 8 == 0 && a.F_s <= 768 && a.L % 2 == 0 && (a.L * 32 + 1024) * 2 < ((int64_t)1 << 31);
+}
+
+hipError_t bwd_w_dn(const TailArgs &a, const void *X, const int32_t *idx, const void *dY, float *dW, float *dbias,
+                    int beta, void *ws, hipStream_t s) {
+    const int Bp = (int)round_up(a.B, 32);
+    hipError_t e = transpose_x(a, X, ws, s);
+    if (e != hipSuccess) return e;
+    switch (a.F_in) {
+        case 32: return wd_f<32>(a, ws, idx, dY, dW, dbias, beta, Bp, s);
+        case 64: return wd_f<64>(a, ws, idx, dY, dW, dbias, beta, Bp, s);
+        case 128: return wd_f<128>(a, ws, idx, dY, dW, dbias, beta, Bp, s);
     }
     return hipErrorInvalidValue;
 }
