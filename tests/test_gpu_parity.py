@@ -78,6 +78,12 @@ SMALL = [
     ("bf16_g1_fs200_b31", 31, 200, 2050, 1, 64, BF16),
     ("bf16_g2_l130", 40, 256, 130, 2, 64, BF16),
     ("bf16_g8_fs520", 64, 520, 2048, 8, 64, BF16),
+    # the dense backward-weight (G = 1, 2): more 64-label blocks than CUs (a second block for some
+    # workgroups) ending in a 6-label block, a single row with 128-slot supports, and feature
+    # counts short of the four waves' tiles with a padded K step
+    ("bf16_g1_l19206", 40, 768, 64 * 300 + 6, 1, 64, BF16),
+    ("bf16_g2_f128_b1", 1, 512, 384, 2, 128, BF16),
+    ("bf16_g2_fs640_b96", 96, 640, 4096, 2, 64, BF16),
     # 256-slot supports (the VALU kernels)
     ("bf16_g32_f256", 40, 768, 2048, 32, 256, BF16),
     ("f32_g8", 32, 256, 4096, 8, 32, F32),
