@@ -635,20 +635,25 @@ static hipError_t fd_f(const haste::TailArgs &a, const FdGeom &g, const void *X,
 //   dW[l, t] = sum over rows b of dY[b, l] X[b, idx[g(l), t]]   (Section 3.2, the backward-weight
 //   product): the entries of D = dY^T X [labels][F_s] at each label's support.
 // With one or two labels per group a gather kernel shares a gathered X column among at most two
-// labels, and its cost is an LDS gather per (label, slot, row).  Here a workgroup of 4 waves (one
-// per SIMD) owns 64 labels and forms D for all F_s features over the whole batch: wave w keeps
-// D[64 labels][features 16 NFT w ..] in its matrix-core accumulators (192 registers at NFT = 12,
-// in the AGPRs).  Per K step of 32 rows, with v_mfma_f32_16x16x32_bf16 (M = labels, N = features,
-// K = rows):
+// labels, and its cost is an LDS gather per (label, slot, row).  Here a workgroup of 8 waves (two
+// per SIMD) owns a block of 64 labels at a time and forms D for all F_s features over the whole
+// batch: wave w keeps D[64 labels][features 16 NFT w ..] in its matrix-core accumulators (96
+// registers at NFT = 6).  Per K step of 32 rows, with v_mfma_f32_16x16x32_bf16 (M = labels,
+// N = features, K = rows):
 //   A = dY^T: the step's [32 rows][64 labels] block, staged in LDS and read transposed with
 //       ds_read_b64_tr_b16 (lane (label l16, q) receives rows 8q .. 8q+7 of its label);
 //   B = X^T from the block-major copy (16 bytes per lane: rows 8q .. 8q+7 of one feature; 1 KiB
-//       of 16 whole features per wave instruction, L2-resident).
-// The product does F_s / F_in times the multiply-adds the layer needs (12x at 64 slots of 768),
-// which the matrix cores absorb; X^T is read once per 64 labels.  After the batch, the D slices
-// are staged in LDS as [feature][64 labels] fp32 (rows of 272 bytes: the 16 lanes of one write
-// land on distinct banks), a round of WPR waves at a time, and each thread picks out its dW cells
-// (label, slot) whose feature lies in the round's range; the cells leave as contiguous rows.
+//       of 16 whole features per wave instruction, L2-resident), the next step's loads issued one
+//       per feature tile between the products.
+// dY (from HBM) is loaded four steps ahead, after the step's X^T loads, so that waiting for X^T
+// (the load counter completes in order) does not wait for it.  The product does F_s / F_in times
+// the multiply-adds the layer needs (12x at 64 slots of 768), which the matrix cores absorb; X^T
+// is read once per 64 labels, and that stream (384 KB per block at 256 rows, through each CU's L1)
+// is what bounds the kernel.  After the batch, the D slices are staged in LDS as [feature][64
+// labels] fp32 (rows of 272 bytes: the 16 lanes of one write land on distinct banks), a round of
+// WPR waves at a time, and each thread picks out its dW cells (label, slot) whose feature lies in
+// the round's range; the cells leave as contiguous rows.  Workgroups are persistent (one per CU):
+// the next block's supports, first dY rows and first X^T tiles are loaded before the extraction.
 // Rows past B meet zero X^T rows (and are loaded as zeros), and the K steps run in whole periods
 // of four (a padded step reads past the X^T copy, i.e. zeros), so the accumulators have one path.
 // ---------------------------------------------------------------------------------------------
@@ -749,7 +754,10 @@ void k_bwd_w_dn(const bf16_t *__restrict__ Xb, const int32_t *__restrict__ idx, 
     // K steps in whole periods of four (the dY ring below; a padded step reads zeros)
     const int nk = Bp / 32;
     const int nkp = (nk + 3) & ~3;
-    bf16x8_t bo[2][NFT];   // X^T of steps k (parity) and k + 1
+    // X^T of steps k and k + 1: step s in bo[s mod XR], loaded XR - 1 steps ahead (a deeper ring
+    // with one wave per SIMD ran out of registers and was three times slower)
+    constexpr int XR = 2;
+    bf16x8_t bo[XR][NFT];
     u32x4_t yv[4];         // dY of steps k + 1 .. k + 4, step s in yv[s mod 4]
     int fe[NC];
 
@@ -764,7 +772,8 @@ void k_bwd_w_dn(const bf16_t *__restrict__ Xb, const int32_t *__restrict__ idx, 
         const u32x4_t y0 = load_y(lab0, nlab, 0);
 #pragma unroll
         for (int j = 1; j <= 4; ++j) yv[j & 3] = load_y(lab0, nlab, j);
-        load_x(0, bo[0]);
+#pragma unroll
+        for (int j = 0; j < XR - 1; ++j) load_x(j, bo[j]);
         if (ystage) *(lds_u32x4_t *)(uintptr_t)yst = y0;
         store_fe(fe);
         __syncthreads();                           // step 0 and the supports staged
@@ -775,12 +784,11 @@ void k_bwd_w_dn(const bf16_t *__restrict__ Xb, const int32_t *__restrict__ idx, 
 #pragma unroll
             for (int nt = 0; nt < NFT; ++nt) acc[m][nt] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
         db = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
-        // Step k (U = k mod 4): its dY is in staging slot k mod 2 and its X^T in bo[k mod 2].  It
+        // Step k (U = k mod 4): its dY is in staging slot k mod 2 and its X^T in bo[k mod XR].  It
         // stages step k + 1's dY (loaded four steps earlier) into the other slot, whose step k - 1
         // was read before the last barrier, and loads step k + 5's dY in its place; step k + 1's X^T
-        // loads are issued one per feature tile between the products (issued together, the four
-        // waves' 48 loads queue at the texture unit and each wave waits there before its first
-        // product).
+        // loads are issued one per feature tile between the products (issued together, the waves'
+        // 48 loads queue at the texture unit and each wave waits there before its first product).
         auto step = [&](int k, auto uc) __attribute__((always_inline)) {
             constexpr int U = decltype(uc)::value;
             constexpr int PAR = U & 1, J = (U + 1) & 3;
@@ -792,12 +800,13 @@ void k_bwd_w_dn(const bf16_t *__restrict__ Xb, const int32_t *__restrict__ idx, 
             if (ystage) *(lds_u32x4_t *)(uintptr_t)(yst + (1 - PAR) * SB) = yv[J];
             yv[J] = load_y(lab0, nlab, k + 5);
             __builtin_amdgcn_sched_barrier(0);
-            const int kb = (k + 1) * F_s * 64;
+            constexpr int XC = U % XR, XN = (U + XR - 1) % XR;   // this step's slot; the one step k - 1 freed
+            const int kb = (k + XR - 1) * F_s * 64;
 #pragma unroll
             for (int nt = 0; nt < NFT; ++nt) {
-                bo[1 - PAR][nt] = as_bf16x8(__builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(xb.r, xo, kb + 1024 * nt, 0)));
+                bo[XN][nt] = as_bf16x8(__builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(xb.r, xo, kb + 1024 * nt, 0)));
 #pragma unroll
-                for (int m = 0; m < 4; ++m) acc[m][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[m], bo[PAR][nt], acc[m][nt], 0, 0, 0);
+                for (int m = 0; m < 4; ++m) acc[m][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[m], bo[XC][nt], acc[m][nt], 0, 0, 0);
             }
             if constexpr (WITH_DB) db = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ad, ones, db, 0, 0, 0);
             static_for<NFT>([&](auto) __attribute__((always_inline)) {
@@ -822,7 +831,8 @@ void k_bwd_w_dn(const bf16_t *__restrict__ Xb, const int32_t *__restrict__ idx, 
         const u32x4_t y0 = load_y(lab0n, nlabn, 0);
 #pragma unroll
         for (int j = 1; j <= 4; ++j) yv[j & 3] = load_y(lab0n, nlabn, j);
-        load_x(0, bo[0]);
+#pragma unroll
+        for (int j = 0; j < XR - 1; ++j) load_x(j, bo[j]);
 
         // extraction: round r stages the slices of waves WPR r .. WPR r + WPR - 1 (features
         // FPW WPR r .. + FPW WPR - 1) as D^T [feature][label]; lane (l16, q) of tile (m, nt) holds
