@@ -984,12 +984,14 @@ hipError_t fwd_dn(const TailArgs &a, const void *X, const int32_t *idx, const vo
 }
 
 // backward-weight: bf16, G in {1, 2}, F_in in {32, 64, 128}, F_s a multiple of 8 up to 768 (the
-// four waves' accumulators); dY rows dword-aligned (L even) and 32 rows of them within the 31-bit
-// range of a buffer offset.  The X^T copy of the workspace is the other backward-weight kernels'.
+// eight waves' accumulators); dY rows dword-aligned (L even) and 32 rows of them within the 31-bit
+// range of a buffer offset, and the whole X^T copy (read past by a padded step) within that range
+// too.  The X^T copy of the workspace is the other backward-weight kernels'.
 bool bwd_w_dn_supported(const TailArgs &a) {
     if (a.dtype != HASTE_DTYPE_BF16 || !(a.G == 1 || a.G == 2)) return false;
     if (!(a.F_in == 32 || a.F_in == 64 || a.F_in == 128)) return false;
-    return a.F_s > 0 && a.F_s % 8 == 0 && a.F_s <= 768 && a.L % 2 == 0 && (a.L * 32 + 1024) * 2 < ((int64_t)1 << 31);
+    return a.F_s > 0 && a.F_s % 8 == 0 && a.F_s <= 768 && a.L % 2 == 0 && (a.L * 32 + 1024) * 2 < ((int64_t)1 << 31) &&
+           (round_up(a.B, 128) + 128) * a.F_s * 2 < ((int64_t)1 << 31);
 }
 
 hipError_t bwd_w_dn(const TailArgs &a, const void *X, const int32_t *idx, const void *dY, float *dW, float *dbias,
