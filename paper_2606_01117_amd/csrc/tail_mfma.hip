@@ -1208,7 +1208,9 @@ __global__ __launch_bounds__((kBxConsumers + kBxProducers) * 64) void k_bwd_x(
         else produce(std::integral_constant<int, 8>{});
     } else {
         // ---- consumers: rows 16bh .. 16bh + 15 of the tile ----
+        // (their per-group chain sets the pace: they issue ahead of the producers on a shared SIMD)
         const int bh = wave;
+        __builtin_amdgcn_s_setprio(2);
         const int last = n - 1;
         auto cl = [&](int v) { return v < last ? v : last; };
 
