@@ -456,6 +456,10 @@ __global__ __launch_bounds__(256, BN <= 128 ? 2 : 1) void k_gemm4(
             __builtin_amdgcn_sched_barrier(0);
         }
     }
+    // the epilogue issues ahead of the other workgroup's products on a shared SIMD, so that it
+    // ends sooner and frees its LDS and the next tile starts (measured: forward with the loss
+    // gradient 81 -> 77 us on the 65K head)
+    __builtin_amdgcn_s_setprio(1);
     wait_vmcnt<0>();   // no load may still be writing LDS
     __syncthreads();   // and no wave still reads a stage: the LDS now stages the output
 
