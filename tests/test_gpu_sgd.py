@@ -73,6 +73,9 @@ CASES = [
     ("fused_p150_skewed", 64, 768, 4096, 32, 64, BF16, -150, True, True),
     ("fused_p200_skewed_f128", 48, 512, 4096, 32, 128, BF16, -200, False, True),
     ("composed_g8", 70, 768, 3072, 8, 32, BF16, 5, True, True),
+    # small groups: dW from the dense backward-weight (G = 1, 2) in the workspace, then the step
+    ("composed_g1", 40, 768, 2050, 1, 64, BF16, 6, True, True),
+    ("composed_g2_f128", 33, 512, 4096, 2, 128, BF16, 5, False, True),
     ("composed_f32_g8", 32, 256, 4096, 8, 32, F32, 5, False, False),
 ]
 

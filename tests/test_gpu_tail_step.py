@@ -61,6 +61,11 @@ CASES = [
     ("g32_fs896", 40, 896, 4096, 32, 64, BF16, 6, False, 0),   # X^T past the prefetch; bwd_x takes F_s <= 910
     ("composed_g16", 64, 768, 4096, 16, 64, BF16, 8, False, 0),
     ("composed_f32", 32, 256, 4096, 8, 32, F32, 5, True, 1),
+    # small groups: the forward forms the gradient as it stores, then the dense backward-weight
+    # (G = 1, 2) or the gather kernel (G = 4) and the scattered-tile backward-feature
+    ("small_g1", 40, 768, 2050, 1, 64, BF16, 6, True, 1),
+    ("small_g2_f128", 33, 512, 4096, 2, 128, BF16, 5, False, 0),
+    ("small_g4", 64, 768, 4096, 4, 64, BF16, 8, True, 0),
 ]
 
 
@@ -96,7 +101,9 @@ def test_tail_step_workspace_checked(hs):
 
 @pytest.mark.parametrize("case", [("g32_f64", 64, 768, 4096, 32, 64, 8, True), ("g32_f128", 70, 768, 4096, 32, 128, 5, False),
                                   ("g32_f64_p120_bucketed", 50, 512, 4096, 32, 64, 120, True),
-                                  ("composed_g16", 48, 512, 4096, 16, 64, 4, False)], ids=lambda c: c[0])
+                                  ("composed_g16", 48, 512, 4096, 16, 64, 4, False),
+                                  ("composed_g1", 40, 768, 2050, 1, 64, 6, True),
+                                  ("composed_g2", 33, 256, 1030, 2, 32, 3, False)], ids=lambda c: c[0])
 def test_tail_step_sgd_equals_the_two_calls(hs, case):
     import torch
     name, B, F_s, L, G, F_in, P, with_bias = case
