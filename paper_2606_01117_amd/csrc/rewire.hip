@@ -35,8 +35,18 @@ __global__ __launch_bounds__(256) void k_rw_scores(const T *__restrict__ W, int6
     if (i >= K * F) return;
     const int64_t k = i / F;
     const int j = (int)(i - k * F);
+    // the labels' weights 8 at a time, all 8 loads in flight before they are summed in order
     float s = 0.0f;
-    for (int g = 0; g < G; ++g) s += fabsf(load_f32(W, (k * G + g) * F + j));
+    const T *w = W + k * G * F + j;
+    int g = 0;
+    for (; g + 8 <= G; g += 8) {
+        float v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = load_f32(w, (int64_t)(g + u) * F);
+#pragma unroll
+        for (int u = 0; u < 8; ++u) s += fabsf(v[u]);
+    }
+    for (; g < G; ++g) s += fabsf(load_f32(w, (int64_t)g * F));
     keys[i] = __float_as_uint(s);
 }
 
@@ -54,10 +64,31 @@ __global__ __launch_bounds__(256) void k_rw_hist(const uint32_t *__restrict__ ke
     h[threadIdx.x] = 0u;
     __syncthreads();
     const uint32_t prefix = st->prefix, pmask = st->pmask;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
-        const uint32_t key = keys[i];
+    // four keys per 16-byte load, four loads in flight per thread (the keys array is 256-byte
+    // aligned); the last n mod 4 keys one by one
+    const uint4 *k4 = reinterpret_cast<const uint4 *>(keys);
+    const int64_t n4 = n / 4, stride = (int64_t)gridDim.x * blockDim.x;
+    auto count = [&](uint32_t key) {
         if ((key & pmask) == prefix) atomicAdd(&h[(key >> shift) & 255u], 1u);
+    };
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += 4 * stride) {
+        uint4 v[4];
+        bool ok[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            ok[u] = i + u * stride < n4;
+            v[u] = ok[u] ? k4[i + u * stride] : make_uint4(0u, 0u, 0u, 0u);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            if (ok[u]) {
+                count(v[u].x);
+                count(v[u].y);
+                count(v[u].z);
+                count(v[u].w);
+            }
     }
+    if (blockIdx.x == 0 && threadIdx.x < n - 4 * n4) count(keys[4 * n4 + threadIdx.x]);
     __syncthreads();
     if (h[threadIdx.x]) atomicAdd(&hist[threadIdx.x], h[threadIdx.x]);
 }
@@ -104,27 +135,31 @@ __global__ __launch_bounds__(256) void k_rw_eqcount(const uint32_t *__restrict__
     if (threadIdx.x == 0) cnt[blockIdx.x] = tot;
 }
 
-// exclusive prefix of the per-block counts, in block order (one workgroup)
-__global__ __launch_bounds__(256) void k_rw_scan(uint32_t *__restrict__ cnt, int64_t nb) {
-    __shared__ uint32_t part[256];
-    __shared__ uint32_t carry;
-    if (threadIdx.x == 0) carry = 0u;
+// exclusive prefix of the per-block counts, in block order (one workgroup of 1024 threads): each
+// thread sums a contiguous run of counts, one scan of the 1024 run sums, then each thread writes
+// its run's prefixes (integer sums: the same values in any order)
+constexpr int kRwScanThreads = 1024;
+__global__ __launch_bounds__(kRwScanThreads) void k_rw_scan(uint32_t *__restrict__ cnt, int64_t nb) {
+    __shared__ uint32_t part[kRwScanThreads];
+    const int t = threadIdx.x;
+    const int64_t per = (nb + kRwScanThreads - 1) / kRwScanThreads;
+    const int64_t b = t * per, e = b + per < nb ? b + per : nb;
+    uint32_t sum = 0u;
+#pragma unroll 8
+    for (int64_t i = b; i < e; ++i) sum += cnt[i];
+    part[t] = sum;
     __syncthreads();
-    for (int64_t base = 0; base < nb; base += 256) {
-        const int64_t i = base + threadIdx.x;
-        const uint32_t v = i < nb ? cnt[i] : 0u;
-        part[threadIdx.x] = v;
+    for (int off = 1; off < kRwScanThreads; off <<= 1) {   // inclusive Hillis-Steele scan
+        const uint32_t a = t >= off ? part[t - off] : 0u;
         __syncthreads();
-        for (int off = 1; off < 256; off <<= 1) {   // inclusive Hillis-Steele scan
-            const uint32_t a = threadIdx.x >= off ? part[threadIdx.x - off] : 0u;
-            __syncthreads();
-            part[threadIdx.x] += a;
-            __syncthreads();
-        }
-        if (i < nb) cnt[i] = carry + part[threadIdx.x] - v;
+        part[t] += a;
         __syncthreads();
-        if (threadIdx.x == 255) carry += part[255];
-        __syncthreads();
+    }
+    uint32_t run = part[t] - sum;
+    for (int64_t i = b; i < e; ++i) {
+        const uint32_t v = cnt[i];
+        cnt[i] = run;
+        run += v;
     }
 }
 
@@ -163,12 +198,14 @@ __global__ __launch_bounds__(256) void k_rw_mark(const uint32_t *__restrict__ ke
 constexpr int kRwWaves = 4;
 constexpr int kRwMaxF = 256;
 
-template <typename T>
+// NPL: 64-slot words of a support (F <= 64 NPL)
+template <typename T, int NPL>
 __global__ __launch_bounds__(64 * kRwWaves) void k_rw_regrow(int32_t *__restrict__ idx, T *__restrict__ W,
                                                              float *__restrict__ mom, const uint8_t *__restrict__ mask,
                                                              int64_t K, int G, int F, int H, int init_random,
                                                              uint64_t seed, float scale) {
     __shared__ uint32_t used_s[kRwWaves][32];
+    __shared__ uint32_t upre_s[kRwWaves][32];
     __shared__ int32_t feat_s[kRwWaves][kRwMaxF];
     __shared__ int32_t src_s[kRwWaves][kRwMaxF];
     __shared__ uint8_t mk_s[kRwWaves][kRwMaxF];
@@ -176,63 +213,118 @@ __global__ __launch_bounds__(64 * kRwWaves) void k_rw_regrow(int32_t *__restrict
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
     const int64_t k = (int64_t)blockIdx.x * kRwWaves + wv;
     if (k >= K) return;   // wave-uniform; this kernel has no workgroup barrier
-    uint32_t *used = used_s[wv];
+    uint32_t *used = used_s[wv], *upre = upre_s[wv];
     int32_t *feat = feat_s[wv], *src = src_s[wv];
     uint8_t *mk = mk_s[wv];
     float *row = row_s[wv];
     const int64_t KF = K * F;
 
-    // the group's slots, their marks, and the features it keeps
+    // the group's slots, their marks (also as one 64-bit ballot per 64 slots), and the features it
+    // keeps
     used[lane & 31] = 0u;
-    int any = 0;
-    for (int j = lane; j < F; j += 64) {
-        feat[j] = idx[k * F + j];
-        mk[j] = mask[k * F + j];
-        any |= mk[j];
+    constexpr int NPW = NPL;
+    uint64_t pm[NPW];
+    int n_pruned = 0;
+#pragma unroll
+    for (int w = 0; w < NPW; ++w) {
+        const int j = lane + 64 * w;
+        uint8_t m = 0;
+        if (j < F) {
+            feat[j] = idx[k * F + j];
+            m = mask[k * F + j];
+            mk[j] = m;
+        }
+        pm[w] = __builtin_amdgcn_ballot_w64(m != 0);
+        n_pruned += __popcll(pm[w]);
     }
-    if (!__builtin_amdgcn_ballot_w64(any != 0)) return;
+    if (n_pruned == 0) return;   // wave-uniform
     for (int j = lane; j < F; j += 64)
         if (!mk[j]) atomicOr(&used[feat[j] >> 5], 1u << (feat[j] & 31));
-    int n_used = 0;
-    for (int j = 0; j < F; ++j) n_used += mk[j] ? 0 : 1;
 
-    // draws, slots in ascending order: the (r mod n_free)-th free feature, found by a wave scan of
-    // the free counts of the bitmap's words (lane w holds word w; words past H have no free bits)
-    const int nw = (H + 31) >> 5;
-    for (int j = 0; j < F; ++j) {
-        if (!mk[j]) continue;   // uniform: every lane reads the same entry
-        const uint64_t t = splitmix64_at(seed, (uint64_t)(k * F + j)) % (uint64_t)(H - n_used);
-        uint32_t freew = 0u;
-        if (lane < nw) {
-            const int lo = 32 * lane;
-            const uint32_t valid = H - lo >= 32 ? 0xFFFFFFFFu : ((1u << (H - lo)) - 1u);
-            freew = ~used[lane] & valid;
+    // Draws, pruned slots in ascending order: the (r mod n_free)-th free feature, r the slot's
+    // SplitMix64 value.  The d-th draw has n_free = H - (F - n_pruned) - d, so every draw's
+    // r mod n_free is computed at once, on the lane of its slot; only the selection is sequential.
+    // In 32-bit steps (n_free <= H <= 1024, so every product fits):
+    //   r mod n = ((r_hi mod n) (2^32 mod n) + r_lo mod n) mod n.
+    uint32_t tt[NPW];
+    {
+        int d0 = 0;   // pruned slots in earlier words
+#pragma unroll
+        for (int w = 0; w < NPW; ++w) {
+            const int j = lane + 64 * w;
+            tt[w] = 0u;
+            if ((pm[w] >> lane) & 1u) {
+                const int d = d0 + __popcll(pm[w] & ((1ull << lane) - 1ull));
+                const uint64_t r = splitmix64_at(seed, (uint64_t)(k * F + j));
+                const uint32_t nf = (uint32_t)(H - (F - n_pruned) - d);
+                const uint32_t p32 = (0xFFFFFFFFu % nf + 1u) % nf;   // 2^32 mod nf
+                tt[w] = ((uint32_t)(r >> 32) % nf * p32 % nf + (uint32_t)r % nf) % nf;
+            }
+            d0 += __popcll(pm[w]);
         }
-        // inclusive prefix of the free counts over lanes 0..63
-        uint32_t c = __popc(freew), inc = c;
-        for (int off = 1; off < 64; off <<= 1) {
-            const uint32_t a = __shfl_up(inc, off, 64);
-            if (lane >= off) inc += a;
-        }
-        const uint32_t before = inc - c;
-        const bool mine = (uint64_t)before <= t && t < (uint64_t)inc;
-        int f = 0;
-        if (mine) {
-            uint32_t w = freew;
-            for (uint32_t s = (uint32_t)(t - before); s > 0; --s) w &= w - 1u;   // drop the lower free bits
-            f = 32 * lane + __ffs(w) - 1;
-        }
-        const uint64_t who = __builtin_amdgcn_ballot_w64(mine);
-        f = __shfl(f, (int)__builtin_ctzll(who), 64);
-        if (lane == 0) used[f >> 5] |= 1u << (f & 31);
-        feat[j] = f;
-        ++n_used;
     }
+    // Lane w holds the free bits of bitmap word w (words past H have none) and the inclusive
+    // prefix of the free counts, scanned once; a draw removes one bit, so the lane that held it
+    // and every later prefix drop by one, with no further scan.
+    const int nw = (H + 31) >> 5;
+    uint32_t freew = 0u, valid = 0u;
+    if (lane < nw) {
+        const int lo = 32 * lane;
+        valid = H - lo >= 32 ? 0xFFFFFFFFu : ((1u << (H - lo)) - 1u);
+        freew = ~used[lane] & valid;
+    }
+    uint32_t c = __popc(freew), inc = c;
+    for (int off = 1; off < 64; off <<= 1) {
+        const uint32_t a = __shfl_up(inc, off, 64);
+        if (lane >= off) inc += a;
+    }
+#pragma unroll
+    for (int w = 0; w < NPW; ++w)
+        for (uint64_t rem = pm[w]; rem != 0u; rem &= rem - 1u) {
+            const int sl = (int)__builtin_ctzll(rem);
+            const uint32_t t = __builtin_amdgcn_readlane(tt[w], sl);
+            const uint32_t before = inc - c;
+            const bool mine = before <= t && t < inc;
+            // the holder's (t - before)-th free bit: a binary search on popcounts of halves
+            uint32_t sel = mine ? t - before : 0u;
+            int pos = 0;
+#pragma unroll
+            for (int half = 16; half > 0; half >>= 1) {
+                const uint32_t cnt = __popc((freew >> pos) & ((1u << half) - 1u));
+                if (sel >= cnt) {
+                    sel -= cnt;
+                    pos += half;
+                }
+            }
+            const int holder = (int)__builtin_ctzll(__builtin_amdgcn_ballot_w64(mine));
+            const int f = __builtin_amdgcn_readlane(32 * lane + pos, holder);
+            if (lane == holder) {
+                freew &= ~(1u << (f & 31));
+                --c;
+            }
+            if (lane >= holder) --inc;
+            if (lane == 0) feat[64 * w + sl] = f;
+        }
 
-    // new positions: the rank of each slot's feature in the row (features are distinct)
+    // new positions: the rank of each slot's feature among the row's features, from the final
+    // bitmap (the features are distinct): used features in earlier words, plus the used bits of
+    // its word below it
+    {
+        const uint32_t usedw = ~freew & valid;
+        const uint32_t uc = __popc(usedw);
+        uint32_t ui = uc;
+        for (int off = 1; off < 64; off <<= 1) {
+            const uint32_t a = __shfl_up(ui, off, 64);
+            if (lane >= off) ui += a;
+        }
+        if (lane < nw) {
+            used[lane] = usedw;
+            upre[lane] = ui - uc;
+        }
+    }
     for (int j = lane; j < F; j += 64) {
-        int p = 0;
-        for (int i = 0; i < F; ++i) p += feat[i] < feat[j] ? 1 : 0;
+        const int f = feat[j];
+        const int p = (int)(upre[f >> 5] + __popc(used[f >> 5] & ((1u << (f & 31)) - 1u)));
         src[p] = j;
     }
     for (int p = lane; p < F; p += 64) idx[k * F + p] = feat[src[p]];
@@ -264,7 +356,10 @@ __global__ __launch_bounds__(64 * kRwWaves) void k_rw_regrow(int32_t *__restrict
 
 namespace haste {
 
-bool rewire_supported(const TailArgs &a) { return a.F_in <= kRwMaxF && a.F_s <= kMaxFs; }
+// the regrowth addresses a group's weights (and velocity) with 32-bit offsets within its block
+bool rewire_supported(const TailArgs &a) {
+    return a.F_in <= kRwMaxF && a.F_s <= kMaxFs && a.G * a.F_in * 4 < ((int64_t)1 << 31);
+}
 
 static int64_t rw_blocks(const TailArgs &a) { return cdiv((a.L / a.G) * a.F_in, kRwBlock); }
 
@@ -293,23 +388,29 @@ hipError_t rewire(const TailArgs &a, int32_t *idx, void *W, float *m, int64_t n_
     else
         hipLaunchKernelGGL((k_rw_scores<float>), g1, dim3(256), 0, s, (const float *)W, K, (int)a.G, (int)a.F_in, keys);
     hipLaunchKernelGGL(k_rw_init, dim3(1), dim3(256), 0, s, hist, st, (uint64_t)(n_prune - 1));
-    const int64_t hb = cdiv(KF, 256) < 1024 ? cdiv(KF, 256) : 1024;
+    const int64_t hb = cdiv(KF, 1024) < 1024 ? (cdiv(KF, 1024) < 1 ? 1 : cdiv(KF, 1024)) : 1024;
     for (int shift = 24; shift >= 0; shift -= 8) {
         hipLaunchKernelGGL(k_rw_hist, dim3((unsigned)hb), dim3(256), 0, s, keys, KF, st, shift, hist);
         hipLaunchKernelGGL(k_rw_pick, dim3(1), dim3(256), 0, s, hist, st, shift);
     }
     const int64_t nb = rw_blocks(a);
     hipLaunchKernelGGL(k_rw_eqcount, dim3((unsigned)nb), dim3(256), 0, s, keys, KF, st, cnt);
-    hipLaunchKernelGGL(k_rw_scan, dim3(1), dim3(256), 0, s, cnt, nb);
+    hipLaunchKernelGGL(k_rw_scan, dim3(1), dim3(kRwScanThreads), 0, s, cnt, nb);
     hipLaunchKernelGGL(k_rw_mark, dim3((unsigned)nb), dim3(256), 0, s, keys, KF, st, cnt, mask);
     const float scale = (float)(1.0 / sqrt((double)a.F_in)) * 5.9604644775390625e-08f;   // a 2^-24, exact
     const dim3 g2((unsigned)cdiv(K, kRwWaves));
-    if (bf)
-        hipLaunchKernelGGL((k_rw_regrow<bf16_t>), g2, dim3(64 * kRwWaves), 0, s, idx, (bf16_t *)W, m, mask, K,
-                           (int)a.G, (int)a.F_in, (int)a.F_s, init_random, seed, scale);
-    else
-        hipLaunchKernelGGL((k_rw_regrow<float>), g2, dim3(64 * kRwWaves), 0, s, idx, (float *)W, m, mask, K, (int)a.G,
-                           (int)a.F_in, (int)a.F_s, init_random, seed, scale);
+    auto regrow = [&](auto tag, auto npl) {
+        using T = decltype(tag);
+        hipLaunchKernelGGL((k_rw_regrow<T, decltype(npl)::value>), g2, dim3(64 * kRwWaves), 0, s, idx, (T *)W, m,
+                           mask, K, (int)a.G, (int)a.F_in, (int)a.F_s, init_random, seed, scale);
+    };
+    auto by_words = [&](auto tag) {
+        if (a.F_in <= 64) regrow(tag, std::integral_constant<int, 1>{});
+        else if (a.F_in <= 128) regrow(tag, std::integral_constant<int, 2>{});
+        else regrow(tag, std::integral_constant<int, 4>{});
+    };
+    if (bf) by_words(bf16_t{});
+    else by_words(float{});
     return hipGetLastError();
 }
 
