@@ -52,6 +52,10 @@ CASES = [
     ("bf16_many_blocks", 4096, 2, 64, 1024, BF16, 0.02, 1, False),
     # the widest support the regrowth takes (four slots per lane)
     ("bf16_g8_f256", 400, 8, 256, 768, BF16, 0.1, 1, True),
+    # supports that end inside a 64-slot word: two words with most slots pruned (few free features
+    # per draw), and four words over the largest feature bitmap (H = 1024)
+    ("bf16_g4_f100_rho09", 300, 4, 100, 512, BF16, 0.9, 1, True),
+    ("f32_g2_f200_h1024", 200, 2, 200, 1024, F32, 0.4, 1, False),
 ]
 
 
