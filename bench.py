@@ -39,6 +39,7 @@ MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16 MFMA
 PROFILES = os.path.join(ROOT, "profiles")
 COPY_BYTES = 1 << 30            # plain device copy used to calibrate the HBM byte counters
 FLUSH_BYTES = 512 << 20         # written before each timed step of a working set the MALL could hold
+WARM_S = 0.2                    # untimed GPU work after host-side setup, before the first timed phase
 
 # kernels launched by each call (patterns matched at the start of rocprofv3's kernel names; the
 # fused kernel's third template argument is its output: 1 stores dW, 2 applies the momentum step)
@@ -273,6 +274,21 @@ def cpu_baseline(wl, X, idx, W, dY, Wh, dYh, pos_tail):
             "per_call_ms": {k: round(1e3 * v, 1) for k, v in parts.items()}}
 
 
+def warm_up(run_pass, min_passes):
+    """Untimed passes before a timed phase: at least min_passes, and at least WARM_S seconds of them,
+    so that the GPU's clocks have left the idle state that host-side setup (drawing inputs) leaves
+    them in. With a few passes only, the first phase after such a pause ran about 12% slower in every
+    kernel. Synchronises every four passes, so that the wall clock follows the GPU."""
+    import torch
+    t0, n = time.perf_counter(), 0
+    while n < min_passes or time.perf_counter() - t0 < WARM_S:
+        run_pass()
+        n += 1
+        if n % 4 == 0:
+            torch.cuda.synchronize()
+    torch.cuda.synchronize()
+
+
 def main():
     args = parse()
     if args.summarize_trace:
@@ -426,6 +442,7 @@ def main():
                        "alg_bytes": b, "flops": f}
         return d
 
+    warm_up(lambda: [fn() for _, fn in separate], 0)   # once, after the host-side input setup
     sep_ms, sep_per, _ = timed(separate)
     unf_ms, unf_per, _ = timed(unfused)
     step_ms, per_call, wall_ms = timed(fused)
@@ -576,10 +593,7 @@ def gsweep(args, hs, synth, torch, np):
         """Mean ms per pass of the calls in order, and of each call (events between the calls), over n
         passes after the warm-up passes. The calls of a pass run back to back, as in a step, so no
         call is timed with its working set left in the caches by a repeat of itself."""
-        for _ in range(max(1, args.warmup)):
-            for f in fns:
-                f()
-        torch.cuda.synchronize()
+        warm_up(lambda: [f() for f in fns], max(1, args.warmup))
         evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(fns) + 1)] for _ in range(n)]
         for r in range(n):
             evs[r][0].record(st)
@@ -628,10 +642,7 @@ def bottleneck(wl, Xd, Wd, dYd, args):
     dY = bf(dYd)                                       # [B, L]
     dYt = dY.t().contiguous()                          # [L, B]
     ops = [lambda: torch.matmul(Xr, Wt), lambda: torch.matmul(dYt, Xr), lambda: torch.matmul(dY, Wn)]
-    for _ in range(args.warmup):
-        for f in ops:
-            f()
-    torch.cuda.synchronize()
+    warm_up(lambda: [f() for f in ops], args.warmup)
     st = torch.cuda.current_stream()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record(st)
