@@ -567,11 +567,11 @@ __host__ __device__ constexpr int fb_wt_region(int f_in) { return 32 * f_in * 2 
 
 // The X^T block (two with dbx: the next slab's is staged while the current one is in use), the
 // target bitmaps (two, or three with dbx) and the staged dY block; or at the end the dW staging of
-// half the waves
+// every wave
 static size_t fb_lds(int F_s, int F_in, bool dbx) {
     const size_t main = (size_t)(dbx ? 2 : 1) * haste::round_up((int64_t)F_s * kBw2XRow, 16) +
                         (size_t)(dbx ? 3 : 2) * kFbMaxSpan * 4 + (size_t)32 * kFbYRow;
-    const size_t out = (size_t)(fb_waves(F_in) / 2) * 32 * (F_in + 4) * 4;
+    const size_t out = (size_t)fb_waves(F_in) * 32 * (F_in + 4) * 4;
     return main > out ? main : out;
 }
 
@@ -913,49 +913,44 @@ __global__ __launch_bounds__(64 * fb_waves(F_IN)) void k_fwd_bce(
 
     if constexpr (WITH_DW) {
         // dW: as in the backward-weight kernel, a wave stages its unit's [32 labels][F_IN] fp32 block
-        // in LDS and writes it as whole contiguous runs; half the waves at a time.  With the
-        // momentum step, the same runs read the unit's W and velocity and write the velocity and
-        // the next weights instead.  dbias from the q = 0 lanes.
+        // in its own LDS region (every wave at once: each reads back only its own block) and writes
+        // it as whole contiguous runs.  With the momentum step, the same runs read the unit's W and
+        // velocity and write the velocity and the next weights instead.  dbias from the q = 0 lanes.
         constexpr int OS = F_IN + 4;
-        float *ostg = reinterpret_cast<float *>(fbs) + (wave % (NW / 2)) * 32 * OS;
+        float *ostg = reinterpret_cast<float *>(fbs) + wave * 32 * OS;
         const Buf ob(OUT == kFbOutSGD ? (void *)(mom + lb * F_IN) : (void *)(dW + lb * F_IN),
                      (uint32_t)(nl * F_IN * 4));   // this unit's labels only
         const Buf wb(W + lb * F_IN, (uint32_t)(nl * F_IN * 2));
         const Buf nb(W_next + lb * F_IN, (uint32_t)(OUT == kFbOutSGD ? nl * F_IN * 2 : 0));
+        __syncthreads();   // every wave is done with the staged slabs
 #pragma unroll
-        for (int half = 0; half < 2; ++half) {
-            __syncthreads();   // every wave is done with the staged slabs / the previous half's staging
-            if (wave / (NW / 2) == half) {
+        for (int nt = 0; nt < 2; ++nt)
 #pragma unroll
-                for (int nt = 0; nt < 2; ++nt)
+            for (int st = 0; st < NST; ++st)
+                *reinterpret_cast<float4 *>(ostg + (16 * nt + l16) * OS + 16 * st + 4 * q) =
+                    make_float4(acc[st][nt][0], acc[st][nt][1], acc[st][nt][2], acc[st][nt][3]);
 #pragma unroll
-                    for (int st = 0; st < NST; ++st)
-                        *reinterpret_cast<float4 *>(ostg + (16 * nt + l16) * OS + 16 * st + 4 * q) =
-                            make_float4(acc[st][nt][0], acc[st][nt][1], acc[st][nt][2], acc[st][nt][3]);
-#pragma unroll
-                for (int i = 0; i < F_IN / 8; ++i) {
-                    const int e = 64 * i + lane;
-                    const int r = e / (F_IN / 4), c = (e % (F_IN / 4)) * 4;
-                    float4 val = *reinterpret_cast<const float4 *>(ostg + r * OS + c);
-                    if constexpr (OUT == kFbOutSGD) {
-                        // slots 4e .. 4e+3 of the unit's block: W (4 bf16) and velocity (4 fp32)
-                        const uint2 wv = wb.ld8((uint32_t)(e * 8));
-                        float4 mv = __builtin_bit_cast(float4, ob.ld16((uint32_t)(e * 16)));
-                        float n0, n1, n2, n3;
-                        sgd_step(bf16_to_f32((bf16_t)(wv.x & 0xffffu)), val.x, mv.x, n0, lr, momentum, weight_decay);
-                        sgd_step(bf16_to_f32((bf16_t)(wv.x >> 16)), val.y, mv.y, n1, lr, momentum, weight_decay);
-                        sgd_step(bf16_to_f32((bf16_t)(wv.y & 0xffffu)), val.z, mv.z, n2, lr, momentum, weight_decay);
-                        sgd_step(bf16_to_f32((bf16_t)(wv.y >> 16)), val.w, mv.w, n3, lr, momentum, weight_decay);
-                        ob.st16<kStreaming>(__builtin_bit_cast(uint4, mv), (uint32_t)(e * 16));
-                        nb.st8<kStreaming>(make_uint2(pack_bf16(n0, n1), pack_bf16(n2, n3)), (uint32_t)(e * 8));
-                    } else {
-                        if (beta) {
-                            const float4 o = __builtin_bit_cast(float4, ob.ld16((uint32_t)(e * 16)));
-                            val.x += o.x; val.y += o.y; val.z += o.z; val.w += o.w;
-                        }
-                        ob.st16<kStreaming>(__builtin_bit_cast(uint4, val), (uint32_t)(e * 16));
-                    }
+        for (int i = 0; i < F_IN / 8; ++i) {
+            const int e = 64 * i + lane;
+            const int r = e / (F_IN / 4), c = (e % (F_IN / 4)) * 4;
+            float4 val = *reinterpret_cast<const float4 *>(ostg + r * OS + c);
+            if constexpr (OUT == kFbOutSGD) {
+                // slots 4e .. 4e+3 of the unit's block: W (4 bf16) and velocity (4 fp32)
+                const uint2 wv = wb.ld8((uint32_t)(e * 8));
+                float4 mv = __builtin_bit_cast(float4, ob.ld16((uint32_t)(e * 16)));
+                float n0, n1, n2, n3;
+                sgd_step(bf16_to_f32((bf16_t)(wv.x & 0xffffu)), val.x, mv.x, n0, lr, momentum, weight_decay);
+                sgd_step(bf16_to_f32((bf16_t)(wv.x >> 16)), val.y, mv.y, n1, lr, momentum, weight_decay);
+                sgd_step(bf16_to_f32((bf16_t)(wv.y & 0xffffu)), val.z, mv.z, n2, lr, momentum, weight_decay);
+                sgd_step(bf16_to_f32((bf16_t)(wv.y >> 16)), val.w, mv.w, n3, lr, momentum, weight_decay);
+                ob.st16<kStreaming>(__builtin_bit_cast(uint4, mv), (uint32_t)(e * 16));
+                nb.st8<kStreaming>(make_uint2(pack_bf16(n0, n1), pack_bf16(n2, n3)), (uint32_t)(e * 8));
+            } else {
+                if (beta) {
+                    const float4 o = __builtin_bit_cast(float4, ob.ld16((uint32_t)(e * 16)));
+                    val.x += o.x; val.y += o.y; val.z += o.z; val.w += o.w;
                 }
+                ob.st16<kStreaming>(__builtin_bit_cast(uint4, val), (uint32_t)(e * 16));
             }
         }
         if constexpr (WITH_DB) {
